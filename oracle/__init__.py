@@ -1,0 +1,323 @@
+"""fp64 CPU oracle for the VestigeKV decode-time hot path (test infrastructure).
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The product path (the HIP library and
+its Python binding) never touches it.  It shares no code with the HIP path:
+the C source here is compiled on its own with gcc.
+
+Each function names the passage of the paper (arXiv 2609.03949) it follows;
+see ``vkvref.c`` for the arithmetic.  Arrays are numpy; bf16 values travel
+as ``uint16`` bit patterns.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "vkvref.c")
+_LIB = os.path.join(_HERE, "libvkvref.so")
+
+D_LAT, D_ROPE, D_ROW = 512, 64, 576
+MODE_ROPE, MODE_DIGEST, MODE_ROPE_DIGEST = 1, 2, 3
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (fp64, no FMA contraction, OpenMP)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        cmd = ["gcc", "-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math", "-fPIC",
+               "-shared", "-Wall", "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i64 = ctypes.c_int64
+        i32 = ctypes.c_int
+        lib.vkvref_bf16_to_f64.restype = ctypes.c_double
+        lib.vkvref_bf16_to_f64.argtypes = [ctypes.c_uint16]
+        lib.vkvref_round_bf16.restype = ctypes.c_uint16
+        lib.vkvref_round_bf16.argtypes = [ctypes.c_double]
+        lib.vkvref_ru_f32.restype = ctypes.c_float
+        lib.vkvref_ru_f32.argtypes = [ctypes.c_double]
+        lib.vkvref_ru_sqrt_f32.restype = ctypes.c_float
+        lib.vkvref_ru_sqrt_f32.argtypes = [ctypes.c_double]
+        lib.vkvref_frob2.restype = ctypes.c_double
+        lib.vkvref_frob2.argtypes = [P, i32]
+        lib.vkvref_gershgorin.restype = ctypes.c_double
+        lib.vkvref_gershgorin.argtypes = [P, i32]
+        lib.vkvref_digest_build.restype = i32
+        lib.vkvref_digest_build.argtypes = [P, i64, i64, i64, P, i32, i32, P, i64, P, P, P, i32]
+        lib.vkvref_query_prep.restype = i32
+        lib.vkvref_query_prep.argtypes = [P, P, i64, i64, P, i32, i32, P, P, P, P]
+        lib.vkvref_index_keys.restype = i32
+        lib.vkvref_index_keys.argtypes = [P, i64, i32, P, i64, i64, P, P, i32]
+        lib.vkvref_select.restype = i32
+        lib.vkvref_select.argtypes = [P, i64, i64, P, P]
+        lib.vkvref_upper_bounds.restype = i32
+        lib.vkvref_upper_bounds.argtypes = [P, i64, i32, P, P, P, P, i64, P, P, P, i64, P, i32]
+        lib.vkvref_admit.restype = i64
+        lib.vkvref_admit.argtypes = [P, i64, P, i64, ctypes.c_double, P, i64]
+        lib.vkvref_attend.restype = i32
+        lib.vkvref_attend.argtypes = [P, P, i64, P, i64, P, i64, ctypes.c_double, P, P, i32]
+        lib.vkvref_full_scores.restype = i32
+        lib.vkvref_full_scores.argtypes = [P, P, i64, P, i64, i64, P, i32]
+        lib.vkvref_max_threads.restype = i32
+        lib.vkvref_max_threads.argtypes = []
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: np.ndarray | None):
+    if a is None:
+        return None
+    assert a.flags["C_CONTIGUOUS"], "oracle arrays must be C-contiguous"
+    return a.ctypes.data
+
+
+def _u16(a) -> np.ndarray:
+    a = np.ascontiguousarray(a)
+    if a.dtype != np.uint16:
+        a = a.view(np.uint16) if a.dtype.itemsize == 2 else a.astype(np.uint16)
+    return a
+
+
+def max_threads() -> int:
+    return int(_load().vkvref_max_threads())
+
+
+# --------------------------------------------------------------- scalar helpers
+
+def bf16_to_f64(bits: int) -> float:
+    return float(_load().vkvref_bf16_to_f64(int(bits)))
+
+
+def round_bf16(x: float) -> int:
+    """fp64 -> bf16 bits, one round-to-nearest-even."""
+    return int(_load().vkvref_round_bf16(float(x)))
+
+
+def ru_f32(x: float) -> float:
+    return float(_load().vkvref_ru_f32(float(x)))
+
+
+def ru_sqrt_f32(x: float) -> float:
+    return float(_load().vkvref_ru_sqrt_f32(float(x)))
+
+
+def decode_bf16(a: np.ndarray) -> np.ndarray:
+    """bf16 bits -> fp64 values (exact)."""
+    a = _u16(a)
+    return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+# --------------------------------------------------------------- basis checks
+
+def frob2(P: np.ndarray) -> float:
+    P = _u16(P)
+    return float(_load().vkvref_frob2(_ptr(P), int(P.shape[0]) if P.size else 0))
+
+
+def gershgorin(P: np.ndarray) -> float:
+    """max_j sum_k |(P P^T)_jk| in fp64 -- an upper bound of ||P||_2^2."""
+    P = _u16(P)
+    return float(_load().vkvref_gershgorin(_ptr(P), int(P.shape[0])))
+
+
+# --------------------------------------------------------------- the path
+
+def digest_build(cache: np.ndarray, P: np.ndarray | None, r: int, with_rope: bool = True,
+                 scalars: bool = True, nthreads: int = 0):
+    """Index build over every row of cache [B, T, 576] (Sec. 4.2, index entry).
+
+    Returns (index [B,T,n] uint16, eta, eps, gamma [B,T] float32 or None)."""
+    cache = _u16(cache)
+    B, T, stride = cache.shape
+    if P is None or r == 0:
+        P = np.zeros((1, D_LAT), np.uint16)
+        r = 0
+    P = _u16(P)
+    n = (D_ROPE if with_rope else 0) + r
+    index = np.zeros((B, T, max(n, 1)), np.uint16)
+    eta = eps = gam = None
+    if scalars:
+        eta = np.zeros((B, T), np.float32)
+        eps = np.zeros((B, T), np.float32)
+        gam = np.zeros((B, T), np.float32)
+    _load().vkvref_digest_build(_ptr(cache), B, T, stride, _ptr(P), int(r), int(with_rope),
+                                _ptr(index), index.shape[2], _ptr(eta), _ptr(eps), _ptr(gam),
+                                int(nthreads))
+    return index[:, :, :n], eta, eps, gam
+
+
+def query_prep(q_lat: np.ndarray, q_rope: np.ndarray, P: np.ndarray | None, r: int, mode: int):
+    """Index-space queries qt [B,H,n] and head scalars (a, n, e) [B,H]."""
+    q_lat = _u16(q_lat)
+    q_rope = _u16(q_rope)
+    B, H, _ = q_lat.shape
+    if P is None or r == 0:
+        P = np.zeros((1, D_LAT), np.uint16)
+        r = 0
+    P = _u16(P)
+    n = (D_ROPE if mode & 1 else 0) + (r if mode & 2 else 0)
+    qt = np.zeros((B, H, max(n, 1)), np.uint16)
+    a = np.zeros((B, H), np.float32)
+    nq = np.zeros((B, H), np.float32)
+    e = np.zeros((B, H), np.float32)
+    _load().vkvref_query_prep(_ptr(q_lat), _ptr(q_rope), B, H, _ptr(P), int(r), int(mode),
+                              _ptr(qt), _ptr(a), _ptr(nq), _ptr(e))
+    return qt[:, :, :n].copy(), a, nq, e
+
+
+def index_rows(cache_seq: np.ndarray, index_seq: np.ndarray | None, mode: int, r: int,
+               index_has_rope: bool = True) -> np.ndarray:
+    """The index vectors x_u [T, n] scored for one sequence, per mode."""
+    if mode == MODE_ROPE:
+        if index_seq is not None and index_has_rope:
+            return np.ascontiguousarray(_u16(index_seq)[:, :D_ROPE])
+        return np.ascontiguousarray(_u16(cache_seq)[:, D_LAT:D_ROW])
+    off = D_ROPE if index_has_rope else 0
+    dig = _u16(index_seq)[:, off:off + r]
+    if mode == MODE_DIGEST:
+        return np.ascontiguousarray(dig)
+    rope = _u16(cache_seq)[:, D_LAT:D_ROW] if not index_has_rope else _u16(index_seq)[:, :D_ROPE]
+    return np.ascontiguousarray(np.concatenate([rope, dig], axis=1))
+
+
+def index_keys(qt_seq: np.ndarray, x: np.ndarray, A: int, check_exact: bool = False,
+               nthreads: int = 0):
+    """key_u = max_h qt_h . x_u for u in [0, A), fp64 (Eq. (trigger), first two terms).
+
+    Returns (key [A] float64, number of inexact (u,h) sums or None)."""
+    qt_seq = _u16(qt_seq)
+    x = _u16(x)
+    H, n = qt_seq.shape
+    key = np.zeros(max(A, 1), np.float64)
+    bad = ctypes.c_int64(0)
+    _load().vkvref_index_keys(_ptr(qt_seq), H, n, _ptr(x), x.shape[1], int(A), _ptr(key),
+                              ctypes.addressof(bad) if check_exact else None, int(nthreads))
+    return key[:A], (int(bad.value) if check_exact else None)
+
+
+def select(key: np.ndarray, k: int):
+    """Top-k of [0, A) by (key desc, index asc), ascending; theta = min key in S."""
+    key = np.ascontiguousarray(key, np.float64)
+    A = key.shape[0]
+    sel = np.zeros(max(k, 1), np.int32)
+    theta = ctypes.c_double(0.0)
+    rc = _load().vkvref_select(_ptr(key) if A else None, A, int(k), _ptr(sel),
+                               ctypes.addressof(theta))
+    if rc != 0:
+        raise ValueError("k out of range")
+    return sel[:k].copy(), float(theta.value)
+
+
+def upper_bounds(qt_seq, a, nq, e, x, eta, eps, gam, A: int, nthreads: int = 0) -> np.ndarray:
+    """UB_u = max_h (s^_h(u) + B_h(u)), fp64 (Lemma (Index certificate))."""
+    qt_seq = _u16(qt_seq)
+    x = _u16(x)
+    H, n = qt_seq.shape
+    f = lambda v: np.ascontiguousarray(v, np.float32)
+    a, nq, e, eta, eps, gam = map(f, (a, nq, e, eta, eps, gam))
+    ub = np.zeros(max(A, 1), np.float64)
+    _load().vkvref_upper_bounds(_ptr(qt_seq), H, n, _ptr(a), _ptr(nq), _ptr(e), _ptr(x),
+                                x.shape[1], _ptr(eta), _ptr(eps), _ptr(gam), int(A), _ptr(ub),
+                                int(nthreads))
+    return ub[:A]
+
+
+def admit(ub: np.ndarray, sel: np.ndarray, theta: float, cap: int | None = None):
+    """Rows of [0, A) outside S with UB > theta, ascending; returns (adm, count)."""
+    ub = np.ascontiguousarray(ub, np.float64)
+    sel = np.ascontiguousarray(sel, np.int32)
+    A = ub.shape[0]
+    if cap is None:
+        cap = A
+    adm = np.zeros(max(cap, 1), np.int32)
+    cnt = _load().vkvref_admit(_ptr(ub) if A else None, A, _ptr(sel) if sel.size else None,
+                               sel.shape[0], float(theta), _ptr(adm), int(cap))
+    return adm[:min(cnt, cap)].copy(), int(cnt)
+
+
+def attend(q_lat_seq, q_rope_seq, cache_seq, rows, scale: float, nthreads: int = 0):
+    """Exact softmax attention of all heads over cache rows ``rows`` (Eq. (setup)).
+
+    Returns (out [H,512] float64, lse [H] float64)."""
+    q_lat_seq = _u16(q_lat_seq)
+    q_rope_seq = _u16(q_rope_seq)
+    cache_seq = _u16(cache_seq)
+    rows = np.ascontiguousarray(rows, np.int32)
+    H = q_lat_seq.shape[0]
+    out = np.zeros((H, D_LAT), np.float64)
+    lse = np.zeros(H, np.float64)
+    _load().vkvref_attend(_ptr(q_lat_seq), _ptr(q_rope_seq), H, _ptr(cache_seq),
+                          cache_seq.shape[1], _ptr(rows) if rows.size else None, rows.shape[0],
+                          float(scale), _ptr(out), _ptr(lse), int(nthreads))
+    return out, lse
+
+
+def full_scores(q_lat_seq, q_rope_seq, cache_seq, A: int, nthreads: int = 0) -> np.ndarray:
+    """Unscaled full 576-dim scores s_h(u) [A, H] of archived rows (fp64)."""
+    q_lat_seq = _u16(q_lat_seq)
+    q_rope_seq = _u16(q_rope_seq)
+    cache_seq = _u16(cache_seq)
+    H = q_lat_seq.shape[0]
+    s = np.zeros((max(A, 1), H), np.float64)
+    _load().vkvref_full_scores(_ptr(q_lat_seq), _ptr(q_rope_seq), H, _ptr(cache_seq),
+                               cache_seq.shape[1], int(A), _ptr(s), int(nthreads))
+    return s[:A]
+
+
+def attend_list(k_sel: np.ndarray, A: int, T: int, adm: np.ndarray | None = None) -> np.ndarray:
+    """The attended multiset of one sequence: S, then the recent window [A, T),
+    then the admitted rows (Sec. 4.2 figure: kept/recent tier plus fetched rows)."""
+    parts = [np.asarray(k_sel, np.int32), np.arange(A, T, dtype=np.int32)]
+    if adm is not None:
+        parts.append(np.asarray(adm, np.int32))
+    return np.concatenate(parts)
+
+
+def step(cache, q_lat, q_rope, index, P, r: int, mode: int, W: int, k: int, scale: float,
+         two_tier: bool = False, eta=None, eps=None, gam=None, cap=None, seqs=None,
+         index_has_rope: bool = True, nthreads: int = 0):
+    """One whole decode step on the oracle for the sequences ``seqs``:
+    keys -> top-k -> [bound + admission] -> attention.
+
+    Returns a dict of per-sequence results."""
+    cache = _u16(cache)
+    B, T, _ = cache.shape
+    A = T - W
+    qt, a, nq, e = query_prep(q_lat, q_rope, P, r, mode)
+    res = {"sel": {}, "theta": {}, "adm": {}, "adm_count": {}, "out": {}, "lse": {}, "key": {}}
+    for b in (range(B) if seqs is None else seqs):
+        x = index_rows(cache[b], None if index is None else index[b], mode, r, index_has_rope)
+        key, _ = index_keys(qt[b], x, A, nthreads=nthreads)
+        sel, theta = select(key, k)
+        adm = None
+        if two_tier:
+            ub = upper_bounds(qt[b], a[b], nq[b], e[b], x, eta[b], eps[b], gam[b], A, nthreads)
+            adm, cnt = admit(ub, sel, theta, cap)
+            res["adm"][b] = adm
+            res["adm_count"][b] = cnt
+        rows = attend_list(sel, A, T, adm)
+        out, lse = attend(q_lat[b], q_rope[b], cache[b], rows, scale, nthreads)
+        res["sel"][b] = sel
+        res["theta"][b] = theta
+        res["out"][b] = out
+        res["lse"][b] = lse
+        res["key"][b] = key
+    return res
