@@ -1,0 +1,290 @@
+#!/usr/bin/env python3
+"""Throughput of the VestigeKV decode step on one MI355X.
+
+One step = query prep -> index scan (score) -> exact top-k (select) ->
+[certified admission] -> gather-attend, over one batch of synthetic MLA
+decode state resident in HBM.  Default workload: 32 sequences x 128 heads x
+131072 cached rows (rho = 1/32 budget + 512 recent rows, rope + rank-64
+digest index) -- the long-context configuration the metric is quoted on.
+
+Prints ONE JSON line.  ``value`` = archived rows scored per second =
+B * (T - W) / t_step.  ``roofline`` is for the dominant kernel (the index
+scan), timed with HIP events on the stream it runs on.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "archived KV rows scored+attended/sec per decode step; % of HBM peak BW"
+HBM_PEAK_GBS = 8000.0
+SCORE_SOURCE = os.path.join(ROOT, "paper_2609_03949_amd", "csrc", "k_score.hip")
+
+
+def log(msg: str):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def source_hash(path: str) -> str:
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def traffic_for(kernel: str, workload: str, launches_per_step: int):
+    """HBM bytes per launch from the committed rocprofv3 --pmc summary, or
+    None when it is missing or was taken on a different kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("source_sha256_16") != source_hash(SCORE_SOURCE):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="cfg4")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target CPU time of the oracle sample")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run a plain 1 GiB device copy (counter scale for --pmc runs)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(sequences shard across GPUs with no communication; see DESIGN.md).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2609_03949_amd as vkv
+    from paper_2609_03949_amd import budget, synth
+
+    cfg = synth.CONFIGS[args.config]
+    dev = torch.device("cuda:0")
+    log(f"workload {synth.describe(cfg)}")
+    t0 = time.time()
+    wl = synth.make_workload(cfg, dev)
+    torch.cuda.synchronize()
+    log(f"generated inputs in {time.time() - t0:.1f}s")
+    ctx = vkv.Context(0)
+    B, H, T, W, A, k = wl["B"], wl["H"], wl["T"], wl["W"], wl["A"], wl["k"]
+    mode, r = cfg.mode, cfg.r
+    two_tier = cfg.two_tier
+
+    # ---- index build (the compression event; timed separately, not in the step)
+    if mode == synth.MODE_ROPE:
+        cols, has_rope = 0, True
+    elif mode == synth.MODE_DIGEST:
+        cols, has_rope = r, False
+    else:
+        cols, has_rope = 64 + r, True
+    index = torch.empty(B, T, cols, dtype=torch.bfloat16, device=dev) if cols else None
+    eta = eps = gam = None
+    if two_tier:
+        eta = torch.empty(B, T, dtype=torch.float32, device=dev)
+        eps = torch.empty_like(eta)
+        gam = torch.empty_like(eta)
+    digest_ms = None
+    if index is not None or two_tier:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        vkv.digest_build(ctx, wl["cache"], wl["P"], r if mode != synth.MODE_ROPE else 0,
+                         has_rope, index, eta, eps, gam)
+        e1.record()
+        torch.cuda.synchronize()
+        digest_ms = e0.elapsed_time(e1)
+        log(f"index build {digest_ms:.2f} ms")
+    step = vkv.Step(wl["cache"], wl["q_lat"], wl["q_rope"], W, mode,
+                    r if mode != synth.MODE_ROPE else 0, index=index, index_has_rope=has_rope,
+                    P=wl["P"], eta=eta, eps=eps, gam=gam)
+    bufs = vkv.Buffers(step, k, two_tier=two_tier)
+    stream = torch.cuda.current_stream()
+
+    stages = ["query_prep", "score", "select"] + (["admit"] if two_tier else []) + ["attend"]
+
+    def run_step(ev=None):
+        def mark(i):
+            if ev is not None:
+                ev[i].record(stream)
+        mark(0)
+        vkv.query_prep(ctx, step, bufs.ws, stream)
+        mark(1)
+        vkv.score(ctx, step, bufs.ws, bufs.key, bufs.ub, stream)
+        mark(2)
+        vkv.select(ctx, step, bufs.ws, k, bufs.key, bufs.sel, bufs.theta, stream)
+        mark(3)
+        j = 3
+        if two_tier:
+            vkv.admit(ctx, step, bufs.ws, k, bufs.sel, bufs.theta, bufs.ub, bufs.adm,
+                      bufs.adm_count, bufs.cap, stream)
+            j += 1
+            mark(j)
+        vkv.attend(ctx, step, bufs.ws, k, bufs.sel, bufs.adm, bufs.adm_count, bufs.cap,
+                   cfg.scale, bufs.out, bufs.lse, stream)
+        mark(j + 1)
+
+    for _ in range(args.warmup):
+        run_step()
+    torch.cuda.synchronize()
+    if args.copy_probe:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("copy probe: 3 x 1 GiB device copies done")
+        del src, dst
+
+    nev = len(stages) + 1
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    for s in range(args.steps):
+        run_step(evs[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    per_stage = {name: float(np.mean([evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(args.steps)]))
+                 for i, name in enumerate(stages)}
+    step_ms = float(np.mean([evs[s][0].elapsed_time(evs[s][-1]) for s in range(args.steps)]))
+    total_ms = evs[0][0].elapsed_time(evs[-1][-1])
+    ms_per_step = total_ms / args.steps
+    adm_total = int(bufs.adm_count.sum().item()) if two_tier else 0
+    log(f"stages (ms): {json.dumps({k_: round(v, 4) for k_, v in per_stage.items()})}; "
+        f"step {ms_per_step:.4f} ms (event-per-step mean {step_ms:.4f}); wall {wall / args.steps * 1e3:.4f} ms")
+
+    rows_per_s = B * A / (ms_per_step * 1e-3)
+    sb = budget.step_bytes(B, H, T, W, k, mode, r, two_tier, adm_total)
+    step_gbs = sb["total"] / (ms_per_step * 1e-3) / 1e9
+    scan_bytes = sb["scan"]
+    score_ms = per_stage["score"]
+    achieved = scan_bytes / (score_ms * 1e-3) / 1e9
+    workload = args.config
+    traffic = traffic_for("score_kernel", workload, 1)
+    line = {
+        "metric": METRIC,
+        "value": rows_per_s,
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": synth.describe(cfg),
+            "B": B, "H": H, "T": T, "W": W, "k": k, "r": r,
+            "mode": synth.MODE_NAMES[mode], "two_tier": two_tier,
+        },
+        "hbm_frac_step": step_gbs / HBM_PEAK_GBS,
+        "step_gbs": step_gbs,
+        "step_bytes": sb,
+        "stage_ms": per_stage,
+        "attended_rows_per_seq": k + W + (adm_total / B if two_tier else 0),
+        "index_build_ms": digest_ms,
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "score_kernel (index scan)",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic,
+            "bytes_per_launch": scan_bytes,
+            "launch_ms": score_ms,
+        },
+    }
+
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(wl, cfg, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+    ctx.close()
+
+
+def cpu_baseline(wl, cfg, target_s: float):
+    """The fp64 oracle, as it stands, on whole sequences of the same workload:
+    index keys -> top-k -> [bound + admission] -> attention.  The oracle's own
+    index build for the sample runs first and is not timed (it is the
+    compression event, timed separately on both sides)."""
+    import numpy as np
+
+    import oracle
+    from paper_2609_03949_amd import synth
+
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    oracle.build(force=False)
+    nthreads = oracle.max_threads()
+    mode, r, W, k = cfg.mode, cfg.r, wl["W"], wl["k"]
+    rr = r if mode != synth.MODE_ROPE else 0
+    if mode == synth.MODE_ROPE:
+        has_rope, cols = True, 0
+    elif mode == synth.MODE_DIGEST:
+        has_rope, cols = False, r
+    else:
+        has_rope, cols = True, 64 + r
+    done_rows = 0
+    elapsed = 0.0
+    seqs_done = 0
+    b = 0
+    build_s = 0.0
+    while elapsed < target_s and b < wl["B"]:
+        import torch
+        t = torch.tensor([b], device=wl["cache"].device)
+        cache = synth.to_numpy_bits(wl["cache"].index_select(0, t))
+        q_lat = synth.to_numpy_bits(wl["q_lat"].index_select(0, t))
+        q_rope = synth.to_numpy_bits(wl["q_rope"].index_select(0, t))
+        P = synth.to_numpy_bits(wl["P"]) if wl["P"] is not None else None
+        tb = time.perf_counter()
+        index = eta = eps = gam = None
+        if cols or cfg.two_tier:
+            index, eta, eps, gam = oracle.digest_build(cache, P, rr, with_rope=has_rope,
+                                                       scalars=cfg.two_tier, nthreads=nthreads)
+            if not cols:
+                index = None
+        build_s += time.perf_counter() - tb
+        t0 = time.perf_counter()
+        oracle.step(cache, q_lat, q_rope, index, P, rr, mode, W, k, cfg.scale,
+                    two_tier=cfg.two_tier, eta=eta, eps=eps, gam=gam, index_has_rope=has_rope,
+                    nthreads=nthreads)
+        elapsed += time.perf_counter() - t0
+        done_rows += wl["A"]
+        seqs_done += 1
+        b += 1
+        log(f"cpu oracle: sequence {b - 1} done, {elapsed:.1f}s timed so far")
+    lscpu = ""
+    try:
+        import subprocess
+        lscpu = [l for l in subprocess.run(["lscpu"], capture_output=True, text=True).stdout.splitlines()
+                 if l.startswith("Model name")][0].split(":", 1)[1].strip()
+    except Exception:
+        pass
+    return {
+        "value": done_rows / elapsed,
+        "unit": "rows/s",
+        "cores": nthreads,
+        "kind": "oracle",
+        "sample": f"{seqs_done} whole sequence(s) of the same workload (A={wl['A']} archived rows each), "
+                  f"one full step each; fp64 oracle with OpenMP over rows; oracle index build "
+                  f"({build_s:.1f}s) not timed",
+        "cpu": lscpu,
+        "timed_s": elapsed,
+    }
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,228 @@
+/*
+ * vkv.h -- C ABI of libvkv: the decode-time hot path of VestigeKV
+ * (arXiv 2609.03949) on AMD Instinct MI355X (gfx950).
+ *
+ * One decode step over a multi-head-latent-attention KV cache whose rows are
+ * 576 bf16 wide (512 content latent + 64 decoupled branch; Sec. 3, Eq. (setup)):
+ *
+ *   vkv_digest_build  index of every cache row: [branch ; RNE_bf16(P c_u)] and
+ *                     the row certificate scalars (Sec. 4.2, index entry; run
+ *                     once per context, the paper's compression event)
+ *   vkv_query_prep    query side of the scan: the query digest and head scalars
+ *   vkv_score         index score of every archived row from the narrow slice:
+ *                     the exact-branch and sketch terms of Eq. (trigger),
+ *                     maximised over heads (fp32 MFMA, with a certified error)
+ *   vkv_select        exact per-sequence top-k by (score desc, index asc)
+ *   vkv_admit         optional two-tier admission: rows outside the top-k whose
+ *                     certified upper bound (Lemma (Index certificate)) exceeds
+ *                     the k-th selected score
+ *   vkv_attend        exact softmax attention over the selected rows, the
+ *                     recent window and the admitted rows, on full 576-wide
+ *                     rows (Lemma (Exchangeability): fetched rows join the
+ *                     softmax as exact copies)
+ *   vkv_step_run      query_prep -> score -> select -> [admit] -> attend in one call
+ *
+ * Conventions (all entry points):
+ *   - Pointers are DEVICE pointers unless stated.  The caller owns every
+ *     buffer; the library never allocates or frees caller memory.  Per-step
+ *     scratch lives in a caller-provided workspace (vkv_workspace_size).
+ *   - bf16 values are passed as uint16_t bit patterns.  Index lists are
+ *     int32, sorted ascending.
+ *   - Every call is asynchronous on `stream` (a hipStream_t, NULL = default
+ *     stream) and does no device synchronisation, except vkv_digest_build in
+ *     certificate mode (it reads back the contractivity check of P once).
+ *   - Arguments are validated before anything is launched; on error the
+ *     return code is negative, outputs are untouched and vkv_last_error()
+ *     describes the failure.  No C++ exception or abort crosses the ABI.
+ *   - A context is bound to one device and may be used from one host thread
+ *     at a time.
+ */
+#ifndef VKV_H
+#define VKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------ status codes */
+#define VKV_OK 0
+#define VKV_E_ARG (-1)            /* null pointer, bad enum, k or cap out of range */
+#define VKV_E_SHAPE (-2)          /* sizes out of the supported range */
+#define VKV_E_ALIGN (-3)          /* pointer or stride not 16-byte aligned */
+#define VKV_E_UNSUPPORTED (-4)    /* valid request this build does not implement */
+#define VKV_E_NOT_CONTRACTIVE (-5)/* certificate requested with ||P||_2 not certified <= 1 */
+#define VKV_E_HIP (-6)            /* a HIP runtime call failed */
+#define VKV_E_WORKSPACE (-7)      /* workspace null or smaller than vkv_workspace_size */
+#define VKV_E_DEBUG_ROWS (-8)     /* VKV_DEBUG_ROWS row-set assertion failed */
+
+/* ---------------------------------------------------------- scoring modes */
+#define VKV_MODE_ROPE 1           /* 64 branch dims only (read in place or from the index) */
+#define VKV_MODE_DIGEST 2         /* r sketch dims only */
+#define VKV_MODE_ROPE_DIGEST 3    /* 64 branch dims + r sketch dims (the paper's index) */
+
+#define VKV_D_LAT 512
+#define VKV_D_ROPE 64
+#define VKV_D_ROW 576
+
+typedef struct vkv_ctx vkv_ctx;
+
+/*
+ * One decode step's inputs.  Shapes: B sequences, H heads, T cache rows per
+ * sequence, W recent rows.  Rows [0, A) with A = T - W are archived (scored);
+ * rows [A, T) are the recent window (always attended, never scored).
+ *
+ *   q_lat   [B, H, 512] bf16, contiguous: absorbed content query W_UK^T q^c
+ *   q_rope  [B, H, 64]  bf16, contiguous: branch query q^r
+ *   cache   row u of sequence b at cache + b*cache_batch_stride + u*cache_row_stride
+ *           (elements); 576 bf16 = [c_u (512) ; r_u (64)]
+ *   index   packed index rows from vkv_digest_build, same addressing with
+ *           index_row_stride / index_batch_stride; columns are
+ *           [r_u (64, iff index_has_rope) ; digest (r)].  May be NULL in
+ *           VKV_MODE_ROPE, which then reads cache[..., 512:576] in place.
+ *   P       [r, 512] bf16 digest basis (modes with a digest)
+ *   eta, eps, gam  [B, T] fp32 row certificate scalars from vkv_digest_build
+ *           (needed by vkv_admit only), built with the same P and r
+ *   mode    VKV_MODE_*; r in {0} for ROPE, else a multiple of 32 in [32, 512]
+ *
+ * Supported: 1 <= B <= 65535, 1 <= H <= 128, 1 <= T < 2^31, 0 <= W <= T.
+ * The index width n = (64 if mode has rope) + (r if mode has digest) must be
+ * a multiple of 32 and at most 576; row strides and base pointers must be
+ * 16-byte aligned.
+ */
+typedef struct vkv_step {
+    int64_t B, H, T, W;
+    int32_t mode, r;
+    const uint16_t* q_lat;
+    const uint16_t* q_rope;
+    const uint16_t* cache;
+    int64_t cache_row_stride, cache_batch_stride;
+    const uint16_t* index;
+    int64_t index_row_stride, index_batch_stride;
+    int32_t index_has_rope;
+    int32_t reserved0;
+    const uint16_t* P;
+    const float* eta;
+    const float* eps;
+    const float* gam;
+} vkv_step;
+
+/* Context on HIP device `device`.  Owns a few KB of device scratch for the
+ * contractivity check and the last error string.  Reads VKV_DEBUG_ROWS from
+ * the environment: if set to a non-zero value, vkv_select / vkv_admit
+ * synchronise and assert the row-set invariants (in range, strictly
+ * ascending, |S| = k, S outside the recent window, admitted rows outside S,
+ * count <= cap), returning VKV_E_DEBUG_ROWS on violation. */
+int vkv_create(vkv_ctx** out, int device);
+int vkv_destroy(vkv_ctx* ctx);
+const char* vkv_status_string(int status);
+const char* vkv_last_error(const vkv_ctx* ctx);
+/* Library version as major*10000 + minor*100 + patch. */
+int vkv_version(void);
+
+/*
+ * Index build (Sec. 4.2: archived row u keeps (r_u, V_r^T c_u, eta_u); the
+ * paper draws the basis from the context's own queries, here P is given).
+ * For every row u < T of every sequence:
+ *   index[b,u,:] = [ r_u (bit copy, iff with_rope) ; d_u ],
+ *   d_u[j] = RNE_bf16( sum_{i<512} P[j,i] c_u[i] )   (fp64, i ascending, one rounding)
+ * If eta != NULL (certificate mode; eps and gam must then be non-NULL too),
+ * also the row scalars, each an fp32 upper bound rounded toward +inf:
+ *   eta_u >= sqrt(c_u^T (I - P^T P) c_u),  eps_u >= ||d_u - P c_u||,  gam_u >= ||P c_u||
+ * Certificate mode first checks on the device that ||P||_2 <= 1 (Gershgorin on
+ * P P^T with margin) and synchronises the stream to read the verdict; it
+ * returns VKV_E_NOT_CONTRACTIVE, writing nothing, if the check fails.
+ * r = 0 is allowed (no digest; eta_u >= ||c_u||, eps = gam = 0).  index may be
+ * NULL when only the scalars are wanted.
+ */
+int vkv_digest_build(vkv_ctx* ctx, const uint16_t* cache, int64_t B, int64_t T,
+                     int64_t cache_row_stride, int64_t cache_batch_stride, const uint16_t* P,
+                     int32_t r, int32_t with_rope, uint16_t* index, int64_t index_row_stride,
+                     int64_t index_batch_stride, float* eta, float* eps, float* gam,
+                     void* stream);
+
+/* Bytes of device workspace a step with budget k and admission capacity cap
+ * (0 without admission) needs; the workspace must be 256-byte aligned. */
+int vkv_workspace_size(const vkv_step* st, int64_t k, int64_t cap, size_t* bytes);
+
+/*
+ * Query side of the index scan, once per step (Eq. (trigger): V_r^T q^c' and
+ * the residual scale of the certificate):
+ *   qt[b,h,:] = [ q_rope (mode has the branch) ; RNE_bf16(P q_lat) (mode has a digest) ]
+ * (fp64, i ascending, one rounding) and the head certificate scalars, fp32
+ * rounded toward +inf:  a_h >= sqrt(q^T (I - P^T P) q),  n_h >= ||qd_h||,
+ * e_h >= ||qd_h - P q||, all into the workspace.  Must precede vkv_score.
+ */
+int vkv_query_prep(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Index scores (Eq. (trigger), first two terms; lambda > 0 dropped as it does
+ * not change the ranking):
+ *   key[b,u] ~= max_h  sum_d qt[b,h,d] x_u[d],   u in [0, A)
+ * with x_u the mode's index row and qt = [q_rope ; RNE_bf16(P q_lat)].  Computed
+ * with bf16 MFMA and fp32 accumulation; the workspace records a certified
+ * bound E on |key - exact| that vkv_select uses.  If ub != NULL (two-tier mode;
+ * needs st->eta/eps/gam), also
+ *   ub[b,u] ~= max_h ( s^_h(u) + a_h eta_u + n_h eps_u + e_h gam_u )
+ * the Cauchy-Schwarz upper bound of the full score (Lemma (Index certificate)).
+ * key, ub: [B, A] fp32, contiguous.  ws is the workspace vkv_query_prep filled
+ * for this step; it must then be passed unchanged to the vkv_select /
+ * vkv_admit / vkv_attend calls of the same step.
+ */
+int vkv_score(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, float* key,
+              float* ub, void* stream);
+
+/*
+ * Exact top-k: S_b = the first k rows of [0, A) ordered by (exact index score
+ * desc, row index asc), written ascending to sel[b*k .. b*k+k).  Rows whose
+ * fp32 key lies within the certified band of the k-th key are re-scored in
+ * fp64 (fixed order: d ascending) so the set equals the fp64 definition bit
+ * for bit.  theta[b] (fp64) = min over S_b of the exact score (-inf if k = 0).
+ * 0 <= k <= A.  key is the output of vkv_score with the same ws.
+ */
+int vkv_select(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k,
+               const float* key, int32_t* sel, double* theta, void* stream);
+
+/*
+ * Two-tier admission (Lemma (Index certificate) with the bf16 rounding of the
+ * stored sketch): admitted_b = { u in [0, A) \ S_b : UB_u > theta_b } ascending,
+ *   UB_u = max_h fl64( s^_h(u) + fma(a_h, eta_u, fma(n_h, eps_u, e_h gam_u)) ).
+ * Ambiguous rows are decided in fp64 as above.  adm [B, cap] int32; adm_count[b]
+ * = the true count (may exceed cap; then only the first cap rows are written).
+ * Needs mode ROPE or ROPE_DIGEST (the key must contain the exact branch
+ * summand), ub from vkv_score, and sel/theta from vkv_select with the same ws.
+ * Soundness needs ||P||_2 <= 1, which vkv_digest_build certifies.
+ */
+int vkv_admit(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k,
+              const int32_t* sel, const double* theta, const float* ub, int32_t* adm,
+              int32_t* adm_count, int64_t cap, void* stream);
+
+/*
+ * Exact attention of every head over the attended multiset of sequence b:
+ *   sel[b, 0..k)  ++  [A, T)  ++  adm[b, 0..min(adm_count[b], cap))
+ *   s_h(u) = scale * ( q_lat[b,h] . c_u + q_rope[b,h] . r_u )        (576 dims)
+ *   out[b,h,:] = RNE_bf16( sum_u softmax_u(s_h) c_u[0:512] )           [B, H, 512]
+ *   lse[b,h]   = log sum_u exp(s_h(u))   (natural log)                  [B, H] fp32
+ * bf16 MFMA, fp32 accumulation, online softmax, split-KV with an LSE merge
+ * (the appendix's kernel mapping: fetched rows are one more split-KV
+ * partition).  adm/adm_count may be NULL (cap must then be 0).  An empty set
+ * gives out = 0 and lse = -inf.  cap must not exceed the workspace's cap.
+ */
+int vkv_attend(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k,
+               const int32_t* sel, const int32_t* adm, const int32_t* adm_count, int64_t cap,
+               float scale, uint16_t* out, float* lse, void* stream);
+
+/* query_prep -> score -> select -> [admit iff adm_count != NULL] -> attend,
+ * same arguments as the individual calls (key and ub are the caller's
+ * intermediates). */
+int vkv_step_run(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k,
+                 float* key, float* ub, int32_t* sel, double* theta, int32_t* adm,
+                 int32_t* adm_count, int64_t cap, float scale, uint16_t* out, float* lse,
+                 void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VKV_H */

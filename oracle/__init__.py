@@ -56,8 +56,6 @@ def _load():
         lib.vkvref_ru_f32.argtypes = [ctypes.c_double]
         lib.vkvref_ru_sqrt_f32.restype = ctypes.c_float
         lib.vkvref_ru_sqrt_f32.argtypes = [ctypes.c_double]
-        lib.vkvref_frob2.restype = ctypes.c_double
-        lib.vkvref_frob2.argtypes = [P, i32]
         lib.vkvref_gershgorin.restype = ctypes.c_double
         lib.vkvref_gershgorin.argtypes = [P, i32]
         lib.vkvref_digest_build.restype = i32
@@ -126,11 +124,6 @@ def decode_bf16(a: np.ndarray) -> np.ndarray:
 
 
 # --------------------------------------------------------------- basis checks
-
-def frob2(P: np.ndarray) -> float:
-    P = _u16(P)
-    return float(_load().vkvref_frob2(_ptr(P), int(P.shape[0]) if P.size else 0))
-
 
 def gershgorin(P: np.ndarray) -> float:
     """max_j sum_k |(P P^T)_jk| in fp64 -- an upper bound of ||P||_2^2."""

@@ -95,17 +95,6 @@ float vkvref_ru_sqrt_f32(double x) {
 
 /* ------------------------------------------------------- digest basis P */
 
-/* ||P||_F^2, summed row-major in fp64. */
-double vkvref_frob2(const uint16_t* P, int r) {
-    double acc = 0.0;
-    for (int j = 0; j < r; ++j)
-        for (int i = 0; i < D_LAT; ++i) {
-            double p = vkvref_bf16_to_f64(P[(int64_t)j * D_LAT + i]);
-            acc = fma(p, p, acc);
-        }
-    return acc;
-}
-
 /* Gershgorin certificate that the bf16 basis is contractive (||P||_2 <= 1),
  * which makes M = I - P^T P positive semidefinite so that Cauchy-Schwarz in
  * the M-seminorm bounds the sketch residual (Lemma (Index certificate)).
@@ -137,9 +126,10 @@ double vkvref_gershgorin(const uint16_t* P, int r) {
  *   derr  >= ||d - P v||                (eps_u for a row, e_h for a head)
  *   pnorm >= ||P v||                    (gamma_u for a row)
  * The fp64 values carry rounding error; the margins G make them upper
- * bounds of the exact real quantities. */
-static void project_and_bound(const double* v, const uint16_t* P, int r, double NP,
-                              uint16_t* d, float* resid, float* dnorm, float* derr,
+ * bounds of the exact real quantities.  The bound on ||P v - w|| uses
+ * ||P||_F^2 <= r, which holds for every contractive basis (the only case in
+ * which the scalars are used). */
+static void project_and_bound(const double* v, const uint16_t* P, int r, uint16_t* d, float* resid, float* dnorm, float* derr,
                               float* pnorm) {
     double w[D_LAT];
     double Nv = 0.0;
@@ -162,7 +152,7 @@ static void project_and_bound(const double* v, const uint16_t* P, int r, double 
         Nd = fma(dj, dj, Nd);
     }
     const double G = VKVREF_G;
-    double Dm = G * (double)vkvref_ru_sqrt_f32(NP * Nv);   /* >= ||P v - w|| */
+    double Dm = G * (double)vkvref_ru_sqrt_f32((double)r * Nv);   /* >= ||P v - w|| */
     double sw = (double)vkvref_ru_sqrt_f32(Nw);
     double X = ((Nv - Nw) + G * (Nv + Nw)) + (2.0 * Dm) * sw;
     *resid = vkvref_ru_sqrt_f32((X > 0.0 ? X : 0.0) * (1.0 + G));
@@ -181,7 +171,6 @@ int vkvref_digest_build(const uint16_t* cache, int64_t B, int64_t T, int64_t row
                         const uint16_t* P, int r, int with_rope, uint16_t* index,
                         int64_t index_stride, float* eta, float* eps, float* gam,
                         int nthreads) {
-    double NP = vkvref_frob2(P, r);
     int64_t n = (int64_t)B * T;
 #ifdef _OPENMP
     if (nthreads > 0) omp_set_num_threads(nthreads);
@@ -194,7 +183,7 @@ int vkvref_digest_build(const uint16_t* cache, int64_t B, int64_t T, int64_t row
         uint16_t* out = index ? index + ru * index_stride : NULL;
         uint16_t dig[D_LAT];
         float e0, e1, e2, e3;
-        project_and_bound(c, P, r, NP, dig, &e0, &e3, &e1, &e2);
+        project_and_bound(c, P, r, dig, &e0, &e3, &e1, &e2);
         if (out) {
             int off = 0;
             if (with_rope) {
@@ -219,14 +208,13 @@ int vkvref_digest_build(const uint16_t* cache, int64_t B, int64_t T, int64_t row
 int vkvref_query_prep(const uint16_t* q_lat, const uint16_t* q_rope, int64_t B, int64_t H,
                       const uint16_t* P, int r, int mode, uint16_t* qt, float* a, float* nq,
                       float* e) {
-    double NP = vkvref_frob2(P, r);
     int n = ((mode & 1) ? D_ROPE : 0) + ((mode & 2) ? r : 0);
     for (int64_t bh = 0; bh < B * H; ++bh) {
         double q[D_LAT];
         for (int i = 0; i < D_LAT; ++i) q[i] = vkvref_bf16_to_f64(q_lat[bh * D_LAT + i]);
         uint16_t dig[D_LAT];
         float s_resid, s_dn, s_derr, s_pn;
-        project_and_bound(q, P, r, NP, dig, &s_resid, &s_dn, &s_derr, &s_pn);
+        project_and_bound(q, P, r, dig, &s_resid, &s_dn, &s_derr, &s_pn);
         uint16_t* o = qt + bh * n;
         int off = 0;
         if (mode & 1) {

@@ -1,0 +1,471 @@
+// vkv_api.hip -- the C ABI of libvkv: validation, workspace layout, launches.
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "vkv_internal.h"
+
+using namespace vkv;
+
+struct vkv_ctx {
+    int device;
+    int debug_rows;
+    double* gram;          // [512] device scratch for the contractivity check
+    char err[512];
+};
+
+static thread_local char g_err[512];
+
+static int fail(vkv_ctx* ctx, int code, const char* fmt, ...) {
+    char* buf = ctx ? ctx->err : g_err;
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, 512, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+#define HIP_TRY(ctx, expr)                                                                 \
+    do {                                                                                   \
+        hipError_t _e = (expr);                                                            \
+        if (_e != hipSuccess) return fail((ctx), VKV_E_HIP, "%s: %s", #expr, hipGetErrorString(_e)); \
+    } while (0)
+
+static inline bool al16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+static inline size_t up256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+// ------------------------------------------------------------ validation
+
+static int index_width(const vkv_step* st) {
+    return ((st->mode & 1) ? D_ROPE : 0) + ((st->mode & 2) ? st->r : 0);
+}
+
+static int check_step(vkv_ctx* ctx, const vkv_step* st) {
+    if (!st) return fail(ctx, VKV_E_ARG, "step is NULL");
+    if (st->B < 1 || st->B > 65535) return fail(ctx, VKV_E_SHAPE, "B=%lld outside [1, 65535]", (long long)st->B);
+    if (st->H < 1 || st->H > 128) return fail(ctx, VKV_E_SHAPE, "H=%lld outside [1, 128]", (long long)st->H);
+    if (st->T < 1 || st->T >= (1ll << 31)) return fail(ctx, VKV_E_SHAPE, "T=%lld outside [1, 2^31)", (long long)st->T);
+    if (st->W < 0 || st->W > st->T) return fail(ctx, VKV_E_SHAPE, "W=%lld outside [0, T]", (long long)st->W);
+    if (st->mode < 1 || st->mode > 3) return fail(ctx, VKV_E_ARG, "mode=%d is not a VKV_MODE_*", st->mode);
+    if (st->mode == VKV_MODE_ROPE) {
+        if (st->r != 0) return fail(ctx, VKV_E_ARG, "mode ROPE needs r = 0 (got %d)", st->r);
+    } else {
+        if (st->r < 32 || st->r > 512 || st->r % 32)
+            return fail(ctx, VKV_E_UNSUPPORTED, "r=%d: need a multiple of 32 in [32, 512]", st->r);
+    }
+    const int n = index_width(st);
+    if (n % 32 || n > D_ROW) return fail(ctx, VKV_E_UNSUPPORTED, "index width %d", n);
+    if (!st->q_lat || !st->q_rope || !st->cache) return fail(ctx, VKV_E_ARG, "q_lat, q_rope and cache are required");
+    if (!al16(st->q_lat) || !al16(st->q_rope) || !al16(st->cache))
+        return fail(ctx, VKV_E_ALIGN, "q_lat, q_rope and cache must be 16-byte aligned");
+    if (st->cache_row_stride < D_ROW || st->cache_row_stride % 8)
+        return fail(ctx, VKV_E_ALIGN, "cache_row_stride=%lld: need >= 576 and a multiple of 8",
+                    (long long)st->cache_row_stride);
+    if (st->cache_batch_stride % 8 || (st->B > 1 && st->cache_batch_stride < st->T * st->cache_row_stride))
+        return fail(ctx, VKV_E_ALIGN, "cache_batch_stride=%lld invalid", (long long)st->cache_batch_stride);
+    if (st->index) {
+        if (!al16(st->index)) return fail(ctx, VKV_E_ALIGN, "index must be 16-byte aligned");
+        const int cols = (st->index_has_rope ? D_ROPE : 0) + ((st->mode & 2) ? st->r : 0);
+        if (st->index_row_stride < cols || st->index_row_stride % 8)
+            return fail(ctx, VKV_E_ALIGN, "index_row_stride=%lld: need >= %d and a multiple of 8",
+                        (long long)st->index_row_stride, cols);
+        if (st->index_batch_stride % 8 || (st->B > 1 && st->index_batch_stride < st->T * st->index_row_stride))
+            return fail(ctx, VKV_E_ALIGN, "index_batch_stride=%lld invalid", (long long)st->index_batch_stride);
+        if ((st->mode & 1) && !st->index_has_rope)
+            return fail(ctx, VKV_E_UNSUPPORTED, "modes with the branch need an index built with_rope");
+    } else if (st->mode != VKV_MODE_ROPE) {
+        return fail(ctx, VKV_E_ARG, "modes with a digest need the index");
+    }
+    if ((st->mode & 2) && (!st->P || !al16(st->P))) return fail(ctx, VKV_E_ARG, "digest modes need a 16-byte aligned P");
+    return VKV_OK;
+}
+
+// ----------------------------------------------------- workspace layout
+
+static void attend_split(const vkv_step* st, int64_t k, int64_t cap, int64_t* splits, int64_t* rps) {
+    const int64_t nmax = k + st->W + cap;
+    const int64_t groups = st->B * ((st->H + ATT_HEADS - 1) / ATT_HEADS);
+    int64_t want = std::max<int64_t>(1, (512 + groups - 1) / groups);      // ~2 workgroups per CU
+    int64_t rows = (nmax + want - 1) / want;
+    rows = std::max<int64_t>(rows, 128);
+    rows = std::min<int64_t>(rows, 4096);
+    rows = (rows + ATT_CHUNK - 1) / ATT_CHUNK * ATT_CHUNK;
+    *rps = rows;
+    *splits = std::max<int64_t>(1, (nmax + rows - 1) / rows);
+}
+
+static WsLayout layout(const vkv_step* st, int64_t k, int64_t cap) {
+    WsLayout L{};
+    const int64_t B = st->B, H = st->H;
+    L.A = st->T - st->W;
+    L.n = index_width(st);
+    L.nch = std::max<int64_t>(1, (L.A + CHUNK - 1) / CHUNK);
+    L.cap = cap;
+    const int64_t Aw = std::max<int64_t>(L.A, 1);
+    size_t o = 0;
+    L.qt = o; o = up256(o + (size_t)(B * H * L.n * 2));
+    L.wproj = o; o = up256(o + (size_t)(B * H * std::max(st->r, 1) * 8));
+    L.hsc = o; o = up256(o + (size_t)(B * H * 16));
+    L.seq = o; o = up256(o + (size_t)(B * SQ_WORDS * 4));
+    L.hist = o; o = up256(o + (size_t)(B * RADIX_BINS * 4));
+    L.flags = o; o = up256(o + (size_t)(B * Aw));
+    L.flags2 = o; o = up256(o + (size_t)(B * Aw));
+    L.ccount = o; o = up256(o + (size_t)(B * L.nch * CC_WORDS * 4));
+    L.amb = o; o = up256(o + (size_t)(B * Aw * 4));
+    L.ambkey = o; o = up256(o + (size_t)(B * Aw * 8));
+    // everything above is independent of k and cap; the attention partials last
+    attend_split(st, k, cap, &L.splits, &L.rows_per_split);
+    L.part_o = o; o = up256(o + (size_t)(B * L.splits * H * D_LAT * 4));
+    L.part_ml = o; o = up256(o + (size_t)(B * L.splits * H * 2 * 4));
+    L.total = o;
+    return L;
+}
+
+static int check_ws(vkv_ctx* ctx, const void* ws, size_t bytes, size_t need) {
+    if (!ws) return fail(ctx, VKV_E_WORKSPACE, "workspace is NULL");
+    if (((uintptr_t)ws & 255u) != 0) return fail(ctx, VKV_E_ALIGN, "workspace must be 256-byte aligned");
+    if (bytes < need) return fail(ctx, VKV_E_WORKSPACE, "workspace of %zu bytes, need %zu", bytes, need);
+    return VKV_OK;
+}
+
+static void index_operand(const vkv_step* st, const uint16_t** x, int64_t* xs, int64_t* xbs) {
+    if (st->mode == VKV_MODE_ROPE && !st->index) {
+        *x = st->cache + D_LAT;
+        *xs = st->cache_row_stride;
+        *xbs = st->cache_batch_stride;
+        return;
+    }
+    const int off = (st->mode == VKV_MODE_DIGEST && st->index_has_rope) ? D_ROPE : 0;
+    *x = st->index + off;
+    *xs = st->index_row_stride;
+    *xbs = st->index_batch_stride;
+}
+
+static SelectArgs select_args(const vkv_step* st, const WsLayout& L, char* w) {
+    SelectArgs a{};
+    index_operand(st, &a.x, &a.xs, &a.xbs);
+    a.qt = reinterpret_cast<const uint16_t*>(w + L.qt);
+    a.hsc = reinterpret_cast<const float*>(w + L.hsc);
+    a.eta = st->eta;
+    a.eps = st->eps;
+    a.gam = st->gam;
+    a.T = st->T;
+    a.seq = reinterpret_cast<uint32_t*>(w + L.seq);
+    a.hist = reinterpret_cast<uint32_t*>(w + L.hist);
+    a.flags = reinterpret_cast<uint8_t*>(w + L.flags);
+    a.flags2 = reinterpret_cast<uint8_t*>(w + L.flags2);
+    a.ccount = reinterpret_cast<uint32_t*>(w + L.ccount);
+    a.amb = reinterpret_cast<int32_t*>(w + L.amb);
+    a.ambkey = reinterpret_cast<double*>(w + L.ambkey);
+    a.A = L.A;
+    a.nch = L.nch;
+    a.B = (int)st->B;
+    a.H = (int)st->H;
+    a.n = (int)L.n;
+    return a;
+}
+
+// ------------------------------------------------------- debug row sets
+
+static int debug_check_sel(vkv_ctx* ctx, const vkv_step* st, int64_t k, const int32_t* sel, hipStream_t s) {
+    if (!ctx->debug_rows || k == 0) return VKV_OK;
+    const int64_t A = st->T - st->W;
+    std::vector<int32_t> h((size_t)(st->B * k));
+    HIP_TRY(ctx, hipMemcpyAsync(h.data(), sel, h.size() * 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(ctx, hipStreamSynchronize(s));
+    for (int64_t b = 0; b < st->B; ++b)
+        for (int64_t i = 0; i < k; ++i) {
+            const int32_t u = h[(size_t)(b * k + i)];
+            if (u < 0 || u >= A) return fail(ctx, VKV_E_DEBUG_ROWS, "sel[%lld][%lld]=%d outside the archive", (long long)b, (long long)i, u);
+            if (i > 0 && u <= h[(size_t)(b * k + i - 1)])
+                return fail(ctx, VKV_E_DEBUG_ROWS, "sel[%lld] not strictly ascending at %lld", (long long)b, (long long)i);
+        }
+    return VKV_OK;
+}
+
+static int debug_check_adm(vkv_ctx* ctx, const vkv_step* st, int64_t k, const int32_t* sel, const int32_t* adm,
+                           const int32_t* cnt, int64_t cap, hipStream_t s) {
+    if (!ctx->debug_rows) return VKV_OK;
+    const int64_t A = st->T - st->W;
+    std::vector<int32_t> hs((size_t)(st->B * std::max<int64_t>(k, 1)));
+    std::vector<int32_t> ha((size_t)(st->B * std::max<int64_t>(cap, 1)));
+    std::vector<int32_t> hc((size_t)st->B);
+    if (k) HIP_TRY(ctx, hipMemcpyAsync(hs.data(), sel, (size_t)(st->B * k) * 4, hipMemcpyDeviceToHost, s));
+    if (cap) HIP_TRY(ctx, hipMemcpyAsync(ha.data(), adm, (size_t)(st->B * cap) * 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(ctx, hipMemcpyAsync(hc.data(), cnt, (size_t)st->B * 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(ctx, hipStreamSynchronize(s));
+    for (int64_t b = 0; b < st->B; ++b) {
+        const int64_t m = std::min<int64_t>(hc[(size_t)b], cap);
+        if (hc[(size_t)b] < 0 || hc[(size_t)b] > A - k)
+            return fail(ctx, VKV_E_DEBUG_ROWS, "adm_count[%lld]=%d impossible", (long long)b, hc[(size_t)b]);
+        const int32_t* sb = hs.data() + b * k;
+        for (int64_t i = 0; i < m; ++i) {
+            const int32_t u = ha[(size_t)(b * cap + i)];
+            if (u < 0 || u >= A) return fail(ctx, VKV_E_DEBUG_ROWS, "adm[%lld][%lld]=%d outside the archive", (long long)b, (long long)i, u);
+            if (i > 0 && u <= ha[(size_t)(b * cap + i - 1)])
+                return fail(ctx, VKV_E_DEBUG_ROWS, "adm[%lld] not strictly ascending", (long long)b);
+            if (std::binary_search(sb, sb + k, u))
+                return fail(ctx, VKV_E_DEBUG_ROWS, "adm[%lld] row %d is also selected", (long long)b, u);
+        }
+    }
+    return VKV_OK;
+}
+
+// ================================================================ C ABI
+
+extern "C" {
+
+int vkv_version(void) { return 100; }
+
+const char* vkv_status_string(int status) {
+    switch (status) {
+        case VKV_OK: return "ok";
+        case VKV_E_ARG: return "invalid argument";
+        case VKV_E_SHAPE: return "unsupported shape";
+        case VKV_E_ALIGN: return "misaligned pointer or stride";
+        case VKV_E_UNSUPPORTED: return "unsupported configuration";
+        case VKV_E_NOT_CONTRACTIVE: return "digest basis not certified contractive";
+        case VKV_E_HIP: return "HIP runtime error";
+        case VKV_E_WORKSPACE: return "workspace missing or too small";
+        case VKV_E_DEBUG_ROWS: return "row-set assertion failed";
+        default: return "unknown status";
+    }
+}
+
+const char* vkv_last_error(const vkv_ctx* ctx) { return ctx ? ctx->err : g_err; }
+
+int vkv_create(vkv_ctx** out, int device) {
+    if (!out) return fail(nullptr, VKV_E_ARG, "out is NULL");
+    int ndev = 0;
+    hipError_t e = hipGetDeviceCount(&ndev);
+    if (e != hipSuccess) return fail(nullptr, VKV_E_HIP, "hipGetDeviceCount: %s", hipGetErrorString(e));
+    if (device < 0 || device >= ndev) return fail(nullptr, VKV_E_ARG, "device %d of %d", device, ndev);
+    e = hipSetDevice(device);
+    if (e != hipSuccess) return fail(nullptr, VKV_E_HIP, "hipSetDevice: %s", hipGetErrorString(e));
+    vkv_ctx* c = (vkv_ctx*)calloc(1, sizeof(vkv_ctx));
+    if (!c) return fail(nullptr, VKV_E_ARG, "out of host memory");
+    c->device = device;
+    const char* dbg = getenv("VKV_DEBUG_ROWS");
+    c->debug_rows = (dbg && dbg[0] && strcmp(dbg, "0") != 0) ? 1 : 0;
+    e = hipMalloc(&c->gram, 512 * sizeof(double));
+    if (e != hipSuccess) {
+        free(c);
+        return fail(nullptr, VKV_E_HIP, "hipMalloc: %s", hipGetErrorString(e));
+    }
+    *out = c;
+    return VKV_OK;
+}
+
+int vkv_destroy(vkv_ctx* ctx) {
+    if (!ctx) return VKV_OK;
+    (void)hipSetDevice(ctx->device);
+    (void)hipFree(ctx->gram);
+    free(ctx);
+    return VKV_OK;
+}
+
+int vkv_digest_build(vkv_ctx* ctx, const uint16_t* cache, int64_t B, int64_t T, int64_t cache_row_stride,
+                     int64_t cache_batch_stride, const uint16_t* P, int32_t r, int32_t with_rope, uint16_t* index,
+                     int64_t index_row_stride, int64_t index_batch_stride, float* eta, float* eps, float* gam,
+                     void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    hipStream_t s = (hipStream_t)stream;
+    if (!cache) return fail(ctx, VKV_E_ARG, "cache is NULL");
+    if (B < 1 || B > 65535 || T < 1 || T >= (1ll << 31)) return fail(ctx, VKV_E_SHAPE, "B=%lld T=%lld", (long long)B, (long long)T);
+    if (r < 0 || r > 512 || (r % 32)) return fail(ctx, VKV_E_UNSUPPORTED, "r=%d: need 0 or a multiple of 32 up to 512", r);
+    if (r > 0 && (!P || !al16(P))) return fail(ctx, VKV_E_ARG, "P must be a 16-byte aligned device pointer");
+    if (!al16(cache) || cache_row_stride < D_ROW || cache_row_stride % 8 || cache_batch_stride % 8 ||
+        (B > 1 && cache_batch_stride < T * cache_row_stride))
+        return fail(ctx, VKV_E_ALIGN, "cache strides");
+    const int cols = (with_rope ? D_ROPE : 0) + r;
+    if (index) {
+        if (!al16(index) || index_row_stride < cols || index_row_stride % 8 || index_batch_stride % 8 ||
+            (B > 1 && index_batch_stride < T * index_row_stride))
+            return fail(ctx, VKV_E_ALIGN, "index strides");
+    }
+    const bool cert = eta != nullptr;
+    if (cert && (!eps || !gam)) return fail(ctx, VKV_E_ARG, "eta, eps and gam go together");
+    if (!cert && !index) return fail(ctx, VKV_E_ARG, "nothing to build");
+    if (cert && r > 0) {
+        HIP_TRY(ctx, launch_gram_rows(P, r, ctx->gram, s));
+        std::vector<double> rows((size_t)r);
+        HIP_TRY(ctx, hipMemcpyAsync(rows.data(), ctx->gram, (size_t)r * 8, hipMemcpyDeviceToHost, s));
+        HIP_TRY(ctx, hipStreamSynchronize(s));
+        double g = 0.0;
+        for (double v : rows) g = std::max(g, v);
+        if (!(g <= 1.0 - 0x1p-20))
+            return fail(ctx, VKV_E_NOT_CONTRACTIVE, "Gershgorin bound of ||P||_2^2 is %.9g > 1", g);
+    }
+    DigestArgs a{cache, cache_row_stride, cache_batch_stride, P, r, with_rope ? 1 : 0, index,
+                 index_row_stride, index_batch_stride, eta, eps, gam, B, T};
+    HIP_TRY(ctx, launch_digest(a, s));
+    return VKV_OK;
+}
+
+int vkv_workspace_size(const vkv_step* st, int64_t k, int64_t cap, size_t* bytes) {
+    if (!bytes) return fail(nullptr, VKV_E_ARG, "bytes is NULL");
+    int rc = check_step(nullptr, st);
+    if (rc) return rc;
+    const int64_t A = st->T - st->W;
+    if (k < 0 || k > A) return fail(nullptr, VKV_E_ARG, "k=%lld outside [0, A=%lld]", (long long)k, (long long)A);
+    if (cap < 0 || cap > A) return fail(nullptr, VKV_E_ARG, "cap=%lld outside [0, A]", (long long)cap);
+    *bytes = layout(st, k, cap).total;
+    return VKV_OK;
+}
+
+int vkv_query_prep(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    int rc = check_step(ctx, st);
+    if (rc) return rc;
+    WsLayout L = layout(st, 0, 0);
+    if ((rc = check_ws(ctx, ws, ws_bytes, L.part_o))) return rc;
+    char* w = (char*)ws;
+    QprepArgs q{st->q_lat, st->q_rope, st->P, (int)st->B, (int)st->H, st->r, st->mode, (int)L.n,
+                reinterpret_cast<uint16_t*>(w + L.qt), reinterpret_cast<double*>(w + L.wproj),
+                reinterpret_cast<float*>(w + L.hsc), reinterpret_cast<uint32_t*>(w + L.seq)};
+    HIP_TRY(ctx, launch_qprep(q, (hipStream_t)stream));
+    return VKV_OK;
+}
+
+int vkv_score(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, float* key, float* ub, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    int rc = check_step(ctx, st);
+    if (rc) return rc;
+    WsLayout L = layout(st, 0, 0);
+    if ((rc = check_ws(ctx, ws, ws_bytes, L.part_o))) return rc;
+    if (!key && L.A > 0) return fail(ctx, VKV_E_ARG, "key is NULL");
+    if (ub && (!st->eta || !st->eps || !st->gam)) return fail(ctx, VKV_E_ARG, "ub needs eta, eps and gam");
+    if (ub && st->mode == VKV_MODE_DIGEST) return fail(ctx, VKV_E_UNSUPPORTED, "the bound needs the branch summand in the key");
+    hipStream_t s = (hipStream_t)stream;
+    char* w = (char*)ws;
+    ScoreArgs a{};
+    index_operand(st, &a.x, &a.xs, &a.xbs);
+    a.qt = reinterpret_cast<const uint16_t*>(w + L.qt);
+    a.hsc = reinterpret_cast<const float*>(w + L.hsc);
+    a.eta = st->eta;
+    a.eps = st->eps;
+    a.gam = st->gam;
+    a.T = st->T;
+    a.key = key;
+    a.ub = ub;
+    a.seq = reinterpret_cast<uint32_t*>(w + L.seq);
+    a.A = L.A;
+    a.B = (int)st->B;
+    a.H = (int)st->H;
+    a.n = (int)L.n;
+    HIP_TRY(ctx, launch_score(a, s));
+    return VKV_OK;
+}
+
+int vkv_select(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, const float* key, int32_t* sel,
+               double* theta, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    int rc = check_step(ctx, st);
+    if (rc) return rc;
+    WsLayout L = layout(st, 0, 0);
+    if ((rc = check_ws(ctx, ws, ws_bytes, L.part_o))) return rc;
+    if (k < 0 || k > L.A) return fail(ctx, VKV_E_ARG, "k=%lld outside [0, A=%lld]", (long long)k, (long long)L.A);
+    if (!theta || (k > 0 && (!sel || !key))) return fail(ctx, VKV_E_ARG, "key, sel and theta are required");
+    hipStream_t s = (hipStream_t)stream;
+    SelectArgs a = select_args(st, L, (char*)ws);
+    a.key = key;
+    a.sel = sel;
+    a.theta = theta;
+    a.k = k;
+    HIP_TRY(ctx, launch_select(a, s));
+    return debug_check_sel(ctx, st, k, sel, s);
+}
+
+int vkv_admit(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, const int32_t* sel,
+              const double* theta, const float* ub, int32_t* adm, int32_t* adm_count, int64_t cap, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    int rc = check_step(ctx, st);
+    if (rc) return rc;
+    WsLayout L = layout(st, 0, 0);
+    if ((rc = check_ws(ctx, ws, ws_bytes, L.part_o))) return rc;
+    if (st->mode == VKV_MODE_DIGEST) return fail(ctx, VKV_E_UNSUPPORTED, "admission needs the branch summand in the key");
+    if (!st->eta || !st->eps || !st->gam) return fail(ctx, VKV_E_ARG, "admission needs eta, eps and gam");
+    if (k < 0 || k > L.A) return fail(ctx, VKV_E_ARG, "k=%lld outside [0, A]", (long long)k);
+    if (cap < 0 || cap > L.A) return fail(ctx, VKV_E_ARG, "cap=%lld outside [0, A]", (long long)cap);
+    if (!theta || !adm_count || (L.A > 0 && !ub) || (cap > 0 && !adm) || (k > 0 && !sel))
+        return fail(ctx, VKV_E_ARG, "sel, theta, ub, adm and adm_count are required");
+    hipStream_t s = (hipStream_t)stream;
+    SelectArgs a = select_args(st, L, (char*)ws);
+    a.ub = ub;
+    a.sel = const_cast<int32_t*>(sel);
+    a.theta = const_cast<double*>(theta);
+    a.adm = adm;
+    a.adm_count = adm_count;
+    a.k = k;
+    a.cap = cap;
+    HIP_TRY(ctx, launch_admit(a, s));
+    return debug_check_adm(ctx, st, k, sel, adm, adm_count, cap, s);
+}
+
+int vkv_attend(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, const int32_t* sel,
+               const int32_t* adm, const int32_t* adm_count, int64_t cap, float scale, uint16_t* out, float* lse,
+               void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    int rc = check_step(ctx, st);
+    if (rc) return rc;
+    const int64_t A = st->T - st->W;
+    if (k < 0 || k > A) return fail(ctx, VKV_E_ARG, "k=%lld outside [0, A]", (long long)k);
+    if (cap < 0 || cap > A) return fail(ctx, VKV_E_ARG, "cap=%lld outside [0, A]", (long long)cap);
+    if (cap > 0 && (!adm || !adm_count)) return fail(ctx, VKV_E_ARG, "cap > 0 needs adm and adm_count");
+    if (cap == 0) {
+        adm = nullptr;
+        adm_count = nullptr;
+    }
+    if (!out || !lse || (k > 0 && !sel)) return fail(ctx, VKV_E_ARG, "sel, out and lse are required");
+    if (!al16(out)) return fail(ctx, VKV_E_ALIGN, "out must be 16-byte aligned");
+    if (!(scale > 0.f) || !(scale < 1e30f)) return fail(ctx, VKV_E_ARG, "scale must be positive and finite");
+    WsLayout L = layout(st, k, cap);
+    if ((rc = check_ws(ctx, ws, ws_bytes, L.total))) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    char* w = (char*)ws;
+    AttendArgs a{};
+    a.q_lat = st->q_lat;
+    a.q_rope = st->q_rope;
+    a.cache = st->cache;
+    a.cs = st->cache_row_stride;
+    a.cbs = st->cache_batch_stride;
+    a.sel = sel;
+    a.adm = adm;
+    a.adm_count = adm_count;
+    a.k = k;
+    a.W = st->W;
+    a.A = A;
+    a.cap = cap;
+    a.rows_per_split = L.rows_per_split;
+    a.splits = (int)L.splits;
+    a.B = (int)st->B;
+    a.H = (int)st->H;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.part_o = reinterpret_cast<float*>(w + L.part_o);
+    a.part_ml = reinterpret_cast<float*>(w + L.part_ml);
+    a.out = out;
+    a.lse = lse;
+    HIP_TRY(ctx, launch_attend(a, s));
+    return VKV_OK;
+}
+
+int vkv_step_run(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, float* key, float* ub,
+                 int32_t* sel, double* theta, int32_t* adm, int32_t* adm_count, int64_t cap, float scale, uint16_t* out,
+                 float* lse, void* stream) {
+    const bool two_tier = adm_count != nullptr;
+    int rc = vkv_query_prep(ctx, st, ws, ws_bytes, stream);
+    if (rc) return rc;
+    if ((rc = vkv_score(ctx, st, ws, ws_bytes, key, two_tier ? ub : nullptr, stream))) return rc;
+    if ((rc = vkv_select(ctx, st, ws, ws_bytes, k, key, sel, theta, stream))) return rc;
+    if (two_tier) {
+        if ((rc = vkv_admit(ctx, st, ws, ws_bytes, k, sel, theta, ub, adm, adm_count, cap, stream))) return rc;
+    }
+    return vkv_attend(ctx, st, ws, ws_bytes, k, sel, two_tier ? adm : nullptr, two_tier ? adm_count : nullptr,
+                      two_tier ? cap : 0, scale, out, lse, stream);
+}
+
+}  // extern "C"

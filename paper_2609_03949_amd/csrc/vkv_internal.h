@@ -1,0 +1,240 @@
+// vkv_internal.h -- shared declarations of the libvkv HIP sources (gfx950).
+//
+// Device helpers for bit-exact fp64 -> bf16 rounding, upward roundings used by
+// the certificate scalars, the order-preserving key encoding of the radix
+// select, and the launch interfaces of the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/vkv.h"
+
+namespace vkv {
+
+constexpr int D_LAT = 512;
+constexpr int D_ROPE = 64;
+constexpr int D_ROW = 576;
+
+// Margin that turns fp64 norm computations into rigorous upper bounds:
+// 2^-40 exceeds 16x the worst relative error of a 512-term fp64 dot product.
+constexpr double CERT_G = 0x1p-40;
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x8_t __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// ------------------------------------------------------------ bit casts
+
+__host__ __device__ __forceinline__ uint32_t f2u(float f) { return __builtin_bit_cast(uint32_t, f); }
+__host__ __device__ __forceinline__ float u2f(uint32_t u) { return __builtin_bit_cast(float, u); }
+__host__ __device__ __forceinline__ uint64_t d2u(double d) { return __builtin_bit_cast(uint64_t, d); }
+
+// ------------------------------------------------------------ bf16 helpers
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+    return __uint_as_float(((uint32_t)b) << 16);
+}
+
+// fp32 -> bf16, round to nearest even (finite inputs; NaN kept quiet).
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x0040u);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// fp64 -> bf16 in a single round-to-nearest-even step, by integer arithmetic
+// on the fp64 significand (no intermediate fp32 rounding).
+__host__ __device__ __forceinline__ uint16_t f64_to_bf16_rne(double x) {
+    uint64_t u = d2u(x);
+    uint16_t sign = (uint16_t)((u >> 48) & 0x8000u);
+    uint64_t ax = u & 0x7FFFFFFFFFFFFFFFull;
+    if (ax > 0x7FF0000000000000ull) return 0x7FC0;          // NaN
+    if (ax == 0x7FF0000000000000ull) return sign | 0x7F80;   // inf
+    int be = (int)(ax >> 52);
+    if (be == 0) return sign;                                // fp64 subnormal: far below bf16
+    int E = be - 1023;
+    if (E > 127) return sign | 0x7F80;
+    if (E < -134) return sign;
+    uint64_t m = (ax & 0x000FFFFFFFFFFFFFull) | 0x0010000000000000ull;
+    int shift = (E >= -126) ? 45 : (-81 - E);                // bits below the bf16 quantum
+    uint64_t q = m >> shift;
+    uint64_t rem = m & ((1ull << shift) - 1ull);
+    uint64_t half = 1ull << (shift - 1);
+    if (rem > half || (rem == half && (q & 1ull))) q += 1ull;
+    uint32_t bits = (E >= -126) ? (uint32_t)(((E + 127) << 7) + (int)(q - 128ull)) : (uint32_t)q;
+    if (bits > 0x7F80u) bits = 0x7F80u;
+    return (uint16_t)(sign | bits);
+}
+
+// ------------------------------------------------------- upward roundings
+
+__host__ __device__ __forceinline__ float next_up_f32(float f) {
+    uint32_t b = f2u(f);
+    if ((b & 0x7FFFFFFFu) >= 0x7F800000u) return f;          // inf / nan
+    if ((b & 0x7FFFFFFFu) == 0u) return u2f(1u);  // +-0 -> min subnormal
+    return u2f((b & 0x80000000u) ? b - 1u : b + 1u);
+}
+
+// Smallest float f with (double)f >= x.
+__host__ __device__ __forceinline__ float ru_f32(double x) {
+    float f = (float)x;
+    if ((double)f < x) f = next_up_f32(f);
+    return f;
+}
+
+// Smallest float f >= 0 with f*f >= x, decided with exact fp64 products.
+__host__ __device__ __forceinline__ float ru_sqrt_f32(double x) {
+    if (!(x > 0.0)) return 0.0f;
+    if (!(x < 0x1.fffffep+127 * 0x1.fffffep+127)) return u2f(0x7F800000u);   // beyond FLT_MAX^2
+    float f = (float)sqrt(x);                                // within an ulp of the answer
+    while ((double)f * (double)f < x) f = next_up_f32(f);
+    while (f > 0.0f) {
+        float p = u2f(f2u(f) - 1u);
+        if ((double)p * (double)p >= x) f = p;
+        else break;
+    }
+    return f;
+}
+
+// Order-preserving map float -> uint32 (larger float -> larger uint).
+__host__ __device__ __forceinline__ uint32_t key_to_ord(float f) {
+    uint32_t u = f2u(f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__host__ __device__ __forceinline__ float ord_to_key(uint32_t o) {
+    uint32_t u = (o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o;
+    return u2f(u);
+}
+
+// ----------------------------------------------------------- workspace
+
+// Per-sequence state words (uint32 each), kept in the workspace.
+enum SeqWord : int {
+    SQ_QMAX = 0,    // float bits: max_h ||qt_h|| (upper bound)
+    SQ_NU2MAX = 1,  // float bits: max_u ||x_u||^2 (fp32 sum)
+    SQ_BMAX = 2,    // float bits: max_u (amax eta + nmax eps + emax gam)
+    SQ_AMAX = 3,
+    SQ_NMAX = 4,
+    SQ_EMAX = 5,
+    SQ_EKEY = 6,    // float: certified |key - exact| bound
+    SQ_EUB = 7,     // float: certified |ub - exact| bound
+    SQ_PREFIX = 8,  // radix select: ordered-key prefix found so far
+    SQ_KREM = 9,    // radix select: rank still to find inside the prefix
+    SQ_DONE = 10,   // last-block counter
+    SQ_NIN = 11,    // rows certainly in S
+    SQ_NAMB = 12,   // ambiguous rows (select) / (admit)
+    SQ_NADM = 13,   // admitted rows (total)
+    SQ_WORDS = 16
+};
+
+constexpr int CHUNK = 2048;        // rows per classify / compaction block
+constexpr int CC_WORDS = 8;        // per-chunk counters
+enum ChunkWord : int { CC_IN = 0, CC_AMB = 1, CC_SELAMB = 2, CC_ADM = 3, CC_AAMB = 4, CC_ADMAMB = 5 };
+constexpr int RADIX_BINS = 2048;
+constexpr int ATT_CHUNK = 32;      // rows per attention tile
+constexpr int ATT_HEADS = 64;      // heads per attention workgroup (4 waves x 16)
+
+struct WsLayout {
+    size_t qt, wproj, hsc, seq, hist, flags, flags2, ccount, amb, ambkey, part_o, part_ml, total;
+    int64_t A, n, nch, splits, rows_per_split, cap;
+};
+
+// ------------------------------------------------------ kernel interfaces
+
+struct QprepArgs {
+    const uint16_t* q_lat;
+    const uint16_t* q_rope;
+    const uint16_t* P;
+    int B, H, r, mode, n;
+    uint16_t* qt;      // [B,H,n]
+    double* wproj;     // [B,H,r]
+    float* hsc;        // [B,H,4]: a, nq, e, ||qt||
+    uint32_t* seq;     // [B,SQ_WORDS]
+};
+
+struct ScoreArgs {
+    const uint16_t* x;     // index rows (already offset to the first scored column)
+    int64_t xs, xbs;       // row / batch stride, elements
+    const uint16_t* qt;    // [B,H,n]
+    const float* hsc;      // [B,H,4]
+    const float* eta;      // [B,T] (UB only)
+    const float* eps;
+    const float* gam;
+    int64_t T;
+    float* key;            // [B,A]
+    float* ub;             // [B,A] or null
+    uint32_t* seq;
+    int64_t A;
+    int B, H, n;
+};
+
+struct DigestArgs {
+    const uint16_t* cache;
+    int64_t cs, cbs;
+    const uint16_t* P;
+    int r, with_rope;
+    uint16_t* index;
+    int64_t is, ibs;
+    float* eta;
+    float* eps;
+    float* gam;
+    int64_t B, T;
+};
+
+struct SelectArgs {
+    const float* key;      // [B,A]
+    const float* ub;       // [B,A] (admit)
+    const uint16_t* x;     // index rows for fp64 re-scoring
+    int64_t xs, xbs;
+    const uint16_t* qt;
+    const float* hsc;
+    const float* eta;
+    const float* eps;
+    const float* gam;
+    int64_t T;
+    uint32_t* seq;
+    uint32_t* hist;        // [B,RADIX_BINS]
+    uint8_t* flags;        // [B,A]
+    uint8_t* flags2;       // [B,A]
+    uint32_t* ccount;      // [B,nch,CC_WORDS]
+    int32_t* amb;          // [B,A]
+    double* ambkey;        // [B,A]
+    int32_t* sel;          // [B,k]
+    double* theta;         // [B]
+    int32_t* adm;          // [B,cap]
+    int32_t* adm_count;    // [B]
+    int64_t A, k, cap, nch;
+    int B, H, n;
+};
+
+struct AttendArgs {
+    const uint16_t* q_lat;
+    const uint16_t* q_rope;
+    const uint16_t* cache;
+    int64_t cs, cbs;
+    const int32_t* sel;
+    const int32_t* adm;
+    const int32_t* adm_count;
+    int64_t k, W, A, cap;
+    int64_t rows_per_split;
+    int splits;
+    int B, H;
+    float scale_log2;      // scale * log2(e)
+    float* part_o;         // [B, splits, H, 512]
+    float* part_ml;        // [B, splits, H, 2]
+    uint16_t* out;         // [B,H,512]
+    float* lse;            // [B,H]
+};
+
+hipError_t launch_qprep(const QprepArgs& a, hipStream_t s);
+hipError_t launch_score(const ScoreArgs& a, hipStream_t s);
+hipError_t launch_digest(const DigestArgs& a, hipStream_t s);
+hipError_t launch_gram_rows(const uint16_t* P, int r, double* rowsum, hipStream_t s);
+hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+hipError_t launch_admit(const SelectArgs& a, hipStream_t s);
+hipError_t launch_attend(const AttendArgs& a, hipStream_t s);
+
+}  // namespace vkv

@@ -1,0 +1,366 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Bar: selected and admitted index sets bit-exact, theta equal in fp64, index
+digests and certificate scalars bit-exact, attention outputs within 2e-2
+relative L2 per (b, h) and lse within 1e-3.  Sizes span several tiles and a
+ragged tail; the full-size configs are checked on sampled sequences.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_03949_amd as vkv
+from paper_2609_03949_amd import synth
+
+from _harness import gpu_index, gpu_step, host_inputs, index_cols, oracle_step, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+OUT_TOL = 2e-2
+LSE_TOL = 1e-3
+
+
+def say(msg):
+    print(f"[gpu] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    vkv.load()
+    c = vkv.Context(0)
+    yield c
+    c.close()
+
+
+def check_step(wl, g, o, seqs, two_tier=False, exact_out=False):
+    for j, b in enumerate(seqs):
+        ob = o[b]
+        assert np.array_equal(g["sel"][b], ob["sel"]), f"sel differs for sequence {b}"
+        if len(ob["sel"]):
+            assert g["theta"][b] == ob["theta"], (b, g["theta"][b], ob["theta"])
+        if two_tier:
+            assert int(g["adm_count"][b]) == ob["adm_count"], (b, g["adm_count"][b], ob["adm_count"])
+            m = min(ob["adm_count"], g["adm"].shape[1])
+            assert np.array_equal(g["adm"][b, :m], ob["adm"][:m]), f"admitted set differs for {b}"
+        err = rel_l2(g["out"][b], ob["out"])
+        assert err < OUT_TOL, (b, err)
+        fin = np.isfinite(ob["lse"])
+        assert np.array_equal(fin, np.isfinite(g["lse"][b]))
+        assert np.all(np.abs(g["lse"][b][fin] - ob["lse"][fin]) < LSE_TOL)
+    return True
+
+
+# ------------------------------------------------------------ index build
+
+@pytest.mark.parametrize("basis,r,with_rope", [
+    ("orthonormal", 64, True), ("gaussian", 64, True), ("orthonormal", 256, False),
+    ("identity", 512, True), ("zero", 64, True), ("orthonormal", 32, False),
+])
+def test_digest_build_bit_exact(ctx, basis, r, with_rope):
+    say(f"digest_build basis={basis} r={r} rope={with_rope}")
+    cfg = synth.CONFIGS["cfg3"].with_(H=4)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=1000)
+    P = synth.make_basis(basis, r).cuda()
+    cert = basis != "gaussian"          # the Gaussian basis is not contractive
+    cache = wl["cache"]
+    cols = (64 if with_rope else 0) + r
+    index = torch.empty(2, 1000, cols, dtype=torch.bfloat16, device="cuda")
+    eta = torch.empty(2, 1000, device="cuda") if cert else None
+    eps = torch.empty(2, 1000, device="cuda") if cert else None
+    gam = torch.empty(2, 1000, device="cuda") if cert else None
+    vkv.digest_build(ctx, cache, P, r, with_rope, index, eta, eps, gam)
+    torch.cuda.synchronize()
+    ci = synth.to_numpy_bits(cache)
+    Pi = synth.to_numpy_bits(P)
+    oi, oe, oep, og = oracle.digest_build(ci, Pi, r, with_rope=with_rope, scalars=cert)
+    assert np.array_equal(synth.to_numpy_bits(index), oi)
+    if cert:
+        assert np.array_equal(eta.cpu().numpy().view(np.uint32), oe.view(np.uint32))
+        assert np.array_equal(eps.cpu().numpy().view(np.uint32), oep.view(np.uint32))
+        assert np.array_equal(gam.cpu().numpy().view(np.uint32), og.view(np.uint32))
+
+
+def test_digest_build_refuses_non_contractive_basis(ctx):
+    say("digest_build non-contractive")
+    wl = synth.make_workload(synth.CONFIGS["cfg0"].with_(H=2), "cuda", T=256)
+    P = synth.make_basis("gaussian", 64).cuda()     # ||P||_2 ~ 3.8
+    index = torch.full((1, 256, 128), 7, dtype=torch.int16, device="cuda").view(torch.bfloat16)
+    eta = torch.full((1, 256), 5.0, device="cuda")
+    eps = torch.full_like(eta, 5.0)
+    gam = torch.full_like(eta, 5.0)
+    with pytest.raises(vkv.VkvError) as ei:
+        vkv.digest_build(ctx, wl["cache"], P, 64, True, index, eta, eps, gam)
+    assert ei.value.code == -5
+    torch.cuda.synchronize()
+    assert torch.all(eta == 5.0) and torch.all(index.view(torch.int16) == 7)
+
+
+# ------------------------------------------------------ reduced configs
+
+REDUCED = [
+    ("cfg0", dict(T=5000)),
+    ("cfg1", dict(B=3, T=6000)),
+    ("cfg2_r64", dict(B=2, T=7000)),
+    ("cfg2_r192", dict(B=2, T=7000)),
+    ("cfg2_r256", dict(B=2, T=7000)),
+    ("cfg4", dict(B=3, T=9000)),
+]
+
+
+@pytest.mark.parametrize("name,kw", REDUCED)
+def test_step_parity_reduced(ctx, name, kw):
+    cfg = synth.CONFIGS[name]
+    say(f"step parity {name} {kw}")
+    wl = synth.make_workload(cfg, "cuda", **kw)
+    k = max(1, wl["A"] // 32) if name != "cfg0" else wl["A"] // 8
+    g, _ = gpu_step(ctx, wl, k=k)
+    seqs = list(range(wl["B"]))
+    o, _ = oracle_step(wl, seqs, k=k)
+    check_step(wl, g, o, seqs)
+
+
+def test_step_parity_two_tier_reduced(ctx):
+    cfg = synth.CONFIGS["cfg3"]
+    say("two-tier parity cfg3 reduced")
+    wl = synth.make_workload(cfg, "cuda", B=2, T=5000)
+    k = wl["A"] // 32
+    g, _ = gpu_step(ctx, wl, k=k, two_tier=True)
+    o, _ = oracle_step(wl, [0, 1], k=k, two_tier=True)
+    check_step(wl, g, o, [0, 1], two_tier=True)
+
+
+@pytest.mark.parametrize("basis,r,H", [("identity", 448, 16), ("orthonormal", 256, 8),
+                                       ("identity", 512, 4)])
+def test_two_tier_partial_admission(ctx, basis, r, H):
+    """A basis that captures most of the latent makes the bound tight enough
+    that only some rows are admitted: exercises the fp64 band decisions."""
+    say(f"two-tier partial basis={basis} r={r} H={H}")
+    cfg = synth.CONFIGS["cfg3"].with_(H=H, r=r, rows="gaussian", needles=4)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=3000, basis=basis)
+    k = 60
+    g, _ = gpu_step(ctx, wl, k=k, two_tier=True)
+    o, _ = oracle_step(wl, [0, 1], k=k, two_tier=True)
+    check_step(wl, g, o, [0, 1], two_tier=True)
+
+
+def test_two_tier_capacity_overflow(ctx):
+    say("two-tier capacity overflow")
+    cfg = synth.CONFIGS["cfg3"].with_(H=8)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=2000)
+    k = 50
+    cap = 100
+    g, _ = gpu_step(ctx, wl, k=k, two_tier=True, cap=cap)
+    o, _ = oracle_step(wl, [0, 1], k=k, two_tier=True, cap=cap)
+    for b in (0, 1):
+        assert g["adm_count"][b] == o[b]["adm_count"] > cap
+        assert np.array_equal(g["adm"][b, :cap], o[b]["adm"][:cap])
+    check_step(wl, g, o, [0, 1], two_tier=True)
+
+
+# ------------------------------------------------------------ edge cases
+
+@pytest.mark.parametrize("H", [1, 8, 24, 64, 128])
+def test_head_counts(ctx, H):
+    say(f"heads H={H}")
+    cfg = synth.CONFIGS["cfg4"].with_(H=H)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=3000)
+    g, _ = gpu_step(ctx, wl, k=97)
+    o, _ = oracle_step(wl, [0, 1], k=97)
+    check_step(wl, g, o, [0, 1])
+
+
+@pytest.mark.parametrize("mode,r", [(synth.MODE_DIGEST, 32), (synth.MODE_DIGEST, 512),
+                                    (synth.MODE_ROPE_DIGEST, 128), (synth.MODE_ROPE_DIGEST, 512),
+                                    (synth.MODE_ROPE_DIGEST, 256)])
+def test_widths(ctx, mode, r):
+    say(f"width mode={mode} r={r}")
+    cfg = synth.CONFIGS["cfg2_r64"].with_(mode=mode, r=r, H=16)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=2500)
+    g, _ = gpu_step(ctx, wl, k=77)
+    o, _ = oracle_step(wl, [0, 1], k=77)
+    check_step(wl, g, o, [0, 1])
+
+
+@pytest.mark.parametrize("k", [0, 1, 2, "A-1", "A"])
+def test_budget_extremes(ctx, k):
+    say(f"budget k={k}")
+    cfg = synth.CONFIGS["cfg0"].with_(H=16)
+    wl = synth.make_workload(cfg, "cuda", T=2100)
+    kk = {"A-1": wl["A"] - 1, "A": wl["A"]}.get(k, k)
+    g, _ = gpu_step(ctx, wl, k=kk)
+    o, _ = oracle_step(wl, [0], k=kk)
+    check_step(wl, g, o, [0])
+
+
+def test_full_budget_is_dense_attention(ctx):
+    """k = A attends every row: the output is dense attention (kill-switch)."""
+    say("k = A dense")
+    cfg = synth.CONFIGS["cfg4"].with_(H=32)
+    wl = synth.make_workload(cfg, "cuda", B=1, T=3000)
+    g, _ = gpu_step(ctx, wl, k=wl["A"])
+    cache, q_lat, q_rope, _ = host_inputs(wl, [0])
+    out, lse = oracle.attend(q_lat[0], q_rope[0], cache[0], np.arange(wl["T"], dtype=np.int32),
+                             wl["scale"])
+    assert rel_l2(g["out"][0], out) < OUT_TOL
+    assert np.max(np.abs(g["lse"][0] - lse)) < LSE_TOL
+
+
+def test_single_attended_row_is_bit_exact(ctx):
+    say("single row")
+    cfg = synth.CONFIGS["cfg0"].with_(H=16, W=0)
+    wl = synth.make_workload(cfg, "cuda", T=700)
+    g, _ = gpu_step(ctx, wl, k=1)
+    o, _ = oracle_step(wl, [0], k=1)
+    u = int(o[0]["sel"][0])
+    assert g["sel"][0][0] == u
+    cache, _, _, _ = host_inputs(wl, [0])
+    want = np.repeat(cache[0, u:u + 1, :512], 16, axis=0)
+    assert np.array_equal(g["out_bits"][0], want)
+
+
+def test_empty_attended_set(ctx):
+    say("empty set")
+    cfg = synth.CONFIGS["cfg0"].with_(H=4, W=0)
+    wl = synth.make_workload(cfg, "cuda", T=300)
+    g, _ = gpu_step(ctx, wl, k=0)
+    assert np.all(g["out"][0] == 0) and np.all(np.isneginf(g["lse"][0]))
+
+
+def test_no_archive(ctx):
+    say("W = T")
+    cfg = synth.CONFIGS["cfg4"].with_(H=16, W=512)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=512)
+    g, _ = gpu_step(ctx, wl, k=0)
+    o, _ = oracle_step(wl, [0, 1], k=0)
+    check_step(wl, g, o, [0, 1])
+
+
+def test_all_equal_keys_take_lowest_indices(ctx):
+    """q_rope = 0 and a zero digest query: every key ties at 0."""
+    say("all ties")
+    cfg = synth.CONFIGS["cfg1"].with_(H=8)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=3000)
+    wl["q_rope"].zero_()
+    g, _ = gpu_step(ctx, wl, k=300)
+    for b in range(2):
+        assert np.array_equal(g["sel"][b], np.arange(300))
+        assert g["theta"][b] == 0.0
+    o, _ = oracle_step(wl, [0, 1], k=300)
+    check_step(wl, g, o, [0, 1])
+
+
+def test_duplicated_rows_and_near_ties(ctx):
+    """Rows duplicated many times (exact ties of the exact key) and rows a
+    few ulps apart at the threshold."""
+    say("duplicates / near ties")
+    cfg = synth.CONFIGS["cfg4"].with_(H=16)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=4000)
+    c = wl["cache"]
+    src = torch.randint(0, 50, (3000,), generator=torch.Generator().manual_seed(3)).cuda()
+    c[:, :3000] = c[:, src]
+    # perturb some copies by one bf16 ulp in one coordinate
+    bits = c.view(torch.int16)
+    bits[:, 1000:1200, 5] += 1
+    g, _ = gpu_step(ctx, wl, k=400)
+    o, _ = oracle_step(wl, [0, 1], k=400)
+    check_step(wl, g, o, [0, 1])
+
+
+def test_cancellation_heavy_scores_stay_within_bound(ctx):
+    """Index rows built so that each score is a sum of large terms that cancel:
+    the fp32 MFMA key must stay within the certified bound, and selection
+    stays exact."""
+    say("cancellation")
+    cfg = synth.CONFIGS["cfg1"].with_(H=16)
+    wl = synth.make_workload(cfg, "cuda", B=1, T=4096)
+    r = wl["cache"][0, :, 512:].float()
+    big = torch.randn(4096, 32, device="cuda", generator=torch.Generator("cuda").manual_seed(5)) * 64
+    r[:, :32] = big
+    r[:, 32:] = -big + 1e-2 * torch.randn(4096, 32, device="cuda")
+    wl["cache"][0, :, 512:] = r.to(torch.bfloat16)
+    q = torch.ones(16, 64, device="cuda") + 1e-3 * torch.randn(16, 64, device="cuda")
+    wl["q_rope"][0] = q.to(torch.bfloat16)
+    g, _ = gpu_step(ctx, wl, k=128)
+    o, _ = oracle_step(wl, [0], k=128)
+    key = o[0]["key"]
+    cache, _, q_rope, _ = host_inputs(wl, [0])
+    xn = np.linalg.norm(oracle.decode_bf16(cache[0, :, 512:]), axis=1).max()
+    qn = np.linalg.norm(oracle.decode_bf16(q_rope[0]), axis=1).max()
+    bound = 8 * 64 * 2.0 ** -23 * qn * xn
+    err = np.max(np.abs(g["key"][0, :wl["A"]].astype(np.float64) - key))
+    say(f"max key error {err:.3e}, bound {bound:.3e}")
+    assert err <= bound / 8
+    check_step(wl, g, o, [0])
+
+
+def test_determinism(ctx):
+    say("determinism")
+    cfg = synth.CONFIGS["cfg3"].with_(H=16)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=4000)
+    g1, _ = gpu_step(ctx, wl, k=100, two_tier=True)
+    g2, _ = gpu_step(ctx, wl, k=100, two_tier=True)
+    for key in ("sel", "theta", "out_bits", "lse", "adm", "adm_count", "key", "ub"):
+        assert np.array_equal(g1[key], g2[key]), key
+
+
+def test_debug_rows_assertion_passes(ctx, monkeypatch):
+    say("VKV_DEBUG_ROWS")
+    monkeypatch.setenv("VKV_DEBUG_ROWS", "1")
+    c = vkv.Context(0)
+    cfg = synth.CONFIGS["cfg3"].with_(H=8)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=2000)
+    g, _ = gpu_step(c, wl, k=64, two_tier=True)
+    o, _ = oracle_step(wl, [0, 1], k=64, two_tier=True)
+    check_step(wl, g, o, [0, 1], two_tier=True)
+    c.close()
+
+
+def test_argument_errors_leave_outputs_untouched(ctx):
+    say("argument errors")
+    cfg = synth.CONFIGS["cfg0"].with_(H=4)
+    wl = synth.make_workload(cfg, "cuda", T=500)
+    index, has_rope, *_ = gpu_index(ctx, wl, False)
+    step = vkv.Step(wl["cache"], wl["q_lat"], wl["q_rope"], wl["W"], wl["mode"], wl["r"],
+                    index=index, index_has_rope=has_rope, P=wl["P"])
+    bufs = vkv.Buffers(step, 10)
+    bufs.sel.fill_(-7)
+    with pytest.raises(vkv.VkvError) as ei:
+        vkv.select(ctx, step, bufs.ws, wl["A"] + 1, bufs.key, bufs.sel, bufs.theta)
+    assert ei.value.code == -1
+    with pytest.raises(vkv.VkvError) as ei:
+        vkv.query_prep(ctx, step, bufs.ws[:128])
+    assert ei.value.code == -7
+    torch.cuda.synchronize()
+    assert torch.all(bufs.sel == -7)
+
+
+# ------------------------------------------------------- full-size configs
+
+FULL = ["cfg0", "cfg1", "cfg2_r64", "cfg2_r128", "cfg2_r192", "cfg2_r256", "cfg3", "cfg4"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_config_sampled(ctx, name):
+    """Each config at its full size, in the bench's launch configuration,
+    checked on the first and last sequence (the oracle computes those whole)."""
+    cfg = synth.CONFIGS[name]
+    say(f"full-size {synth.describe(cfg)}")
+    wl = synth.make_workload(cfg, "cuda")
+    g, _ = gpu_step(ctx, wl, two_tier=cfg.two_tier)
+    seqs = sorted({0, wl["B"] - 1})
+    o, _ = oracle_step(wl, seqs, two_tier=cfg.two_tier, nthreads=0)
+    check_step(wl, g, o, seqs, two_tier=cfg.two_tier)
+    if cfg.two_tier:
+        frac = [g["adm_count"][b] / (wl["A"] - wl["k"]) for b in seqs]
+        say(f"admitted fraction of non-selected archive rows: {frac}")
+    needles = [len(np.intersect1d(g["sel"][b], wl["needles"][b].numpy())) / max(1, len(wl["needles"][b]))
+               for b in seqs]
+    say(f"needle recall of S (context only): {needles}")
+    del wl
+    torch.cuda.empty_cache()

@@ -173,7 +173,7 @@ def test_digest_zero_basis_gives_full_norm_certificate(oracle_mod):
     assert np.all(index[0, :, 64:] == 0)
     cn = np.linalg.norm(dec(lat), axis=1)
     assert np.all(eta[0] >= cn) and np.allclose(eta[0], cn, rtol=1e-6)
-    assert np.all(eps[0] == 0) and np.all(gam[0] == 0)
+    assert np.all(eps[0] <= 1e-8 * cn) and np.all(gam[0] <= 1e-8 * cn)
 
 
 def test_digest_random_basis_against_exact_rationals(oracle_mod):
