@@ -6,7 +6,7 @@
 // in one rounding, then the upper bounds
 //   eta_u >= sqrt(c^T (I - P^T P) c),  eps_u >= ||d - P c||,  gamma_u >= ||P c||
 // evaluated in a fixed fp64 order and rounded toward +inf.  Not on the
-// per-step path.  A block owns 32 rows (16 when r > 256); the basis is held
+// per-step path.  A block owns 32 rows; the basis is held
 // transposed in LDS, 64 columns at a time.
 #include "vkv_internal.h"
 
@@ -113,30 +113,48 @@ hipError_t launch_digest(const DigestArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
-// Gershgorin row sums of P P^T: rowsum[j] = sum_k |sum_i P[j,i] P[k,i]|.
-__global__ __launch_bounds__(256) void gram_rows_kernel(const uint16_t* P, int r, double* rowsum) {
-    __shared__ double s_red[256];
+// Gershgorin row sums of P P^T: rowsum[j] = sum_k |sum_i P[j,i] P[k,i]|, with
+// flag[j] = 1 if any fp64 addition on the way rounded (TwoSum error != 0).
+// bf16 products are exact in fp64, so flag 0 means rowsum[j] is exact.
+__device__ __forceinline__ double two_sum_add(double a, double b, int* inexact) {
+    const double s = a + b;
+    const double bp = s - a;
+    const double err = (a - (s - bp)) + (b - bp);
+    if (err != 0.0) *inexact = 1;
+    return s;
+}
+
+__global__ __launch_bounds__(256) void gram_rows_kernel(const uint16_t* P, int r, double* rowsum, double* flag) {
+    __shared__ double s_g[512];
+    __shared__ int s_f[512];
     const int j = blockIdx.x;
     const int tid = threadIdx.x;
-    double part = 0.0;
     for (int k = tid; k < r; k += 256) {
         double gk = 0.0;
-        for (int i = 0; i < D_LAT; ++i)
-            gk = fma((double)bf16_to_f32(P[(int64_t)j * D_LAT + i]), (double)bf16_to_f32(P[(int64_t)k * D_LAT + i]), gk);
-        part += fabs(gk);
+        int inexact = 0;
+        for (int i = 0; i < D_LAT; ++i) {
+            const double p = (double)bf16_to_f32(P[(int64_t)j * D_LAT + i]) * (double)bf16_to_f32(P[(int64_t)k * D_LAT + i]);
+            gk = two_sum_add(gk, p, &inexact);
+        }
+        s_g[k] = gk;
+        s_f[k] = inexact;
     }
-    s_red[tid] = part;
     __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
-        if (tid < w) s_red[tid] += s_red[tid + w];
-        __syncthreads();
+    if (tid == 0) {
+        double acc = 0.0;
+        int inexact = 0;
+        for (int k = 0; k < r; ++k) {
+            acc = two_sum_add(acc, fabs(s_g[k]), &inexact);
+            inexact |= s_f[k];
+        }
+        rowsum[j] = acc;
+        flag[j] = inexact ? 1.0 : 0.0;
     }
-    if (tid == 0) rowsum[j] = s_red[0];
 }
 
 hipError_t launch_gram_rows(const uint16_t* P, int r, double* rowsum, hipStream_t s) {
     if (r <= 0) return hipSuccess;
-    hipLaunchKernelGGL(gram_rows_kernel, dim3(r), dim3(256), 0, s, P, r, rowsum);
+    hipLaunchKernelGGL(gram_rows_kernel, dim3(r), dim3(256), 0, s, P, r, rowsum, rowsum + 512);
     return hipGetLastError();
 }
 

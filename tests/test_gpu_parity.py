@@ -305,8 +305,11 @@ def test_determinism(ctx):
     wl = synth.make_workload(cfg, "cuda", B=2, T=4000)
     g1, _ = gpu_step(ctx, wl, k=100, two_tier=True)
     g2, _ = gpu_step(ctx, wl, k=100, two_tier=True)
-    for key in ("sel", "theta", "out_bits", "lse", "adm", "adm_count", "key", "ub"):
+    for key in ("sel", "theta", "out_bits", "lse", "adm_count", "key", "ub"):
         assert np.array_equal(g1[key], g2[key]), key
+    for b in range(2):
+        m = int(g1["adm_count"][b])
+        assert np.array_equal(g1["adm"][b, :m], g2["adm"][b, :m])
 
 
 def test_debug_rows_assertion_passes(ctx, monkeypatch):
