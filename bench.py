@@ -122,9 +122,9 @@ def main():
         mark(0)
         vkv.query_prep(ctx, step, bufs.ws, stream)
         mark(1)
-        vkv.score(ctx, step, bufs.ws, bufs.key, bufs.ub, stream)
+        vkv.score(ctx, step, bufs.ws, None, bufs.ub, stream)
         mark(2)
-        vkv.select(ctx, step, bufs.ws, k, bufs.key, bufs.sel, bufs.theta, stream)
+        vkv.select(ctx, step, bufs.ws, k, bufs.sel, bufs.theta, stream)
         mark(3)
         j = 3
         if two_tier:

@@ -160,11 +160,14 @@ int vkv_query_prep(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, 
 /*
  * Index scores (Eq. (trigger), first two terms; lambda > 0 dropped as it does
  * not change the ranking):
- *   key[b,u] ~= max_h  sum_d qt[b,h,d] x_u[d],   u in [0, A)
- * with x_u the mode's index row and qt = [q_rope ; RNE_bf16(P q_lat)].  Computed
- * with bf16 MFMA and fp32 accumulation; the workspace records a certified
- * bound E on |key - exact| that vkv_select uses.  If ub != NULL (two-tier mode;
- * needs st->eta/eps/gam), also
+ *   key~[b,u] ~= max_h  sum_d qt[b,h,d] x_u[d],   u in [0, A)
+ * with x_u the mode's index row and qt from vkv_query_prep.  bf16 MFMA with
+ * fp32 accumulation.  For every row the workspace receives the certified
+ * interval [key~ - E_u, key~ + E_u] of the fp64 index score, where
+ *   E_u = 2 (n + n/32) 2^-23 max_h ||qt_h|| ||x_u||
+ * bounds the fp32 accumulation error (Cauchy-Schwarz on sum |q_d x_d|);
+ * vkv_select uses these intervals.  key (may be NULL) receives key~ itself,
+ * for diagnostics.  If ub != NULL (two-tier mode; needs st->eta/eps/gam), also
  *   ub[b,u] ~= max_h ( s^_h(u) + a_h eta_u + n_h eps_u + e_h gam_u )
  * the Cauchy-Schwarz upper bound of the full score (Lemma (Index certificate)).
  * key, ub: [B, A] fp32, contiguous.  ws is the workspace vkv_query_prep filled
@@ -176,14 +179,15 @@ int vkv_score(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, float
 
 /*
  * Exact top-k: S_b = the first k rows of [0, A) ordered by (exact index score
- * desc, row index asc), written ascending to sel[b*k .. b*k+k).  Rows whose
- * fp32 key lies within the certified band of the k-th key are re-scored in
- * fp64 (fixed order: d ascending) so the set equals the fp64 definition bit
+ * desc, row index asc), written ascending to sel[b*k .. b*k+k).  The exact
+ * score is the fp64 dot product with d ascending; rows whose certified
+ * interval (from vkv_score) can decide the question are classified from it,
+ * the others are re-scored in fp64, so the set equals the fp64 definition bit
  * for bit.  theta[b] (fp64) = min over S_b of the exact score (-inf if k = 0).
- * 0 <= k <= A.  key is the output of vkv_score with the same ws.
+ * 0 <= k <= A.  Reads the intervals vkv_score left in ws.
  */
 int vkv_select(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k,
-               const float* key, int32_t* sel, double* theta, void* stream);
+               int32_t* sel, double* theta, void* stream);
 
 /*
  * Two-tier admission (Lemma (Index certificate) with the bf16 rounding of the

@@ -84,7 +84,7 @@ def load():
     lib.vkv_workspace_size.argtypes = [sp, i64, i64, ctypes.POINTER(ctypes.c_size_t)]
     lib.vkv_query_prep.argtypes = [P, sp, P, ctypes.c_size_t, P]
     lib.vkv_score.argtypes = [P, sp, P, ctypes.c_size_t, P, P, P]
-    lib.vkv_select.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P, P]
+    lib.vkv_select.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P]
     lib.vkv_admit.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P, P, P, i64, P]
     lib.vkv_attend.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P, i64, ctypes.c_float, P, P, P]
     lib.vkv_step_run.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P, P, P, P, i64,
@@ -206,16 +206,16 @@ def query_prep(ctx: Context, step: Step, ws: torch.Tensor, stream=None):
     ctx.check(ctx.lib.vkv_query_prep(ctx.handle, step.ref, _ptr(ws), ws.numel(), _stream(stream)))
 
 
-def score(ctx: Context, step: Step, ws: torch.Tensor, key: torch.Tensor,
+def score(ctx: Context, step: Step, ws: torch.Tensor, key: Optional[torch.Tensor] = None,
           ub: Optional[torch.Tensor] = None, stream=None):
     ctx.check(ctx.lib.vkv_score(ctx.handle, step.ref, _ptr(ws), ws.numel(), _ptr(key), _ptr(ub),
                                 _stream(stream)))
 
 
-def select(ctx: Context, step: Step, ws: torch.Tensor, k: int, key: torch.Tensor,
-           sel: torch.Tensor, theta: torch.Tensor, stream=None):
-    ctx.check(ctx.lib.vkv_select(ctx.handle, step.ref, _ptr(ws), ws.numel(), int(k), _ptr(key),
-                                 _ptr(sel), _ptr(theta), _stream(stream)))
+def select(ctx: Context, step: Step, ws: torch.Tensor, k: int, sel: torch.Tensor,
+           theta: torch.Tensor, stream=None):
+    ctx.check(ctx.lib.vkv_select(ctx.handle, step.ref, _ptr(ws), ws.numel(), int(k), _ptr(sel),
+                                 _ptr(theta), _stream(stream)))
 
 
 def admit(ctx: Context, step: Step, ws: torch.Tensor, k: int, sel: torch.Tensor,

@@ -88,17 +88,37 @@ __global__ __launch_bounds__(ATT_THREADS, 2) void attend_kernel(AttendArgs a) {
         __syncthreads();
         if (tid < ATT_CHUNK) s_rows[tid] = (tid < nr) ? attended_row(a, b, c0 + tid) : 0;
         __syncthreads();
-        for (int p = tid; p < ATT_CHUNK * (D_ROW / 8); p += ATT_THREADS) {
-            const int rl = p / (D_ROW / 8), pc = p % (D_ROW / 8);
-            u16x8_t v = u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
-            if (rl < nr) v = *reinterpret_cast<const u16x8_t*>(cb + (int64_t)s_rows[rl] * a.cs + 8 * pc);
-            *reinterpret_cast<u16x8_t*>(&s_k[rl][8 * pc]) = v;
-            if (pc < D_LAT / 8) {
-                const int pos = pv_slot(rl);
+        // gather: 32 rows x 72 pieces of 16 B = 9 pieces per thread, loaded in
+        // three batches of three (each batch in flight together; the register
+        // budget does not allow all nine)
+        constexpr int NPIECE = ATT_CHUNK * (D_ROW / 8) / ATT_THREADS;
+        constexpr int NBATCH = 3;
+        static_assert(NPIECE * ATT_THREADS == ATT_CHUNK * (D_ROW / 8), "tile must split evenly");
+        static_assert(NPIECE % NBATCH == 0, "batches must split evenly");
+#pragma unroll 1
+        for (int j0 = 0; j0 < NPIECE; j0 += NBATCH) {
+            u16x8_t v[NBATCH];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int e2 = (e + pc) & 7;
-                    s_vt[8 * pc + e2][pos] = v[e2];
+            for (int j = 0; j < NBATCH; ++j) {
+                const int p = tid + ATT_THREADS * (j0 + j);
+                const int rl = p / (D_ROW / 8), pc = p % (D_ROW / 8);
+                v[j] = (rl < nr) ? *reinterpret_cast<const u16x8_t*>(cb + (int64_t)s_rows[rl] * a.cs + 8 * pc)
+                                 : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+            }
+#pragma unroll
+            for (int j = 0; j < NBATCH; ++j) {
+                const int p = tid + ATT_THREADS * (j0 + j);
+                const int rl = p / (D_ROW / 8), pc = p % (D_ROW / 8);
+                *reinterpret_cast<u16x8_t*>(&s_k[rl][8 * pc]) = v[j];
+                if (pc < D_LAT / 8) {
+                    // staggered element order spreads the 64 lanes over the LDS banks
+                    const int pos = pv_slot(rl);
+                    const int rot = pc + (pc >> 3);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int e2 = (e + rot) & 7;
+                        s_vt[8 * pc + e2][pos] = v[j][e2];
+                    }
                 }
             }
         }

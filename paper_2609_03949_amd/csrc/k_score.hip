@@ -18,92 +18,164 @@ namespace vkv {
 
 // Stage 1: w[b,h,j] = sum_i P[j,i] q_lat[b,h,i] (fp64, i ascending) and the
 // query digest qt[b,h,off+j] = RNE_bf16(w).  A block owns 64 basis rows (held
-// transposed in LDS) and 4 heads.  Block (0,0,b) also clears the step state.
+// transposed in LDS) and 16 heads; each thread runs four independent fp64
+// chains (four heads).  Block (0,0,b) also clears the step state of b.
+constexpr int QP_HEADS = 16;
+
 __global__ __launch_bounds__(256) void qprep_project_kernel(QprepArgs a) {
     __shared__ uint16_t s_pt[D_LAT][66];   // P^T tile, padded against bank conflicts
-    __shared__ double s_q[4][D_LAT];
+    __shared__ float s_q[QP_HEADS][D_LAT];
     const int b = blockIdx.z;
     const int tid = threadIdx.x;
-    if (blockIdx.x == 0 && blockIdx.y == 0 && tid < SQ_WORDS) a.seq[b * SQ_WORDS + tid] = 0u;
+    if (blockIdx.x == 0 && blockIdx.y == 0) {
+        if (tid < SQ_WORDS) a.seq[b * SQ_WORDS + tid] = (tid == SQ_KMIN) ? 0xFFFFFFFFu : 0u;
+        for (int i = tid; i < 2 * HIST_BINS; i += 256) a.hist[(int64_t)b * 2 * HIST_BINS + i] = 0u;
+    }
     if (a.r == 0 || !(a.mode & 2)) return;
     const int j0 = 64 * blockIdx.x;
     const int jn = min(64, a.r - j0);
-    const int h0 = 4 * blockIdx.y;
-    for (int idx = tid; idx < jn * D_LAT; idx += 256) {
-        int jl = idx / D_LAT, i = idx % D_LAT;
-        s_pt[i][jl] = a.P[(int64_t)(j0 + jl) * D_LAT + i];
-    }
-    for (int idx = tid; idx < 4 * D_LAT; idx += 256) {
-        int hl = idx / D_LAT, i = idx % D_LAT;
-        int h = h0 + hl;
-        s_q[hl][i] = (h < a.H) ? (double)bf16_to_f32(a.q_lat[((int64_t)b * a.H + h) * D_LAT + i]) : 0.0;
+    const int h0 = QP_HEADS * blockIdx.y;
+    {
+        // P rows j0.. as 16-byte pieces (64 per row), all loads in flight together
+        constexpr int PPT = 64 * 64 / 256;   // pieces per thread for a full 64-row tile
+        u16x8_t pv[PPT];
+#pragma unroll
+        for (int j = 0; j < PPT; ++j) {
+            const int idx = tid + 256 * j;
+            const int jl = idx >> 6, p = idx & 63;
+            pv[j] = (jl < jn) ? *reinterpret_cast<const u16x8_t*>(a.P + (int64_t)(j0 + jl) * D_LAT + 8 * p)
+                              : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+        }
+        constexpr int QPT = QP_HEADS * 64 / 256;
+        u16x8_t qv[QPT];
+#pragma unroll
+        for (int j = 0; j < QPT; ++j) {
+            const int idx = tid + 256 * j;
+            const int hl = idx >> 6, p = idx & 63;
+            const int h = h0 + hl;
+            qv[j] = (h < a.H) ? *reinterpret_cast<const u16x8_t*>(a.q_lat + ((int64_t)b * a.H + h) * D_LAT + 8 * p)
+                              : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+        }
+#pragma unroll
+        for (int j = 0; j < PPT; ++j) {
+            const int idx = tid + 256 * j;
+            const int jl = idx >> 6, p = idx & 63;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) s_pt[8 * p + e][jl] = pv[j][e];
+        }
+#pragma unroll
+        for (int j = 0; j < QPT; ++j) {
+            const int idx = tid + 256 * j;
+            const int hl = idx >> 6, p = idx & 63;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) s_q[hl][8 * p + e] = bf16_to_f32(qv[j][e]);
+        }
     }
     __syncthreads();
-    const int hl = tid >> 6, jl = tid & 63;
-    const int h = h0 + hl, j = j0 + jl;
-    if (h >= a.H || jl >= jn) return;
-    double acc = 0.0;
-    for (int i = 0; i < D_LAT; ++i) acc = fma((double)bf16_to_f32(s_pt[i][jl]), s_q[hl][i], acc);
-    const int64_t bh = (int64_t)b * a.H + h;
-    a.wproj[bh * a.r + j] = acc;
+    const int jl = tid & 63, hg = tid >> 6;
+    if (jl >= jn) return;
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll 4
+    for (int i = 0; i < D_LAT; ++i) {
+        const double p = (double)bf16_to_f32(s_pt[i][jl]);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[t] = fma(p, (double)s_q[4 * hg + t][i], acc[t]);
+    }
     const int off = (a.mode & 1) ? D_ROPE : 0;
-    a.qt[bh * a.n + off + j] = f64_to_bf16_rne(acc);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const int h = h0 + 4 * hg + t;
+        if (h >= a.H) continue;
+        const int64_t bh = (int64_t)b * a.H + h;
+        a.wproj[bh * a.r + j0 + jl] = acc[t];
+        a.qt[bh * a.n + off + j0 + jl] = f64_to_bf16_rne(acc[t]);
+    }
 }
 
-// Stage 2 (one wave per head): certificate scalars of the head, each an fp32
+// Stage 2 (16 heads per wave): certificate scalars of each head, each an fp32
 // upper bound (Lemma (Index certificate) plus the bf16 rounding of the stored
-// sketch; fixed fp64 evaluation order):
+// sketch; fixed fp64 evaluation order, the same as the oracle's):
 //   a_h >= sqrt(q^T (I - P^T P) q),  n_h >= ||qd_h||,  e_h >= ||qd_h - P q||
-// plus ||qt_h|| for the scorer's error bound, and the rope half of qt.
+// plus ||qt_h|| for the scorer's error bound, and the rope half of qt.  Lane
+// 4*hl + t runs sum t of head hl sequentially: t=0 ||q||^2, t=1 ||w||^2,
+// t=2 ||qd - w||^2, t=3 ||qd||^2.
+constexpr int QF_HEADS = 16;
+
 __global__ __launch_bounds__(64) void qprep_finish_kernel(QprepArgs a) {
-    const int bh = blockIdx.x;
-    const int b = bh / a.H;
     const int lane = threadIdx.x;
-    const uint16_t* q = a.q_lat + (int64_t)bh * D_LAT;
-    const double* w = a.wproj + (int64_t)bh * a.r;
-    uint16_t* qt = a.qt + (int64_t)bh * a.n;
+    const int hl = lane >> 2, t = lane & 3;
+    const int64_t bh = (int64_t)blockIdx.x * QF_HEADS + hl;
+    const bool have = bh < (int64_t)a.B * a.H;
+    const int64_t bhc = have ? bh : 0;
+    const int b = (int)(bhc / a.H);
     const int off = (a.mode & 1) ? D_ROPE : 0;
     const int rd = (a.mode & 2) ? a.r : 0;
-    if (a.mode & 1) qt[lane] = a.q_rope[(int64_t)bh * D_ROPE + lane];
-    // four sequential fp64 sums, one per lane, in the oracle's order
+    uint16_t* qt = a.qt + bhc * a.n;
+    const double* w = a.wproj + bhc * a.r;
+    // rope half of qt: 8 pieces of 16 B per head, 4 lanes per head
+    if ((a.mode & 1) && have) {
+        const u16x8_t* src = reinterpret_cast<const u16x8_t*>(a.q_rope + bhc * D_ROPE);
+        u16x8_t* dst = reinterpret_cast<u16x8_t*>(qt);
+        dst[t] = src[t];
+        dst[t + 4] = src[t + 4];
+    }
     double acc = 0.0;
-    if (lane == 0) {
-        for (int i = 0; i < D_LAT; ++i) {
-            double v = (double)bf16_to_f32(q[i]);
-            acc = fma(v, v, acc);
-        }
-    } else if (lane == 1) {
-        for (int j = 0; j < rd; ++j) acc = fma(w[j], w[j], acc);
-    } else if (lane == 2) {
-        for (int j = 0; j < rd; ++j) {
-            double t = (double)bf16_to_f32(qt[off + j]) - w[j];
-            acc = fma(t, t, acc);
-        }
-    } else if (lane == 3) {
-        for (int j = 0; j < rd; ++j) {
-            double d = (double)bf16_to_f32(qt[off + j]);
-            acc = fma(d, d, acc);
+    if (have) {
+        if (t == 0) {
+            const u16x8_t* q = reinterpret_cast<const u16x8_t*>(a.q_lat + bhc * D_LAT);
+#pragma unroll 1
+            for (int p0 = 0; p0 < D_LAT / 8; p0 += 8) {
+                u16x8_t v[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) v[j] = q[p0 + j];
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const double x = (double)bf16_to_f32(v[j][e]);
+                        acc = fma(x, x, acc);
+                    }
+            }
+        } else if (t == 1) {
+#pragma unroll 8
+            for (int j = 0; j < rd; ++j) acc = fma(w[j], w[j], acc);
+        } else {
+            const uint16_t* qd = qt + off;
+#pragma unroll 8
+            for (int j = 0; j < rd; ++j) {
+                const double d = (double)bf16_to_f32(qd[j]);
+                if (t == 2) {
+                    const double e = d - w[j];
+                    acc = fma(e, e, acc);
+                } else {
+                    acc = fma(d, d, acc);
+                }
+            }
         }
     }
-    const double Nq = __shfl(acc, 0), Nw = __shfl(acc, 1), Ne = __shfl(acc, 2), Nd = __shfl(acc, 3);
-    // ||qt_h||^2 over all n columns (an upper bound only; order irrelevant)
-    double s2 = 0.0;
-    for (int d = lane; d < a.n; d += 64) {
-        double v = (double)bf16_to_f32(qt[d]);
-        s2 += v * v;
+    const int base = lane & ~3;
+    const double Nq = __shfl(acc, base + 0), Nw = __shfl(acc, base + 1);
+    const double Ne = __shfl(acc, base + 2), Nd = __shfl(acc, base + 3);
+    // ||q_rope||^2 (an upper-bound input only; order irrelevant)
+    double r2 = 0.0;
+    if ((a.mode & 1) && have) {
+        for (int i = t; i < D_ROPE; i += 4) {
+            const double v = (double)bf16_to_f32(a.q_rope[bhc * D_ROPE + i]);
+            r2 += v * v;
+        }
     }
-    for (int o = 32; o > 0; o >>= 1) s2 += __shfl_xor(s2, o);
-    if (lane == 0) {
+    r2 += __shfl_xor(r2, 1);
+    r2 += __shfl_xor(r2, 2);
+    if (t == 0 && have) {
         const double G = CERT_G;
-        double Dm = G * (double)ru_sqrt_f32((double)rd * Nq);
-        double sw = (double)ru_sqrt_f32(Nw);
-        double X = ((Nq - Nw) + G * (Nq + Nw)) + (2.0 * Dm) * sw;
-        float ah = ru_sqrt_f32((X > 0.0 ? X : 0.0) * (1.0 + G));
-        float eh = ru_f32((double)ru_sqrt_f32(Ne) * (1.0 + G) + Dm);
-        float nh = ru_sqrt_f32(Nd * (1.0 + G));
-        float qn = ru_sqrt_f32(s2 * (1.0 + 0x1p-30));
-        float4 hs = make_float4(ah, nh, eh, qn);
-        reinterpret_cast<float4*>(a.hsc)[bh] = hs;
+        const double Dm = G * (double)ru_sqrt_f32((double)rd * Nq);
+        const double sw = (double)ru_sqrt_f32(Nw);
+        const double X = ((Nq - Nw) + G * (Nq + Nw)) + (2.0 * Dm) * sw;
+        const float ah = ru_sqrt_f32((X > 0.0 ? X : 0.0) * (1.0 + G));
+        const float eh = ru_f32((double)ru_sqrt_f32(Ne) * (1.0 + G) + Dm);
+        const float nh = ru_sqrt_f32(Nd * (1.0 + G));
+        const float qn = ru_sqrt_f32((r2 + Nd) * (1.0 + 0x1p-30));
+        reinterpret_cast<float4*>(a.hsc)[bhc] = make_float4(ah, nh, eh, qn);
         uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
         atomicMax(sq + SQ_QMAX, __float_as_uint(qn));
         atomicMax(sq + SQ_AMAX, __float_as_uint(ah));
@@ -114,11 +186,11 @@ __global__ __launch_bounds__(64) void qprep_finish_kernel(QprepArgs a) {
 
 hipError_t launch_qprep(const QprepArgs& a, hipStream_t s) {
     int jt = (a.r > 0 && (a.mode & 2)) ? (a.r + 63) / 64 : 1;
-    dim3 g1(jt, (a.H + 3) / 4, a.B);
+    dim3 g1(jt, (a.H + QP_HEADS - 1) / QP_HEADS, a.B);
     hipLaunchKernelGGL(qprep_project_kernel, g1, dim3(256), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(qprep_finish_kernel, dim3(a.B * a.H), dim3(64), 0, s, a);
+    hipLaunchKernelGGL(qprep_finish_kernel, dim3((a.B * a.H + QF_HEADS - 1) / QF_HEADS), dim3(64), 0, s, a);
     return hipGetLastError();
 }
 
@@ -138,7 +210,84 @@ __device__ __forceinline__ float wave_max_all(float m) {
     return m;
 }
 
+__device__ __forceinline__ float next_down_f32(float f) { return -next_up_f32(-f); }
+
+// Per-row certified interval of the key: |key~_u - key_u| <= E_u with
+//   E_u = 2 (n + n/32) 2^-23 max_h ||qt_h|| ||x_u||  (+ a subnormal term),
+// the fp32 MFMA accumulation bound (each of the <= n + n/32 fp32 additions of
+// the dot product errs by at most 2^-23 of a partial sum bounded by
+// sum_d |q_d x_d| <= ||qt|| ||x|| by Cauchy-Schwarz; factor 2 of slack).  The
+// scorer stores (key~ + E_u, key~ - E_u) rounded outward.
+struct RowBand {
+    float ec, eabs;
+};
+
+__device__ __forceinline__ RowBand row_band_of(const uint32_t* sq, int n) {
+    const float qmax = __uint_as_float(sq[SQ_QMAX]);
+    RowBand r;
+    r.ec = 2.0f * (float)(n + n / 32) * 0x1p-23f * qmax;
+    r.eabs = (float)n * 0x1p-120f;
+    return r;
+}
+
+// ||x||^2 of this lane's 8*KS index dims (exact bf16 products, fp32 sums)
+template <int KS>
+__device__ __forceinline__ float row_sq(const bf16x8_t (&xf)[KS]) {
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    float s2 = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const bf16x2_t p = {xf[ks][2 * e], xf[ks][2 * e + 1]};
+            s2 = __builtin_amdgcn_fdot2_f32_bf16(p, p, s2, false);
+        }
+    return s2;
+}
+
+// Epilogue of one 16-row tile for the lane holding row `row`:
+// key (max over heads, already reduced), ||x||^2 partial of the lane.
+struct TileOut {
+    float vmax, wmin, nu2m, bmm;
+};
+
+__device__ __forceinline__ void tile_epilogue(const ScoreArgs& a, int b, int g, int64_t row, bool valid, float m,
+                                              float s2, const RowBand& rb, TileOut& t) {
+    s2 += __shfl_xor(s2, 16);
+    s2 += __shfl_xor(s2, 32);
+    const float nu = sqrtf(s2) * (1.0f + 0x1p-16f);
+    const float eu = fmaf(rb.ec, nu, rb.eabs);
+    const float v = next_up_f32(m + eu);
+    const float w = next_down_f32(m - eu);
+    if (valid) {
+        t.nu2m = fmaxf(t.nu2m, s2);
+        t.vmax = fmaxf(t.vmax, v);
+        t.wmin = fminf(t.wmin, w);
+        if (g == 0) {
+            const int64_t o = (int64_t)b * a.A + row;
+            reinterpret_cast<float2*>(a.vw)[o] = make_float2(v, w);
+            if (a.key) a.key[o] = m;
+        }
+    }
+}
+
+__device__ __forceinline__ void score_finish(const ScoreArgs& a, int b, int lane, TileOut t, bool ub) {
+    t.nu2m = wave_max_all(t.nu2m);
+    t.vmax = wave_max_all(t.vmax);
+    t.wmin = -wave_max_all(-t.wmin);
+    if (ub) t.bmm = wave_max_all(t.bmm);
+    if (lane == 0) {
+        uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
+        atomicMax(sq + SQ_NU2MAX, __float_as_uint(t.nu2m));
+        atomicMin(sq + SQ_KMIN, key_to_ord(t.wmin));
+        atomicMax(sq + SQ_KMAX, key_to_ord(t.vmax));
+        if (ub) atomicMax(sq + SQ_BMAX, __float_as_uint(t.bmm));
+    }
+}
+
 // HT head tiles of 16 and KS dim steps of 32 held in VGPRs (HT*KS <= 32).
+// Head slots beyond H repeat a real head (h mod H), which leaves the maximum
+// over heads unchanged and needs no masking in the loop.
 template <int HT, int KS, bool UB>
 __global__ __launch_bounds__(256, 2) void score_kernel(ScoreArgs a) {
     __shared__ float4 s_hs[UB ? 128 : 1];
@@ -146,58 +295,57 @@ __global__ __launch_bounds__(256, 2) void score_kernel(ScoreArgs a) {
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63, g = lane >> 4, c = lane & 15;
     if (UB) {
-        for (int h = tid; h < a.H; h += 256)
-            s_hs[h] = reinterpret_cast<const float4*>(a.hsc)[(int64_t)b * a.H + h];
+        for (int h = tid; h < 16 * HT; h += 256)
+            s_hs[h] = reinterpret_cast<const float4*>(a.hsc)[(int64_t)b * a.H + (h % a.H)];
         __syncthreads();
     }
     const int64_t r0 = ((int64_t)blockIdx.x * 4 + wave) * (16 * SCORE_TPW);
     if (r0 >= a.A) return;
     const int64_t rend = min(a.A, r0 + (int64_t)(16 * SCORE_TPW));
+    const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
+    const RowBand rb = row_band_of(sq, a.n);
 
     bf16x8_t qf[HT][KS];
     const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
 #pragma unroll
     for (int ht = 0; ht < HT; ++ht) {
-        const int h = 16 * ht + c;
+        const int h = (16 * ht + c) % a.H;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            if (h < a.H)
-                qf[ht][ks] = *reinterpret_cast<const bf16x8_t*>(qtb + (int64_t)h * a.n + 32 * ks + 8 * g);
-            else
-                qf[ht][ks] = bf16x8_t{};
-        }
+        for (int ks = 0; ks < KS; ++ks)
+            qf[ht][ks] = *reinterpret_cast<const bf16x8_t*>(qtb + (int64_t)h * a.n + 32 * ks + 8 * g);
     }
     const uint16_t* xb = a.x + (int64_t)b * a.xbs;
     float amax = 0.f, nmax = 0.f, emax = 0.f;
     if (UB) {
-        const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
         amax = __uint_as_float(sq[SQ_AMAX]);
         nmax = __uint_as_float(sq[SQ_NMAX]);
         emax = __uint_as_float(sq[SQ_EMAX]);
     }
-    float nu2m = 0.f, bmm = 0.f;
+    TileOut to{-INFINITY, INFINITY, 0.f, 0.f};
+    const int64_t rlast = rend - 1;
 
-    bf16x8_t xf[KS];
-    {
-        const int64_t row = r0 + c;
+    // PF tiles in flight ahead of the one on the matrix cores (one when the
+    // bound is also evaluated, for registers); rows past the end are clamped
+    // to the last row (loaded, never stored)
+    constexpr int PF = UB ? 1 : 2;
+    bf16x8_t xf[KS], x1[KS];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            xf[ks] = (row < rend) ? *reinterpret_cast<const bf16x8_t*>(xb + row * a.xs + 32 * ks + 8 * g)
-                                  : bf16x8_t{};
+    for (int ks = 0; ks < KS; ++ks) {
+        const int64_t row0 = min(r0 + c, rlast), row1 = min(r0 + 16 + c, rlast);
+        xf[ks] = *reinterpret_cast<const bf16x8_t*>(xb + row0 * a.xs + 32 * ks + 8 * g);
+        if (PF == 2) x1[ks] = *reinterpret_cast<const bf16x8_t*>(xb + row1 * a.xs + 32 * ks + 8 * g);
     }
     for (int64_t t0 = r0; t0 < rend; t0 += 16) {
         const int64_t row = t0 + c;
         const bool valid = row < rend;
-        // prefetch the next tile while this one runs on the matrix cores
-        bf16x8_t xn[KS];
-        const int64_t nrow = row + 16;
+        bf16x8_t x2[KS];
+        const int64_t nrow = min(row + 16 * PF, rlast);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-            xn[ks] = (nrow < rend) ? *reinterpret_cast<const bf16x8_t*>(xb + nrow * a.xs + 32 * ks + 8 * g)
-                                   : bf16x8_t{};
+            x2[ks] = *reinterpret_cast<const bf16x8_t*>(xb + nrow * a.xs + 32 * ks + 8 * g);
         float et = 0.f, ep = 0.f, ga = 0.f;
-        if (UB && valid) {
-            const int64_t o = (int64_t)b * a.T + row;
+        if (UB) {
+            const int64_t o = (int64_t)b * a.T + min(row, rlast);
             et = a.eta[o];
             ep = a.eps[o];
             ga = a.gam[o];
@@ -210,51 +358,40 @@ __global__ __launch_bounds__(256, 2) void score_kernel(ScoreArgs a) {
 #pragma unroll
             for (int ht = 0; ht < HT; ++ht)
                 acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[ht][ks], xf[ks], acc[ht], 0, 0, 0);
-        // acc[ht][i] = score of head 16*ht + 4*g + i for row t0 + c
+        // keep the per-head bound scalars in LDS (re-read per tile) instead of
+        // letting them be hoisted into 4 * 16 * HT registers
+        if (UB) asm volatile("" ::: "memory");
+        // acc[ht][i] = score of head slot 16*ht + 4*g + i for row t0 + c
         float m = -INFINITY;
         float ubv = -INFINITY;
 #pragma unroll
         for (int ht = 0; ht < HT; ++ht)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int h = 16 * ht + 4 * g + i;
-                if (h < a.H) {
-                    m = fmaxf(m, acc[ht][i]);
-                    if (UB) {
-                        const float4 hs = s_hs[h];
-                        const float bh = fmaf(hs.x, et, fmaf(hs.y, ep, hs.z * ga));
-                        ubv = fmaxf(ubv, acc[ht][i] + bh);
-                    }
+                m = fmaxf(m, acc[ht][i]);
+                if (UB) {
+                    const float4 hs = s_hs[16 * ht + 4 * g + i];
+                    ubv = fmaxf(ubv, acc[ht][i] + fmaf(hs.x, et, fmaf(hs.y, ep, hs.z * ga)));
                 }
             }
         m = wave_max16(m);
-        float s2 = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float v = (float)xf[ks][e];
-                s2 = fmaf(v, v, s2);
-            }
-        s2 += __shfl_xor(s2, 16);
-        s2 += __shfl_xor(s2, 32);
-        if (valid) nu2m = fmaxf(nu2m, s2);
+        tile_epilogue(a, b, g, row, valid, m, row_sq<KS>(xf), rb, to);
         if (UB) {
             ubv = wave_max16(ubv);
-            if (valid) bmm = fmaxf(bmm, fmaf(amax, et, fmaf(nmax, ep, emax * ga)));
+            if (valid) to.bmm = fmaxf(to.bmm, fmaf(amax, et, fmaf(nmax, ep, emax * ga)));
             if (g == 0 && valid) a.ub[(int64_t)b * a.A + row] = ubv;
         }
-        if (g == 0 && valid) a.key[(int64_t)b * a.A + row] = m;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) xf[ks] = xn[ks];
+        for (int ks = 0; ks < KS; ++ks) {
+            if (PF == 2) {
+                xf[ks] = x1[ks];
+                x1[ks] = x2[ks];
+            } else {
+                xf[ks] = x2[ks];
+            }
+        }
     }
-    nu2m = wave_max_all(nu2m);
-    if (UB) bmm = wave_max_all(bmm);
-    if (lane == 0) {
-        uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-        atomicMax(sq + SQ_NU2MAX, __float_as_uint(nu2m));
-        if (UB) atomicMax(sq + SQ_BMAX, __float_as_uint(bmm));
-    }
+    score_finish(a, b, lane, to, UB);
 }
 
 // Any head count / width within the limits: heads and dims in runtime loops,
@@ -266,127 +403,295 @@ __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
     const int b = blockIdx.y;
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63, g = lane >> 4, c = lane & 15;
+    const int KS = a.n / 32;
+    const int HT = (a.H + 15) / 16;
     if (UB) {
-        for (int h = tid; h < a.H; h += 256)
-            s_hs[h] = reinterpret_cast<const float4*>(a.hsc)[(int64_t)b * a.H + h];
+        for (int h = tid; h < 16 * HT; h += 256)
+            s_hs[h] = reinterpret_cast<const float4*>(a.hsc)[(int64_t)b * a.H + (h % a.H)];
         __syncthreads();
     }
     const int64_t r0 = ((int64_t)blockIdx.x * 4 + wave) * (16 * SCORE_TPW);
     if (r0 >= a.A) return;
     const int64_t rend = min(a.A, r0 + (int64_t)(16 * SCORE_TPW));
-    const int KS = a.n / 32;
-    const int HT = (a.H + 15) / 16;
+    const int64_t rlast = rend - 1;
+    const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
+    const RowBand rb = row_band_of(sq, a.n);
     const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
     const uint16_t* xb = a.x + (int64_t)b * a.xbs;
     float amax = 0.f, nmax = 0.f, emax = 0.f;
     if (UB) {
-        const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
         amax = __uint_as_float(sq[SQ_AMAX]);
         nmax = __uint_as_float(sq[SQ_NMAX]);
         emax = __uint_as_float(sq[SQ_EMAX]);
     }
-    float nu2m = 0.f, bmm = 0.f;
+    TileOut to{-INFINITY, INFINITY, 0.f, 0.f};
     for (int64_t t0 = r0; t0 < rend; t0 += 16) {
         const int64_t row = t0 + c;
         const bool valid = row < rend;
+        const int64_t lrow = min(row, rlast);
         bf16x8_t xf[KSMAX];
 #pragma unroll
         for (int ks = 0; ks < KSMAX; ++ks)
-            xf[ks] = (valid && ks < KS) ? *reinterpret_cast<const bf16x8_t*>(xb + row * a.xs + 32 * ks + 8 * g)
-                                        : bf16x8_t{};
+            xf[ks] = (ks < KS) ? *reinterpret_cast<const bf16x8_t*>(xb + lrow * a.xs + 32 * ks + 8 * g) : bf16x8_t{};
         float et = 0.f, ep = 0.f, ga = 0.f;
-        if (UB && valid) {
-            const int64_t o = (int64_t)b * a.T + row;
+        if (UB) {
+            const int64_t o = (int64_t)b * a.T + lrow;
             et = a.eta[o];
             ep = a.eps[o];
             ga = a.gam[o];
         }
         float m = -INFINITY, ubv = -INFINITY;
         for (int ht = 0; ht < HT; ++ht) {
-            const int hq = 16 * ht + c;
+            const int hq = (16 * ht + c) % a.H;
             f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < KSMAX; ++ks) {
                 if (ks < KS) {
-                    bf16x8_t q = (hq < a.H) ? *reinterpret_cast<const bf16x8_t*>(qtb + (int64_t)hq * a.n + 32 * ks + 8 * g)
-                                            : bf16x8_t{};
+                    const bf16x8_t q = *reinterpret_cast<const bf16x8_t*>(qtb + (int64_t)hq * a.n + 32 * ks + 8 * g);
                     acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q, xf[ks], acc, 0, 0, 0);
                 }
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int h = 16 * ht + 4 * g + i;
-                if (h < a.H) {
-                    m = fmaxf(m, acc[i]);
-                    if (UB) {
-                        const float4 hs = s_hs[h];
-                        ubv = fmaxf(ubv, acc[i] + fmaf(hs.x, et, fmaf(hs.y, ep, hs.z * ga)));
-                    }
+                m = fmaxf(m, acc[i]);
+                if (UB) {
+                    const float4 hs = s_hs[16 * ht + 4 * g + i];
+                    ubv = fmaxf(ubv, acc[i] + fmaf(hs.x, et, fmaf(hs.y, ep, hs.z * ga)));
                 }
             }
         }
         m = wave_max16(m);
-        float s2 = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < KSMAX; ++ks)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float v = (float)xf[ks][e];
-                s2 = fmaf(v, v, s2);
-            }
-        s2 += __shfl_xor(s2, 16);
-        s2 += __shfl_xor(s2, 32);
-        if (valid) nu2m = fmaxf(nu2m, s2);
+        tile_epilogue(a, b, g, row, valid, m, row_sq<KSMAX>(xf), rb, to);
         if (UB) {
             ubv = wave_max16(ubv);
-            if (valid) bmm = fmaxf(bmm, fmaf(amax, et, fmaf(nmax, ep, emax * ga)));
+            if (valid) to.bmm = fmaxf(to.bmm, fmaf(amax, et, fmaf(nmax, ep, emax * ga)));
             if (g == 0 && valid) a.ub[(int64_t)b * a.A + row] = ubv;
         }
-        if (g == 0 && valid) a.key[(int64_t)b * a.A + row] = m;
     }
-    nu2m = wave_max_all(nu2m);
-    if (UB) bmm = wave_max_all(bmm);
-    if (lane == 0) {
-        uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-        atomicMax(sq + SQ_NU2MAX, __float_as_uint(nu2m));
-        if (UB) atomicMax(sq + SQ_BMAX, __float_as_uint(bmm));
+    score_finish(a, b, lane, to, UB);
+}
+
+// --------------------------------------------------- LDS-pipelined scorer
+//
+// The streaming form used when the bound is not evaluated.  Each wave owns a
+// private ring of NST LDS stages; a stage holds one 16-row tile of index rows
+// and is filled by direct global->LDS loads (global_load_lds_dwordx4: lane l's
+// 16 B land at stage + 16 l), so NST tiles are in flight per wave without
+// costing registers, and every load instruction covers whole contiguous rows.
+// Within a stage, chunk C of tile row R is stored at slot (C - R) mod (n/8),
+// which makes the MFMA-layout reads (16 rows x 16 B per pass) bank-conflict
+// free.  The loop has no other vector-memory operations, so `s_waitcnt vmcnt`
+// with the count of younger tile loads tells exactly when a stage is ready;
+// results go to LDS and are written out after the loop.
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void gbl_void_t;
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt immediate");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
+}
+
+// wait until at most `rem` tiles (KS loads each) younger than the current one
+// are still in flight (rem is wave-uniform, 0 <= rem < NST)
+template <int KS, int NST>
+__device__ __forceinline__ void wait_tiles(int rem) {
+    switch (rem) {
+        case 0: wait_vmcnt<0>(); break;
+        case 1: if (NST > 1) wait_vmcnt<(NST > 1 ? 1 : 0) * KS>(); break;
+        case 2: if (NST > 2) wait_vmcnt<(NST > 2 ? 2 : 0) * KS>(); break;
+        case 3: if (NST > 3) wait_vmcnt<(NST > 3 ? 3 : 0) * KS>(); break;
+        case 4: if (NST > 4) wait_vmcnt<(NST > 4 ? 4 : 0) * KS>(); break;
+        case 5: if (NST > 5) wait_vmcnt<(NST > 5 ? 5 : 0) * KS>(); break;
+        case 6: if (NST > 6) wait_vmcnt<(NST > 6 ? 6 : 0) * KS>(); break;
+        default: if (NST > 7) wait_vmcnt<(NST > 7 ? 7 : 0) * KS>(); break;
     }
+}
+
+constexpr int STAGE_BUDGET = 16384;   // bytes of tile ring per wave
+constexpr int STREAM_WAVES = 4;       // waves per block
+
+template <int KS>
+struct StreamGeom {
+    static constexpr int N = 32 * KS;          // index dims per row
+    static constexpr int N8 = N / 8;           // 16-byte slots per row
+    static constexpr int STAGE = 16 * N * 2;   // one 16-row tile; KS loads of 1 KB
+    static constexpr int NST = (STAGE_BUDGET / STAGE) > 8 ? 8 : ((STAGE_BUDGET / STAGE) < 2 ? 2 : (STAGE_BUDGET / STAGE));
+    static constexpr int WAVE = NST * STAGE;
+};
+
+// The streaming scorer: each wave owns a contiguous span of `tpw` tiles of
+// one sequence and keeps NST tiles in flight, loaded straight into an LDS ring
+// (global_load_lds_dwordx4, 1 KB per instruction: KS instructions per tile).
+// Slot S of row R in a stage holds the row's 16-byte chunk (S + R) mod N8, so
+// the MFMA operand reads (16 rows, one chunk each) hit distinct banks.  The
+// per-lane source offsets are the same for every tile (only the wave-uniform
+// tile base moves), so a steady-state tile costs no address arithmetic.  Row
+// results are latched into lane 16*(t%4) + c and written every fourth tile as
+// 64 consecutive rows.  Those stores share vmcnt with the ring loads: every
+// wait counts ring loads only, which is safe whether or not stores complete in
+// order with loads (loads complete in order among themselves).
+template <int HT, int KS>
+__global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int tpw) {
+    using Gm = StreamGeom<KS>;
+    constexpr int N8 = Gm::N8, STAGE = Gm::STAGE, NST = Gm::NST;
+    extern __shared__ __align__(16) uint8_t smem[];
+    const int b = blockIdx.y;
+    const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    uint8_t* wbase = smem + wave * Gm::WAVE;
+    const int64_t r0 = ((int64_t)blockIdx.x * STREAM_WAVES + wave) * (16 * (int64_t)tpw);
+    if (r0 >= a.A) return;
+    const int64_t rend = min(a.A, r0 + 16 * (int64_t)tpw);
+    const int ntl = (int)((rend - r0 + 15) / 16);
+    const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
+    const RowBand rb = row_band_of(sq, a.n);
+
+    bf16x8_t qf[HT][KS];
+    const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
+#pragma unroll
+    for (int ht = 0; ht < HT; ++ht) {
+        const int h = (16 * ht + c) % a.H;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+            qf[ht][ks] = *reinterpret_cast<const bf16x8_t*>(qtb + (int64_t)h * a.n + 32 * ks + 8 * g);
+    }
+    wait_vmcnt<0>();   // query fragments resident before the ring's count starts
+
+    const uint32_t rowb = (uint32_t)(a.xs * 2);   // row stride in bytes
+    const uint8_t* span = reinterpret_cast<const uint8_t*>(a.x + (int64_t)b * a.xbs + r0 * a.xs);
+    uint32_t voff[KS];
+    int vrow[KS];
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+        const int q = 64 * j + lane;
+        const int R = q / N8, S = q % N8;
+        vrow[j] = R;
+        voff[j] = (uint32_t)R * rowb + 16u * (uint32_t)((S + R) % N8);
+    }
+    auto issue = [&](int t, int stage) {
+        const uint8_t* tb = span + (int64_t)t * 16 * rowb;
+        const int nv = (int)min((int64_t)16, rend - (r0 + 16 * (int64_t)t));   // rows of this tile
+#pragma unroll
+        for (int j = 0; j < KS; ++j) {
+            uint32_t o = voff[j];
+            if (nv < 16 && vrow[j] >= nv) o -= (uint32_t)(vrow[j] - (nv - 1)) * rowb;   // past-the-end rows re-read the last
+            __builtin_amdgcn_global_load_lds((gbl_void_t*)(tb + o), (lds_void_t*)(wbase + stage * STAGE + 1024 * j),
+                                             16, 0, 0);
+        }
+    };
+    for (int t = 0; t < NST && t < ntl; ++t) issue(t, t);
+
+    TileOut to{-INFINITY, INFINITY, 0.f, 0.f};
+    float lm = 0.f, ls2 = 0.f;   // latched row results: lane 16*(t%4)+c holds row 16t+c
+    float2* vwo = reinterpret_cast<float2*>(a.vw) + (int64_t)b * a.A + r0;
+    float* ko = a.key ? a.key + (int64_t)b * a.A + r0 : nullptr;
+    for (int t = 0; t < ntl; ++t) {
+        if (t <= ntl - NST) wait_vmcnt<(NST - 1) * KS>();
+        else wait_tiles<KS, NST>(ntl - 1 - t);
+        const int stage = t % NST;
+        const uint8_t* st = wbase + stage * STAGE;
+        bf16x8_t xf[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const int S = (4 * ks + g - c + 16 * N8) % N8;
+            xf[ks] = *reinterpret_cast<const bf16x8_t*>(st + c * (2 * Gm::N) + 16 * S);
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // stage read out before it is refilled
+        if (t + NST < ntl) issue(t + NST, stage);
+        f32x4_t acc[HT];
+#pragma unroll
+        for (int ht = 0; ht < HT; ++ht) acc[ht] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+            for (int ht = 0; ht < HT; ++ht)
+                acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[ht][ks], xf[ks], acc[ht], 0, 0, 0);
+        // acc[ht][i] = score of head slot 16*ht + 4*g + i for row 16t + c
+        float m = -INFINITY;
+#pragma unroll
+        for (int ht = 0; ht < HT; ++ht)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) m = fmaxf(m, acc[ht][i]);
+        m = wave_max16(m);
+        float s2 = row_sq<KS>(xf);
+        s2 += __shfl_xor(s2, 16);
+        s2 += __shfl_xor(s2, 32);
+        if (g == (t & 3)) {
+            lm = m;
+            ls2 = s2;
+        }
+        if ((t & 3) == 3 || t == ntl - 1) {
+            // rows 16*(t & ~3) + lane
+            const int rl = 16 * (t & ~3) + lane;
+            const float nu = sqrtf(ls2) * (1.0f + 0x1p-16f);
+            const float eu = fmaf(rb.ec, nu, rb.eabs);
+            const float v = next_up_f32(lm + eu);
+            const float w = next_down_f32(lm - eu);
+            if (r0 + rl < rend) {
+                to.nu2m = fmaxf(to.nu2m, ls2);
+                to.vmax = fmaxf(to.vmax, v);
+                to.wmin = fminf(to.wmin, w);
+                vwo[rl] = make_float2(v, w);
+                if (ko) ko[rl] = lm;
+            }
+        }
+    }
+    score_finish(a, b, lane, to, false);
+}
+
+// tiles per wave: enough waves for two blocks per CU, spans of 8..512 tiles
+static int stream_tpw(const ScoreArgs& a) {
+    const int64_t tiles = (int64_t)a.B * ((a.A + 15) / 16);
+    const int64_t waves = 2LL * 256 * STREAM_WAVES;
+    int64_t tpw = (tiles + waves - 1) / waves;
+    tpw = tpw < 8 ? 8 : (tpw > 512 ? 512 : tpw);
+    return (int)tpw;
 }
 
 template <int HT, int KS>
-static void launch_fast(const ScoreArgs& a, dim3 grid, hipStream_t s) {
-    if (a.ub)
+static void launch_fast(const ScoreArgs& a, hipStream_t s) {
+    if (a.ub) {
+        dim3 grid((unsigned)((a.A + SCORE_ROWS_PER_BLOCK - 1) / SCORE_ROWS_PER_BLOCK), a.B);
         hipLaunchKernelGGL((score_kernel<HT, KS, true>), grid, dim3(256), 0, s, a);
-    else
-        hipLaunchKernelGGL((score_kernel<HT, KS, false>), grid, dim3(256), 0, s, a);
+    } else {
+        const int tpw = stream_tpw(a);
+        const int64_t rows_per_block = (int64_t)STREAM_WAVES * 16 * tpw;
+        dim3 grid((unsigned)((a.A + rows_per_block - 1) / rows_per_block), a.B);
+        const size_t sm = STREAM_WAVES * (size_t)StreamGeom<KS>::WAVE;
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&score_stream_kernel<HT, KS>),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
+        hipLaunchKernelGGL((score_stream_kernel<HT, KS>), grid, dim3(256), sm, s, a, tpw);
+    }
 }
 
 template <int HT>
-static bool dispatch_ks(const ScoreArgs& a, dim3 grid, hipStream_t s, int KS) {
+static bool dispatch_ks(const ScoreArgs& a, hipStream_t s, int KS) {
     switch (KS) {
-        case 1: launch_fast<HT, 1>(a, grid, s); return true;
-        case 2: launch_fast<HT, 2>(a, grid, s); return true;
-        case 3: launch_fast<HT, 3>(a, grid, s); return true;
-        case 4: launch_fast<HT, 4>(a, grid, s); return true;
-        case 5: if (HT <= 4) { launch_fast<(HT <= 4 ? HT : 4), 5>(a, grid, s); return true; } return false;
-        case 6: if (HT <= 4) { launch_fast<(HT <= 4 ? HT : 4), 6>(a, grid, s); return true; } return false;
-        case 7: if (HT <= 4) { launch_fast<(HT <= 4 ? HT : 4), 7>(a, grid, s); return true; } return false;
-        case 8: if (HT <= 4) { launch_fast<(HT <= 4 ? HT : 4), 8>(a, grid, s); return true; } return false;
+        case 1: launch_fast<HT, 1>(a, s); return true;
+        case 2: launch_fast<HT, 2>(a, s); return true;
+        case 3: launch_fast<HT, 3>(a, s); return true;
+        case 4: launch_fast<HT, 4>(a, s); return true;
+        case 5: if (HT <= 4) { launch_fast<(HT <= 4 ? HT : 4), 5>(a, s); return true; } return false;
+        case 6: if (HT <= 4) { launch_fast<(HT <= 4 ? HT : 4), 6>(a, s); return true; } return false;
+        case 7: if (HT <= 4) { launch_fast<(HT <= 4 ? HT : 4), 7>(a, s); return true; } return false;
+        case 8: if (HT <= 4) { launch_fast<(HT <= 4 ? HT : 4), 8>(a, s); return true; } return false;
         default: return false;
     }
 }
 
 hipError_t launch_score(const ScoreArgs& a, hipStream_t s) {
     if (a.A <= 0) return hipSuccess;
-    dim3 grid((unsigned)((a.A + SCORE_ROWS_PER_BLOCK - 1) / SCORE_ROWS_PER_BLOCK), a.B);
     const int KS = a.n / 32;
     const int HT = (a.H + 15) / 16;
     bool done = false;
-    if (HT == 1) done = dispatch_ks<1>(a, grid, s, KS);
-    else if (HT == 2) done = dispatch_ks<2>(a, grid, s, KS);
-    else if (HT <= 4) done = dispatch_ks<4>(a, grid, s, KS);
-    else if (HT <= 8) done = dispatch_ks<8>(a, grid, s, KS);
+    if (HT == 1) done = dispatch_ks<1>(a, s, KS);
+    else if (HT == 2) done = dispatch_ks<2>(a, s, KS);
+    else if (HT <= 4) done = dispatch_ks<4>(a, s, KS);
+    else if (HT <= 8) done = dispatch_ks<8>(a, s, KS);
     if (!done) {
+        dim3 grid((unsigned)((a.A + SCORE_ROWS_PER_BLOCK - 1) / SCORE_ROWS_PER_BLOCK), a.B);
         if (a.ub)
             hipLaunchKernelGGL((score_generic_kernel<true>), grid, dim3(256), 0, s, a);
         else

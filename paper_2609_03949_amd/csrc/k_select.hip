@@ -1,130 +1,76 @@
 // k_select.hip -- exact per-sequence top-k and the certified two-tier admission.
 //
-// Selection (per sequence b, archive rows [0, A)):
-//   1. radix select (11 + 11 + 10 bits of the order-preserving key encoding)
-//      finds the k-th largest fp32 key t~; per-pass histograms live in LDS and
-//      are merged in global memory; the last block of a pass picks the digit.
-//   2. with the certified bound E on |key~ - key| (key = the fp64 index score),
-//      rows with key~ > t~ + 2E are certainly selected and rows with
-//      key~ < t~ - 2E certainly not (order statistics are 1-Lipschitz);
-//   3. the rows in between are re-scored in fp64 (d ascending, the exact
-//      definition) and ranked by (score desc, index asc) among themselves;
+// Selection (per sequence b, archive rows [0, A)), given fp32 keys key~ with a
+// certified bound |key~ - key| <= E (key = the fp64 index score):
+//   1. one histogram pass over 4096 linear bins of [min key~, max key~] finds
+//      the bin holding the k-th largest key~, i.e. a bracket [t_lo, t_hi] of it;
+//   2. rows with key~ > t_hi + 2E are certainly selected and rows with
+//      key~ < t_lo - 2E certainly not (order statistics are 1-Lipschitz in the
+//      max norm, so the k-th exact key lies within E of the k-th key~); the
+//      rows in between are appended to an ambiguous list;
+//   3. the ambiguous rows are re-scored in fp64 (d ascending: the exact
+//      definition) and ranked among themselves by (score desc, index asc); the
+//      first k - n_in join S, and the one of rank k - n_in - 1 gives theta;
 //   4. an ordered compaction writes S ascending.
-// Admission (Lemma (Index certificate)): the same band argument on the upper
-// bound UB_u against theta = min over S of the exact score.
+// Admission (Lemma (Index certificate)) applies the same band argument to the
+// upper bound UB_u against theta.
 #include "vkv_internal.h"
 
 namespace vkv {
 
 constexpr int SEL_THREADS = 256;
+constexpr int HIST_KEYS_PER_BLOCK = 16384;
+constexpr int REFINE_BLOCKS = 8;
+constexpr int RANK_BLOCKS = 16;
 
 // ------------------------------------------------------------ error bounds
 
-// nu_max >= max_u ||x_u|| from the scorer's fp32 sum of squares.
+// nu_max >= max_u ||x_u|| from the scorer's fp32 sums of squares.
 __device__ __forceinline__ double nu_max_of(const uint32_t* sq, int n) {
     const double nu2 = (double)__uint_as_float(sq[SQ_NU2MAX]);
     return sqrt(nu2 * (1.0 + (double)n * 0x1p-22)) * (1.0 + 0x1p-20);
 }
 
-// |fp32 MFMA key - fp64 key| <= E: products of bf16 are exact in fp32; each
-// of the <= n + n/32 fp32 roundings of a partial sum is at most 2^-23 of
-// sum|q_d x_d| <= ||qt|| ||x|| (Cauchy-Schwarz); factor 8 of slack, plus an
-// absolute term for flushed subnormal products.
+// |fp32 MFMA key - fp64 key| <= E.  bf16 products are exact in fp32; the dot
+// product of width n goes through at most n + n/32 fp32 additions (32-product
+// MFMA steps plus the accumulator), each with relative error <= 2^-23 (so even
+// truncation is covered) of a partial sum bounded by sum_d |q_d x_d| <=
+// ||qt|| ||x|| (Cauchy-Schwarz): |error| <= (n + n/32) 2^-23 ||qt|| ||x|| to
+// first order; factor 2 of slack, plus an absolute term for flushed
+// subnormal products.
 __device__ __forceinline__ double key_error_of(const uint32_t* sq, int n) {
     const double qmax = (double)__uint_as_float(sq[SQ_QMAX]);
-    return 8.0 * (double)n * 0x1p-23 * qmax * nu_max_of(sq, n) + (double)n * 0x1p-120;
+    return 2.0 * (double)(n + n / 32) * 0x1p-23 * qmax * nu_max_of(sq, n) + (double)n * 0x1p-120;
 }
 
-// ------------------------------------------------------------------ init
-
-__global__ __launch_bounds__(SEL_THREADS) void select_init_kernel(SelectArgs a) {
-    const int b = blockIdx.x;
-    const int tid = threadIdx.x;
-    uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    if (tid == 0) {
-        sq[SQ_EKEY] = __float_as_uint(ru_f32(key_error_of(sq, a.n)));
-        sq[SQ_PREFIX] = 0u;
-        sq[SQ_KREM] = (uint32_t)a.k;
-        sq[SQ_DONE] = 0u;
-        sq[SQ_NIN] = 0u;
-        sq[SQ_NAMB] = 0u;
-        a.theta[b] = -INFINITY;
-    }
-    for (int i = tid; i < RADIX_BINS; i += SEL_THREADS) a.hist[(int64_t)b * RADIX_BINS + i] = 0u;
-    for (int64_t i = tid; i < a.nch * CC_WORDS; i += SEL_THREADS) a.ccount[(int64_t)b * a.nch * CC_WORDS + i] = 0u;
+// fp32 evaluation of s^ + B in the scorer: |error| <= E + 2^-21 (smax + bmax); 2x slack.
+__device__ __forceinline__ double ub_error_of(const uint32_t* sq, int n) {
+    const double E = key_error_of(sq, n);
+    const double smax = (double)__uint_as_float(sq[SQ_QMAX]) * nu_max_of(sq, n);
+    const double bmax = (double)__uint_as_float(sq[SQ_BMAX]) * (1.0 + 0x1p-20);
+    return E * (1.0 + 0x1p-20) + 0x1p-20 * (smax + bmax);
 }
 
-__global__ __launch_bounds__(SEL_THREADS) void fill_flags_kernel(uint8_t* flags, int64_t n, uint8_t v) {
+__device__ __forceinline__ float rd_f32(double x) {
+    float f = (float)x;
+    if ((double)f > x) f = -next_up_f32(-f);
+    return f;
+}
+
+// ------------------------------------------------------------ small kernels
+
+__global__ __launch_bounds__(SEL_THREADS) void fill_u8_kernel(uint8_t* p, int64_t n, uint8_t v) {
     for (int64_t i = (int64_t)blockIdx.x * SEL_THREADS + threadIdx.x; i < n; i += (int64_t)gridDim.x * SEL_THREADS)
-        flags[i] = v;
+        p[i] = v;
 }
 
-// ------------------------------------------------------------ radix select
-
-constexpr int RADIX_KEYS_PER_BLOCK = 8192;
-
-__global__ __launch_bounds__(SEL_THREADS) void radix_pass_kernel(SelectArgs a, int pass) {
-    __shared__ uint32_t s_hist[RADIX_BINS];
-    __shared__ uint32_t s_part[SEL_THREADS];
-    __shared__ int s_last;
-    const int b = blockIdx.y;
-    const int tid = threadIdx.x;
-    uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    uint32_t* gh = a.hist + (int64_t)b * RADIX_BINS;
-    const uint32_t prefix = sq[SQ_PREFIX];
-    const int pshift = (pass == 0) ? 32 : (pass == 1 ? 21 : 10);   // bits of the prefix position
-    const int dshift = (pass == 0) ? 21 : (pass == 1 ? 10 : 0);
-    const uint32_t dmask = (pass == 2) ? 0x3FFu : 0x7FFu;
-    for (int i = tid; i < RADIX_BINS; i += SEL_THREADS) s_hist[i] = 0u;
-    __syncthreads();
-    const float* kb = a.key + (int64_t)b * a.A;
-    const int64_t u0 = (int64_t)blockIdx.x * RADIX_KEYS_PER_BLOCK;
-    const int64_t u1 = min(a.A, u0 + RADIX_KEYS_PER_BLOCK);
-    for (int64_t u = u0 + tid; u < u1; u += SEL_THREADS) {
-        const uint32_t o = key_to_ord(kb[u]);
-        if (pass == 0 || (o >> pshift) == prefix) atomicAdd(&s_hist[(o >> dshift) & dmask], 1u);
-    }
-    __syncthreads();
-    for (int i = tid; i < RADIX_BINS; i += SEL_THREADS)
-        if (s_hist[i]) atomicAdd(&gh[i], s_hist[i]);
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) s_last = (atomicAdd(&sq[SQ_DONE], 1u) == gridDim.x - 1);
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    // last block: choose the digit holding the krem-th largest key
-    const uint32_t krem = sq[SQ_KREM];
-    const int nb = (int)dmask + 1;
-    const int per = (nb + SEL_THREADS - 1) / SEL_THREADS;
-    uint32_t local = 0;
-    for (int d = tid * per; d < min(nb, (tid + 1) * per); ++d) {
-        const uint32_t h = __hip_atomic_load(&gh[d], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_hist[d] = h;
-        local += h;
-    }
-    s_part[tid] = local;
-    __syncthreads();
-    // exclusive suffix sum over threads (count of keys in higher bins)
-    uint32_t above = 0;
-    for (int t = tid + 1; t < SEL_THREADS; ++t) above += s_part[t];
-    if (above < krem && krem <= above + local) {
-        uint32_t run = above;
-        for (int d = min(nb, (tid + 1) * per) - 1; d >= tid * per; --d) {
-            if (run + s_hist[d] >= krem) {
-                sq[SQ_PREFIX] = (pass == 0 ? 0u : (prefix << (pass == 2 ? 10 : 11))) | (uint32_t)d;
-                sq[SQ_KREM] = krem - run;
-                break;
-            }
-            run += s_hist[d];
-        }
-    }
-    __syncthreads();
-    for (int i = tid; i < RADIX_BINS; i += SEL_THREADS) gh[i] = 0u;
-    if (tid == 0) sq[SQ_DONE] = 0u;
+__global__ __launch_bounds__(64) void select_empty_kernel(SelectArgs a) {
+    // k = 0: nothing selected, theta = -inf, chunk counters cleared
+    const int b = blockIdx.x;
+    if (threadIdx.x == 0) a.theta[b] = -INFINITY;
+    if (threadIdx.x == 1) a.seq[(int64_t)b * SQ_WORDS + SQ_NAMB2] = 0u;
+    for (int64_t i = threadIdx.x; i < a.nch * CC_WORDS; i += 64) a.ccount[(int64_t)b * a.nch * CC_WORDS + i] = 0u;
 }
-
-// ----------------------------------------------------------- classify
 
 __device__ __forceinline__ uint32_t block_sum_u32(uint32_t v, uint32_t* s_red) {
     const int tid = threadIdx.x;
@@ -137,36 +83,178 @@ __device__ __forceinline__ uint32_t block_sum_u32(uint32_t v, uint32_t* s_red) {
     return t;
 }
 
+// ---------------------------------------------------------- histogram pass
+
+__device__ __forceinline__ float bin_scale(float lo, float hi) {
+    const float range = hi - lo;
+    return (range > 0.f && range < INFINITY) ? (float)HIST_BINS / range : 0.f;
+}
+
+__device__ __forceinline__ int bin_of(float x, float lo, float scale) {
+    const float t = (x - lo) * scale;
+    const int bi = (t > 0.f) ? (int)t : 0;
+    return bi < HIST_BINS ? bi : HIST_BINS - 1;
+}
+
+// Sum over threads t' >= tid of v (block of SEL_THREADS threads).
+__device__ __forceinline__ uint32_t block_suffix_incl(uint32_t v, uint32_t* s_w) {
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t t = __shfl_down(v, o);
+        if (lane + o < 64) v += t;
+    }
+    __syncthreads();
+    if (lane == 0) s_w[w] = v;
+    __syncthreads();
+    uint32_t add = 0;
+    for (int w2 = w + 1; w2 < SEL_THREADS / 64; ++w2) add += s_w[w2];
+    return v + add;
+}
+
+// Histograms of v_u = key~_u + E_u and w_u = key~_u - E_u over linear bins of
+// [min w, max v].  The last block to finish finds the bins holding the k-th
+// largest v and the k-th largest w and stores
+//   HI >= k-th largest v  and  LO <= k-th largest w
+// (bin edges widened past the fp32 rounding of the binning).  Since
+// w_u <= key_u <= v_u, the k-th largest exact key lies in [LO, HI].
+__global__ __launch_bounds__(SEL_THREADS) void hist_kernel(SelectArgs a) {
+    __shared__ uint32_t s_hv[HIST_BINS];
+    __shared__ uint32_t s_hw[HIST_BINS];
+    __shared__ uint32_t s_w[SEL_THREADS / 64];
+    __shared__ int s_last;
+    const int b = blockIdx.y;
+    const int tid = threadIdx.x;
+    uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
+    uint32_t* gv = a.hist + (int64_t)b * 2 * HIST_BINS;
+    uint32_t* gw = gv + HIST_BINS;
+    if (blockIdx.x == 0 && tid == 0) {
+        sq[SQ_NIN] = 0u;
+        sq[SQ_NAMB] = 0u;
+        sq[SQ_NAMB2] = 0u;
+        a.theta[b] = -INFINITY;
+    }
+    const float lo = ord_to_key(sq[SQ_KMIN]);
+    const float hi = ord_to_key(sq[SQ_KMAX]);
+    const float scale = bin_scale(lo, hi);
+    for (int i = tid; i < HIST_BINS; i += SEL_THREADS) {
+        s_hv[i] = 0u;
+        s_hw[i] = 0u;
+    }
+    __syncthreads();
+    const float2* vw = reinterpret_cast<const float2*>(a.vw) + (int64_t)b * a.A;
+    const int64_t u0 = (int64_t)blockIdx.x * HIST_KEYS_PER_BLOCK;
+    const int64_t u1 = min(a.A, u0 + HIST_KEYS_PER_BLOCK);
+    for (int64_t u = u0 + tid; u < u1; u += SEL_THREADS) {
+        const float2 p = vw[u];
+        atomicAdd(&s_hv[bin_of(p.x, lo, scale)], 1u);
+        atomicAdd(&s_hw[bin_of(p.y, lo, scale)], 1u);
+    }
+    __syncthreads();
+    for (int i = tid; i < HIST_BINS; i += SEL_THREADS) {
+        if (s_hv[i]) atomicAdd(&gv[i], s_hv[i]);
+        if (s_hw[i]) atomicAdd(&gw[i], s_hw[i]);
+    }
+    __threadfence();
+    __syncthreads();
+    if (tid == 0) s_last = (atomicAdd(&sq[SQ_DONE], 1u) == gridDim.x - 1);
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();
+    constexpr int PER = HIST_BINS / SEL_THREADS;
+    uint32_t lv = 0, lw = 0;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int d = tid * PER + j;
+        const uint32_t hv = __hip_atomic_load(&gv[d], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint32_t hw = __hip_atomic_load(&gw[d], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_hv[d] = hv;
+        s_hw[d] = hw;
+        lv += hv;
+        lw += hw;
+    }
+    const uint32_t sv = block_suffix_incl(lv, s_w);
+    const uint32_t sw = block_suffix_incl(lw, s_w);
+    const uint32_t k = (uint32_t)a.k;
+    const double w_bin = (scale > 0.f) ? 1.0 / (double)scale : 0.0;
+    const double slack = fabs((double)lo) * 0x1p-22 + 0x1p-100;
+    if (sv - lv < k && k <= sv) {
+        uint32_t run = sv - lv;
+        for (int d = (tid + 1) * PER - 1; d >= tid * PER; --d) {
+            if (run + s_hv[d] >= k) {
+                double edge = (double)hi;
+                if (scale > 0.f) edge = fmin(edge, (double)lo + (double)(d + 1) * w_bin * (1.0 + 0x1p-20) + slack);
+                sq[SQ_THI] = __float_as_uint(ru_f32(edge));
+                break;
+            }
+            run += s_hv[d];
+        }
+    }
+    if (sw - lw < k && k <= sw) {
+        uint32_t run = sw - lw;
+        for (int d = (tid + 1) * PER - 1; d >= tid * PER; --d) {
+            if (run + s_hw[d] >= k) {
+                double edge = (double)lo;
+                if (scale > 0.f) edge = fmax(edge, (double)lo + (double)d * w_bin * (1.0 - 0x1p-20) - slack);
+                sq[SQ_TLO] = __float_as_uint(rd_f32(edge));
+                break;
+            }
+            run += s_hw[d];
+        }
+    }
+    __syncthreads();
+    for (int i = tid; i < 2 * HIST_BINS; i += SEL_THREADS) gv[i] = 0u;
+    if (tid == 0) sq[SQ_DONE] = 0u;
+}
+
+// ----------------------------------------------------------- classify
+
+// Append the rows of a wave whose predicate holds to list[base..) (order
+// within the list is irrelevant: the ranking below is by (key, index)).
+__device__ __forceinline__ void wave_append(bool pred, int32_t value, uint32_t* counter, int32_t* list) {
+    const uint64_t mask = __ballot(pred);
+    if (mask == 0) return;
+    const int lane = threadIdx.x & 63;
+    const int leader = __ffsll((unsigned long long)mask) - 1;
+    uint32_t base = 0;
+    if (lane == leader) base = atomicAdd(counter, (uint32_t)__popcll(mask));
+    base = __shfl(base, leader);
+    if (pred) list[base + __popcll(mask & ((1ull << lane) - 1ull))] = value;
+}
+
 __global__ __launch_bounds__(SEL_THREADS) void classify_kernel(SelectArgs a) {
     __shared__ uint32_t s_red[SEL_THREADS / 64];
     const int b = blockIdx.y;
     const int c = blockIdx.x;
     const int tid = threadIdx.x;
     uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    const double th = (double)ord_to_key(sq[SQ_PREFIX]);
-    const double E = (double)__uint_as_float(sq[SQ_EKEY]);
-    const double band = 2.0 * E * (1.0 + 0x1p-20) + fabs(th) * 0x1p-50;
-    const double hi = th + band, lo = th - band;
-    const float* kb = a.key + (int64_t)b * a.A;
+    const float LO = __uint_as_float(sq[SQ_TLO]);
+    const float HI = __uint_as_float(sq[SQ_THI]);
+    const float2* vw = reinterpret_cast<const float2*>(a.vw) + (int64_t)b * a.A;
     uint8_t* fb = a.flags + (int64_t)b * a.A;
-    uint32_t nin = 0, namb = 0;
+    int32_t* amb = a.amb + (int64_t)b * a.A;
+    uint32_t nin = 0;
     const int64_t u0 = (int64_t)c * CHUNK;
     const int64_t u1 = min(a.A, u0 + CHUNK);
-    for (int64_t u = u0 + tid; u < u1; u += SEL_THREADS) {
-        const double kv = (double)kb[u];
-        uint8_t f = (kv > hi) ? 1 : ((kv < lo) ? 0 : 2);
-        fb[u] = f;
+    for (int64_t base = u0; base < u1; base += SEL_THREADS) {
+        const int64_t u = base + tid;
+        uint8_t f = 0;
+        if (u < u1) {
+            const float2 p = vw[u];
+            // selected for sure: key >= w > HI >= theta*;  out for sure: key <= v < LO <= theta*
+            f = (p.y > HI) ? 1 : ((p.x < LO) ? 0 : 2);
+            fb[u] = f;
+        }
         nin += (f == 1);
-        namb += (f == 2);
+        wave_append(f == 2, (int32_t)u, &sq[SQ_NAMB], amb);
     }
     nin = block_sum_u32(nin, s_red);
-    namb = block_sum_u32(namb, s_red);
     if (tid == 0) {
         uint32_t* cc = a.ccount + ((int64_t)b * a.nch + c) * CC_WORDS;
         cc[CC_IN] = nin;
-        cc[CC_AMB] = namb;
+        cc[CC_SELAMB] = 0u;
+        cc[CC_ADM] = 0u;
+        cc[CC_ADMAMB] = 0u;
         atomicAdd(&sq[SQ_NIN], nin);
-        atomicAdd(&sq[SQ_NAMB], namb);
     }
 }
 
@@ -176,7 +264,7 @@ struct CompactArgs {
     const uint8_t* flags;
     uint8_t target;
     const uint32_t* ccount;
-    int w0, w1;            // count words of a chunk (w1 < 0: none)
+    int w0, w1;            // count words of a chunk
     int32_t* out;
     int64_t out_stride;
     int64_t cap;
@@ -192,9 +280,11 @@ __global__ __launch_bounds__(SEL_THREADS) void compact_kernel(CompactArgs a) {
     const int tid = threadIdx.x;
     const uint32_t* cc = a.ccount + (int64_t)b * a.nch * CC_WORDS;
     uint32_t part = 0;
-    for (int64_t q = tid; q < c; q += SEL_THREADS)
-        part += cc[q * CC_WORDS + a.w0] + (a.w1 >= 0 ? cc[q * CC_WORDS + a.w1] : 0u);
+    for (int64_t q = tid; q < c; q += SEL_THREADS) part += cc[q * CC_WORDS + a.w0] + cc[q * CC_WORDS + a.w1];
     const uint32_t base = block_sum_u32(part, s_red);
+    const uint32_t mine = cc[(int64_t)c * CC_WORDS + a.w0] + cc[(int64_t)c * CC_WORDS + a.w1];
+    if (a.total && c == a.nch - 1 && tid == 0) a.total[b] = (int32_t)(base + mine);
+    if (mine == 0) return;
     // each thread owns 8 consecutive rows of the chunk
     const int64_t u0 = (int64_t)c * CHUNK + 8 * tid;
     const uint8_t* fb = a.flags + (int64_t)b * a.A;
@@ -222,12 +312,10 @@ __global__ __launch_bounds__(SEL_THREADS) void compact_kernel(CompactArgs a) {
             if ((int64_t)pos < a.cap) ob[pos] = (int32_t)(u0 + e);
             ++pos;
         }
-    if (a.total && c == a.nch - 1 && tid == SEL_THREADS - 1) a.total[b] = (int32_t)(base + s_scan[tid]);
 }
 
 static hipError_t run_compact(const SelectArgs& s, const uint8_t* flags, uint8_t target, int w0, int w1,
-                              int32_t* out, int64_t out_stride, int64_t cap, int32_t* total,
-                              hipStream_t st) {
+                              int32_t* out, int64_t out_stride, int64_t cap, int32_t* total, hipStream_t st) {
     CompactArgs c{flags, target, s.ccount, w0, w1, out, out_stride, cap, total, s.A, s.nch};
     hipLaunchKernelGGL(compact_kernel, dim3((unsigned)s.nch, s.B), dim3(SEL_THREADS), 0, st, c);
     return hipGetLastError();
@@ -235,37 +323,96 @@ static hipError_t run_compact(const SelectArgs& s, const uint8_t* flags, uint8_t
 
 // --------------------------------------------------------- fp64 re-scoring
 
-// Exact index score of row u for head h: fp64, d ascending, from +0 (the
-// definition; bf16 products are exact in fp64, so fma == mul + add).
-__device__ __forceinline__ double exact_score(const uint16_t* qrow, const uint16_t* xrow, int n) {
-    double acc = 0.0;
-    for (int d = 0; d < n; ++d) acc = fma((double)bf16_to_f32(qrow[d]), (double)bf16_to_f32(xrow[d]), acc);
-    return acc;
-}
+// Exact index scores of 8 rows per block iteration: thread (slot, hq) runs the
+// fp64 dot products (d ascending, from +0; bf16 products are exact in fp64) of
+// heads hq, hq+32, hq+64, hq+96 for row slot `slot`, with qt held transposed
+// in LDS (head-contiguous, conflict-free) when it fits.
+constexpr int RF_ROWS = 8;
+constexpr int RF_QT_MAX = 32768;   // elements of qt staged in LDS (64 KB)
 
-__device__ __forceinline__ double wave_max_f64(double v) {
-    for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o));
-    return v;
-}
-
-constexpr int REFINE_BLOCKS = 16;
-
-__global__ __launch_bounds__(SEL_THREADS) void refine_keys_kernel(SelectArgs a) {
+template <bool UB, bool QLDS>
+__global__ __launch_bounds__(SEL_THREADS) void refine_kernel(SelectArgs a) {
+    __shared__ uint16_t s_qt[QLDS ? RF_QT_MAX : 1];     // [n][128]
+    __shared__ __align__(16) uint16_t s_x[RF_ROWS][D_ROW];
     const int b = blockIdx.y;
-    const int lane = threadIdx.x & 63;
-    const int wave = blockIdx.x * (SEL_THREADS / 64) + (threadIdx.x >> 6);
-    const int nwaves = gridDim.x * (SEL_THREADS / 64);
-    const uint32_t namb = a.seq[(int64_t)b * SQ_WORDS + SQ_NAMB];
+    const int tid = threadIdx.x;
+    const int slot = tid >> 5, hq = tid & 31;
+    const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
+    const uint32_t namb = sq[UB ? SQ_NAMB2 : SQ_NAMB];
+    if ((uint32_t)(blockIdx.x * RF_ROWS) >= namb) return;
     const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
-    const uint16_t* xb = a.x + (int64_t)b * a.xbs;
-    for (int64_t i = wave; i < namb; i += nwaves) {
-        const int32_t u = a.amb[(int64_t)b * a.A + i];
-        const uint16_t* xr = xb + (int64_t)u * a.xs;
-        double best = -INFINITY;
-        for (int h = lane; h < a.H; h += 64) best = fmax(best, exact_score(qtb + (int64_t)h * a.n, xr, a.n));
-        best = wave_max_f64(best);
-        if (lane == 0) a.ambkey[(int64_t)b * a.A + i] = best;
+    if (QLDS) {
+        // coalesced reads along d, transposed writes (head-contiguous rows)
+        for (int idx = tid; idx < a.n * 128; idx += SEL_THREADS) {
+            const int h = idx / a.n, d = idx % a.n;
+            s_qt[d * 128 + h] = (h < a.H) ? qtb[(int64_t)h * a.n + d] : (uint16_t)0;
+        }
     }
+    const uint16_t* xb = a.x + (int64_t)b * a.xbs;
+    const int32_t* amb = a.amb + (int64_t)b * a.A;
+    const double th = UB ? a.theta[b] : 0.0;
+    const float4* hs = reinterpret_cast<const float4*>(a.hsc) + (int64_t)b * a.H;
+    for (uint32_t i0 = blockIdx.x * RF_ROWS; i0 < namb; i0 += gridDim.x * RF_ROWS) {
+        __syncthreads();
+        for (int idx = tid; idx < RF_ROWS * (a.n / 8); idx += SEL_THREADS) {
+            const int rl = idx / (a.n / 8), p = idx % (a.n / 8);
+            u16x8_t v = u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+            if (i0 + rl < namb) v = *reinterpret_cast<const u16x8_t*>(xb + (int64_t)amb[i0 + rl] * a.xs + 8 * p);
+            *reinterpret_cast<u16x8_t*>(&s_x[rl][8 * p]) = v;
+        }
+        __syncthreads();
+        const uint32_t i = i0 + slot;
+        double acc[4] = {0.0, 0.0, 0.0, 0.0};
+        for (int d = 0; d < a.n; ++d) {
+            const double xv = (double)bf16_to_f32(s_x[slot][d]);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int h = hq + 32 * j;
+                const uint16_t qb = QLDS ? s_qt[d * 128 + h] : ((h < a.H) ? qtb[(int64_t)h * a.n + d] : (uint16_t)0);
+                acc[j] = fma((double)bf16_to_f32(qb), xv, acc[j]);
+            }
+        }
+        double best = -INFINITY;
+        const int64_t u = (i < namb) ? (int64_t)amb[i] : 0;
+        double et = 0.0, ep = 0.0, ga = 0.0;
+        if (UB && i < namb) {
+            const int64_t o = (int64_t)b * a.T + u;
+            et = (double)a.eta[o];
+            ep = (double)a.eps[o];
+            ga = (double)a.gam[o];
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int h = hq + 32 * j;
+            if (h < a.H) {
+                double v = acc[j];
+                if (UB) {
+                    const float4 q = hs[h];
+                    v = v + fma((double)q.x, et, fma((double)q.y, ep, (double)q.z * ga));
+                }
+                best = fmax(best, v);
+            }
+        }
+        for (int o = 16; o > 0; o >>= 1) best = fmax(best, __shfl_xor(best, o));
+        if (hq == 0 && i < namb) {
+            if (!UB) {
+                a.ambkey[(int64_t)b * a.A + i] = best;
+            } else if (best > th) {
+                a.flags2[(int64_t)b * a.A + u] = 3;
+                atomicAdd(&a.ccount[((int64_t)b * a.nch + u / CHUNK) * CC_WORDS + CC_ADMAMB], 1u);
+            }
+        }
+    }
+}
+
+template <bool UB>
+static hipError_t run_refine(const SelectArgs& a, hipStream_t s) {
+    dim3 g(REFINE_BLOCKS, a.B);
+    if ((int64_t)a.n * 128 <= RF_QT_MAX)
+        hipLaunchKernelGGL((refine_kernel<UB, true>), g, dim3(SEL_THREADS), 0, s, a);
+    else
+        hipLaunchKernelGGL((refine_kernel<UB, false>), g, dim3(SEL_THREADS), 0, s, a);
+    return hipGetLastError();
 }
 
 // Rank of each ambiguous row among the ambiguous rows by (exact key desc,
@@ -310,53 +457,26 @@ __global__ __launch_bounds__(SEL_THREADS) void rank_select_kernel(SelectArgs a) 
 }
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(select_init_kernel, dim3(a.B), dim3(SEL_THREADS), 0, s, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    if (a.A == 0) return hipSuccess;
-    if (a.k == 0) {
-        hipLaunchKernelGGL(fill_flags_kernel, dim3(256), dim3(SEL_THREADS), 0, s, a.flags, (int64_t)a.B * a.A,
-                           (uint8_t)0);
+    hipError_t e;
+    if (a.A == 0 || a.k == 0) {
+        hipLaunchKernelGGL(select_empty_kernel, dim3(a.B), dim3(64), 0, s, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if (a.A == 0) return hipSuccess;
+        hipLaunchKernelGGL(fill_u8_kernel, dim3(256), dim3(SEL_THREADS), 0, s, a.flags, (int64_t)a.B * a.A, (uint8_t)0);
         return hipGetLastError();
     }
-    dim3 rg((unsigned)((a.A + RADIX_KEYS_PER_BLOCK - 1) / RADIX_KEYS_PER_BLOCK), a.B);
-    for (int p = 0; p < 3; ++p) {
-        hipLaunchKernelGGL(radix_pass_kernel, rg, dim3(SEL_THREADS), 0, s, a, p);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
-    dim3 cg((unsigned)a.nch, a.B);
-    hipLaunchKernelGGL(classify_kernel, cg, dim3(SEL_THREADS), 0, s, a);
+    dim3 hg((unsigned)((a.A + HIST_KEYS_PER_BLOCK - 1) / HIST_KEYS_PER_BLOCK), a.B);
+    hipLaunchKernelGGL(hist_kernel, hg, dim3(SEL_THREADS), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = run_compact(a, a.flags, 2, CC_AMB, -1, a.amb, a.A, a.A, nullptr, s)) != hipSuccess) return e;
-    hipLaunchKernelGGL(refine_keys_kernel, dim3(REFINE_BLOCKS, a.B), dim3(SEL_THREADS), 0, s, a);
+    hipLaunchKernelGGL(classify_kernel, dim3((unsigned)a.nch, a.B), dim3(SEL_THREADS), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(rank_select_kernel, dim3(REFINE_BLOCKS, a.B), dim3(SEL_THREADS), 0, s, a);
+    if ((e = run_refine<false>(a, s)) != hipSuccess) return e;
+    hipLaunchKernelGGL(rank_select_kernel, dim3(RANK_BLOCKS, a.B), dim3(SEL_THREADS), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return run_compact(a, a.flags, 1, CC_IN, CC_SELAMB, a.sel, a.k, a.k, nullptr, s);
 }
 
 // ---------------------------------------------------------------- admit
-
-__global__ __launch_bounds__(SEL_THREADS) void admit_init_kernel(SelectArgs a) {
-    const int b = blockIdx.x;
-    const int tid = threadIdx.x;
-    uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    if (tid == 0) {
-        const double E = key_error_of(sq, a.n);
-        const double smax = (double)__uint_as_float(sq[SQ_QMAX]) * nu_max_of(sq, a.n);
-        const double bmax = (double)__uint_as_float(sq[SQ_BMAX]) * (1.0 + 0x1p-20);
-        // fp32 evaluation of s^ + B: |error| <= E + 2^-21 (smax + bmax); 2x slack
-        sq[SQ_EUB] = __float_as_uint(ru_f32(E * (1.0 + 0x1p-20) + 0x1p-20 * (smax + bmax)));
-        sq[SQ_NAMB] = 0u;
-        sq[SQ_NADM] = 0u;
-    }
-    uint32_t* cc = a.ccount + (int64_t)b * a.nch * CC_WORDS;
-    for (int64_t q = tid; q < a.nch; q += SEL_THREADS) {
-        cc[q * CC_WORDS + CC_ADM] = 0u;
-        cc[q * CC_WORDS + CC_AAMB] = 0u;
-        cc[q * CC_WORDS + CC_ADMAMB] = 0u;
-    }
-}
 
 __global__ __launch_bounds__(SEL_THREADS) void admit_classify_kernel(SelectArgs a) {
     __shared__ uint32_t s_red[SEL_THREADS / 64];
@@ -365,83 +485,49 @@ __global__ __launch_bounds__(SEL_THREADS) void admit_classify_kernel(SelectArgs 
     const int tid = threadIdx.x;
     uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
     const double th = a.theta[b];
-    const double E = (double)__uint_as_float(sq[SQ_EUB]);
+    const double E = ub_error_of(sq, a.n) * (1.0 + 0x1p-20);
     const float* ubb = a.ub + (int64_t)b * a.A;
     const uint8_t* fb = a.flags + (int64_t)b * a.A;
     uint8_t* f2 = a.flags2 + (int64_t)b * a.A;
-    uint32_t nadm = 0, namb = 0;
+    int32_t* amb = a.amb + (int64_t)b * a.A;
+    uint32_t nadm = 0;
     const int64_t u0 = (int64_t)c * CHUNK;
     const int64_t u1 = min(a.A, u0 + CHUNK);
-    for (int64_t u = u0 + tid; u < u1; u += SEL_THREADS) {
+    for (int64_t base = u0; base < u1; base += SEL_THREADS) {
+        const int64_t u = base + tid;
         uint8_t f = 0;
-        if (fb[u] != 1) {
-            if (th == -INFINITY) {
-                f = 3;
-            } else {
-                const double t = (double)ubb[u];
-                const double band = E * (1.0 + 0x1p-20) + fabs(t) * 0x1p-50 + fabs(th) * 0x1p-50;
-                f = (t - band > th) ? 3 : ((t + band <= th) ? 0 : 4);
+        if (u < u1) {
+            if (fb[u] != 1) {
+                if (th == -INFINITY) {
+                    f = 3;
+                } else {
+                    const double t = (double)ubb[u];
+                    const double band = E + fabs(t) * 0x1p-50 + fabs(th) * 0x1p-50;
+                    f = (t - band > th) ? 3 : ((t + band <= th) ? 0 : 4);
+                }
             }
+            f2[u] = f;
         }
-        f2[u] = f;
         nadm += (f == 3);
-        namb += (f == 4);
+        wave_append(f == 4, (int32_t)u, &sq[SQ_NAMB2], amb);
     }
     nadm = block_sum_u32(nadm, s_red);
-    namb = block_sum_u32(namb, s_red);
-    if (tid == 0) {
-        uint32_t* cc = a.ccount + ((int64_t)b * a.nch + c) * CC_WORDS;
-        cc[CC_ADM] = nadm;
-        cc[CC_AAMB] = namb;
-        atomicAdd(&sq[SQ_NAMB], namb);
-    }
+    if (tid == 0) a.ccount[((int64_t)b * a.nch + c) * CC_WORDS + CC_ADM] = nadm;
 }
 
-__global__ __launch_bounds__(SEL_THREADS) void admit_refine_kernel(SelectArgs a) {
-    const int b = blockIdx.y;
-    const int lane = threadIdx.x & 63;
-    const int wave = blockIdx.x * (SEL_THREADS / 64) + (threadIdx.x >> 6);
-    const int nwaves = gridDim.x * (SEL_THREADS / 64);
-    const uint32_t namb = a.seq[(int64_t)b * SQ_WORDS + SQ_NAMB];
-    const double th = a.theta[b];
-    const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
-    const uint16_t* xb = a.x + (int64_t)b * a.xbs;
-    const float4* hs = reinterpret_cast<const float4*>(a.hsc) + (int64_t)b * a.H;
-    for (int64_t i = wave; i < namb; i += nwaves) {
-        const int32_t u = a.amb[(int64_t)b * a.A + i];
-        const uint16_t* xr = xb + (int64_t)u * a.xs;
-        const int64_t o = (int64_t)b * a.T + u;
-        const double et = (double)a.eta[o], ep = (double)a.eps[o], ga = (double)a.gam[o];
-        double best = -INFINITY;
-        for (int h = lane; h < a.H; h += 64) {
-            const double s = exact_score(qtb + (int64_t)h * a.n, xr, a.n);
-            const float4 q = hs[h];
-            const double bh = fma((double)q.x, et, fma((double)q.y, ep, (double)q.z * ga));
-            best = fmax(best, s + bh);
-        }
-        best = wave_max_f64(best);
-        if (lane == 0 && best > th) {
-            a.flags2[(int64_t)b * a.A + u] = 3;
-            atomicAdd(&a.ccount[((int64_t)b * a.nch + u / CHUNK) * CC_WORDS + CC_ADMAMB], 1u);
-        }
-    }
+__global__ __launch_bounds__(64) void zero_counts_kernel(int32_t* p, int n) {
+    for (int i = threadIdx.x; i < n; i += 64) p[i] = 0;
 }
 
 hipError_t launch_admit(const SelectArgs& a, hipStream_t s) {
     hipError_t e;
     if (a.A == 0) {
-        hipLaunchKernelGGL(fill_flags_kernel, dim3(1), dim3(SEL_THREADS), 0, s, reinterpret_cast<uint8_t*>(a.adm_count),
-                           (int64_t)a.B * 4, (uint8_t)0);
+        hipLaunchKernelGGL(zero_counts_kernel, dim3(1), dim3(64), 0, s, a.adm_count, a.B);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL(admit_init_kernel, dim3(a.B), dim3(SEL_THREADS), 0, s, a);
+    hipLaunchKernelGGL(admit_classify_kernel, dim3((unsigned)a.nch, a.B), dim3(SEL_THREADS), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    dim3 cg((unsigned)a.nch, a.B);
-    hipLaunchKernelGGL(admit_classify_kernel, cg, dim3(SEL_THREADS), 0, s, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = run_compact(a, a.flags2, 4, CC_AAMB, -1, a.amb, a.A, a.A, nullptr, s)) != hipSuccess) return e;
-    hipLaunchKernelGGL(admit_refine_kernel, dim3(REFINE_BLOCKS, a.B), dim3(SEL_THREADS), 0, s, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = run_refine<true>(a, s)) != hipSuccess) return e;
     return run_compact(a, a.flags2, 3, CC_ADM, CC_ADMAMB, a.adm, a.cap, a.cap, a.adm_count, s);
 }
 

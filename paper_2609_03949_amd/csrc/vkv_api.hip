@@ -111,7 +111,8 @@ static WsLayout layout(const vkv_step* st, int64_t k, int64_t cap) {
     L.wproj = o; o = up256(o + (size_t)(B * H * std::max(st->r, 1) * 8));
     L.hsc = o; o = up256(o + (size_t)(B * H * 16));
     L.seq = o; o = up256(o + (size_t)(B * SQ_WORDS * 4));
-    L.hist = o; o = up256(o + (size_t)(B * RADIX_BINS * 4));
+    L.hist = o; o = up256(o + (size_t)(B * 2 * HIST_BINS * 4));
+    L.vw = o; o = up256(o + (size_t)(B * Aw * 8));
     L.flags = o; o = up256(o + (size_t)(B * Aw));
     L.flags2 = o; o = up256(o + (size_t)(B * Aw));
     L.ccount = o; o = up256(o + (size_t)(B * L.nch * CC_WORDS * 4));
@@ -156,6 +157,7 @@ static SelectArgs select_args(const vkv_step* st, const WsLayout& L, char* w) {
     a.T = st->T;
     a.seq = reinterpret_cast<uint32_t*>(w + L.seq);
     a.hist = reinterpret_cast<uint32_t*>(w + L.hist);
+    a.vw = reinterpret_cast<const float*>(w + L.vw);
     a.flags = reinterpret_cast<uint8_t*>(w + L.flags);
     a.flags2 = reinterpret_cast<uint8_t*>(w + L.flags2);
     a.ccount = reinterpret_cast<uint32_t*>(w + L.ccount);
@@ -332,7 +334,8 @@ int vkv_query_prep(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, 
     char* w = (char*)ws;
     QprepArgs q{st->q_lat, st->q_rope, st->P, (int)st->B, (int)st->H, st->r, st->mode, (int)L.n,
                 reinterpret_cast<uint16_t*>(w + L.qt), reinterpret_cast<double*>(w + L.wproj),
-                reinterpret_cast<float*>(w + L.hsc), reinterpret_cast<uint32_t*>(w + L.seq)};
+                reinterpret_cast<float*>(w + L.hsc), reinterpret_cast<uint32_t*>(w + L.seq),
+                reinterpret_cast<uint32_t*>(w + L.hist)};
     HIP_TRY(ctx, launch_qprep(q, (hipStream_t)stream));
     return VKV_OK;
 }
@@ -343,7 +346,6 @@ int vkv_score(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, float
     if (rc) return rc;
     WsLayout L = layout(st, 0, 0);
     if ((rc = check_ws(ctx, ws, ws_bytes, L.part_o))) return rc;
-    if (!key && L.A > 0) return fail(ctx, VKV_E_ARG, "key is NULL");
     if (ub && (!st->eta || !st->eps || !st->gam)) return fail(ctx, VKV_E_ARG, "ub needs eta, eps and gam");
     if (ub && st->mode == VKV_MODE_DIGEST) return fail(ctx, VKV_E_UNSUPPORTED, "the bound needs the branch summand in the key");
     hipStream_t s = (hipStream_t)stream;
@@ -358,6 +360,7 @@ int vkv_score(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, float
     a.T = st->T;
     a.key = key;
     a.ub = ub;
+    a.vw = reinterpret_cast<float*>(w + L.vw);
     a.seq = reinterpret_cast<uint32_t*>(w + L.seq);
     a.A = L.A;
     a.B = (int)st->B;
@@ -367,18 +370,17 @@ int vkv_score(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, float
     return VKV_OK;
 }
 
-int vkv_select(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, const float* key, int32_t* sel,
-               double* theta, void* stream) {
+int vkv_select(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, int32_t* sel, double* theta,
+               void* stream) {
     if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
     int rc = check_step(ctx, st);
     if (rc) return rc;
     WsLayout L = layout(st, 0, 0);
     if ((rc = check_ws(ctx, ws, ws_bytes, L.part_o))) return rc;
     if (k < 0 || k > L.A) return fail(ctx, VKV_E_ARG, "k=%lld outside [0, A=%lld]", (long long)k, (long long)L.A);
-    if (!theta || (k > 0 && (!sel || !key))) return fail(ctx, VKV_E_ARG, "key, sel and theta are required");
+    if (!theta || (k > 0 && !sel)) return fail(ctx, VKV_E_ARG, "sel and theta are required");
     hipStream_t s = (hipStream_t)stream;
     SelectArgs a = select_args(st, L, (char*)ws);
-    a.key = key;
     a.sel = sel;
     a.theta = theta;
     a.k = k;
@@ -466,7 +468,7 @@ int vkv_step_run(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, in
     int rc = vkv_query_prep(ctx, st, ws, ws_bytes, stream);
     if (rc) return rc;
     if ((rc = vkv_score(ctx, st, ws, ws_bytes, key, two_tier ? ub : nullptr, stream))) return rc;
-    if ((rc = vkv_select(ctx, st, ws, ws_bytes, k, key, sel, theta, stream))) return rc;
+    if ((rc = vkv_select(ctx, st, ws, ws_bytes, k, sel, theta, stream))) return rc;
     if (two_tier) {
         if ((rc = vkv_admit(ctx, st, ws, ws_bytes, k, sel, theta, ub, adm, adm_count, cap, stream))) return rc;
     }

@@ -119,26 +119,26 @@ enum SeqWord : int {
     SQ_AMAX = 3,
     SQ_NMAX = 4,
     SQ_EMAX = 5,
-    SQ_EKEY = 6,    // float: certified |key - exact| bound
-    SQ_EUB = 7,     // float: certified |ub - exact| bound
-    SQ_PREFIX = 8,  // radix select: ordered-key prefix found so far
-    SQ_KREM = 9,    // radix select: rank still to find inside the prefix
-    SQ_DONE = 10,   // last-block counter
+    SQ_KMIN = 6,    // ordered encoding of min_u (key~ - E_u)   (scorer, atomicMin)
+    SQ_KMAX = 7,    // ordered encoding of max_u (key~ + E_u)   (scorer, atomicMax)
+    SQ_TLO = 8,     // float bits: LO <= k-th largest of (key~ - E_u)
+    SQ_THI = 9,     // float bits: HI >= k-th largest of (key~ + E_u)
+    SQ_DONE = 10,   // last-block counter of the histogram pass
     SQ_NIN = 11,    // rows certainly in S
-    SQ_NAMB = 12,   // ambiguous rows (select) / (admit)
-    SQ_NADM = 13,   // admitted rows (total)
+    SQ_NAMB = 12,   // ambiguous rows of the selection
+    SQ_NAMB2 = 13,  // ambiguous rows of the admission
     SQ_WORDS = 16
 };
 
 constexpr int CHUNK = 2048;        // rows per classify / compaction block
-constexpr int CC_WORDS = 8;        // per-chunk counters
-enum ChunkWord : int { CC_IN = 0, CC_AMB = 1, CC_SELAMB = 2, CC_ADM = 3, CC_AAMB = 4, CC_ADMAMB = 5 };
-constexpr int RADIX_BINS = 2048;
+constexpr int CC_WORDS = 4;        // per-chunk counters
+enum ChunkWord : int { CC_IN = 0, CC_SELAMB = 1, CC_ADM = 2, CC_ADMAMB = 3 };
+constexpr int HIST_BINS = 4096;
 constexpr int ATT_CHUNK = 32;      // rows per attention tile
 constexpr int ATT_HEADS = 64;      // heads per attention workgroup (4 waves x 16)
 
 struct WsLayout {
-    size_t qt, wproj, hsc, seq, hist, flags, flags2, ccount, amb, ambkey, part_o, part_ml, total;
+    size_t qt, wproj, hsc, seq, hist, vw, flags, flags2, ccount, amb, ambkey, part_o, part_ml, total;
     int64_t A, n, nch, splits, rows_per_split, cap;
 };
 
@@ -153,6 +153,7 @@ struct QprepArgs {
     double* wproj;     // [B,H,r]
     float* hsc;        // [B,H,4]: a, nq, e, ||qt||
     uint32_t* seq;     // [B,SQ_WORDS]
+    uint32_t* hist;    // [B,2,HIST_BINS] (cleared here for the selection)
 };
 
 struct ScoreArgs {
@@ -164,8 +165,9 @@ struct ScoreArgs {
     const float* eps;
     const float* gam;
     int64_t T;
-    float* key;            // [B,A]
+    float* key;            // [B,A] or null (diagnostic)
     float* ub;             // [B,A] or null
+    float* vw;             // [B,A,2]: key~ + E_u, key~ - E_u (rounded outward)
     uint32_t* seq;
     int64_t A;
     int B, H, n;
@@ -185,7 +187,7 @@ struct DigestArgs {
 };
 
 struct SelectArgs {
-    const float* key;      // [B,A]
+    const float* vw;       // [B,A,2] from the scorer
     const float* ub;       // [B,A] (admit)
     const uint16_t* x;     // index rows for fp64 re-scoring
     int64_t xs, xbs;
@@ -196,7 +198,7 @@ struct SelectArgs {
     const float* gam;
     int64_t T;
     uint32_t* seq;
-    uint32_t* hist;        // [B,RADIX_BINS]
+    uint32_t* hist;        // [B,2,HIST_BINS]
     uint8_t* flags;        // [B,A]
     uint8_t* flags2;       // [B,A]
     uint32_t* ccount;      // [B,nch,CC_WORDS]

@@ -101,7 +101,7 @@ def test_null_context_is_refused(lib):
     s = _step()
     P = ctypes.c_void_p
     assert lib.vkv_score(None, ctypes.byref(s), P(1 << 20), 1 << 20, P(1 << 20), None, None) == -1
-    assert lib.vkv_select(None, ctypes.byref(s), None, 0, 1, None, None, None, None) == -1
+    assert lib.vkv_select(None, ctypes.byref(s), None, 0, 1, None, None, None) == -1
     assert lib.vkv_attend(None, ctypes.byref(s), None, 0, 1, None, None, None, 0, ctypes.c_float(0.1),
                           None, None, None) == -1
     assert b"ctx" in lib.vkv_last_error(None)

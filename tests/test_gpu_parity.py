@@ -334,7 +334,7 @@ def test_argument_errors_leave_outputs_untouched(ctx):
     bufs = vkv.Buffers(step, 10)
     bufs.sel.fill_(-7)
     with pytest.raises(vkv.VkvError) as ei:
-        vkv.select(ctx, step, bufs.ws, wl["A"] + 1, bufs.key, bufs.sel, bufs.theta)
+        vkv.select(ctx, step, bufs.ws, wl["A"] + 1, bufs.sel, bufs.theta)
     assert ei.value.code == -1
     with pytest.raises(vkv.VkvError) as ei:
         vkv.query_prep(ctx, step, bufs.ws[:128])
