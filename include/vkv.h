@@ -162,12 +162,12 @@ int vkv_query_prep(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, 
  * not change the ranking):
  *   key~[b,u] ~= max_h  sum_d qt[b,h,d] x_u[d],   u in [0, A)
  * with x_u the mode's index row and qt from vkv_query_prep.  bf16 MFMA with
- * fp32 accumulation.  For every row the workspace receives the certified
- * interval [key~ - E_u, key~ + E_u] of the fp64 index score, where
- *   E_u = 2 (n + n/32) 2^-23 max_h ||qt_h|| ||x_u||
- * bounds the fp32 accumulation error (Cauchy-Schwarz on sum |q_d x_d|);
- * vkv_select uses these intervals.  key (may be NULL) receives key~ itself,
- * for diagnostics.  If ub != NULL (two-tier mode; needs st->eta/eps/gam), also
+ * fp32 accumulation.  The workspace receives key~ for every row and the
+ * per-sequence maxima of ||qt_h|| and ||x_u||, from which vkv_select takes
+ * the certified interval [key~ - E, key~ + E] of every fp64 index score,
+ *   E = 2 (n + n/32) 2^-23 max_h ||qt_h|| max_u ||x_u||
+ * (the fp32 accumulation error, by Cauchy-Schwarz on sum |q_d x_d|).  key
+ * (may be NULL) receives key~ as well, for diagnostics.  If ub != NULL (two-tier mode; needs st->eta/eps/gam), also
  *   ub[b,u] ~= max_h ( s^_h(u) + a_h eta_u + n_h eps_u + e_h gam_u )
  * the Cauchy-Schwarz upper bound of the full score (Lemma (Index certificate)).
  * key, ub: [B, A] fp32, contiguous.  ws is the workspace vkv_query_prep filled

@@ -210,26 +210,6 @@ __device__ __forceinline__ float wave_max_all(float m) {
     return m;
 }
 
-__device__ __forceinline__ float next_down_f32(float f) { return -next_up_f32(-f); }
-
-// Per-row certified interval of the key: |key~_u - key_u| <= E_u with
-//   E_u = 2 (n + n/32) 2^-23 max_h ||qt_h|| ||x_u||  (+ a subnormal term),
-// the fp32 MFMA accumulation bound (each of the <= n + n/32 fp32 additions of
-// the dot product errs by at most 2^-23 of a partial sum bounded by
-// sum_d |q_d x_d| <= ||qt|| ||x|| by Cauchy-Schwarz; factor 2 of slack).  The
-// scorer stores (key~ + E_u, key~ - E_u) rounded outward.
-struct RowBand {
-    float ec, eabs;
-};
-
-__device__ __forceinline__ RowBand row_band_of(const uint32_t* sq, int n) {
-    const float qmax = __uint_as_float(sq[SQ_QMAX]);
-    RowBand r;
-    r.ec = 2.0f * (float)(n + n / 32) * 0x1p-23f * qmax;
-    r.eabs = (float)n * 0x1p-120f;
-    return r;
-}
-
 // ||x||^2 of this lane's 8*KS index dims (exact bf16 products, fp32 sums)
 template <int KS>
 __device__ __forceinline__ float row_sq(const bf16x8_t (&xf)[KS]) {
@@ -245,27 +225,25 @@ __device__ __forceinline__ float row_sq(const bf16x8_t (&xf)[KS]) {
     return s2;
 }
 
-// Epilogue of one 16-row tile for the lane holding row `row`:
-// key (max over heads, already reduced), ||x||^2 partial of the lane.
+// Epilogue of one 16-row tile for the lane holding row `row`: key~ (max over
+// heads, already reduced) and the lane's partial of ||x||^2.  The scorer
+// keeps the per-sequence extremes of key~ and of ||x||^2; the selection
+// derives the certified band of every key from them.
 struct TileOut {
-    float vmax, wmin, nu2m, bmm;
+    float kmax, kmin, nu2m, bmm;
 };
 
 __device__ __forceinline__ void tile_epilogue(const ScoreArgs& a, int b, int g, int64_t row, bool valid, float m,
-                                              float s2, const RowBand& rb, TileOut& t) {
+                                              float s2, TileOut& t) {
     s2 += __shfl_xor(s2, 16);
     s2 += __shfl_xor(s2, 32);
-    const float nu = sqrtf(s2) * (1.0f + 0x1p-16f);
-    const float eu = fmaf(rb.ec, nu, rb.eabs);
-    const float v = next_up_f32(m + eu);
-    const float w = next_down_f32(m - eu);
     if (valid) {
         t.nu2m = fmaxf(t.nu2m, s2);
-        t.vmax = fmaxf(t.vmax, v);
-        t.wmin = fminf(t.wmin, w);
+        t.kmax = fmaxf(t.kmax, m);
+        t.kmin = fminf(t.kmin, m);
         if (g == 0) {
             const int64_t o = (int64_t)b * a.A + row;
-            reinterpret_cast<float2*>(a.vw)[o] = make_float2(v, w);
+            a.kt[o] = m;
             if (a.key) a.key[o] = m;
         }
     }
@@ -273,14 +251,14 @@ __device__ __forceinline__ void tile_epilogue(const ScoreArgs& a, int b, int g, 
 
 __device__ __forceinline__ void score_finish(const ScoreArgs& a, int b, int lane, TileOut t, bool ub) {
     t.nu2m = wave_max_all(t.nu2m);
-    t.vmax = wave_max_all(t.vmax);
-    t.wmin = -wave_max_all(-t.wmin);
+    t.kmax = wave_max_all(t.kmax);
+    t.kmin = -wave_max_all(-t.kmin);
     if (ub) t.bmm = wave_max_all(t.bmm);
     if (lane == 0) {
         uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
         atomicMax(sq + SQ_NU2MAX, __float_as_uint(t.nu2m));
-        atomicMin(sq + SQ_KMIN, key_to_ord(t.wmin));
-        atomicMax(sq + SQ_KMAX, key_to_ord(t.vmax));
+        atomicMin(sq + SQ_KMIN, key_to_ord(t.kmin));
+        atomicMax(sq + SQ_KMAX, key_to_ord(t.kmax));
         if (ub) atomicMax(sq + SQ_BMAX, __float_as_uint(t.bmm));
     }
 }
@@ -303,7 +281,6 @@ __global__ __launch_bounds__(256, 2) void score_kernel(ScoreArgs a) {
     if (r0 >= a.A) return;
     const int64_t rend = min(a.A, r0 + (int64_t)(16 * SCORE_TPW));
     const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    const RowBand rb = row_band_of(sq, a.n);
 
     bf16x8_t qf[HT][KS];
     const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
@@ -375,7 +352,7 @@ __global__ __launch_bounds__(256, 2) void score_kernel(ScoreArgs a) {
                 }
             }
         m = wave_max16(m);
-        tile_epilogue(a, b, g, row, valid, m, row_sq<KS>(xf), rb, to);
+        tile_epilogue(a, b, g, row, valid, m, row_sq<KS>(xf), to);
         if (UB) {
             ubv = wave_max16(ubv);
             if (valid) to.bmm = fmaxf(to.bmm, fmaf(amax, et, fmaf(nmax, ep, emax * ga)));
@@ -415,7 +392,6 @@ __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
     const int64_t rend = min(a.A, r0 + (int64_t)(16 * SCORE_TPW));
     const int64_t rlast = rend - 1;
     const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    const RowBand rb = row_band_of(sq, a.n);
     const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
     const uint16_t* xb = a.x + (int64_t)b * a.xbs;
     float amax = 0.f, nmax = 0.f, emax = 0.f;
@@ -461,7 +437,7 @@ __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
             }
         }
         m = wave_max16(m);
-        tile_epilogue(a, b, g, row, valid, m, row_sq<KSMAX>(xf), rb, to);
+        tile_epilogue(a, b, g, row, valid, m, row_sq<KSMAX>(xf), to);
         if (UB) {
             ubv = wave_max16(ubv);
             if (valid) to.bmm = fmaxf(to.bmm, fmaf(amax, et, fmaf(nmax, ep, emax * ga)));
@@ -471,19 +447,26 @@ __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
     score_finish(a, b, lane, to, UB);
 }
 
-// --------------------------------------------------- LDS-pipelined scorer
+// ------------------------------------------------------ streaming scorer
 //
-// The streaming form used when the bound is not evaluated.  Each wave owns a
-// private ring of NST LDS stages; a stage holds one 16-row tile of index rows
-// and is filled by direct global->LDS loads (global_load_lds_dwordx4: lane l's
-// 16 B land at stage + 16 l), so NST tiles are in flight per wave without
-// costing registers, and every load instruction covers whole contiguous rows.
-// Within a stage, chunk C of tile row R is stored at slot (C - R) mod (n/8),
-// which makes the MFMA-layout reads (16 rows x 16 B per pass) bank-conflict
-// free.  The loop has no other vector-memory operations, so `s_waitcnt vmcnt`
-// with the count of younger tile loads tells exactly when a stage is ready;
-// results go to LDS and are written out after the loop.
-
+// The form used when the bound is not evaluated.  A block owns a contiguous
+// span of one sequence's archive; its four waves take alternate 16-row tiles
+// of it (so the block streams one region of HBM), each through a private LDS
+// ring of NST stages filled by direct global->LDS loads
+// (global_load_lds_dwordx4, 1 KB per instruction, KS instructions per tile,
+// non-temporal: the index is read once per step).  Slot S of row R in a stage
+// holds the row's 16-byte chunk (S + R) mod N8, so the MFMA operand reads (16
+// rows, one chunk each) hit distinct banks; the per-lane source offsets are
+// the same for every tile, only the wave-uniform tile base moves.
+//
+// Per tile: the heads x rows contraction on the matrix cores (queries resident
+// in VGPRs) overlaps the read-out of the next tile from the ring; the per-lane
+// maximum over head slots and sum of squares are kept for four tiles, then a
+// reduce-scatter over the four 16-lane groups (permlane swaps) leaves row c of
+// tile t4+j in lane 16j+c.  Row keys collect in LDS and are written every
+// RES_GROUPS groups: stores share vmcnt with the ring loads, so they are kept
+// rare, and every wait counts ring loads only -- safe whether or not stores
+// complete in order with loads (loads complete in order among themselves).
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void gbl_void_t;
 
@@ -511,6 +494,7 @@ __device__ __forceinline__ void wait_tiles(int rem) {
 
 constexpr int STAGE_BUDGET = 16384;   // bytes of tile ring per wave
 constexpr int STREAM_WAVES = 4;       // waves per block
+constexpr int RES_GROUPS = 16;        // 4-tile groups of row keys buffered per wave
 
 template <int KS>
 struct StreamGeom {
@@ -518,35 +502,29 @@ struct StreamGeom {
     static constexpr int N8 = N / 8;           // 16-byte slots per row
     static constexpr int STAGE = 16 * N * 2;   // one 16-row tile; KS loads of 1 KB
     static constexpr int NST = (STAGE_BUDGET / STAGE) > 8 ? 8 : ((STAGE_BUDGET / STAGE) < 2 ? 2 : (STAGE_BUDGET / STAGE));
-    static constexpr int WAVE = NST * STAGE;
+    static constexpr int RES = RES_GROUPS * 64 * 4;
+    static constexpr int WAVE = NST * STAGE + RES;
 };
 
-// The streaming scorer: each wave owns a contiguous span of `tpw` tiles of
-// one sequence and keeps NST tiles in flight, loaded straight into an LDS ring
-// (global_load_lds_dwordx4, 1 KB per instruction: KS instructions per tile).
-// Slot S of row R in a stage holds the row's 16-byte chunk (S + R) mod N8, so
-// the MFMA operand reads (16 rows, one chunk each) hit distinct banks.  The
-// per-lane source offsets are the same for every tile (only the wave-uniform
-// tile base moves), so a steady-state tile costs no address arithmetic.  Row
-// results are latched into lane 16*(t%4) + c and written every fourth tile as
-// 64 consecutive rows.  Those stores share vmcnt with the ring loads: every
-// wait counts ring loads only, which is safe whether or not stores complete in
-// order with loads (loads complete in order among themselves).
 template <int HT, int KS>
 __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int tpw) {
     using Gm = StreamGeom<KS>;
     constexpr int N8 = Gm::N8, STAGE = Gm::STAGE, NST = Gm::NST;
+    constexpr int TST = STREAM_WAVES;   // block tiles between consecutive tiles of a wave
     extern __shared__ __align__(16) uint8_t smem[];
     const int b = blockIdx.y;
     const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     uint8_t* wbase = smem + wave * Gm::WAVE;
-    const int64_t r0 = ((int64_t)blockIdx.x * STREAM_WAVES + wave) * (16 * (int64_t)tpw);
-    if (r0 >= a.A) return;
-    const int64_t rend = min(a.A, r0 + 16 * (int64_t)tpw);
-    const int ntl = (int)((rend - r0 + 15) / 16);
-    const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    const RowBand rb = row_band_of(sq, a.n);
+    float* s_res = reinterpret_cast<float*>(wbase + NST * STAGE);
+    // block span [bs0, bs1); this wave's tile j covers rows r0 + 16 TST j + [0, 16)
+    const int64_t bs0 = (int64_t)blockIdx.x * STREAM_WAVES * 16 * tpw;
+    if (bs0 >= a.A) return;
+    const int64_t bs1 = min(a.A, bs0 + (int64_t)STREAM_WAVES * 16 * tpw);
+    const int64_t nbt = (bs1 - bs0 + 15) / 16;
+    if (wave >= nbt) return;
+    const int ntl = (int)((nbt - 1 - wave) / TST + 1);
+    const int64_t r0 = bs0 + 16 * wave;
 
     bf16x8_t qf[HT][KS];
     const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
@@ -571,35 +549,55 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
         voff[j] = (uint32_t)R * rowb + 16u * (uint32_t)((S + R) % N8);
     }
     auto issue = [&](int t, int stage) {
-        const uint8_t* tb = span + (int64_t)t * 16 * rowb;
-        const int nv = (int)min((int64_t)16, rend - (r0 + 16 * (int64_t)t));   // rows of this tile
+        const uint8_t* tb = span + (int64_t)t * (TST * 16) * rowb;
+        const int nv = (int)min((int64_t)16, bs1 - (r0 + (int64_t)(TST * 16) * t));   // rows of this tile
 #pragma unroll
         for (int j = 0; j < KS; ++j) {
             uint32_t o = voff[j];
             if (nv < 16 && vrow[j] >= nv) o -= (uint32_t)(vrow[j] - (nv - 1)) * rowb;   // past-the-end rows re-read the last
             __builtin_amdgcn_global_load_lds((gbl_void_t*)(tb + o), (lds_void_t*)(wbase + stage * STAGE + 1024 * j),
-                                             16, 0, 0);
+                                             16, 0, 2 /* nt */);
         }
     };
     for (int t = 0; t < NST && t < ntl; ++t) issue(t, t);
 
-    TileOut to{-INFINITY, INFINITY, 0.f, 0.f};
-    float lm = 0.f, ls2 = 0.f;   // latched row results: lane 16*(t%4)+c holds row 16t+c
-    float2* vwo = reinterpret_cast<float2*>(a.vw) + (int64_t)b * a.A + r0;
-    float* ko = a.key ? a.key + (int64_t)b * a.A + r0 : nullptr;
-    for (int t = 0; t < ntl; ++t) {
-        if (t <= ntl - NST) wait_vmcnt<(NST - 1) * KS>();
-        else wait_tiles<KS, NST>(ntl - 1 - t);
-        const int stage = t % NST;
-        const uint8_t* st = wbase + stage * STAGE;
-        bf16x8_t xf[KS];
+    // operand fragments of tile t from its ring stage
+    auto read_tile = [&](int t, bf16x8_t (&x)[KS]) {
+        const uint8_t* st = wbase + (t % NST) * STAGE;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             const int S = (4 * ks + g - c + 16 * N8) % N8;
-            xf[ks] = *reinterpret_cast<const bf16x8_t*>(st + c * (2 * Gm::N) + 16 * S);
+            x[ks] = *reinterpret_cast<const bf16x8_t*>(st + c * (2 * Gm::N) + 16 * S);
         }
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // stage read out before it is refilled
-        if (t + NST < ntl) issue(t + NST, stage);
+    };
+    bf16x8_t xf[KS];
+    wait_tiles<KS, NST>(min(NST - 1, ntl - 1));
+    read_tile(0, xf);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // stage read out before it is refilled
+    if (NST < ntl) issue(NST, 0);
+
+    TileOut to{-INFINITY, INFINITY, 0.f, 0.f};
+    float* kto = a.kt + (int64_t)b * a.A;
+    // the row held by this lane in 4-tile group q of the wave
+    auto group_row = [&](int q) { return r0 + (int64_t)(TST * 16) * (4 * q + g) + c; };
+    auto flush = [&](int q0, int nq) {
+        for (int q = 0; q < nq; ++q) {
+            const int64_t row = group_row(q0 + q);
+            const float k = s_res[64 * q + lane];
+            if (row < bs1) {
+                kto[row] = k;
+                if (a.key) a.key[(int64_t)b * a.A + row] = k;
+            }
+        }
+    };
+    // Per-lane partials of the four tiles of a group: pm = max over this
+    // lane's head slots, ps = sum of squares over this lane's dims.
+    float pm0 = -INFINITY, pm1 = -INFINITY, pm2 = -INFINITY, pm3 = -INFINITY;
+    float ps0 = 0.f, ps1 = 0.f, ps2 = 0.f, ps3 = 0.f;
+
+    for (int t = 0; t < ntl; ++t) {
+        // the matrix-core contraction of tile t (operands in xf) while tile
+        // t+1 is read out of the ring, then the per-lane partials of tile t
         f32x4_t acc[HT];
 #pragma unroll
         for (int ht = 0; ht < HT; ++ht) acc[ht] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -608,35 +606,70 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
 #pragma unroll
             for (int ht = 0; ht < HT; ++ht)
                 acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[ht][ks], xf[ks], acc[ht], 0, 0, 0);
-        // acc[ht][i] = score of head slot 16*ht + 4*g + i for row 16t + c
-        float m = -INFINITY;
+        const float ps = row_sq<KS>(xf);
+        bf16x8_t xn[KS];
+        const bool more = t + 1 < ntl;
+        if (more) {
+            wait_tiles<KS, NST>(min(NST - 1, ntl - 2 - t));
+            read_tile(t + 1, xn);
+        }
+        // acc[ht][i] = score of head slot 16*ht + 4*g + i for row c of tile t
+        float pm = -INFINITY;
 #pragma unroll
         for (int ht = 0; ht < HT; ++ht)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) m = fmaxf(m, acc[ht][i]);
-        m = wave_max16(m);
-        float s2 = row_sq<KS>(xf);
-        s2 += __shfl_xor(s2, 16);
-        s2 += __shfl_xor(s2, 32);
-        if (g == (t & 3)) {
-            lm = m;
-            ls2 = s2;
+            for (int i = 0; i < 4; ++i) pm = fmaxf(pm, acc[ht][i]);
+        const int j = t & 3;
+        if (j == 0) {
+            pm1 = pm2 = pm3 = -INFINITY;
+            ps1 = ps2 = ps3 = 0.f;
         }
-        if ((t & 3) == 3 || t == ntl - 1) {
-            // rows 16*(t & ~3) + lane
-            const int rl = 16 * (t & ~3) + lane;
-            const float nu = sqrtf(ls2) * (1.0f + 0x1p-16f);
-            const float eu = fmaf(rb.ec, nu, rb.eabs);
-            const float v = next_up_f32(lm + eu);
-            const float w = next_down_f32(lm - eu);
-            if (r0 + rl < rend) {
-                to.nu2m = fmaxf(to.nu2m, ls2);
-                to.vmax = fmaxf(to.vmax, v);
-                to.wmin = fminf(to.wmin, w);
-                vwo[rl] = make_float2(v, w);
-                if (ko) ko[rl] = lm;
-            }
+        pm0 = (j == 0) ? pm : pm0;
+        pm1 = (j == 1) ? pm : pm1;
+        pm2 = (j == 2) ? pm : pm2;
+        pm3 = (j == 3) ? pm : pm3;
+        ps0 = (j == 0) ? ps : ps0;
+        ps1 = (j == 1) ? ps : ps1;
+        ps2 = (j == 2) ? ps : ps2;
+        ps3 = (j == 3) ? ps : ps3;
+        if (more) {
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // stage read out before it is refilled
+            if (t + 1 + NST < ntl) issue(t + 1 + NST, (t + 1) % NST);
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) xf[ks] = xn[ks];
         }
+        if (j != 3 && more) continue;
+        // reduce-scatter over the four 16-lane groups: afterwards lane 16j + c
+        // holds the maximum and the sum of squares of row c of tile 4q + j
+        const int q = t >> 2;
+        float m, s2;
+        {
+            auto sw32 = [](float x, float y) {
+                const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+                return f32x2_t{__uint_as_float(r[0]), __uint_as_float(r[1])};
+            };
+            auto sw16 = [](float x, float y) {
+                const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+                return f32x2_t{__uint_as_float(r[0]), __uint_as_float(r[1])};
+            };
+            f32x2_t u = sw32(pm0, pm2), v = sw32(pm1, pm3);
+            const float m02 = fmaxf(u[0], u[1]), m13 = fmaxf(v[0], v[1]);
+            u = sw16(m02, m13);
+            m = fmaxf(u[0], u[1]);
+            u = sw32(ps0, ps2);
+            v = sw32(ps1, ps3);
+            const float s02 = u[0] + u[1], s13 = v[0] + v[1];
+            u = sw16(s02, s13);
+            s2 = u[0] + u[1];
+        }
+        if (group_row(q) < bs1) {
+            to.nu2m = fmaxf(to.nu2m, s2);
+            to.kmax = fmaxf(to.kmax, m);
+            to.kmin = fminf(to.kmin, m);
+        }
+        const int qb = q % RES_GROUPS;
+        s_res[64 * qb + lane] = m;
+        if (qb == RES_GROUPS - 1 || !more) flush(q - qb, qb + 1);
     }
     score_finish(a, b, lane, to, false);
 }
@@ -657,7 +690,7 @@ static void launch_fast(const ScoreArgs& a, hipStream_t s) {
         hipLaunchKernelGGL((score_kernel<HT, KS, true>), grid, dim3(256), 0, s, a);
     } else {
         const int tpw = stream_tpw(a);
-        const int64_t rows_per_block = (int64_t)STREAM_WAVES * 16 * tpw;
+        const int64_t rows_per_block = (int64_t)STREAM_WAVES * 16 * tpw;   // block span
         dim3 grid((unsigned)((a.A + rows_per_block - 1) / rows_per_block), a.B);
         const size_t sm = STREAM_WAVES * (size_t)StreamGeom<KS>::WAVE;
         (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&score_stream_kernel<HT, KS>),

@@ -1,13 +1,13 @@
 // k_select.hip -- exact per-sequence top-k and the certified two-tier admission.
 //
 // Selection (per sequence b, archive rows [0, A)), given fp32 keys key~ with a
-// certified bound |key~ - key| <= E (key = the fp64 index score):
-//   1. one histogram pass over 4096 linear bins of [min key~, max key~] finds
-//      the bin holding the k-th largest key~, i.e. a bracket [t_lo, t_hi] of it;
-//   2. rows with key~ > t_hi + 2E are certainly selected and rows with
-//      key~ < t_lo - 2E certainly not (order statistics are 1-Lipschitz in the
-//      max norm, so the k-th exact key lies within E of the k-th key~); the
-//      rows in between are appended to an ambiguous list;
+// certified bound |key~ - key| <= E for every row (key = the fp64 index score,
+// E from the per-sequence maxima of ||qt_h|| and ||x_u||):
+//   1. one histogram pass over 4096 linear bins of [min key~ - E, max key~ + E]
+//      of v = key~ + E and w = key~ - E (rounded outward) brackets the k-th
+//      largest exact key: HI >= k-th largest v and LO <= k-th largest w;
+//   2. rows with w > HI are certainly selected and rows with v < LO certainly
+//      not; the rows in between are appended to an ambiguous list;
 //   3. the ambiguous rows are re-scored in fp64 (d ascending: the exact
 //      definition) and ranked among themselves by (score desc, index asc); the
 //      first k - n_in join S, and the one of rank k - n_in - 1 gives theta;
@@ -20,7 +20,7 @@ namespace vkv {
 
 constexpr int SEL_THREADS = 256;
 constexpr int HIST_KEYS_PER_BLOCK = 16384;
-constexpr int REFINE_BLOCKS = 8;
+constexpr int REFINE_BLOCKS = 32;
 constexpr int RANK_BLOCKS = 16;
 
 // ------------------------------------------------------------ error bounds
@@ -43,6 +43,11 @@ __device__ __forceinline__ double key_error_of(const uint32_t* sq, int n) {
     return 2.0 * (double)(n + n / 32) * 0x1p-23 * qmax * nu_max_of(sq, n) + (double)n * 0x1p-120;
 }
 
+// E rounded up to fp32, and the outward-rounded band of one key.
+__device__ __forceinline__ float key_band_f32(const uint32_t* sq, int n) { return ru_f32(key_error_of(sq, n)); }
+__device__ __forceinline__ float band_hi(float k, float E) { return next_up_f32(k + E); }
+__device__ __forceinline__ float band_lo(float k, float E) { return next_down_f32(k - E); }
+
 // fp32 evaluation of s^ + B in the scorer: |error| <= E + 2^-21 (smax + bmax); 2x slack.
 __device__ __forceinline__ double ub_error_of(const uint32_t* sq, int n) {
     const double E = key_error_of(sq, n);
@@ -53,7 +58,7 @@ __device__ __forceinline__ double ub_error_of(const uint32_t* sq, int n) {
 
 __device__ __forceinline__ float rd_f32(double x) {
     float f = (float)x;
-    if ((double)f > x) f = -next_up_f32(-f);
+    if ((double)f > x) f = next_down_f32(f);
     return f;
 }
 
@@ -111,12 +116,14 @@ __device__ __forceinline__ uint32_t block_suffix_incl(uint32_t v, uint32_t* s_w)
     return v + add;
 }
 
-// Histograms of v_u = key~_u + E_u and w_u = key~_u - E_u over linear bins of
-// [min w, max v].  The last block to finish finds the bins holding the k-th
+// Histograms of v_u = key~_u + E and w_u = key~_u - E over linear bins of
+// [min v, max v].  The last block to finish finds the bins holding the k-th
 // largest v and the k-th largest w and stores
 //   HI >= k-th largest v  and  LO <= k-th largest w
 // (bin edges widened past the fp32 rounding of the binning).  Since
 // w_u <= key_u <= v_u, the k-th largest exact key lies in [LO, HI].
+constexpr int HIST_BATCH = 16;   // keys per thread in flight
+
 __global__ __launch_bounds__(SEL_THREADS) void hist_kernel(SelectArgs a) {
     __shared__ uint32_t s_hv[HIST_BINS];
     __shared__ uint32_t s_hw[HIST_BINS];
@@ -133,21 +140,33 @@ __global__ __launch_bounds__(SEL_THREADS) void hist_kernel(SelectArgs a) {
         sq[SQ_NAMB2] = 0u;
         a.theta[b] = -INFINITY;
     }
-    const float lo = ord_to_key(sq[SQ_KMIN]);
-    const float hi = ord_to_key(sq[SQ_KMAX]);
+    const float E = key_band_f32(sq, a.n);
+    const float lo = band_lo(ord_to_key(sq[SQ_KMIN]), E);
+    const float hi = band_hi(ord_to_key(sq[SQ_KMAX]), E);
     const float scale = bin_scale(lo, hi);
     for (int i = tid; i < HIST_BINS; i += SEL_THREADS) {
         s_hv[i] = 0u;
         s_hw[i] = 0u;
     }
     __syncthreads();
-    const float2* vw = reinterpret_cast<const float2*>(a.vw) + (int64_t)b * a.A;
+    const float* kt = a.kt + (int64_t)b * a.A;
     const int64_t u0 = (int64_t)blockIdx.x * HIST_KEYS_PER_BLOCK;
     const int64_t u1 = min(a.A, u0 + HIST_KEYS_PER_BLOCK);
-    for (int64_t u = u0 + tid; u < u1; u += SEL_THREADS) {
-        const float2 p = vw[u];
-        atomicAdd(&s_hv[bin_of(p.x, lo, scale)], 1u);
-        atomicAdd(&s_hw[bin_of(p.y, lo, scale)], 1u);
+    for (int64_t ub = u0; ub < u1; ub += HIST_BATCH * SEL_THREADS) {
+        float k[HIST_BATCH];
+#pragma unroll
+        for (int j = 0; j < HIST_BATCH; ++j) {
+            const int64_t u = ub + tid + (int64_t)j * SEL_THREADS;
+            k[j] = (u < u1) ? kt[u] : 0.f;
+        }
+#pragma unroll
+        for (int j = 0; j < HIST_BATCH; ++j) {
+            const int64_t u = ub + tid + (int64_t)j * SEL_THREADS;
+            if (u < u1) {
+                atomicAdd(&s_hv[bin_of(band_hi(k[j], E), lo, scale)], 1u);
+                atomicAdd(&s_hw[bin_of(band_lo(k[j], E), lo, scale)], 1u);
+            }
+        }
     }
     __syncthreads();
     for (int i = tid; i < HIST_BINS; i += SEL_THREADS) {
@@ -223,25 +242,33 @@ __device__ __forceinline__ void wave_append(bool pred, int32_t value, uint32_t* 
 
 __global__ __launch_bounds__(SEL_THREADS) void classify_kernel(SelectArgs a) {
     __shared__ uint32_t s_red[SEL_THREADS / 64];
+    constexpr int PER = CHUNK / SEL_THREADS;
     const int b = blockIdx.y;
     const int c = blockIdx.x;
     const int tid = threadIdx.x;
     uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
     const float LO = __uint_as_float(sq[SQ_TLO]);
     const float HI = __uint_as_float(sq[SQ_THI]);
-    const float2* vw = reinterpret_cast<const float2*>(a.vw) + (int64_t)b * a.A;
+    const float E = key_band_f32(sq, a.n);
+    const float* kt = a.kt + (int64_t)b * a.A;
     uint8_t* fb = a.flags + (int64_t)b * a.A;
     int32_t* amb = a.amb + (int64_t)b * a.A;
-    uint32_t nin = 0;
     const int64_t u0 = (int64_t)c * CHUNK;
     const int64_t u1 = min(a.A, u0 + CHUNK);
-    for (int64_t base = u0; base < u1; base += SEL_THREADS) {
-        const int64_t u = base + tid;
+    float k[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int64_t u = u0 + tid + (int64_t)j * SEL_THREADS;
+        k[j] = (u < u1) ? kt[u] : 0.f;
+    }
+    uint32_t nin = 0;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int64_t u = u0 + tid + (int64_t)j * SEL_THREADS;
         uint8_t f = 0;
         if (u < u1) {
-            const float2 p = vw[u];
             // selected for sure: key >= w > HI >= theta*;  out for sure: key <= v < LO <= theta*
-            f = (p.y > HI) ? 1 : ((p.x < LO) ? 0 : 2);
+            f = (band_lo(k[j], E) > HI) ? 1 : ((band_hi(k[j], E) < LO) ? 0 : 2);
             fb[u] = f;
         }
         nin += (f == 1);
@@ -323,17 +350,21 @@ static hipError_t run_compact(const SelectArgs& s, const uint8_t* flags, uint8_t
 
 // --------------------------------------------------------- fp64 re-scoring
 
-// Exact index scores of 8 rows per block iteration: thread (slot, hq) runs the
-// fp64 dot products (d ascending, from +0; bf16 products are exact in fp64) of
-// heads hq, hq+32, hq+64, hq+96 for row slot `slot`, with qt held transposed
-// in LDS (head-contiguous, conflict-free) when it fits.
+// Exact index scores of the ambiguous rows, RF_ROWS rows per block iteration:
+// thread (slot, hq) runs the fp64 dot products (d ascending, from +0; bf16
+// products are exact in fp64) of heads hq, hq+32, hq+64, hq+96 for row slot
+// `slot`, with qt held transposed in LDS (head-contiguous, conflict-free) when
+// it fits.  The rows of the next iteration are loaded while the current ones
+// are scored (double-buffered LDS).
 constexpr int RF_ROWS = 8;
 constexpr int RF_QT_MAX = 32768;   // elements of qt staged in LDS (64 KB)
+constexpr int RF_PIECES = (RF_ROWS * D_ROW / 8 + SEL_THREADS - 1) / SEL_THREADS;   // 16-byte row pieces per thread (max)
 
 template <bool UB, bool QLDS>
 __global__ __launch_bounds__(SEL_THREADS) void refine_kernel(SelectArgs a) {
-    __shared__ uint16_t s_qt[QLDS ? RF_QT_MAX : 1];     // [n][128]
-    __shared__ __align__(16) uint16_t s_x[RF_ROWS][D_ROW];
+    constexpr int XW = QLDS ? RF_QT_MAX / 128 : D_ROW;                // row width held (n <= XW)
+    __shared__ __align__(16) uint16_t s_qt[QLDS ? RF_QT_MAX : 8];     // [n][128]
+    __shared__ __align__(16) uint16_t s_x[2][RF_ROWS][XW];
     const int b = blockIdx.y;
     const int tid = threadIdx.x;
     const int slot = tid >> 5, hq = tid & 31;
@@ -341,30 +372,64 @@ __global__ __launch_bounds__(SEL_THREADS) void refine_kernel(SelectArgs a) {
     const uint32_t namb = sq[UB ? SQ_NAMB2 : SQ_NAMB];
     if ((uint32_t)(blockIdx.x * RF_ROWS) >= namb) return;
     const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
+    const int n8 = a.n / 8;
     if (QLDS) {
-        // coalesced reads along d, transposed writes (head-contiguous rows)
-        for (int idx = tid; idx < a.n * 128; idx += SEL_THREADS) {
-            const int h = idx / a.n, d = idx % a.n;
-            s_qt[d * 128 + h] = (h < a.H) ? qtb[(int64_t)h * a.n + d] : (uint16_t)0;
+        // 16-byte pieces of qt, all loads in flight, then transposed writes
+        constexpr int QP = RF_QT_MAX / 8 / SEL_THREADS;
+        u16x8_t v[QP];
+#pragma unroll
+        for (int j = 0; j < QP; ++j) {
+            const int p = tid + SEL_THREADS * j;
+            const int h = p & 127, d8 = p >> 7;
+            v[j] = (d8 < n8 && h < a.H) ? *reinterpret_cast<const u16x8_t*>(qtb + (int64_t)h * a.n + 8 * d8)
+                                        : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+        }
+#pragma unroll
+        for (int j = 0; j < QP; ++j) {
+            const int p = tid + SEL_THREADS * j;
+            const int h = p & 127, d8 = p >> 7;
+            if (d8 < n8)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) s_qt[(8 * d8 + e) * 128 + h] = v[j][e];
         }
     }
     const uint16_t* xb = a.x + (int64_t)b * a.xbs;
     const int32_t* amb = a.amb + (int64_t)b * a.A;
     const double th = UB ? a.theta[b] : 0.0;
     const float4* hs = reinterpret_cast<const float4*>(a.hsc) + (int64_t)b * a.H;
-    for (uint32_t i0 = blockIdx.x * RF_ROWS; i0 < namb; i0 += gridDim.x * RF_ROWS) {
-        __syncthreads();
-        for (int idx = tid; idx < RF_ROWS * (a.n / 8); idx += SEL_THREADS) {
-            const int rl = idx / (a.n / 8), p = idx % (a.n / 8);
-            u16x8_t v = u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
-            if (i0 + rl < namb) v = *reinterpret_cast<const u16x8_t*>(xb + (int64_t)amb[i0 + rl] * a.xs + 8 * p);
-            *reinterpret_cast<u16x8_t*>(&s_x[rl][8 * p]) = v;
+    const uint32_t step = gridDim.x * RF_ROWS;
+    // row pieces of iteration i0 into registers
+    u16x8_t pf[RF_PIECES];
+    auto fetch = [&](uint32_t i0) {
+#pragma unroll
+        for (int j = 0; j < RF_PIECES; ++j) {
+            const int idx = tid + SEL_THREADS * j;
+            const int rl = idx / n8, p = idx % n8;
+            pf[j] = u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+            if (rl < RF_ROWS && i0 + rl < namb)
+                pf[j] = *reinterpret_cast<const u16x8_t*>(xb + (int64_t)amb[i0 + rl] * a.xs + 8 * p);
         }
-        __syncthreads();
+    };
+    auto park = [&](int buf) {
+#pragma unroll
+        for (int j = 0; j < RF_PIECES; ++j) {
+            const int idx = tid + SEL_THREADS * j;
+            const int rl = idx / n8, p = idx % n8;
+            if (rl < RF_ROWS) *reinterpret_cast<u16x8_t*>(&s_x[buf][rl][8 * p]) = pf[j];
+        }
+    };
+    uint32_t i0 = blockIdx.x * RF_ROWS;
+    fetch(i0);
+    park(0);
+    __syncthreads();
+    for (int buf = 0; i0 < namb; i0 += step, buf ^= 1) {
+        const bool more = i0 + step < namb;
+        if (more) fetch(i0 + step);
         const uint32_t i = i0 + slot;
         double acc[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll 8
         for (int d = 0; d < a.n; ++d) {
-            const double xv = (double)bf16_to_f32(s_x[slot][d]);
+            const double xv = (double)bf16_to_f32(s_x[buf][slot][d]);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int h = hq + 32 * j;
@@ -402,6 +467,8 @@ __global__ __launch_bounds__(SEL_THREADS) void refine_kernel(SelectArgs a) {
                 atomicAdd(&a.ccount[((int64_t)b * a.nch + u / CHUNK) * CC_WORDS + CC_ADMAMB], 1u);
             }
         }
+        if (more) park(buf ^ 1);
+        __syncthreads();
     }
 }
 
@@ -417,41 +484,68 @@ static hipError_t run_refine(const SelectArgs& a, hipStream_t s) {
 
 // Rank of each ambiguous row among the ambiguous rows by (exact key desc,
 // index asc); the first k - n_in are selected.  theta = the key at rank
-// k - n_in - 1, which is the k-th largest exact key overall.
+// k - n_in - 1, which is the k-th largest exact key overall.  A block ranks
+// RK_ROWS rows: thread (row r, quarter q) counts the rows ahead of r in the
+// q-th quarter of each tile of the list (staged in LDS), then the four
+// partial counts are summed.
+constexpr int RK_ROWS = SEL_THREADS / 4;
+constexpr int RK_TILE = 2048;
+
 __global__ __launch_bounds__(SEL_THREADS) void rank_select_kernel(SelectArgs a) {
-    __shared__ double s_k[SEL_THREADS];
-    __shared__ int32_t s_u[SEL_THREADS];
+    __shared__ double s_k[RK_TILE];
+    __shared__ int32_t s_u[RK_TILE];
+    __shared__ uint32_t s_r[4][RK_ROWS];
     const int b = blockIdx.y;
     const int tid = threadIdx.x;
+    const int r = tid % RK_ROWS, q = tid / RK_ROWS;
     const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
     const int64_t namb = sq[SQ_NAMB];
     const int64_t need = a.k - (int64_t)sq[SQ_NIN];
     const double* kb = a.ambkey + (int64_t)b * a.A;
     const int32_t* ub = a.amb + (int64_t)b * a.A;
-    for (int64_t base = (int64_t)blockIdx.x * SEL_THREADS; base < namb; base += (int64_t)gridDim.x * SEL_THREADS) {
-        const int64_t i = base + tid;
+    for (int64_t base = (int64_t)blockIdx.x * RK_ROWS; base < namb; base += (int64_t)gridDim.x * RK_ROWS) {
+        const int64_t i = base + r;
         const bool have = i < namb;
         const double ki = have ? kb[i] : 0.0;
         const int32_t ui = have ? ub[i] : 0;
-        int64_t rank = 0;
-        for (int64_t t0 = 0; t0 < namb; t0 += SEL_THREADS) {
+        uint32_t rank = 0;
+        for (int64_t t0 = 0; t0 < namb; t0 += RK_TILE) {
+            const int lim = (int)min((int64_t)RK_TILE, namb - t0);
             __syncthreads();
-            if (t0 + tid < namb) {
-                s_k[tid] = kb[t0 + tid];
-                s_u[tid] = ub[t0 + tid];
+            constexpr int PER = RK_TILE / SEL_THREADS;
+            double kv[PER];
+            int32_t uv[PER];
+#pragma unroll
+            for (int j = 0; j < PER; ++j) {
+                const int e = tid + SEL_THREADS * j;
+                kv[j] = (e < lim) ? kb[t0 + e] : 0.0;
+                uv[j] = (e < lim) ? ub[t0 + e] : 0;
+            }
+#pragma unroll
+            for (int j = 0; j < PER; ++j) {
+                s_k[tid + SEL_THREADS * j] = kv[j];
+                s_u[tid + SEL_THREADS * j] = uv[j];
             }
             __syncthreads();
-            const int lim = (int)min((int64_t)SEL_THREADS, namb - t0);
-            if (have)
-                for (int j = 0; j < lim; ++j) {
+            if (have) {
+                const int qlen = (lim + 3) / 4;
+                const int j0 = q * qlen, j1 = min(lim, j0 + qlen);
+#pragma unroll 4
+                for (int j = j0; j < j1; ++j) {
                     const double kj = s_k[j];
                     rank += (kj > ki) || (kj == ki && s_u[j] < ui);
                 }
+            }
         }
-        if (have && rank < need) {
-            a.flags[(int64_t)b * a.A + ui] = 1;
-            atomicAdd(&a.ccount[((int64_t)b * a.nch + ui / CHUNK) * CC_WORDS + CC_SELAMB], 1u);
-            if (rank == need - 1) a.theta[b] = ki;
+        s_r[q][r] = rank;
+        __syncthreads();
+        if (q == 0 && have) {
+            const int64_t rk = (int64_t)s_r[0][r] + s_r[1][r] + s_r[2][r] + s_r[3][r];
+            if (rk < need) {
+                a.flags[(int64_t)b * a.A + ui] = 1;
+                atomicAdd(&a.ccount[((int64_t)b * a.nch + ui / CHUNK) * CC_WORDS + CC_SELAMB], 1u);
+                if (rk == need - 1) a.theta[b] = ki;
+            }
         }
     }
 }

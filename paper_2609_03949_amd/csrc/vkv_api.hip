@@ -112,7 +112,7 @@ static WsLayout layout(const vkv_step* st, int64_t k, int64_t cap) {
     L.hsc = o; o = up256(o + (size_t)(B * H * 16));
     L.seq = o; o = up256(o + (size_t)(B * SQ_WORDS * 4));
     L.hist = o; o = up256(o + (size_t)(B * 2 * HIST_BINS * 4));
-    L.vw = o; o = up256(o + (size_t)(B * Aw * 8));
+    L.kt = o; o = up256(o + (size_t)(B * Aw * 4));
     L.flags = o; o = up256(o + (size_t)(B * Aw));
     L.flags2 = o; o = up256(o + (size_t)(B * Aw));
     L.ccount = o; o = up256(o + (size_t)(B * L.nch * CC_WORDS * 4));
@@ -157,7 +157,7 @@ static SelectArgs select_args(const vkv_step* st, const WsLayout& L, char* w) {
     a.T = st->T;
     a.seq = reinterpret_cast<uint32_t*>(w + L.seq);
     a.hist = reinterpret_cast<uint32_t*>(w + L.hist);
-    a.vw = reinterpret_cast<const float*>(w + L.vw);
+    a.kt = reinterpret_cast<const float*>(w + L.kt);
     a.flags = reinterpret_cast<uint8_t*>(w + L.flags);
     a.flags2 = reinterpret_cast<uint8_t*>(w + L.flags2);
     a.ccount = reinterpret_cast<uint32_t*>(w + L.ccount);
@@ -360,7 +360,7 @@ int vkv_score(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, float
     a.T = st->T;
     a.key = key;
     a.ub = ub;
-    a.vw = reinterpret_cast<float*>(w + L.vw);
+    a.kt = reinterpret_cast<float*>(w + L.kt);
     a.seq = reinterpret_cast<uint32_t*>(w + L.seq);
     a.A = L.A;
     a.B = (int)st->B;

@@ -22,6 +22,7 @@ constexpr double CERT_G = 0x1p-40;
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef uint16_t u16x8_t __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -78,6 +79,8 @@ __host__ __device__ __forceinline__ float next_up_f32(float f) {
     return u2f((b & 0x80000000u) ? b - 1u : b + 1u);
 }
 
+__host__ __device__ __forceinline__ float next_down_f32(float f) { return -next_up_f32(-f); }
+
 // Smallest float f with (double)f >= x.
 __host__ __device__ __forceinline__ float ru_f32(double x) {
     float f = (float)x;
@@ -119,10 +122,10 @@ enum SeqWord : int {
     SQ_AMAX = 3,
     SQ_NMAX = 4,
     SQ_EMAX = 5,
-    SQ_KMIN = 6,    // ordered encoding of min_u (key~ - E_u)   (scorer, atomicMin)
-    SQ_KMAX = 7,    // ordered encoding of max_u (key~ + E_u)   (scorer, atomicMax)
-    SQ_TLO = 8,     // float bits: LO <= k-th largest of (key~ - E_u)
-    SQ_THI = 9,     // float bits: HI >= k-th largest of (key~ + E_u)
+    SQ_KMIN = 6,    // ordered encoding of min_u key~_u   (scorer, atomicMin)
+    SQ_KMAX = 7,    // ordered encoding of max_u key~_u   (scorer, atomicMax)
+    SQ_TLO = 8,     // float bits: LO <= k-th largest of (key~ - E)
+    SQ_THI = 9,     // float bits: HI >= k-th largest of (key~ + E)
     SQ_DONE = 10,   // last-block counter of the histogram pass
     SQ_NIN = 11,    // rows certainly in S
     SQ_NAMB = 12,   // ambiguous rows of the selection
@@ -138,7 +141,7 @@ constexpr int ATT_CHUNK = 32;      // rows per attention tile
 constexpr int ATT_HEADS = 64;      // heads per attention workgroup (4 waves x 16)
 
 struct WsLayout {
-    size_t qt, wproj, hsc, seq, hist, vw, flags, flags2, ccount, amb, ambkey, part_o, part_ml, total;
+    size_t qt, wproj, hsc, seq, hist, kt, flags, flags2, ccount, amb, ambkey, part_o, part_ml, total;
     int64_t A, n, nch, splits, rows_per_split, cap;
 };
 
@@ -167,7 +170,7 @@ struct ScoreArgs {
     int64_t T;
     float* key;            // [B,A] or null (diagnostic)
     float* ub;             // [B,A] or null
-    float* vw;             // [B,A,2]: key~ + E_u, key~ - E_u (rounded outward)
+    float* kt;             // [B,A]: key~ (fp32 matrix-core index keys)
     uint32_t* seq;
     int64_t A;
     int B, H, n;
@@ -187,7 +190,7 @@ struct DigestArgs {
 };
 
 struct SelectArgs {
-    const float* vw;       // [B,A,2] from the scorer
+    const float* kt;       // [B,A] key~ from the scorer
     const float* ub;       // [B,A] (admit)
     const uint16_t* x;     // index rows for fp64 re-scoring
     int64_t xs, xbs;
