@@ -6,24 +6,35 @@
 // 576 dims and the value is the 512-dim latent (Sec. 3, Eq. (setup)):
 //   s_h(u) = scale * (q_lat_h . c_u + q_rope_h . r_u),   o_h = sum_u softmax(s_h)_u c_u
 //
-// Work split: workgroup = (split of the row list, group of 64 heads, b);
-// 4 waves x 16 heads.  Per tile of 32 rows the gathered rows are staged in
-// LDS twice: row-major (for S = K Q^T, K = rows as the MFMA A operand) and
-// transposed (for O += P V, V as the B operand).  P never leaves registers:
-// the S accumulator layout of a lane (4 rows x 1 head per 16-row tile) is
-// exactly the A-operand layout of the PV product when the 32 rows of the
-// tile are fed to the K dimension in a permuted order, and the transposed V
-// tile is written in that same order.  Online softmax in the log2 domain;
-// each split emits (unnormalised O, running max, running sum) and a second
-// kernel merges the splits by their log-sum-exp (the appendix's kernel
-// mapping: fetched rows are one more split-KV partition).
+// Work split: workgroup = (split of the row list, group of 128 heads, b);
+// 8 waves x 16 heads, so every gathered row serves all heads of the group.
+// Tiles of 32 rows are double-buffered in LDS: while tile i is scored and
+// accumulated, tile i+1 streams in by direct global->LDS loads
+// (global_load_lds_dwordx4), row-major with piece p of tile row r at slot
+// (p + r) mod 72 (conflict-free MFMA operand reads).  Once a tile has landed
+// its latent half is also written transposed (for O += P V, V as the B
+// operand).  P never leaves registers: the S accumulator layout of a lane (4
+// rows x 1 head per 16-row tile) is exactly the A-operand layout of the PV
+// product when the 32 rows of the tile are fed to the K dimension in a
+// permuted order, and the transposed tile is written in that same order.
+// Online softmax in the log2 domain; each split emits (unnormalised O,
+// running max, running sum) and a second kernel merges the splits by their
+// log-sum-exp (the appendix's kernel mapping: fetched rows are one more
+// split-KV partition).
 #include "vkv_internal.h"
 
 namespace vkv {
 
-constexpr int ATT_THREADS = 256;
-constexpr int KROW = D_ROW + 8;       // LDS row stride of the row-major tile (u16), 1168 B
-constexpr int VT_STRIDE = 40;         // LDS stride of the transposed tile (u16), 80 B
+constexpr int ATT_WAVES = ATT_HEADS / 16;     // 8
+constexpr int ATT_THREADS = 64 * ATT_WAVES;  // 512
+constexpr int ROW_PIECES = D_ROW / 8;        // 72 pieces of 16 B per row
+constexpr int TILE_BYTES = ATT_CHUNK * D_ROW * 2;            // 36 KB
+constexpr int TILE_LOADS = TILE_BYTES / 1024;                // 36 loads of 1 KB
+constexpr int VT_STRIDE = 40;                // LDS stride of the transposed tile (u16), 80 B
+constexpr int VT_BYTES = D_LAT * VT_STRIDE * 2;              // 40 KB
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void gbl_void_t;
 
 // Position of tile row rl on the K axis of the PV product: rows
 // 16*mt + 4*g + i (held by lane group g at accumulator slot i of M-tile mt)
@@ -38,14 +49,24 @@ __device__ __forceinline__ int32_t attended_row(const AttendArgs& a, int b, int6
     return a.adm[(int64_t)b * a.cap + (p - a.k - a.W)];
 }
 
-__global__ __launch_bounds__(ATT_THREADS, 2) void attend_kernel(AttendArgs a) {
-    __shared__ __align__(16) uint16_t s_k[ATT_CHUNK][KROW];
-    __shared__ __align__(16) uint16_t s_vt[D_LAT][VT_STRIDE];
-    __shared__ int32_t s_rows[ATT_CHUNK];
+// byte offset of piece p of tile row r in a row-major stage: the slot is p
+// with its low three bits XORed by (r / 2) mod 8, which spreads the 16 rows
+// read by one MFMA operand load over all LDS banks (rows are 1152 B apart,
+// i.e. alternate between two bank halves)
+__device__ __forceinline__ int kslot(int r, int p) {
+    return r * (D_ROW * 2) + 16 * (p ^ ((r >> 1) & 7));
+}
+
+__global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
+    extern __shared__ __align__(16) uint8_t smem[];
+    uint8_t* s_k = smem;                                      // [2][TILE_BYTES]
+    uint8_t* s_vt = smem + 2 * TILE_BYTES;                    // [2][D_LAT][VT_STRIDE] u16
+    int32_t* s_rows = reinterpret_cast<int32_t*>(smem + 2 * TILE_BYTES + 2 * VT_BYTES);   // the split's rows
 
     const int sp = blockIdx.x, hg = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x;
-    const int wave = tid >> 6, lane = tid & 63, g = lane >> 4, c = lane & 15;
+    const int lane = tid & 63, g = lane >> 4, c = lane & 15;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t nadm = (a.adm && a.cap > 0) ? min((int64_t)max(a.adm_count[b], 0), a.cap) : 0;
     const int64_t N = a.k + a.W + nadm;
     const int64_t p0 = (int64_t)sp * a.rows_per_split;
@@ -62,8 +83,44 @@ __global__ __launch_bounds__(ATT_THREADS, 2) void attend_kernel(AttendArgs a) {
         }
         return;
     }
+    const int ntile = (int)((p1 - p0 + ATT_CHUNK - 1) / ATT_CHUNK);
     const int h0 = hg * ATT_HEADS + wave * 16;
     const int hq = h0 + c;
+    const uint16_t* cb = a.cache + (int64_t)b * a.cbs;
+
+    // the split's row list into LDS (all loads in flight), once
+    const int nrow = (int)(p1 - p0);
+    {
+        constexpr int PER = ATT_MAX_SPLIT_ROWS / ATT_THREADS;
+        int32_t rv[PER];
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int i = tid + ATT_THREADS * j;
+            rv[j] = (i < nrow) ? attended_row(a, b, p0 + i) : 0;
+        }
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int i = tid + ATT_THREADS * j;
+            if (i < nrow) s_rows[i] = rv[j];
+        }
+    }
+    __syncthreads();
+    // direct loads of tile t into stage t & 1 (load instruction j goes to wave
+    // j % 8); rows past the end of the list repeat its last row (loaded, never
+    // weighted)
+    auto issue = [&](int t) {
+        uint8_t* st = s_k + (t & 1) * TILE_BYTES;
+        for (int j = wave; j < TILE_LOADS; j += ATT_WAVES) {
+            const int q = 64 * j + lane;               // destination slot
+            const int r = q / ROW_PIECES, s = q % ROW_PIECES;
+            const int p = s ^ ((r >> 1) & 7);
+            const int i = min(ATT_CHUNK * t + r, nrow - 1);
+            const uint16_t* src = cb + (int64_t)s_rows[i] * a.cs + 8 * p;
+            __builtin_amdgcn_global_load_lds((gbl_void_t*)src, (lds_void_t*)(st + 1024 * j), 16, 0, 0);
+        }
+    };
+    issue(0);
+
     // Q fragments (B operand of S^T = K Q^T): head hq, dims 32*ks + 8*g .. +8
     bf16x8_t qf[D_ROW / 32];
 #pragma unroll
@@ -81,59 +138,45 @@ __global__ __launch_bounds__(ATT_THREADS, 2) void attend_kernel(AttendArgs a) {
     f32x4_t o[D_LAT / 16];
 #pragma unroll
     for (int t = 0; t < D_LAT / 16; ++t) o[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    const uint16_t* cb = a.cache + (int64_t)b * a.cbs;
 
-    for (int64_t c0 = p0; c0 < p1; c0 += ATT_CHUNK) {
-        const int nr = (int)min((int64_t)ATT_CHUNK, p1 - c0);
-        __syncthreads();
-        if (tid < ATT_CHUNK) s_rows[tid] = (tid < nr) ? attended_row(a, b, c0 + tid) : 0;
-        __syncthreads();
-        // gather: 32 rows x 72 pieces of 16 B = 9 pieces per thread, loaded in
-        // three batches of three (each batch in flight together; the register
-        // budget does not allow all nine)
-        constexpr int NPIECE = ATT_CHUNK * (D_ROW / 8) / ATT_THREADS;
-        constexpr int NBATCH = 3;
-        static_assert(NPIECE * ATT_THREADS == ATT_CHUNK * (D_ROW / 8), "tile must split evenly");
-        static_assert(NPIECE % NBATCH == 0, "batches must split evenly");
-#pragma unroll 1
-        for (int j0 = 0; j0 < NPIECE; j0 += NBATCH) {
-            u16x8_t v[NBATCH];
+    for (int t = 0; t < ntile; ++t) {
+        const int cur = t & 1;
+        const int nr = (int)min((int64_t)ATT_CHUNK, p1 - (p0 + (int64_t)ATT_CHUNK * t));
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's loads of tile t have landed
+        __syncthreads();                                   // ... and every wave's
+        if (t + 1 < ntile) issue(t + 1);
+        const uint8_t* kt = s_k + cur * TILE_BYTES;
+        uint16_t* vt = reinterpret_cast<uint16_t*>(s_vt + cur * VT_BYTES);
+        // latent half transposed: each thread 4 pieces (row r, dims 8pc..8pc+7);
+        // the 32 lanes of a half-wave take the 32 rows of one piece, so one
+        // store instruction covers 32 consecutive K slots of 2 rows of V^T
 #pragma unroll
-            for (int j = 0; j < NBATCH; ++j) {
-                const int p = tid + ATT_THREADS * (j0 + j);
-                const int rl = p / (D_ROW / 8), pc = p % (D_ROW / 8);
-                v[j] = (rl < nr) ? *reinterpret_cast<const u16x8_t*>(cb + (int64_t)s_rows[rl] * a.cs + 8 * pc)
-                                 : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
-            }
+        for (int jj = 0; jj < ATT_CHUNK * (D_LAT / 8) / ATT_THREADS; ++jj) {
+            const int pi = tid + ATT_THREADS * jj;
+            const int r = pi & (ATT_CHUNK - 1), pc = pi >> 5;
+            const u16x8_t v = *reinterpret_cast<const u16x8_t*>(kt + kslot(r, pc));
+            uint16_t* dst = vt + (8 * pc) * VT_STRIDE + pv_slot(r);
 #pragma unroll
-            for (int j = 0; j < NBATCH; ++j) {
-                const int p = tid + ATT_THREADS * (j0 + j);
-                const int rl = p / (D_ROW / 8), pc = p % (D_ROW / 8);
-                *reinterpret_cast<u16x8_t*>(&s_k[rl][8 * pc]) = v[j];
-                if (pc < D_LAT / 8) {
-                    // staggered element order spreads the 64 lanes over the LDS banks
-                    const int pos = pv_slot(rl);
-                    const int rot = pc + (pc >> 3);
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const int e2 = (e + rot) & 7;
-                        s_vt[8 * pc + e2][pos] = v[j][e2];
-                    }
-                }
-            }
+            for (int e = 0; e < 8; ++e) dst[e * VT_STRIDE] = v[e];
         }
-        __syncthreads();
-        // S^T[row][head] for the 32 rows (two 16-row M tiles) and 16 heads
+        // operand of (row 16 mt + c, piece 4 ks + g): with x = (c / 2) mod 8 the
+        // slot is 4 (ks ^ (x / 4)) + (g ^ (x mod 4)), so one base per ks parity
         f32x4_t sacc[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
+        {
+            const int x = (c >> 1) & 7;
+            const uint8_t* ke = kt + c * (D_ROW * 2) + 16 * (g ^ (x & 3)) + 64 * (x >> 2);
+            const uint8_t* ko = kt + c * (D_ROW * 2) + 16 * (g ^ (x & 3)) - 64 * (x >> 2);
 #pragma unroll
-        for (int ks = 0; ks < D_ROW / 32; ++ks)
+            for (int ks = 0; ks < D_ROW / 32; ++ks)
 #pragma unroll
-            for (int mt = 0; mt < 2; ++mt) {
-                const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(&s_k[16 * mt + c][32 * ks + 8 * g]);
-                sacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[ks], sacc[mt], 0, 0, 0);
-            }
+                for (int mt = 0; mt < 2; ++mt) {
+                    const uint8_t* src = ((ks & 1) ? ko : ke) + 16 * mt * (D_ROW * 2) + 64 * ks;
+                    const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(src);
+                    sacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[ks], sacc[mt], 0, 0, 0);
+                }
+        }
         // sacc[mt][i] = score of row 16*mt + 4*g + i for head hq
-        float t[2][4];
+        float sc[2][4];
         float cmax = -INFINITY;
 #pragma unroll
         for (int mt = 0; mt < 2; ++mt)
@@ -141,7 +184,7 @@ __global__ __launch_bounds__(ATT_THREADS, 2) void attend_kernel(AttendArgs a) {
             for (int i = 0; i < 4; ++i) {
                 const int rl = 16 * mt + 4 * g + i;
                 const float v = (rl < nr) ? sacc[mt][i] * a.scale_log2 : -INFINITY;
-                t[mt][i] = v;
+                sc[mt][i] = v;
                 cmax = fmaxf(cmax, v);
             }
         cmax = fmaxf(cmax, __shfl_xor(cmax, 16));
@@ -154,7 +197,7 @@ __global__ __launch_bounds__(ATT_THREADS, 2) void attend_kernel(AttendArgs a) {
         for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const float p = exp2f(t[mt][i] - m_new);
+                const float p = exp2f(sc[mt][i] - m_new);
                 psum += p;
                 pa[4 * mt + i] = (__bf16)p;
             }
@@ -165,11 +208,12 @@ __global__ __launch_bounds__(ATT_THREADS, 2) void attend_kernel(AttendArgs a) {
         float al[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) al[i] = __shfl(alpha, 4 * g + i);
+        __syncthreads();   // transposed tile complete
 #pragma unroll
         for (int tt = 0; tt < D_LAT / 16; ++tt) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) o[tt][i] *= al[i];
-            const bf16x8_t vb = *reinterpret_cast<const bf16x8_t*>(&s_vt[16 * tt + c][8 * g]);
+            const bf16x8_t vb = *reinterpret_cast<const bf16x8_t*>(&vt[(16 * tt + c) * VT_STRIDE + 8 * g]);
             o[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, o[tt], 0, 0, 0);
         }
     }
@@ -225,9 +269,14 @@ __global__ __launch_bounds__(128) void attend_combine_kernel(AttendArgs a) {
     if (tid == 0) a.lse[bh] = (M + log2f(L)) * 0.69314718055994530942f;
 }
 
+constexpr size_t ATT_SMEM = 2 * (size_t)TILE_BYTES + 2 * (size_t)VT_BYTES + ATT_MAX_SPLIT_ROWS * sizeof(int32_t);
+
 hipError_t launch_attend(const AttendArgs& a, hipStream_t s) {
     dim3 grid((unsigned)a.splits, (unsigned)((a.H + ATT_HEADS - 1) / ATT_HEADS), (unsigned)a.B);
-    hipLaunchKernelGGL(attend_kernel, grid, dim3(ATT_THREADS), 0, s, a);
+    hipError_t e0 = hipFuncSetAttribute(reinterpret_cast<const void*>(attend_kernel),
+                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)ATT_SMEM);
+    if (e0 != hipSuccess) return e0;
+    hipLaunchKernelGGL(attend_kernel, grid, dim3(ATT_THREADS), ATT_SMEM, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(attend_combine_kernel, dim3((unsigned)(a.B * a.H)), dim3(128), 0, s, a);

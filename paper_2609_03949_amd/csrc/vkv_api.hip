@@ -89,10 +89,10 @@ static int check_step(vkv_ctx* ctx, const vkv_step* st) {
 static void attend_split(const vkv_step* st, int64_t k, int64_t cap, int64_t* splits, int64_t* rps) {
     const int64_t nmax = k + st->W + cap;
     const int64_t groups = st->B * ((st->H + ATT_HEADS - 1) / ATT_HEADS);
-    int64_t want = std::max<int64_t>(1, (512 + groups - 1) / groups);      // ~2 workgroups per CU
+    int64_t want = std::max<int64_t>(1, (256 + groups - 1) / groups);      // ~1 workgroup per CU
     int64_t rows = (nmax + want - 1) / want;
     rows = std::max<int64_t>(rows, 128);
-    rows = std::min<int64_t>(rows, 4096);
+    rows = std::min<int64_t>(rows, ATT_MAX_SPLIT_ROWS);
     rows = (rows + ATT_CHUNK - 1) / ATT_CHUNK * ATT_CHUNK;
     *rps = rows;
     *splits = std::max<int64_t>(1, (nmax + rows - 1) / rows);

@@ -138,7 +138,8 @@ constexpr int CC_WORDS = 4;        // per-chunk counters
 enum ChunkWord : int { CC_IN = 0, CC_SELAMB = 1, CC_ADM = 2, CC_ADMAMB = 3 };
 constexpr int HIST_BINS = 4096;
 constexpr int ATT_CHUNK = 32;      // rows per attention tile
-constexpr int ATT_HEADS = 64;      // heads per attention workgroup (4 waves x 16)
+constexpr int ATT_HEADS = 128;     // heads per attention workgroup (8 waves x 16)
+constexpr int ATT_MAX_SPLIT_ROWS = 1024;   // rows of one split (row list held in LDS)
 
 struct WsLayout {
     size_t qt, wproj, hsc, seq, hist, kt, flags, flags2, ccount, amb, ambkey, part_o, part_ml, total;
