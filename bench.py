@@ -62,7 +62,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
-              "(sequences shard across GPUs with no communication; see DESIGN.md).",
+              "(sequences are independent and would shard across GPUs with no communication).",
               file=sys.stderr)
         sys.exit(2)
 

@@ -13,7 +13,7 @@ SOURCES = ["vkv_api.hip", "k_score.hip", "k_digest.hip", "k_select.hip", "k_atte
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     "-ffp-contract=off",
-    # packed fp32 instructions stay off
+    # hipcc must not form packed fp32 (v_pk_*_f32) instructions on its own
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
 ]
