@@ -61,7 +61,7 @@ def main():
                     help="also run a plain 1 GiB device copy (counter scale for --pmc runs)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
+        print("bench.py measures one GPU: libvkv has no multi-GPU path "
               "(sequences are independent and would shard across GPUs with no communication).",
               file=sys.stderr)
         sys.exit(2)
