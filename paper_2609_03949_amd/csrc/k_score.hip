@@ -17,14 +17,18 @@ namespace vkv {
 // ----------------------------------------------------------- query prep
 
 // Stage 1: w[b,h,j] = sum_i P[j,i] q_lat[b,h,i] (fp64, i ascending) and the
-// query digest qt[b,h,off+j] = RNE_bf16(w).  A block owns 64 basis rows (held
-// transposed in LDS) and 16 heads; each thread runs four independent fp64
-// chains (four heads).  Block (0,0,b) also clears the step state of b.
+// query digest qt[b,h,off+j] = RNE_bf16(w).  A block owns 64 basis rows and
+// 16 heads; each thread runs four independent fp64 chains (four heads of one
+// basis row).  The i axis is walked in chunks of 128 held in LDS as fp64 (P^T
+// and the queries, converted once), and the next chunk is fetched into
+// registers while the current one is consumed.  Block (0,0,b) also clears the
+// step state of sequence b.
 constexpr int QP_HEADS = 16;
+constexpr int QP_IC = 128;
 
 __global__ __launch_bounds__(256) void qprep_project_kernel(QprepArgs a) {
-    __shared__ uint16_t s_pt[D_LAT][66];   // P^T tile, padded against bank conflicts
-    __shared__ float s_q[QP_HEADS][D_LAT];
+    __shared__ __align__(16) double s_p[QP_IC][64];         // P^T chunk: [i][j]
+    __shared__ __align__(16) double s_q[QP_IC][QP_HEADS];   // query chunk: [i][head]
     const int b = blockIdx.z;
     const int tid = threadIdx.x;
     if (blockIdx.x == 0 && blockIdx.y == 0) {
@@ -35,52 +39,58 @@ __global__ __launch_bounds__(256) void qprep_project_kernel(QprepArgs a) {
     const int j0 = 64 * blockIdx.x;
     const int jn = min(64, a.r - j0);
     const int h0 = QP_HEADS * blockIdx.y;
-    {
-        // P rows j0.. as 16-byte pieces (64 per row), all loads in flight together
-        constexpr int PPT = 64 * 64 / 256;   // pieces per thread for a full 64-row tile
-        u16x8_t pv[PPT];
+    // chunk c: P rows j0.. (lane row = p & 63, piece p >> 6) and query rows
+    // h0.. (head = p & 15, piece p >> 4), 16-byte pieces of 8 i each
+    u16x8_t pv[4], qv;
+    auto fetch = [&](int c) {
 #pragma unroll
-        for (int j = 0; j < PPT; ++j) {
-            const int idx = tid + 256 * j;
-            const int jl = idx >> 6, p = idx & 63;
-            pv[j] = (jl < jn) ? *reinterpret_cast<const u16x8_t*>(a.P + (int64_t)(j0 + jl) * D_LAT + 8 * p)
-                              : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+        for (int jj = 0; jj < 4; ++jj) {
+            const int p = tid + 256 * jj;
+            const int row = p & 63, pc = p >> 6;
+            pv[jj] = (row < jn) ? *reinterpret_cast<const u16x8_t*>(a.P + (int64_t)(j0 + row) * D_LAT + QP_IC * c + 8 * pc)
+                                : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
         }
-        constexpr int QPT = QP_HEADS * 64 / 256;
-        u16x8_t qv[QPT];
+        const int hh = tid & 15, pc = tid >> 4;
+        qv = (h0 + hh < a.H) ? *reinterpret_cast<const u16x8_t*>(a.q_lat + ((int64_t)b * a.H + h0 + hh) * D_LAT + QP_IC * c + 8 * pc)
+                             : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    };
+    auto park = [&]() {
 #pragma unroll
-        for (int j = 0; j < QPT; ++j) {
-            const int idx = tid + 256 * j;
-            const int hl = idx >> 6, p = idx & 63;
-            const int h = h0 + hl;
-            qv[j] = (h < a.H) ? *reinterpret_cast<const u16x8_t*>(a.q_lat + ((int64_t)b * a.H + h) * D_LAT + 8 * p)
-                              : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+        for (int jj = 0; jj < 4; ++jj) {
+            const int p = tid + 256 * jj;
+            const int row = p & 63, pc = p >> 6;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) s_p[8 * pc + e][row] = (double)bf16_to_f32(pv[jj][e]);
         }
+        const int hh = tid & 15, pc = tid >> 4;
 #pragma unroll
-        for (int j = 0; j < PPT; ++j) {
-            const int idx = tid + 256 * j;
-            const int jl = idx >> 6, p = idx & 63;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) s_pt[8 * p + e][jl] = pv[j][e];
-        }
-#pragma unroll
-        for (int j = 0; j < QPT; ++j) {
-            const int idx = tid + 256 * j;
-            const int hl = idx >> 6, p = idx & 63;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) s_q[hl][8 * p + e] = bf16_to_f32(qv[j][e]);
-        }
-    }
-    __syncthreads();
+        for (int e = 0; e < 8; ++e) s_q[8 * pc + e][hh] = (double)bf16_to_f32(qv[e]);
+    };
     const int jl = tid & 63, hg = tid >> 6;
-    if (jl >= jn) return;
     double acc[4] = {0.0, 0.0, 0.0, 0.0};
-#pragma unroll 4
-    for (int i = 0; i < D_LAT; ++i) {
-        const double p = (double)bf16_to_f32(s_pt[i][jl]);
-#pragma unroll
-        for (int t = 0; t < 4; ++t) acc[t] = fma(p, (double)s_q[4 * hg + t][i], acc[t]);
+    fetch(0);
+    park();
+    __syncthreads();
+    for (int c = 0; c < D_LAT / QP_IC; ++c) {
+        const bool more = c + 1 < D_LAT / QP_IC;
+        if (more) fetch(c + 1);
+#pragma unroll 8
+        for (int i = 0; i < QP_IC; ++i) {
+            const double p = s_p[i][jl];
+            const double2 qa = *reinterpret_cast<const double2*>(&s_q[i][4 * hg]);
+            const double2 qb = *reinterpret_cast<const double2*>(&s_q[i][4 * hg + 2]);
+            acc[0] = fma(p, qa.x, acc[0]);
+            acc[1] = fma(p, qa.y, acc[1]);
+            acc[2] = fma(p, qb.x, acc[2]);
+            acc[3] = fma(p, qb.y, acc[3]);
+        }
+        __syncthreads();
+        if (more) {
+            park();
+            __syncthreads();
+        }
     }
+    if (jl >= jn) return;
     const int off = (a.mode & 1) ? D_ROPE : 0;
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
@@ -96,20 +106,51 @@ __global__ __launch_bounds__(256) void qprep_project_kernel(QprepArgs a) {
 // upper bound (Lemma (Index certificate) plus the bf16 rounding of the stored
 // sketch; fixed fp64 evaluation order, the same as the oracle's):
 //   a_h >= sqrt(q^T (I - P^T P) q),  n_h >= ||qd_h||,  e_h >= ||qd_h - P q||
-// plus ||qt_h|| for the scorer's error bound, and the rope half of qt.  Lane
-// 4*hl + t runs sum t of head hl sequentially: t=0 ||q||^2, t=1 ||w||^2,
-// t=2 ||qd - w||^2, t=3 ||qd||^2.
+// plus ||qt_h|| for the scorer's error bound, and the rope half of qt.  The
+// wave first stages its heads' q_lat, projections and digests in LDS (all
+// loads in flight); then lane 4*hl + t runs sum t of head hl sequentially:
+// t=0 ||q||^2, t=1 ||w||^2, t=2 ||qd - w||^2, t=3 ||qd||^2.
 constexpr int QF_HEADS = 16;
+constexpr int QF_RMAX = 512;
 
 __global__ __launch_bounds__(64) void qprep_finish_kernel(QprepArgs a) {
+    __shared__ __align__(16) uint16_t s_ql[QF_HEADS][D_LAT];   // 16 KB
+    __shared__ __align__(16) uint16_t s_qd[QF_HEADS][QF_RMAX]; // 16 KB
     const int lane = threadIdx.x;
     const int hl = lane >> 2, t = lane & 3;
-    const int64_t bh = (int64_t)blockIdx.x * QF_HEADS + hl;
-    const bool have = bh < (int64_t)a.B * a.H;
-    const int64_t bhc = have ? bh : 0;
-    const int b = (int)(bhc / a.H);
+    const int64_t bh0 = (int64_t)blockIdx.x * QF_HEADS;
+    const int64_t nbh = (int64_t)a.B * a.H;
     const int off = (a.mode & 1) ? D_ROPE : 0;
     const int rd = (a.mode & 2) ? a.r : 0;
+    {
+        // q_lat rows: 16 heads x 64 pieces; digests: 16 heads x rd/8 pieces
+        constexpr int PER = QF_HEADS * (D_LAT / 8) / 64;
+        u16x8_t v[PER];
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int p = lane + 64 * j;
+            const int h = p >> 6, pc = p & 63;
+            v[j] = (bh0 + h < nbh) ? *reinterpret_cast<const u16x8_t*>(a.q_lat + (bh0 + h) * D_LAT + 8 * pc)
+                                   : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+        }
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int p = lane + 64 * j;
+            *reinterpret_cast<u16x8_t*>(&s_ql[p >> 6][8 * (p & 63)]) = v[j];
+        }
+        const int r8 = rd / 8;
+        for (int p = lane; p < QF_HEADS * r8; p += 64) {
+            const int h = p / r8, pc = p % r8;
+            u16x8_t d = u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+            if (bh0 + h < nbh) d = *reinterpret_cast<const u16x8_t*>(a.qt + (bh0 + h) * a.n + off + 8 * pc);
+            *reinterpret_cast<u16x8_t*>(&s_qd[h][8 * pc]) = d;
+        }
+    }
+    __syncthreads();
+    const int64_t bh = bh0 + hl;
+    const bool have = bh < nbh;
+    const int64_t bhc = have ? bh : 0;
+    const int b = (int)(bhc / a.H);
     uint16_t* qt = a.qt + bhc * a.n;
     const double* w = a.wproj + bhc * a.r;
     // rope half of qt: 8 pieces of 16 B per head, 4 lanes per head
@@ -122,33 +163,40 @@ __global__ __launch_bounds__(64) void qprep_finish_kernel(QprepArgs a) {
     double acc = 0.0;
     if (have) {
         if (t == 0) {
-            const u16x8_t* q = reinterpret_cast<const u16x8_t*>(a.q_lat + bhc * D_LAT);
-#pragma unroll 1
-            for (int p0 = 0; p0 < D_LAT / 8; p0 += 8) {
-                u16x8_t v[8];
+#pragma unroll 4
+            for (int p = 0; p < D_LAT / 8; ++p) {
+                const u16x8_t v = *reinterpret_cast<const u16x8_t*>(&s_ql[hl][8 * p]);
 #pragma unroll
-                for (int j = 0; j < 8; ++j) v[j] = q[p0 + j];
-#pragma unroll
-                for (int j = 0; j < 8; ++j)
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const double x = (double)bf16_to_f32(v[j][e]);
-                        acc = fma(x, x, acc);
-                    }
+                for (int e = 0; e < 8; ++e) {
+                    const double x = (double)bf16_to_f32(v[e]);
+                    acc = fma(x, x, acc);
+                }
             }
         } else if (t == 1) {
-#pragma unroll 8
-            for (int j = 0; j < rd; ++j) acc = fma(w[j], w[j], acc);
+            for (int j0 = 0; j0 < rd; j0 += 8) {
+                double wv[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) wv[e] = w[j0 + e];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc = fma(wv[e], wv[e], acc);
+            }
         } else {
-            const uint16_t* qd = qt + off;
-#pragma unroll 8
-            for (int j = 0; j < rd; ++j) {
-                const double d = (double)bf16_to_f32(qd[j]);
+            for (int j0 = 0; j0 < rd; j0 += 8) {
+                double wv[8];
                 if (t == 2) {
-                    const double e = d - w[j];
-                    acc = fma(e, e, acc);
-                } else {
-                    acc = fma(d, d, acc);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) wv[e] = w[j0 + e];
+                }
+                const u16x8_t dv = *reinterpret_cast<const u16x8_t*>(&s_qd[hl][j0]);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const double d = (double)bf16_to_f32(dv[e]);
+                    if (t == 2) {
+                        const double ee = d - wv[e];
+                        acc = fma(ee, ee, acc);
+                    } else {
+                        acc = fma(d, d, acc);
+                    }
                 }
             }
         }

@@ -3,15 +3,22 @@
 // Selection (per sequence b, archive rows [0, A)), given fp32 keys key~ with a
 // certified bound |key~ - key| <= E for every row (key = the fp64 index score,
 // E from the per-sequence maxima of ||qt_h|| and ||x_u||):
-//   1. one histogram pass over 4096 linear bins of [min key~ - E, max key~ + E]
-//      of v = key~ + E and w = key~ - E (rounded outward) brackets the k-th
-//      largest exact key: HI >= k-th largest v and LO <= k-th largest w;
+//   1. a strided sample of the keys places a bracket [t_lo, t_hi] around the
+//      k-th largest key~; one counting pass counts the keys above t_hi and
+//      histograms the keys inside it over 4096 fine bins, and finds the bin of
+//      the k-th largest key~ (if the sample missed, the same block redoes the
+//      histogram over the whole key range).  With v = key~ + E and w = key~ - E
+//      (rounded outward) this gives HI >= k-th largest v and LO <= k-th
+//      largest w, so the k-th largest exact key lies in [LO, HI];
 //   2. rows with w > HI are certainly selected and rows with v < LO certainly
 //      not; the rows in between are appended to an ambiguous list;
-//   3. the ambiguous rows are re-scored in fp64 (d ascending: the exact
-//      definition) and ranked among themselves by (score desc, index asc); the
-//      first k - n_in join S, and the one of rank k - n_in - 1 gives theta;
-//   4. an ordered compaction writes S ascending.
+//   3. each ambiguous row's heads are scored again in fp32 (any order: the
+//      same bound E holds) and only the heads that can still hold the maximum
+//      (within 2E of it) are re-scored in fp64 with d ascending -- the exact
+//      definition -- as independent (row, head) chains;
+//   4. the ambiguous rows are ranked among themselves by (exact key desc,
+//      index asc); the first k - n_in join S, and rank k - n_in - 1 gives theta;
+//   5. an ordered compaction writes S ascending.
 // Admission (Lemma (Index certificate)) applies the same band argument to the
 // upper bound UB_u against theta.
 #include "vkv_internal.h"
@@ -19,9 +26,20 @@
 namespace vkv {
 
 constexpr int SEL_THREADS = 256;
-constexpr int HIST_KEYS_PER_BLOCK = 16384;
-constexpr int REFINE_BLOCKS = 32;
+constexpr int SAMPLE_MAX = 4096;             // keys sampled per sequence to place the bracket
+constexpr int COUNT_KEYS_PER_BLOCK = 4096;   // keys per block of the counting pass
+constexpr int KEY_BATCH = 16;                // keys per thread in flight
+constexpr int EX_BLOCKS = 16;                // per sequence: blocks of the exact-key pass
 constexpr int RANK_BLOCKS = 16;
+
+// order-preserving encoding of fp64 (for 64-bit atomic max); -0 maps as +0
+__device__ __forceinline__ uint64_t f64_to_ord(double d) {
+    const uint64_t u = d2u(d == 0.0 ? 0.0 : d);
+    return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+__device__ __forceinline__ double ord_to_f64(uint64_t o) {
+    return u2d((o >> 63) ? (o & 0x7FFFFFFFFFFFFFFFull) : ~o);
+}
 
 // ------------------------------------------------------------ error bounds
 
@@ -116,113 +134,233 @@ __device__ __forceinline__ uint32_t block_suffix_incl(uint32_t v, uint32_t* s_w)
     return v + add;
 }
 
-// Histograms of v_u = key~_u + E and w_u = key~_u - E over linear bins of
-// [min v, max v].  The last block to finish finds the bins holding the k-th
-// largest v and the k-th largest w and stores
-//   HI >= k-th largest v  and  LO <= k-th largest w
-// (bin edges widened past the fp32 rounding of the binning).  Since
-// w_u <= key_u <= v_u, the k-th largest exact key lies in [LO, HI].
-constexpr int HIST_BATCH = 16;   // keys per thread in flight
+// ------------------------------------------------------------ the bracket
 
-__global__ __launch_bounds__(SEL_THREADS) void hist_kernel(SelectArgs a) {
-    __shared__ uint32_t s_hv[HIST_BINS];
-    __shared__ uint32_t s_hw[HIST_BINS];
+// Bin d of the linear bins of [lo, lo + HIST_BINS / scale): keys x with
+// bin_of(x) = d satisfy edge_lo(d) <= x <= edge_hi(d) (the fp32 rounding of the
+// binning is covered by the widening).
+__device__ __forceinline__ double edge_hi_of(int d, float lo, float hi, float scale) {
+    if (!(scale > 0.f)) return (double)hi;
+    const double w = 1.0 / (double)scale;
+    const double slack = fabs((double)lo) * 0x1p-22 + 0x1p-100;
+    return fmin((double)hi, (double)lo + (double)(d + 1) * w * (1.0 + 0x1p-20) + slack);
+}
+__device__ __forceinline__ double edge_lo_of(int d, float lo, float scale) {
+    if (!(scale > 0.f)) return (double)lo;
+    const double w = 1.0 / (double)scale;
+    const double slack = fabs((double)lo) * 0x1p-22 + 0x1p-100;
+    return fmax((double)lo, (double)lo + (double)d * w * (1.0 - 0x1p-20) - slack);
+}
+
+// In a block of SEL_THREADS threads holding a histogram s_h[HIST_BINS]: the
+// bin d where the count of keys in bins >= d first reaches `target` (1 <=
+// target <= total).  Returns -1 in threads that do not own it.
+__device__ __forceinline__ int find_rank_bin(const uint32_t* s_h, uint32_t target, uint32_t* s_w) {
+    constexpr int PER = HIST_BINS / SEL_THREADS;
+    const int tid = threadIdx.x;
+    uint32_t loc = 0;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) loc += s_h[tid * PER + j];
+    const uint32_t suf = block_suffix_incl(loc, s_w);
+    int found = -1;
+    if (suf - loc < target && target <= suf) {
+        uint32_t run = suf - loc;
+        for (int d = (tid + 1) * PER - 1; d >= tid * PER; --d) {
+            run += s_h[d];
+            if (run >= target) {
+                found = d;
+                break;
+            }
+        }
+    }
+    return found;
+}
+
+// The bracket of the k-th largest key~ placed from a sample of up to
+// SAMPLE_MAX keys (runs of 32 consecutive keys at evenly spaced offsets; all
+// keys if A <= SAMPLE_MAX): [t_lo, t_hi] with sample ranks k_s -/+ (4 sqrt(k_s)
+// + 16), k_s = k m / A, from a histogram of the sample over its own range.  A
+// deterministic function of the keys, so every block that evaluates it gets
+// the same bracket.  Only a heuristic: the bracket pass checks it.
+__device__ void sample_bracket(const SelectArgs& a, int b, const uint32_t* sq, uint32_t* s_h, uint32_t* s_w,
+                               float* s_mm, float& t_lo, float& t_hi) {
+    const int tid = threadIdx.x;
+    const int64_t A = a.A;
+    const int m = (int)min(A, (int64_t)SAMPLE_MAX);
+    const float* kt = a.kt + (int64_t)b * A;
+    constexpr int PER = SAMPLE_MAX / SEL_THREADS;
+    constexpr int RUN = 32;
+    const int nrun = (m + RUN - 1) / RUN;
+    const int64_t stride = (m < A && nrun > 1) ? (A - RUN) / (nrun - 1) : 0;
+    float v[PER];
+    float lo = INFINITY, hi = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int i = tid + SEL_THREADS * j;
+        const int64_t u = (m == A) ? i : min(A - 1, (int64_t)(i / RUN) * stride + (i % RUN));
+        v[j] = (i < m) ? kt[u] : 0.f;
+        if (i < m) {
+            lo = fminf(lo, v[j]);
+            hi = fmaxf(hi, v[j]);
+        }
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+        lo = fminf(lo, __shfl_xor(lo, o));
+        hi = fmaxf(hi, __shfl_xor(hi, o));
+    }
+    if ((tid & 63) == 0) {
+        s_mm[tid >> 6] = lo;
+        s_mm[4 + (tid >> 6)] = hi;
+    }
+    for (int i = tid; i < HIST_BINS; i += SEL_THREADS) s_h[i] = 0u;
+    __syncthreads();
+    lo = fminf(fminf(s_mm[0], s_mm[1]), fminf(s_mm[2], s_mm[3]));
+    hi = fmaxf(fmaxf(s_mm[4], s_mm[5]), fmaxf(s_mm[6], s_mm[7]));
+    const float scale = bin_scale(lo, hi);
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int i = tid + SEL_THREADS * j;
+        if (i < m) atomicAdd(&s_h[bin_of(v[j], lo, scale)], 1u);
+    }
+    __syncthreads();
+    const double ks = (double)a.k * (double)m / (double)A;
+    const double dl = 4.0 * sqrt(ks) + 16.0;
+    const int64_t c_hi = (int64_t)floor(ks - dl);   // fewer than c_hi samples above t_hi
+    const int64_t c_lo = (int64_t)ceil(ks + dl);    // at least c_lo samples at or above t_lo
+    const int d_hi = (c_hi >= 1) ? find_rank_bin(s_h, (uint32_t)c_hi, s_w) : -1;
+    const int d_lo = (c_lo <= m) ? find_rank_bin(s_h, (uint32_t)c_lo, s_w) : -1;
+    __syncthreads();
+    // no cut on a side the sample cannot place: the scorer's key extremes
+    if (tid == 0) {
+        s_mm[0] = ord_to_key(sq[SQ_KMAX]);
+        s_mm[1] = ord_to_key(sq[SQ_KMIN]);
+    }
+    __syncthreads();
+    if (d_hi >= 0) s_mm[0] = scale > 0.f ? lo + (float)(d_hi + 1) / scale : hi;
+    if (d_lo >= 0) s_mm[1] = scale > 0.f ? lo + (float)d_lo / scale : lo;
+    __syncthreads();
+    t_hi = s_mm[0];
+    t_lo = s_mm[1];
+    __syncthreads();
+}
+
+// Counting pass: every block places the sampled bracket, then counts its keys
+// above t_hi and histograms those in [t_lo, t_hi] over HIST_BINS fine bins
+// (the bulk of the keys, below t_lo, costs one compare), into per-sequence
+// global counters by atomics.
+__global__ __launch_bounds__(SEL_THREADS) void count_kernel(SelectArgs a) {
+    __shared__ uint32_t s_h[HIST_BINS];
     __shared__ uint32_t s_w[SEL_THREADS / 64];
-    __shared__ int s_last;
+    __shared__ float s_mm[8];
     const int b = blockIdx.y;
     const int tid = threadIdx.x;
     uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    uint32_t* gv = a.hist + (int64_t)b * 2 * HIST_BINS;
-    uint32_t* gw = gv + HIST_BINS;
+    uint32_t* gh = a.hist + (int64_t)b * 2 * HIST_BINS;
+    float tlo, thi;
+    sample_bracket(a, b, sq, s_h, s_w, s_mm, tlo, thi);
     if (blockIdx.x == 0 && tid == 0) {
-        sq[SQ_NIN] = 0u;
+        sq[SQ_BLO] = __float_as_uint(tlo);
+        sq[SQ_BHI] = __float_as_uint(thi);
         sq[SQ_NAMB] = 0u;
         sq[SQ_NAMB2] = 0u;
-        a.theta[b] = -INFINITY;
     }
-    const float E = key_band_f32(sq, a.n);
-    const float lo = band_lo(ord_to_key(sq[SQ_KMIN]), E);
-    const float hi = band_hi(ord_to_key(sq[SQ_KMAX]), E);
-    const float scale = bin_scale(lo, hi);
-    for (int i = tid; i < HIST_BINS; i += SEL_THREADS) {
-        s_hv[i] = 0u;
-        s_hw[i] = 0u;
-    }
+    const float scale = bin_scale(tlo, thi);
+    for (int i = tid; i < HIST_BINS; i += SEL_THREADS) s_h[i] = 0u;
     __syncthreads();
     const float* kt = a.kt + (int64_t)b * a.A;
-    const int64_t u0 = (int64_t)blockIdx.x * HIST_KEYS_PER_BLOCK;
-    const int64_t u1 = min(a.A, u0 + HIST_KEYS_PER_BLOCK);
-    for (int64_t ub = u0; ub < u1; ub += HIST_BATCH * SEL_THREADS) {
-        float k[HIST_BATCH];
+    const int64_t u0 = (int64_t)blockIdx.x * COUNT_KEYS_PER_BLOCK;
+    const int64_t u1 = min(a.A, u0 + COUNT_KEYS_PER_BLOCK);
+    uint32_t above = 0;
+    for (int64_t ub = u0; ub < u1; ub += KEY_BATCH * SEL_THREADS) {
+        float k[KEY_BATCH];
 #pragma unroll
-        for (int j = 0; j < HIST_BATCH; ++j) {
+        for (int j = 0; j < KEY_BATCH; ++j) {
             const int64_t u = ub + tid + (int64_t)j * SEL_THREADS;
             k[j] = (u < u1) ? kt[u] : 0.f;
         }
 #pragma unroll
-        for (int j = 0; j < HIST_BATCH; ++j) {
+        for (int j = 0; j < KEY_BATCH; ++j) {
             const int64_t u = ub + tid + (int64_t)j * SEL_THREADS;
-            if (u < u1) {
-                atomicAdd(&s_hv[bin_of(band_hi(k[j], E), lo, scale)], 1u);
-                atomicAdd(&s_hw[bin_of(band_lo(k[j], E), lo, scale)], 1u);
-            }
+            if (u >= u1) continue;
+            if (k[j] > thi) ++above;
+            else if (k[j] >= tlo) atomicAdd(&s_h[bin_of(k[j], tlo, scale)], 1u);
         }
     }
-    __syncthreads();
-    for (int i = tid; i < HIST_BINS; i += SEL_THREADS) {
-        if (s_hv[i]) atomicAdd(&gv[i], s_hv[i]);
-        if (s_hw[i]) atomicAdd(&gw[i], s_hw[i]);
-    }
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) s_last = (atomicAdd(&sq[SQ_DONE], 1u) == gridDim.x - 1);
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    constexpr int PER = HIST_BINS / SEL_THREADS;
-    uint32_t lv = 0, lw = 0;
+    above = block_sum_u32(above, s_w);
+    if (tid == 0 && above) atomicAdd(&sq[SQ_ABOVE], above);
+    for (int i = tid; i < HIST_BINS; i += SEL_THREADS)
+        if (s_h[i]) atomicAdd(&gh[i], s_h[i]);
+}
+
+// One block per sequence, after the counting pass: the bin of the k-th
+// largest key~ and the band around it,
+//   THI = up(edge_hi + E) >= k-th largest v,  TLO = down(edge_lo - E) <= k-th largest w.
+// If the sample missed (the k-th key~ lies outside [t_lo, t_hi]) the block
+// histograms the sequence's whole key range itself.
+__global__ __launch_bounds__(SEL_THREADS) void bracket_kernel(SelectArgs a) {
+    __shared__ uint32_t s_h[HIST_BINS];
+    __shared__ uint32_t s_w[SEL_THREADS / 64];
+    __shared__ int s_bin;
+    const int b = blockIdx.x;
+    const int tid = threadIdx.x;
+    uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
+    uint32_t* gh = a.hist + (int64_t)b * 2 * HIST_BINS;
+    const float tlo = __uint_as_float(sq[SQ_BLO]);
+    const float thi = __uint_as_float(sq[SQ_BHI]);
+    const uint32_t tot_above = sq[SQ_ABOVE];
+    uint32_t inr = 0;
+    {
+        constexpr int PER = HIST_BINS / SEL_THREADS;
+        uint32_t hv[PER];
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        const int d = tid * PER + j;
-        const uint32_t hv = __hip_atomic_load(&gv[d], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const uint32_t hw = __hip_atomic_load(&gw[d], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_hv[d] = hv;
-        s_hw[d] = hw;
-        lv += hv;
-        lw += hw;
-    }
-    const uint32_t sv = block_suffix_incl(lv, s_w);
-    const uint32_t sw = block_suffix_incl(lw, s_w);
-    const uint32_t k = (uint32_t)a.k;
-    const double w_bin = (scale > 0.f) ? 1.0 / (double)scale : 0.0;
-    const double slack = fabs((double)lo) * 0x1p-22 + 0x1p-100;
-    if (sv - lv < k && k <= sv) {
-        uint32_t run = sv - lv;
-        for (int d = (tid + 1) * PER - 1; d >= tid * PER; --d) {
-            if (run + s_hv[d] >= k) {
-                double edge = (double)hi;
-                if (scale > 0.f) edge = fmin(edge, (double)lo + (double)(d + 1) * w_bin * (1.0 + 0x1p-20) + slack);
-                sq[SQ_THI] = __float_as_uint(ru_f32(edge));
-                break;
-            }
-            run += s_hv[d];
+        for (int j = 0; j < PER; ++j) hv[j] = gh[tid + SEL_THREADS * j];
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            s_h[tid + SEL_THREADS * j] = hv[j];
+            inr += hv[j];
+            gh[tid + SEL_THREADS * j] = 0u;
         }
     }
-    if (sw - lw < k && k <= sw) {
-        uint32_t run = sw - lw;
-        for (int d = (tid + 1) * PER - 1; d >= tid * PER; --d) {
-            if (run + s_hw[d] >= k) {
-                double edge = (double)lo;
-                if (scale > 0.f) edge = fmax(edge, (double)lo + (double)d * w_bin * (1.0 - 0x1p-20) - slack);
-                sq[SQ_TLO] = __float_as_uint(rd_f32(edge));
-                break;
+    inr = block_sum_u32(inr, s_w);
+    const float E = key_band_f32(sq, a.n);
+    const int64_t need = a.k - (int64_t)tot_above;
+    const bool ok = need >= 1 && need <= (int64_t)inr;
+    float lo = tlo, hi = thi, sc = bin_scale(tlo, thi);
+    if (!ok) {
+        // the sample missed: histogram the whole key range in this block
+        lo = ord_to_key(sq[SQ_KMIN]);
+        hi = ord_to_key(sq[SQ_KMAX]);
+        sc = bin_scale(lo, hi);
+        __syncthreads();
+        for (int i = tid; i < HIST_BINS; i += SEL_THREADS) s_h[i] = 0u;
+        __syncthreads();
+        const float* kb = a.kt + (int64_t)b * a.A;
+        for (int64_t ub = 0; ub < a.A; ub += KEY_BATCH * SEL_THREADS) {
+            float k[KEY_BATCH];
+#pragma unroll
+            for (int j = 0; j < KEY_BATCH; ++j) {
+                const int64_t u = ub + tid + (int64_t)j * SEL_THREADS;
+                k[j] = (u < a.A) ? kb[u] : 0.f;
             }
-            run += s_hw[d];
+#pragma unroll
+            for (int j = 0; j < KEY_BATCH; ++j) {
+                const int64_t u = ub + tid + (int64_t)j * SEL_THREADS;
+                if (u < a.A) atomicAdd(&s_h[bin_of(k[j], lo, sc)], 1u);
+            }
         }
     }
+    const uint32_t target = (uint32_t)(ok ? need : a.k);
+    if (tid == 0) s_bin = -1;
     __syncthreads();
-    for (int i = tid; i < 2 * HIST_BINS; i += SEL_THREADS) gv[i] = 0u;
-    if (tid == 0) sq[SQ_DONE] = 0u;
+    const int d = find_rank_bin(s_h, target, s_w);
+    if (d >= 0) s_bin = d;
+    __syncthreads();
+    if (tid == 0) {
+        const int db = s_bin < 0 ? 0 : s_bin;
+        sq[SQ_THI] = __float_as_uint(band_hi(ru_f32(edge_hi_of(db, lo, hi, sc)), E));
+        sq[SQ_TLO] = __float_as_uint(band_lo(rd_f32(edge_lo_of(db, lo, sc)), E));
+        a.theta[b] = -INFINITY;
+    }
 }
 
 // ----------------------------------------------------------- classify
@@ -281,7 +419,6 @@ __global__ __launch_bounds__(SEL_THREADS) void classify_kernel(SelectArgs a) {
         cc[CC_SELAMB] = 0u;
         cc[CC_ADM] = 0u;
         cc[CC_ADMAMB] = 0u;
-        atomicAdd(&sq[SQ_NIN], nin);
     }
 }
 
@@ -350,135 +487,170 @@ static hipError_t run_compact(const SelectArgs& s, const uint8_t* flags, uint8_t
 
 // --------------------------------------------------------- fp64 re-scoring
 
-// Exact index scores of the ambiguous rows, RF_ROWS rows per block iteration:
-// thread (slot, hq) runs the fp64 dot products (d ascending, from +0; bf16
-// products are exact in fp64) of heads hq, hq+32, hq+64, hq+96 for row slot
-// `slot`, with qt held transposed in LDS (head-contiguous, conflict-free) when
-// it fits.  The rows of the next iteration are loaded while the current ones
-// are scored (double-buffered LDS).
-constexpr int RF_ROWS = 8;
-constexpr int RF_QT_MAX = 32768;   // elements of qt staged in LDS (64 KB)
-constexpr int RF_PIECES = (RF_ROWS * D_ROW / 8 + SEL_THREADS - 1) / SEL_THREADS;   // 16-byte row pieces per thread (max)
+// Exact keys of the ambiguous rows, a tile of 16 rows per wave.  The rows are
+// gathered straight into the MFMA operand layout (lane 16 g + c: row c, dims
+// 32 ks + 8 g ..) and scored against every head with fp32 accumulation -- the
+// scorer's arithmetic, so |s~ - s| <= E for every (row, head).  Only heads
+// within 2E of their row's maximum can hold the exact maximum; each such
+// (row, head) pair gets its fp64 chain (d ascending from +0: the exact
+// definition) from one lane, and the row's exact key is the maximum over its
+// pairs (LDS atomic max on the order-preserving encoding).  With UB the
+// screened quantity is s^_h + B_h(u) (Lemma (Index certificate)) and the
+// margin is that bound's own fp32 error.
+constexpr int EX_QT_MAX = 32768;   // qt elements staged in LDS (64 KB)
+
+template <bool UB>
+__device__ __forceinline__ double exact_chain(const uint16_t* q, const uint16_t* x, int n, float4 hs, double et,
+                                              double ep, double ga) {
+    double acc = 0.0;
+    const int n8 = n / 8;
+    for (int p0 = 0; p0 < n8; p0 += 8) {
+        u16x8_t qv[8], xv[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const bool in = p0 + j < n8;
+            qv[j] = in ? *reinterpret_cast<const u16x8_t*>(q + 8 * (p0 + j)) : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+            xv[j] = in ? *reinterpret_cast<const u16x8_t*>(x + 8 * (p0 + j)) : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            if (p0 + j >= n8) break;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc = fma((double)bf16_to_f32(qv[j][e]), (double)bf16_to_f32(xv[j][e]), acc);
+        }
+    }
+    if (UB) acc = acc + fma((double)hs.x, et, fma((double)hs.y, ep, (double)hs.z * ga));
+    return acc;
+}
 
 template <bool UB, bool QLDS>
-__global__ __launch_bounds__(SEL_THREADS) void refine_kernel(SelectArgs a) {
-    constexpr int XW = QLDS ? RF_QT_MAX / 128 : D_ROW;                // row width held (n <= XW)
-    __shared__ __align__(16) uint16_t s_qt[QLDS ? RF_QT_MAX : 8];     // [n][128]
-    __shared__ __align__(16) uint16_t s_x[2][RF_ROWS][XW];
+__global__ __launch_bounds__(SEL_THREADS) void exact_keys_kernel(SelectArgs a) {
+    __shared__ __align__(16) uint16_t s_qt[QLDS ? EX_QT_MAX : 8];   // [H][n]
+    __shared__ float4 s_hs[128];
+    __shared__ unsigned long long s_best[4][16];
+    __shared__ uint32_t s_list[4][64];
     const int b = blockIdx.y;
-    const int tid = threadIdx.x;
-    const int slot = tid >> 5, hq = tid & 31;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4, c = lane & 15;
     const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    const uint32_t namb = sq[UB ? SQ_NAMB2 : SQ_NAMB];
-    if ((uint32_t)(blockIdx.x * RF_ROWS) >= namb) return;
+    const int64_t namb = sq[UB ? SQ_NAMB2 : SQ_NAMB];
+    if ((int64_t)blockIdx.x * 64 >= namb) return;
     const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
     const int n8 = a.n / 8;
     if (QLDS) {
-        // 16-byte pieces of qt, all loads in flight, then transposed writes
-        constexpr int QP = RF_QT_MAX / 8 / SEL_THREADS;
+        constexpr int QP = EX_QT_MAX / 8 / SEL_THREADS;
         u16x8_t v[QP];
 #pragma unroll
         for (int j = 0; j < QP; ++j) {
             const int p = tid + SEL_THREADS * j;
-            const int h = p & 127, d8 = p >> 7;
-            v[j] = (d8 < n8 && h < a.H) ? *reinterpret_cast<const u16x8_t*>(qtb + (int64_t)h * a.n + 8 * d8)
-                                        : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+            v[j] = (p < a.H * n8) ? *reinterpret_cast<const u16x8_t*>(qtb + 8 * (int64_t)p)
+                                  : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
         }
 #pragma unroll
         for (int j = 0; j < QP; ++j) {
             const int p = tid + SEL_THREADS * j;
-            const int h = p & 127, d8 = p >> 7;
-            if (d8 < n8)
-#pragma unroll
-                for (int e = 0; e < 8; ++e) s_qt[(8 * d8 + e) * 128 + h] = v[j][e];
+            if (p < a.H * n8) *reinterpret_cast<u16x8_t*>(&s_qt[8 * p]) = v[j];
         }
     }
+    if (UB && tid < a.H) s_hs[tid] = reinterpret_cast<const float4*>(a.hsc)[(int64_t)b * a.H + tid];
+    __syncthreads();
+    const uint16_t* qsrc = QLDS ? s_qt : qtb;
     const uint16_t* xb = a.x + (int64_t)b * a.xbs;
     const int32_t* amb = a.amb + (int64_t)b * a.A;
-    const double th = UB ? a.theta[b] : 0.0;
-    const float4* hs = reinterpret_cast<const float4*>(a.hsc) + (int64_t)b * a.H;
-    const uint32_t step = gridDim.x * RF_ROWS;
-    // row pieces of iteration i0 into registers
-    u16x8_t pf[RF_PIECES];
-    auto fetch = [&](uint32_t i0) {
+    uint64_t* ak = a.ambkey + (int64_t)b * a.A;
+    const float E = ru_f32(UB ? ub_error_of(sq, a.n) * (1.0 + 0x1p-20) : key_error_of(sq, a.n));
+    const float margin = next_up_f32(2.0f * E);
+    const int KS = a.n / 32, HT = (a.H + 15) / 16;
+    for (int64_t t0 = ((int64_t)blockIdx.x * 4 + wave) * 16; t0 < namb; t0 += (int64_t)gridDim.x * 64) {
+        const int64_t i = min(t0 + c, namb - 1);
+        const int64_t u = amb[i];
+        const uint16_t* x = xb + u * a.xs;
+        f32x4_t acc[8];
 #pragma unroll
-        for (int j = 0; j < RF_PIECES; ++j) {
-            const int idx = tid + SEL_THREADS * j;
-            const int rl = idx / n8, p = idx % n8;
-            pf[j] = u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
-            if (rl < RF_ROWS && i0 + rl < namb)
-                pf[j] = *reinterpret_cast<const u16x8_t*>(xb + (int64_t)amb[i0 + rl] * a.xs + 8 * p);
-        }
-    };
-    auto park = [&](int buf) {
+        for (int ht = 0; ht < 8; ++ht) acc[ht] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int ks = 0; ks < KS; ++ks) {
+            const bf16x8_t xf = *reinterpret_cast<const bf16x8_t*>(x + 32 * ks + 8 * g);
 #pragma unroll
-        for (int j = 0; j < RF_PIECES; ++j) {
-            const int idx = tid + SEL_THREADS * j;
-            const int rl = idx / n8, p = idx % n8;
-            if (rl < RF_ROWS) *reinterpret_cast<u16x8_t*>(&s_x[buf][rl][8 * p]) = pf[j];
-        }
-    };
-    uint32_t i0 = blockIdx.x * RF_ROWS;
-    fetch(i0);
-    park(0);
-    __syncthreads();
-    for (int buf = 0; i0 < namb; i0 += step, buf ^= 1) {
-        const bool more = i0 + step < namb;
-        if (more) fetch(i0 + step);
-        const uint32_t i = i0 + slot;
-        double acc[4] = {0.0, 0.0, 0.0, 0.0};
-#pragma unroll 8
-        for (int d = 0; d < a.n; ++d) {
-            const double xv = (double)bf16_to_f32(s_x[buf][slot][d]);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int h = hq + 32 * j;
-                const uint16_t qb = QLDS ? s_qt[d * 128 + h] : ((h < a.H) ? qtb[(int64_t)h * a.n + d] : (uint16_t)0);
-                acc[j] = fma((double)bf16_to_f32(qb), xv, acc[j]);
-            }
-        }
-        double best = -INFINITY;
-        const int64_t u = (i < namb) ? (int64_t)amb[i] : 0;
-        double et = 0.0, ep = 0.0, ga = 0.0;
-        if (UB && i < namb) {
-            const int64_t o = (int64_t)b * a.T + u;
-            et = (double)a.eta[o];
-            ep = (double)a.eps[o];
-            ga = (double)a.gam[o];
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int h = hq + 32 * j;
-            if (h < a.H) {
-                double v = acc[j];
-                if (UB) {
-                    const float4 q = hs[h];
-                    v = v + fma((double)q.x, et, fma((double)q.y, ep, (double)q.z * ga));
+            for (int ht = 0; ht < 8; ++ht) {
+                if (ht < HT) {
+                    const int h = (16 * ht + c) % a.H;
+                    const bf16x8_t qf = *reinterpret_cast<const bf16x8_t*>(qsrc + (int64_t)h * a.n + 32 * ks + 8 * g);
+                    acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf, xf, acc[ht], 0, 0, 0);
                 }
-                best = fmax(best, v);
             }
         }
-        for (int o = 16; o > 0; o >>= 1) best = fmax(best, __shfl_xor(best, o));
-        if (hq == 0 && i < namb) {
-            if (!UB) {
-                a.ambkey[(int64_t)b * a.A + i] = best;
-            } else if (best > th) {
-                a.flags2[(int64_t)b * a.A + u] = 3;
-                atomicAdd(&a.ccount[((int64_t)b * a.nch + u / CHUNK) * CC_WORDS + CC_ADMAMB], 1u);
-            }
+        // acc[ht][q] = screened value of head 16 ht + 4 g + q for row c
+        float et = 0.f, ep = 0.f, ga = 0.f;
+        if (UB) {
+            const int64_t o = (int64_t)b * a.T + u;
+            et = a.eta[o];
+            ep = a.eps[o];
+            ga = a.gam[o];
         }
-        if (more) park(buf ^ 1);
-        __syncthreads();
+        float m = -INFINITY;
+#pragma unroll
+        for (int ht = 0; ht < 8; ++ht)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int h = 16 * ht + 4 * g + q;
+                float v = -INFINITY;
+                if (ht < HT && h < a.H) {
+                    v = acc[ht][q];
+                    if (UB) {
+                        const float4 hs = s_hs[h];
+                        v += fmaf(hs.x, et, fmaf(hs.y, ep, hs.z * ga));
+                    }
+                }
+                acc[ht][q] = v;
+                m = fmaxf(m, v);
+            }
+        m = fmaxf(m, __shfl_xor(m, 16));
+        m = fmaxf(m, __shfl_xor(m, 32));
+        const float thr = next_down_f32(m - margin);
+        if (lane < 16) s_best[wave][lane] = (unsigned long long)f64_to_ord(-INFINITY);
+        // candidates in rounds of up to 64 pairs, one fp64 chain per lane
+        int nl = 0;
+        auto flush = [&]() {
+            if (lane < nl) {
+                const uint32_t e = s_list[wave][lane];
+                const int cr = (int)(e >> 8), h = (int)(e & 255);
+                const int64_t ir = t0 + cr;
+                const int64_t ur = amb[ir];
+                const int64_t o = (int64_t)b * a.T + ur;
+                const float4 hs = UB ? s_hs[h] : make_float4(0.f, 0.f, 0.f, 0.f);
+                const double v = exact_chain<UB>(qtb + (int64_t)h * a.n, xb + ur * a.xs, a.n, hs,
+                                                 UB ? (double)a.eta[o] : 0.0, UB ? (double)a.eps[o] : 0.0,
+                                                 UB ? (double)a.gam[o] : 0.0);
+                atomicMax(&s_best[wave][cr], (unsigned long long)f64_to_ord(v));
+            }
+            nl = 0;
+        };
+#pragma unroll
+        for (int ht = 0; ht < 8; ++ht)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const bool cand = (t0 + c < namb) && acc[ht][q] >= thr && acc[ht][q] > -INFINITY;
+                const uint64_t bal = __ballot(cand);
+                const int cnt = __popcll(bal);
+                if (cnt == 0) continue;
+                if (nl + cnt > 64) flush();
+                if (cand) {
+                    const int pos = nl + __popcll(bal & ((1ull << lane) - 1ull));
+                    s_list[wave][pos] = ((uint32_t)c << 8) | (uint32_t)(16 * ht + 4 * g + q);
+                }
+                nl += cnt;
+            }
+        flush();
+        if (lane < 16 && t0 + lane < namb) ak[t0 + lane] = s_best[wave][lane];
     }
 }
 
 template <bool UB>
-static hipError_t run_refine(const SelectArgs& a, hipStream_t s) {
-    dim3 g(REFINE_BLOCKS, a.B);
-    if ((int64_t)a.n * 128 <= RF_QT_MAX)
-        hipLaunchKernelGGL((refine_kernel<UB, true>), g, dim3(SEL_THREADS), 0, s, a);
+static hipError_t run_exact_keys(const SelectArgs& a, hipStream_t s) {
+    dim3 g(EX_BLOCKS, a.B);
+    if ((int64_t)a.H * a.n <= EX_QT_MAX)
+        hipLaunchKernelGGL((exact_keys_kernel<UB, true>), g, dim3(SEL_THREADS), 0, s, a);
     else
-        hipLaunchKernelGGL((refine_kernel<UB, false>), g, dim3(SEL_THREADS), 0, s, a);
+        hipLaunchKernelGGL((exact_keys_kernel<UB, false>), g, dim3(SEL_THREADS), 0, s, a);
     return hipGetLastError();
 }
 
@@ -498,15 +670,21 @@ __global__ __launch_bounds__(SEL_THREADS) void rank_select_kernel(SelectArgs a) 
     const int b = blockIdx.y;
     const int tid = threadIdx.x;
     const int r = tid % RK_ROWS, q = tid / RK_ROWS;
+    __shared__ uint32_t s_red[SEL_THREADS / 64];
     const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
     const int64_t namb = sq[SQ_NAMB];
-    const int64_t need = a.k - (int64_t)sq[SQ_NIN];
-    const double* kb = a.ambkey + (int64_t)b * a.A;
+    if ((int64_t)blockIdx.x * RK_ROWS >= namb) return;
+    // rows certainly in S: the sum of the chunk counts of the classification
+    uint32_t nin = 0;
+    for (int64_t c = tid; c < a.nch; c += SEL_THREADS) nin += a.ccount[((int64_t)b * a.nch + c) * CC_WORDS + CC_IN];
+    nin = block_sum_u32(nin, s_red);
+    const int64_t need = a.k - (int64_t)nin;
+    const uint64_t* kb = a.ambkey + (int64_t)b * a.A;
     const int32_t* ub = a.amb + (int64_t)b * a.A;
     for (int64_t base = (int64_t)blockIdx.x * RK_ROWS; base < namb; base += (int64_t)gridDim.x * RK_ROWS) {
         const int64_t i = base + r;
         const bool have = i < namb;
-        const double ki = have ? kb[i] : 0.0;
+        const double ki = have ? ord_to_f64(kb[i]) : 0.0;
         const int32_t ui = have ? ub[i] : 0;
         uint32_t rank = 0;
         for (int64_t t0 = 0; t0 < namb; t0 += RK_TILE) {
@@ -518,7 +696,7 @@ __global__ __launch_bounds__(SEL_THREADS) void rank_select_kernel(SelectArgs a) 
 #pragma unroll
             for (int j = 0; j < PER; ++j) {
                 const int e = tid + SEL_THREADS * j;
-                kv[j] = (e < lim) ? kb[t0 + e] : 0.0;
+                kv[j] = (e < lim) ? ord_to_f64(kb[t0 + e]) : 0.0;
                 uv[j] = (e < lim) ? ub[t0 + e] : 0;
             }
 #pragma unroll
@@ -552,19 +730,21 @@ __global__ __launch_bounds__(SEL_THREADS) void rank_select_kernel(SelectArgs a) 
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
     hipError_t e;
-    if (a.A == 0 || a.k == 0) {
+    if (a.k == 0) {
         hipLaunchKernelGGL(select_empty_kernel, dim3(a.B), dim3(64), 0, s, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (a.A == 0) return hipSuccess;
         hipLaunchKernelGGL(fill_u8_kernel, dim3(256), dim3(SEL_THREADS), 0, s, a.flags, (int64_t)a.B * a.A, (uint8_t)0);
         return hipGetLastError();
     }
-    dim3 hg((unsigned)((a.A + HIST_KEYS_PER_BLOCK - 1) / HIST_KEYS_PER_BLOCK), a.B);
-    hipLaunchKernelGGL(hist_kernel, hg, dim3(SEL_THREADS), 0, s, a);
+    dim3 cg((unsigned)((a.A + COUNT_KEYS_PER_BLOCK - 1) / COUNT_KEYS_PER_BLOCK), a.B);
+    hipLaunchKernelGGL(count_kernel, cg, dim3(SEL_THREADS), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(bracket_kernel, dim3(a.B), dim3(SEL_THREADS), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(classify_kernel, dim3((unsigned)a.nch, a.B), dim3(SEL_THREADS), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = run_refine<false>(a, s)) != hipSuccess) return e;
+    if ((e = run_exact_keys<false>(a, s)) != hipSuccess) return e;
     hipLaunchKernelGGL(rank_select_kernel, dim3(RANK_BLOCKS, a.B), dim3(SEL_THREADS), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return run_compact(a, a.flags, 1, CC_IN, CC_SELAMB, a.sel, a.k, a.k, nullptr, s);
@@ -574,6 +754,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
 
 __global__ __launch_bounds__(SEL_THREADS) void admit_classify_kernel(SelectArgs a) {
     __shared__ uint32_t s_red[SEL_THREADS / 64];
+    constexpr int PER = CHUNK / SEL_THREADS;
     const int b = blockIdx.y;
     const int c = blockIdx.x;
     const int tid = threadIdx.x;
@@ -584,20 +765,29 @@ __global__ __launch_bounds__(SEL_THREADS) void admit_classify_kernel(SelectArgs 
     const uint8_t* fb = a.flags + (int64_t)b * a.A;
     uint8_t* f2 = a.flags2 + (int64_t)b * a.A;
     int32_t* amb = a.amb + (int64_t)b * a.A;
-    uint32_t nadm = 0;
     const int64_t u0 = (int64_t)c * CHUNK;
     const int64_t u1 = min(a.A, u0 + CHUNK);
-    for (int64_t base = u0; base < u1; base += SEL_THREADS) {
-        const int64_t u = base + tid;
+    float t[PER];
+    uint8_t fin[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int64_t u = u0 + tid + (int64_t)j * SEL_THREADS;
+        t[j] = (u < u1) ? ubb[u] : 0.f;
+        fin[j] = (u < u1) ? fb[u] : (uint8_t)1;
+    }
+    uint32_t nadm = 0;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int64_t u = u0 + tid + (int64_t)j * SEL_THREADS;
         uint8_t f = 0;
         if (u < u1) {
-            if (fb[u] != 1) {
+            if (fin[j] != 1) {
                 if (th == -INFINITY) {
                     f = 3;
                 } else {
-                    const double t = (double)ubb[u];
-                    const double band = E + fabs(t) * 0x1p-50 + fabs(th) * 0x1p-50;
-                    f = (t - band > th) ? 3 : ((t + band <= th) ? 0 : 4);
+                    const double tv = (double)t[j];
+                    const double band = E + fabs(tv) * 0x1p-50 + fabs(th) * 0x1p-50;
+                    f = (tv - band > th) ? 3 : ((tv + band <= th) ? 0 : 4);
                 }
             }
             f2[u] = f;
@@ -607,6 +797,23 @@ __global__ __launch_bounds__(SEL_THREADS) void admit_classify_kernel(SelectArgs 
     }
     nadm = block_sum_u32(nadm, s_red);
     if (tid == 0) a.ccount[((int64_t)b * a.nch + c) * CC_WORDS + CC_ADM] = nadm;
+}
+
+// Ambiguous rows of the admission, decided on their exact bound.
+__global__ __launch_bounds__(SEL_THREADS) void admit_decide_kernel(SelectArgs a) {
+    const int b = blockIdx.y;
+    const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
+    const int64_t namb = sq[SQ_NAMB2];
+    const double th = a.theta[b];
+    const uint64_t* ak = a.ambkey + (int64_t)b * a.A;
+    const int32_t* amb = a.amb + (int64_t)b * a.A;
+    for (int64_t i = (int64_t)blockIdx.x * SEL_THREADS + threadIdx.x; i < namb; i += (int64_t)gridDim.x * SEL_THREADS) {
+        if (ord_to_f64(ak[i]) > th) {
+            const int32_t u = amb[i];
+            a.flags2[(int64_t)b * a.A + u] = 3;
+            atomicAdd(&a.ccount[((int64_t)b * a.nch + u / CHUNK) * CC_WORDS + CC_ADMAMB], 1u);
+        }
+    }
 }
 
 __global__ __launch_bounds__(64) void zero_counts_kernel(int32_t* p, int n) {
@@ -621,7 +828,9 @@ hipError_t launch_admit(const SelectArgs& a, hipStream_t s) {
     }
     hipLaunchKernelGGL(admit_classify_kernel, dim3((unsigned)a.nch, a.B), dim3(SEL_THREADS), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = run_refine<true>(a, s)) != hipSuccess) return e;
+    if ((e = run_exact_keys<true>(a, s)) != hipSuccess) return e;
+    hipLaunchKernelGGL(admit_decide_kernel, dim3(EX_BLOCKS, a.B), dim3(SEL_THREADS), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     return run_compact(a, a.flags2, 3, CC_ADM, CC_ADMAMB, a.adm, a.cap, a.cap, a.adm_count, s);
 }
 

@@ -162,7 +162,7 @@ static SelectArgs select_args(const vkv_step* st, const WsLayout& L, char* w) {
     a.flags2 = reinterpret_cast<uint8_t*>(w + L.flags2);
     a.ccount = reinterpret_cast<uint32_t*>(w + L.ccount);
     a.amb = reinterpret_cast<int32_t*>(w + L.amb);
-    a.ambkey = reinterpret_cast<double*>(w + L.ambkey);
+    a.ambkey = reinterpret_cast<uint64_t*>(w + L.ambkey);
     a.A = L.A;
     a.nch = L.nch;
     a.B = (int)st->B;

@@ -31,6 +31,7 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 __host__ __device__ __forceinline__ uint32_t f2u(float f) { return __builtin_bit_cast(uint32_t, f); }
 __host__ __device__ __forceinline__ float u2f(uint32_t u) { return __builtin_bit_cast(float, u); }
 __host__ __device__ __forceinline__ uint64_t d2u(double d) { return __builtin_bit_cast(uint64_t, d); }
+__host__ __device__ __forceinline__ double u2d(uint64_t u) { return __builtin_bit_cast(double, u); }
 
 // ------------------------------------------------------------ bf16 helpers
 
@@ -126,11 +127,13 @@ enum SeqWord : int {
     SQ_KMAX = 7,    // ordered encoding of max_u key~_u   (scorer, atomicMax)
     SQ_TLO = 8,     // float bits: LO <= k-th largest of (key~ - E)
     SQ_THI = 9,     // float bits: HI >= k-th largest of (key~ + E)
-    SQ_DONE = 10,   // last-block counter of the histogram pass
-    SQ_NIN = 11,    // rows certainly in S
+    SQ_DONE = 10,   // (unused)
     SQ_NAMB = 12,   // ambiguous rows of the selection
     SQ_NAMB2 = 13,  // ambiguous rows of the admission
-    SQ_WORDS = 16
+    SQ_BLO = 14,    // float bits: lower end of the sampled bracket of the k-th key~
+    SQ_BHI = 15,    // float bits: upper end of the sampled bracket
+    SQ_ABOVE = 16,  // keys~ above the sampled bracket
+    SQ_WORDS = 32
 };
 
 constexpr int CHUNK = 2048;        // rows per classify / compaction block
@@ -206,8 +209,8 @@ struct SelectArgs {
     uint8_t* flags;        // [B,A]
     uint8_t* flags2;       // [B,A]
     uint32_t* ccount;      // [B,nch,CC_WORDS]
-    int32_t* amb;          // [B,A]
-    double* ambkey;        // [B,A]
+    int32_t* amb;          // [B,A] ambiguous rows
+    uint64_t* ambkey;      // [B,A] their exact keys (order-preserving encoding of fp64)
     int32_t* sel;          // [B,k]
     double* theta;         // [B]
     int32_t* adm;          // [B,cap]

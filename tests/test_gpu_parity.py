@@ -272,6 +272,36 @@ def test_duplicated_rows_and_near_ties(ctx):
     check_step(wl, g, o, [0, 1])
 
 
+def test_bracket_missed_by_the_sample(ctx):
+    """The largest keys sit only at rows the strided key sample never reads
+    (A = 16384: the sample takes every 4th row); the counting pass finds the
+    sampled bracket wrong and redoes the histogram over the whole key range."""
+    say("sample miss")
+    cfg = synth.CONFIGS["cfg1"].with_(H=16, needles=0)
+    wl = synth.make_workload(cfg, "cuda", B=1, T=16384 + 256)
+    rows = torch.arange(1, 4096, 4, device="cuda")
+    wl["cache"][0, rows, 512:] = (wl["cache"][0, rows, 512:].float() * 8).to(torch.bfloat16)
+    g, _ = gpu_step(ctx, wl, k=256)
+    o, _ = oracle_step(wl, [0], k=256)
+    check_step(wl, g, o, [0])
+    assert set(g["sel"][0].tolist()) <= set(rows.tolist())
+
+
+@pytest.mark.parametrize("H", [16, 128])
+def test_identical_heads_make_every_head_a_candidate(ctx, H):
+    """All heads carry the same query: every head ties for the maximum of every
+    ambiguous row, so all of them go through the fp64 pass (H = 16: as queued
+    (row, head) pairs; H = 128: in the re-screening wave itself)."""
+    say(f"identical heads H={H}")
+    cfg = synth.CONFIGS["cfg4"].with_(H=H)
+    wl = synth.make_workload(cfg, "cuda", B=1, T=6000)
+    wl["q_lat"][0] = wl["q_lat"][0, :1].expand(H, -1)
+    wl["q_rope"][0] = wl["q_rope"][0, :1].expand(H, -1)
+    g, _ = gpu_step(ctx, wl, k=500)
+    o, _ = oracle_step(wl, [0], k=500)
+    check_step(wl, g, o, [0])
+
+
 def test_cancellation_heavy_scores_stay_within_bound(ctx):
     """Index rows built so that each score is a sum of large terms that cancel:
     the fp32 MFMA key must stay within the certified bound, and selection
