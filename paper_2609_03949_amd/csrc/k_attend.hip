@@ -166,14 +166,23 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
             const int x = (c >> 1) & 7;
             const uint8_t* ke = kt + c * (D_ROW * 2) + 16 * (g ^ (x & 3)) + 64 * (x >> 2);
             const uint8_t* ko = kt + c * (D_ROW * 2) + 16 * (g ^ (x & 3)) - 64 * (x >> 2);
+            // operands one k-step ahead of the matrix cores
+            bf16x8_t kb[2][2];
 #pragma unroll
-            for (int ks = 0; ks < D_ROW / 32; ++ks)
+            for (int mt = 0; mt < 2; ++mt)
+                kb[0][mt] = *reinterpret_cast<const bf16x8_t*>(ke + 16 * mt * (D_ROW * 2));
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt) {
-                    const uint8_t* src = ((ks & 1) ? ko : ke) + 16 * mt * (D_ROW * 2) + 64 * ks;
-                    const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(src);
-                    sacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[ks], sacc[mt], 0, 0, 0);
+            for (int ks = 0; ks < D_ROW / 32; ++ks) {
+                if (ks + 1 < D_ROW / 32) {
+#pragma unroll
+                    for (int mt = 0; mt < 2; ++mt)
+                        kb[(ks + 1) & 1][mt] = *reinterpret_cast<const bf16x8_t*>(
+                            (((ks + 1) & 1) ? ko : ke) + 16 * mt * (D_ROW * 2) + 64 * (ks + 1));
                 }
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt)
+                    sacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[ks & 1][mt], qf[ks], sacc[mt], 0, 0, 0);
+            }
         }
         // sacc[mt][i] = score of row 16*mt + 4*g + i for head hq
         float sc[2][4];
@@ -209,12 +218,20 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) al[i] = __shfl(alpha, 4 * g + i);
         __syncthreads();   // transposed tile complete
+        // rescale the accumulators only when some head's running max moved
+        if (__ballot(alpha != 1.0f)) {
+#pragma unroll
+            for (int tt = 0; tt < D_LAT / 16; ++tt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) o[tt][i] *= al[i];
+        }
+        const uint16_t* vrow = &vt[c * VT_STRIDE + 8 * g];
+        bf16x8_t vb[2];
+        vb[0] = *reinterpret_cast<const bf16x8_t*>(vrow);
 #pragma unroll
         for (int tt = 0; tt < D_LAT / 16; ++tt) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) o[tt][i] *= al[i];
-            const bf16x8_t vb = *reinterpret_cast<const bf16x8_t*>(&vt[(16 * tt + c) * VT_STRIDE + 8 * g]);
-            o[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, o[tt], 0, 0, 0);
+            if (tt + 1 < D_LAT / 16) vb[(tt + 1) & 1] = *reinterpret_cast<const bf16x8_t*>(vrow + 16 * (tt + 1) * VT_STRIDE);
+            o[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb[tt & 1], o[tt], 0, 0, 0);
         }
     }
     // o[tt][i] = unnormalised output of head h0 + 4*g + i, dim 16*tt + c

@@ -17,18 +17,19 @@ namespace vkv {
 // ----------------------------------------------------------- query prep
 
 // Stage 1: w[b,h,j] = sum_i P[j,i] q_lat[b,h,i] (fp64, i ascending) and the
-// query digest qt[b,h,off+j] = RNE_bf16(w).  A block owns 64 basis rows and
-// 16 heads; each thread runs four independent fp64 chains (four heads of one
+// query digest qt[b,h,off+j] = RNE_bf16(w).  A block owns 32 basis rows and
+// 16 heads; each thread runs two independent fp64 chains (two heads of one
 // basis row).  The i axis is walked in chunks of 128 held in LDS as fp64 (P^T
 // and the queries, converted once), and the next chunk is fetched into
 // registers while the current one is consumed.  Block (0,0,b) also clears the
 // step state of sequence b.
 constexpr int QP_HEADS = 16;
+constexpr int QP_ROWS = 32;
 constexpr int QP_IC = 128;
 
 __global__ __launch_bounds__(256) void qprep_project_kernel(QprepArgs a) {
-    __shared__ __align__(16) double s_p[QP_IC][64];         // P^T chunk: [i][j]
-    __shared__ __align__(16) double s_q[QP_IC][QP_HEADS];   // query chunk: [i][head]
+    __shared__ __align__(16) double s_p[QP_IC][QP_ROWS];     // P^T chunk: [i][j]
+    __shared__ __align__(16) double s_q[QP_IC][QP_HEADS];    // query chunk: [i][head]
     const int b = blockIdx.z;
     const int tid = threadIdx.x;
     if (blockIdx.x == 0 && blockIdx.y == 0) {
@@ -36,17 +37,17 @@ __global__ __launch_bounds__(256) void qprep_project_kernel(QprepArgs a) {
         for (int i = tid; i < 2 * HIST_BINS; i += 256) a.hist[(int64_t)b * 2 * HIST_BINS + i] = 0u;
     }
     if (a.r == 0 || !(a.mode & 2)) return;
-    const int j0 = 64 * blockIdx.x;
-    const int jn = min(64, a.r - j0);
+    const int j0 = QP_ROWS * blockIdx.x;
+    const int jn = min(QP_ROWS, a.r - j0);
     const int h0 = QP_HEADS * blockIdx.y;
-    // chunk c: P rows j0.. (lane row = p & 63, piece p >> 6) and query rows
+    // chunk c: P rows j0.. (lane row = p & 31, piece p >> 5) and query rows
     // h0.. (head = p & 15, piece p >> 4), 16-byte pieces of 8 i each
-    u16x8_t pv[4], qv;
+    u16x8_t pv[2], qv;
     auto fetch = [&](int c) {
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
+        for (int jj = 0; jj < 2; ++jj) {
             const int p = tid + 256 * jj;
-            const int row = p & 63, pc = p >> 6;
+            const int row = p & 31, pc = p >> 5;
             pv[jj] = (row < jn) ? *reinterpret_cast<const u16x8_t*>(a.P + (int64_t)(j0 + row) * D_LAT + QP_IC * c + 8 * pc)
                                 : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
         }
@@ -56,9 +57,9 @@ __global__ __launch_bounds__(256) void qprep_project_kernel(QprepArgs a) {
     };
     auto park = [&]() {
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
+        for (int jj = 0; jj < 2; ++jj) {
             const int p = tid + 256 * jj;
-            const int row = p & 63, pc = p >> 6;
+            const int row = p & 31, pc = p >> 5;
 #pragma unroll
             for (int e = 0; e < 8; ++e) s_p[8 * pc + e][row] = (double)bf16_to_f32(pv[jj][e]);
         }
@@ -66,8 +67,8 @@ __global__ __launch_bounds__(256) void qprep_project_kernel(QprepArgs a) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) s_q[8 * pc + e][hh] = (double)bf16_to_f32(qv[e]);
     };
-    const int jl = tid & 63, hg = tid >> 6;
-    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+    const int jl = tid & 31, hg = tid >> 5;    // heads 2 hg, 2 hg + 1
+    double acc0 = 0.0, acc1 = 0.0;
     fetch(0);
     park();
     __syncthreads();
@@ -77,12 +78,9 @@ __global__ __launch_bounds__(256) void qprep_project_kernel(QprepArgs a) {
 #pragma unroll 8
         for (int i = 0; i < QP_IC; ++i) {
             const double p = s_p[i][jl];
-            const double2 qa = *reinterpret_cast<const double2*>(&s_q[i][4 * hg]);
-            const double2 qb = *reinterpret_cast<const double2*>(&s_q[i][4 * hg + 2]);
-            acc[0] = fma(p, qa.x, acc[0]);
-            acc[1] = fma(p, qa.y, acc[1]);
-            acc[2] = fma(p, qb.x, acc[2]);
-            acc[3] = fma(p, qb.y, acc[3]);
+            const double2 q2 = *reinterpret_cast<const double2*>(&s_q[i][2 * hg]);
+            acc0 = fma(p, q2.x, acc0);
+            acc1 = fma(p, q2.y, acc1);
         }
         __syncthreads();
         if (more) {
@@ -93,12 +91,13 @@ __global__ __launch_bounds__(256) void qprep_project_kernel(QprepArgs a) {
     if (jl >= jn) return;
     const int off = (a.mode & 1) ? D_ROPE : 0;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        const int h = h0 + 4 * hg + t;
+    for (int t = 0; t < 2; ++t) {
+        const int h = h0 + 2 * hg + t;
         if (h >= a.H) continue;
         const int64_t bh = (int64_t)b * a.H + h;
-        a.wproj[bh * a.r + j0 + jl] = acc[t];
-        a.qt[bh * a.n + off + j0 + jl] = f64_to_bf16_rne(acc[t]);
+        const double v = t ? acc1 : acc0;
+        a.wproj[bh * a.r + j0 + jl] = v;
+        a.qt[bh * a.n + off + j0 + jl] = f64_to_bf16_rne(v);
     }
 }
 
@@ -116,6 +115,7 @@ constexpr int QF_RMAX = 512;
 __global__ __launch_bounds__(64) void qprep_finish_kernel(QprepArgs a) {
     __shared__ __align__(16) uint16_t s_ql[QF_HEADS][D_LAT];   // 16 KB
     __shared__ __align__(16) uint16_t s_qd[QF_HEADS][QF_RMAX]; // 16 KB
+    __shared__ __align__(16) double s_w[QF_HEADS][QF_RMAX];    // 64 KB
     const int lane = threadIdx.x;
     const int hl = lane >> 2, t = lane & 3;
     const int64_t bh0 = (int64_t)blockIdx.x * QF_HEADS;
@@ -138,12 +138,40 @@ __global__ __launch_bounds__(64) void qprep_finish_kernel(QprepArgs a) {
             const int p = lane + 64 * j;
             *reinterpret_cast<u16x8_t*>(&s_ql[p >> 6][8 * (p & 63)]) = v[j];
         }
-        const int r8 = rd / 8;
-        for (int p = lane; p < QF_HEADS * r8; p += 64) {
-            const int h = p / r8, pc = p % r8;
-            u16x8_t d = u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
-            if (bh0 + h < nbh) d = *reinterpret_cast<const u16x8_t*>(a.qt + (bh0 + h) * a.n + off + 8 * pc);
-            *reinterpret_cast<u16x8_t*>(&s_qd[h][8 * pc]) = d;
+        // digests (16 B = 8 values) and projections (16 B = 2 values), 4 of
+        // each per lane per round, loads in flight together
+        const int r8 = rd / 8, r2 = rd / 2;
+        for (int p0 = 0; p0 < QF_HEADS * r8; p0 += 256) {
+            u16x8_t d[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int p = p0 + lane + 64 * j;
+                const int h = p / max(r8, 1), pc = p % max(r8, 1);
+                d[j] = (p < QF_HEADS * r8 && bh0 + h < nbh)
+                           ? *reinterpret_cast<const u16x8_t*>(a.qt + (bh0 + h) * a.n + off + 8 * pc)
+                           : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int p = p0 + lane + 64 * j;
+                if (p < QF_HEADS * r8) *reinterpret_cast<u16x8_t*>(&s_qd[p / r8][8 * (p % r8)]) = d[j];
+            }
+        }
+        for (int p0 = 0; p0 < QF_HEADS * r2; p0 += 512) {
+            double2 wv[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int p = p0 + lane + 64 * j;
+                const int h = p / max(r2, 1), pc = p % max(r2, 1);
+                wv[j] = (p < QF_HEADS * r2 && bh0 + h < nbh)
+                            ? *reinterpret_cast<const double2*>(a.wproj + (bh0 + h) * a.r + 2 * pc)
+                            : make_double2(0.0, 0.0);
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int p = p0 + lane + 64 * j;
+                if (p < QF_HEADS * r2) *reinterpret_cast<double2*>(&s_w[p / r2][2 * (p % r2)]) = wv[j];
+            }
         }
     }
     __syncthreads();
@@ -152,7 +180,7 @@ __global__ __launch_bounds__(64) void qprep_finish_kernel(QprepArgs a) {
     const int64_t bhc = have ? bh : 0;
     const int b = (int)(bhc / a.H);
     uint16_t* qt = a.qt + bhc * a.n;
-    const double* w = a.wproj + bhc * a.r;
+    const double* w = &s_w[hl][0];
     // rope half of qt: 8 pieces of 16 B per head, 4 lanes per head
     if ((a.mode & 1) && have) {
         const u16x8_t* src = reinterpret_cast<const u16x8_t*>(a.q_rope + bhc * D_ROPE);
@@ -214,16 +242,31 @@ __global__ __launch_bounds__(64) void qprep_finish_kernel(QprepArgs a) {
     }
     r2 += __shfl_xor(r2, 1);
     r2 += __shfl_xor(r2, 2);
+    float ah = 0.f, eh = 0.f, nh = 0.f, qn = 0.f;
     if (t == 0 && have) {
         const double G = CERT_G;
         const double Dm = G * (double)ru_sqrt_f32((double)rd * Nq);
         const double sw = (double)ru_sqrt_f32(Nw);
         const double X = ((Nq - Nw) + G * (Nq + Nw)) + (2.0 * Dm) * sw;
-        const float ah = ru_sqrt_f32((X > 0.0 ? X : 0.0) * (1.0 + G));
-        const float eh = ru_f32((double)ru_sqrt_f32(Ne) * (1.0 + G) + Dm);
-        const float nh = ru_sqrt_f32(Nd * (1.0 + G));
-        const float qn = ru_sqrt_f32((r2 + Nd) * (1.0 + 0x1p-30));
+        ah = ru_sqrt_f32((X > 0.0 ? X : 0.0) * (1.0 + G));
+        eh = ru_f32((double)ru_sqrt_f32(Ne) * (1.0 + G) + Dm);
+        nh = ru_sqrt_f32(Nd * (1.0 + G));
+        qn = ru_sqrt_f32((r2 + Nd) * (1.0 + 0x1p-30));
         reinterpret_cast<float4*>(a.hsc)[bhc] = make_float4(ah, nh, eh, qn);
+    }
+    // per-sequence maxima (all values are >= 0, so float order = bit order):
+    // reduced over the wave's heads first when they all belong to one sequence
+    const int64_t bl = min(bh0 + QF_HEADS, nbh) - 1;
+    const bool one_seq = (bh0 / a.H) == (bl / a.H);
+    if (one_seq) {
+        for (int o = 4; o < 64; o <<= 1) {
+            ah = fmaxf(ah, __shfl_xor(ah, o));
+            eh = fmaxf(eh, __shfl_xor(eh, o));
+            nh = fmaxf(nh, __shfl_xor(nh, o));
+            qn = fmaxf(qn, __shfl_xor(qn, o));
+        }
+    }
+    if (t == 0 && have && (!one_seq || hl == 0)) {
         uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
         atomicMax(sq + SQ_QMAX, __float_as_uint(qn));
         atomicMax(sq + SQ_AMAX, __float_as_uint(ah));
@@ -233,7 +276,7 @@ __global__ __launch_bounds__(64) void qprep_finish_kernel(QprepArgs a) {
 }
 
 hipError_t launch_qprep(const QprepArgs& a, hipStream_t s) {
-    int jt = (a.r > 0 && (a.mode & 2)) ? (a.r + 63) / 64 : 1;
+    int jt = (a.r > 0 && (a.mode & 2)) ? (a.r + QP_ROWS - 1) / QP_ROWS : 1;
     dim3 g1(jt, (a.H + QP_HEADS - 1) / QP_HEADS, a.B);
     hipLaunchKernelGGL(qprep_project_kernel, g1, dim3(256), 0, s, a);
     hipError_t e = hipGetLastError();
