@@ -52,7 +52,7 @@ extern "C" {
 #define VKV_E_ARG (-1)            /* null pointer, bad enum, k or cap out of range */
 #define VKV_E_SHAPE (-2)          /* sizes out of the supported range */
 #define VKV_E_ALIGN (-3)          /* pointer or stride not 16-byte aligned */
-#define VKV_E_UNSUPPORTED (-4)    /* valid request this build does not implement */
+#define VKV_E_UNSUPPORTED (-4)    /* valid request the library does not implement */
 #define VKV_E_NOT_CONTRACTIVE (-5)/* certificate requested with ||P||_2 not certified <= 1 */
 #define VKV_E_HIP (-6)            /* a HIP runtime call failed */
 #define VKV_E_WORKSPACE (-7)      /* workspace null or smaller than vkv_workspace_size */
@@ -220,11 +220,22 @@ int vkv_attend(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int6
 
 /* query_prep -> score -> select -> [admit iff adm_count != NULL] -> attend,
  * same arguments as the individual calls (key and ub are the caller's
- * intermediates). */
+ * intermediates), all queued on `stream`; validates every stage's arguments
+ * before it launches anything. */
 int vkv_step_run(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k,
                  float* key, float* ub, int32_t* sel, double* theta, int32_t* adm,
                  int32_t* adm_count, int64_t cap, float scale, uint16_t* out, float* lse,
                  void* stream);
+
+/* enable != 0: vkv_step_run records a pair of HIP events around its score
+ * scan, on the call's stream, for up to 512 calls; vkv_score_timing reads
+ * them.  Either call clears what was recorded. */
+int vkv_set_timing(vkv_ctx* ctx, int enable);
+
+/* Durations in ms of the score scans recorded since timing was enabled or last
+ * read, in launch order, into ms[0..max); waits for those events and forgets
+ * them.  Returns the number written (>= 0) or a negative VKV_E_* status. */
+int vkv_score_timing(vkv_ctx* ctx, float* ms, int max);
 
 #ifdef __cplusplus
 }

@@ -31,7 +31,7 @@ _LIB_PATH = os.path.join(_HERE, "libvkv.so")
 exported_symbols = (
     "vkv_create", "vkv_destroy", "vkv_status_string", "vkv_last_error", "vkv_version",
     "vkv_digest_build", "vkv_workspace_size", "vkv_query_prep", "vkv_score", "vkv_select", "vkv_admit",
-    "vkv_attend", "vkv_step_run",
+    "vkv_attend", "vkv_step_run", "vkv_set_timing", "vkv_score_timing",
 )
 
 
@@ -89,11 +89,14 @@ def load():
     lib.vkv_attend.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P, i64, ctypes.c_float, P, P, P]
     lib.vkv_step_run.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P, P, P, P, i64,
                                  ctypes.c_float, P, P, P]
+    lib.vkv_set_timing.argtypes = [P, ctypes.c_int]
+    lib.vkv_score_timing.argtypes = [P, ctypes.POINTER(ctypes.c_float), ctypes.c_int]
     for name in exported_symbols:
         getattr(lib, name).restype = getattr(lib, name).restype or ctypes.c_int
     for name in ("vkv_create", "vkv_destroy", "vkv_digest_build", "vkv_workspace_size",
                  "vkv_query_prep", "vkv_score",
-                 "vkv_select", "vkv_admit", "vkv_attend", "vkv_step_run", "vkv_version"):
+                 "vkv_select", "vkv_admit", "vkv_attend", "vkv_step_run", "vkv_version",
+                 "vkv_set_timing", "vkv_score_timing"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -127,6 +130,18 @@ class Context:
     def check(self, rc: int):
         if rc != 0:
             raise VkvError(rc, self.lib.vkv_last_error(self.handle).decode())
+
+    def set_timing(self, enable: bool):
+        """Record the duration of the score scan of each ``step_run``."""
+        self.check(self.lib.vkv_set_timing(self.handle, 1 if enable else 0))
+
+    def score_timing(self) -> list:
+        """ms of each score scan ``step_run`` timed since the last read."""
+        buf = (ctypes.c_float * 512)()
+        n = self.lib.vkv_score_timing(self.handle, buf, 512)
+        if n < 0:
+            self.check(n)
+        return [float(buf[i]) for i in range(n)]
 
     def close(self):
         if self.handle:

@@ -11,10 +11,15 @@
 
 using namespace vkv;
 
+constexpr int TIMING_SLOTS = 512;  // score launches timed between two vkv_score_timing calls
+
 struct vkv_ctx {
     int device;
     int debug_rows;
     double* gram;          // [1024] device scratch for the contractivity check
+    int timing;            // vkv_step_run records events around its score launch
+    hipEvent_t* tev;       // [2 * TIMING_SLOTS] start/end events of timed score launches
+    int tcount;            // timed launches recorded since the last read
     char err[512];
 };
 
@@ -146,28 +151,114 @@ static void index_operand(const vkv_step* st, const uint16_t** x, int64_t* xs, i
     *xbs = st->index_batch_stride;
 }
 
-static SelectArgs select_args(const vkv_step* st, const WsLayout& L, char* w) {
-    SelectArgs a{};
+// A run of sequences [b0, b0 + nb) of a step: every per-sequence array (inputs,
+// outputs and the workspace's, all with the sequence as leading dimension) is
+// offset to b0 and the kernels see nb sequences.
+struct Chunk {
+    int64_t b0, nb;
+};
+
+// bytes per sequence of each workspace array (the leading-dimension strides of layout())
+struct WsStrides {
+    size_t qt, wproj, hsc, seq, hist, kt, flags, ccount, amb, ambkey, part_o, part_ml;
+};
+
+static WsStrides ws_strides(const vkv_step* st, const WsLayout& L) {
+    const int64_t H = st->H, Aw = std::max<int64_t>(L.A, 1);
+    return WsStrides{(size_t)(H * L.n * 2), (size_t)(H * std::max(st->r, 1) * 8), (size_t)(H * 16),
+                     (size_t)(SQ_WORDS * 4), (size_t)(2 * HIST_BINS * 4), (size_t)(Aw * 4), (size_t)Aw,
+                     (size_t)(L.nch * CC_WORDS * 4), (size_t)(Aw * 4), (size_t)(Aw * 8),
+                     (size_t)(L.splits * H * D_LAT * 4), (size_t)(L.splits * H * 2 * 4)};
+}
+
+static QprepArgs qprep_args(const vkv_step* st, const WsLayout& L, char* w, Chunk c) {
+    const WsStrides z = ws_strides(st, L);
+    const int64_t b0 = c.b0;
+    return QprepArgs{st->q_lat + b0 * st->H * D_LAT, st->q_rope + b0 * st->H * D_ROPE, st->P, (int)c.nb, (int)st->H,
+                     st->r, st->mode, (int)L.n, reinterpret_cast<uint16_t*>(w + L.qt + b0 * z.qt),
+                     reinterpret_cast<double*>(w + L.wproj + b0 * z.wproj),
+                     reinterpret_cast<float*>(w + L.hsc + b0 * z.hsc), reinterpret_cast<uint32_t*>(w + L.seq + b0 * z.seq),
+                     reinterpret_cast<uint32_t*>(w + L.hist + b0 * z.hist)};
+}
+
+static ScoreArgs score_args(const vkv_step* st, const WsLayout& L, char* w, Chunk c, float* key, float* ub) {
+    const WsStrides z = ws_strides(st, L);
+    const int64_t b0 = c.b0;
+    ScoreArgs a{};
     index_operand(st, &a.x, &a.xs, &a.xbs);
-    a.qt = reinterpret_cast<const uint16_t*>(w + L.qt);
-    a.hsc = reinterpret_cast<const float*>(w + L.hsc);
-    a.eta = st->eta;
-    a.eps = st->eps;
-    a.gam = st->gam;
+    a.x += b0 * a.xbs;
+    a.qt = reinterpret_cast<const uint16_t*>(w + L.qt + b0 * z.qt);
+    a.hsc = reinterpret_cast<const float*>(w + L.hsc + b0 * z.hsc);
+    a.eta = st->eta ? st->eta + b0 * st->T : nullptr;
+    a.eps = st->eps ? st->eps + b0 * st->T : nullptr;
+    a.gam = st->gam ? st->gam + b0 * st->T : nullptr;
     a.T = st->T;
-    a.seq = reinterpret_cast<uint32_t*>(w + L.seq);
-    a.hist = reinterpret_cast<uint32_t*>(w + L.hist);
-    a.kt = reinterpret_cast<const float*>(w + L.kt);
-    a.flags = reinterpret_cast<uint8_t*>(w + L.flags);
-    a.flags2 = reinterpret_cast<uint8_t*>(w + L.flags2);
-    a.ccount = reinterpret_cast<uint32_t*>(w + L.ccount);
-    a.amb = reinterpret_cast<int32_t*>(w + L.amb);
-    a.ambkey = reinterpret_cast<uint64_t*>(w + L.ambkey);
+    a.key = key ? key + b0 * L.A : nullptr;
+    a.ub = ub ? ub + b0 * L.A : nullptr;
+    a.kt = reinterpret_cast<float*>(w + L.kt + b0 * z.kt);
+    a.seq = reinterpret_cast<uint32_t*>(w + L.seq + b0 * z.seq);
     a.A = L.A;
-    a.nch = L.nch;
-    a.B = (int)st->B;
+    a.B = (int)c.nb;
     a.H = (int)st->H;
     a.n = (int)L.n;
+    return a;
+}
+
+static SelectArgs select_args(const vkv_step* st, const WsLayout& L, char* w, Chunk c) {
+    const WsStrides z = ws_strides(st, L);
+    const int64_t b0 = c.b0;
+    SelectArgs a{};
+    index_operand(st, &a.x, &a.xs, &a.xbs);
+    a.x += b0 * a.xbs;
+    a.qt = reinterpret_cast<const uint16_t*>(w + L.qt + b0 * z.qt);
+    a.hsc = reinterpret_cast<const float*>(w + L.hsc + b0 * z.hsc);
+    a.eta = st->eta ? st->eta + b0 * st->T : nullptr;
+    a.eps = st->eps ? st->eps + b0 * st->T : nullptr;
+    a.gam = st->gam ? st->gam + b0 * st->T : nullptr;
+    a.T = st->T;
+    a.seq = reinterpret_cast<uint32_t*>(w + L.seq + b0 * z.seq);
+    a.hist = reinterpret_cast<uint32_t*>(w + L.hist + b0 * z.hist);
+    a.kt = reinterpret_cast<const float*>(w + L.kt + b0 * z.kt);
+    a.flags = reinterpret_cast<uint8_t*>(w + L.flags + b0 * z.flags);
+    a.flags2 = reinterpret_cast<uint8_t*>(w + L.flags2 + b0 * z.flags);
+    a.ccount = reinterpret_cast<uint32_t*>(w + L.ccount + b0 * z.ccount);
+    a.amb = reinterpret_cast<int32_t*>(w + L.amb + b0 * z.amb);
+    a.ambkey = reinterpret_cast<uint64_t*>(w + L.ambkey + b0 * z.ambkey);
+    a.A = L.A;
+    a.nch = L.nch;
+    a.B = (int)c.nb;
+    a.H = (int)st->H;
+    a.n = (int)L.n;
+    return a;
+}
+
+static AttendArgs attend_args(const vkv_step* st, const WsLayout& L, char* w, Chunk c, int64_t k, const int32_t* sel,
+                              const int32_t* adm, const int32_t* adm_count, int64_t cap, float scale, uint16_t* out,
+                              float* lse) {
+    const WsStrides z = ws_strides(st, L);
+    const int64_t b0 = c.b0;
+    AttendArgs a{};
+    a.q_lat = st->q_lat + b0 * st->H * D_LAT;
+    a.q_rope = st->q_rope + b0 * st->H * D_ROPE;
+    a.cache = st->cache + b0 * st->cache_batch_stride;
+    a.cs = st->cache_row_stride;
+    a.cbs = st->cache_batch_stride;
+    a.sel = sel ? sel + b0 * k : nullptr;
+    a.adm = adm ? adm + b0 * cap : nullptr;
+    a.adm_count = adm_count ? adm_count + b0 : nullptr;
+    a.k = k;
+    a.W = st->W;
+    a.A = L.A;
+    a.cap = cap;
+    a.rows_per_split = L.rows_per_split;
+    a.splits = (int)L.splits;
+    a.B = (int)c.nb;
+    a.H = (int)st->H;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.part_o = reinterpret_cast<float*>(w + L.part_o + b0 * z.part_o);
+    a.part_ml = reinterpret_cast<float*>(w + L.part_ml + b0 * z.part_ml);
+    a.out = out + b0 * st->H * D_LAT;
+    a.lse = lse + b0 * st->H;
     return a;
 }
 
@@ -265,6 +356,10 @@ int vkv_create(vkv_ctx** out, int device) {
 int vkv_destroy(vkv_ctx* ctx) {
     if (!ctx) return VKV_OK;
     (void)hipSetDevice(ctx->device);
+    if (ctx->tev) {
+        for (int i = 0; i < 2 * TIMING_SLOTS; ++i) (void)hipEventDestroy(ctx->tev[i]);
+        free(ctx->tev);
+    }
     (void)hipFree(ctx->gram);
     free(ctx);
     return VKV_OK;
@@ -325,92 +420,155 @@ int vkv_workspace_size(const vkv_step* st, int64_t k, int64_t cap, size_t* bytes
     return VKV_OK;
 }
 
-int vkv_query_prep(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, void* stream) {
-    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+}  // extern "C"
+
+// ------------------------------------------- validation and launch, per stage
+
+static int check_prep(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes) {
     int rc = check_step(ctx, st);
     if (rc) return rc;
-    WsLayout L = layout(st, 0, 0);
-    if ((rc = check_ws(ctx, ws, ws_bytes, L.part_o))) return rc;
-    char* w = (char*)ws;
-    QprepArgs q{st->q_lat, st->q_rope, st->P, (int)st->B, (int)st->H, st->r, st->mode, (int)L.n,
-                reinterpret_cast<uint16_t*>(w + L.qt), reinterpret_cast<double*>(w + L.wproj),
-                reinterpret_cast<float*>(w + L.hsc), reinterpret_cast<uint32_t*>(w + L.seq),
-                reinterpret_cast<uint32_t*>(w + L.hist)};
-    HIP_TRY(ctx, launch_qprep(q, (hipStream_t)stream));
+    return check_ws(ctx, ws, ws_bytes, layout(st, 0, 0).part_o);
+}
+
+static int check_score(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, float* ub) {
+    int rc = check_prep(ctx, st, ws, ws_bytes);
+    if (rc) return rc;
+    if (ub && (!st->eta || !st->eps || !st->gam)) return fail(ctx, VKV_E_ARG, "ub needs eta, eps and gam");
+    if (ub && st->mode == VKV_MODE_DIGEST) return fail(ctx, VKV_E_UNSUPPORTED, "the bound needs the branch summand in the key");
+    return VKV_OK;
+}
+
+static int check_select(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, int32_t* sel,
+                        double* theta) {
+    int rc = check_prep(ctx, st, ws, ws_bytes);
+    if (rc) return rc;
+    const int64_t A = st->T - st->W;
+    if (k < 0 || k > A) return fail(ctx, VKV_E_ARG, "k=%lld outside [0, A=%lld]", (long long)k, (long long)A);
+    if (!theta || (k > 0 && !sel)) return fail(ctx, VKV_E_ARG, "sel and theta are required");
+    return VKV_OK;
+}
+
+static int check_admit(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, const int32_t* sel,
+                       const double* theta, const float* ub, int32_t* adm, int32_t* adm_count, int64_t cap) {
+    int rc = check_prep(ctx, st, ws, ws_bytes);
+    if (rc) return rc;
+    const int64_t A = st->T - st->W;
+    if (st->mode == VKV_MODE_DIGEST) return fail(ctx, VKV_E_UNSUPPORTED, "admission needs the branch summand in the key");
+    if (!st->eta || !st->eps || !st->gam) return fail(ctx, VKV_E_ARG, "admission needs eta, eps and gam");
+    if (k < 0 || k > A) return fail(ctx, VKV_E_ARG, "k=%lld outside [0, A]", (long long)k);
+    if (cap < 0 || cap > A) return fail(ctx, VKV_E_ARG, "cap=%lld outside [0, A]", (long long)cap);
+    if (!theta || !adm_count || (A > 0 && !ub) || (cap > 0 && !adm) || (k > 0 && !sel))
+        return fail(ctx, VKV_E_ARG, "sel, theta, ub, adm and adm_count are required");
+    return VKV_OK;
+}
+
+static int check_attend(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, const int32_t* sel,
+                        const int32_t* adm, const int32_t* adm_count, int64_t cap, float scale, uint16_t* out,
+                        float* lse) {
+    int rc = check_step(ctx, st);
+    if (rc) return rc;
+    const int64_t A = st->T - st->W;
+    if (k < 0 || k > A) return fail(ctx, VKV_E_ARG, "k=%lld outside [0, A]", (long long)k);
+    if (cap < 0 || cap > A) return fail(ctx, VKV_E_ARG, "cap=%lld outside [0, A]", (long long)cap);
+    if (cap > 0 && (!adm || !adm_count)) return fail(ctx, VKV_E_ARG, "cap > 0 needs adm and adm_count");
+    if (!out || !lse || (k > 0 && !sel)) return fail(ctx, VKV_E_ARG, "sel, out and lse are required");
+    if (!al16(out)) return fail(ctx, VKV_E_ALIGN, "out must be 16-byte aligned");
+    if (!(scale > 0.f) || !(scale < 1e30f)) return fail(ctx, VKV_E_ARG, "scale must be positive and finite");
+    return check_ws(ctx, ws, ws_bytes, layout(st, k, cap).total);
+}
+
+static hipError_t run_prep(const vkv_step* st, char* w, Chunk c, hipStream_t s) {
+    return launch_qprep(qprep_args(st, layout(st, 0, 0), w, c), s);
+}
+
+static hipError_t run_score(const vkv_step* st, char* w, Chunk c, float* key, float* ub, hipStream_t s) {
+    return launch_score(score_args(st, layout(st, 0, 0), w, c, key, ub), s);
+}
+
+static hipError_t run_select(const vkv_step* st, char* w, Chunk c, int64_t k, int32_t* sel, double* theta,
+                             hipStream_t s) {
+    SelectArgs a = select_args(st, layout(st, 0, 0), w, c);
+    a.sel = sel ? sel + c.b0 * k : nullptr;
+    a.theta = theta + c.b0;
+    a.k = k;
+    return launch_select(a, s);
+}
+
+static hipError_t run_admit(const vkv_step* st, char* w, Chunk c, int64_t k, const int32_t* sel, const double* theta,
+                            const float* ub, int32_t* adm, int32_t* adm_count, int64_t cap, hipStream_t s) {
+    const WsLayout L = layout(st, 0, 0);
+    SelectArgs a = select_args(st, L, w, c);
+    a.ub = ub ? ub + c.b0 * L.A : nullptr;
+    a.sel = sel ? const_cast<int32_t*>(sel) + c.b0 * k : nullptr;
+    a.theta = const_cast<double*>(theta) + c.b0;
+    a.adm = adm ? adm + c.b0 * cap : nullptr;
+    a.adm_count = adm_count + c.b0;
+    a.k = k;
+    a.cap = cap;
+    return launch_admit(a, s);
+}
+
+static hipError_t run_attend(const vkv_step* st, char* w, Chunk c, int64_t k, const int32_t* sel, const int32_t* adm,
+                             const int32_t* adm_count, int64_t cap, float scale, uint16_t* out, float* lse,
+                             hipStream_t s) {
+    if (cap == 0) {
+        adm = nullptr;
+        adm_count = nullptr;
+    }
+    return launch_attend(attend_args(st, layout(st, k, cap), w, c, k, sel, adm, adm_count, cap, scale, out, lse), s);
+}
+
+static int ensure_timing_events(vkv_ctx* ctx) {
+    if (ctx->tev) return VKV_OK;
+    hipEvent_t* ev = (hipEvent_t*)calloc(2 * TIMING_SLOTS, sizeof(hipEvent_t));
+    if (!ev) return fail(ctx, VKV_E_ARG, "out of host memory");
+    for (int i = 0; i < 2 * TIMING_SLOTS; ++i) {
+        hipError_t e = hipEventCreate(&ev[i]);
+        if (e != hipSuccess) {
+            for (int j = 0; j < i; ++j) (void)hipEventDestroy(ev[j]);
+            free(ev);
+            return fail(ctx, VKV_E_HIP, "hipEventCreate: %s", hipGetErrorString(e));
+        }
+    }
+    ctx->tev = ev;
+    return VKV_OK;
+}
+
+extern "C" {
+
+int vkv_query_prep(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    int rc = check_prep(ctx, st, ws, ws_bytes);
+    if (rc) return rc;
+    HIP_TRY(ctx, run_prep(st, (char*)ws, Chunk{0, st->B}, (hipStream_t)stream));
     return VKV_OK;
 }
 
 int vkv_score(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, float* key, float* ub, void* stream) {
     if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
-    int rc = check_step(ctx, st);
+    int rc = check_score(ctx, st, ws, ws_bytes, ub);
     if (rc) return rc;
-    WsLayout L = layout(st, 0, 0);
-    if ((rc = check_ws(ctx, ws, ws_bytes, L.part_o))) return rc;
-    if (ub && (!st->eta || !st->eps || !st->gam)) return fail(ctx, VKV_E_ARG, "ub needs eta, eps and gam");
-    if (ub && st->mode == VKV_MODE_DIGEST) return fail(ctx, VKV_E_UNSUPPORTED, "the bound needs the branch summand in the key");
-    hipStream_t s = (hipStream_t)stream;
-    char* w = (char*)ws;
-    ScoreArgs a{};
-    index_operand(st, &a.x, &a.xs, &a.xbs);
-    a.qt = reinterpret_cast<const uint16_t*>(w + L.qt);
-    a.hsc = reinterpret_cast<const float*>(w + L.hsc);
-    a.eta = st->eta;
-    a.eps = st->eps;
-    a.gam = st->gam;
-    a.T = st->T;
-    a.key = key;
-    a.ub = ub;
-    a.kt = reinterpret_cast<float*>(w + L.kt);
-    a.seq = reinterpret_cast<uint32_t*>(w + L.seq);
-    a.A = L.A;
-    a.B = (int)st->B;
-    a.H = (int)st->H;
-    a.n = (int)L.n;
-    HIP_TRY(ctx, launch_score(a, s));
+    HIP_TRY(ctx, run_score(st, (char*)ws, Chunk{0, st->B}, key, ub, (hipStream_t)stream));
     return VKV_OK;
 }
 
 int vkv_select(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, int32_t* sel, double* theta,
                void* stream) {
     if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
-    int rc = check_step(ctx, st);
+    int rc = check_select(ctx, st, ws, ws_bytes, k, sel, theta);
     if (rc) return rc;
-    WsLayout L = layout(st, 0, 0);
-    if ((rc = check_ws(ctx, ws, ws_bytes, L.part_o))) return rc;
-    if (k < 0 || k > L.A) return fail(ctx, VKV_E_ARG, "k=%lld outside [0, A=%lld]", (long long)k, (long long)L.A);
-    if (!theta || (k > 0 && !sel)) return fail(ctx, VKV_E_ARG, "sel and theta are required");
     hipStream_t s = (hipStream_t)stream;
-    SelectArgs a = select_args(st, L, (char*)ws);
-    a.sel = sel;
-    a.theta = theta;
-    a.k = k;
-    HIP_TRY(ctx, launch_select(a, s));
+    HIP_TRY(ctx, run_select(st, (char*)ws, Chunk{0, st->B}, k, sel, theta, s));
     return debug_check_sel(ctx, st, k, sel, s);
 }
 
 int vkv_admit(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, const int32_t* sel,
               const double* theta, const float* ub, int32_t* adm, int32_t* adm_count, int64_t cap, void* stream) {
     if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
-    int rc = check_step(ctx, st);
+    int rc = check_admit(ctx, st, ws, ws_bytes, k, sel, theta, ub, adm, adm_count, cap);
     if (rc) return rc;
-    WsLayout L = layout(st, 0, 0);
-    if ((rc = check_ws(ctx, ws, ws_bytes, L.part_o))) return rc;
-    if (st->mode == VKV_MODE_DIGEST) return fail(ctx, VKV_E_UNSUPPORTED, "admission needs the branch summand in the key");
-    if (!st->eta || !st->eps || !st->gam) return fail(ctx, VKV_E_ARG, "admission needs eta, eps and gam");
-    if (k < 0 || k > L.A) return fail(ctx, VKV_E_ARG, "k=%lld outside [0, A]", (long long)k);
-    if (cap < 0 || cap > L.A) return fail(ctx, VKV_E_ARG, "cap=%lld outside [0, A]", (long long)cap);
-    if (!theta || !adm_count || (L.A > 0 && !ub) || (cap > 0 && !adm) || (k > 0 && !sel))
-        return fail(ctx, VKV_E_ARG, "sel, theta, ub, adm and adm_count are required");
     hipStream_t s = (hipStream_t)stream;
-    SelectArgs a = select_args(st, L, (char*)ws);
-    a.ub = ub;
-    a.sel = const_cast<int32_t*>(sel);
-    a.theta = const_cast<double*>(theta);
-    a.adm = adm;
-    a.adm_count = adm_count;
-    a.k = k;
-    a.cap = cap;
-    HIP_TRY(ctx, launch_admit(a, s));
+    HIP_TRY(ctx, run_admit(st, (char*)ws, Chunk{0, st->B}, k, sel, theta, ub, adm, adm_count, cap, s));
     return debug_check_adm(ctx, st, k, sel, adm, adm_count, cap, s);
 }
 
@@ -418,62 +576,65 @@ int vkv_attend(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int6
                const int32_t* adm, const int32_t* adm_count, int64_t cap, float scale, uint16_t* out, float* lse,
                void* stream) {
     if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
-    int rc = check_step(ctx, st);
+    int rc = check_attend(ctx, st, ws, ws_bytes, k, sel, adm, adm_count, cap, scale, out, lse);
     if (rc) return rc;
-    const int64_t A = st->T - st->W;
-    if (k < 0 || k > A) return fail(ctx, VKV_E_ARG, "k=%lld outside [0, A]", (long long)k);
-    if (cap < 0 || cap > A) return fail(ctx, VKV_E_ARG, "cap=%lld outside [0, A]", (long long)cap);
-    if (cap > 0 && (!adm || !adm_count)) return fail(ctx, VKV_E_ARG, "cap > 0 needs adm and adm_count");
-    if (cap == 0) {
-        adm = nullptr;
-        adm_count = nullptr;
-    }
-    if (!out || !lse || (k > 0 && !sel)) return fail(ctx, VKV_E_ARG, "sel, out and lse are required");
-    if (!al16(out)) return fail(ctx, VKV_E_ALIGN, "out must be 16-byte aligned");
-    if (!(scale > 0.f) || !(scale < 1e30f)) return fail(ctx, VKV_E_ARG, "scale must be positive and finite");
-    WsLayout L = layout(st, k, cap);
-    if ((rc = check_ws(ctx, ws, ws_bytes, L.total))) return rc;
-    hipStream_t s = (hipStream_t)stream;
-    char* w = (char*)ws;
-    AttendArgs a{};
-    a.q_lat = st->q_lat;
-    a.q_rope = st->q_rope;
-    a.cache = st->cache;
-    a.cs = st->cache_row_stride;
-    a.cbs = st->cache_batch_stride;
-    a.sel = sel;
-    a.adm = adm;
-    a.adm_count = adm_count;
-    a.k = k;
-    a.W = st->W;
-    a.A = A;
-    a.cap = cap;
-    a.rows_per_split = L.rows_per_split;
-    a.splits = (int)L.splits;
-    a.B = (int)st->B;
-    a.H = (int)st->H;
-    a.scale_log2 = scale * 1.4426950408889634f;
-    a.part_o = reinterpret_cast<float*>(w + L.part_o);
-    a.part_ml = reinterpret_cast<float*>(w + L.part_ml);
-    a.out = out;
-    a.lse = lse;
-    HIP_TRY(ctx, launch_attend(a, s));
+    HIP_TRY(ctx, run_attend(st, (char*)ws, Chunk{0, st->B}, k, sel, adm, adm_count, cap, scale, out, lse,
+                            (hipStream_t)stream));
     return VKV_OK;
+}
+
+int vkv_set_timing(vkv_ctx* ctx, int enable) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    if (enable) {
+        int rc = ensure_timing_events(ctx);
+        if (rc) return rc;
+    }
+    ctx->timing = enable ? 1 : 0;
+    ctx->tcount = 0;
+    return VKV_OK;
+}
+
+int vkv_score_timing(vkv_ctx* ctx, float* ms, int max) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    if (!ms || max < 1) return fail(ctx, VKV_E_ARG, "ms and max >= 1 are required");
+    const int n = std::min(ctx->tcount, max);
+    for (int i = 0; i < n; ++i) {
+        HIP_TRY(ctx, hipEventSynchronize(ctx->tev[2 * i + 1]));
+        HIP_TRY(ctx, hipEventElapsedTime(&ms[i], ctx->tev[2 * i], ctx->tev[2 * i + 1]));
+    }
+    ctx->tcount = 0;
+    return n;
 }
 
 int vkv_step_run(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, float* key, float* ub,
                  int32_t* sel, double* theta, int32_t* adm, int32_t* adm_count, int64_t cap, float scale, uint16_t* out,
                  float* lse, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
     const bool two_tier = adm_count != nullptr;
-    int rc = vkv_query_prep(ctx, st, ws, ws_bytes, stream);
-    if (rc) return rc;
-    if ((rc = vkv_score(ctx, st, ws, ws_bytes, key, two_tier ? ub : nullptr, stream))) return rc;
-    if ((rc = vkv_select(ctx, st, ws, ws_bytes, k, sel, theta, stream))) return rc;
-    if (two_tier) {
-        if ((rc = vkv_admit(ctx, st, ws, ws_bytes, k, sel, theta, ub, adm, adm_count, cap, stream))) return rc;
-    }
-    return vkv_attend(ctx, st, ws, ws_bytes, k, sel, two_tier ? adm : nullptr, two_tier ? adm_count : nullptr,
-                      two_tier ? cap : 0, scale, out, lse, stream);
+    float* ubp = two_tier ? ub : nullptr;
+    int rc;
+    if ((rc = check_score(ctx, st, ws, ws_bytes, ubp))) return rc;
+    if ((rc = check_select(ctx, st, ws, ws_bytes, k, sel, theta))) return rc;
+    if (two_tier && (rc = check_admit(ctx, st, ws, ws_bytes, k, sel, theta, ub, adm, adm_count, cap))) return rc;
+    const int64_t acap = two_tier ? cap : 0;
+    if ((rc = check_attend(ctx, st, ws, ws_bytes, k, sel, two_tier ? adm : nullptr, two_tier ? adm_count : nullptr,
+                           acap, scale, out, lse)))
+        return rc;
+    hipStream_t s = (hipStream_t)stream;
+    char* w = (char*)ws;
+    const Chunk all{0, st->B};
+    HIP_TRY(ctx, run_prep(st, w, all, s));
+    const bool timed = ctx->timing && ctx->tcount < TIMING_SLOTS;
+    if (timed) HIP_TRY(ctx, hipEventRecord(ctx->tev[2 * ctx->tcount], s));
+    HIP_TRY(ctx, run_score(st, w, all, key, ubp, s));
+    if (timed) HIP_TRY(ctx, hipEventRecord(ctx->tev[2 * ctx->tcount++ + 1], s));
+    HIP_TRY(ctx, run_select(st, w, all, k, sel, theta, s));
+    if (two_tier) HIP_TRY(ctx, run_admit(st, w, all, k, sel, theta, ub, adm, adm_count, cap, s));
+    HIP_TRY(ctx, run_attend(st, w, all, k, sel, two_tier ? adm : nullptr, two_tier ? adm_count : nullptr, acap,
+                            scale, out, lse, s));
+    if ((rc = debug_check_sel(ctx, st, k, sel, s))) return rc;
+    if (two_tier) return debug_check_adm(ctx, st, k, sel, adm, adm_count, cap, s);
+    return VKV_OK;
 }
 
 }  // extern "C"

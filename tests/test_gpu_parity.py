@@ -342,6 +342,25 @@ def test_determinism(ctx):
         assert np.array_equal(g1["adm"][b, :m], g2["adm"][b, :m])
 
 
+def test_score_timing_records_each_step():
+    say("score timing events")
+    c = vkv.Context(0)
+    cfg = synth.CONFIGS["cfg1"].with_(H=16)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=3000)
+    pack = gpu_index(c, wl, False)
+    c.set_timing(True)
+    g = [gpu_step(c, wl, k=64, index_pack=pack)[0] for _ in range(3)]
+    ms = c.score_timing()
+    assert len(ms) == 3 and all(t > 0 for t in ms), ms
+    assert c.score_timing() == []
+    c.set_timing(False)
+    gpu_step(c, wl, k=64, index_pack=pack)
+    assert c.score_timing() == []
+    for key in ("sel", "theta", "out_bits", "lse"):
+        assert np.array_equal(g[0][key], g[2][key]), key
+    c.close()
+
+
 def test_debug_rows_assertion_passes(ctx, monkeypatch):
     say("VKV_DEBUG_ROWS")
     monkeypatch.setenv("VKV_DEBUG_ROWS", "1")
