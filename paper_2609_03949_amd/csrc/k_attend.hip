@@ -8,19 +8,22 @@
 //
 // Work split: workgroup = (split of the row list, group of 128 heads, b);
 // 8 waves x 16 heads, so every gathered row serves all heads of the group.
-// Tiles of 32 rows are double-buffered in LDS: while tile i is scored and
-// accumulated, tile i+1 streams in by direct global->LDS loads
-// (global_load_lds_dwordx4), row-major with piece p of tile row r at slot
-// (p + r) mod 72 (conflict-free MFMA operand reads).  Once a tile has landed
-// its latent half is also written transposed (for O += P V, V as the B
-// operand).  P never leaves registers: the S accumulator layout of a lane (4
-// rows x 1 head per 16-row tile) is exactly the A-operand layout of the PV
-// product when the 32 rows of the tile are fed to the K dimension in a
-// permuted order, and the transposed tile is written in that same order.
+// Tiles of 32 rows stream through a ring of three LDS stages by direct
+// global->LDS loads (global_load_lds_dwordx4), issued two tiles ahead, so one
+// workgroup barrier per tile suffices.  Stage layout: row-major, piece p (16 B)
+// of tile row r at slot 72 r + (p ^ f(r)); f spreads both operand reads below
+// over all LDS banks.  S^T = K Q^T reads K rows as the A operand; O += P V
+// reads V = the latent half of the same stage with the transposing LDS load
+// (ds_read_b64_tr_b16), so no transposed copy is written.  P never leaves
+// registers: the S accumulator layout of a lane (4 rows x 1 head per 16-row
+// tile) is the A-operand layout of the PV product when the 32 rows of the tile
+// are fed to the K dimension in a permuted order, which the V reads follow.
 // Online softmax in the log2 domain; each split emits (unnormalised O,
 // running max, running sum) and a second kernel merges the splits by their
 // log-sum-exp (the appendix's kernel mapping: fetched rows are one more
 // split-KV partition).
+#include <type_traits>
+
 #include "vkv_internal.h"
 
 namespace vkv {
@@ -30,18 +33,12 @@ constexpr int ATT_THREADS = 64 * ATT_WAVES;  // 512
 constexpr int ROW_PIECES = D_ROW / 8;        // 72 pieces of 16 B per row
 constexpr int TILE_BYTES = ATT_CHUNK * D_ROW * 2;            // 36 KB
 constexpr int TILE_LOADS = TILE_BYTES / 1024;                // 36 loads of 1 KB
-constexpr int VT_STRIDE = 40;                // LDS stride of the transposed tile (u16), 80 B
-constexpr int VT_BYTES = D_LAT * VT_STRIDE * 2;              // 40 KB
+constexpr int ATT_STAGES = 3;
+constexpr int ROW_BYTES = D_ROW * 2;                         // 1152
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void gbl_void_t;
-
-// Position of tile row rl on the K axis of the PV product: rows
-// 16*mt + 4*g + i (held by lane group g at accumulator slot i of M-tile mt)
-// go to K slot 8*g + 4*mt + i.
-__device__ __forceinline__ int pv_slot(int rl) {
-    return 8 * ((rl & 15) >> 2) + 4 * (rl >> 4) + (rl & 3);
-}
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ int32_t attended_row(const AttendArgs& a, int b, int64_t p) {
     if (p < a.k) return a.sel[(int64_t)b * a.k + p];
@@ -49,19 +46,69 @@ __device__ __forceinline__ int32_t attended_row(const AttendArgs& a, int b, int6
     return a.adm[(int64_t)b * a.cap + (p - a.k - a.W)];
 }
 
-// byte offset of piece p of tile row r in a row-major stage: the slot is p
-// with its low three bits XORed by (r / 2) mod 8, which spreads the 16 rows
-// read by one MFMA operand load over all LDS banks (rows are 1152 B apart,
-// i.e. alternate between two bank halves)
-__device__ __forceinline__ int kslot(int r, int p) {
-    return r * (D_ROW * 2) + 16 * (p ^ ((r >> 1) & 7));
+// XOR applied to the piece index of tile row r (low three bits only, so each
+// aligned group of 8 pieces maps onto itself).  With 16-byte slots the bank
+// group of a slot is its index mod 16; f makes distinct groups for (a) the 16
+// rows of one piece (K operand reads) and (b) 8 consecutive rows x 2 adjacent
+// pieces (transposing V reads).
+__device__ __forceinline__ int piece_xor(int r) { return 2 * ((r >> 1) & 3) + ((r >> 3) & 1); }
+
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// Compile-time loop: f(std::integral_constant<int, I>) for I = 0 .. N-1.
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        static_for<I + 1, N>(f);
+    }
+}
+
+// op-reduction of x over the four 16-lane groups (lanes c, c+16, c+32, c+48),
+// result in all of them: two cross-lane swaps, no LDS traffic
+template <typename Op>
+__device__ __forceinline__ float allreduce_groups(float x, Op op) {
+    const uint32_t u = __float_as_uint(x);
+    const auto r32 = __builtin_amdgcn_permlane32_swap(u, u, false, false);   // lane l ^ 32
+    const float y = op(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
+    const uint32_t v = __float_as_uint(y);
+    const auto r16 = __builtin_amdgcn_permlane16_swap(v, v, false, false);   // lane l ^ 16
+    return op(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
+}
+
+// Operand reads of the tile stages, issued as explicit LDS instructions: the
+// compiler sees no LDS read of a stage, so it never makes them wait for the
+// direct loads still in flight into the other stages, and the lgkmcnt waits
+// before each use are explicit (lds_wait: at most N of this wave's LDS
+// operations outstanding; LDS operations complete in order).  The kernel
+// issues no scalar memory loads inside the tile loop, so lgkmcnt counts LDS
+// operations only there.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+template <int OFF>
+__device__ __forceinline__ bf16x8_t lds_read128(uint32_t addr) {
+    bf16x8_t v;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(OFF));
+    return v;
+}
+// transposing read: within each 16-lane group, lane j supplies the address of
+// 4 consecutive 16-bit elements D[j][0..3], and lane i receives D[4e + i/4][i % 4]
+// for e = 0..3
+template <int OFF>
+__device__ __forceinline__ i16x4_t lds_read_tr16(uint32_t addr) {
+    i16x4_t v;
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(OFF));
+    return v;
+}
+template <int N, typename T0, typename T1>
+__device__ __forceinline__ void lds_wait(T0& x, T1& y) {
+    asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(x), "+v"(y) : "n"(N));
 }
 
 __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
-    extern __shared__ __align__(16) uint8_t smem[];
-    uint8_t* s_k = smem;                                      // [2][TILE_BYTES]
-    uint8_t* s_vt = smem + 2 * TILE_BYTES;                    // [2][D_LAT][VT_STRIDE] u16
-    int32_t* s_rows = reinterpret_cast<int32_t*>(smem + 2 * TILE_BYTES + 2 * VT_BYTES);   // the split's rows
+    __shared__ __align__(16) uint8_t s_k[ATT_STAGES * TILE_BYTES];   // the ring of tile stages
+    __shared__ int32_t s_rows[ATT_MAX_SPLIT_ROWS];                    // the split's rows
 
     const int sp = blockIdx.x, hg = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x;
@@ -105,21 +152,39 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
         }
     }
     __syncthreads();
-    // direct loads of tile t into stage t & 1 (load instruction j goes to wave
-    // j % 8); rows past the end of the list repeat its last row (loaded, never
-    // weighted)
-    auto issue = [&](int t) {
-        uint8_t* st = s_k + (t & 1) * TILE_BYTES;
-        for (int j = wave; j < TILE_LOADS; j += ATT_WAVES) {
-            const int q = 64 * j + lane;               // destination slot
-            const int r = q / ROW_PIECES, s = q % ROW_PIECES;
-            const int p = s ^ ((r >> 1) & 7);
-            const int i = min(ATT_CHUNK * t + r, nrow - 1);
-            const uint16_t* src = cb + (int64_t)s_rows[i] * a.cs + 8 * p;
-            __builtin_amdgcn_global_load_lds((gbl_void_t*)src, (lds_void_t*)(st + 1024 * j), 16, 0, 0);
+    // Direct loads of tile t into stage t mod 3: load instruction j (1 KB,
+    // slots 64 j .. 64 j + 63) belongs to wave j mod 8, so waves 0-3 issue 5
+    // per tile and waves 4-7 issue 4.  Slot q holds piece (q mod 72) ^ f(r) of
+    // tile row r = q / 72.  Rows past the end of the list repeat its last row
+    // (loaded, never weighted).
+    constexpr int MAXJ = (TILE_LOADS + ATT_WAVES - 1) / ATT_WAVES;   // 5
+    const int nj = (TILE_LOADS - wave + ATT_WAVES - 1) / ATT_WAVES;  // 5 or 4
+    auto issue = [&](int t, uint8_t* st) {
+        // the per-load slot arithmetic is redone each time (an opaque copy of
+        // the lane index keeps the compiler from holding it across the loop)
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        int row[MAXJ], off[MAXJ];
+#pragma unroll
+        for (int i = 0; i < MAXJ; ++i) {   // all row lookups first (in bounds for every i)
+            const int q = 64 * (wave + ATT_WAVES * i) + ln;
+            const int r = q / ROW_PIECES;
+            row[i] = s_rows[min(ATT_CHUNK * t + r, nrow - 1)];
+            off[i] = 8 * ((q - ROW_PIECES * r) ^ piece_xor(r));
+        }
+        static_assert(MAXJ == 5, "row lookups tied below");
+        asm volatile("" : "+v"(row[0]), "+v"(row[1]), "+v"(row[2]), "+v"(row[3]), "+v"(row[4]));   // one LDS round trip
+#pragma unroll
+        for (int i = 0; i < MAXJ; ++i) {
+            if (i < nj) {
+                const uint16_t* src = cb + (int64_t)row[i] * a.cs + off[i];
+                __builtin_amdgcn_global_load_lds((gbl_void_t*)src, (lds_void_t*)(st + 1024 * (wave + ATT_WAVES * i)),
+                                                 16, 0, 0);
+            }
         }
     };
-    issue(0);
+    issue(0, s_k);
+    if (ntile > 1) issue(1, s_k + TILE_BYTES);
 
     // Q fragments (B operand of S^T = K Q^T): head hq, dims 32*ks + 8*g .. +8
     bf16x8_t qf[D_ROW / 32];
@@ -134,55 +199,76 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
             qf[ks] = bf16x8_t{};
         }
     }
+    // consume the query loads here, so no wait for them lands inside the tile loop
+#pragma unroll
+    for (int ks = 0; ks < D_ROW / 32; ++ks) asm volatile("" : "+v"(qf[ks]));
     float m_run = -INFINITY, l_run = 0.f;
     f32x4_t o[D_LAT / 16];
 #pragma unroll
     for (int t = 0; t < D_LAT / 16; ++t) o[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+    // K operand of (row 16 mt + c, piece 4 ks + g): slot low bits (4 (ks & 1) + g) ^ f(c),
+    // so one byte offset per ks parity, plus 128 B per pair of k-steps.
+    // V operand (transposing reads): lane j = 4e + q of group g reads tile row
+    // 4g + e (and 16 + 4g + e), dims 16 tt + 4q .. +3, i.e. piece 2tt + q/2,
+    // half q mod 2; the piece's low bits (2 (tt mod 4) + q/2) ^ f(row) give one
+    // offset per tt mod 4, plus 128 B per four tt (f(16 + r) = f(r)).
+    // Both are recomputed per tile from an opaque copy of the lane index, so the
+    // compiler keeps no per-stage copies of them across the loop.
+    struct Offs {
+        int k_even, k_odd, v_base, v_h, v_f;
+    };
+    auto offsets = [&]() {
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        const int cc = ln & 15, gg = ln >> 4, fc = piece_xor(cc);
+        const int e = cc >> 2, q = ln & 3;
+        return Offs{cc * ROW_BYTES + 16 * (gg ^ fc), cc * ROW_BYTES + 16 * ((4 + gg) ^ fc),
+                    (4 * gg + e) * ROW_BYTES + 8 * (q & 1), q >> 1, piece_xor(4 * gg + e)};
+    };
+    const int cnt_next = nj;   // this wave's loads of one tile
+
+    const uint32_t k_lds = lds_addr(s_k);
+    int stage = 0;   // t mod 3
     for (int t = 0; t < ntile; ++t) {
-        const int cur = t & 1;
         const int nr = (int)min((int64_t)ATT_CHUNK, p1 - (p0 + (int64_t)ATT_CHUNK * t));
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's loads of tile t have landed
-        __syncthreads();                                   // ... and every wave's
-        if (t + 1 < ntile) issue(t + 1);
-        const uint8_t* kt = s_k + cur * TILE_BYTES;
-        uint16_t* vt = reinterpret_cast<uint16_t*>(s_vt + cur * VT_BYTES);
-        // latent half transposed: each thread 4 pieces (row r, dims 8pc..8pc+7);
-        // the 32 lanes of a half-wave take the 32 rows of one piece, so one
-        // store instruction covers 32 consecutive K slots of 2 rows of V^T
-#pragma unroll
-        for (int jj = 0; jj < ATT_CHUNK * (D_LAT / 8) / ATT_THREADS; ++jj) {
-            const int pi = tid + ATT_THREADS * jj;
-            const int r = pi & (ATT_CHUNK - 1), pc = pi >> 5;
-            const u16x8_t v = *reinterpret_cast<const u16x8_t*>(kt + kslot(r, pc));
-            uint16_t* dst = vt + (8 * pc) * VT_STRIDE + pv_slot(r);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) dst[e * VT_STRIDE] = v[e];
+        // this wave's loads of tile t have landed (only tile t+1's may still be in flight) ...
+        if (t + 1 < ntile) {
+            if (cnt_next == 5) asm volatile("s_waitcnt vmcnt(5)" ::: "memory");
+            else asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+        } else {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         }
-        // operand of (row 16 mt + c, piece 4 ks + g): with x = (c / 2) mod 8 the
-        // slot is 4 (ks ^ (x / 4)) + (g ^ (x mod 4)), so one base per ks parity
+        // ... and every wave's; every wave is also done with tile t-1, whose stage tile t+2 reuses
+        wg_barrier();
+        const int stage2 = stage == 0 ? 2 : stage - 1;   // (t + 2) mod 3
+        if (t + 2 < ntile) issue(t + 2, s_k + stage2 * TILE_BYTES);
+        const uint32_t kt = k_lds + (uint32_t)(stage * TILE_BYTES);
+        stage = stage == 2 ? 0 : stage + 1;
+        const Offs of = offsets();
         f32x4_t sacc[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
         {
-            const int x = (c >> 1) & 7;
-            const uint8_t* ke = kt + c * (D_ROW * 2) + 16 * (g ^ (x & 3)) + 64 * (x >> 2);
-            const uint8_t* ko = kt + c * (D_ROW * 2) + 16 * (g ^ (x & 3)) - 64 * (x >> 2);
-            // operands one k-step ahead of the matrix cores
-            bf16x8_t kb[2][2];
-#pragma unroll
-            for (int mt = 0; mt < 2; ++mt)
-                kb[0][mt] = *reinterpret_cast<const bf16x8_t*>(ke + 16 * mt * (D_ROW * 2));
-#pragma unroll
-            for (int ks = 0; ks < D_ROW / 32; ++ks) {
-                if (ks + 1 < D_ROW / 32) {
-#pragma unroll
-                    for (int mt = 0; mt < 2; ++mt)
-                        kb[(ks + 1) & 1][mt] = *reinterpret_cast<const bf16x8_t*>(
-                            (((ks + 1) & 1) ? ko : ke) + 16 * mt * (D_ROW * 2) + 64 * (ks + 1));
-                }
+            // K operands SD k-steps ahead of the matrix cores
+            constexpr int SD = 2, KSN = D_ROW / 32;
+            const uint32_t ke = kt + of.k_even, ko = kt + of.k_odd;
+            bf16x8_t kb[SD + 1][2];
+            auto kload = [&](auto kc) {
+                constexpr int ks = decltype(kc)::value;
+                constexpr int off = 128 * (ks >> 1);
+                const uint32_t base = (ks & 1) ? ko : ke;
+                kb[ks % (SD + 1)][0] = lds_read128<off>(base);
+                kb[ks % (SD + 1)][1] = lds_read128<off + 16 * ROW_BYTES>(base);
+            };
+            static_for<0, SD>(kload);
+            static_for<0, KSN>([&](auto kc) {
+                constexpr int ks = decltype(kc)::value;
+                if constexpr (ks + SD < KSN) kload(std::integral_constant<int, ks + SD>{});
+                constexpr int after = 2 * ((ks + SD < KSN) ? SD : (KSN - 1 - ks));
+                lds_wait<after>(kb[ks % (SD + 1)][0], kb[ks % (SD + 1)][1]);
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt)
-                    sacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[ks & 1][mt], qf[ks], sacc[mt], 0, 0, 0);
-            }
+                    sacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[ks % (SD + 1)][mt], qf[ks], sacc[mt], 0, 0, 0);
+            });
         }
         // sacc[mt][i] = score of row 16*mt + 4*g + i for head hq
         float sc[2][4];
@@ -196,8 +282,7 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
                 sc[mt][i] = v;
                 cmax = fmaxf(cmax, v);
             }
-        cmax = fmaxf(cmax, __shfl_xor(cmax, 16));
-        cmax = fmaxf(cmax, __shfl_xor(cmax, 32));
+        cmax = allreduce_groups(cmax, [](float x, float y) { return fmaxf(x, y); });
         const float m_new = fmaxf(m_run, cmax);
         const float alpha = exp2f(m_run - m_new);
         bf16x8_t pa;
@@ -210,29 +295,45 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
                 psum += p;
                 pa[4 * mt + i] = (__bf16)p;
             }
-        psum += __shfl_xor(psum, 16);
-        psum += __shfl_xor(psum, 32);
+        psum = allreduce_groups(psum, [](float x, float y) { return x + y; });
         l_run = l_run * alpha + psum;
         m_run = m_new;
-        float al[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) al[i] = __shfl(alpha, 4 * g + i);
-        __syncthreads();   // transposed tile complete
+        // the softmax's cross-lane reads complete before the PV reads are issued
+        asm volatile("" : "+v"(l_run), "+v"(pa));
         // rescale the accumulators only when some head's running max moved
         if (__ballot(alpha != 1.0f)) {
+            float al[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) al[i] = __shfl(alpha, 4 * g + i);
 #pragma unroll
             for (int tt = 0; tt < D_LAT / 16; ++tt)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) o[tt][i] *= al[i];
         }
-        const uint16_t* vrow = &vt[c * VT_STRIDE + 8 * g];
-        bf16x8_t vb[2];
-        vb[0] = *reinterpret_cast<const bf16x8_t*>(vrow);
-#pragma unroll
-        for (int tt = 0; tt < D_LAT / 16; ++tt) {
-            if (tt + 1 < D_LAT / 16) vb[(tt + 1) & 1] = *reinterpret_cast<const bf16x8_t*>(vrow + 16 * (tt + 1) * VT_STRIDE);
-            o[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb[tt & 1], o[tt], 0, 0, 0);
-        }
+        // O += P V: B operand of dims 16 tt .. +15 = tile rows (4g + e, 16 + 4g + e)
+        // at dim 16 tt + c, read VD steps ahead; dims in the order tt = 4 a + be
+        // (be outer), so one address per be is live
+        constexpr int VD = 3, TTN = D_LAT / 16;
+        i16x4_t vv[VD + 1][2];
+        uint32_t voff[4];
+        auto vload = [&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            constexpr int tt = 4 * (i & 7) + (i >> 3);
+            if constexpr ((i & 7) == 0) voff[i >> 3] = kt + of.v_base + 16 * ((2 * (tt & 3) + of.v_h) ^ of.v_f);
+            vv[i % (VD + 1)][0] = lds_read_tr16<128 * (tt >> 2)>(voff[i >> 3]);
+            vv[i % (VD + 1)][1] = lds_read_tr16<128 * (tt >> 2) + 16 * ROW_BYTES>(voff[i >> 3]);
+        };
+        static_for<0, VD>(vload);
+        static_for<0, TTN>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            constexpr int tt = 4 * (i & 7) + (i >> 3);
+            if constexpr (i + VD < TTN) vload(std::integral_constant<int, i + VD>{});
+            constexpr int after = 2 * ((i + VD < TTN) ? VD : (TTN - 1 - i));
+            lds_wait<after>(vv[i % (VD + 1)][0], vv[i % (VD + 1)][1]);
+            bf16x8_t vop;
+            __builtin_memcpy(&vop, vv[i % (VD + 1)], 16);
+            o[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vop, o[tt], 0, 0, 0);
+        });
     }
     // o[tt][i] = unnormalised output of head h0 + 4*g + i, dim 16*tt + c
 #pragma unroll
@@ -286,14 +387,9 @@ __global__ __launch_bounds__(128) void attend_combine_kernel(AttendArgs a) {
     if (tid == 0) a.lse[bh] = (M + log2f(L)) * 0.69314718055994530942f;
 }
 
-constexpr size_t ATT_SMEM = 2 * (size_t)TILE_BYTES + 2 * (size_t)VT_BYTES + ATT_MAX_SPLIT_ROWS * sizeof(int32_t);
-
 hipError_t launch_attend(const AttendArgs& a, hipStream_t s) {
     dim3 grid((unsigned)a.splits, (unsigned)((a.H + ATT_HEADS - 1) / ATT_HEADS), (unsigned)a.B);
-    hipError_t e0 = hipFuncSetAttribute(reinterpret_cast<const void*>(attend_kernel),
-                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)ATT_SMEM);
-    if (e0 != hipSuccess) return e0;
-    hipLaunchKernelGGL(attend_kernel, grid, dim3(ATT_THREADS), ATT_SMEM, s, a);
+    hipLaunchKernelGGL(attend_kernel, grid, dim3(ATT_THREADS), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(attend_combine_kernel, dim3((unsigned)(a.B * a.H)), dim3(128), 0, s, a);
