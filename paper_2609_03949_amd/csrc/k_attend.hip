@@ -33,7 +33,11 @@ constexpr int ATT_THREADS = 64 * ATT_WAVES;  // 512
 constexpr int ROW_PIECES = D_ROW / 8;        // 72 pieces of 16 B per row
 constexpr int TILE_BYTES = ATT_CHUNK * D_ROW * 2;            // 36 KB
 constexpr int TILE_LOADS = TILE_BYTES / 1024;                // 36 loads of 1 KB
-constexpr int ATT_STAGES = 3;
+#ifndef ATT_STAGES_OVERRIDE
+constexpr int ATT_STAGES = 3;                // ring depth: tiles in flight = ATT_STAGES - 1
+#else
+constexpr int ATT_STAGES = ATT_STAGES_OVERRIDE;
+#endif
 constexpr int ROW_BYTES = D_ROW * 2;                         // 1152
 
 typedef __attribute__((address_space(3))) void lds_void_t;
@@ -54,6 +58,21 @@ __device__ __forceinline__ int32_t attended_row(const AttendArgs& a, int b, int6
 __device__ __forceinline__ int piece_xor(int r) { return 2 * ((r >> 1) & 3) + ((r >> 3) & 1); }
 
 __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// Wait until at most `tiles` tiles of this wave's direct loads (`per` = 4 or 5
+// loads each) are still in flight; `tiles` and `per` are wave-uniform.
+__device__ __forceinline__ void wait_tiles_behind(int tiles, int per) {
+    // any count below the true one is also safe (loads complete in order), only slower
+    switch (tiles * per) {
+        case 15: asm volatile("s_waitcnt vmcnt(15)" ::: "memory"); break;
+        case 12: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
+        case 10: asm volatile("s_waitcnt vmcnt(10)" ::: "memory"); break;
+        case 8: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+        case 5: asm volatile("s_waitcnt vmcnt(5)" ::: "memory"); break;
+        case 4: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
+        default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    }
+}
 
 // Compile-time loop: f(std::integral_constant<int, I>) for I = 0 .. N-1.
 template <int I, int N, typename F>
@@ -118,7 +137,8 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
     const int64_t N = a.k + a.W + nadm;
     const int64_t p0 = (int64_t)sp * a.rows_per_split;
     const int64_t p1 = min(N, p0 + a.rows_per_split);
-    float* po = a.part_o + ((int64_t)b * a.splits + sp) * a.H * D_LAT;
+    const int HG = (a.H + ATT_HEADS - 1) / ATT_HEADS;
+    float* po = a.part_o + (((int64_t)b * a.splits + sp) * HG + hg) * (ATT_HEADS * D_LAT);
     float* pml = a.part_ml + ((int64_t)b * a.splits + sp) * a.H * 2;
     if (p0 >= p1) {
         if (tid < ATT_HEADS) {
@@ -183,8 +203,10 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
             }
         }
     };
-    issue(0, s_k);
-    if (ntile > 1) issue(1, s_k + TILE_BYTES);
+    constexpr int PD = ATT_STAGES - 1;   // tiles issued ahead
+#pragma unroll
+    for (int t = 0; t < PD; ++t)
+        if (t < ntile) issue(t, s_k + t * TILE_BYTES);
 
     // Q fragments (B operand of S^T = K Q^T): head hq, dims 32*ks + 8*g .. +8
     bf16x8_t qf[D_ROW / 32];
@@ -229,22 +251,17 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
     const int cnt_next = nj;   // this wave's loads of one tile
 
     const uint32_t k_lds = lds_addr(s_k);
-    int stage = 0;   // t mod 3
+    int stage = 0;   // t mod ATT_STAGES
     for (int t = 0; t < ntile; ++t) {
         const int nr = (int)min((int64_t)ATT_CHUNK, p1 - (p0 + (int64_t)ATT_CHUNK * t));
-        // this wave's loads of tile t have landed (only tile t+1's may still be in flight) ...
-        if (t + 1 < ntile) {
-            if (cnt_next == 5) asm volatile("s_waitcnt vmcnt(5)" ::: "memory");
-            else asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-        } else {
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        }
-        // ... and every wave's; every wave is also done with tile t-1, whose stage tile t+2 reuses
+        // this wave's loads of tile t have landed (tiles t+1 .. t+PD-1 may still be in flight) ...
+        wait_tiles_behind(min(PD - 1, ntile - 1 - t), cnt_next);
+        // ... and every wave's; every wave is also done with tile t-1, whose stage tile t+PD reuses
         wg_barrier();
-        const int stage2 = stage == 0 ? 2 : stage - 1;   // (t + 2) mod 3
-        if (t + 2 < ntile) issue(t + 2, s_k + stage2 * TILE_BYTES);
+        const int stage_pd = stage == 0 ? ATT_STAGES - 1 : stage - 1;   // (t + PD) mod ATT_STAGES
+        if (t + PD < ntile) issue(t + PD, s_k + stage_pd * TILE_BYTES);
         const uint32_t kt = k_lds + (uint32_t)(stage * TILE_BYTES);
-        stage = stage == 2 ? 0 : stage + 1;
+        stage = stage == ATT_STAGES - 1 ? 0 : stage + 1;
         const Offs of = offsets();
         f32x4_t sacc[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
         {
@@ -335,56 +352,75 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
             o[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vop, o[tt], 0, 0, 0);
         });
     }
-    // o[tt][i] = unnormalised output of head h0 + 4*g + i, dim 16*tt + c
+    // o[tt][i] = unnormalised output of head h0 + 4*g + i, dim 16*tt + c; the
+    // partial is stored in that register order (one 1 KB store per tt and wave)
+    float* pw = po + (int64_t)wave * (D_LAT / 16) * 64 * 4;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int h = h0 + 4 * g + i;
-        if (h < a.H) {
-#pragma unroll
-            for (int tt = 0; tt < D_LAT / 16; ++tt) po[(int64_t)h * D_LAT + 16 * tt + c] = o[tt][i];
-        }
-    }
+    for (int tt = 0; tt < D_LAT / 16; ++tt) *reinterpret_cast<f32x4_t*>(pw + (tt * 64 + lane) * 4) = o[tt];
     if (g == 0 && hq < a.H) {
         pml[2 * hq] = m_run;
         pml[2 * hq + 1] = l_run;
     }
 }
 
-// Merge the splits of each (b, h) by log-sum-exp; bf16 output, natural-log lse.
+// Merge the splits of four heads by log-sum-exp; bf16 output, natural-log lse.
+// Block = (b, head group, wave, lane group g) of the attention kernel: heads
+// hb + i (i = 0..3) with hb = 128 hg + 16 wave + 4 g; thread j covers dims
+// 4j .. 4j+3 (tt = j / 4, lanes 16 g + 4 (j mod 4) .. +3 of the partials).
 __global__ __launch_bounds__(128) void attend_combine_kernel(AttendArgs a) {
-    const int bh = blockIdx.x;
-    const int b = bh / a.H, h = bh % a.H;
-    const int tid = threadIdx.x;
-    float M = -INFINITY;
-    for (int s = 0; s < a.splits; ++s) M = fmaxf(M, a.part_ml[(((int64_t)b * a.splits + s) * a.H + h) * 2]);
-    uint16_t* out = a.out + (int64_t)bh * D_LAT;
-    if (M == -INFINITY) {
-        for (int d = tid; d < D_LAT; d += 128) out[d] = 0;
-        if (tid == 0) a.lse[bh] = -INFINITY;
-        return;
-    }
-    float L = 0.f;
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    const int HG = (a.H + ATT_HEADS - 1) / ATT_HEADS;
+    const int q = blockIdx.x % 32, hg = (blockIdx.x / 32) % HG, b = blockIdx.x / (32 * HG);
+    const int wave = q >> 2, g = q & 3;
+    const int hb = hg * ATT_HEADS + 16 * wave + 4 * g;
+    if (hb >= a.H) return;
+    const int j = threadIdx.x, tt = j >> 2, c0 = 4 * (j & 3);
+    float M[4], L[4] = {0.f, 0.f, 0.f, 0.f};
+    float acc[4][4] = {};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) M[i] = -INFINITY;
     for (int s = 0; s < a.splits; ++s) {
-        const int64_t base = ((int64_t)b * a.splits + s) * a.H + h;
-        const float ms = a.part_ml[base * 2];
-        if (ms == -INFINITY) continue;
-        const float w = exp2f(ms - M);
-        L += w * a.part_ml[base * 2 + 1];
-        const float4 v = *reinterpret_cast<const float4*>(a.part_o + base * D_LAT + 4 * tid);
-        acc[0] += w * v.x;
-        acc[1] += w * v.y;
-        acc[2] += w * v.z;
-        acc[3] += w * v.w;
+        const float* ml = a.part_ml + (((int64_t)b * a.splits + s) * a.H) * 2;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (hb + i < a.H) M[i] = fmaxf(M[i], ml[2 * (hb + i)]);
     }
-    const float inv = 1.0f / L;
-    ushort4 r;
-    r.x = f32_to_bf16_rne(acc[0] * inv);
-    r.y = f32_to_bf16_rne(acc[1] * inv);
-    r.z = f32_to_bf16_rne(acc[2] * inv);
-    r.w = f32_to_bf16_rne(acc[3] * inv);
-    *reinterpret_cast<ushort4*>(out + 4 * tid) = r;
-    if (tid == 0) a.lse[bh] = (M + log2f(L)) * 0.69314718055994530942f;
+    for (int s = 0; s < a.splits; ++s) {
+        const float* ml = a.part_ml + (((int64_t)b * a.splits + s) * a.H) * 2;
+        float w[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float ms = (hb + i < a.H) ? ml[2 * (hb + i)] : -INFINITY;
+            w[i] = (ms == -INFINITY) ? 0.f : exp2f(ms - M[i]);
+            if (ms != -INFINITY) L[i] += w[i] * ml[2 * (hb + i) + 1];
+        }
+        const float* src = a.part_o + (((int64_t)b * a.splits + s) * HG + hg) * (ATT_HEADS * D_LAT) +
+                           (int64_t)wave * (D_LAT / 16) * 64 * 4 + (tt * 64 + 16 * g + c0) * 4;
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) {
+            const f32x4_t v = *reinterpret_cast<const f32x4_t*>(src + 4 * cc);
+            // a split without rows never wrote its partial: weight 0 must not touch it
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[cc][i] += (w[i] > 0.f) ? w[i] * v[i] : 0.f;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int h = hb + i;
+        if (h >= a.H) continue;
+        uint16_t* out = a.out + ((int64_t)b * a.H + h) * D_LAT + 4 * j;
+        ushort4 r{0, 0, 0, 0};
+        if (M[i] != -INFINITY) {
+            const float inv = 1.0f / L[i];
+            r.x = f32_to_bf16_rne(acc[0][i] * inv);
+            r.y = f32_to_bf16_rne(acc[1][i] * inv);
+            r.z = f32_to_bf16_rne(acc[2][i] * inv);
+            r.w = f32_to_bf16_rne(acc[3][i] * inv);
+        }
+        *reinterpret_cast<ushort4*>(out) = r;
+        if (j == 0)
+            a.lse[(int64_t)b * a.H + h] =
+                (M[i] == -INFINITY) ? -INFINITY : (M[i] + log2f(L[i])) * 0.69314718055994530942f;
+    }
 }
 
 hipError_t launch_attend(const AttendArgs& a, hipStream_t s) {
@@ -392,7 +428,8 @@ hipError_t launch_attend(const AttendArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(attend_kernel, grid, dim3(ATT_THREADS), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(attend_combine_kernel, dim3((unsigned)(a.B * a.H)), dim3(128), 0, s, a);
+    const unsigned hgs = (unsigned)((a.H + ATT_HEADS - 1) / ATT_HEADS);
+    hipLaunchKernelGGL(attend_combine_kernel, dim3((unsigned)a.B * hgs * 32u), dim3(128), 0, s, a);
     return hipGetLastError();
 }
 

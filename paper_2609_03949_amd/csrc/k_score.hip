@@ -10,278 +10,253 @@
 // loaded straight from global memory in MFMA operand layout, so each lane
 // issues 16-byte loads of one row.  The heads maximum is taken in registers
 // (4 heads per lane per tile, then two cross-lane steps).
+#include <type_traits>
+
 #include "vkv_internal.h"
 
 namespace vkv {
 
 // ----------------------------------------------------------- query prep
 
-// Stage 1: w[b,h,j] = sum_i P[j,i] q_lat[b,h,i] (fp64, i ascending) and the
-// query digest qt[b,h,off+j] = RNE_bf16(w).  A block owns 32 basis rows and
-// 16 heads; each thread runs two independent fp64 chains (two heads of one
-// basis row).  The i axis is walked in chunks of 128 held in LDS as fp64 (P^T
-// and the queries, converted once), and the next chunk is fetched into
-// registers while the current one is consumed.  Block (0,0,b) also clears the
-// step state of sequence b.
-constexpr int QP_HEADS = 16;
-constexpr int QP_ROWS = 32;
-constexpr int QP_IC = 128;
+// Query prep, one kernel: w[b,h,j] = sum_i P[j,i] q_lat[b,h,i] (fp64, i
+// ascending), the query digest qt[b,h,off+j] = RNE_bf16(w) and the rope half of
+// qt, Nq[b,h] = ||q_lat||^2 (fp64, i ascending), and the head's certificate
+// scalars.  Each of w and Nq is a sequential chain of 512 fp64 FMAs; a block
+// owns QH heads of one sequence and all r basis rows, and its threads run 4
+// projection chains each (basis rows 2jp, 2jp+1 x heads 2hp, 2hp+1) while
+// wave 0 also runs the Nq chains.  P and the queries stay bf16 in LDS (direct
+// loads, a chunk of the i axis at a time) and are widened to fp64 in
+// registers: fp64 operands from LDS would otherwise bound the loop.  Block
+// (0,b) also clears the step state of sequence b.
+constexpr int QP_THREADS = 256;
+constexpr int QP_PBYTES = 65536;   // LDS for a chunk of P (bf16)
 
-__global__ __launch_bounds__(256) void qprep_project_kernel(QprepArgs a) {
-    __shared__ __align__(16) double s_p[QP_IC][QP_ROWS];     // P^T chunk: [i][j]
-    __shared__ __align__(16) double s_q[QP_IC][QP_HEADS];    // query chunk: [i][head]
-    const int b = blockIdx.z;
-    const int tid = threadIdx.x;
-    if (blockIdx.x == 0 && blockIdx.y == 0) {
-        if (tid < SQ_WORDS) a.seq[b * SQ_WORDS + tid] = (tid == SQ_KMIN) ? 0xFFFFFFFFu : 0u;
-        for (int i = tid; i < 2 * HIST_BINS; i += 256) a.hist[(int64_t)b * 2 * HIST_BINS + i] = 0u;
-    }
-    if (a.r == 0 || !(a.mode & 2)) return;
-    const int j0 = QP_ROWS * blockIdx.x;
-    const int jn = min(QP_ROWS, a.r - j0);
-    const int h0 = QP_HEADS * blockIdx.y;
-    // chunk c: P rows j0.. (lane row = p & 31, piece p >> 5) and query rows
-    // h0.. (head = p & 15, piece p >> 4), 16-byte pieces of 8 i each
-    u16x8_t pv[2], qv;
-    auto fetch = [&](int c) {
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-            const int p = tid + 256 * jj;
-            const int row = p & 31, pc = p >> 5;
-            pv[jj] = (row < jn) ? *reinterpret_cast<const u16x8_t*>(a.P + (int64_t)(j0 + row) * D_LAT + QP_IC * c + 8 * pc)
-                                : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
-        }
-        const int hh = tid & 15, pc = tid >> 4;
-        qv = (h0 + hh < a.H) ? *reinterpret_cast<const u16x8_t*>(a.q_lat + ((int64_t)b * a.H + h0 + hh) * D_LAT + QP_IC * c + 8 * pc)
-                             : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
-    };
-    auto park = [&]() {
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-            const int p = tid + 256 * jj;
-            const int row = p & 31, pc = p >> 5;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) s_p[8 * pc + e][row] = (double)bf16_to_f32(pv[jj][e]);
-        }
-        const int hh = tid & 15, pc = tid >> 4;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) s_q[8 * pc + e][hh] = (double)bf16_to_f32(qv[e]);
-    };
-    const int jl = tid & 31, hg = tid >> 5;    // heads 2 hg, 2 hg + 1
-    double acc0 = 0.0, acc1 = 0.0;
-    fetch(0);
-    park();
-    __syncthreads();
-    for (int c = 0; c < D_LAT / QP_IC; ++c) {
-        const bool more = c + 1 < D_LAT / QP_IC;
-        if (more) fetch(c + 1);
-#pragma unroll 8
-        for (int i = 0; i < QP_IC; ++i) {
-            const double p = s_p[i][jl];
-            const double2 q2 = *reinterpret_cast<const double2*>(&s_q[i][2 * hg]);
-            acc0 = fma(p, q2.x, acc0);
-            acc1 = fma(p, q2.y, acc1);
-        }
-        __syncthreads();
-        if (more) {
-            park();
-            __syncthreads();
-        }
-    }
-    if (jl >= jn) return;
-    const int off = (a.mode & 1) ? D_ROPE : 0;
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-        const int h = h0 + 2 * hg + t;
-        if (h >= a.H) continue;
-        const int64_t bh = (int64_t)b * a.H + h;
-        const double v = t ? acc1 : acc0;
-        a.wproj[bh * a.r + j0 + jl] = v;
-        a.qt[bh * a.n + off + j0 + jl] = f64_to_bf16_rne(v);
-    }
+__host__ __device__ inline int qp_heads(int r) {
+    if (r <= 0) return 16;
+    int hb = (1024 / r) & ~1;
+    return hb < 2 ? 2 : (hb > 16 ? 16 : hb);
+}
+__host__ __device__ inline int qp_chunk(int r) {   // a power of two dividing 512
+    int ic = D_LAT;
+    while (ic > 8 && ic * r * 2 > QP_PBYTES) ic >>= 1;
+    return ic;
 }
 
-// Stage 2 (16 heads per wave): certificate scalars of each head, each an fp32
-// upper bound (Lemma (Index certificate) plus the bf16 rounding of the stored
-// sketch; fixed fp64 evaluation order, the same as the oracle's):
-//   a_h >= sqrt(q^T (I - P^T P) q),  n_h >= ||qd_h||,  e_h >= ||qd_h - P q||
-// plus ||qt_h|| for the scorer's error bound, and the rope half of qt.  The
-// wave first stages its heads' q_lat, projections and digests in LDS (all
-// loads in flight); then lane 4*hl + t runs sum t of head hl sequentially:
-// t=0 ||q||^2, t=1 ||w||^2, t=2 ||qd - w||^2, t=3 ||qd||^2.
-constexpr int QF_HEADS = 16;
-constexpr int QF_RMAX = 512;
+// slot of 16-byte piece ib (8 i) of LDS row j: XOR-swizzled so that the 16
+// rows 2jp (or 2jp+1, or 0..15) read by 16 lanes at one ib fall into distinct
+// bank groups
+__device__ __forceinline__ int qp_slot(int j, int ib, int per_row) {
+    const int m = (per_row < 16 ? per_row : 16) - 1;
+    return j * per_row + (ib ^ ((j >> 1) & m));
+}
 
-__global__ __launch_bounds__(64) void qprep_finish_kernel(QprepArgs a) {
-    __shared__ __align__(16) uint16_t s_ql[QF_HEADS][D_LAT];   // 16 KB
-    __shared__ __align__(16) uint16_t s_qd[QF_HEADS][QF_RMAX]; // 16 KB
-    __shared__ __align__(16) double s_w[QF_HEADS][QF_RMAX];    // 64 KB
-    const int lane = threadIdx.x;
-    const int hl = lane >> 2, t = lane & 3;
-    const int64_t bh0 = (int64_t)blockIdx.x * QF_HEADS;
-    const int64_t nbh = (int64_t)a.B * a.H;
-    const int off = (a.mode & 1) ? D_ROPE : 0;
-    const int rd = (a.mode & 2) ? a.r : 0;
-    {
-        // q_lat rows: 16 heads x 64 pieces; digests: 16 heads x rd/8 pieces
-        constexpr int PER = QF_HEADS * (D_LAT / 8) / 64;
-        u16x8_t v[PER];
-#pragma unroll
-        for (int j = 0; j < PER; ++j) {
-            const int p = lane + 64 * j;
-            const int h = p >> 6, pc = p & 63;
-            v[j] = (bh0 + h < nbh) ? *reinterpret_cast<const u16x8_t*>(a.q_lat + (bh0 + h) * D_LAT + 8 * pc)
-                                   : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
-        }
-#pragma unroll
-        for (int j = 0; j < PER; ++j) {
-            const int p = lane + 64 * j;
-            *reinterpret_cast<u16x8_t*>(&s_ql[p >> 6][8 * (p & 63)]) = v[j];
-        }
-        // digests (16 B = 8 values) and projections (16 B = 2 values), 4 of
-        // each per lane per round, loads in flight together
-        const int r8 = rd / 8, r2 = rd / 2;
-        for (int p0 = 0; p0 < QF_HEADS * r8; p0 += 256) {
-            u16x8_t d[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int p = p0 + lane + 64 * j;
-                const int h = p / max(r8, 1), pc = p % max(r8, 1);
-                d[j] = (p < QF_HEADS * r8 && bh0 + h < nbh)
-                           ? *reinterpret_cast<const u16x8_t*>(a.qt + (bh0 + h) * a.n + off + 8 * pc)
-                           : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
-            }
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int p = p0 + lane + 64 * j;
-                if (p < QF_HEADS * r8) *reinterpret_cast<u16x8_t*>(&s_qd[p / r8][8 * (p % r8)]) = d[j];
-            }
-        }
-        for (int p0 = 0; p0 < QF_HEADS * r2; p0 += 512) {
-            double2 wv[8];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int p = p0 + lane + 64 * j;
-                const int h = p / max(r2, 1), pc = p % max(r2, 1);
-                wv[j] = (p < QF_HEADS * r2 && bh0 + h < nbh)
-                            ? *reinterpret_cast<const double2*>(a.wproj + (bh0 + h) * a.r + 2 * pc)
-                            : make_double2(0.0, 0.0);
-            }
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int p = p0 + lane + 64 * j;
-                if (p < QF_HEADS * r2) *reinterpret_cast<double2*>(&s_w[p / r2][2 * (p % r2)]) = wv[j];
-            }
-        }
+__global__ __launch_bounds__(QP_THREADS) void qprep_project_kernel(QprepArgs a) {
+    __shared__ __align__(16) uint8_t s_p[QP_PBYTES];            // P chunk, [j][i] bf16, swizzled
+    __shared__ __align__(16) uint8_t s_q[16 * D_LAT * 2];       // query chunk, [h][i] bf16
+    const int b = blockIdx.y;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    if (blockIdx.x == 0) {
+        if (tid < SQ_WORDS) a.seq[b * SQ_WORDS + tid] = (tid == SQ_KMIN) ? 0xFFFFFFFFu : 0u;
+        for (int i = tid; i < 2 * HIST_BINS; i += QP_THREADS) a.hist[(int64_t)b * 2 * HIST_BINS + i] = 0u;
     }
-    __syncthreads();
-    const int64_t bh = bh0 + hl;
-    const bool have = bh < nbh;
-    const int64_t bhc = have ? bh : 0;
-    const int b = (int)(bhc / a.H);
-    uint16_t* qt = a.qt + bhc * a.n;
-    const double* w = &s_w[hl][0];
-    // rope half of qt: 8 pieces of 16 B per head, 4 lanes per head
-    if ((a.mode & 1) && have) {
-        const u16x8_t* src = reinterpret_cast<const u16x8_t*>(a.q_rope + bhc * D_ROPE);
-        u16x8_t* dst = reinterpret_cast<u16x8_t*>(qt);
-        dst[t] = src[t];
-        dst[t + 4] = src[t + 4];
-    }
-    double acc = 0.0;
-    if (have) {
-        if (t == 0) {
-#pragma unroll 4
-            for (int p = 0; p < D_LAT / 8; ++p) {
-                const u16x8_t v = *reinterpret_cast<const u16x8_t*>(&s_ql[hl][8 * p]);
+    const int r = (a.mode & 2) ? a.r : 0;
+    const int HB = qp_heads(r), IC = qp_chunk(r), PR = IC / 8;
+    const int hb0 = HB * blockIdx.x;
+    const bool proj = tid < HB * r / 4;   // threads whose chains are stored
+    const int rp = r > 0 ? r / 2 : 1;
+    const int jp = tid % rp, hp = tid / rp;
+    const int hpc = min(hp, HB / 2 - 1);  // the others repeat valid chains
+    const bool nqc = tid < HB;
+    double a00 = 0.0, a10 = 0.0, a01 = 0.0, a11 = 0.0, anq = 0.0;
+    auto wide = [](uint32_t w, int hi) { return (double)__uint_as_float(hi ? (w & 0xFFFF0000u) : (w << 16)); };
+    for (int c = 0; c < D_LAT / IC; ++c) {
+        // chunk c into LDS by direct loads: P pieces (row j, 8 i), then query pieces (head h, 8 i)
+        const int np = r * PR, nq = HB * PR;
+        for (int s0 = 64 * wave; s0 < np; s0 += QP_THREADS) {
+            const int sl = s0 + lane;   // np is a multiple of 64
+            const int j = sl / PR, ib = (sl % PR) ^ ((j >> 1) & ((PR < 16 ? PR : 16) - 1));
+            __builtin_amdgcn_global_load_lds(
+                (__attribute__((address_space(1))) void*)(a.P + (int64_t)j * D_LAT + IC * c + 8 * ib),
+                (__attribute__((address_space(3))) void*)(s_p + 16 * s0), 16, 0, 0);
+        }
+        for (int p = tid; p < nq; p += QP_THREADS) {
+            const int h = p / PR, ib = p % PR;
+            u16x8_t v = u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+            if (hb0 + h < a.H)
+                v = *reinterpret_cast<const u16x8_t*>(a.q_lat + ((int64_t)b * a.H + hb0 + h) * D_LAT + IC * c + 8 * ib);
+            *reinterpret_cast<u16x8_t*>(s_q + 16 * qp_slot(h, ib, PR)) = v;
+        }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        // branch-free inner loops (wave-uniform choice): wave 0 also runs the
+        // Nq chains (lanes 0..15 own them; the others repeat them)
+        auto run = [&](auto with_proj, auto with_nq) {
+            constexpr bool WP = decltype(with_proj)::value, WN = decltype(with_nq)::value;
+            const u32x4_t* PP = reinterpret_cast<const u32x4_t*>(s_p);
+            const u32x4_t* Q = reinterpret_cast<const u32x4_t*>(s_q);
+            const int sj0 = 2 * jp, sj1 = 2 * jp + 1, sh0 = 2 * hpc, sh1 = 2 * hpc + 1, sn = lane & 15;
+#pragma unroll 2
+            for (int ib = 0; ib < PR; ++ib) {
+                u32x4_t p0{}, p1{}, q0{}, q1{}, qn{};
+                if constexpr (WP) {
+                    p0 = PP[qp_slot(sj0, ib, PR)];
+                    p1 = PP[qp_slot(sj1, ib, PR)];
+                    q0 = Q[qp_slot(sh0, ib, PR)];
+                    q1 = Q[qp_slot(sh1, ib, PR)];
+                }
+                if constexpr (WN) qn = Q[qp_slot(sn, ib, PR)];
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
-                    const double x = (double)bf16_to_f32(v[e]);
-                    acc = fma(x, x, acc);
-                }
-            }
-        } else if (t == 1) {
-            for (int j0 = 0; j0 < rd; j0 += 8) {
-                double wv[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) wv[e] = w[j0 + e];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) acc = fma(wv[e], wv[e], acc);
-            }
-        } else {
-            for (int j0 = 0; j0 < rd; j0 += 8) {
-                double wv[8];
-                if (t == 2) {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) wv[e] = w[j0 + e];
-                }
-                const u16x8_t dv = *reinterpret_cast<const u16x8_t*>(&s_qd[hl][j0]);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const double d = (double)bf16_to_f32(dv[e]);
-                    if (t == 2) {
-                        const double ee = d - wv[e];
-                        acc = fma(ee, ee, acc);
-                    } else {
-                        acc = fma(d, d, acc);
+                    if constexpr (WP) {
+                        const double x0 = wide(p0[e >> 1], e & 1), x1 = wide(p1[e >> 1], e & 1);
+                        const double y0 = wide(q0[e >> 1], e & 1), y1 = wide(q1[e >> 1], e & 1);
+                        a00 = fma(x0, y0, a00);
+                        a10 = fma(x1, y0, a10);
+                        a01 = fma(x0, y1, a01);
+                        a11 = fma(x1, y1, a11);
+                    }
+                    if constexpr (WN) {
+                        const double x = wide(qn[e >> 1], e & 1);
+                        anq = fma(x, x, anq);
                     }
                 }
             }
+        };
+        using T_ = std::true_type;
+        using F_ = std::false_type;
+        if (r > 0) {
+            if (wave == 0) run(T_{}, T_{});
+            else run(T_{}, F_{});
+        } else if (wave == 0) {
+            run(F_{}, T_{});
+        }
+        __syncthreads();
+    }
+    // certificate scalars of each head (fp32 upper bounds; Lemma (Index
+    // certificate) plus the bf16 rounding of the stored sketch; fixed fp64
+    // evaluation order, the same as the oracle's):
+    //   a_h >= sqrt(q^T (I - P^T P) q),  n_h >= ||qd_h||,  e_h >= ||qd_h - P q||
+    // plus ||qt_h|| for the scorer's error bound.  w and Nq go through LDS (the
+    // P chunk is free); lane 4 hl + t of wave 0 runs sum t of head hl:
+    // t=0 Nq, t=1 ||w||^2, t=2 ||qd - w||^2, t=3 ||qd||^2 (j ascending).
+    const int off = (a.mode & 1) ? D_ROPE : 0;
+    double* s_w = reinterpret_cast<double*>(s_p);   // [HB][r] w, [HB][r] qd, then Nq[HB]
+    double* s_d = s_w + HB * r;
+    double* s_nq = s_d + HB * r;
+    if (nqc) s_nq[tid] = anq;
+    if (proj) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            const int hl = 2 * hp + t;
+            const int h = hb0 + hl;
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int j = 2 * jp + u;
+                const double v = t ? (u ? a11 : a01) : (u ? a10 : a00);
+                const uint16_t d = f64_to_bf16_rne(v);
+                s_w[hl * r + j] = v;
+                s_d[hl * r + j] = (double)bf16_to_f32(d);
+                if (h < a.H) a.qt[((int64_t)b * a.H + h) * a.n + off + j] = d;
+            }
+        }
+    }
+    __syncthreads();
+    if (wave != 0) return;
+    const int hl = lane >> 2, t = lane & 3;
+    const int h = hb0 + hl;
+    const bool have = hl < HB && h < a.H;
+    const int64_t bhc = (int64_t)b * a.H + (have ? h : 0);
+    // rope half of qt (8 pieces of 16 B per head, 4 lanes per head) and
+    // ||q_rope||^2 (an upper-bound input only; order irrelevant)
+    double r2 = 0.0;
+    if ((a.mode & 1) && have) {
+        const u16x8_t* src = reinterpret_cast<const u16x8_t*>(a.q_rope + bhc * D_ROPE);
+        u16x8_t* dst = reinterpret_cast<u16x8_t*>(a.qt + bhc * a.n);
+        const u16x8_t v0 = src[t], v1 = src[t + 4];
+        dst[t] = v0;
+        dst[t + 4] = v1;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const double x0 = (double)bf16_to_f32(v0[e]), x1 = (double)bf16_to_f32(v1[e]);
+            r2 += x0 * x0 + x1 * x1;
+        }
+    }
+    r2 += __shfl_xor(r2, 1);
+    r2 += __shfl_xor(r2, 2);
+    double acc = 0.0;
+    if (have) {
+        const double* w = s_w + hl * r;
+        const double* dq = s_d + hl * r;
+        if (t == 0) {
+            acc = s_nq[hl];
+        } else if (t == 1) {
+            for (int j = 0; j < r; ++j) acc = fma(w[j], w[j], acc);
+        } else if (t == 2) {
+            for (int j = 0; j < r; ++j) {
+                const double ee = dq[j] - w[j];
+                acc = fma(ee, ee, acc);
+            }
+        } else {
+            for (int j = 0; j < r; ++j) acc = fma(dq[j], dq[j], acc);
         }
     }
     const int base = lane & ~3;
     const double Nq = __shfl(acc, base + 0), Nw = __shfl(acc, base + 1);
     const double Ne = __shfl(acc, base + 2), Nd = __shfl(acc, base + 3);
-    // ||q_rope||^2 (an upper-bound input only; order irrelevant)
-    double r2 = 0.0;
-    if ((a.mode & 1) && have) {
-        for (int i = t; i < D_ROPE; i += 4) {
-            const double v = (double)bf16_to_f32(a.q_rope[bhc * D_ROPE + i]);
-            r2 += v * v;
-        }
-    }
-    r2 += __shfl_xor(r2, 1);
-    r2 += __shfl_xor(r2, 2);
-    float ah = 0.f, eh = 0.f, nh = 0.f, qn = 0.f;
     if (t == 0 && have) {
         const double G = CERT_G;
-        const double Dm = G * (double)ru_sqrt_f32((double)rd * Nq);
+        const double Dm = G * (double)ru_sqrt_f32((double)r * Nq);
         const double sw = (double)ru_sqrt_f32(Nw);
         const double X = ((Nq - Nw) + G * (Nq + Nw)) + (2.0 * Dm) * sw;
-        ah = ru_sqrt_f32((X > 0.0 ? X : 0.0) * (1.0 + G));
-        eh = ru_f32((double)ru_sqrt_f32(Ne) * (1.0 + G) + Dm);
-        nh = ru_sqrt_f32(Nd * (1.0 + G));
-        qn = ru_sqrt_f32((r2 + Nd) * (1.0 + 0x1p-30));
+        const float ah = ru_sqrt_f32((X > 0.0 ? X : 0.0) * (1.0 + G));
+        const float eh = ru_f32((double)ru_sqrt_f32(Ne) * (1.0 + G) + Dm);
+        const float nh = ru_sqrt_f32(Nd * (1.0 + G));
+        const float qn = ru_sqrt_f32((r2 + Nd) * (1.0 + 0x1p-30));
         reinterpret_cast<float4*>(a.hsc)[bhc] = make_float4(ah, nh, eh, qn);
     }
-    // per-sequence maxima (all values are >= 0, so float order = bit order):
-    // reduced over the wave's heads first when they all belong to one sequence
-    const int64_t bl = min(bh0 + QF_HEADS, nbh) - 1;
-    const bool one_seq = (bh0 / a.H) == (bl / a.H);
-    if (one_seq) {
-        for (int o = 4; o < 64; o <<= 1) {
-            ah = fmaxf(ah, __shfl_xor(ah, o));
-            eh = fmaxf(eh, __shfl_xor(eh, o));
-            nh = fmaxf(nh, __shfl_xor(nh, o));
-            qn = fmaxf(qn, __shfl_xor(qn, o));
-        }
+}
+
+// Per-sequence maxima of the head scalars (a, n, e, ||qt||), for the error
+// bounds of the scorer and the selection: computed by wave 0 of the first
+// block of each sequence in the scorer launch (the query prep of the step has
+// finished and cleared the words); all values are >= 0.
+__device__ __forceinline__ void store_head_maxima(const ScoreArgs& a, int b, int lane) {
+    float4 m = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int h = lane; h < a.H; h += 64) {
+        const float4 v = reinterpret_cast<const float4*>(a.hsc)[(int64_t)b * a.H + h];
+        m = make_float4(fmaxf(m.x, v.x), fmaxf(m.y, v.y), fmaxf(m.z, v.z), fmaxf(m.w, v.w));
     }
-    if (t == 0 && have && (!one_seq || hl == 0)) {
+    for (int o = 32; o > 0; o >>= 1) {
+        m.x = fmaxf(m.x, __shfl_xor(m.x, o));
+        m.y = fmaxf(m.y, __shfl_xor(m.y, o));
+        m.z = fmaxf(m.z, __shfl_xor(m.z, o));
+        m.w = fmaxf(m.w, __shfl_xor(m.w, o));
+    }
+    if (lane == 0) {
         uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-        atomicMax(sq + SQ_QMAX, __float_as_uint(qn));
-        atomicMax(sq + SQ_AMAX, __float_as_uint(ah));
-        atomicMax(sq + SQ_NMAX, __float_as_uint(nh));
-        atomicMax(sq + SQ_EMAX, __float_as_uint(eh));
+        sq[SQ_AMAX] = __float_as_uint(m.x);
+        sq[SQ_NMAX] = __float_as_uint(m.y);
+        sq[SQ_EMAX] = __float_as_uint(m.z);
+        sq[SQ_QMAX] = __float_as_uint(m.w);
+    }
+}
+
+// maxima of (a, n, e) over the head scalars staged in LDS
+__device__ __forceinline__ void staged_head_maxima(const float4* s_hs, int n, float& amax, float& nmax, float& emax) {
+    amax = nmax = emax = 0.f;
+    for (int i = 0; i < n; ++i) {
+        const float4 v = s_hs[i];
+        amax = fmaxf(amax, v.x);
+        nmax = fmaxf(nmax, v.y);
+        emax = fmaxf(emax, v.z);
     }
 }
 
 hipError_t launch_qprep(const QprepArgs& a, hipStream_t s) {
-    int jt = (a.r > 0 && (a.mode & 2)) ? (a.r + QP_ROWS - 1) / QP_ROWS : 1;
-    dim3 g1(jt, (a.H + QP_HEADS - 1) / QP_HEADS, a.B);
-    hipLaunchKernelGGL(qprep_project_kernel, g1, dim3(256), 0, s, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(qprep_finish_kernel, dim3((a.B * a.H + QF_HEADS - 1) / QF_HEADS), dim3(64), 0, s, a);
+    const int r = (a.mode & 2) ? a.r : 0;
+    dim3 g1((a.H + qp_heads(r) - 1) / qp_heads(r), a.B);
+    hipLaunchKernelGGL(qprep_project_kernel, g1, dim3(QP_THREADS), 0, s, a);
     return hipGetLastError();
 }
 
@@ -368,6 +343,7 @@ __global__ __launch_bounds__(256, 2) void score_kernel(ScoreArgs a) {
             s_hs[h] = reinterpret_cast<const float4*>(a.hsc)[(int64_t)b * a.H + (h % a.H)];
         __syncthreads();
     }
+    if (blockIdx.x == 0 && threadIdx.x < 64) store_head_maxima(a, b, threadIdx.x);
     const int64_t r0 = ((int64_t)blockIdx.x * 4 + wave) * (16 * SCORE_TPW);
     if (r0 >= a.A) return;
     const int64_t rend = min(a.A, r0 + (int64_t)(16 * SCORE_TPW));
@@ -384,11 +360,7 @@ __global__ __launch_bounds__(256, 2) void score_kernel(ScoreArgs a) {
     }
     const uint16_t* xb = a.x + (int64_t)b * a.xbs;
     float amax = 0.f, nmax = 0.f, emax = 0.f;
-    if (UB) {
-        amax = __uint_as_float(sq[SQ_AMAX]);
-        nmax = __uint_as_float(sq[SQ_NMAX]);
-        emax = __uint_as_float(sq[SQ_EMAX]);
-    }
+    if (UB) staged_head_maxima(s_hs, 16 * HT, amax, nmax, emax);
     TileOut to{-INFINITY, INFINITY, 0.f, 0.f};
     const int64_t rlast = rend - 1;
 
@@ -478,6 +450,7 @@ __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
             s_hs[h] = reinterpret_cast<const float4*>(a.hsc)[(int64_t)b * a.H + (h % a.H)];
         __syncthreads();
     }
+    if (blockIdx.x == 0 && threadIdx.x < 64) store_head_maxima(a, b, threadIdx.x);
     const int64_t r0 = ((int64_t)blockIdx.x * 4 + wave) * (16 * SCORE_TPW);
     if (r0 >= a.A) return;
     const int64_t rend = min(a.A, r0 + (int64_t)(16 * SCORE_TPW));
@@ -486,11 +459,7 @@ __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
     const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
     const uint16_t* xb = a.x + (int64_t)b * a.xbs;
     float amax = 0.f, nmax = 0.f, emax = 0.f;
-    if (UB) {
-        amax = __uint_as_float(sq[SQ_AMAX]);
-        nmax = __uint_as_float(sq[SQ_NMAX]);
-        emax = __uint_as_float(sq[SQ_EMAX]);
-    }
+    if (UB) staged_head_maxima(s_hs, 16 * HT, amax, nmax, emax);
     TileOut to{-INFINITY, INFINITY, 0.f, 0.f};
     for (int64_t t0 = r0; t0 < rend; t0 += 16) {
         const int64_t row = t0 + c;
@@ -609,6 +578,7 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
     uint8_t* wbase = smem + wave * Gm::WAVE;
     float* s_res = reinterpret_cast<float*>(wbase + NST * STAGE);
     // block span [bs0, bs1); this wave's tile j covers rows r0 + 16 TST j + [0, 16)
+    if (blockIdx.x == 0 && threadIdx.x < 64) store_head_maxima(a, b, threadIdx.x);
     const int64_t bs0 = (int64_t)blockIdx.x * STREAM_WAVES * 16 * tpw;
     if (bs0 >= a.A) return;
     const int64_t bs1 = min(a.A, bs0 + (int64_t)STREAM_WAVES * 16 * tpw);

@@ -113,7 +113,6 @@ static WsLayout layout(const vkv_step* st, int64_t k, int64_t cap) {
     const int64_t Aw = std::max<int64_t>(L.A, 1);
     size_t o = 0;
     L.qt = o; o = up256(o + (size_t)(B * H * L.n * 2));
-    L.wproj = o; o = up256(o + (size_t)(B * H * std::max(st->r, 1) * 8));
     L.hsc = o; o = up256(o + (size_t)(B * H * 16));
     L.seq = o; o = up256(o + (size_t)(B * SQ_WORDS * 4));
     L.hist = o; o = up256(o + (size_t)(B * 2 * HIST_BINS * 4));
@@ -125,7 +124,8 @@ static WsLayout layout(const vkv_step* st, int64_t k, int64_t cap) {
     L.ambkey = o; o = up256(o + (size_t)(B * Aw * 8));
     // everything above is independent of k and cap; the attention partials last
     attend_split(st, k, cap, &L.splits, &L.rows_per_split);
-    L.part_o = o; o = up256(o + (size_t)(B * L.splits * H * D_LAT * 4));
+    const int64_t HG = (H + ATT_HEADS - 1) / ATT_HEADS;   // partials padded to whole head groups
+    L.part_o = o; o = up256(o + (size_t)(B * L.splits * HG * ATT_HEADS * D_LAT * 4));
     L.part_ml = o; o = up256(o + (size_t)(B * L.splits * H * 2 * 4));
     L.total = o;
     return L;
@@ -160,15 +160,16 @@ struct Chunk {
 
 // bytes per sequence of each workspace array (the leading-dimension strides of layout())
 struct WsStrides {
-    size_t qt, wproj, hsc, seq, hist, kt, flags, ccount, amb, ambkey, part_o, part_ml;
+    size_t qt, hsc, seq, hist, kt, flags, ccount, amb, ambkey, part_o, part_ml;
 };
 
 static WsStrides ws_strides(const vkv_step* st, const WsLayout& L) {
     const int64_t H = st->H, Aw = std::max<int64_t>(L.A, 1);
-    return WsStrides{(size_t)(H * L.n * 2), (size_t)(H * std::max(st->r, 1) * 8), (size_t)(H * 16),
+    return WsStrides{(size_t)(H * L.n * 2), (size_t)(H * 16),
                      (size_t)(SQ_WORDS * 4), (size_t)(2 * HIST_BINS * 4), (size_t)(Aw * 4), (size_t)Aw,
                      (size_t)(L.nch * CC_WORDS * 4), (size_t)(Aw * 4), (size_t)(Aw * 8),
-                     (size_t)(L.splits * H * D_LAT * 4), (size_t)(L.splits * H * 2 * 4)};
+                     (size_t)(L.splits * ((H + ATT_HEADS - 1) / ATT_HEADS) * ATT_HEADS * D_LAT * 4),
+                     (size_t)(L.splits * H * 2 * 4)};
 }
 
 static QprepArgs qprep_args(const vkv_step* st, const WsLayout& L, char* w, Chunk c) {
@@ -176,7 +177,6 @@ static QprepArgs qprep_args(const vkv_step* st, const WsLayout& L, char* w, Chun
     const int64_t b0 = c.b0;
     return QprepArgs{st->q_lat + b0 * st->H * D_LAT, st->q_rope + b0 * st->H * D_ROPE, st->P, (int)c.nb, (int)st->H,
                      st->r, st->mode, (int)L.n, reinterpret_cast<uint16_t*>(w + L.qt + b0 * z.qt),
-                     reinterpret_cast<double*>(w + L.wproj + b0 * z.wproj),
                      reinterpret_cast<float*>(w + L.hsc + b0 * z.hsc), reinterpret_cast<uint32_t*>(w + L.seq + b0 * z.seq),
                      reinterpret_cast<uint32_t*>(w + L.hist + b0 * z.hist)};
 }

@@ -120,7 +120,7 @@ enum SeqWord : int {
     SQ_QMAX = 0,    // float bits: max_h ||qt_h|| (upper bound)
     SQ_NU2MAX = 1,  // float bits: max_u ||x_u||^2 (fp32 sum)
     SQ_BMAX = 2,    // float bits: max_u (amax eta + nmax eps + emax gam)
-    SQ_AMAX = 3,
+    SQ_AMAX = 3,    // float bits: max_h a_h, n_h, e_h (written by the scorer launch)
     SQ_NMAX = 4,
     SQ_EMAX = 5,
     SQ_KMIN = 6,    // ordered encoding of min_u key~_u   (scorer, atomicMin)
@@ -145,7 +145,7 @@ constexpr int ATT_HEADS = 128;     // heads per attention workgroup (8 waves x 1
 constexpr int ATT_MAX_SPLIT_ROWS = 1024;   // rows of one split (row list held in LDS)
 
 struct WsLayout {
-    size_t qt, wproj, hsc, seq, hist, kt, flags, flags2, ccount, amb, ambkey, part_o, part_ml, total;
+    size_t qt, hsc, seq, hist, kt, flags, flags2, ccount, amb, ambkey, part_o, part_ml, total;
     int64_t A, n, nch, splits, rows_per_split, cap;
 };
 
@@ -157,7 +157,6 @@ struct QprepArgs {
     const uint16_t* P;
     int B, H, r, mode, n;
     uint16_t* qt;      // [B,H,n]
-    double* wproj;     // [B,H,r]
     float* hsc;        // [B,H,4]: a, nq, e, ||qt||
     uint32_t* seq;     // [B,SQ_WORDS]
     uint32_t* hist;    // [B,2,HIST_BINS] (cleared here for the selection)
@@ -232,7 +231,7 @@ struct AttendArgs {
     int splits;
     int B, H;
     float scale_log2;      // scale * log2(e)
-    float* part_o;         // [B, splits, H, 512]
+    float* part_o;         // [B, splits, head groups, 8 waves, 32, 64 lanes, 4] (register order)
     float* part_ml;        // [B, splits, H, 2]
     uint16_t* out;         // [B,H,512]
     float* lse;            // [B,H]
