@@ -8,9 +8,10 @@
 //
 // Work split: workgroup = (split of the row list, group of 128 heads, b);
 // 8 waves x 16 heads, so every gathered row serves all heads of the group.
-// Tiles of 32 rows stream through a ring of three LDS stages by direct
-// global->LDS loads (global_load_lds_dwordx4), issued two tiles ahead, so one
-// workgroup barrier per tile suffices.  Stage layout: row-major, piece p (16 B)
+// Tiles of 32 rows stream through a ring of four LDS stages by direct
+// global->LDS loads (global_load_lds_dwordx4): tiles go in groups of two, the
+// next group is loaded while the current one is processed, and one workgroup
+// barrier per group suffices.  Stage layout: row-major, piece p (16 B)
 // of tile row r at slot 72 r + (p ^ f(r)); f spreads both operand reads below
 // over all LDS banks.  S^T = K Q^T reads K rows as the A operand; O += P V
 // reads V = the latent half of the same stage with the transposing LDS load
@@ -33,11 +34,8 @@ constexpr int ATT_THREADS = 64 * ATT_WAVES;  // 512
 constexpr int ROW_PIECES = D_ROW / 8;        // 72 pieces of 16 B per row
 constexpr int TILE_BYTES = ATT_CHUNK * D_ROW * 2;            // 36 KB
 constexpr int TILE_LOADS = TILE_BYTES / 1024;                // 36 loads of 1 KB
-#ifndef ATT_STAGES_OVERRIDE
-constexpr int ATT_STAGES = 3;                // ring depth: tiles in flight = ATT_STAGES - 1
-#else
-constexpr int ATT_STAGES = ATT_STAGES_OVERRIDE;
-#endif
+constexpr int ATT_GROUP = 2;                 // tiles per workgroup barrier
+constexpr int ATT_STAGES = 2 * ATT_GROUP;    // ring depth: the group in use and the next in flight
 constexpr int ROW_BYTES = D_ROW * 2;                         // 1152
 
 typedef __attribute__((address_space(3))) void lds_void_t;
@@ -58,21 +56,6 @@ __device__ __forceinline__ int32_t attended_row(const AttendArgs& a, int b, int6
 __device__ __forceinline__ int piece_xor(int r) { return 2 * ((r >> 1) & 3) + ((r >> 3) & 1); }
 
 __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
-
-// Wait until at most `tiles` tiles of this wave's direct loads (`per` = 4 or 5
-// loads each) are still in flight; `tiles` and `per` are wave-uniform.
-__device__ __forceinline__ void wait_tiles_behind(int tiles, int per) {
-    // any count below the true one is also safe (loads complete in order), only slower
-    switch (tiles * per) {
-        case 15: asm volatile("s_waitcnt vmcnt(15)" ::: "memory"); break;
-        case 12: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
-        case 10: asm volatile("s_waitcnt vmcnt(10)" ::: "memory"); break;
-        case 8: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
-        case 5: asm volatile("s_waitcnt vmcnt(5)" ::: "memory"); break;
-        case 4: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
-        default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
-    }
-}
 
 // Compile-time loop: f(std::integral_constant<int, I>) for I = 0 .. N-1.
 template <int I, int N, typename F>
@@ -203,9 +186,8 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
             }
         }
     };
-    constexpr int PD = ATT_STAGES - 1;   // tiles issued ahead
 #pragma unroll
-    for (int t = 0; t < PD; ++t)
+    for (int t = 0; t < ATT_GROUP; ++t)
         if (t < ntile) issue(t, s_k + t * TILE_BYTES);
 
     // Q fragments (B operand of S^T = K Q^T): head hq, dims 32*ks + 8*g .. +8
@@ -248,18 +230,24 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
         return Offs{cc * ROW_BYTES + 16 * (gg ^ fc), cc * ROW_BYTES + 16 * ((4 + gg) ^ fc),
                     (4 * gg + e) * ROW_BYTES + 8 * (q & 1), q >> 1, piece_xor(4 * gg + e)};
     };
-    const int cnt_next = nj;   // this wave's loads of one tile
 
     const uint32_t k_lds = lds_addr(s_k);
     int stage = 0;   // t mod ATT_STAGES
     for (int t = 0; t < ntile; ++t) {
         const int nr = (int)min((int64_t)ATT_CHUNK, p1 - (p0 + (int64_t)ATT_CHUNK * t));
-        // this wave's loads of tile t have landed (tiles t+1 .. t+PD-1 may still be in flight) ...
-        wait_tiles_behind(min(PD - 1, ntile - 1 - t), cnt_next);
-        // ... and every wave's; every wave is also done with tile t-1, whose stage tile t+PD reuses
-        wg_barrier();
-        const int stage_pd = stage == 0 ? ATT_STAGES - 1 : stage - 1;   // (t + PD) mod ATT_STAGES
-        if (t + PD < ntile) issue(t + PD, s_k + stage_pd * TILE_BYTES);
+        if (t % ATT_GROUP == 0) {
+            // this wave's loads of the group t .. t+ATT_GROUP-1 have landed (nothing
+            // else is in flight) ...
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            // ... and every wave's; every wave is also done with the previous group,
+            // whose stages the next group reuses
+            wg_barrier();
+#pragma unroll
+            for (int u = 0; u < ATT_GROUP; ++u) {
+                const int tn = t + ATT_GROUP + u;
+                if (tn < ntile) issue(tn, s_k + (tn % ATT_STAGES) * TILE_BYTES);
+            }
+        }
         const uint32_t kt = k_lds + (uint32_t)(stage * TILE_BYTES);
         stage = stage == ATT_STAGES - 1 ? 0 : stage + 1;
         const Offs of = offsets();
