@@ -19,8 +19,10 @@
 // registers: the S accumulator layout of a lane (4 rows x 1 head per 16-row
 // tile) is the A-operand layout of the PV product when the 32 rows of the tile
 // are fed to the K dimension in a permuted order, which the V reads follow.
-// Online softmax in the log2 domain; each split emits (unnormalised O,
-// running max, running sum) and a second kernel merges the splits by their
+// Online softmax in the log2 domain against a reference maximum that moves
+// only when a score exceeds it by more than a factor 2^8 (so P <= 256 in bf16 and the
+// accumulators are rarely rescaled); each split emits (unnormalised O,
+// reference max, running sum) and a second kernel merges the splits by their
 // log-sum-exp (the appendix's kernel mapping: fetched rows are one more
 // split-KV partition).
 #include <type_traits>
@@ -35,6 +37,7 @@ constexpr int ROW_PIECES = D_ROW / 8;        // 72 pieces of 16 B per row
 constexpr int TILE_BYTES = ATT_CHUNK * D_ROW * 2;            // 36 KB
 constexpr int TILE_LOADS = TILE_BYTES / 1024;                // 36 loads of 1 KB
 constexpr int ATT_GROUP = 2;                 // tiles per workgroup barrier
+constexpr float ATT_SLACK = 8.0f;            // lag allowed to the softmax reference maximum (log2 units)
 constexpr int ATT_STAGES = 2 * ATT_GROUP;    // ring depth: the group in use and the next in flight
 constexpr int ROW_BYTES = D_ROW * 2;                         // 1152
 
@@ -288,15 +291,18 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
                 cmax = fmaxf(cmax, v);
             }
         cmax = allreduce_groups(cmax, [](float x, float y) { return fmaxf(x, y); });
-        const float m_new = fmaxf(m_run, cmax);
-        const float alpha = exp2f(m_run - m_new);
+        // the reference maximum moves only when a score exceeds it by more than
+        // ATT_SLACK (log2 units), so P <= 2^ATT_SLACK and most tiles rescale nothing
+        const bool move = cmax > m_run + ATT_SLACK;
+        const float m_new = move ? cmax : m_run;
+        const float alpha = move ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
         bf16x8_t pa;
         float psum = 0.f;
 #pragma unroll
         for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const float p = exp2f(sc[mt][i] - m_new);
+                const float p = __builtin_amdgcn_exp2f(sc[mt][i] - m_new);
                 psum += p;
                 pa[4 * mt + i] = (__bf16)p;
             }
@@ -305,8 +311,8 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
         m_run = m_new;
         // the softmax's cross-lane reads complete before the PV reads are issued
         asm volatile("" : "+v"(l_run), "+v"(pa));
-        // rescale the accumulators only when some head's running max moved
-        if (__ballot(alpha != 1.0f)) {
+        // rescale the accumulators only when some head's reference maximum moved
+        if (__ballot(move)) {
             float al[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) al[i] = __shfl(alpha, 4 * g + i);
