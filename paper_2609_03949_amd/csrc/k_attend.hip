@@ -124,7 +124,7 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
     const int64_t p0 = (int64_t)sp * a.rows_per_split;
     const int64_t p1 = min(N, p0 + a.rows_per_split);
     const int HG = (a.H + ATT_HEADS - 1) / ATT_HEADS;
-    float* po = a.part_o + (((int64_t)b * a.splits + sp) * HG + hg) * (ATT_HEADS * D_LAT);
+    uint16_t* po = a.part_o + (((int64_t)b * a.splits + sp) * HG + hg) * (ATT_HEADS * D_LAT);
     float* pml = a.part_ml + ((int64_t)b * a.splits + sp) * a.H * 2;
     if (p0 >= p1) {
         if (tid < ATT_HEADS) {
@@ -347,17 +347,23 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
         });
     }
     // o[tt][i] = unnormalised output of head h0 + 4*g + i, dim 16*tt + c; the
-    // partial is stored in that register order (one 1 KB store per tt and wave)
-    float* pw = po + (int64_t)wave * (D_LAT / 16) * 64 * 4;
+    // partial is stored as bf16 (RNE) in that register order (one 512 B store
+    // per tt and wave)
+    uint16_t* pw = po + (int64_t)wave * (D_LAT / 16) * 64 * 4;
 #pragma unroll
-    for (int tt = 0; tt < D_LAT / 16; ++tt) *reinterpret_cast<f32x4_t*>(pw + (tt * 64 + lane) * 4) = o[tt];
+    for (int tt = 0; tt < D_LAT / 16; ++tt) {
+        typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+        const bf16x4_t v = {(__bf16)o[tt][0], (__bf16)o[tt][1], (__bf16)o[tt][2], (__bf16)o[tt][3]};
+        *reinterpret_cast<bf16x4_t*>(pw + (tt * 64 + lane) * 4) = v;
+    }
     if (g == 0 && hq < a.H) {
         pml[2 * hq] = m_run;
         pml[2 * hq + 1] = l_run;
     }
 }
 
-// Merge the splits of four heads by log-sum-exp; bf16 output, natural-log lse.
+// Merge the splits of four heads by log-sum-exp (partials bf16, sums fp32);
+// bf16 output, natural-log lse.
 // Block = (b, head group, wave, lane group g) of the attention kernel: heads
 // hb + i (i = 0..3) with hb = 128 hg + 16 wave + 4 g; thread j covers dims
 // 4j .. 4j+3 (tt = j / 4, lanes 16 g + 4 (j mod 4) .. +3 of the partials).
@@ -372,12 +378,15 @@ __global__ __launch_bounds__(128) void attend_combine_kernel(AttendArgs a) {
     float acc[4][4] = {};
 #pragma unroll
     for (int i = 0; i < 4; ++i) M[i] = -INFINITY;
+    // (both passes unrolled so that the loads of several splits are in flight together)
+#pragma unroll 8
     for (int s = 0; s < a.splits; ++s) {
         const float* ml = a.part_ml + (((int64_t)b * a.splits + s) * a.H) * 2;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
             if (hb + i < a.H) M[i] = fmaxf(M[i], ml[2 * (hb + i)]);
     }
+#pragma unroll 4
     for (int s = 0; s < a.splits; ++s) {
         const float* ml = a.part_ml + (((int64_t)b * a.splits + s) * a.H) * 2;
         float w[4];
@@ -387,11 +396,16 @@ __global__ __launch_bounds__(128) void attend_combine_kernel(AttendArgs a) {
             w[i] = (ms == -INFINITY) ? 0.f : exp2f(ms - M[i]);
             if (ms != -INFINITY) L[i] += w[i] * ml[2 * (hb + i) + 1];
         }
-        const float* src = a.part_o + (((int64_t)b * a.splits + s) * HG + hg) * (ATT_HEADS * D_LAT) +
-                           (int64_t)wave * (D_LAT / 16) * 64 * 4 + (tt * 64 + 16 * g + c0) * 4;
+        const uint16_t* src = a.part_o + (((int64_t)b * a.splits + s) * HG + hg) * (ATT_HEADS * D_LAT) +
+                              (int64_t)wave * (D_LAT / 16) * 64 * 4 + (tt * 64 + 16 * g + c0) * 4;
+        const u32x4_t raw0 = *reinterpret_cast<const u32x4_t*>(src);       // lanes c0, c0+1
+        const u32x4_t raw1 = *reinterpret_cast<const u32x4_t*>(src + 8);   // lanes c0+2, c0+3
 #pragma unroll
         for (int cc = 0; cc < 4; ++cc) {
-            const f32x4_t v = *reinterpret_cast<const f32x4_t*>(src + 4 * cc);
+            const u32x4_t& rw = cc < 2 ? raw0 : raw1;
+            const uint32_t w01 = rw[2 * (cc & 1)], w23 = rw[2 * (cc & 1) + 1];
+            const float v[4] = {__uint_as_float(w01 << 16), __uint_as_float(w01 & 0xFFFF0000u),
+                                __uint_as_float(w23 << 16), __uint_as_float(w23 & 0xFFFF0000u)};
             // a split without rows never wrote its partial: weight 0 must not touch it
 #pragma unroll
             for (int i = 0; i < 4; ++i) acc[cc][i] += (w[i] > 0.f) ? w[i] * v[i] : 0.f;

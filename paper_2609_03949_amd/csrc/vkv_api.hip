@@ -125,7 +125,7 @@ static WsLayout layout(const vkv_step* st, int64_t k, int64_t cap) {
     // everything above is independent of k and cap; the attention partials last
     attend_split(st, k, cap, &L.splits, &L.rows_per_split);
     const int64_t HG = (H + ATT_HEADS - 1) / ATT_HEADS;   // partials padded to whole head groups
-    L.part_o = o; o = up256(o + (size_t)(B * L.splits * HG * ATT_HEADS * D_LAT * 4));
+    L.part_o = o; o = up256(o + (size_t)(B * L.splits * HG * ATT_HEADS * D_LAT * 2));
     L.part_ml = o; o = up256(o + (size_t)(B * L.splits * H * 2 * 4));
     L.total = o;
     return L;
@@ -168,7 +168,7 @@ static WsStrides ws_strides(const vkv_step* st, const WsLayout& L) {
     return WsStrides{(size_t)(H * L.n * 2), (size_t)(H * 16),
                      (size_t)(SQ_WORDS * 4), (size_t)(2 * HIST_BINS * 4), (size_t)(Aw * 4), (size_t)Aw,
                      (size_t)(L.nch * CC_WORDS * 4), (size_t)(Aw * 4), (size_t)(Aw * 8),
-                     (size_t)(L.splits * ((H + ATT_HEADS - 1) / ATT_HEADS) * ATT_HEADS * D_LAT * 4),
+                     (size_t)(L.splits * ((H + ATT_HEADS - 1) / ATT_HEADS) * ATT_HEADS * D_LAT * 2),
                      (size_t)(L.splits * H * 2 * 4)};
 }
 
@@ -255,7 +255,7 @@ static AttendArgs attend_args(const vkv_step* st, const WsLayout& L, char* w, Ch
     a.B = (int)c.nb;
     a.H = (int)st->H;
     a.scale_log2 = scale * 1.4426950408889634f;
-    a.part_o = reinterpret_cast<float*>(w + L.part_o + b0 * z.part_o);
+    a.part_o = reinterpret_cast<uint16_t*>(w + L.part_o + b0 * z.part_o);
     a.part_ml = reinterpret_cast<float*>(w + L.part_ml + b0 * z.part_ml);
     a.out = out + b0 * st->H * D_LAT;
     a.lse = lse + b0 * st->H;

@@ -231,7 +231,7 @@ struct AttendArgs {
     int splits;
     int B, H;
     float scale_log2;      // scale * log2(e)
-    float* part_o;         // [B, splits, head groups, 8 waves, 32, 64 lanes, 4] (register order)
+    uint16_t* part_o;      // bf16 [B, splits, head groups, 8 waves, 32, 64 lanes, 4] (register order)
     float* part_ml;        // [B, splits, H, 2]
     uint16_t* out;         // [B,H,512]
     float* lse;            // [B,H]
