@@ -58,7 +58,6 @@ __global__ __launch_bounds__(QP_THREADS) void qprep_project_kernel(QprepArgs a) 
     const int lane = tid & 63, wave = tid >> 6;
     if (blockIdx.x == 0) {
         if (tid < SQ_WORDS) a.seq[b * SQ_WORDS + tid] = (tid == SQ_KMIN) ? 0xFFFFFFFFu : 0u;
-        for (int i = tid; i < 2 * HIST_BINS; i += QP_THREADS) a.hist[(int64_t)b * 2 * HIST_BINS + i] = 0u;
     }
     const int r = (a.mode & 2) ? a.r : 0;
     const int HB = qp_heads(r), IC = qp_chunk(r), PR = IC / 8;

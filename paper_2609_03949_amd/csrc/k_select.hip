@@ -5,9 +5,9 @@
 // E from the per-sequence maxima of ||qt_h|| and ||x_u||):
 //   1. a strided sample of the keys places a bracket [t_lo, t_hi] around the
 //      k-th largest key~; one counting pass counts the keys above t_hi and
-//      histograms the keys inside it over 4096 fine bins, and finds the bin of
-//      the k-th largest key~ (if the sample missed, the same block redoes the
-//      histogram over the whole key range).  With v = key~ + E and w = key~ - E
+//      lists the keys inside it; one block per sequence histograms the list
+//      over 4096 fine bins and finds the bin of the k-th largest key~ (if the
+//      sample missed, it histograms the whole key range instead).  With v = key~ + E and w = key~ - E
 //      (rounded outward) this gives HI >= k-th largest v and LO <= k-th
 //      largest w, so the k-th largest exact key lies in [LO, HI];
 //   2. rows with w > HI are certainly selected and rows with v < LO certainly
@@ -26,7 +26,8 @@
 namespace vkv {
 
 constexpr int SEL_THREADS = 256;
-constexpr int SAMPLE_MAX = 4096;             // keys sampled per sequence to place the bracket
+constexpr int SAMPLE_MAX = 2048;             // keys sampled per sequence to place the bracket
+constexpr int SAMPLE_BINS = 2048;            // bins of the sample's histogram
 constexpr int COUNT_KEYS_PER_BLOCK = 4096;   // keys per block of the counting pass
 constexpr int KEY_BATCH = 16;                // keys per thread in flight
 constexpr int EX_BLOCKS = 16;                // per sequence: blocks of the exact-key pass
@@ -108,15 +109,17 @@ __device__ __forceinline__ uint32_t block_sum_u32(uint32_t v, uint32_t* s_red) {
 
 // ---------------------------------------------------------- histogram pass
 
+template <int NB = HIST_BINS>
 __device__ __forceinline__ float bin_scale(float lo, float hi) {
     const float range = hi - lo;
-    return (range > 0.f && range < INFINITY) ? (float)HIST_BINS / range : 0.f;
+    return (range > 0.f && range < INFINITY) ? (float)NB / range : 0.f;
 }
 
+template <int NB = HIST_BINS>
 __device__ __forceinline__ int bin_of(float x, float lo, float scale) {
     const float t = (x - lo) * scale;
     const int bi = (t > 0.f) ? (int)t : 0;
-    return bi < HIST_BINS ? bi : HIST_BINS - 1;
+    return bi < NB ? bi : NB - 1;
 }
 
 // Sum over threads t' >= tid of v (block of SEL_THREADS threads).
@@ -152,11 +155,12 @@ __device__ __forceinline__ double edge_lo_of(int d, float lo, float scale) {
     return fmax((double)lo, (double)lo + (double)d * w * (1.0 - 0x1p-20) - slack);
 }
 
-// In a block of SEL_THREADS threads holding a histogram s_h[HIST_BINS]: the
-// bin d where the count of keys in bins >= d first reaches `target` (1 <=
-// target <= total).  Returns -1 in threads that do not own it.
+// In a block of SEL_THREADS threads holding a histogram s_h[NB]: the bin d
+// where the count of keys in bins >= d first reaches `target` (1 <= target <=
+// total).  Returns -1 in threads that do not own it.
+template <int NB = HIST_BINS>
 __device__ __forceinline__ int find_rank_bin(const uint32_t* s_h, uint32_t target, uint32_t* s_w) {
-    constexpr int PER = HIST_BINS / SEL_THREADS;
+    constexpr int PER = NB / SEL_THREADS;
     const int tid = threadIdx.x;
     uint32_t loc = 0;
 #pragma unroll
@@ -212,23 +216,23 @@ __device__ void sample_bracket(const SelectArgs& a, int b, const uint32_t* sq, u
         s_mm[tid >> 6] = lo;
         s_mm[4 + (tid >> 6)] = hi;
     }
-    for (int i = tid; i < HIST_BINS; i += SEL_THREADS) s_h[i] = 0u;
+    for (int i = tid; i < SAMPLE_BINS; i += SEL_THREADS) s_h[i] = 0u;
     __syncthreads();
     lo = fminf(fminf(s_mm[0], s_mm[1]), fminf(s_mm[2], s_mm[3]));
     hi = fmaxf(fmaxf(s_mm[4], s_mm[5]), fmaxf(s_mm[6], s_mm[7]));
-    const float scale = bin_scale(lo, hi);
+    const float scale = bin_scale<SAMPLE_BINS>(lo, hi);
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
         const int i = tid + SEL_THREADS * j;
-        if (i < m) atomicAdd(&s_h[bin_of(v[j], lo, scale)], 1u);
+        if (i < m) atomicAdd(&s_h[bin_of<SAMPLE_BINS>(v[j], lo, scale)], 1u);
     }
     __syncthreads();
     const double ks = (double)a.k * (double)m / (double)A;
     const double dl = 4.0 * sqrt(ks) + 16.0;
     const int64_t c_hi = (int64_t)floor(ks - dl);   // fewer than c_hi samples above t_hi
     const int64_t c_lo = (int64_t)ceil(ks + dl);    // at least c_lo samples at or above t_lo
-    const int d_hi = (c_hi >= 1) ? find_rank_bin(s_h, (uint32_t)c_hi, s_w) : -1;
-    const int d_lo = (c_lo <= m) ? find_rank_bin(s_h, (uint32_t)c_lo, s_w) : -1;
+    const int d_hi = (c_hi >= 1) ? find_rank_bin<SAMPLE_BINS>(s_h, (uint32_t)c_hi, s_w) : -1;
+    const int d_lo = (c_lo <= m) ? find_rank_bin<SAMPLE_BINS>(s_h, (uint32_t)c_lo, s_w) : -1;
     __syncthreads();
     // no cut on a side the sample cannot place: the scorer's key extremes
     if (tid == 0) {
@@ -244,18 +248,28 @@ __device__ void sample_bracket(const SelectArgs& a, int b, const uint32_t* sq, u
     __syncthreads();
 }
 
-// Counting pass: every block places the sampled bracket, then counts its keys
-// above t_hi and histograms those in [t_lo, t_hi] over HIST_BINS fine bins
-// (the bulk of the keys, below t_lo, costs one compare), into per-sequence
-// global counters by atomics.
+// Counting pass: every block places the sampled bracket, counts its keys
+// above t_hi and appends those in [t_lo, t_hi] (the bracket holds a few
+// percent of the keys) to the sequence's list, one atomic per wave; the bulk
+// of the keys, below t_lo, costs one compare.
 __global__ __launch_bounds__(SEL_THREADS) void count_kernel(SelectArgs a) {
-    __shared__ uint32_t s_h[HIST_BINS];
+    __shared__ uint32_t s_h[SAMPLE_BINS];
     __shared__ uint32_t s_w[SEL_THREADS / 64];
     __shared__ float s_mm[8];
     const int b = blockIdx.y;
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63;
     uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    uint32_t* gh = a.hist + (int64_t)b * 2 * HIST_BINS;
+    // this block's keys are loaded together with the sample (one round trip)
+    static_assert(COUNT_KEYS_PER_BLOCK == KEY_BATCH * SEL_THREADS, "one batch of keys per thread");
+    const float* kt = a.kt + (int64_t)b * a.A;
+    const int64_t u0 = (int64_t)blockIdx.x * COUNT_KEYS_PER_BLOCK;
+    const int64_t u1 = min(a.A, u0 + COUNT_KEYS_PER_BLOCK);
+    float k[KEY_BATCH];
+#pragma unroll
+    for (int j = 0; j < KEY_BATCH; ++j) {
+        const int64_t u = u0 + tid + (int64_t)j * SEL_THREADS;
+        k[j] = (u < u1) ? kt[u] : 0.f;
+    }
     float tlo, thi;
     sample_bracket(a, b, sq, s_h, s_w, s_mm, tlo, thi);
     if (blockIdx.x == 0 && tid == 0) {
@@ -264,36 +278,37 @@ __global__ __launch_bounds__(SEL_THREADS) void count_kernel(SelectArgs a) {
         sq[SQ_NAMB] = 0u;
         sq[SQ_NAMB2] = 0u;
     }
-    const float scale = bin_scale(tlo, thi);
-    for (int i = tid; i < HIST_BINS; i += SEL_THREADS) s_h[i] = 0u;
-    __syncthreads();
-    const float* kt = a.kt + (int64_t)b * a.A;
-    const int64_t u0 = (int64_t)blockIdx.x * COUNT_KEYS_PER_BLOCK;
-    const int64_t u1 = min(a.A, u0 + COUNT_KEYS_PER_BLOCK);
-    uint32_t above = 0;
-    for (int64_t ub = u0; ub < u1; ub += KEY_BATCH * SEL_THREADS) {
-        float k[KEY_BATCH];
+    uint32_t above = 0, nin = 0;
 #pragma unroll
-        for (int j = 0; j < KEY_BATCH; ++j) {
-            const int64_t u = ub + tid + (int64_t)j * SEL_THREADS;
-            k[j] = (u < u1) ? kt[u] : 0.f;
-        }
+    for (int j = 0; j < KEY_BATCH; ++j) {
+        const int64_t u = u0 + tid + (int64_t)j * SEL_THREADS;
+        const bool live = u < u1;
+        above += (live && k[j] > thi);
+        nin += (live && k[j] <= thi && k[j] >= tlo);
+    }
+    // wave-inclusive scan of the in-bracket counts, one append slot range per wave
+    uint32_t incl = nin;
 #pragma unroll
-        for (int j = 0; j < KEY_BATCH; ++j) {
-            const int64_t u = ub + tid + (int64_t)j * SEL_THREADS;
-            if (u >= u1) continue;
-            if (k[j] > thi) ++above;
-            else if (k[j] >= tlo) atomicAdd(&s_h[bin_of(k[j], tlo, scale)], 1u);
-        }
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t t = __shfl_up(incl, o);
+        if (lane >= o) incl += t;
+    }
+    uint32_t base = 0;
+    if (lane == 63 && incl) base = atomicAdd(&sq[SQ_NBR], incl);
+    base = __shfl(base, 63) + (incl - nin);
+    float* list = reinterpret_cast<float*>(a.amb) + (int64_t)b * a.A;
+#pragma unroll
+    for (int j = 0; j < KEY_BATCH; ++j) {
+        const int64_t u = u0 + tid + (int64_t)j * SEL_THREADS;
+        if (u < u1 && k[j] <= thi && k[j] >= tlo) list[base++] = k[j];
     }
     above = block_sum_u32(above, s_w);
     if (tid == 0 && above) atomicAdd(&sq[SQ_ABOVE], above);
-    for (int i = tid; i < HIST_BINS; i += SEL_THREADS)
-        if (s_h[i]) atomicAdd(&gh[i], s_h[i]);
 }
 
 // One block per sequence, after the counting pass: the bin of the k-th
-// largest key~ and the band around it,
+// largest key~ (a histogram of the listed in-bracket keys) and the band
+// around it,
 //   THI = up(edge_hi + E) >= k-th largest v,  TLO = down(edge_lo - E) <= k-th largest w.
 // If the sample missed (the k-th key~ lies outside [t_lo, t_hi]) the block
 // histograms the sequence's whole key range itself.
@@ -304,24 +319,29 @@ __global__ __launch_bounds__(SEL_THREADS) void bracket_kernel(SelectArgs a) {
     const int b = blockIdx.x;
     const int tid = threadIdx.x;
     uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    uint32_t* gh = a.hist + (int64_t)b * 2 * HIST_BINS;
     const float tlo = __uint_as_float(sq[SQ_BLO]);
     const float thi = __uint_as_float(sq[SQ_BHI]);
     const uint32_t tot_above = sq[SQ_ABOVE];
-    uint32_t inr = 0;
+    const uint32_t inr = sq[SQ_NBR];
     {
-        constexpr int PER = HIST_BINS / SEL_THREADS;
-        uint32_t hv[PER];
+        // the keys inside the sampled bracket, listed by the counting pass
+        const float sc0 = bin_scale(tlo, thi);
+        for (int i = tid; i < HIST_BINS; i += SEL_THREADS) s_h[i] = 0u;
+        __syncthreads();
+        const float* list = reinterpret_cast<const float*>(a.amb) + (int64_t)b * a.A;
+        for (uint32_t i0 = 0; i0 < inr; i0 += KEY_BATCH * SEL_THREADS) {   // loads of a batch in flight together
+            float v[KEY_BATCH];
 #pragma unroll
-        for (int j = 0; j < PER; ++j) hv[j] = gh[tid + SEL_THREADS * j];
+            for (int j = 0; j < KEY_BATCH; ++j) {
+                const uint32_t i = i0 + tid + j * SEL_THREADS;
+                v[j] = i < inr ? list[i] : 0.f;
+            }
 #pragma unroll
-        for (int j = 0; j < PER; ++j) {
-            s_h[tid + SEL_THREADS * j] = hv[j];
-            inr += hv[j];
-            gh[tid + SEL_THREADS * j] = 0u;
+            for (int j = 0; j < KEY_BATCH; ++j)
+                if (i0 + tid + j * SEL_THREADS < inr) atomicAdd(&s_h[bin_of(v[j], tlo, sc0)], 1u);
         }
+        __syncthreads();
     }
-    inr = block_sum_u32(inr, s_w);
     const float E = key_band_f32(sq, a.n);
     const int64_t need = a.k - (int64_t)tot_above;
     const bool ok = need >= 1 && need <= (int64_t)inr;

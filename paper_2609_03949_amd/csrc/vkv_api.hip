@@ -115,7 +115,6 @@ static WsLayout layout(const vkv_step* st, int64_t k, int64_t cap) {
     L.qt = o; o = up256(o + (size_t)(B * H * L.n * 2));
     L.hsc = o; o = up256(o + (size_t)(B * H * 16));
     L.seq = o; o = up256(o + (size_t)(B * SQ_WORDS * 4));
-    L.hist = o; o = up256(o + (size_t)(B * 2 * HIST_BINS * 4));
     L.kt = o; o = up256(o + (size_t)(B * Aw * 4));
     L.flags = o; o = up256(o + (size_t)(B * Aw));
     L.flags2 = o; o = up256(o + (size_t)(B * Aw));
@@ -160,13 +159,13 @@ struct Chunk {
 
 // bytes per sequence of each workspace array (the leading-dimension strides of layout())
 struct WsStrides {
-    size_t qt, hsc, seq, hist, kt, flags, ccount, amb, ambkey, part_o, part_ml;
+    size_t qt, hsc, seq, kt, flags, ccount, amb, ambkey, part_o, part_ml;
 };
 
 static WsStrides ws_strides(const vkv_step* st, const WsLayout& L) {
     const int64_t H = st->H, Aw = std::max<int64_t>(L.A, 1);
     return WsStrides{(size_t)(H * L.n * 2), (size_t)(H * 16),
-                     (size_t)(SQ_WORDS * 4), (size_t)(2 * HIST_BINS * 4), (size_t)(Aw * 4), (size_t)Aw,
+                     (size_t)(SQ_WORDS * 4), (size_t)(Aw * 4), (size_t)Aw,
                      (size_t)(L.nch * CC_WORDS * 4), (size_t)(Aw * 4), (size_t)(Aw * 8),
                      (size_t)(L.splits * ((H + ATT_HEADS - 1) / ATT_HEADS) * ATT_HEADS * D_LAT * 2),
                      (size_t)(L.splits * H * 2 * 4)};
@@ -177,8 +176,7 @@ static QprepArgs qprep_args(const vkv_step* st, const WsLayout& L, char* w, Chun
     const int64_t b0 = c.b0;
     return QprepArgs{st->q_lat + b0 * st->H * D_LAT, st->q_rope + b0 * st->H * D_ROPE, st->P, (int)c.nb, (int)st->H,
                      st->r, st->mode, (int)L.n, reinterpret_cast<uint16_t*>(w + L.qt + b0 * z.qt),
-                     reinterpret_cast<float*>(w + L.hsc + b0 * z.hsc), reinterpret_cast<uint32_t*>(w + L.seq + b0 * z.seq),
-                     reinterpret_cast<uint32_t*>(w + L.hist + b0 * z.hist)};
+                     reinterpret_cast<float*>(w + L.hsc + b0 * z.hsc), reinterpret_cast<uint32_t*>(w + L.seq + b0 * z.seq)};
 }
 
 static ScoreArgs score_args(const vkv_step* st, const WsLayout& L, char* w, Chunk c, float* key, float* ub) {
@@ -217,7 +215,6 @@ static SelectArgs select_args(const vkv_step* st, const WsLayout& L, char* w, Ch
     a.gam = st->gam ? st->gam + b0 * st->T : nullptr;
     a.T = st->T;
     a.seq = reinterpret_cast<uint32_t*>(w + L.seq + b0 * z.seq);
-    a.hist = reinterpret_cast<uint32_t*>(w + L.hist + b0 * z.hist);
     a.kt = reinterpret_cast<const float*>(w + L.kt + b0 * z.kt);
     a.flags = reinterpret_cast<uint8_t*>(w + L.flags + b0 * z.flags);
     a.flags2 = reinterpret_cast<uint8_t*>(w + L.flags2 + b0 * z.flags);

@@ -127,7 +127,7 @@ enum SeqWord : int {
     SQ_KMAX = 7,    // ordered encoding of max_u key~_u   (scorer, atomicMax)
     SQ_TLO = 8,     // float bits: LO <= k-th largest of (key~ - E)
     SQ_THI = 9,     // float bits: HI >= k-th largest of (key~ + E)
-    SQ_DONE = 10,   // (unused)
+    SQ_NBR = 10,    // keys~ inside the sampled bracket (listed by the counting pass)
     SQ_NAMB = 12,   // ambiguous rows of the selection
     SQ_NAMB2 = 13,  // ambiguous rows of the admission
     SQ_BLO = 14,    // float bits: lower end of the sampled bracket of the k-th key~
@@ -145,7 +145,7 @@ constexpr int ATT_HEADS = 128;     // heads per attention workgroup (8 waves x 1
 constexpr int ATT_MAX_SPLIT_ROWS = 1024;   // rows of one split (row list held in LDS)
 
 struct WsLayout {
-    size_t qt, hsc, seq, hist, kt, flags, flags2, ccount, amb, ambkey, part_o, part_ml, total;
+    size_t qt, hsc, seq, kt, flags, flags2, ccount, amb, ambkey, part_o, part_ml, total;
     int64_t A, n, nch, splits, rows_per_split, cap;
 };
 
@@ -158,8 +158,7 @@ struct QprepArgs {
     int B, H, r, mode, n;
     uint16_t* qt;      // [B,H,n]
     float* hsc;        // [B,H,4]: a, nq, e, ||qt||
-    uint32_t* seq;     // [B,SQ_WORDS]
-    uint32_t* hist;    // [B,2,HIST_BINS] (cleared here for the selection)
+    uint32_t* seq;     // [B,SQ_WORDS] (cleared here for the step)
 };
 
 struct ScoreArgs {
@@ -204,11 +203,10 @@ struct SelectArgs {
     const float* gam;
     int64_t T;
     uint32_t* seq;
-    uint32_t* hist;        // [B,2,HIST_BINS]
     uint8_t* flags;        // [B,A]
     uint8_t* flags2;       // [B,A]
     uint32_t* ccount;      // [B,nch,CC_WORDS]
-    int32_t* amb;          // [B,A] ambiguous rows
+    int32_t* amb;          // [B,A] keys~ inside the sampled bracket (as float bits), then the ambiguous rows
     uint64_t* ambkey;      // [B,A] their exact keys (order-preserving encoding of fp64)
     int32_t* sel;          // [B,k]
     double* theta;         // [B]
