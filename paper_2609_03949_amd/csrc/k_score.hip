@@ -519,13 +519,17 @@ __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
 // the same for every tile, only the wave-uniform tile base moves.
 //
 // Per tile: the heads x rows contraction on the matrix cores (queries resident
-// in VGPRs) overlaps the read-out of the next tile from the ring; the per-lane
-// maximum over head slots and sum of squares are kept for four tiles, then a
-// reduce-scatter over the four 16-lane groups (permlane swaps) leaves row c of
-// tile t4+j in lane 16j+c.  Row keys collect in LDS and are written every
-// RES_GROUPS groups: stores share vmcnt with the ring loads, so they are kept
-// rare, and every wait counts ring loads only -- safe whether or not stores
-// complete in order with loads (loads complete in order among themselves).
+// in VGPRs), then the read-out of the next tile from the ring and the refill
+// of its stage; the per-lane maximum over head slots and sum of squares are
+// kept for four tiles, then a reduce-scatter over the four 16-lane groups
+// (permlane swaps) leaves row c of tile 4q+j in lane 16j+c.  The keys of the
+// whole span collect in LDS and are stored after the last tile: key stores
+// mixed into the stream of index reads cost more than a tenth of the scan's
+// time on MI355X, one burst at the end costs a few microseconds.  The bulk of
+// the span runs in a loop of four tiles with fixed stages and fixed wait
+// counts; the last tiles, whose look-ahead loads would run past the span,
+// take a loop with run-time counts.  Every wait counts the ring loads issued
+// after the awaited tile (loads complete in order among themselves).
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void gbl_void_t;
 
@@ -551,31 +555,54 @@ __device__ __forceinline__ void wait_tiles(int rem) {
     }
 }
 
-constexpr int STAGE_BUDGET = 16384;   // bytes of tile ring per wave
+constexpr int STAGE_BUDGET = 12288;   // bytes of tile ring per wave
 constexpr int STREAM_WAVES = 4;       // waves per block
-constexpr int RES_GROUPS = 16;        // 4-tile groups of row keys buffered per wave
+constexpr int STREAM_TPW_MAX = 128;   // tiles per wave, bounded by the LDS key buffer
 
 template <int KS>
 struct StreamGeom {
     static constexpr int N = 32 * KS;          // index dims per row
     static constexpr int N8 = N / 8;           // 16-byte slots per row
     static constexpr int STAGE = 16 * N * 2;   // one 16-row tile; KS loads of 1 KB
-    static constexpr int NST = (STAGE_BUDGET / STAGE) > 8 ? 8 : ((STAGE_BUDGET / STAGE) < 2 ? 2 : (STAGE_BUDGET / STAGE));
-    static constexpr int RES = RES_GROUPS * 64 * 4;
-    static constexpr int WAVE = NST * STAGE + RES;
+    // ring depth 4 or 2, so that a run of four tiles maps to fixed stages
+    static constexpr int NST = STAGE_BUDGET / STAGE >= 4 ? 4 : 2;
+    static constexpr int RUN = 4;                       // tiles per fixed-stage run
+    static constexpr int KEYS = 16 * STREAM_TPW_MAX * 4;   // the span's keys (fp32)
+    static constexpr int WAVE = NST * STAGE + KEYS;     // 16 KB per wave at 128 dims
 };
+
+__device__ __forceinline__ f32x2_t swap32(float x, float y) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+    return f32x2_t{__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+__device__ __forceinline__ f32x2_t swap16(float x, float y) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+    return f32x2_t{__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+// reduce-scatter of four per-lane partials over the four 16-lane groups:
+// lane 16j + c receives the reduction over the groups of v_j at position c
+__device__ __forceinline__ float group_max(float v0, float v1, float v2, float v3) {
+    f32x2_t u = swap32(v0, v2), w = swap32(v1, v3);
+    u = swap16(fmaxf(u[0], u[1]), fmaxf(w[0], w[1]));
+    return fmaxf(u[0], u[1]);
+}
+__device__ __forceinline__ float group_sum(float v0, float v1, float v2, float v3) {
+    f32x2_t u = swap32(v0, v2), w = swap32(v1, v3);
+    u = swap16(u[0] + u[1], w[0] + w[1]);
+    return u[0] + u[1];
+}
 
 template <int HT, int KS>
 __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int tpw) {
     using Gm = StreamGeom<KS>;
-    constexpr int N8 = Gm::N8, STAGE = Gm::STAGE, NST = Gm::NST;
+    constexpr int N8 = Gm::N8, STAGE = Gm::STAGE, NST = Gm::NST, RUN = Gm::RUN;
     constexpr int TST = STREAM_WAVES;   // block tiles between consecutive tiles of a wave
     extern __shared__ __align__(16) uint8_t smem[];
     const int b = blockIdx.y;
     const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     uint8_t* wbase = smem + wave * Gm::WAVE;
-    float* s_res = reinterpret_cast<float*>(wbase + NST * STAGE);
+    float* s_key = reinterpret_cast<float*>(wbase + NST * STAGE);   // [64 q + lane]
     // block span [bs0, bs1); this wave's tile j covers rows r0 + 16 TST j + [0, 16)
     if (blockIdx.x == 0 && threadIdx.x < 64) store_head_maxima(a, b, threadIdx.x);
     const int64_t bs0 = (int64_t)blockIdx.x * STREAM_WAVES * 16 * tpw;
@@ -608,77 +635,116 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
         vrow[j] = R;
         voff[j] = (uint32_t)R * rowb + 16u * (uint32_t)((S + R) % N8);
     }
+    // loads of tile t into `stage`; rows past the span re-read its last row
     auto issue = [&](int t, int stage) {
         const uint8_t* tb = span + (int64_t)t * (TST * 16) * rowb;
         const int nv = (int)min((int64_t)16, bs1 - (r0 + (int64_t)(TST * 16) * t));   // rows of this tile
 #pragma unroll
         for (int j = 0; j < KS; ++j) {
             uint32_t o = voff[j];
-            if (nv < 16 && vrow[j] >= nv) o -= (uint32_t)(vrow[j] - (nv - 1)) * rowb;   // past-the-end rows re-read the last
+            if (nv < 16 && vrow[j] >= nv) o -= (uint32_t)(vrow[j] - (nv - 1)) * rowb;
             __builtin_amdgcn_global_load_lds((gbl_void_t*)(tb + o), (lds_void_t*)(wbase + stage * STAGE + 1024 * j),
                                              16, 0, 2 /* nt */);
         }
     };
-    for (int t = 0; t < NST && t < ntl; ++t) issue(t, t);
-
-    // operand fragments of tile t from its ring stage
-    auto read_tile = [&](int t, bf16x8_t (&x)[KS]) {
-        const uint8_t* st = wbase + (t % NST) * STAGE;
+    // loads of a tile that lies wholly inside the span
+    auto issue_full = [&](int t, int stage) {
+        const uint8_t* tb = span + (int64_t)t * (TST * 16) * rowb;
+#pragma unroll
+        for (int j = 0; j < KS; ++j)
+            __builtin_amdgcn_global_load_lds((gbl_void_t*)(tb + voff[j]),
+                                             (lds_void_t*)(wbase + stage * STAGE + 1024 * j), 16, 0, 2 /* nt */);
+    };
+    // operand fragments of the tile in `stage`
+    auto read_stage = [&](int stage, bf16x8_t (&x)[KS]) {
+        const uint8_t* st = wbase + stage * STAGE;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             const int S = (4 * ks + g - c + 16 * N8) % N8;
             x[ks] = *reinterpret_cast<const bf16x8_t*>(st + c * (2 * Gm::N) + 16 * S);
         }
     };
-    bf16x8_t xf[KS];
-    wait_tiles<KS, NST>(min(NST - 1, ntl - 1));
-    read_tile(0, xf);
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // stage read out before it is refilled
-    if (NST < ntl) issue(NST, 0);
-
-    TileOut to{-INFINITY, INFINITY, 0.f, 0.f};
-    float* kto = a.kt + (int64_t)b * a.A;
-    // the row held by this lane in 4-tile group q of the wave
-    auto group_row = [&](int q) { return r0 + (int64_t)(TST * 16) * (4 * q + g) + c; };
-    auto flush = [&](int q0, int nq) {
-        for (int q = 0; q < nq; ++q) {
-            const int64_t row = group_row(q0 + q);
-            const float k = s_res[64 * q + lane];
-            if (row < bs1) {
-                kto[row] = k;
-                if (a.key) a.key[(int64_t)b * a.A + row] = k;
-            }
-        }
-    };
-    // Per-lane partials of the four tiles of a group: pm = max over this
-    // lane's head slots, ps = sum of squares over this lane's dims.
-    float pm0 = -INFINITY, pm1 = -INFINITY, pm2 = -INFINITY, pm3 = -INFINITY;
-    float ps0 = 0.f, ps1 = 0.f, ps2 = 0.f, ps3 = 0.f;
-
-    for (int t = 0; t < ntl; ++t) {
-        // the matrix-core contraction of tile t (operands in xf) while tile
-        // t+1 is read out of the ring, then the per-lane partials of tile t
-        f32x4_t acc[HT];
+    // scores of this lane's head slots for the tile whose fragments are in x
+    auto contract = [&](const bf16x8_t (&x)[KS], f32x4_t (&acc)[HT]) {
 #pragma unroll
         for (int ht = 0; ht < HT; ++ht) acc[ht] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
             for (int ht = 0; ht < HT; ++ht)
-                acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[ht][ks], xf[ks], acc[ht], 0, 0, 0);
-        const float ps = row_sq<KS>(xf);
-        bf16x8_t xn[KS];
-        const bool more = t + 1 < ntl;
-        if (more) {
-            wait_tiles<KS, NST>(min(NST - 1, ntl - 2 - t));
-            read_tile(t + 1, xn);
-        }
-        // acc[ht][i] = score of head slot 16*ht + 4*g + i for row c of tile t
+                acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[ht][ks], x[ks], acc[ht], 0, 0, 0);
+    };
+    auto head_max = [&](const f32x4_t (&acc)[HT]) {
         float pm = -INFINITY;
 #pragma unroll
         for (int ht = 0; ht < HT; ++ht)
 #pragma unroll
             for (int i = 0; i < 4; ++i) pm = fmaxf(pm, acc[ht][i]);
+        return pm;
+    };
+    for (int t = 0; t < NST && t < ntl; ++t) issue(t, t);
+
+    TileOut to{-INFINITY, INFINITY, 0.f, 0.f};
+    // row of group q (tiles 4q..4q+3) held by this lane: row c of tile 4q + g
+    auto group_row = [&](int q) { return r0 + (int64_t)(TST * 16) * (4 * q + g) + c; };
+    auto group_out = [&](int q, float m, float s2) {
+        if (group_row(q) < bs1) {
+            to.nu2m = fmaxf(to.nu2m, s2);
+            to.kmax = fmaxf(to.kmax, m);
+            to.kmin = fminf(to.kmin, m);
+        }
+        s_key[64 * q + lane] = m;
+    };
+
+    bf16x8_t xf[KS];
+    wait_tiles<KS, NST>(min(NST - 1, ntl - 1));
+    read_stage(0, xf);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // stage read out before it is refilled
+    if (NST < ntl) issue(NST, 0);
+
+    // runs of RUN tiles whose look-ahead loads (up to tile RUN (s+1) + NST)
+    // stay inside the span: fixed stages, fixed wait counts
+    // (rows wider than 192 dims leave no registers for the unrolled run;
+    // those shapes take the run-time loop throughout)
+    const int nrun = (KS <= 6 && ntl > NST) ? (ntl - NST - 1) / RUN : 0;
+    for (int s = 0; s < nrun; ++s) {
+        float pmv[RUN], psv[RUN];
+#pragma unroll
+        for (int j = 0; j < RUN; ++j) {
+            f32x4_t acc[HT];
+            contract(xf, acc);
+            psv[j] = row_sq<KS>(xf);
+            __builtin_amdgcn_sched_barrier(0);
+            wait_vmcnt<(NST - 1) * KS>();
+            bf16x8_t xn[KS];
+            read_stage((j + 1) % NST, xn);
+            pmv[j] = head_max(acc);
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // stage read out before it is refilled
+            issue_full(RUN * s + j + 1 + NST, (j + 1) % NST);
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) xf[ks] = xn[ks];
+            __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int j4 = 0; j4 < RUN; j4 += 4)
+            group_out((RUN * s + j4) / 4, group_max(pmv[j4], pmv[j4 + 1], pmv[j4 + 2], pmv[j4 + 3]),
+                      group_sum(psv[j4], psv[j4 + 1], psv[j4 + 2], psv[j4 + 3]));
+    }
+
+    // the remaining tiles, with run-time stages and wait counts
+    float pm0 = -INFINITY, pm1 = -INFINITY, pm2 = -INFINITY, pm3 = -INFINITY;
+    float ps0 = 0.f, ps1 = 0.f, ps2 = 0.f, ps3 = 0.f;
+    for (int t = RUN * nrun; t < ntl; ++t) {
+        f32x4_t acc[HT];
+        contract(xf, acc);
+        const float ps = row_sq<KS>(xf);
+        bf16x8_t xn[KS];
+        const bool more = t + 1 < ntl;
+        if (more) {
+            wait_tiles<KS, NST>(min(NST - 1, ntl - 2 - t));
+            read_stage((t + 1) % NST, xn);
+        }
+        const float pm = head_max(acc);
         const int j = t & 3;
         if (j == 0) {
             pm1 = pm2 = pm3 = -INFINITY;
@@ -699,47 +765,29 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
             for (int ks = 0; ks < KS; ++ks) xf[ks] = xn[ks];
         }
         if (j != 3 && more) continue;
-        // reduce-scatter over the four 16-lane groups: afterwards lane 16j + c
-        // holds the maximum and the sum of squares of row c of tile 4q + j
-        const int q = t >> 2;
-        float m, s2;
-        {
-            auto sw32 = [](float x, float y) {
-                const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(y), false, false);
-                return f32x2_t{__uint_as_float(r[0]), __uint_as_float(r[1])};
-            };
-            auto sw16 = [](float x, float y) {
-                const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(y), false, false);
-                return f32x2_t{__uint_as_float(r[0]), __uint_as_float(r[1])};
-            };
-            f32x2_t u = sw32(pm0, pm2), v = sw32(pm1, pm3);
-            const float m02 = fmaxf(u[0], u[1]), m13 = fmaxf(v[0], v[1]);
-            u = sw16(m02, m13);
-            m = fmaxf(u[0], u[1]);
-            u = sw32(ps0, ps2);
-            v = sw32(ps1, ps3);
-            const float s02 = u[0] + u[1], s13 = v[0] + v[1];
-            u = sw16(s02, s13);
-            s2 = u[0] + u[1];
+        group_out(t >> 2, group_max(pm0, pm1, pm2, pm3), group_sum(ps0, ps1, ps2, ps3));
+    }
+    // the span's keys, each lane its own LDS words
+    float* kto = a.kt + (int64_t)b * a.A;
+    float* kuo = a.key ? a.key + (int64_t)b * a.A : nullptr;
+    for (int q = 0; q < (ntl + 3) / 4; ++q) {
+        const int64_t row = group_row(q);
+        if (row < bs1) {
+            const float m = s_key[64 * q + lane];
+            kto[row] = m;
+            if (kuo) kuo[row] = m;
         }
-        if (group_row(q) < bs1) {
-            to.nu2m = fmaxf(to.nu2m, s2);
-            to.kmax = fmaxf(to.kmax, m);
-            to.kmin = fminf(to.kmin, m);
-        }
-        const int qb = q % RES_GROUPS;
-        s_res[64 * qb + lane] = m;
-        if (qb == RES_GROUPS - 1 || !more) flush(q - qb, qb + 1);
     }
     score_finish(a, b, lane, to, false);
 }
 
-// tiles per wave: enough waves for two blocks per CU, spans of 8..512 tiles
+// tiles per wave: enough waves for two blocks per CU, spans of 8..STREAM_TPW_MAX tiles
+// (the key buffer in LDS holds STREAM_TPW_MAX tiles of keys per wave)
 static int stream_tpw(const ScoreArgs& a) {
     const int64_t tiles = (int64_t)a.B * ((a.A + 15) / 16);
     const int64_t waves = 2LL * 256 * STREAM_WAVES;
     int64_t tpw = (tiles + waves - 1) / waves;
-    tpw = tpw < 8 ? 8 : (tpw > 512 ? 512 : tpw);
+    tpw = tpw < 8 ? 8 : (tpw > STREAM_TPW_MAX ? STREAM_TPW_MAX : tpw);
     return (int)tpw;
 }
 
