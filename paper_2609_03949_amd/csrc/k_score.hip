@@ -7,9 +7,8 @@
 // (64 + r bf16 per row) from HBM and runs the heads x rows contraction on the
 // matrix cores (v_mfma_f32_16x16x32_bf16): A = qt (16 heads x 32 dims per
 // fragment, resident in VGPRs for the whole wave), B = 16 index rows x 32 dims
-// loaded straight from global memory in MFMA operand layout, so each lane
-// issues 16-byte loads of one row.  The heads maximum is taken in registers
-// (4 heads per lane per tile, then two cross-lane steps).
+// read from an LDS ring that direct global->LDS loads fill.  The heads maximum
+// is taken in registers (4 heads per lane per tile, then cross-lane steps).
 #include <type_traits>
 
 #include "vkv_internal.h"
@@ -19,104 +18,91 @@ namespace vkv {
 // ----------------------------------------------------------- query prep
 
 // Query prep, one kernel: w[b,h,j] = sum_i P[j,i] q_lat[b,h,i] (fp64, i
-// ascending), the query digest qt[b,h,off+j] = RNE_bf16(w) and the rope half of
-// qt, Nq[b,h] = ||q_lat||^2 (fp64, i ascending), and the head's certificate
-// scalars.  Each of w and Nq is a sequential chain of 512 fp64 FMAs; a block
-// owns QH heads of one sequence and all r basis rows, and its threads run 4
-// projection chains each (basis rows 2jp, 2jp+1 x heads 2hp, 2hp+1) while
-// wave 0 also runs the Nq chains.  P and the queries stay bf16 in LDS (direct
-// loads, a chunk of the i axis at a time) and are widened to fp64 in
-// registers: fp64 operands from LDS would otherwise bound the loop.  Block
+// ascending, one rounding per term), the query digest qt[b,h,off+j] =
+// RNE_bf16(w) and the rope half of qt, Nq[b,h] = ||q_lat||^2 (fp64, i
+// ascending), and the head's certificate scalars.  A block owns 16 heads of
+// one sequence.  The projection runs on the fp64 matrix cores: one
+// v_mfma_f64_16x16x4f64 per 4 consecutive i adds the 4 products to the
+// accumulator one after another in k order, each with a single rounding (the
+// same result bit for bit as the sequential FMA chain, checked on MI355X over
+// a million accumulations with inputs spread over 2^120), so a chain of 128
+// of them, i ascending, is the fp64 definition.  Wave w computes basis tile w
+// (16 heads x 16 basis rows) of the current chunk of 128 basis rows; wave 0
+// also runs the Nq chains on the vector unit between its matrix steps.  The
+// query rows and the chunk of P are staged as bf16 by direct loads into rows
+// padded to QP_ROW bytes, so the operand reads (16 rows, one 16-bit element
+// each) fall into distinct banks; they are widened in registers.  Block
 // (0,b) also clears the step state of sequence b.
-constexpr int QP_THREADS = 256;
-constexpr int QP_PBYTES = 65536;   // LDS for a chunk of P (bf16)
+constexpr int QP_ROW = 1040;          // LDS bytes per staged row of 512 bf16
+constexpr int QP_CHUNK_ROWS = 128;    // basis rows staged at a time: one 16-row tile per wave
+constexpr int QP_MAX_WAVES = QP_CHUNK_ROWS / 16;
 
-__host__ __device__ inline int qp_heads(int r) {
-    if (r <= 0) return 16;
-    int hb = (1024 / r) & ~1;
-    return hb < 2 ? 2 : (hb > 16 ? 16 : hb);
-}
-__host__ __device__ inline int qp_chunk(int r) {   // a power of two dividing 512
-    int ic = D_LAT;
-    while (ic > 8 && ic * r * 2 > QP_PBYTES) ic >>= 1;
-    return ic;
-}
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
 
-// slot of 16-byte piece ib (8 i) of LDS row j: XOR-swizzled so that the 16
-// rows 2jp (or 2jp+1, or 0..15) read by 16 lanes at one ib fall into distinct
-// bank groups
-__device__ __forceinline__ int qp_slot(int j, int ib, int per_row) {
-    const int m = (per_row < 16 ? per_row : 16) - 1;
-    return j * per_row + (ib ^ ((j >> 1) & m));
+__device__ __forceinline__ double bits_to_f64(uint16_t v) { return (double)__uint_as_float((uint32_t)v << 16); }
+
+__host__ __device__ inline int qp_waves(int r) {
+    const int t = r / 16;
+    return t < 1 ? 1 : (t > QP_MAX_WAVES ? QP_MAX_WAVES : t);
 }
 
-__global__ __launch_bounds__(QP_THREADS) void qprep_project_kernel(QprepArgs a) {
-    __shared__ __align__(16) uint8_t s_p[QP_PBYTES];            // P chunk, [j][i] bf16, swizzled
-    __shared__ __align__(16) uint8_t s_q[16 * D_LAT * 2];       // query chunk, [h][i] bf16
-    const int b = blockIdx.y;
-    const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+__global__ __launch_bounds__(64 * QP_MAX_WAVES) void qprep_project_kernel(QprepArgs a) {
+    __shared__ __align__(16) uint8_t s_q[16 * QP_ROW];              // the block's 16 query rows, [h][i]
+    __shared__ __align__(16) uint8_t s_p[QP_CHUNK_ROWS * QP_ROW];   // a chunk of P rows, then its w values
+    __shared__ double s_nq[16];
+    const int b = blockIdx.y, hb0 = 16 * blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int nw = blockDim.x >> 6;
     if (blockIdx.x == 0) {
         if (tid < SQ_WORDS) a.seq[b * SQ_WORDS + tid] = (tid == SQ_KMIN) ? 0xFFFFFFFFu : 0u;
     }
     const int r = (a.mode & 2) ? a.r : 0;
-    const int HB = qp_heads(r), IC = qp_chunk(r), PR = IC / 8;
-    const int hb0 = HB * blockIdx.x;
-    const bool proj = tid < HB * r / 4;   // threads whose chains are stored
-    const int rp = r > 0 ? r / 2 : 1;
-    const int jp = tid % rp, hp = tid / rp;
-    const int hpc = min(hp, HB / 2 - 1);  // the others repeat valid chains
-    const bool nqc = tid < HB;
-    double a00 = 0.0, a10 = 0.0, a01 = 0.0, a11 = 0.0, anq = 0.0;
-    auto wide = [](uint32_t w, int hi) { return (double)__uint_as_float(hi ? (w & 0xFFFF0000u) : (w << 16)); };
-    for (int c = 0; c < D_LAT / IC; ++c) {
-        // chunk c into LDS by direct loads: P pieces (row j, 8 i), then query pieces (head h, 8 i)
-        const int np = r * PR, nq = HB * PR;
-        for (int s0 = 64 * wave; s0 < np; s0 += QP_THREADS) {
-            const int sl = s0 + lane;   // np is a multiple of 64
-            const int j = sl / PR, ib = (sl % PR) ^ ((j >> 1) & ((PR < 16 ? PR : 16) - 1));
-            __builtin_amdgcn_global_load_lds(
-                (__attribute__((address_space(1))) void*)(a.P + (int64_t)j * D_LAT + IC * c + 8 * ib),
-                (__attribute__((address_space(3))) void*)(s_p + 16 * s0), 16, 0, 0);
-        }
-        for (int p = tid; p < nq; p += QP_THREADS) {
-            const int h = p / PR, ib = p % PR;
-            u16x8_t v = u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
-            if (hb0 + h < a.H)
-                v = *reinterpret_cast<const u16x8_t*>(a.q_lat + ((int64_t)b * a.H + hb0 + h) * D_LAT + IC * c + 8 * ib);
-            *reinterpret_cast<u16x8_t*>(s_q + 16 * qp_slot(h, ib, PR)) = v;
-        }
+    const int off = (a.mode & 1) ? D_ROPE : 0;
+    typedef __attribute__((address_space(3))) void lds_t;
+    typedef __attribute__((address_space(1))) void gbl_t;
+    // query rows: one 1 KB direct load per row; rows past H are zero
+    for (int row = wave; row < 16; row += nw) {
+        const int h = hb0 + row;
+        if (h < a.H)
+            __builtin_amdgcn_global_load_lds((gbl_t*)(a.q_lat + ((int64_t)b * a.H + h) * D_LAT + 8 * lane),
+                                             (lds_t*)(s_q + row * QP_ROW), 16, 0, 0);
+        else
+            *reinterpret_cast<u32x4_t*>(s_q + row * QP_ROW + 16 * lane) = u32x4_t{0u, 0u, 0u, 0u};
+    }
+    // operand rows of this lane: A = query row (lane mod 16), B = basis row
+    // 16 wave + (lane mod 16) of the chunk; element k = lane / 16 of each step
+    const uint16_t* qa = reinterpret_cast<const uint16_t*>(s_q + (lane & 15) * QP_ROW) + (lane >> 4);
+    const uint16_t* pb = reinterpret_cast<const uint16_t*>(s_p + (16 * wave + (lane & 15)) * QP_ROW) + (lane >> 4);
+    const uint16_t* qn = reinterpret_cast<const uint16_t*>(s_q + (lane & 15) * QP_ROW);   // Nq: head lane mod 16
+    double* s_w = reinterpret_cast<double*>(s_p);   // [16][QP_CHUNK_ROWS] w, then RNE(w), once the chunk is used
+    double* s_d = s_w + 16 * QP_CHUNK_ROWS;
+    double anq = 0.0;
+    // tail sums of lane 4 hl + t of wave 0, j ascending over all chunks:
+    // t=1 ||w||^2, t=2 ||qd - w||^2, t=3 ||qd||^2 (t=0 takes Nq at the end)
+    const int hl = lane >> 2, t = lane & 3;
+    double tsum = 0.0;
+    const int nchunk = (r + QP_CHUNK_ROWS - 1) / QP_CHUNK_ROWS;
+    for (int ch = 0; ch < (nchunk > 0 ? nchunk : 1); ++ch) {
+        const int j0 = ch * QP_CHUNK_ROWS;
+        const int nj = min(QP_CHUNK_ROWS, r - j0);   // basis rows of this chunk (<= 0 without a digest)
+        for (int row = wave; row < nj; row += nw)
+            __builtin_amdgcn_global_load_lds((gbl_t*)(a.P + (int64_t)(j0 + row) * D_LAT + 8 * lane),
+                                             (lds_t*)(s_p + row * QP_ROW), 16, 0, 0);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
-        // branch-free inner loops (wave-uniform choice): wave 0 also runs the
-        // Nq chains (lanes 0..15 own them; the others repeat them)
-        auto run = [&](auto with_proj, auto with_nq) {
-            constexpr bool WP = decltype(with_proj)::value, WN = decltype(with_nq)::value;
-            const u32x4_t* PP = reinterpret_cast<const u32x4_t*>(s_p);
-            const u32x4_t* Q = reinterpret_cast<const u32x4_t*>(s_q);
-            const int sj0 = 2 * jp, sj1 = 2 * jp + 1, sh0 = 2 * hpc, sh1 = 2 * hpc + 1, sn = lane & 15;
-#pragma unroll 2
-            for (int ib = 0; ib < PR; ++ib) {
-                u32x4_t p0{}, p1{}, q0{}, q1{}, qn{};
-                if constexpr (WP) {
-                    p0 = PP[qp_slot(sj0, ib, PR)];
-                    p1 = PP[qp_slot(sj1, ib, PR)];
-                    q0 = Q[qp_slot(sh0, ib, PR)];
-                    q1 = Q[qp_slot(sh1, ib, PR)];
-                }
-                if constexpr (WN) qn = Q[qp_slot(sn, ib, PR)];
+        const bool tile = 16 * wave < nj;
+        const bool nq = ch == 0 && wave == 0;
+        f64x4_t acc = f64x4_t{0.0, 0.0, 0.0, 0.0};
+        auto chain = [&](auto with_tile, auto with_nq) {
+            constexpr bool WT = decltype(with_tile)::value, WN = decltype(with_nq)::value;
+#pragma unroll 8
+            for (int s = 0; s < D_LAT / 4; ++s) {
+                if constexpr (WT) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(bits_to_f64(qa[4 * s]), bits_to_f64(pb[4 * s]),
+                                                                              acc, 0, 0, 0);
+                if constexpr (WN) {
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    if constexpr (WP) {
-                        const double x0 = wide(p0[e >> 1], e & 1), x1 = wide(p1[e >> 1], e & 1);
-                        const double y0 = wide(q0[e >> 1], e & 1), y1 = wide(q1[e >> 1], e & 1);
-                        a00 = fma(x0, y0, a00);
-                        a10 = fma(x1, y0, a10);
-                        a01 = fma(x0, y1, a01);
-                        a11 = fma(x1, y1, a11);
-                    }
-                    if constexpr (WN) {
-                        const double x = wide(qn[e >> 1], e & 1);
+                    for (int k = 0; k < 4; ++k) {
+                        const double x = bits_to_f64(qn[4 * s + k]);
                         anq = fma(x, x, anq);
                     }
                 }
@@ -124,47 +110,48 @@ __global__ __launch_bounds__(QP_THREADS) void qprep_project_kernel(QprepArgs a) 
         };
         using T_ = std::true_type;
         using F_ = std::false_type;
-        if (r > 0) {
-            if (wave == 0) run(T_{}, T_{});
-            else run(T_{}, F_{});
-        } else if (wave == 0) {
-            run(F_{}, T_{});
+        if (tile && nq) chain(T_{}, T_{});
+        else if (tile) chain(T_{}, F_{});
+        else if (nq) chain(F_{}, T_{});
+        __syncthreads();   // the chunk's rows are read out; its LDS takes the w values
+        if (tile) {
+            // acc[i] = w of head 4 i + lane / 16, basis row j0 + 16 wave + lane mod 16
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int hh = 4 * i + (lane >> 4), jl = 16 * wave + (lane & 15);
+                const double v = acc[i];
+                const uint16_t d = f64_to_bf16_rne(v);
+                s_w[hh * QP_CHUNK_ROWS + jl] = v;
+                s_d[hh * QP_CHUNK_ROWS + jl] = (double)bf16_to_f32(d);
+                if (hb0 + hh < a.H) a.qt[((int64_t)b * a.H + hb0 + hh) * a.n + off + j0 + jl] = d;
+            }
         }
+        if (nq && lane < 16) s_nq[lane] = anq;
         __syncthreads();
+        if (wave == 0 && t > 0 && nj > 0) {
+            const double* w = s_w + hl * QP_CHUNK_ROWS;
+            const double* dq = s_d + hl * QP_CHUNK_ROWS;
+            if (t == 1) {
+                for (int j = 0; j < nj; ++j) tsum = fma(w[j], w[j], tsum);
+            } else if (t == 2) {
+                for (int j = 0; j < nj; ++j) {
+                    const double ee = dq[j] - w[j];
+                    tsum = fma(ee, ee, tsum);
+                }
+            } else {
+                for (int j = 0; j < nj; ++j) tsum = fma(dq[j], dq[j], tsum);
+            }
+        }
+        __syncthreads();   // before the next chunk's rows overwrite the w values
     }
+    if (wave != 0) return;
     // certificate scalars of each head (fp32 upper bounds; Lemma (Index
     // certificate) plus the bf16 rounding of the stored sketch; fixed fp64
     // evaluation order, the same as the oracle's):
     //   a_h >= sqrt(q^T (I - P^T P) q),  n_h >= ||qd_h||,  e_h >= ||qd_h - P q||
-    // plus ||qt_h|| for the scorer's error bound.  w and Nq go through LDS (the
-    // P chunk is free); lane 4 hl + t of wave 0 runs sum t of head hl:
-    // t=0 Nq, t=1 ||w||^2, t=2 ||qd - w||^2, t=3 ||qd||^2 (j ascending).
-    const int off = (a.mode & 1) ? D_ROPE : 0;
-    double* s_w = reinterpret_cast<double*>(s_p);   // [HB][r] w, [HB][r] qd, then Nq[HB]
-    double* s_d = s_w + HB * r;
-    double* s_nq = s_d + HB * r;
-    if (nqc) s_nq[tid] = anq;
-    if (proj) {
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-            const int hl = 2 * hp + t;
-            const int h = hb0 + hl;
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                const int j = 2 * jp + u;
-                const double v = t ? (u ? a11 : a01) : (u ? a10 : a00);
-                const uint16_t d = f64_to_bf16_rne(v);
-                s_w[hl * r + j] = v;
-                s_d[hl * r + j] = (double)bf16_to_f32(d);
-                if (h < a.H) a.qt[((int64_t)b * a.H + h) * a.n + off + j] = d;
-            }
-        }
-    }
-    __syncthreads();
-    if (wave != 0) return;
-    const int hl = lane >> 2, t = lane & 3;
+    // plus ||qt_h|| for the scorer's error bound.
     const int h = hb0 + hl;
-    const bool have = hl < HB && h < a.H;
+    const bool have = h < a.H;
     const int64_t bhc = (int64_t)b * a.H + (have ? h : 0);
     // rope half of qt (8 pieces of 16 B per head, 4 lanes per head) and
     // ||q_rope||^2 (an upper-bound input only; order irrelevant)
@@ -183,26 +170,10 @@ __global__ __launch_bounds__(QP_THREADS) void qprep_project_kernel(QprepArgs a) 
     }
     r2 += __shfl_xor(r2, 1);
     r2 += __shfl_xor(r2, 2);
-    double acc = 0.0;
-    if (have) {
-        const double* w = s_w + hl * r;
-        const double* dq = s_d + hl * r;
-        if (t == 0) {
-            acc = s_nq[hl];
-        } else if (t == 1) {
-            for (int j = 0; j < r; ++j) acc = fma(w[j], w[j], acc);
-        } else if (t == 2) {
-            for (int j = 0; j < r; ++j) {
-                const double ee = dq[j] - w[j];
-                acc = fma(ee, ee, acc);
-            }
-        } else {
-            for (int j = 0; j < r; ++j) acc = fma(dq[j], dq[j], acc);
-        }
-    }
+    const double acc_t = t == 0 ? s_nq[hl] : tsum;
     const int base = lane & ~3;
-    const double Nq = __shfl(acc, base + 0), Nw = __shfl(acc, base + 1);
-    const double Ne = __shfl(acc, base + 2), Nd = __shfl(acc, base + 3);
+    const double Nq = __shfl(acc_t, base + 0), Nw = __shfl(acc_t, base + 1);
+    const double Ne = __shfl(acc_t, base + 2), Nd = __shfl(acc_t, base + 3);
     if (t == 0 && have) {
         const double G = CERT_G;
         const double Dm = G * (double)ru_sqrt_f32((double)r * Nq);
@@ -211,8 +182,8 @@ __global__ __launch_bounds__(QP_THREADS) void qprep_project_kernel(QprepArgs a) 
         const float ah = ru_sqrt_f32((X > 0.0 ? X : 0.0) * (1.0 + G));
         const float eh = ru_f32((double)ru_sqrt_f32(Ne) * (1.0 + G) + Dm);
         const float nh = ru_sqrt_f32(Nd * (1.0 + G));
-        const float qn = ru_sqrt_f32((r2 + Nd) * (1.0 + 0x1p-30));
-        reinterpret_cast<float4*>(a.hsc)[bhc] = make_float4(ah, nh, eh, qn);
+        const float qn2 = ru_sqrt_f32((r2 + Nd) * (1.0 + 0x1p-30));
+        reinterpret_cast<float4*>(a.hsc)[bhc] = make_float4(ah, nh, eh, qn2);
     }
 }
 
@@ -254,8 +225,8 @@ __device__ __forceinline__ void staged_head_maxima(const float4* s_hs, int n, fl
 
 hipError_t launch_qprep(const QprepArgs& a, hipStream_t s) {
     const int r = (a.mode & 2) ? a.r : 0;
-    dim3 g1((a.H + qp_heads(r) - 1) / qp_heads(r), a.B);
-    hipLaunchKernelGGL(qprep_project_kernel, g1, dim3(QP_THREADS), 0, s, a);
+    dim3 g1((a.H + 15) / 16, a.B);
+    hipLaunchKernelGGL(qprep_project_kernel, g1, dim3(64 * qp_waves(r)), 0, s, a);
     return hipGetLastError();
 }
 

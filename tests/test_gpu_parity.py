@@ -101,6 +101,67 @@ def test_digest_build_refuses_non_contractive_basis(ctx):
     assert torch.all(eta == 5.0) and torch.all(index.view(torch.int16) == 7)
 
 
+# ------------------------------------------------------------ query prep
+
+def _wide_bf16(rng, shape, lo, hi):
+    """bf16-representable values sign * (1 + m/128) * 2^e, e uniform in [lo, hi):
+    the fp64 sums of their products round at many steps, so a summation
+    order other than i ascending changes some results."""
+    m = rng.integers(0, 128, shape)
+    e = rng.integers(lo, hi, shape)
+    sg = rng.choice([-1.0, 1.0], shape)
+    return torch.from_numpy((sg * np.ldexp(1.0 + m / 128.0, e)).astype(np.float32)).to(torch.bfloat16)
+
+
+@pytest.mark.parametrize("mode,r", [(synth.MODE_ROPE_DIGEST, 64), (synth.MODE_ROPE_DIGEST, 160),
+                                    (synth.MODE_DIGEST, 512), (synth.MODE_ROPE, 0)])
+def test_query_prep_bit_exact_under_rounding(ctx, mode, r):
+    """qt and the head certificate scalars against the oracle, bit for bit, with
+    queries and basis spread over 2^60: the projection and ||q||^2 are fp64
+    chains with i ascending (white-box: qt and the scalars are read from the
+    first two regions of the workspace)."""
+    say(f"query prep rounding mode={mode} r={r}")
+    rng = np.random.default_rng(11 + r)
+    B, H, T = 2, 24, 64
+    q_lat = _wide_bf16(rng, (B, H, 512), -30, 30)
+    q_rope = _wide_bf16(rng, (B, H, 64), -8, 8)
+    P = _wide_bf16(rng, (max(r, 1), 512), -20, 20) if r else None
+    cache = torch.from_numpy(rng.standard_normal((B, T, 576)).astype(np.float32)).to(torch.bfloat16)
+    dev = "cuda"
+    q_lat, q_rope, cache = q_lat.to(dev), q_rope.to(dev), cache.to(dev)
+    Pd = P.to(dev) if P is not None else None
+    cols, has_rope = index_cols(mode, r)
+    index = torch.zeros(B, T, cols, dtype=torch.bfloat16, device=dev) if cols else None
+    step = vkv.Step(cache, q_lat, q_rope, 0, mode, r, index=index, index_has_rope=has_rope, P=Pd)
+    ws = vkv.alloc_workspace(step, 1)
+    vkv.query_prep(ctx, step, ws)
+    torch.cuda.synchronize()
+    n = (64 if mode & 1 else 0) + (r if mode & 2 else 0)
+    nb = B * H * n * 2
+    qt = ws[:nb].cpu().numpy().view(np.uint16).reshape(B, H, n)
+    h0 = (nb + 255) // 256 * 256
+    hsc = ws[h0:h0 + B * H * 16].cpu().numpy().view(np.float32).reshape(B, H, 4)
+    Pb = synth.to_numpy_bits(P) if P is not None else None
+    qt_o, a_o, n_o, e_o = oracle.query_prep(synth.to_numpy_bits(q_lat.cpu()), synth.to_numpy_bits(q_rope.cpu()),
+                                            Pb, r, mode)
+    assert np.array_equal(qt, qt_o)
+    assert np.array_equal(hsc[..., 0], a_o)
+    assert np.array_equal(hsc[..., 1], n_o)
+    assert np.array_equal(hsc[..., 2], e_o)
+    if r:
+        # the inputs do separate summation orders: the sequential fp64 sums
+        # (products exact, one rounding per term) differ from a blocked order
+        ql = q_lat.cpu().float().numpy().astype(np.float64)
+        Pf = P.float().numpy().astype(np.float64)
+        w_seq = np.zeros((B, H, r))
+        for i in range(512):
+            w_seq = w_seq + ql[:, :, i:i + 1] * Pf[None, None, :, i]
+        w_blk = np.zeros((B, H, r))
+        for i0 in range(0, 512, 64):
+            w_blk = w_blk + np.einsum("bhi,ji->bhj", ql[:, :, i0:i0 + 64], Pf[:, i0:i0 + 64])
+        assert np.count_nonzero(w_seq != w_blk) > 0
+
+
 # ------------------------------------------------------ reduced configs
 
 REDUCED = [
