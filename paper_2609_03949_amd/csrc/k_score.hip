@@ -24,9 +24,10 @@ namespace vkv {
 // one sequence.  The projection runs on the fp64 matrix cores: one
 // v_mfma_f64_16x16x4f64 per 4 consecutive i adds the 4 products to the
 // accumulator one after another in k order, each with a single rounding (the
-// same result bit for bit as the sequential FMA chain, checked on MI355X over
-// a million accumulations with inputs spread over 2^120), so a chain of 128
-// of them, i ascending, is the fp64 definition.  Wave w computes basis tile w
+// same bits as the sequential FMA chain; the GPU tests compare the digest with
+// the fp64 oracle on inputs spread over 2^60, where other summation orders
+// give other bits), so a chain of 128 of them, i ascending, is the fp64
+// definition.  Wave w computes basis tile w
 // (16 heads x 16 basis rows) of the current chunk of 128 basis rows; wave 0
 // also runs the Nq chains on the vector unit between its matrix steps.  The
 // query rows and the chunk of P are staged as bf16 by direct loads into rows
