@@ -6,110 +6,167 @@
 // in one rounding, then the upper bounds
 //   eta_u >= sqrt(c^T (I - P^T P) c),  eps_u >= ||d - P c||,  gamma_u >= ||P c||
 // evaluated in a fixed fp64 order and rounded toward +inf.  Not on the
-// per-step path.  A block owns 32 rows; the basis is held
-// transposed in LDS, 64 columns at a time.
+// per-step path.
+//
+// The projection runs on the fp64 matrix cores: v_mfma_f64_16x16x4f64 adds its
+// 4 products (k = 0..3) to the accumulator one after another, each with a
+// single rounding, so 128 of them with i ascending give the sequential fp64
+// sum bit for bit (bf16 products are exact in fp64).  A block owns DG_ROWS
+// consecutive rows of one sequence and takes the basis in chunks of 64 rows
+// (one 16-row tile per wave): each chunk is staged once in LDS, and the
+// block's rows stream past it 16 at a time (double-buffered: the next tile is
+// loaded into registers during the current tile's chain).
+// Rows and basis rows sit in LDS rows padded to DG_ROW bytes, so the operand
+// reads (16 rows, one 16-bit element each) fall into distinct banks.  The
+// row sums over j (||y||^2, ||d - y||^2) continue chunk after chunk in j
+// order; ||c||^2 runs on the vector unit of wave 0 between its matrix steps.
+#include <type_traits>
+
 #include "vkv_internal.h"
 
 namespace vkv {
 
 constexpr int DG_THREADS = 256;
+constexpr int DG_ROW = 1040;       // LDS bytes per staged row of 512 bf16
+constexpr int DG_CHUNK = 64;       // basis rows per chunk: 16 per wave
+constexpr int DG_ROWS = 512;       // cache rows per block (32 tiles of 16)
 
-__global__ __launch_bounds__(DG_THREADS) void digest_kernel(DigestArgs a, int rows_per_block) {
-    extern __shared__ __align__(16) unsigned char smem[];
-    uint16_t(*s_pt)[66] = reinterpret_cast<uint16_t(*)[66]>(smem);                       // [512][66]
-    double(*s_c)[D_LAT] = reinterpret_cast<double(*)[D_LAT]>(smem + D_LAT * 66 * 2);     // [4][512]
-    double(*s_y)[64] = reinterpret_cast<double(*)[64]>(smem + D_LAT * 66 * 2 + 4 * D_LAT * 8);  // [R][64]
+typedef __attribute__((address_space(3))) void dg_lds_t;
+typedef __attribute__((address_space(1))) void dg_gbl_t;
+
+__global__ __launch_bounds__(DG_THREADS) void digest_kernel(DigestArgs a) {
+    __shared__ __align__(16) uint8_t s_p[DG_CHUNK * DG_ROW];        // a chunk of basis rows
+    __shared__ __align__(16) uint8_t s_c[2][16 * DG_ROW];           // two tiles of cache rows
+    __shared__ double s_y[16][DG_CHUNK];                            // y of the current tile and chunk
+    __shared__ double s_acc[DG_ROWS][2];                            // running ||y||^2, ||d - y||^2
+    __shared__ double s_nc[DG_ROWS];                                // ||c||^2
 
     const int b = blockIdx.y;
-    const int tid = threadIdx.x;
-    const int64_t u0 = (int64_t)blockIdx.x * rows_per_block;
-    const int nrows = (int)min((int64_t)rows_per_block, a.T - u0);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t u0 = (int64_t)blockIdx.x * DG_ROWS;
+    const int nrows = (int)min((int64_t)DG_ROWS, a.T - u0);
     if (nrows <= 0) return;
+    const int ntile = (nrows + 15) / 16;
     const uint16_t* cb = a.cache + (int64_t)b * a.cbs;
     uint16_t* ib = a.index ? a.index + (int64_t)b * a.ibs : nullptr;
     const int off = a.with_rope ? D_ROPE : 0;
+    const bool cert = a.eta != nullptr;
+    for (int i = tid; i < DG_ROWS; i += DG_THREADS) s_acc[i][0] = s_acc[i][1] = 0.0;
 
-    // running sums of the row owners (thread rho < nrows), in j order
-    double Ny = 0.0, Ne = 0.0;
-
-    const int ntile = (a.r + 63) / 64;
-    for (int jt = 0; jt < ntile; ++jt) {
-        const int j0 = 64 * jt;
-        const int jn = min(64, a.r - j0);
-        __syncthreads();
-        for (int idx = tid; idx < jn * D_LAT; idx += DG_THREADS) {
-            const int jl = idx / D_LAT, i = idx % D_LAT;
-            s_pt[i][jl] = a.P[(int64_t)(j0 + jl) * D_LAT + i];
+    // tile t of the block's rows into buffer t & 1 (4 rows per wave, one 1 KB
+    // load each); rows past T are zero
+    auto stage_tile = [&](int t) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int rl = 4 * wave + q, rr = 16 * t + rl;
+            uint8_t* dst = s_c[t & 1] + rl * DG_ROW;
+            if (rr < nrows)
+                __builtin_amdgcn_global_load_lds((dg_gbl_t*)(cb + (u0 + rr) * a.cs + 8 * lane), (dg_lds_t*)dst, 16, 0, 0);
+            else
+                *reinterpret_cast<u32x4_t*>(dst + 16 * lane) = u32x4_t{0u, 0u, 0u, 0u};
         }
-        for (int rg = 0; rg < nrows; rg += 4) {
-            __syncthreads();
-            for (int idx = tid; idx < 4 * D_LAT; idx += DG_THREADS) {
-                const int rl = idx / D_LAT, i = idx % D_LAT;
-                const int rr = rg + rl;
-                s_c[rl][i] = (rr < nrows) ? (double)bf16_to_f32(cb[(u0 + rr) * a.cs + i]) : 0.0;
+    };
+    const int nchunk = a.r > 0 ? (a.r + DG_CHUNK - 1) / DG_CHUNK : 1;
+    for (int ch = 0; ch < nchunk; ++ch) {
+        const int j0 = ch * DG_CHUNK;
+        const int jn = a.r > 0 ? min(DG_CHUNK, a.r - j0) : 0;
+        __syncthreads();   // the previous chunk's reads of s_p and s_c are done
+        for (int row = wave; row < jn; row += DG_THREADS / 64)
+            __builtin_amdgcn_global_load_lds((dg_gbl_t*)(a.P + (int64_t)(j0 + row) * D_LAT + 8 * lane),
+                                             (dg_lds_t*)(s_p + row * DG_ROW), 16, 0, 0);
+        stage_tile(0);
+        const bool tile = 16 * wave < jn;
+        const bool nc = ch == 0 && wave == 0 && cert;
+        // operand rows: A = cache row (lane mod 16) of the tile, B = basis row
+        // 16 wave + (lane mod 16) of the chunk; element k = lane / 16 of each step
+        const uint16_t* pb = reinterpret_cast<const uint16_t*>(s_p + (16 * wave + (lane & 15)) * DG_ROW) + (lane >> 4);
+        for (int t = 0; t < ntile; ++t) {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();   // tile t (and the chunk) landed; buffer (t+1)&1 and s_y are free
+            // tile t+1 into registers now, into LDS after the chain: no direct
+            // load into LDS is in flight while the chain reads it, so the
+            // compiler's LDS wait counts stay exact
+            u32x4_t nx[4];
+            const bool more = t + 1 < ntile;
+            if (more) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int rr = 16 * (t + 1) + 4 * wave + q;
+                    nx[q] = rr < nrows ? *reinterpret_cast<const u32x4_t*>(cb + (u0 + rr) * a.cs + 8 * lane)
+                                       : u32x4_t{0u, 0u, 0u, 0u};
+                }
             }
-            __syncthreads();
-            const int rl = tid >> 6, jl = tid & 63;
-            const int rr = rg + rl;
-            if (rr < nrows && jl < jn) {
-                double acc = 0.0;
-                for (int i = 0; i < D_LAT; ++i) acc = fma((double)bf16_to_f32(s_pt[i][jl]), s_c[rl][i], acc);
-                s_y[rr][jl] = acc;
-                if (ib) ib[(u0 + rr) * a.is + off + j0 + jl] = f64_to_bf16_rne(acc);
+            const uint16_t* ca = reinterpret_cast<const uint16_t*>(s_c[t & 1] + (lane & 15) * DG_ROW) + (lane >> 4);
+            const uint16_t* cn = reinterpret_cast<const uint16_t*>(s_c[t & 1] + (lane & 15) * DG_ROW);
+            f64x4_t acc = f64x4_t{0.0, 0.0, 0.0, 0.0};
+            double anc = 0.0;
+            if (tile && nc) acc = mfma_f64_rowdot512<true>(ca, pb, cn, anc);
+            else if (tile) acc = mfma_f64_rowdot512<false>(ca, pb, cn, anc);
+            else if (nc) {
+                for (int i = 0; i < D_LAT; ++i) {
+                    const double x = bf16_bits_f64(cn[i]);
+                    anc = fma(x, x, anc);
+                }
             }
-        }
-        __syncthreads();
-        if (tid < nrows) {
-            for (int jl = 0; jl < jn; ++jl) {
-                const double y = s_y[tid][jl];
-                Ny = fma(y, y, Ny);
+            if (more) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    *reinterpret_cast<u32x4_t*>(s_c[(t + 1) & 1] + (4 * wave + q) * DG_ROW + 16 * lane) = nx[q];
             }
-            for (int jl = 0; jl < jn; ++jl) {
-                const double y = s_y[tid][jl];
-                const double t = (double)bf16_to_f32(f64_to_bf16_rne(y)) - y;
-                Ne = fma(t, t, Ne);
+            if (nc && lane < 16 && 16 * t + lane < nrows) s_nc[16 * t + lane] = anc;
+            if (tile) {
+                // acc[i] = y of tile row 4 i + lane / 16, basis row j0 + 16 wave + lane mod 16
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int rl = 4 * i + (lane >> 4), jl = 16 * wave + (lane & 15);
+                    const double y = acc[i];
+                    s_y[rl][jl] = y;
+                    const int rr = 16 * t + rl;
+                    if (ib && rr < nrows) ib[(u0 + rr) * a.is + off + j0 + jl] = f64_to_bf16_rne(y);
+                }
+            }
+            if (ch == 0 && ib && a.with_rope) {
+                // branch copy (the exact summand of every future logit): 16 rows x 128 B
+                const int rl = tid >> 4, p = tid & 15;
+                const int rr = 16 * t + rl;
+                if (p < D_ROPE / 8 && rr < nrows)
+                    *reinterpret_cast<u16x8_t*>(ib + (u0 + rr) * a.is + 8 * p) =
+                        *reinterpret_cast<const u16x8_t*>(cb + (u0 + rr) * a.cs + D_LAT + 8 * p);
+            }
+            if (!cert) continue;
+            __syncthreads();   // s_y complete
+            if (wave == 0 && lane < 32) {
+                // lane rl + 16 m continues sum m of tile row rl over this chunk's j, ascending
+                const int rl = lane & 15, m = lane >> 4, rr = 16 * t + rl;
+                double sacc = rr < nrows ? s_acc[rr][m] : 0.0;
+                for (int jl = 0; jl < jn; ++jl) {
+                    const double y = s_y[rl][jl];
+                    const double v = m ? (double)bf16_to_f32(f64_to_bf16_rne(y)) - y : y;
+                    sacc = fma(v, v, sacc);
+                }
+                if (rr < nrows) s_acc[rr][m] = sacc;
             }
         }
     }
-    // branch copy (the exact summand of every future logit)
-    if (ib && a.with_rope) {
-        for (int idx = tid; idx < nrows * (D_ROPE / 8); idx += DG_THREADS) {
-            const int rr = idx / (D_ROPE / 8), p = idx % (D_ROPE / 8);
-            *reinterpret_cast<u16x8_t*>(ib + (u0 + rr) * a.is + 8 * p) =
-                *reinterpret_cast<const u16x8_t*>(cb + (u0 + rr) * a.cs + D_LAT + 8 * p);
-        }
-    }
-    if (a.eta && tid < nrows) {
-        const uint16_t* c = cb + (u0 + tid) * a.cs;
-        double Nc = 0.0;
-        for (int i = 0; i < D_LAT; ++i) {
-            const double v = (double)bf16_to_f32(c[i]);
-            Nc = fma(v, v, Nc);
-        }
+    if (!cert) return;
+    __syncthreads();
+    for (int rr = tid; rr < nrows; rr += DG_THREADS) {
+        const double Nc = s_nc[rr], Ny = s_acc[rr][0], Ne = s_acc[rr][1];
         const double G = CERT_G;
         const double Dm = G * (double)ru_sqrt_f32((double)a.r * Nc);
         const double sy = (double)ru_sqrt_f32(Ny);
         const double X = ((Nc - Ny) + G * (Nc + Ny)) + (2.0 * Dm) * sy;
-        const int64_t o = (int64_t)b * a.T + u0 + tid;
+        const int64_t o = (int64_t)b * a.T + u0 + rr;
         a.eta[o] = ru_sqrt_f32((X > 0.0 ? X : 0.0) * (1.0 + G));
         a.eps[o] = ru_f32((double)ru_sqrt_f32(Ne) * (1.0 + G) + Dm);
         a.gam[o] = ru_f32(sy * (1.0 + G) + Dm);
     }
 }
 
-static size_t digest_smem(int rows_per_block) {
-    return (size_t)D_LAT * 66 * 2 + 4 * D_LAT * 8 + (size_t)rows_per_block * 64 * 8;
-}
-
 hipError_t launch_digest(const DigestArgs& a, hipStream_t s) {
     if (a.T <= 0) return hipSuccess;
-    const int rpb = 32;
-    const size_t sm = digest_smem(rpb);
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(digest_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
-    if (e != hipSuccess) return e;
-    dim3 grid((unsigned)((a.T + rpb - 1) / rpb), (unsigned)a.B);
-    hipLaunchKernelGGL(digest_kernel, grid, dim3(DG_THREADS), sm, s, a, rpb);
+    dim3 grid((unsigned)((a.T + DG_ROWS - 1) / DG_ROWS), (unsigned)a.B);
+    hipLaunchKernelGGL(digest_kernel, grid, dim3(DG_THREADS), 0, s, a);
     return hipGetLastError();
 }
 

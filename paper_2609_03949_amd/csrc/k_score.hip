@@ -38,10 +38,6 @@ constexpr int QP_ROW = 1040;          // LDS bytes per staged row of 512 bf16
 constexpr int QP_CHUNK_ROWS = 128;    // basis rows staged at a time: one 16-row tile per wave
 constexpr int QP_MAX_WAVES = QP_CHUNK_ROWS / 16;
 
-typedef double f64x4_t __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ double bits_to_f64(uint16_t v) { return (double)__uint_as_float((uint32_t)v << 16); }
-
 __host__ __device__ inline int qp_waves(int r) {
     const int t = r / 16;
     return t < 1 ? 1 : (t > QP_MAX_WAVES ? QP_MAX_WAVES : t);
@@ -94,26 +90,14 @@ __global__ __launch_bounds__(64 * QP_MAX_WAVES) void qprep_project_kernel(QprepA
         const bool tile = 16 * wave < nj;
         const bool nq = ch == 0 && wave == 0;
         f64x4_t acc = f64x4_t{0.0, 0.0, 0.0, 0.0};
-        auto chain = [&](auto with_tile, auto with_nq) {
-            constexpr bool WT = decltype(with_tile)::value, WN = decltype(with_nq)::value;
-#pragma unroll 8
-            for (int s = 0; s < D_LAT / 4; ++s) {
-                if constexpr (WT) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(bits_to_f64(qa[4 * s]), bits_to_f64(pb[4 * s]),
-                                                                              acc, 0, 0, 0);
-                if constexpr (WN) {
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        const double x = bits_to_f64(qn[4 * s + k]);
-                        anq = fma(x, x, anq);
-                    }
-                }
+        if (tile && nq) acc = mfma_f64_rowdot512<true>(qa, pb, qn, anq);
+        else if (tile) acc = mfma_f64_rowdot512<false>(qa, pb, qn, anq);
+        else if (nq) {
+            for (int i = 0; i < D_LAT; ++i) {
+                const double x = bf16_bits_f64(qn[i]);
+                anq = fma(x, x, anq);
             }
-        };
-        using T_ = std::true_type;
-        using F_ = std::false_type;
-        if (tile && nq) chain(T_{}, T_{});
-        else if (tile) chain(T_{}, F_{});
-        else if (nq) chain(F_{}, T_{});
+        }
         __syncthreads();   // the chunk's rows are read out; its LDS takes the w values
         if (tile) {
             // acc[i] = w of head 4 i + lane / 16, basis row j0 + 16 wave + lane mod 16

@@ -243,4 +243,64 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_admit(const SelectArgs& a, hipStream_t s);
 hipError_t launch_attend(const AttendArgs& a, hipStream_t s);
 
+// ------------------------------------------- fp64 matrix-core row products
+
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ double bf16_bits_f64(uint16_t v) { return (double)__uint_as_float((uint32_t)v << 16); }
+
+// One 16x16 tile of fp64 row products over 512 dims, i ascending:
+//   D[m][n] = sum_{i<512} A[m][i] B[n][i]
+// with A, B rows of bf16 staged in LDS.  v_mfma_f64_16x16x4f64 adds its four
+// products (k = 0..3) to the accumulator one after another, each with one
+// rounding, so 128 of them in i order give the sequential fp64 sum (bf16
+// products are exact in fp64).  pa / pb point at element lane / 16 of this
+// lane's A row (lane mod 16) and B row; step s reads element 4 s of each.
+// Result: lane l, element e = D[4 e + l / 16][l mod 16].  With WN the vector
+// unit also accumulates n2 += x^2 over pn[0..512) in order (one fp64 FMA per
+// element, between the matrix steps).  The operand reads of each group of 4
+// steps are issued one group ahead (scheduling barriers keep them there; at
+// most 10 reads are then younger than the awaited ones, within the range of
+// an lgkmcnt wait).
+template <bool WN>
+__device__ __forceinline__ f64x4_t mfma_f64_rowdot512(const uint16_t* pa, const uint16_t* pb, const uint16_t* pn,
+                                                      double& n2) {
+    constexpr int G = 4, NG = 512 / 4 / G;
+    f64x4_t acc = f64x4_t{0.0, 0.0, 0.0, 0.0};
+    uint16_t ra[2][G], rb[2][G];
+    u16x8_t rn[2][G / 2];
+    auto load = [&](int g, int buf) {
+#pragma unroll
+        for (int e = 0; e < G; ++e) {
+            ra[buf][e] = pa[4 * (G * g + e)];
+            rb[buf][e] = pb[4 * (G * g + e)];
+        }
+        if constexpr (WN) {
+#pragma unroll
+            for (int e = 0; e < G / 2; ++e) rn[buf][e] = *reinterpret_cast<const u16x8_t*>(pn + 4 * G * g + 8 * e);
+        }
+    };
+    load(0, 0);
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+        if (g + 1 < NG) load(g + 1, (g + 1) & 1);
+        __builtin_amdgcn_sched_barrier(0);
+        const int buf = g & 1;
+#pragma unroll
+        for (int e = 0; e < G; ++e) {
+            acc = __builtin_amdgcn_mfma_f64_16x16x4f64(bf16_bits_f64(ra[buf][e]), bf16_bits_f64(rb[buf][e]), acc, 0, 0,
+                                                      0);
+            if constexpr (WN) {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const double x = bf16_bits_f64(rn[buf][e / 2][4 * (e & 1) + k]);
+                    n2 = fma(x, x, n2);
+                }
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    return acc;
+}
+
 }  // namespace vkv

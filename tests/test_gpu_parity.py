@@ -86,6 +86,43 @@ def test_digest_build_bit_exact(ctx, basis, r, with_rope):
         assert np.array_equal(gam.cpu().numpy().view(np.uint32), og.view(np.uint32))
 
 
+@pytest.mark.parametrize("r,cert", [(160, True), (64, False)])
+def test_digest_build_bit_exact_under_rounding(ctx, r, cert):
+    """Index digests and row scalars against the oracle, bit for bit, with latent
+    rows spread over 2^60 and a small-entry basis (contractive, so the
+    certificate mode runs): the fp64 sums round at many steps, so only the
+    i-ascending order reproduces them."""
+    say(f"digest_build rounding r={r} cert={cert}")
+    rng = np.random.default_rng(5 + r)
+    B, T = 2, 700
+    cache = _wide_bf16(rng, (B, T, 576), -30, 30).cuda()
+    P = _wide_bf16(rng, (r, 512), -24, -14).cuda()
+    index = torch.empty(B, T, 64 + r, dtype=torch.bfloat16, device="cuda")
+    eta = torch.empty(B, T, device="cuda") if cert else None
+    eps = torch.empty(B, T, device="cuda") if cert else None
+    gam = torch.empty(B, T, device="cuda") if cert else None
+    vkv.digest_build(ctx, cache, P, r, True, index, eta, eps, gam)
+    torch.cuda.synchronize()
+    ci = synth.to_numpy_bits(cache)
+    Pi = synth.to_numpy_bits(P)
+    oi, oe, oep, og = oracle.digest_build(ci, Pi, r, with_rope=True, scalars=cert)
+    assert np.array_equal(synth.to_numpy_bits(index), oi)
+    if cert:
+        assert np.array_equal(eta.cpu().numpy().view(np.uint32), oe.view(np.uint32))
+        assert np.array_equal(eps.cpu().numpy().view(np.uint32), oep.view(np.uint32))
+        assert np.array_equal(gam.cpu().numpy().view(np.uint32), og.view(np.uint32))
+    # the inputs separate summation orders (sequential vs blocked fp64 sums)
+    c = cache[0, :64, :512].cpu().float().numpy().astype(np.float64)
+    Pf = P.cpu().float().numpy().astype(np.float64)
+    y_seq = np.zeros((64, r))
+    for i in range(512):
+        y_seq = y_seq + c[:, i:i + 1] * Pf[None, :, i]
+    y_blk = np.zeros((64, r))
+    for i0 in range(0, 512, 64):
+        y_blk = y_blk + c[:, i0:i0 + 64] @ Pf[:, i0:i0 + 64].T
+    assert np.count_nonzero(y_seq != y_blk) > 0
+
+
 def test_digest_build_refuses_non_contractive_basis(ctx):
     say("digest_build non-contractive")
     wl = synth.make_workload(synth.CONFIGS["cfg0"].with_(H=2), "cuda", T=256)
