@@ -427,6 +427,40 @@ def test_cancellation_heavy_scores_stay_within_bound(ctx):
     check_step(wl, g, o, [0])
 
 
+@pytest.mark.parametrize("mode,r,H,B,T", [
+    (synth.MODE_ROPE_DIGEST, 64, 128, 2, 9000),     # 128 dims, the scan's main shape
+    (synth.MODE_ROPE, 0, 128, 2, 7001),             # 64 dims, ragged archive
+    (synth.MODE_ROPE_DIGEST, 128, 64, 2, 5003),     # 192 dims
+    (synth.MODE_DIGEST, 256, 32, 1, 4000),          # 256 dims (run-time loop only)
+    (synth.MODE_ROPE_DIGEST, 64, 16, 2, 262144),    # long spans: many four-tile runs per wave
+])
+def test_every_key_within_certified_bound(ctx, mode, r, H, B, T):
+    """key~ of every archived row against the oracle's exact key, within the
+    documented bound E = 2 (n + n/32) 2^-23 max_h ||qt_h|| max_u ||x_u||: a key
+    lost, misplaced or mis-computed anywhere in a span would break it."""
+    say(f"keys within bound mode={mode} r={r} H={H} B={B} T={T}")
+    cfg = synth.CONFIGS["cfg4"].with_(mode=mode, r=r, H=H)
+    wl = synth.make_workload(cfg, "cuda", B=B, T=T)
+    k = max(1, wl["A"] // 32)
+    g, _ = gpu_step(ctx, wl, k=k)
+    seqs = list(range(B))
+    o, (cache, q_lat, q_rope, P, index, *_rest) = oracle_step(wl, seqs, k=k)
+    rr = r if mode != synth.MODE_ROPE else 0
+    cols, has_rope = index_cols(mode, r)
+    qt, *_ = oracle.query_prep(q_lat, q_rope, P, rr, mode)
+    A = wl["A"]
+    for j, b in enumerate(seqs):
+        x = oracle.index_rows(cache[j], index[j] if index is not None else None, mode, rr, has_rope)
+        n = x.shape[1]
+        qn = np.linalg.norm(oracle.decode_bf16(qt[j]), axis=1).max()
+        xn = np.linalg.norm(oracle.decode_bf16(x[:A]), axis=1).max()
+        E = 2 * (n + n / 32) * 2.0 ** -23 * qn * xn
+        err = np.abs(g["key"][b, :A].astype(np.float64) - o[b]["key"])
+        say(f"  seq {b}: max |key~ - key| {err.max():.3e}, bound {E:.3e}")
+        assert np.all(err <= E), (b, int(np.argmax(err)), err.max(), E)
+    check_step(wl, g, o, seqs)
+
+
 def test_determinism(ctx):
     say("determinism")
     cfg = synth.CONFIGS["cfg3"].with_(H=16)
