@@ -284,111 +284,6 @@ __device__ __forceinline__ void score_finish(const ScoreArgs& a, int b, int lane
     }
 }
 
-// HT head tiles of 16 and KS dim steps of 32 held in VGPRs (HT*KS <= 32).
-// Head slots beyond H repeat a real head (h mod H), which leaves the maximum
-// over heads unchanged and needs no masking in the loop.
-template <int HT, int KS, bool UB>
-__global__ __launch_bounds__(256, 2) void score_kernel(ScoreArgs a) {
-    __shared__ float4 s_hs[UB ? 128 : 1];
-    const int b = blockIdx.y;
-    const int tid = threadIdx.x;
-    const int wave = tid >> 6, lane = tid & 63, g = lane >> 4, c = lane & 15;
-    if (UB) {
-        for (int h = tid; h < 16 * HT; h += 256)
-            s_hs[h] = reinterpret_cast<const float4*>(a.hsc)[(int64_t)b * a.H + (h % a.H)];
-        __syncthreads();
-    }
-    if (blockIdx.x == 0 && threadIdx.x < 64) store_head_maxima(a, b, threadIdx.x);
-    const int64_t r0 = ((int64_t)blockIdx.x * 4 + wave) * (16 * SCORE_TPW);
-    if (r0 >= a.A) return;
-    const int64_t rend = min(a.A, r0 + (int64_t)(16 * SCORE_TPW));
-    const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-
-    bf16x8_t qf[HT][KS];
-    const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
-#pragma unroll
-    for (int ht = 0; ht < HT; ++ht) {
-        const int h = (16 * ht + c) % a.H;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            qf[ht][ks] = *reinterpret_cast<const bf16x8_t*>(qtb + (int64_t)h * a.n + 32 * ks + 8 * g);
-    }
-    const uint16_t* xb = a.x + (int64_t)b * a.xbs;
-    float amax = 0.f, nmax = 0.f, emax = 0.f;
-    if (UB) staged_head_maxima(s_hs, 16 * HT, amax, nmax, emax);
-    TileOut to{-INFINITY, INFINITY, 0.f, 0.f};
-    const int64_t rlast = rend - 1;
-
-    // PF tiles in flight ahead of the one on the matrix cores (one when the
-    // bound is also evaluated, for registers); rows past the end are clamped
-    // to the last row (loaded, never stored)
-    constexpr int PF = UB ? 1 : 2;
-    bf16x8_t xf[KS], x1[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-        const int64_t row0 = min(r0 + c, rlast), row1 = min(r0 + 16 + c, rlast);
-        xf[ks] = *reinterpret_cast<const bf16x8_t*>(xb + row0 * a.xs + 32 * ks + 8 * g);
-        if (PF == 2) x1[ks] = *reinterpret_cast<const bf16x8_t*>(xb + row1 * a.xs + 32 * ks + 8 * g);
-    }
-    for (int64_t t0 = r0; t0 < rend; t0 += 16) {
-        const int64_t row = t0 + c;
-        const bool valid = row < rend;
-        bf16x8_t x2[KS];
-        const int64_t nrow = min(row + 16 * PF, rlast);
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            x2[ks] = *reinterpret_cast<const bf16x8_t*>(xb + nrow * a.xs + 32 * ks + 8 * g);
-        float et = 0.f, ep = 0.f, ga = 0.f;
-        if (UB) {
-            const int64_t o = (int64_t)b * a.T + min(row, rlast);
-            et = a.eta[o];
-            ep = a.eps[o];
-            ga = a.gam[o];
-        }
-        f32x4_t acc[HT];
-#pragma unroll
-        for (int ht = 0; ht < HT; ++ht) acc[ht] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-            for (int ht = 0; ht < HT; ++ht)
-                acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[ht][ks], xf[ks], acc[ht], 0, 0, 0);
-        // keep the per-head bound scalars in LDS (re-read per tile) instead of
-        // letting them be hoisted into 4 * 16 * HT registers
-        if (UB) asm volatile("" ::: "memory");
-        // acc[ht][i] = score of head slot 16*ht + 4*g + i for row t0 + c
-        float m = -INFINITY;
-        float ubv = -INFINITY;
-#pragma unroll
-        for (int ht = 0; ht < HT; ++ht)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                m = fmaxf(m, acc[ht][i]);
-                if (UB) {
-                    const float4 hs = s_hs[16 * ht + 4 * g + i];
-                    ubv = fmaxf(ubv, acc[ht][i] + fmaf(hs.x, et, fmaf(hs.y, ep, hs.z * ga)));
-                }
-            }
-        m = wave_max16(m);
-        tile_epilogue(a, b, g, row, valid, m, row_sq<KS>(xf), to);
-        if (UB) {
-            ubv = wave_max16(ubv);
-            if (valid) to.bmm = fmaxf(to.bmm, fmaf(amax, et, fmaf(nmax, ep, emax * ga)));
-            if (g == 0 && valid) a.ub[(int64_t)b * a.A + row] = ubv;
-        }
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            if (PF == 2) {
-                xf[ks] = x1[ks];
-                x1[ks] = x2[ks];
-            } else {
-                xf[ks] = x2[ks];
-            }
-        }
-    }
-    score_finish(a, b, lane, to, UB);
-}
-
 // Any head count / width within the limits: heads and dims in runtime loops,
 // query fragments re-read from the (cache-resident) qt buffer per tile.
 template <bool UB>
@@ -464,7 +359,7 @@ __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
 
 // ------------------------------------------------------ streaming scorer
 //
-// The form used when the bound is not evaluated.  A block owns a contiguous
+// A block owns a contiguous
 // span of one sequence's archive; its four waves take alternate 16-row tiles
 // of it (so the block streams one region of HBM), each through a private LDS
 // ring of NST stages filled by direct global->LDS loads
@@ -486,6 +381,16 @@ __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
 // counts; the last tiles, whose look-ahead loads would run past the span,
 // take a loop with run-time counts.  Every wait counts the ring loads issued
 // after the awaited tile (loads complete in order among themselves).
+//
+// With the admission bound (UB): the tile's row scalars eta, eps, gam come
+// with the tile, one more direct load of 64 dwords per tile (lanes 16j + c:
+// scalar j of row c; the fourth group repeats eta), so lane 16j + c reads its
+// own dword of the stage, which is the B operand of a v_mfma_f32_16x16x4_f32
+// with A = the head scalars (lane 16j + c: a, n, e, 0 of head slot c): one
+// such step per head tile adds B_h(u) = a_h eta_u + n_h eps_u + e_h gam_u to
+// the finished scores, UB_u = max_h (s^_h(u) + B_h(u)).  Four fp32 products
+// and sums of non-negative terms (all scalars are >= 0) on top of the score:
+// the selection's band for UB covers that error.
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void gbl_void_t;
 
@@ -495,19 +400,19 @@ __device__ __forceinline__ void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
 }
 
-// wait until at most `rem` tiles (KS loads each) younger than the current one
+// wait until at most `rem` tiles (LPT loads each) younger than the current one
 // are still in flight (rem is wave-uniform, 0 <= rem < NST)
-template <int KS, int NST>
+template <int LPT, int NST>
 __device__ __forceinline__ void wait_tiles(int rem) {
     switch (rem) {
         case 0: wait_vmcnt<0>(); break;
-        case 1: if (NST > 1) wait_vmcnt<(NST > 1 ? 1 : 0) * KS>(); break;
-        case 2: if (NST > 2) wait_vmcnt<(NST > 2 ? 2 : 0) * KS>(); break;
-        case 3: if (NST > 3) wait_vmcnt<(NST > 3 ? 3 : 0) * KS>(); break;
-        case 4: if (NST > 4) wait_vmcnt<(NST > 4 ? 4 : 0) * KS>(); break;
-        case 5: if (NST > 5) wait_vmcnt<(NST > 5 ? 5 : 0) * KS>(); break;
-        case 6: if (NST > 6) wait_vmcnt<(NST > 6 ? 6 : 0) * KS>(); break;
-        default: if (NST > 7) wait_vmcnt<(NST > 7 ? 7 : 0) * KS>(); break;
+        case 1: if (NST > 1) wait_vmcnt<(NST > 1 ? 1 : 0) * LPT>(); break;
+        case 2: if (NST > 2) wait_vmcnt<(NST > 2 ? 2 : 0) * LPT>(); break;
+        case 3: if (NST > 3) wait_vmcnt<(NST > 3 ? 3 : 0) * LPT>(); break;
+        case 4: if (NST > 4) wait_vmcnt<(NST > 4 ? 4 : 0) * LPT>(); break;
+        case 5: if (NST > 5) wait_vmcnt<(NST > 5 ? 5 : 0) * LPT>(); break;
+        case 6: if (NST > 6) wait_vmcnt<(NST > 6 ? 6 : 0) * LPT>(); break;
+        default: if (NST > 7) wait_vmcnt<(NST > 7 ? 7 : 0) * LPT>(); break;
     }
 }
 
@@ -515,7 +420,7 @@ constexpr int STAGE_BUDGET = 12288;   // bytes of tile ring per wave
 constexpr int STREAM_WAVES = 4;       // waves per block
 constexpr int STREAM_TPW_MAX = 128;   // tiles per wave, bounded by the LDS key buffer
 
-template <int KS>
+template <int KS, bool UB>
 struct StreamGeom {
     static constexpr int N = 32 * KS;          // index dims per row
     static constexpr int N8 = N / 8;           // 16-byte slots per row
@@ -523,8 +428,12 @@ struct StreamGeom {
     // ring depth 4 or 2, so that a run of four tiles maps to fixed stages
     static constexpr int NST = STAGE_BUDGET / STAGE >= 4 ? 4 : 2;
     static constexpr int RUN = 4;                       // tiles per fixed-stage run
-    static constexpr int KEYS = 16 * STREAM_TPW_MAX * 4;   // the span's keys (fp32)
-    static constexpr int WAVE = NST * STAGE + KEYS;     // 16 KB per wave at 128 dims
+    static constexpr int LPT = KS + (UB ? 1 : 0);       // ring loads per tile
+    static constexpr int RV = UB ? 256 : 0;             // per stage: the tile's row scalars
+    // the span's keys (fp32); with UB the first half holds the keys and the
+    // second half the bounds of at most STREAM_TPW_MAX / 2 tiles
+    static constexpr int KEYS = 16 * STREAM_TPW_MAX * 4;
+    static constexpr int WAVE = NST * (STAGE + RV) + KEYS;   // 16 KB per wave at 128 dims
 };
 
 __device__ __forceinline__ f32x2_t swap32(float x, float y) {
@@ -548,37 +457,64 @@ __device__ __forceinline__ float group_sum(float v0, float v1, float v2, float v
     return u[0] + u[1];
 }
 
-template <int HT, int KS>
+// v_j = x for j == i, the others unchanged (i wave-uniform, v in registers)
+__device__ __forceinline__ void put4(float& v0, float& v1, float& v2, float& v3, int i, float x) {
+    v0 = (i == 0) ? x : v0;
+    v1 = (i == 1) ? x : v1;
+    v2 = (i == 2) ? x : v2;
+    v3 = (i == 3) ? x : v3;
+}
+
+template <int HT, int KS, bool UB>
 __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int tpw) {
-    using Gm = StreamGeom<KS>;
-    constexpr int N8 = Gm::N8, STAGE = Gm::STAGE, NST = Gm::NST, RUN = Gm::RUN;
+    using Gm = StreamGeom<KS, UB>;
+    constexpr int N8 = Gm::N8, STAGE = Gm::STAGE, NST = Gm::NST, RUN = Gm::RUN, LPT = Gm::LPT;
     constexpr int TST = STREAM_WAVES;   // block tiles between consecutive tiles of a wave
     extern __shared__ __align__(16) uint8_t smem[];
     const int b = blockIdx.y;
     const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     uint8_t* wbase = smem + wave * Gm::WAVE;
-    float* s_key = reinterpret_cast<float*>(wbase + NST * STAGE);   // [64 q + lane]
+    uint8_t* rvbase = wbase + NST * STAGE;                                   // [NST][64] row scalars
+    float* s_key = reinterpret_cast<float*>(wbase + NST * (STAGE + Gm::RV));   // [64 q + lane]
+    float* s_ub = s_key + 16 * STREAM_TPW_MAX / 2;                            // (UB) [64 q + lane]
     // block span [bs0, bs1); this wave's tile j covers rows r0 + 16 TST j + [0, 16)
     if (blockIdx.x == 0 && threadIdx.x < 64) store_head_maxima(a, b, threadIdx.x);
     const int64_t bs0 = (int64_t)blockIdx.x * STREAM_WAVES * 16 * tpw;
     if (bs0 >= a.A) return;
     const int64_t bs1 = min(a.A, bs0 + (int64_t)STREAM_WAVES * 16 * tpw);
     const int64_t nbt = (bs1 - bs0 + 15) / 16;
+
+    // the sequence's query rows qt[b] (H x N bf16), staged once per block in
+    // LDS (rows padded by 16 bytes), then read into registers by every wave
+    bf16x8_t qf[HT][KS];
+    {
+        constexpr int QROW = 2 * Gm::N + 16;
+        static_assert(16 * HT * QROW <= STREAM_WAVES * Gm::WAVE, "query rows fit the block's LDS");
+        const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
+        for (int p = threadIdx.x; p < a.H * N8; p += 64 * STREAM_WAVES) {
+            const int h = p / N8, j = p % N8;
+            *reinterpret_cast<bf16x8_t*>(smem + h * QROW + 16 * j) =
+                *reinterpret_cast<const bf16x8_t*>(qtb + (int64_t)h * a.n + 8 * j);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int ht = 0; ht < HT; ++ht) {
+            const int h = (16 * ht + c) % a.H;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                qf[ht][ks] = *reinterpret_cast<const bf16x8_t*>(smem + h * QROW + 64 * ks + 16 * g);
+        }
+        __syncthreads();   // read out before the rings overwrite it
+    }
     if (wave >= nbt) return;
     const int ntl = (int)((nbt - 1 - wave) / TST + 1);
     const int64_t r0 = bs0 + 16 * wave;
 
-    bf16x8_t qf[HT][KS];
-    const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
-#pragma unroll
-    for (int ht = 0; ht < HT; ++ht) {
-        const int h = (16 * ht + c) % a.H;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            qf[ht][ks] = *reinterpret_cast<const bf16x8_t*>(qtb + (int64_t)h * a.n + 32 * ks + 8 * g);
-    }
-    wait_vmcnt<0>();   // query fragments resident before the ring's count starts
+    // (UB) A operand of the bound step: scalar g of head slot 16 ht + c (zero
+    // for g = 3), and in lane 16 g + c the maximum over heads of scalar g
+    float hsf[UB ? HT : 1];
+    float coef = 0.f;
 
     const uint32_t rowb = (uint32_t)(a.xs * 2);   // row stride in bytes
     const uint8_t* span = reinterpret_cast<const uint8_t*>(a.x + (int64_t)b * a.xbs + r0 * a.xs);
@@ -591,6 +527,19 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
         vrow[j] = R;
         voff[j] = (uint32_t)R * rowb + 16u * (uint32_t)((S + R) % N8);
     }
+    // (UB) source of this lane's row scalar: scalar g of row c of tile 0
+    const float* rvsrc = nullptr;
+    if (UB) {
+        const float* base = (g == 1) ? a.eps : (g == 2) ? a.gam : a.eta;
+        rvsrc = base + (int64_t)b * a.T + r0 + c;
+    }
+    auto issue_rv = [&](int t, int stage, int nv) {
+        if (UB) {
+            const int cc = c < nv ? 0 : c - (nv - 1);
+            __builtin_amdgcn_global_load_lds((gbl_void_t*)(rvsrc + (int64_t)t * (TST * 16) - cc),
+                                             (lds_void_t*)(rvbase + 256 * stage), 4, 0, 2 /* nt */);
+        }
+    };
     // loads of tile t into `stage`; rows past the span re-read its last row
     auto issue = [&](int t, int stage) {
         const uint8_t* tb = span + (int64_t)t * (TST * 16) * rowb;
@@ -602,6 +551,7 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
             __builtin_amdgcn_global_load_lds((gbl_void_t*)(tb + o), (lds_void_t*)(wbase + stage * STAGE + 1024 * j),
                                              16, 0, 2 /* nt */);
         }
+        issue_rv(t, stage, nv);
     };
     // loads of a tile that lies wholly inside the span
     auto issue_full = [&](int t, int stage) {
@@ -610,15 +560,17 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
         for (int j = 0; j < KS; ++j)
             __builtin_amdgcn_global_load_lds((gbl_void_t*)(tb + voff[j]),
                                              (lds_void_t*)(wbase + stage * STAGE + 1024 * j), 16, 0, 2 /* nt */);
+        issue_rv(t, stage, 16);
     };
-    // operand fragments of the tile in `stage`
-    auto read_stage = [&](int stage, bf16x8_t (&x)[KS]) {
+    // operand fragments (and the row scalar) of the tile in `stage`
+    auto read_stage = [&](int stage, bf16x8_t (&x)[KS], float& rv) {
         const uint8_t* st = wbase + stage * STAGE;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             const int S = (4 * ks + g - c + 16 * N8) % N8;
             x[ks] = *reinterpret_cast<const bf16x8_t*>(st + c * (2 * Gm::N) + 16 * S);
         }
+        if (UB) rv = reinterpret_cast<const float*>(rvbase + 256 * stage)[lane];
     };
     // scores of this lane's head slots for the tile whose fragments are in x
     auto contract = [&](const bf16x8_t (&x)[KS], f32x4_t (&acc)[HT]) {
@@ -638,23 +590,41 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
             for (int i = 0; i < 4; ++i) pm = fmaxf(pm, acc[ht][i]);
         return pm;
     };
+    // (UB) the scores plus the per-head bound term of the tile's rows
+    auto add_bound = [&](f32x4_t (&acc)[HT], float rv) {
+#pragma unroll
+        for (int ht = 0; ht < HT; ++ht) acc[ht] = __builtin_amdgcn_mfma_f32_16x16x4f32(hsf[ht], rv, acc[ht], 0, 0, 0);
+    };
     for (int t = 0; t < NST && t < ntl; ++t) issue(t, t);
+    if (UB) {
+#pragma unroll
+        for (int ht = 0; ht < HT; ++ht) {
+            const int h = (16 * ht + c) % a.H;
+            hsf[ht] = g < 3 ? a.hsc[((int64_t)b * a.H + h) * 4 + g] : 0.f;
+            coef = fmaxf(coef, hsf[ht]);
+        }
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) coef = fmaxf(coef, __shfl_xor(coef, o));
+    }
+    wait_vmcnt<0>();   // the first tiles (and the head scalars) resident
 
     TileOut to{-INFINITY, INFINITY, 0.f, 0.f};
     // row of group q (tiles 4q..4q+3) held by this lane: row c of tile 4q + g
     auto group_row = [&](int q) { return r0 + (int64_t)(TST * 16) * (4 * q + g) + c; };
-    auto group_out = [&](int q, float m, float s2) {
+    auto group_out = [&](int q, float m, float s2, float u, float bm) {
         if (group_row(q) < bs1) {
             to.nu2m = fmaxf(to.nu2m, s2);
             to.kmax = fmaxf(to.kmax, m);
             to.kmin = fminf(to.kmin, m);
+            if (UB) to.bmm = fmaxf(to.bmm, bm);
         }
         s_key[64 * q + lane] = m;
+        if (UB) s_ub[64 * q + lane] = u;
     };
 
     bf16x8_t xf[KS];
-    wait_tiles<KS, NST>(min(NST - 1, ntl - 1));
-    read_stage(0, xf);
+    float rvc = 0.f;
+    read_stage(0, xf, rvc);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // stage read out before it is refilled
     if (NST < ntl) issue(NST, 0);
 
@@ -664,103 +634,130 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
     // those shapes take the run-time loop throughout)
     const int nrun = (KS <= 6 && ntl > NST) ? (ntl - NST - 1) / RUN : 0;
     for (int s = 0; s < nrun; ++s) {
-        float pmv[RUN], psv[RUN];
+        float pmv[RUN], psv[RUN], puv[RUN], pbv[RUN];
 #pragma unroll
         for (int j = 0; j < RUN; ++j) {
             f32x4_t acc[HT];
             contract(xf, acc);
             psv[j] = row_sq<KS>(xf);
+            if (UB) pbv[j] = coef * rvc;
             __builtin_amdgcn_sched_barrier(0);
-            wait_vmcnt<(NST - 1) * KS>();
+            wait_vmcnt<(NST - 1) * LPT>();
             bf16x8_t xn[KS];
-            read_stage((j + 1) % NST, xn);
+            float rvn = 0.f;
+            read_stage((j + 1) % NST, xn, rvn);
             pmv[j] = head_max(acc);
+            if (UB) {
+                add_bound(acc, rvc);
+                puv[j] = head_max(acc);
+            }
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // stage read out before it is refilled
             issue_full(RUN * s + j + 1 + NST, (j + 1) % NST);
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) xf[ks] = xn[ks];
+            rvc = rvn;
             __builtin_amdgcn_sched_barrier(0);
         }
 #pragma unroll
         for (int j4 = 0; j4 < RUN; j4 += 4)
             group_out((RUN * s + j4) / 4, group_max(pmv[j4], pmv[j4 + 1], pmv[j4 + 2], pmv[j4 + 3]),
-                      group_sum(psv[j4], psv[j4 + 1], psv[j4 + 2], psv[j4 + 3]));
+                      group_sum(psv[j4], psv[j4 + 1], psv[j4 + 2], psv[j4 + 3]),
+                      UB ? group_max(puv[j4], puv[j4 + 1], puv[j4 + 2], puv[j4 + 3]) : 0.f,
+                      UB ? group_sum(pbv[j4], pbv[j4 + 1], pbv[j4 + 2], pbv[j4 + 3]) : 0.f);
     }
 
     // the remaining tiles, with run-time stages and wait counts
     float pm0 = -INFINITY, pm1 = -INFINITY, pm2 = -INFINITY, pm3 = -INFINITY;
     float ps0 = 0.f, ps1 = 0.f, ps2 = 0.f, ps3 = 0.f;
+    float pu0 = -INFINITY, pu1 = -INFINITY, pu2 = -INFINITY, pu3 = -INFINITY;
+    float pb0 = 0.f, pb1 = 0.f, pb2 = 0.f, pb3 = 0.f;
     for (int t = RUN * nrun; t < ntl; ++t) {
         f32x4_t acc[HT];
         contract(xf, acc);
         const float ps = row_sq<KS>(xf);
+        const float pb = UB ? coef * rvc : 0.f;
         bf16x8_t xn[KS];
+        float rvn = 0.f;
         const bool more = t + 1 < ntl;
         if (more) {
-            wait_tiles<KS, NST>(min(NST - 1, ntl - 2 - t));
-            read_stage((t + 1) % NST, xn);
+            wait_tiles<LPT, NST>(min(NST - 1, ntl - 2 - t));
+            read_stage((t + 1) % NST, xn, rvn);
         }
         const float pm = head_max(acc);
+        float pu = -INFINITY;
+        if (UB) {
+            add_bound(acc, rvc);
+            pu = head_max(acc);
+        }
         const int j = t & 3;
         if (j == 0) {
             pm1 = pm2 = pm3 = -INFINITY;
             ps1 = ps2 = ps3 = 0.f;
+            pu1 = pu2 = pu3 = -INFINITY;
+            pb1 = pb2 = pb3 = 0.f;
         }
-        pm0 = (j == 0) ? pm : pm0;
-        pm1 = (j == 1) ? pm : pm1;
-        pm2 = (j == 2) ? pm : pm2;
-        pm3 = (j == 3) ? pm : pm3;
-        ps0 = (j == 0) ? ps : ps0;
-        ps1 = (j == 1) ? ps : ps1;
-        ps2 = (j == 2) ? ps : ps2;
-        ps3 = (j == 3) ? ps : ps3;
+        put4(pm0, pm1, pm2, pm3, j, pm);
+        put4(ps0, ps1, ps2, ps3, j, ps);
+        if (UB) {
+            put4(pu0, pu1, pu2, pu3, j, pu);
+            put4(pb0, pb1, pb2, pb3, j, pb);
+        }
         if (more) {
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // stage read out before it is refilled
             if (t + 1 + NST < ntl) issue(t + 1 + NST, (t + 1) % NST);
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) xf[ks] = xn[ks];
+            rvc = rvn;
         }
         if (j != 3 && more) continue;
-        group_out(t >> 2, group_max(pm0, pm1, pm2, pm3), group_sum(ps0, ps1, ps2, ps3));
+        group_out(t >> 2, group_max(pm0, pm1, pm2, pm3), group_sum(ps0, ps1, ps2, ps3),
+                  UB ? group_max(pu0, pu1, pu2, pu3) : 0.f, UB ? group_sum(pb0, pb1, pb2, pb3) : 0.f);
     }
-    // the span's keys, each lane its own LDS words
+    // the span's keys (and bounds), each lane its own LDS words
     float* kto = a.kt + (int64_t)b * a.A;
     float* kuo = a.key ? a.key + (int64_t)b * a.A : nullptr;
+    float* ubo = UB ? a.ub + (int64_t)b * a.A : nullptr;
     for (int q = 0; q < (ntl + 3) / 4; ++q) {
         const int64_t row = group_row(q);
         if (row < bs1) {
             const float m = s_key[64 * q + lane];
             kto[row] = m;
             if (kuo) kuo[row] = m;
+            if (UB) ubo[row] = s_ub[64 * q + lane];
         }
     }
-    score_finish(a, b, lane, to, false);
+    score_finish(a, b, lane, to, UB);
 }
 
-// tiles per wave: enough waves for two blocks per CU, spans of 8..STREAM_TPW_MAX tiles
-// (the key buffer in LDS holds STREAM_TPW_MAX tiles of keys per wave)
+// tiles per wave: enough waves for two blocks per CU, spans of 8..tmax tiles
+// (the key buffer in LDS holds STREAM_TPW_MAX tiles of keys per wave, or half
+// as many tiles of keys and bounds)
 static int stream_tpw(const ScoreArgs& a) {
     const int64_t tiles = (int64_t)a.B * ((a.A + 15) / 16);
     const int64_t waves = 2LL * 256 * STREAM_WAVES;
+    const int64_t tmax = a.ub ? STREAM_TPW_MAX / 2 : STREAM_TPW_MAX;
     int64_t tpw = (tiles + waves - 1) / waves;
-    tpw = tpw < 8 ? 8 : (tpw > STREAM_TPW_MAX ? STREAM_TPW_MAX : tpw);
+    tpw = tpw < 8 ? 8 : (tpw > tmax ? tmax : tpw);
     return (int)tpw;
+}
+
+template <int HT, int KS, bool UB>
+static void launch_stream(const ScoreArgs& a, hipStream_t s) {
+    const int tpw = stream_tpw(a);
+    const int64_t rows_per_block = (int64_t)STREAM_WAVES * 16 * tpw;   // block span
+    dim3 grid((unsigned)((a.A + rows_per_block - 1) / rows_per_block), a.B);
+    const size_t sm = STREAM_WAVES * (size_t)StreamGeom<KS, UB>::WAVE;
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&score_stream_kernel<HT, KS, UB>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
+    hipLaunchKernelGGL((score_stream_kernel<HT, KS, UB>), grid, dim3(256), sm, s, a, tpw);
 }
 
 template <int HT, int KS>
 static void launch_fast(const ScoreArgs& a, hipStream_t s) {
-    if (a.ub) {
-        dim3 grid((unsigned)((a.A + SCORE_ROWS_PER_BLOCK - 1) / SCORE_ROWS_PER_BLOCK), a.B);
-        hipLaunchKernelGGL((score_kernel<HT, KS, true>), grid, dim3(256), 0, s, a);
-    } else {
-        const int tpw = stream_tpw(a);
-        const int64_t rows_per_block = (int64_t)STREAM_WAVES * 16 * tpw;   // block span
-        dim3 grid((unsigned)((a.A + rows_per_block - 1) / rows_per_block), a.B);
-        const size_t sm = STREAM_WAVES * (size_t)StreamGeom<KS>::WAVE;
-        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&score_stream_kernel<HT, KS>),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
-        hipLaunchKernelGGL((score_stream_kernel<HT, KS>), grid, dim3(256), sm, s, a, tpw);
-    }
+    if (a.ub)
+        launch_stream<HT, KS, true>(a, s);
+    else
+        launch_stream<HT, KS, false>(a, s);
 }
 
 template <int HT>

@@ -461,6 +461,43 @@ def test_every_key_within_certified_bound(ctx, mode, r, H, B, T):
     check_step(wl, g, o, seqs)
 
 
+@pytest.mark.parametrize("mode,r,H,B,T", [
+    (synth.MODE_ROPE_DIGEST, 64, 128, 2, 9000),     # 128 dims, 128 heads: the two-tier shape
+    (synth.MODE_ROPE_DIGEST, 128, 64, 2, 5003),     # 192 dims, ragged archive
+    (synth.MODE_ROPE_DIGEST, 32, 32, 1, 4000),      # 96 dims, 32 heads
+    (synth.MODE_ROPE_DIGEST, 64, 16, 2, 262144),    # long spans: four-tile runs per wave
+])
+def test_every_bound_within_certified_band(ctx, mode, r, H, B, T):
+    """UB~ of every archived row against the oracle's exact bound
+    UB_u = max_h (s^_h(u) + B_h(u)) (Lemma (Index certificate)), within the
+    documented band E + 2^-21 (max |s^| + max_u (amax eta + nmax eps + emax gam))."""
+    say(f"bounds within band mode={mode} r={r} H={H} B={B} T={T}")
+    cfg = synth.CONFIGS["cfg3"].with_(mode=mode, r=r, H=H)
+    wl = synth.make_workload(cfg, "cuda", B=B, T=T)
+    k = max(1, wl["A"] // 32)
+    g, _ = gpu_step(ctx, wl, k=k, two_tier=True)
+    seqs = list(range(B))
+    o, (cache, q_lat, q_rope, P, index, eta, eps, gam) = oracle_step(wl, seqs, k=k, two_tier=True)
+    cols, has_rope = index_cols(mode, r)
+    qt, a, nq, e = oracle.query_prep(q_lat, q_rope, P, r, mode)
+    A = wl["A"]
+    for j, b in enumerate(seqs):
+        x = oracle.index_rows(cache[j], index[j] if index is not None else None, mode, r, has_rope)
+        n = x.shape[1]
+        ub = oracle.upper_bounds(qt[j], a[j], nq[j], e[j], x, eta[j], eps[j], gam[j], A)
+        qn = np.linalg.norm(oracle.decode_bf16(qt[j]), axis=1).max()
+        xn = np.linalg.norm(oracle.decode_bf16(x[:A]), axis=1).max()
+        E = 2 * (n + n / 32) * 2.0 ** -23 * qn * xn
+        f64 = lambda v: np.asarray(v, np.float64)
+        bmax = (f64(a[j]).max() * f64(eta[j][:A]) + f64(nq[j]).max() * f64(eps[j][:A])
+                + f64(e[j]).max() * f64(gam[j][:A])).max()
+        band = E + 2.0 ** -21 * (qn * xn + bmax)
+        err = np.abs(g["ub"][b, :A].astype(np.float64) - ub)
+        say(f"  seq {b}: max |UB~ - UB| {err.max():.3e}, band {band:.3e}")
+        assert np.all(err <= band), (b, int(np.argmax(err)), err.max(), band)
+    check_step(wl, g, o, seqs, two_tier=True)
+
+
 def test_determinism(ctx):
     say("determinism")
     cfg = synth.CONFIGS["cfg3"].with_(H=16)
