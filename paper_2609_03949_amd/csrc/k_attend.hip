@@ -367,6 +367,11 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
 // Block = (b, head group, wave, lane group g) of the attention kernel: heads
 // hb + i (i = 0..3) with hb = 128 hg + 16 wave + 4 g; thread j covers dims
 // 4j .. 4j+3 (tt = j / 4, lanes 16 g + 4 (j mod 4) .. +3 of the partials).
+// Splits are taken COMB_SPLITS at a time with all their loads in flight
+// together (one memory round trip per batch); the running maximum and the
+// accumulators are rescaled when a batch raises the maximum.
+constexpr int COMB_SPLITS = 8;
+
 __global__ __launch_bounds__(128) void attend_combine_kernel(AttendArgs a) {
     const int HG = (a.H + ATT_HEADS - 1) / ATT_HEADS;
     const int q = blockIdx.x % 32, hg = (blockIdx.x / 32) % HG, b = blockIdx.x / (32 * HG);
@@ -378,37 +383,56 @@ __global__ __launch_bounds__(128) void attend_combine_kernel(AttendArgs a) {
     float acc[4][4] = {};
 #pragma unroll
     for (int i = 0; i < 4; ++i) M[i] = -INFINITY;
-    // (both passes unrolled so that the loads of several splits are in flight together)
-#pragma unroll 8
-    for (int s = 0; s < a.splits; ++s) {
-        const float* ml = a.part_ml + (((int64_t)b * a.splits + s) * a.H) * 2;
+    for (int s0 = 0; s0 < a.splits; s0 += COMB_SPLITS) {
+        float ms[COMB_SPLITS][4], ls[COMB_SPLITS][4];
+        u32x4_t raw[COMB_SPLITS][2];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            if (hb + i < a.H) M[i] = fmaxf(M[i], ml[2 * (hb + i)]);
-    }
-#pragma unroll 4
-    for (int s = 0; s < a.splits; ++s) {
-        const float* ml = a.part_ml + (((int64_t)b * a.splits + s) * a.H) * 2;
-        float w[4];
+        for (int u = 0; u < COMB_SPLITS; ++u) {
+            const int s = s0 + u;
+            const bool live = s < a.splits;
+            const float* ml = a.part_ml + (((int64_t)b * a.splits + (live ? s : s0)) * a.H) * 2;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const bool hv = live && hb + i < a.H;
+                ms[u][i] = hv ? ml[2 * (hb + i)] : -INFINITY;
+                ls[u][i] = hv ? ml[2 * (hb + i) + 1] : 0.f;
+            }
+            const uint16_t* src = a.part_o + (((int64_t)b * a.splits + (live ? s : s0)) * HG + hg) * (ATT_HEADS * D_LAT) +
+                                  (int64_t)wave * (D_LAT / 16) * 64 * 4 + (tt * 64 + 16 * g + c0) * 4;
+            raw[u][0] = *reinterpret_cast<const u32x4_t*>(src);       // lanes c0, c0+1
+            raw[u][1] = *reinterpret_cast<const u32x4_t*>(src + 8);   // lanes c0+2, c0+3
+        }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const float ms = (hb + i < a.H) ? ml[2 * (hb + i)] : -INFINITY;
-            w[i] = (ms == -INFINITY) ? 0.f : exp2f(ms - M[i]);
-            if (ms != -INFINITY) L[i] += w[i] * ml[2 * (hb + i) + 1];
+            float mb = M[i];
+#pragma unroll
+            for (int u = 0; u < COMB_SPLITS; ++u) mb = fmaxf(mb, ms[u][i]);
+            if (mb != M[i]) {   // raised (so mb is finite): rescale what is accumulated
+                const float sc = (M[i] == -INFINITY) ? 0.f : exp2f(M[i] - mb);
+                L[i] *= sc;
+#pragma unroll
+                for (int cc = 0; cc < 4; ++cc) acc[cc][i] *= sc;
+                M[i] = mb;
+            }
         }
-        const uint16_t* src = a.part_o + (((int64_t)b * a.splits + s) * HG + hg) * (ATT_HEADS * D_LAT) +
-                              (int64_t)wave * (D_LAT / 16) * 64 * 4 + (tt * 64 + 16 * g + c0) * 4;
-        const u32x4_t raw0 = *reinterpret_cast<const u32x4_t*>(src);       // lanes c0, c0+1
-        const u32x4_t raw1 = *reinterpret_cast<const u32x4_t*>(src + 8);   // lanes c0+2, c0+3
 #pragma unroll
-        for (int cc = 0; cc < 4; ++cc) {
-            const u32x4_t& rw = cc < 2 ? raw0 : raw1;
-            const uint32_t w01 = rw[2 * (cc & 1)], w23 = rw[2 * (cc & 1) + 1];
-            const float v[4] = {__uint_as_float(w01 << 16), __uint_as_float(w01 & 0xFFFF0000u),
-                                __uint_as_float(w23 << 16), __uint_as_float(w23 & 0xFFFF0000u)};
-            // a split without rows never wrote its partial: weight 0 must not touch it
+        for (int u = 0; u < COMB_SPLITS; ++u) {
+            float w[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) acc[cc][i] += (w[i] > 0.f) ? w[i] * v[i] : 0.f;
+            for (int i = 0; i < 4; ++i) {
+                w[i] = (ms[u][i] == -INFINITY) ? 0.f : exp2f(ms[u][i] - M[i]);
+                L[i] += w[i] * ls[u][i];
+            }
+#pragma unroll
+            for (int cc = 0; cc < 4; ++cc) {
+                const u32x4_t& rw = raw[u][cc >> 1];
+                const uint32_t w01 = rw[2 * (cc & 1)], w23 = rw[2 * (cc & 1) + 1];
+                const float v[4] = {__uint_as_float(w01 << 16), __uint_as_float(w01 & 0xFFFF0000u),
+                                    __uint_as_float(w23 << 16), __uint_as_float(w23 & 0xFFFF0000u)};
+                // a split without rows never wrote its partial: weight 0 must not touch it
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[cc][i] += (w[i] > 0.f) ? w[i] * v[i] : 0.f;
+            }
         }
     }
 #pragma unroll
