@@ -30,7 +30,8 @@ constexpr int SAMPLE_MAX = 2048;             // keys sampled per sequence to pla
 constexpr int SAMPLE_BINS = 2048;            // bins of the sample's histogram
 constexpr int COUNT_KEYS_PER_BLOCK = 4096;   // keys per block of the counting pass
 constexpr int KEY_BATCH = 16;                // keys per thread in flight
-constexpr int EX_BLOCKS = 16;                // per sequence: blocks of the exact-key pass
+constexpr int EX_BLOCKS = 4;                 // per sequence: blocks of the exact-key pass (one per CU: 140 KB of LDS)
+constexpr int DECIDE_BLOCKS = 16;            // per sequence: blocks of the admission decision pass
 constexpr int RANK_BLOCKS = 16;
 
 // order-preserving encoding of fp64 (for 64-bit atomic max); -0 maps as +0
@@ -549,6 +550,7 @@ __global__ __launch_bounds__(SEL_THREADS) void exact_keys_kernel(SelectArgs a) {
     __shared__ float4 s_hs[128];
     __shared__ unsigned long long s_best[4][16];
     __shared__ uint32_t s_list[4][64];
+    __shared__ __align__(16) uint16_t s_x[4][16 * D_ROW];   // each wave's 16 gathered rows, for the fp64 chains
     const int b = blockIdx.y;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4, c = lane & 15;
     const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
@@ -589,6 +591,7 @@ __global__ __launch_bounds__(SEL_THREADS) void exact_keys_kernel(SelectArgs a) {
         for (int ht = 0; ht < 8; ++ht) acc[ht] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         for (int ks = 0; ks < KS; ++ks) {
             const bf16x8_t xf = *reinterpret_cast<const bf16x8_t*>(x + 32 * ks + 8 * g);
+            *reinterpret_cast<bf16x8_t*>(&s_x[wave][c * a.n + 32 * ks + 8 * g]) = xf;
 #pragma unroll
             for (int ht = 0; ht < 8; ++ht) {
                 if (ht < HT) {
@@ -627,6 +630,10 @@ __global__ __launch_bounds__(SEL_THREADS) void exact_keys_kernel(SelectArgs a) {
         m = fmaxf(m, __shfl_xor(m, 32));
         const float thr = next_down_f32(m - margin);
         if (lane < 16) s_best[wave][lane] = (unsigned long long)f64_to_ord(-INFINITY);
+        // the rows are in LDS for every lane of the wave (LDS operations of a
+        // wave complete in order)
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_wave_barrier();
         // candidates in rounds of up to 64 pairs, one fp64 chain per lane
         int nl = 0;
         auto flush = [&]() {
@@ -637,7 +644,7 @@ __global__ __launch_bounds__(SEL_THREADS) void exact_keys_kernel(SelectArgs a) {
                 const int64_t ur = amb[ir];
                 const int64_t o = (int64_t)b * a.T + ur;
                 const float4 hs = UB ? s_hs[h] : make_float4(0.f, 0.f, 0.f, 0.f);
-                const double v = exact_chain<UB>(qtb + (int64_t)h * a.n, xb + ur * a.xs, a.n, hs,
+                const double v = exact_chain<UB>(qsrc + (int64_t)h * a.n, &s_x[wave][cr * a.n], a.n, hs,
                                                  UB ? (double)a.eta[o] : 0.0, UB ? (double)a.eps[o] : 0.0,
                                                  UB ? (double)a.gam[o] : 0.0);
                 atomicMax(&s_best[wave][cr], (unsigned long long)f64_to_ord(v));
@@ -849,7 +856,7 @@ hipError_t launch_admit(const SelectArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(admit_classify_kernel, dim3((unsigned)a.nch, a.B), dim3(SEL_THREADS), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = run_exact_keys<true>(a, s)) != hipSuccess) return e;
-    hipLaunchKernelGGL(admit_decide_kernel, dim3(EX_BLOCKS, a.B), dim3(SEL_THREADS), 0, s, a);
+    hipLaunchKernelGGL(admit_decide_kernel, dim3(DECIDE_BLOCKS, a.B), dim3(SEL_THREADS), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return run_compact(a, a.flags2, 3, CC_ADM, CC_ADMAMB, a.adm, a.cap, a.cap, a.adm_count, s);
 }
