@@ -466,6 +466,8 @@ def test_every_key_within_certified_bound(ctx, mode, r, H, B, T):
     (synth.MODE_ROPE_DIGEST, 128, 64, 2, 5003),     # 192 dims, ragged archive
     (synth.MODE_ROPE_DIGEST, 32, 32, 1, 4000),      # 96 dims, 32 heads
     (synth.MODE_ROPE_DIGEST, 64, 16, 2, 262144),    # long spans: four-tile runs per wave
+    (synth.MODE_ROPE_DIGEST, 96, 24, 1, 3001),      # 160 dims; 24 heads in two head tiles (slots repeat heads)
+    (synth.MODE_ROPE_DIGEST, 192, 40, 1, 2500),     # 256 dims (run-time loop only), 40 heads
 ])
 def test_every_bound_within_certified_band(ctx, mode, r, H, B, T):
     """UB~ of every archived row against the oracle's exact bound
