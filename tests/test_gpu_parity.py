@@ -385,6 +385,22 @@ def test_bracket_missed_by_the_sample(ctx):
     assert set(g["sel"][0].tolist()) <= set(rows.tolist())
 
 
+def test_bracket_missed_by_the_sample_long_archive(ctx):
+    """The same miss on an archive of 65536 rows: the sample takes runs of 32
+    rows about 1040 apart, so rows 40..940 are never sampled; the largest keys
+    are planted there, and the bracket pass must fall back to the whole key
+    range of 32 counting blocks' worth of keys."""
+    say("sample miss, long archive")
+    cfg = synth.CONFIGS["cfg1"].with_(H=16, needles=0)
+    wl = synth.make_workload(cfg, "cuda", B=1, T=65536 + 256)
+    rows = torch.arange(40, 940, 3, device="cuda")
+    wl["cache"][0, rows, 512:] = (wl["cache"][0, rows, 512:].float() * 8).to(torch.bfloat16)
+    g, _ = gpu_step(ctx, wl, k=256)
+    o, _ = oracle_step(wl, [0], k=256)
+    check_step(wl, g, o, [0])
+    assert set(g["sel"][0].tolist()) <= set(rows.tolist())
+
+
 @pytest.mark.parametrize("H", [16, 128])
 def test_identical_heads_make_every_head_a_candidate(ctx, H):
     """All heads carry the same query: every head ties for the maximum of every
