@@ -305,7 +305,6 @@ __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
     if (r0 >= a.A) return;
     const int64_t rend = min(a.A, r0 + (int64_t)(16 * SCORE_TPW));
     const int64_t rlast = rend - 1;
-    const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
     const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
     const uint16_t* xb = a.x + (int64_t)b * a.xbs;
     float amax = 0.f, nmax = 0.f, emax = 0.f;
