@@ -418,6 +418,7 @@ __device__ __forceinline__ void wait_tiles(int rem) {
 constexpr int STAGE_BUDGET = 12288;   // bytes of tile ring per wave
 constexpr int STREAM_WAVES = 4;       // waves per block
 constexpr int STREAM_TPW_MAX = 128;   // tiles per wave, bounded by the LDS key buffer
+constexpr int WAVE_LDS = 20480;       // LDS per wave for two blocks of four waves per CU (160 KB)
 
 template <int KS, bool UB>
 struct StreamGeom {
@@ -429,10 +430,17 @@ struct StreamGeom {
     static constexpr int RUN = 4;                       // tiles per fixed-stage run
     static constexpr int LPT = KS + (UB ? 1 : 0);       // ring loads per tile
     static constexpr int RV = UB ? 256 : 0;             // per stage: the tile's row scalars
-    // the span's keys (fp32); with UB the first half holds the keys and the
-    // second half the bounds of at most STREAM_TPW_MAX / 2 tiles
-    static constexpr int KEYS = 16 * STREAM_TPW_MAX * 4;
-    static constexpr int WAVE = NST * (STAGE + RV) + KEYS;   // 16 KB per wave at 128 dims
+    // the span's keys (fp32) for KT tiles: STREAM_TPW_MAX, or fewer where the
+    // ring is so wide that two blocks per CU would not fit otherwise (rows of
+    // 224 and 256 dims); with UB the first half holds the keys and the second
+    // half the bounds of at most KT / 2 tiles
+    static constexpr int RING = NST * (STAGE + RV);
+    static constexpr int KT = RING + 64 * STREAM_TPW_MAX <= WAVE_LDS       ? STREAM_TPW_MAX
+                              : RING + 64 * (STREAM_TPW_MAX / 2) <= WAVE_LDS ? STREAM_TPW_MAX / 2
+                                                                            : STREAM_TPW_MAX / 4;
+    static constexpr int KEYS = 16 * KT * 4;
+    static constexpr int WAVE = RING + KEYS;   // 16 KB per wave at 128 dims
+    static constexpr int TPW_MAX = UB ? KT / 2 : KT;   // tiles one wave may own
 };
 
 __device__ __forceinline__ f32x2_t swap32(float x, float y) {
@@ -476,7 +484,7 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
     uint8_t* wbase = smem + wave * Gm::WAVE;
     uint8_t* rvbase = wbase + NST * STAGE;                                   // [NST][64] row scalars
     float* s_key = reinterpret_cast<float*>(wbase + NST * (STAGE + Gm::RV));   // [64 q + lane]
-    float* s_ub = s_key + 16 * STREAM_TPW_MAX / 2;                            // (UB) [64 q + lane]
+    float* s_ub = s_key + 16 * Gm::KT / 2;                                    // (UB) [64 q + lane]
     // block span [bs0, bs1); this wave's tile j covers rows r0 + 16 TST j + [0, 16)
     if (blockIdx.x == 0 && threadIdx.x < 64) store_head_maxima(a, b, threadIdx.x);
     const int64_t bs0 = (int64_t)blockIdx.x * STREAM_WAVES * 16 * tpw;
@@ -729,12 +737,10 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
 }
 
 // tiles per wave: enough waves for two blocks per CU, spans of 8..tmax tiles
-// (the key buffer in LDS holds STREAM_TPW_MAX tiles of keys per wave, or half
-// as many tiles of keys and bounds)
-static int stream_tpw(const ScoreArgs& a) {
+// (tmax: the tiles whose keys, or keys and bounds, the wave's LDS buffer holds)
+static int stream_tpw(const ScoreArgs& a, int tmax) {
     const int64_t tiles = (int64_t)a.B * ((a.A + 15) / 16);
     const int64_t waves = 2LL * 256 * STREAM_WAVES;
-    const int64_t tmax = a.ub ? STREAM_TPW_MAX / 2 : STREAM_TPW_MAX;
     int64_t tpw = (tiles + waves - 1) / waves;
     tpw = tpw < 8 ? 8 : (tpw > tmax ? tmax : tpw);
     return (int)tpw;
@@ -742,7 +748,7 @@ static int stream_tpw(const ScoreArgs& a) {
 
 template <int HT, int KS, bool UB>
 static void launch_stream(const ScoreArgs& a, hipStream_t s) {
-    const int tpw = stream_tpw(a);
+    const int tpw = stream_tpw(a, StreamGeom<KS, UB>::TPW_MAX);
     const int64_t rows_per_block = (int64_t)STREAM_WAVES * 16 * tpw;   // block span
     dim3 grid((unsigned)((a.A + rows_per_block - 1) / rows_per_block), a.B);
     const size_t sm = STREAM_WAVES * (size_t)StreamGeom<KS, UB>::WAVE;
