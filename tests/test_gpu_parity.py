@@ -516,6 +516,39 @@ def test_every_bound_within_certified_band(ctx, mode, r, H, B, T):
     check_step(wl, g, o, seqs, two_tier=True)
 
 
+def test_longest_spans_at_256_dims_sampled(ctx):
+    """256 index dims (digest r=256): the scorer keeps 64 tiles of keys per
+    wave at this width, and B=8, A=262144 gives every wave exactly 64 tiles.
+    key~ of the rows of every wave's last tile in the first and last blocks,
+    of the archive's last rows and of a strided sample, against the oracle's
+    exact keys (index rows built by the oracle for those rows only), each
+    within its own bound 2 (n + n/32) 2^-23 max_h ||qt_h|| ||x_u||."""
+    say("longest spans at 256 dims, sampled keys")
+    cfg = synth.CONFIGS["cfg2_r256"].with_(H=16)
+    wl = synth.make_workload(cfg, "cuda", B=8, T=262144 + 256)
+    A = wl["A"]
+    assert A == 262144
+    g, _ = gpu_step(ctx, wl, k=A // 128)
+    span = 4 * 16 * 64   # rows of one block: four waves of 64 tiles
+    last = np.arange(span - 64, span)
+    rows = np.unique(np.concatenate([last, span + last, A - span + last, np.arange(A - 100, A),
+                                     np.arange(0, A, 997)]))
+    for b in (0, 7):
+        cache, q_lat, q_rope, P = host_inputs(wl, [b])
+        sub = np.ascontiguousarray(cache[:, rows])
+        index, *_ = oracle.digest_build(sub, P, cfg.r, with_rope=False, scalars=False)
+        qt, *_ = oracle.query_prep(q_lat, q_rope, P, cfg.r, cfg.mode)
+        x = oracle.index_rows(sub[0], index[0], cfg.mode, cfg.r, False)
+        key, _ = oracle.index_keys(qt[0], x, len(rows))
+        n = x.shape[1]
+        qn = np.linalg.norm(oracle.decode_bf16(qt[0]), axis=1).max()
+        xn = np.linalg.norm(oracle.decode_bf16(x), axis=1)
+        E = 2 * (n + n / 32) * 2.0 ** -23 * qn * xn
+        err = np.abs(g["key"][b, rows].astype(np.float64) - key)
+        say(f"  seq {b}: {len(rows)} rows, max |key~ - key| / bound {np.max(err / E):.3f}")
+        assert np.all(err <= E), (b, int(rows[np.argmax(err / E)]))
+
+
 def test_determinism(ctx):
     say("determinism")
     cfg = synth.CONFIGS["cfg3"].with_(H=16)
