@@ -493,7 +493,9 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
     const int64_t nbt = (bs1 - bs0 + 15) / 16;
 
     // the sequence's query rows qt[b] (H x N bf16), staged once per block in
-    // LDS (rows padded by 16 bytes), then read into registers by every wave
+    // LDS (rows padded by 16 bytes), then read into registers by every wave;
+    // head slots beyond H repeat a real head (h mod H), which leaves the
+    // maximum over heads unchanged and needs no masking in the tile loop
     bf16x8_t qf[HT][KS];
     {
         constexpr int QROW = 2 * Gm::N + 16;
