@@ -549,6 +549,46 @@ def test_longest_spans_at_256_dims_sampled(ctx):
         assert np.all(err <= E), (b, int(rows[np.argmax(err / E)]))
 
 
+def test_longest_spans_two_tier_sampled(ctx):
+    """The bound form of the scan at 128 dims keeps keys and bounds of 64
+    tiles per wave; B=8, A=262144 gives every wave exactly 64 tiles.  key~
+    and UB~ of every wave's last tile in the first and last blocks, of the
+    archive's last rows and of a strided sample against the oracle's exact
+    key and bound (index rows and row scalars built by the oracle for those
+    rows only), each within its own band."""
+    say("longest spans, two-tier, sampled keys and bounds")
+    cfg = synth.CONFIGS["cfg3"].with_(H=16)
+    wl = synth.make_workload(cfg, "cuda", B=8, T=262144 + 256)
+    A = wl["A"]
+    assert A == 262144
+    g, _ = gpu_step(ctx, wl, k=A // 32, two_tier=True)
+    span = 4 * 16 * 64   # rows of one block: four waves of 64 tiles
+    last = np.arange(span - 64, span)
+    rows = np.unique(np.concatenate([last, span + last, A - span + last, np.arange(A - 100, A),
+                                     np.arange(0, A, 997)]))
+    f64 = lambda v: np.asarray(v, np.float64)
+    for b in (0, 7):
+        cache, q_lat, q_rope, P = host_inputs(wl, [b])
+        sub = np.ascontiguousarray(cache[:, rows])
+        index, eta, eps, gam = oracle.digest_build(sub, P, cfg.r, with_rope=True, scalars=True)
+        qt, a, nq, e = oracle.query_prep(q_lat, q_rope, P, cfg.r, cfg.mode)
+        x = oracle.index_rows(sub[0], index[0], cfg.mode, cfg.r, True)
+        key, _ = oracle.index_keys(qt[0], x, len(rows))
+        ub = oracle.upper_bounds(qt[0], a[0], nq[0], e[0], x, eta[0], eps[0], gam[0], len(rows))
+        n = x.shape[1]
+        qn = np.linalg.norm(oracle.decode_bf16(qt[0]), axis=1).max()
+        xn = np.linalg.norm(oracle.decode_bf16(x), axis=1)
+        E = 2 * (n + n / 32) * 2.0 ** -23 * qn * xn
+        bu = f64(a[0]).max() * f64(eta[0]) + f64(nq[0]).max() * f64(eps[0]) + f64(e[0]).max() * f64(gam[0])
+        band = E + 2.0 ** -21 * (qn * xn + bu)
+        kerr = np.abs(g["key"][b, rows].astype(np.float64) - key)
+        uerr = np.abs(g["ub"][b, rows].astype(np.float64) - ub)
+        say(f"  seq {b}: {len(rows)} rows, key err / bound {np.max(kerr / E):.3f}, "
+            f"UB err / band {np.max(uerr / band):.3f}")
+        assert np.all(kerr <= E), (b, int(rows[np.argmax(kerr / E)]))
+        assert np.all(uerr <= band), (b, int(rows[np.argmax(uerr / band)]))
+
+
 def test_determinism(ctx):
     say("determinism")
     cfg = synth.CONFIGS["cfg3"].with_(H=16)
