@@ -589,26 +589,27 @@ def test_longest_spans_two_tier_sampled(ctx):
         assert np.all(uerr <= band), (b, int(rows[np.argmax(uerr / band)]))
 
 
-def _random_case(seed):
+def _random_case(seed, long=False):
     """A seeded random step shape: mode, rank, heads, window, context, budget,
-    row distribution, and two-tier on or off (orthonormal basis then)."""
+    row distribution, and two-tier on or off (orthonormal basis then).  The
+    long family takes contexts of 30k..140k rows with at most 32 heads."""
     import random
-    rnd = random.Random(1000 + seed)
+    rnd = random.Random((5000 if long else 1000) + seed)
     mode = rnd.choice([synth.MODE_ROPE, synth.MODE_DIGEST, synth.MODE_ROPE_DIGEST])
     r = 0 if mode == synth.MODE_ROPE else 32 * rnd.randint(1, 8)
     two_tier = mode == synth.MODE_ROPE_DIGEST and rnd.random() < 0.4
     basis = "none" if r == 0 else ("orthonormal" if two_tier else rnd.choice(["orthonormal", "gaussian"]))
     H = rnd.choice([1, 3, 8, 16, 24, 40, 64, 100, 128])
-    if two_tier:
-        H = min(H, 64)
+    if two_tier or long:
+        H = min(H, 32 if long else 64)
     W = rnd.choice([1, 16, 64, 256])
-    T = W + rnd.randint(1, 12000)
+    T = W + (rnd.randint(30000, 140000) if long else rnd.randint(1, 12000))
     A = T - W
     k = rnd.choice([0, 1, rnd.randint(1, A), A, max(1, A // 32)])
     cfg = synth.CONFIGS["cfg0"].with_(mode=mode, r=r, basis=basis, H=H, W=W, k=k, T=T,
                                       rows=rnd.choice(["gaussian", "mixture", "lognormal"]),
                                       needles=rnd.randint(0, 8), two_tier=two_tier, seed=77 + seed)
-    return cfg, rnd.randint(1, 3)
+    return cfg, (1 if long else rnd.randint(1, 3))
 
 
 @pytest.mark.parametrize("seed", list(range(40)))
@@ -616,8 +617,18 @@ def test_random_shapes_against_the_oracle(ctx, seed):
     """Seeded random shapes over modes, ranks, head counts, windows, ragged
     contexts, budgets (0, 1, A, random), row distributions and the two-tier
     admission: the whole step on every sequence against the oracle."""
-    cfg, B = _random_case(seed)
-    say(f"random case {seed}: B={B} {synth.describe(cfg)}")
+    _check_random_case(ctx, *_random_case(seed), f"random case {seed}")
+
+
+@pytest.mark.parametrize("seed", list(range(8)))
+def test_random_long_contexts_against_the_oracle(ctx, seed):
+    """The same over contexts of 30k..140k rows (multi-block counting and
+    bracket, unrolled scan runs, many attention splits), one sequence each."""
+    _check_random_case(ctx, *_random_case(seed, long=True), f"random long case {seed}")
+
+
+def _check_random_case(ctx, cfg, B, name):
+    say(f"{name}: B={B} {synth.describe(cfg)}")
     wl = synth.make_workload(cfg, "cuda", B=B)
     g, _ = gpu_step(ctx, wl, two_tier=cfg.two_tier)
     seqs = list(range(B))
