@@ -67,7 +67,8 @@ def _load():
         lib.vkvref_select.restype = i32
         lib.vkvref_select.argtypes = [P, i64, i64, P, P]
         lib.vkvref_upper_bounds.restype = i32
-        lib.vkvref_upper_bounds.argtypes = [P, i64, i32, P, P, P, P, i64, P, P, P, i64, P, i32]
+        lib.vkvref_upper_bounds.argtypes = [P, i64, i32, P, P, P, P, i64, P, P, P, i64, ctypes.c_double, P,
+                                               i32]
         lib.vkvref_admit.restype = i64
         lib.vkvref_admit.argtypes = [P, i64, P, i64, ctypes.c_double, P, i64]
         lib.vkvref_attend.restype = i32
@@ -219,8 +220,12 @@ def select(key: np.ndarray, k: int):
     return sel[:k].copy(), float(theta.value)
 
 
-def upper_bounds(qt_seq, a, nq, e, x, eta, eps, gam, A: int, nthreads: int = 0) -> np.ndarray:
-    """UB_u = max_h (s^_h(u) + B_h(u)), fp64 (Lemma (Index certificate))."""
+def upper_bounds(qt_seq, a, nq, e, x, eta, eps, gam, A: int, nthreads: int = 0,
+                 cert_mult: float = 1.0) -> np.ndarray:
+    """UB_u = max_h (s^_h(u) + B_h(u)), fp64 (Lemma (Index certificate)).
+
+    cert_mult = z / sqrt(d_c - r) of Eq. (trigger) scales the sketch-residual
+    term a_h eta_u (1 = the sound bound)."""
     qt_seq = _u16(qt_seq)
     x = _u16(x)
     H, n = qt_seq.shape
@@ -228,8 +233,8 @@ def upper_bounds(qt_seq, a, nq, e, x, eta, eps, gam, A: int, nthreads: int = 0) 
     a, nq, e, eta, eps, gam = map(f, (a, nq, e, eta, eps, gam))
     ub = np.zeros(max(A, 1), np.float64)
     _load().vkvref_upper_bounds(_ptr(qt_seq), H, n, _ptr(a), _ptr(nq), _ptr(e), _ptr(x),
-                                x.shape[1], _ptr(eta), _ptr(eps), _ptr(gam), int(A), _ptr(ub),
-                                int(nthreads))
+                                x.shape[1], _ptr(eta), _ptr(eps), _ptr(gam), int(A),
+                                float(cert_mult), _ptr(ub), int(nthreads))
     return ub[:A]
 
 
@@ -286,7 +291,7 @@ def attend_list(k_sel: np.ndarray, A: int, T: int, adm: np.ndarray | None = None
 
 def step(cache, q_lat, q_rope, index, P, r: int, mode: int, W: int, k: int, scale: float,
          two_tier: bool = False, eta=None, eps=None, gam=None, cap=None, seqs=None,
-         index_has_rope: bool = True, nthreads: int = 0):
+         index_has_rope: bool = True, nthreads: int = 0, cert_mult: float = 1.0):
     """One whole decode step on the oracle for the sequences ``seqs``:
     keys -> top-k -> [bound + admission] -> attention.
 
@@ -302,7 +307,8 @@ def step(cache, q_lat, q_rope, index, P, r: int, mode: int, W: int, k: int, scal
         sel, theta = select(key, k)
         adm = None
         if two_tier:
-            ub = upper_bounds(qt[b], a[b], nq[b], e[b], x, eta[b], eps[b], gam[b], A, nthreads)
+            ub = upper_bounds(qt[b], a[b], nq[b], e[b], x, eta[b], eps[b], gam[b], A, nthreads,
+                              cert_mult)
             adm, cnt = admit(ub, sel, theta, cap)
             res["adm"][b] = adm
             res["adm_count"][b] = cnt

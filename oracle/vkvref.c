@@ -325,16 +325,23 @@ int vkvref_select(const double* key, int64_t A, int64_t k, int32_t* sel, double*
 /* ------------------------------------------------------- bound / admit */
 
 /* UB_u = max_h fl64( s^_h(u) + B_h(u) ),
- * B_h(u) = a_h*eta_u + n_h*eps_u + e_h*gamma_u  evaluated as
- *          fma(a_h, eta_u, fma(n_h, eps_u, e_h*gamma_u))  in fp64,
- * with s^_h(u) the index score of head h (as in vkvref_index_keys).
- * |s_h(u) - s^_h(u)| <= B_h(u) is Lemma (Index certificate) plus the bf16
- * rounding of the stored sketch, so UB_u bounds the exact full score. */
+ * B_h(u) = a'_h*eta_u + n_h*eps_u + e_h*gamma_u  evaluated as
+ *          fma(a'_h, eta_u, fma(n_h, eps_u, e_h*gamma_u))  in fp64,
+ * with s^_h(u) the index score of head h (as in vkvref_index_keys) and
+ * a'_h = ru_f32(cert_mult * a_h) (the product of two floats is exact in fp64).
+ * cert_mult is z / sqrt(d_c - r) of Eq. (trigger): cert_mult = 1 is the sound
+ * Cauchy-Schwarz bound, for which |s_h(u) - s^_h(u)| <= B_h(u) is Lemma (Index
+ * certificate) plus the bf16 rounding of the stored sketch, so UB_u bounds
+ * the exact full score; cert_mult < 1 is the calibrated trigger, which scales
+ * only the sketch-residual term (the rounding terms stay rigorous). */
 int vkvref_upper_bounds(const uint16_t* qt, int64_t H, int n, const float* a, const float* nq,
                         const float* e, const uint16_t* x, int64_t x_stride, const float* eta,
-                        const float* eps, const float* gam, int64_t A, double* ub, int nthreads) {
+                        const float* eps, const float* gam, int64_t A, double cert_mult, double* ub,
+                        int nthreads) {
     double* q = (double*)malloc(sizeof(double) * (size_t)(H * n));
+    float* as = (float*)malloc(sizeof(float) * (size_t)(H > 0 ? H : 1));
     for (int64_t i = 0; i < H * n; ++i) q[i] = vkvref_bf16_to_f64(qt[i]);
+    for (int64_t h = 0; h < H; ++h) as[h] = vkvref_ru_f32(cert_mult * (double)a[h]);
 #ifdef _OPENMP
     if (nthreads > 0) omp_set_num_threads(nthreads);
 #pragma omp parallel for schedule(static)
@@ -347,13 +354,14 @@ int vkvref_upper_bounds(const uint16_t* qt, int64_t H, int n, const float* a, co
             const double* qh = q + h * n;
             double acc = 0.0;
             for (int d = 0; d < n; ++d) acc = fma(qh[d], xv[d], acc);
-            double bh = fma((double)a[h], (double)eta[u],
+            double bh = fma((double)as[h], (double)eta[u],
                             fma((double)nq[h], (double)eps[u], (double)e[h] * (double)gam[u]));
             double t = acc + bh;
             if (t > best) best = t;
         }
         ub[u] = best;
     }
+    free(as);
     free(q);
     return 0;
 }

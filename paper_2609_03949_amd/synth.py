@@ -78,6 +78,7 @@ CONFIGS = {
 }
 
 BASIS_SEED = 20260903
+NEEDLE_SIGMAS = 6.0    # planted needle score, in standard deviations of a branch score
 
 
 def describe(cfg: Config) -> str:
@@ -178,8 +179,11 @@ def make_sequence(cfg: Config, b: int, q_lat_b: torch.Tensor, q_rope_b: torch.Te
         ql = q_lat_b[hd].float()
         qr_n = qr.norm(dim=-1, keepdim=True)
         ql_n = ql.norm(dim=-1, keepdim=True)
-        rope[pd] = _plant(rope[pd], qr / qr_n, 6.0 * qr_n)
-        lat[pd] = _plant(lat[pd], ql / ql_n, 6.0 * ql_n)
+        # +6 sigma per branch: for rows ~ N(0, I) the score q.x of a branch has
+        # sigma = ||q||, so the unit-direction component q^.x is set to 6,
+        # which makes q.x = 6 ||q|| = 6 sigma
+        rope[pd] = _plant(rope[pd], qr / qr_n, NEEDLE_SIGMAS)
+        lat[pd] = _plant(lat[pd], ql / ql_n, NEEDLE_SIGMAS)
     row = torch.cat([lat, rope], dim=1)
     if cfg.rows == "lognormal":
         row = row * torch.exp(0.5 * torch.randn(T, 1, generator=g, device=device))

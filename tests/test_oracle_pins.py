@@ -165,15 +165,72 @@ def test_digest_coordinate_selector_and_residual_norm(oracle_mod):
     assert np.all(eps[0] < 1e-8 * np.linalg.norm(c, axis=1))
 
 
-def test_digest_zero_basis_gives_full_norm_certificate(oracle_mod):
-    lat = rand_bf16((8, 512), scale=3.0)
+def _f32_up_sqrt(x: Fraction) -> float:
+    """Smallest float f with f * f >= x (exact rational search)."""
+    f = np.float32(math.sqrt(float(x))) if x > 0 else np.float32(0)
+    while Fraction(float(f)) ** 2 < x:
+        f = np.nextafter(f, np.float32(np.inf))
+    while f > 0:
+        p = np.nextafter(f, np.float32(0))
+        if Fraction(float(p)) ** 2 >= x:
+            f = p
+        else:
+            break
+    return float(f)
+
+
+def test_digest_zero_basis_gives_exact_margin_values(oracle_mod):
+    """P = 0: the sketch is empty, so w = P c = 0 exactly and the only nonzero
+    parts of eps and gamma are the rounding margin of the bound on ||P c - w||,
+    2^-40 * sqrt(r * ||c||^2) rounded up (exact values below, from rational
+    arithmetic); eta is a tight upper bound of ||c||.  Small-integer latents
+    make ||c||^2 an exact fp64 integer."""
+    r = 64
+    lat = small_int_bf16((8, 512), -6, 6)
     cache = _cache_from_latent(lat)
-    Pb = np.zeros((64, 512), np.uint16)
-    index, eta, eps, gam = oracle_mod.digest_build(cache, Pb, 64, with_rope=True)
+    Pb = np.zeros((r, 512), np.uint16)
+    index, eta, eps, gam = oracle_mod.digest_build(cache, Pb, r, with_rope=True)
     assert np.all(index[0, :, 64:] == 0)
-    cn = np.linalg.norm(dec(lat), axis=1)
-    assert np.all(eta[0] >= cn) and np.allclose(eta[0], cn, rtol=1e-6)
-    assert np.all(eps[0] <= 1e-8 * cn) and np.all(gam[0] <= 1e-8 * cn)
+    for u in range(8):
+        N = sum((frac_of_bits(int(b)) ** 2 for b in lat[u]), Fraction(0))
+        margin = Fraction(2) ** -40 * Fraction(_f32_up_sqrt(r * N))
+        assert Fraction(float(eps[0, u])) == margin and Fraction(float(gam[0, u])) == margin
+        e = Fraction(float(eta[0, u]))
+        assert e * e >= N
+        prev = Fraction(float(np.nextafter(np.float32(eta[0, u]), np.float32(0))))
+        assert prev * prev < N * (1 + Fraction(1, 2 ** 36))
+
+
+def test_query_prep_head_scalars_against_exact_rationals(oracle_mod):
+    """Head side of Lemma (Index certificate) with the bf16 rounding of the
+    query digest: a_h, n_h = ||qd_h||, e_h = ||qd_h - P q_h|| are valid upper
+    bounds of the exact quantities and tight (exact rational arithmetic);
+    qd_h = RNE(P q_h) of the exact sum."""
+    r, H = 8, 3
+    q_lat = rand_bf16((1, H, 512))
+    q_rope = rand_bf16((1, H, 64))
+    Pb = synth.to_numpy_bits(synth.make_basis("orthonormal", r))
+    qt, a, nq, e = oracle_mod.query_prep(q_lat, q_rope, Pb, r, oracle_mod.MODE_ROPE_DIGEST)
+    assert np.array_equal(qt[0, :, :64], q_rope[0])
+    for h in range(H):
+        q = [frac_of_bits(int(b)) for b in q_lat[0, h]]
+        w = [sum((frac_of_bits(int(Pb[j, i])) * q[i] for i in range(512)), Fraction(0))
+             for j in range(r)]
+        d = [exact_rne_bf16(v) for v in w]
+        assert list(qt[0, h, 64:]) == d
+        Nq = sum((v * v for v in q), Fraction(0))
+        Nw = sum((v * v for v in w), Fraction(0))
+        Nd = sum((frac_of_bits(dj) ** 2 for dj in d), Fraction(0))
+        Ne = sum(((frac_of_bits(d[j]) - w[j]) ** 2 for j in range(r)), Fraction(0))
+        qn = math.sqrt(float(Nq))
+        # n_h: the smallest float above ||qd|| up to the 2^-40 margin -- tight to ~1 ulp
+        nh = Fraction(float(nq[0, h]))
+        assert nh * nh >= Nd
+        prev = Fraction(float(np.nextafter(np.float32(nq[0, h]), np.float32(0))))
+        assert prev * prev < Nd * (1 + Fraction(1, 2 ** 36))
+        for got, ex in ((a[0, h], Nq - Nw), (e[0, h], Ne)):
+            assert Fraction(float(got)) ** 2 >= ex
+            assert float(got) <= fsqrt_upper(ex) * (1 + 1e-6) + 1e-9 * qn
 
 
 def test_digest_random_basis_against_exact_rationals(oracle_mod):
@@ -258,18 +315,25 @@ def test_full_rank_identity_digest_gives_exact_latent_and_full_scores(oracle_mod
     assert np.array_equal(s, full)
 
 
-def test_keys_are_exact_on_synthetic_workload(oracle_mod):
-    """The exactness self-check: every fp64 key sum of a config-0-shaped
-    workload equals the exact real dot product (so summation order is moot)."""
-    cfg = synth.CONFIGS["cfg0"]
-    wl = synth.make_workload(cfg, "cpu", T=2048)
+@pytest.mark.parametrize("name", sorted(synth.CONFIGS))
+def test_keys_are_exact_on_every_workload(oracle_mod, name):
+    """The exactness self-check on a reduced shape of every workload (one
+    sequence, 1536 rows, the workload's own heads, mode and basis): every
+    sequential fp64 key sum equals the exact real dot product, so on these
+    inputs the sequential definition is the exact one."""
+    cfg = synth.CONFIGS[name]
+    wl = synth.make_workload(cfg, "cpu", B=1, T=1536)
     cache = synth.to_numpy_bits(wl["cache"])
-    Pb = synth.to_numpy_bits(wl["P"])
+    Pb = synth.to_numpy_bits(wl["P"]) if wl["P"] is not None else None
     q_lat = synth.to_numpy_bits(wl["q_lat"])
     q_rope = synth.to_numpy_bits(wl["q_rope"])
-    index, *_ = oracle_mod.digest_build(cache, Pb, cfg.r, scalars=False)
-    qt, *_ = oracle_mod.query_prep(q_lat, q_rope, Pb, cfg.r, cfg.mode)
-    x = oracle_mod.index_rows(cache[0], index[0], cfg.mode, cfg.r)
+    rr = cfg.r if cfg.mode != oracle_mod.MODE_ROPE else 0
+    has_rope = cfg.mode != oracle_mod.MODE_DIGEST
+    index = None
+    if cfg.mode != oracle_mod.MODE_ROPE:
+        index, *_ = oracle_mod.digest_build(cache, Pb, rr, with_rope=has_rope, scalars=False)
+    qt, *_ = oracle_mod.query_prep(q_lat, q_rope, Pb, rr, cfg.mode)
+    x = oracle_mod.index_rows(cache[0], None if index is None else index[0], cfg.mode, rr, has_rope)
     key, bad = oracle_mod.index_keys(qt[0], x, wl["A"], check_exact=True)
     assert bad == 0
 
@@ -504,3 +568,57 @@ def test_read_budget_matches_paper_numbers():
     assert round(1152 / budget.reads_bytes(rho, r, f_mid, index_elem_bytes=4), 1) == \
         g["ratio_vs_dense_full_precision_index_approx"]
     assert round(rho * 576) == g["attended_dims_per_token_at_32x"]
+
+
+# ------------------------------------------------ certificate multiplier (z)
+
+def test_cert_mult_scales_only_the_residual_term(oracle_mod):
+    """Eq. (trigger): z / sqrt(d_c - r) multiplies the sketch-residual term
+    a_h eta_u; the bf16 rounding terms n_h eps_u + e_h gamma_u stay.  Checked
+    against exact rationals on a sample of rows, with a'_h the smallest float
+    >= cert_mult * a_h."""
+    wl, cache, q_lat, q_rope, index, eta, eps, gam, qt, a, nq, e, x = _tiny_two_tier(
+        oracle_mod, r=32, T=200, W=20, H=4)
+    A = wl["A"]
+    sh = dec(x[:A]) @ dec(qt[0]).T                     # exact: the sums are exact here
+    for cm in (0.0, 0.125, 0.3, 1.0):
+        ub = oracle_mod.upper_bounds(qt[0], a[0], nq[0], e[0], x, eta[0], eps[0], gam[0], A,
+                                     cert_mult=cm)
+        a2 = []
+        for h in range(4):
+            want = Fraction(cm) * Fraction(float(a[0, h]))
+            f = np.float32(float(want))
+            if Fraction(float(f)) < want:
+                f = np.nextafter(f, np.float32(np.inf))
+            a2.append(Fraction(float(f)))
+        for u in range(0, A, 17):
+            best = max(Fraction(float(sh[u, h])) + a2[h] * Fraction(float(eta[0, u]))
+                       + Fraction(float(nq[0, h])) * Fraction(float(eps[0, u]))
+                       + Fraction(float(e[0, h])) * Fraction(float(gam[0, u])) for h in range(4))
+            assert abs(Fraction(ub[u]) - best) <= abs(best) * Fraction(1, 2 ** 50)
+
+
+def test_cert_mult_one_is_the_sound_bound_and_admission_is_monotone(oracle_mod):
+    """cert_mult = 1 (z = sqrt(d_c - r)) is the default sound bound; smaller
+    multipliers admit nested subsets; cert_mult = 0 keeps only the rounding
+    slack, so it admits rows whose index score alone nearly beats theta."""
+    wl, cache, q_lat, q_rope, index, eta, eps, gam, qt, a, nq, e, x = _tiny_two_tier(
+        oracle_mod, basis="orthonormal", r=64, T=1024, W=32, H=8, needles=4)
+    A = wl["A"]
+    key, _ = oracle_mod.index_keys(qt[0], x, A)
+    sel, theta = oracle_mod.select(key, A // 32)
+    args = (qt[0], a[0], nq[0], e[0], x, eta[0], eps[0], gam[0], A)
+    ub1 = oracle_mod.upper_bounds(*args)
+    assert np.array_equal(ub1, oracle_mod.upper_bounds(*args, cert_mult=1.0))
+    prev = None
+    for cm in (0.0, 0.05, 0.2, 0.5, 1.0):
+        adm, cnt = oracle_mod.admit(oracle_mod.upper_bounds(*args, cert_mult=cm), sel, theta)
+        if prev is not None:
+            assert set(prev) <= set(adm)
+        prev = adm
+    adm0, _ = oracle_mod.admit(oracle_mod.upper_bounds(*args, cert_mult=0.0), sel, theta)
+    outside = np.setdiff1d(np.arange(A), sel)
+    # every row admitted at cert_mult = 0 has its index score within the rounding slack of theta
+    slack = (nq[0].max() * eps[0, :A].max() + e[0].max() * gam[0, :A].max()) * 1.001
+    assert np.all(key[adm0] > theta - slack)
+    assert len(adm0) < len(outside)
