@@ -117,7 +117,7 @@ def main():
 
     def run_step():
         vkv.step_run(ctx, step, bufs.ws, k, None, bufs.ub, bufs.sel, bufs.theta, bufs.adm,
-                     bufs.adm_count, bufs.cap, cfg.scale, bufs.out, bufs.lse, stream)
+                     bufs.adm_count, bufs.cap, cfg.scale, bufs.out, bufs.lse, stream, bufs.cert_mult)
 
     for _ in range(args.warmup):
         run_step()
@@ -165,14 +165,14 @@ def main():
             ev[0].record(stream)
             vkv.query_prep(ctx, step, bufs.ws, stream)
             ev[1].record(stream)
-            vkv.score(ctx, step, bufs.ws, None, bufs.ub, stream)
+            vkv.score(ctx, step, bufs.ws, None, bufs.ub, stream, bufs.cert_mult)
             ev[2].record(stream)
             vkv.select(ctx, step, bufs.ws, k, bufs.sel, bufs.theta, stream)
             ev[3].record(stream)
             j = 3
             if two_tier:
                 vkv.admit(ctx, step, bufs.ws, k, bufs.sel, bufs.theta, bufs.ub, bufs.adm,
-                          bufs.adm_count, bufs.cap, stream)
+                          bufs.adm_count, bufs.cap, stream, bufs.cert_mult)
                 j += 1
                 ev[j].record(stream)
             vkv.attend(ctx, step, bufs.ws, k, bufs.sel, bufs.adm, bufs.adm_count, bufs.cap,

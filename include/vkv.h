@@ -167,41 +167,59 @@ int vkv_query_prep(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, 
  * the certified interval [key~ - E, key~ + E] of every fp64 index score,
  *   E = 2 (n + n/32) 2^-23 max_h ||qt_h|| max_u ||x_u||
  * (the fp32 accumulation error, by Cauchy-Schwarz on sum |q_d x_d|).  key
- * (may be NULL) receives key~ as well, for diagnostics.  If ub != NULL (two-tier mode; needs st->eta/eps/gam), also
- *   ub[b,u] ~= max_h ( s^_h(u) + a_h eta_u + n_h eps_u + e_h gam_u )
- * the Cauchy-Schwarz upper bound of the full score (Lemma (Index certificate)).
+ * (may be NULL) receives key~ as well, for diagnostics.  If ub != NULL
+ * (two-tier mode; needs st->eta/eps/gam), also
+ *   ub[b,u] ~= max_h ( s^_h(u) + a'_h eta_u + n_h eps_u + e_h gam_u ),
+ *   a'_h = the smallest float >= cert_mult * a_h,
+ * the Cauchy-Schwarz upper bound of the full score (Lemma (Index certificate))
+ * with the certificate term scaled as in Eq. (trigger): cert_mult =
+ * z / sqrt(d_c - r), 1 = the sound bound, smaller = a calibrated trigger (then
+ * the bound is no longer a certificate; the bf16 rounding terms stay).
+ * cert_mult must be finite and >= 0 (ignored when ub is NULL).
  * key, ub: [B, A] fp32, contiguous.  ws is the workspace vkv_query_prep filled
  * for this step; it must then be passed unchanged to the vkv_select /
  * vkv_admit / vkv_attend calls of the same step.
  */
 int vkv_score(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, float* key,
-              float* ub, void* stream);
+              float* ub, float cert_mult, void* stream);
 
 /*
- * Exact top-k: S_b = the first k rows of [0, A) ordered by (exact index score
- * desc, row index asc), written ascending to sel[b*k .. b*k+k).  The exact
- * score is the fp64 dot product with d ascending; rows whose certified
- * interval (from vkv_score) can decide the question are classified from it,
- * the others are re-scored in fp64, so the set equals the fp64 definition bit
- * for bit.  theta[b] (fp64) = min over S_b of the exact score (-inf if k = 0).
- * 0 <= k <= A.  Reads the intervals vkv_score left in ws.
+ * Exact top-k of the index scores: the tier-1 set of the recall tier (Sec. 4.2,
+ * the rows whose index score competes for this query; in the task's reading one
+ * set per sequence, keyed by the maximum over heads of the first two terms of
+ * Eq. (trigger), ties to the lower row index).
+ * S_b = the first k rows of [0, A) ordered by (exact index score desc, row
+ * index asc), written ascending to sel[b*k .. b*k+k).  The exact score is the
+ * fp64 dot product with d ascending; rows whose certified interval (from
+ * vkv_score) decides the question are classified from it, the others are
+ * re-scored in fp64, so the set equals the fp64 definition bit for bit.
+ * theta[b] (fp64) = min over S_b of the exact score (-inf if k = 0).
+ * 0 <= k <= A.  Reads the keys vkv_score left in ws and overwrites only its
+ * own parts of ws, so it may be called again (another k) after one vkv_score.
+ * sel [B, k] int32, theta [B] fp64; errors: VKV_E_ARG (k out of range, NULL
+ * output), VKV_E_WORKSPACE.
  */
 int vkv_select(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k,
                int32_t* sel, double* theta, void* stream);
 
 /*
  * Two-tier admission (Lemma (Index certificate) with the bf16 rounding of the
- * stored sketch): admitted_b = { u in [0, A) \ S_b : UB_u > theta_b } ascending,
- *   UB_u = max_h fl64( s^_h(u) + fma(a_h, eta_u, fma(n_h, eps_u, e_h gam_u)) ).
- * Ambiguous rows are decided in fp64 as above.  adm [B, cap] int32; adm_count[b]
+ * stored sketch; the fired set of Eq. (trigger) against the k-th selected
+ * score): admitted_b = { u in [0, A) \ S_b : UB_u > theta_b } ascending,
+ *   UB_u = max_h fl64( s^_h(u) + fma(a'_h, eta_u, fma(n_h, eps_u, e_h gam_u)) ),
+ *   a'_h = the smallest float >= cert_mult * a_h.
+ * Undecided rows are decided in fp64 as above.  adm [B, cap] int32; adm_count[b]
  * = the true count (may exceed cap; then only the first cap rows are written).
  * Needs mode ROPE or ROPE_DIGEST (the key must contain the exact branch
  * summand), ub from vkv_score, and sel/theta from vkv_select with the same ws.
- * Soundness needs ||P||_2 <= 1, which vkv_digest_build certifies.
+ * The band shortcut uses ub only if vkv_score was given the same cert_mult;
+ * otherwise every row outside S is decided by its exact bound (slower, same
+ * result).  May be called again on the same ws.  Soundness (cert_mult = 1)
+ * needs ||P||_2 <= 1, which vkv_digest_build certifies.
  */
 int vkv_admit(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k,
-              const int32_t* sel, const double* theta, const float* ub, int32_t* adm,
-              int32_t* adm_count, int64_t cap, void* stream);
+              const int32_t* sel, const double* theta, const float* ub, float cert_mult,
+              int32_t* adm, int32_t* adm_count, int64_t cap, void* stream);
 
 /*
  * Exact attention of every head over the attended multiset of sequence b:
@@ -220,12 +238,26 @@ int vkv_attend(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int6
 
 /* query_prep -> score -> select -> [admit iff adm_count != NULL] -> attend,
  * same arguments as the individual calls (key and ub are the caller's
- * intermediates), all queued on `stream`; validates every stage's arguments
- * before it launches anything. */
+ * intermediates; cert_mult is used by the two-tier stages only), all queued on
+ * `stream`; validates every stage's arguments before it launches anything. */
 int vkv_step_run(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k,
                  float* key, float* ub, int32_t* sel, double* theta, int32_t* adm,
-                 int32_t* adm_count, int64_t cap, float scale, uint16_t* out, float* lse,
-                 void* stream);
+                 int32_t* adm_count, int64_t cap, float cert_mult, float scale, uint16_t* out,
+                 float* lse, void* stream);
+
+/*
+ * The executable row-set invariant (the deployment's per-step row-set
+ * assertion, appendix "Measurement integrity: full protocol"), on caller
+ * buffers: every sel[b] row lies in the archive [0, A) and the list is strictly
+ * ascending; if adm_count != NULL, 0 <= adm_count[b] <= A - k and the first
+ * min(adm_count[b], cap) adm[b] rows lie in the archive, strictly ascending
+ * and outside sel[b].  Copies the lists to the host and synchronises `stream`.
+ * Returns VKV_OK, VKV_E_DEBUG_ROWS naming the first violation, or an argument
+ * error.  The same checks run inside vkv_select / vkv_admit / vkv_step_run when
+ * VKV_DEBUG_ROWS is set.
+ */
+int vkv_check_rows(vkv_ctx* ctx, const vkv_step* st, int64_t k, const int32_t* sel,
+                   const int32_t* adm, const int32_t* adm_count, int64_t cap, void* stream);
 
 /* enable != 0: vkv_step_run records a pair of HIP events around its score
  * scan, on the call's stream, for up to 512 calls; vkv_score_timing reads

@@ -19,7 +19,7 @@ import torch  # noqa: F401  (loads the HIP runtime the library binds to)
 __all__ = [
     "VKV_MODE_ROPE", "VKV_MODE_DIGEST", "VKV_MODE_ROPE_DIGEST", "VkvError", "Context", "Step",
     "lib_path", "load", "digest_build", "workspace_size", "query_prep", "score", "select", "admit", "attend",
-    "step_run", "exported_symbols",
+    "step_run", "check_rows", "exported_symbols",
 ]
 
 VKV_MODE_ROPE, VKV_MODE_DIGEST, VKV_MODE_ROPE_DIGEST = 1, 2, 3
@@ -31,7 +31,7 @@ _LIB_PATH = os.path.join(_HERE, "libvkv.so")
 exported_symbols = (
     "vkv_create", "vkv_destroy", "vkv_status_string", "vkv_last_error", "vkv_version",
     "vkv_digest_build", "vkv_workspace_size", "vkv_query_prep", "vkv_score", "vkv_select", "vkv_admit",
-    "vkv_attend", "vkv_step_run", "vkv_set_timing", "vkv_score_timing",
+    "vkv_attend", "vkv_step_run", "vkv_check_rows", "vkv_set_timing", "vkv_score_timing",
 )
 
 
@@ -83,19 +83,21 @@ def load():
     lib.vkv_digest_build.argtypes = [P, P, i64, i64, i64, i64, P, i32, i32, P, i64, i64, P, P, P, P]
     lib.vkv_workspace_size.argtypes = [sp, i64, i64, ctypes.POINTER(ctypes.c_size_t)]
     lib.vkv_query_prep.argtypes = [P, sp, P, ctypes.c_size_t, P]
-    lib.vkv_score.argtypes = [P, sp, P, ctypes.c_size_t, P, P, P]
+    f32 = ctypes.c_float
+    lib.vkv_score.argtypes = [P, sp, P, ctypes.c_size_t, P, P, f32, P]
     lib.vkv_select.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P]
-    lib.vkv_admit.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P, P, P, i64, P]
+    lib.vkv_admit.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P, f32, P, P, i64, P]
     lib.vkv_attend.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P, i64, ctypes.c_float, P, P, P]
     lib.vkv_step_run.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P, P, P, P, i64,
-                                 ctypes.c_float, P, P, P]
+                                 f32, f32, P, P, P]
+    lib.vkv_check_rows.argtypes = [P, sp, i64, P, P, P, i64, P]
     lib.vkv_set_timing.argtypes = [P, ctypes.c_int]
     lib.vkv_score_timing.argtypes = [P, ctypes.POINTER(ctypes.c_float), ctypes.c_int]
     for name in exported_symbols:
         getattr(lib, name).restype = getattr(lib, name).restype or ctypes.c_int
     for name in ("vkv_create", "vkv_destroy", "vkv_digest_build", "vkv_workspace_size",
                  "vkv_query_prep", "vkv_score",
-                 "vkv_select", "vkv_admit", "vkv_attend", "vkv_step_run", "vkv_version",
+                 "vkv_select", "vkv_admit", "vkv_attend", "vkv_step_run", "vkv_check_rows", "vkv_version",
                  "vkv_set_timing", "vkv_score_timing"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
@@ -222,9 +224,9 @@ def query_prep(ctx: Context, step: Step, ws: torch.Tensor, stream=None):
 
 
 def score(ctx: Context, step: Step, ws: torch.Tensor, key: Optional[torch.Tensor] = None,
-          ub: Optional[torch.Tensor] = None, stream=None):
+          ub: Optional[torch.Tensor] = None, stream=None, cert_mult: float = 1.0):
     ctx.check(ctx.lib.vkv_score(ctx.handle, step.ref, _ptr(ws), ws.numel(), _ptr(key), _ptr(ub),
-                                _stream(stream)))
+                                float(cert_mult), _stream(stream)))
 
 
 def select(ctx: Context, step: Step, ws: torch.Tensor, k: int, sel: torch.Tensor,
@@ -235,10 +237,10 @@ def select(ctx: Context, step: Step, ws: torch.Tensor, k: int, sel: torch.Tensor
 
 def admit(ctx: Context, step: Step, ws: torch.Tensor, k: int, sel: torch.Tensor,
           theta: torch.Tensor, ub: torch.Tensor, adm: torch.Tensor, adm_count: torch.Tensor,
-          cap: int, stream=None):
+          cap: int, stream=None, cert_mult: float = 1.0):
     ctx.check(ctx.lib.vkv_admit(ctx.handle, step.ref, _ptr(ws), ws.numel(), int(k), _ptr(sel),
-                                _ptr(theta), _ptr(ub), _ptr(adm), _ptr(adm_count), int(cap),
-                                _stream(stream)))
+                                _ptr(theta), _ptr(ub), float(cert_mult), _ptr(adm), _ptr(adm_count),
+                                int(cap), _stream(stream)))
 
 
 def attend(ctx: Context, step: Step, ws: torch.Tensor, k: int, sel: torch.Tensor,
@@ -252,17 +254,29 @@ def attend(ctx: Context, step: Step, ws: torch.Tensor, k: int, sel: torch.Tensor
 def step_run(ctx: Context, step: Step, ws: torch.Tensor, k: int, key: torch.Tensor,
              ub: Optional[torch.Tensor], sel: torch.Tensor, theta: torch.Tensor,
              adm: Optional[torch.Tensor], adm_count: Optional[torch.Tensor], cap: int,
-             scale: float, out: torch.Tensor, lse: torch.Tensor, stream=None):
+             scale: float, out: torch.Tensor, lse: torch.Tensor, stream=None,
+             cert_mult: float = 1.0):
     ctx.check(ctx.lib.vkv_step_run(ctx.handle, step.ref, _ptr(ws), ws.numel(), int(k), _ptr(key),
                                    _ptr(ub), _ptr(sel), _ptr(theta), _ptr(adm), _ptr(adm_count),
-                                   int(cap), float(scale), _ptr(out), _ptr(lse), _stream(stream)))
+                                   int(cap), float(cert_mult), float(scale), _ptr(out), _ptr(lse),
+                                   _stream(stream)))
+
+
+def check_rows(ctx: Context, step: Step, k: int, sel: Optional[torch.Tensor],
+               adm: Optional[torch.Tensor] = None, adm_count: Optional[torch.Tensor] = None,
+               cap: int = 0, stream=None):
+    """vkv_check_rows: the row-set invariant on caller buffers (synchronises)."""
+    ctx.check(ctx.lib.vkv_check_rows(ctx.handle, step.ref, int(k), _ptr(sel), _ptr(adm),
+                                     _ptr(adm_count), int(cap), _stream(stream)))
 
 
 class Buffers:
     """Output and intermediate buffers of one step, on the step's device."""
 
-    def __init__(self, step: Step, k: int, two_tier: bool = False, cap: Optional[int] = None):
+    def __init__(self, step: Step, k: int, two_tier: bool = False, cap: Optional[int] = None,
+                 cert_mult: float = 1.0):
         dev = step.device
+        self.cert_mult = float(cert_mult)
         B, H, A = step.B, step.H, step.A
         self.k = int(k)
         self.cap = (A if cap is None else int(cap)) if two_tier else 0
@@ -278,4 +292,4 @@ class Buffers:
 
     def run(self, ctx: Context, step: Step, scale: float, stream=None):
         step_run(ctx, step, self.ws, self.k, self.key, self.ub, self.sel, self.theta, self.adm,
-                 self.adm_count, self.cap, scale, self.out, self.lse, stream)
+                 self.adm_count, self.cap, scale, self.out, self.lse, stream, self.cert_mult)

@@ -176,11 +176,15 @@ __global__ __launch_bounds__(64 * QP_MAX_WAVES) void qprep_project_kernel(QprepA
 // bounds of the scorer and the selection: computed by wave 0 of the first
 // block of each sequence in the scorer launch (the query prep of the step has
 // finished and cleared the words); all values are >= 0.
+// a'_h of the bound: the smallest float >= cert_mult * a_h (exact product in fp64)
+__device__ __forceinline__ float scaled_a(float cm, float ah) { return ru_f32((double)cm * (double)ah); }
+
 __device__ __forceinline__ void store_head_maxima(const ScoreArgs& a, int b, int lane) {
     float4 m = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int h = lane; h < a.H; h += 64) {
         const float4 v = reinterpret_cast<const float4*>(a.hsc)[(int64_t)b * a.H + h];
-        m = make_float4(fmaxf(m.x, v.x), fmaxf(m.y, v.y), fmaxf(m.z, v.z), fmaxf(m.w, v.w));
+        const float ax = a.ub ? scaled_a(a.cert_mult, v.x) : v.x;
+        m = make_float4(fmaxf(m.x, ax), fmaxf(m.y, v.y), fmaxf(m.z, v.z), fmaxf(m.w, v.w));
     }
     for (int o = 32; o > 0; o >>= 1) {
         m.x = fmaxf(m.x, __shfl_xor(m.x, o));
@@ -194,6 +198,8 @@ __device__ __forceinline__ void store_head_maxima(const ScoreArgs& a, int b, int
         sq[SQ_NMAX] = __float_as_uint(m.y);
         sq[SQ_EMAX] = __float_as_uint(m.z);
         sq[SQ_QMAX] = __float_as_uint(m.w);
+        // the multiplier the bound below used (an impossible float pattern without one)
+        sq[SQ_CMULT] = a.ub ? __float_as_uint(a.cert_mult) : 0xFFFFFFFFu;
     }
 }
 
@@ -296,8 +302,10 @@ __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
     const int KS = a.n / 32;
     const int HT = (a.H + 15) / 16;
     if (UB) {
-        for (int h = tid; h < 16 * HT; h += 256)
-            s_hs[h] = reinterpret_cast<const float4*>(a.hsc)[(int64_t)b * a.H + (h % a.H)];
+        for (int h = tid; h < 16 * HT; h += 256) {
+            const float4 v = reinterpret_cast<const float4*>(a.hsc)[(int64_t)b * a.H + (h % a.H)];
+            s_hs[h] = make_float4(scaled_a(a.cert_mult, v.x), v.y, v.z, v.w);
+        }
         __syncthreads();
     }
     if (blockIdx.x == 0 && threadIdx.x < 64) store_head_maxima(a, b, threadIdx.x);
@@ -609,7 +617,8 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
 #pragma unroll
         for (int ht = 0; ht < HT; ++ht) {
             const int h = (16 * ht + c) % a.H;
-            hsf[ht] = g < 3 ? a.hsc[((int64_t)b * a.H + h) * 4 + g] : 0.f;
+            const float v = g < 3 ? a.hsc[((int64_t)b * a.H + h) * 4 + g] : 0.f;
+            hsf[ht] = g == 0 ? scaled_a(a.cert_mult, v) : v;
             coef = fmaxf(coef, hsf[ht]);
         }
 #pragma unroll

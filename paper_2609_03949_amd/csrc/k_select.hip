@@ -2,39 +2,52 @@
 //
 // Selection (per sequence b, archive rows [0, A)), given fp32 keys key~ with a
 // certified bound |key~ - key| <= E for every row (key = the fp64 index score,
-// E from the per-sequence maxima of ||qt_h|| and ||x_u||):
-//   1. a strided sample of the keys places a bracket [t_lo, t_hi] around the
-//      k-th largest key~; one counting pass counts the keys above t_hi and
-//      lists the keys inside it; one block per sequence histograms the list
-//      over 4096 fine bins and finds the bin of the k-th largest key~ (if the
-//      sample missed, it histograms the whole key range instead).  With v = key~ + E and w = key~ - E
-//      (rounded outward) this gives HI >= k-th largest v and LO <= k-th
-//      largest w, so the k-th largest exact key lies in [LO, HI];
-//   2. rows with w > HI are certainly selected and rows with v < LO certainly
-//      not; the rows in between are appended to an ambiguous list;
-//   3. each ambiguous row's heads are scored again in fp32 (any order: the
-//      same bound E holds) and only the heads that can still hold the maximum
-//      (within 2E of it) are re-scored in fp64 with d ascending -- the exact
-//      definition -- as independent (row, head) chains;
-//   4. the ambiguous rows are ranked among themselves by (exact key desc,
-//      index asc); the first k - n_in join S, and rank k - n_in - 1 gives theta;
-//   5. an ordered compaction writes S ascending.
+// E from the per-sequence maxima of ||qt_h|| and ||x_u||).  Three launches:
+//   1. bracket (one block per sequence): a strided sample of the keys places
+//      [t_lo, t_hi] around the k-th largest key~ and fixes the early bounds
+//      CLO = down(t_lo - E), CHI = up(t_hi + E);
+//   2. count (one block per 4096 rows): rows with key~ - E > CHI are certainly
+//      selected, rows with key~ + E < CLO certainly not; the others are
+//      candidates, listed in the block's own region of the candidate array
+//      with their keys~; per-block counts (selected, candidates, keys~ above
+//      t_hi).  Nothing is accumulated across blocks or calls;
+//   3. resolve (one block per sequence): a histogram of the candidates inside
+//      [t_lo, t_hi] gives the fine bin of the k-th largest key~ (if the sample
+//      missed, the block histograms the whole key range instead and classifies
+//      every row itself); with v = key~ + E and w = key~ - E rounded outward
+//      this gives HI >= k-th largest v and LO <= k-th largest w, so the k-th
+//      largest exact key lies in [LO, HI].  The candidates with w > HI are
+//      selected, with v < LO not; the rest are undecided.  Their exact keys:
+//      each undecided row's heads are scored again in fp32 (the same bound E
+//      holds) and only the heads within 2E of the row's maximum get the fp64
+//      chain with d ascending, the exact definition.  The undecided rows are
+//      ranked by (exact key desc, index asc) -- pairwise counting, or a radix
+//      select on (key, ~index) when they are many -- and the first
+//      k - n_selected join S; the last of them gives theta.  Finally an
+//      ordered compaction of the flags writes S ascending.
+// Every row certainly selected has exact key >= w > HI >= theta* and every
+// row certainly excluded has exact key <= v < LO <= theta*, so S is the fp64
+// definition bit for bit.
 // Admission (Lemma (Index certificate)) applies the same band argument to the
-// upper bound UB_u against theta.
+// upper bound UB_u against theta: a classification launch per 4096 rows and a
+// resolve block per sequence (exact bounds of the undecided rows, then the
+// ordered compaction of the admitted rows).
 #include "vkv_internal.h"
 
 namespace vkv {
 
-constexpr int SEL_THREADS = 256;
+constexpr int SEL_THREADS = 256;             // counting / classification blocks
+constexpr int CB_PER = CB_KEYS / SEL_THREADS;   // rows per thread of a counting block (16)
+constexpr int RES_THREADS = 512;             // resolve blocks: one per sequence (8 waves)
+constexpr int RES_WAVES = RES_THREADS / 64;
+constexpr int RES_LDS = 144 * 1024;          // dynamic LDS of a resolve block
 constexpr int SAMPLE_MAX = 2048;             // keys sampled per sequence to place the bracket
 constexpr int SAMPLE_BINS = 2048;            // bins of the sample's histogram
-constexpr int COUNT_KEYS_PER_BLOCK = 4096;   // keys per block of the counting pass
-constexpr int KEY_BATCH = 16;                // keys per thread in flight
-constexpr int EX_BLOCKS = 4;                 // per sequence: blocks of the exact-key pass (one per CU: 140 KB of LDS)
-constexpr int DECIDE_BLOCKS = 16;            // per sequence: blocks of the admission decision pass
-constexpr int RANK_BLOCKS = 16;
+constexpr int RANK_QUAD_MAX = RES_THREADS;   // undecided rows ranked pairwise; radix select above
+constexpr int COMPACT_PER = 64;              // flags per thread and round of the ordered compaction
+constexpr int EX_QT_MAX = 32768;             // qt elements staged in LDS (64 KB)
 
-// order-preserving encoding of fp64 (for 64-bit atomic max); -0 maps as +0
+// order-preserving encoding of fp64 (for 64-bit compares); -0 maps as +0
 __device__ __forceinline__ uint64_t f64_to_ord(double d) {
     const uint64_t u = d2u(d == 0.0 ? 0.0 : d);
     return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
@@ -82,33 +95,59 @@ __device__ __forceinline__ float rd_f32(double x) {
     return f;
 }
 
-// ------------------------------------------------------------ small kernels
+// --------------------------------------------------------- block helpers
 
-__global__ __launch_bounds__(SEL_THREADS) void fill_u8_kernel(uint8_t* p, int64_t n, uint8_t v) {
-    for (int64_t i = (int64_t)blockIdx.x * SEL_THREADS + threadIdx.x; i < n; i += (int64_t)gridDim.x * SEL_THREADS)
-        p[i] = v;
-}
-
-__global__ __launch_bounds__(64) void select_empty_kernel(SelectArgs a) {
-    // k = 0: nothing selected, theta = -inf, chunk counters cleared
-    const int b = blockIdx.x;
-    if (threadIdx.x == 0) a.theta[b] = -INFINITY;
-    if (threadIdx.x == 1) a.seq[(int64_t)b * SQ_WORDS + SQ_NAMB2] = 0u;
-    for (int64_t i = threadIdx.x; i < a.nch * CC_WORDS; i += 64) a.ccount[(int64_t)b * a.nch * CC_WORDS + i] = 0u;
-}
-
-__device__ __forceinline__ uint32_t block_sum_u32(uint32_t v, uint32_t* s_red) {
-    const int tid = threadIdx.x;
+template <int NT>
+__device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t* s_red) {
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    if ((tid & 63) == 0) s_red[tid >> 6] = v;
+    if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = v;
     __syncthreads();
     uint32_t t = 0;
-    for (int w = 0; w < SEL_THREADS / 64; ++w) t += s_red[w];
+    for (int w = 0; w < NT / 64; ++w) t += s_red[w];
     __syncthreads();
     return t;
 }
 
-// ---------------------------------------------------------- histogram pass
+// Exclusive prefix of v over the threads in index order; total = the sum.
+template <int NT>
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* s_w, uint32_t& total) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    uint32_t incl = v;
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t t = __shfl_up(incl, o);
+        if (lane >= o) incl += t;
+    }
+    if (lane == 63) s_w[w] = incl;
+    __syncthreads();
+    uint32_t before = 0, tot = 0;
+    for (int i = 0; i < NT / 64; ++i) {
+        const uint32_t c = s_w[i];
+        before += (i < w) ? c : 0u;
+        tot += c;
+    }
+    __syncthreads();
+    total = tot;
+    return before + incl - v;
+}
+
+// Sum over threads t' >= tid of v.
+template <int NT>
+__device__ __forceinline__ uint32_t block_suffix_incl(uint32_t v, uint32_t* s_w) {
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t t = __shfl_down(v, o);
+        if (lane + o < 64) v += t;
+    }
+    __syncthreads();
+    if (lane == 0) s_w[w] = v;
+    __syncthreads();
+    uint32_t add = 0;
+    for (int w2 = w + 1; w2 < NT / 64; ++w2) add += s_w[w2];
+    __syncthreads();
+    return v + add;
+}
+
+// ---------------------------------------------------------- histogram bins
 
 template <int NB = HIST_BINS>
 __device__ __forceinline__ float bin_scale(float lo, float hi) {
@@ -123,22 +162,30 @@ __device__ __forceinline__ int bin_of(float x, float lo, float scale) {
     return bi < NB ? bi : NB - 1;
 }
 
-// Sum over threads t' >= tid of v (block of SEL_THREADS threads).
-__device__ __forceinline__ uint32_t block_suffix_incl(uint32_t v, uint32_t* s_w) {
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t t = __shfl_down(v, o);
-        if (lane + o < 64) v += t;
+// In a block of NT threads holding a histogram s_h[NB]: the bin d where the
+// count of keys in bins >= d first reaches `target` (1 <= target <= total).
+// Returns -1 in threads that do not own it.
+template <int NB, int NT>
+__device__ __forceinline__ int find_rank_bin(const uint32_t* s_h, uint32_t target, uint32_t* s_w) {
+    constexpr int PER = NB / NT;
+    const int tid = threadIdx.x;
+    uint32_t loc = 0;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) loc += s_h[tid * PER + j];
+    const uint32_t suf = block_suffix_incl<NT>(loc, s_w);
+    int found = -1;
+    if (suf - loc < target && target <= suf) {
+        uint32_t run = suf - loc;
+        for (int d = (tid + 1) * PER - 1; d >= tid * PER; --d) {
+            run += s_h[d];
+            if (run >= target) {
+                found = d;
+                break;
+            }
+        }
     }
-    __syncthreads();
-    if (lane == 0) s_w[w] = v;
-    __syncthreads();
-    uint32_t add = 0;
-    for (int w2 = w + 1; w2 < SEL_THREADS / 64; ++w2) add += s_w[w2];
-    return v + add;
+    return found;
 }
-
-// ------------------------------------------------------------ the bracket
 
 // Bin d of the linear bins of [lo, lo + HIST_BINS / scale): keys x with
 // bin_of(x) = d satisfy edge_lo(d) <= x <= edge_hi(d) (the fp32 rounding of the
@@ -156,40 +203,20 @@ __device__ __forceinline__ double edge_lo_of(int d, float lo, float scale) {
     return fmax((double)lo, (double)lo + (double)d * w * (1.0 - 0x1p-20) - slack);
 }
 
-// In a block of SEL_THREADS threads holding a histogram s_h[NB]: the bin d
-// where the count of keys in bins >= d first reaches `target` (1 <= target <=
-// total).  Returns -1 in threads that do not own it.
-template <int NB = HIST_BINS>
-__device__ __forceinline__ int find_rank_bin(const uint32_t* s_h, uint32_t target, uint32_t* s_w) {
-    constexpr int PER = NB / SEL_THREADS;
-    const int tid = threadIdx.x;
-    uint32_t loc = 0;
-#pragma unroll
-    for (int j = 0; j < PER; ++j) loc += s_h[tid * PER + j];
-    const uint32_t suf = block_suffix_incl(loc, s_w);
-    int found = -1;
-    if (suf - loc < target && target <= suf) {
-        uint32_t run = suf - loc;
-        for (int d = (tid + 1) * PER - 1; d >= tid * PER; --d) {
-            run += s_h[d];
-            if (run >= target) {
-                found = d;
-                break;
-            }
-        }
-    }
-    return found;
-}
+// ---------------------------------------------------------- 1. the bracket
 
 // The bracket of the k-th largest key~ placed from a sample of up to
 // SAMPLE_MAX keys (runs of 32 consecutive keys at evenly spaced offsets; all
 // keys if A <= SAMPLE_MAX): [t_lo, t_hi] with sample ranks k_s -/+ (4 sqrt(k_s)
-// + 16), k_s = k m / A, from a histogram of the sample over its own range.  A
-// deterministic function of the keys, so every block that evaluates it gets
-// the same bracket.  Only a heuristic: the bracket pass checks it.
-__device__ void sample_bracket(const SelectArgs& a, int b, const uint32_t* sq, uint32_t* s_h, uint32_t* s_w,
-                               float* s_mm, float& t_lo, float& t_hi) {
+// + 16), k_s = k m / A, from a histogram of the sample over its own range.
+// Only a heuristic: the resolve block checks it.
+__global__ __launch_bounds__(SEL_THREADS) void sel_bracket_kernel(SelectArgs a) {
+    __shared__ uint32_t s_h[SAMPLE_BINS];
+    __shared__ uint32_t s_w[SEL_THREADS / 64];
+    __shared__ float s_mm[8];
+    const int b = blockIdx.x;
     const int tid = threadIdx.x;
+    uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
     const int64_t A = a.A;
     const int m = (int)min(A, (int64_t)SAMPLE_MAX);
     const float* kt = a.kt + (int64_t)b * A;
@@ -197,6 +224,7 @@ __device__ void sample_bracket(const SelectArgs& a, int b, const uint32_t* sq, u
     constexpr int RUN = 32;
     const int nrun = (m + RUN - 1) / RUN;
     const int64_t stride = (m < A && nrun > 1) ? (A - RUN) / (nrun - 1) : 0;
+    const float kmax = ord_to_key(sq[SQ_KMAX]), kmin = ord_to_key(sq[SQ_KMIN]);
     float v[PER];
     float lo = INFINITY, hi = -INFINITY;
 #pragma unroll
@@ -232,293 +260,116 @@ __device__ void sample_bracket(const SelectArgs& a, int b, const uint32_t* sq, u
     const double dl = 4.0 * sqrt(ks) + 16.0;
     const int64_t c_hi = (int64_t)floor(ks - dl);   // fewer than c_hi samples above t_hi
     const int64_t c_lo = (int64_t)ceil(ks + dl);    // at least c_lo samples at or above t_lo
-    const int d_hi = (c_hi >= 1) ? find_rank_bin<SAMPLE_BINS>(s_h, (uint32_t)c_hi, s_w) : -1;
-    const int d_lo = (c_lo <= m) ? find_rank_bin<SAMPLE_BINS>(s_h, (uint32_t)c_lo, s_w) : -1;
-    __syncthreads();
+    const int d_hi = (c_hi >= 1) ? find_rank_bin<SAMPLE_BINS, SEL_THREADS>(s_h, (uint32_t)c_hi, s_w) : -1;
+    const int d_lo = (c_lo <= m) ? find_rank_bin<SAMPLE_BINS, SEL_THREADS>(s_h, (uint32_t)c_lo, s_w) : -1;
     // no cut on a side the sample cannot place: the scorer's key extremes
     if (tid == 0) {
-        s_mm[0] = ord_to_key(sq[SQ_KMAX]);
-        s_mm[1] = ord_to_key(sq[SQ_KMIN]);
+        s_mm[0] = kmax;
+        s_mm[1] = kmin;
     }
     __syncthreads();
     if (d_hi >= 0) s_mm[0] = scale > 0.f ? lo + (float)(d_hi + 1) / scale : hi;
     if (d_lo >= 0) s_mm[1] = scale > 0.f ? lo + (float)d_lo / scale : lo;
     __syncthreads();
-    t_hi = s_mm[0];
-    t_lo = s_mm[1];
-    __syncthreads();
-}
-
-// Counting pass: every block places the sampled bracket, counts its keys
-// above t_hi and appends those in [t_lo, t_hi] (the bracket holds a few
-// percent of the keys) to the sequence's list, one atomic per wave; the bulk
-// of the keys, below t_lo, costs one compare.
-__global__ __launch_bounds__(SEL_THREADS) void count_kernel(SelectArgs a) {
-    __shared__ uint32_t s_h[SAMPLE_BINS];
-    __shared__ uint32_t s_w[SEL_THREADS / 64];
-    __shared__ float s_mm[8];
-    const int b = blockIdx.y;
-    const int tid = threadIdx.x, lane = tid & 63;
-    uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    // this block's keys are loaded together with the sample (one round trip)
-    static_assert(COUNT_KEYS_PER_BLOCK == KEY_BATCH * SEL_THREADS, "one batch of keys per thread");
-    const float* kt = a.kt + (int64_t)b * a.A;
-    const int64_t u0 = (int64_t)blockIdx.x * COUNT_KEYS_PER_BLOCK;
-    const int64_t u1 = min(a.A, u0 + COUNT_KEYS_PER_BLOCK);
-    float k[KEY_BATCH];
-#pragma unroll
-    for (int j = 0; j < KEY_BATCH; ++j) {
-        const int64_t u = u0 + tid + (int64_t)j * SEL_THREADS;
-        k[j] = (u < u1) ? kt[u] : 0.f;
-    }
-    float tlo, thi;
-    sample_bracket(a, b, sq, s_h, s_w, s_mm, tlo, thi);
-    if (blockIdx.x == 0 && tid == 0) {
-        sq[SQ_BLO] = __float_as_uint(tlo);
-        sq[SQ_BHI] = __float_as_uint(thi);
-        sq[SQ_NAMB] = 0u;
-        sq[SQ_NAMB2] = 0u;
-    }
-    uint32_t above = 0, nin = 0;
-#pragma unroll
-    for (int j = 0; j < KEY_BATCH; ++j) {
-        const int64_t u = u0 + tid + (int64_t)j * SEL_THREADS;
-        const bool live = u < u1;
-        above += (live && k[j] > thi);
-        nin += (live && k[j] <= thi && k[j] >= tlo);
-    }
-    // wave-inclusive scan of the in-bracket counts, one append slot range per wave
-    uint32_t incl = nin;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t t = __shfl_up(incl, o);
-        if (lane >= o) incl += t;
-    }
-    uint32_t base = 0;
-    if (lane == 63 && incl) base = atomicAdd(&sq[SQ_NBR], incl);
-    base = __shfl(base, 63) + (incl - nin);
-    float* list = reinterpret_cast<float*>(a.amb) + (int64_t)b * a.A;
-#pragma unroll
-    for (int j = 0; j < KEY_BATCH; ++j) {
-        const int64_t u = u0 + tid + (int64_t)j * SEL_THREADS;
-        if (u < u1 && k[j] <= thi && k[j] >= tlo) list[base++] = k[j];
-    }
-    above = block_sum_u32(above, s_w);
-    if (tid == 0 && above) atomicAdd(&sq[SQ_ABOVE], above);
-}
-
-// One block per sequence, after the counting pass: the bin of the k-th
-// largest key~ (a histogram of the listed in-bracket keys) and the band
-// around it,
-//   THI = up(edge_hi + E) >= k-th largest v,  TLO = down(edge_lo - E) <= k-th largest w.
-// If the sample missed (the k-th key~ lies outside [t_lo, t_hi]) the block
-// histograms the sequence's whole key range itself.
-__global__ __launch_bounds__(SEL_THREADS) void bracket_kernel(SelectArgs a) {
-    __shared__ uint32_t s_h[HIST_BINS];
-    __shared__ uint32_t s_w[SEL_THREADS / 64];
-    __shared__ int s_bin;
-    const int b = blockIdx.x;
-    const int tid = threadIdx.x;
-    uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    const float tlo = __uint_as_float(sq[SQ_BLO]);
-    const float thi = __uint_as_float(sq[SQ_BHI]);
-    const uint32_t tot_above = sq[SQ_ABOVE];
-    const uint32_t inr = sq[SQ_NBR];
-    {
-        // the keys inside the sampled bracket, listed by the counting pass
-        const float sc0 = bin_scale(tlo, thi);
-        for (int i = tid; i < HIST_BINS; i += SEL_THREADS) s_h[i] = 0u;
-        __syncthreads();
-        const float* list = reinterpret_cast<const float*>(a.amb) + (int64_t)b * a.A;
-        for (uint32_t i0 = 0; i0 < inr; i0 += KEY_BATCH * SEL_THREADS) {   // loads of a batch in flight together
-            float v[KEY_BATCH];
-#pragma unroll
-            for (int j = 0; j < KEY_BATCH; ++j) {
-                const uint32_t i = i0 + tid + j * SEL_THREADS;
-                v[j] = i < inr ? list[i] : 0.f;
-            }
-#pragma unroll
-            for (int j = 0; j < KEY_BATCH; ++j)
-                if (i0 + tid + j * SEL_THREADS < inr) atomicAdd(&s_h[bin_of(v[j], tlo, sc0)], 1u);
-        }
-        __syncthreads();
-    }
-    const float E = key_band_f32(sq, a.n);
-    const int64_t need = a.k - (int64_t)tot_above;
-    const bool ok = need >= 1 && need <= (int64_t)inr;
-    float lo = tlo, hi = thi, sc = bin_scale(tlo, thi);
-    if (!ok) {
-        // the sample missed: histogram the whole key range in this block
-        lo = ord_to_key(sq[SQ_KMIN]);
-        hi = ord_to_key(sq[SQ_KMAX]);
-        sc = bin_scale(lo, hi);
-        __syncthreads();
-        for (int i = tid; i < HIST_BINS; i += SEL_THREADS) s_h[i] = 0u;
-        __syncthreads();
-        const float* kb = a.kt + (int64_t)b * a.A;
-        for (int64_t ub = 0; ub < a.A; ub += KEY_BATCH * SEL_THREADS) {
-            float k[KEY_BATCH];
-#pragma unroll
-            for (int j = 0; j < KEY_BATCH; ++j) {
-                const int64_t u = ub + tid + (int64_t)j * SEL_THREADS;
-                k[j] = (u < a.A) ? kb[u] : 0.f;
-            }
-#pragma unroll
-            for (int j = 0; j < KEY_BATCH; ++j) {
-                const int64_t u = ub + tid + (int64_t)j * SEL_THREADS;
-                if (u < a.A) atomicAdd(&s_h[bin_of(k[j], lo, sc)], 1u);
-            }
-        }
-    }
-    const uint32_t target = (uint32_t)(ok ? need : a.k);
-    if (tid == 0) s_bin = -1;
-    __syncthreads();
-    const int d = find_rank_bin(s_h, target, s_w);
-    if (d >= 0) s_bin = d;
-    __syncthreads();
     if (tid == 0) {
-        const int db = s_bin < 0 ? 0 : s_bin;
-        sq[SQ_THI] = __float_as_uint(band_hi(ru_f32(edge_hi_of(db, lo, hi, sc)), E));
-        sq[SQ_TLO] = __float_as_uint(band_lo(rd_f32(edge_lo_of(db, lo, sc)), E));
-        a.theta[b] = -INFINITY;
+        const float t_hi = s_mm[0], t_lo = s_mm[1];
+        const float E = key_band_f32(sq, a.n);
+        sq[SQ_BLO] = __float_as_uint(t_lo);
+        sq[SQ_BHI] = __float_as_uint(t_hi);
+        sq[SQ_CLO] = __float_as_uint(band_lo(t_lo, E));
+        sq[SQ_CHI] = __float_as_uint(band_hi(t_hi, E));
     }
 }
 
-// ----------------------------------------------------------- classify
+// ----------------------------------------------------------- 2. counting
 
-// Append the rows of a wave whose predicate holds to list[base..) (order
-// within the list is irrelevant: the ranking below is by (key, index)).
-__device__ __forceinline__ void wave_append(bool pred, int32_t value, uint32_t* counter, int32_t* list) {
-    const uint64_t mask = __ballot(pred);
-    if (mask == 0) return;
-    const int lane = threadIdx.x & 63;
-    const int leader = __ffsll((unsigned long long)mask) - 1;
-    uint32_t base = 0;
-    if (lane == leader) base = atomicAdd(counter, (uint32_t)__popcll(mask));
-    base = __shfl(base, leader);
-    if (pred) list[base + __popcll(mask & ((1ull << lane) - 1ull))] = value;
-}
-
-__global__ __launch_bounds__(SEL_THREADS) void classify_kernel(SelectArgs a) {
-    __shared__ uint32_t s_red[SEL_THREADS / 64];
-    constexpr int PER = CHUNK / SEL_THREADS;
-    const int b = blockIdx.y;
-    const int c = blockIdx.x;
-    const int tid = threadIdx.x;
-    uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    const float LO = __uint_as_float(sq[SQ_TLO]);
-    const float HI = __uint_as_float(sq[SQ_THI]);
-    const float E = key_band_f32(sq, a.n);
-    const float* kt = a.kt + (int64_t)b * a.A;
-    uint8_t* fb = a.flags + (int64_t)b * a.A;
-    int32_t* amb = a.amb + (int64_t)b * a.A;
-    const int64_t u0 = (int64_t)c * CHUNK;
-    const int64_t u1 = min(a.A, u0 + CHUNK);
-    float k[PER];
+// Rows of the block's region whose predicate held, written at the start of
+// the region (thread order, then j order); returns the block's total.
+__device__ __forceinline__ uint32_t region_append(uint32_t mask, int32_t* cand, float* candkey,
+                                                  const float (&k)[CB_PER], int64_t ub0, uint32_t* s_w) {
+    uint32_t tot;
+    uint32_t pos = block_excl_scan<SEL_THREADS>((uint32_t)__popc(mask), s_w, tot);
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        const int64_t u = u0 + tid + (int64_t)j * SEL_THREADS;
-        k[j] = (u < u1) ? kt[u] : 0.f;
-    }
-    uint32_t nin = 0;
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        const int64_t u = u0 + tid + (int64_t)j * SEL_THREADS;
-        uint8_t f = 0;
-        if (u < u1) {
-            // selected for sure: key >= w > HI >= theta*;  out for sure: key <= v < LO <= theta*
-            f = (band_lo(k[j], E) > HI) ? 1 : ((band_hi(k[j], E) < LO) ? 0 : 2);
-            fb[u] = f;
-        }
-        nin += (f == 1);
-        wave_append(f == 2, (int32_t)u, &sq[SQ_NAMB], amb);
-    }
-    nin = block_sum_u32(nin, s_red);
-    if (tid == 0) {
-        uint32_t* cc = a.ccount + ((int64_t)b * a.nch + c) * CC_WORDS;
-        cc[CC_IN] = nin;
-        cc[CC_SELAMB] = 0u;
-        cc[CC_ADM] = 0u;
-        cc[CC_ADMAMB] = 0u;
-    }
-}
-
-// ---------------------------------------------------- ordered compaction
-
-struct CompactArgs {
-    const uint8_t* flags;
-    uint8_t target;
-    const uint32_t* ccount;
-    int w0, w1;            // count words of a chunk
-    int32_t* out;
-    int64_t out_stride;
-    int64_t cap;
-    int32_t* total;        // [B] or null
-    int64_t A, nch;
-};
-
-__global__ __launch_bounds__(SEL_THREADS) void compact_kernel(CompactArgs a) {
-    __shared__ uint32_t s_scan[SEL_THREADS];
-    __shared__ uint32_t s_red[SEL_THREADS / 64];
-    const int b = blockIdx.y;
-    const int c = blockIdx.x;
-    const int tid = threadIdx.x;
-    const uint32_t* cc = a.ccount + (int64_t)b * a.nch * CC_WORDS;
-    uint32_t part = 0;
-    for (int64_t q = tid; q < c; q += SEL_THREADS) part += cc[q * CC_WORDS + a.w0] + cc[q * CC_WORDS + a.w1];
-    const uint32_t base = block_sum_u32(part, s_red);
-    const uint32_t mine = cc[(int64_t)c * CC_WORDS + a.w0] + cc[(int64_t)c * CC_WORDS + a.w1];
-    if (a.total && c == a.nch - 1 && tid == 0) a.total[b] = (int32_t)(base + mine);
-    if (mine == 0) return;
-    // each thread owns 8 consecutive rows of the chunk
-    const int64_t u0 = (int64_t)c * CHUNK + 8 * tid;
-    const uint8_t* fb = a.flags + (int64_t)b * a.A;
-    uint8_t f[8];
-    uint32_t cnt = 0;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        const int64_t u = u0 + e;
-        f[e] = (u < a.A) ? fb[u] : (uint8_t)0xFF;
-        cnt += (f[e] == a.target);
-    }
-    s_scan[tid] = cnt;
-    __syncthreads();
-    for (int o = 1; o < SEL_THREADS; o <<= 1) {
-        uint32_t v = (tid >= o) ? s_scan[tid - o] : 0u;
-        __syncthreads();
-        s_scan[tid] += v;
-        __syncthreads();
-    }
-    uint32_t pos = base + s_scan[tid] - cnt;
-    int32_t* ob = a.out + (int64_t)b * a.out_stride;
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-        if (f[e] == a.target) {
-            if ((int64_t)pos < a.cap) ob[pos] = (int32_t)(u0 + e);
+    for (int j = 0; j < CB_PER; ++j)
+        if (mask & (1u << j)) {
+            cand[pos] = (int32_t)(ub0 + threadIdx.x + (int64_t)SEL_THREADS * j);
+            if (candkey) candkey[pos] = k[j];
             ++pos;
         }
+    return tot;
 }
 
-static hipError_t run_compact(const SelectArgs& s, const uint8_t* flags, uint8_t target, int w0, int w1,
-                              int32_t* out, int64_t out_stride, int64_t cap, int32_t* total, hipStream_t st) {
-    CompactArgs c{flags, target, s.ccount, w0, w1, out, out_stride, cap, total, s.A, s.nch};
-    hipLaunchKernelGGL(compact_kernel, dim3((unsigned)s.nch, s.B), dim3(SEL_THREADS), 0, st, c);
-    return hipGetLastError();
+__global__ __launch_bounds__(SEL_THREADS) void sel_count_kernel(SelectArgs a) {
+    __shared__ uint32_t s_w[SEL_THREADS / 64];
+    const int b = blockIdx.y, tid = threadIdx.x;
+    const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
+    const int64_t ub0 = (int64_t)blockIdx.x * CB_KEYS;
+    const int64_t ue = min(a.A, ub0 + CB_KEYS);
+    const float* kt = a.kt + (int64_t)b * a.A;
+    float k[CB_PER];
+#pragma unroll
+    for (int j = 0; j < CB_PER; ++j) {
+        const int64_t u = ub0 + tid + (int64_t)SEL_THREADS * j;
+        k[j] = (u < ue) ? kt[u] : 0.f;
+    }
+    const float CLO = __uint_as_float(sq[SQ_CLO]), CHI = __uint_as_float(sq[SQ_CHI]);
+    const float thi = __uint_as_float(sq[SQ_BHI]);
+    const float E = key_band_f32(sq, a.n);
+    uint8_t* fb = a.flags + (int64_t)b * a.fstride;
+    uint32_t nin = 0, nabove = 0, mask = 0;
+#pragma unroll
+    for (int j = 0; j < CB_PER; ++j) {
+        const int64_t u = ub0 + tid + (int64_t)SEL_THREADS * j;
+        if (u < ue) {
+            const uint8_t f = (band_lo(k[j], E) > CHI) ? 1 : ((band_hi(k[j], E) < CLO) ? 0 : 2);
+            fb[u] = f;
+            nin += (f == 1);
+            nabove += (k[j] > thi);
+            mask |= (f == 2) ? (1u << j) : 0u;
+        }
+    }
+    const uint32_t ncand = region_append(mask, a.cand + (int64_t)b * a.A + ub0,
+                                         a.candkey + (int64_t)b * a.A + ub0, k, ub0, s_w);
+    const uint32_t packed = block_sum<SEL_THREADS>(nin | (nabove << 16), s_w);   // both <= 4096
+    if (tid == 0) {
+        uint32_t* w = a.blk + ((int64_t)b * a.nblk + blockIdx.x) * BLK_WORDS;
+        w[BW_IN] = packed & 0xFFFFu;
+        w[BW_CAND] = ncand;
+        w[BW_ABOVE] = packed >> 16;
+    }
 }
 
-// --------------------------------------------------------- fp64 re-scoring
+// ------------------------------------------------------ exact re-scoring
 
-// Exact keys of the ambiguous rows, a tile of 16 rows per wave.  The rows are
-// gathered straight into the MFMA operand layout (lane 16 g + c: row c, dims
-// 32 ks + 8 g ..) and scored against every head with fp32 accumulation -- the
-// scorer's arithmetic, so |s~ - s| <= E for every (row, head).  Only heads
-// within 2E of their row's maximum can hold the exact maximum; each such
-// (row, head) pair gets its fp64 chain (d ascending from +0: the exact
-// definition) from one lane, and the row's exact key is the maximum over its
-// pairs (LDS atomic max on the order-preserving encoding).  With UB the
-// screened quantity is s^_h + B_h(u) (Lemma (Index certificate)) and the
-// margin is that bound's own fp32 error.
-constexpr int EX_QT_MAX = 32768;   // qt elements staged in LDS (64 KB)
+// Carve of a resolve block's dynamic LDS for the exact-key phase.
+struct ExLds {
+    uint16_t* qt;                 // [H][n] (qlds) -- else qt is read from global memory
+    float4* hs;                   // [128] head scalars (a', n, e) for bounds
+    unsigned long long* best;     // [waves][16]
+    uint32_t* list;               // [waves][64]
+    uint16_t* x;                  // [waves][16 rows][n]
+    int nwx;                      // waves that take row tiles
+    bool qlds;
+};
+
+__device__ __forceinline__ ExLds ex_carve(uint8_t* lds, int H, int n) {
+    ExLds e;
+    size_t o = 0;
+    e.qlds = H * n <= EX_QT_MAX;
+    e.qt = reinterpret_cast<uint16_t*>(lds);
+    o += e.qlds ? (size_t)H * n * 2 : 0;
+    o = (o + 15) & ~(size_t)15;
+    e.hs = reinterpret_cast<float4*>(lds + o);
+    o += 128 * 16;
+    e.best = reinterpret_cast<unsigned long long*>(lds + o);
+    o += RES_WAVES * 16 * 8;
+    e.list = reinterpret_cast<uint32_t*>(lds + o);
+    o += RES_WAVES * 64 * 4;
+    e.x = reinterpret_cast<uint16_t*>(lds + o);
+    const int avail = (int)(((size_t)RES_LDS - o) / ((size_t)32 * n));   // 16 rows of n bf16 per wave
+    e.nwx = avail < RES_WAVES ? avail : RES_WAVES;
+    return e;
+}
 
 template <bool UB>
 __device__ __forceinline__ double exact_chain(const uint16_t* q, const uint16_t* x, int n, float4 hs, double et,
@@ -544,273 +395,481 @@ __device__ __forceinline__ double exact_chain(const uint16_t* q, const uint16_t*
     return acc;
 }
 
-template <bool UB, bool QLDS>
-__global__ __launch_bounds__(SEL_THREADS) void exact_keys_kernel(SelectArgs a) {
-    __shared__ __align__(16) uint16_t s_qt[QLDS ? EX_QT_MAX : 8];   // [H][n]
-    __shared__ float4 s_hs[128];
-    __shared__ unsigned long long s_best[4][16];
-    __shared__ uint32_t s_list[4][64];
-    __shared__ __align__(16) uint16_t s_x[4][16 * D_ROW];   // each wave's 16 gathered rows, for the fp64 chains
-    const int b = blockIdx.y;
+// a'_h of the bound: the smallest float >= cert_mult * a_h (exact product in fp64)
+__device__ __forceinline__ float scaled_a(float cm, float ah) { return ru_f32((double)cm * (double)ah); }
+
+// Exact keys (or, with UB, exact bounds) of the rows amb[0..namb) of sequence b
+// into ak[i] (order-preserving encoding), in a resolve block.  A tile of 16
+// rows per wave: the rows are gathered straight into the MFMA operand layout
+// (lane 16 g + c: row c, dims 32 ks + 8 g ..) and scored against every head
+// with fp32 accumulation -- the scorer's arithmetic, so the screened value is
+// within E of the exact one for every (row, head).  Only heads within
+// `margin` (2E) of their row's maximum can hold the exact maximum; each such
+// (row, head) pair gets its fp64 chain (d ascending from +0) from one lane,
+// and the row's exact value is the maximum over its pairs.  margin = +inf
+// evaluates every head exactly.
+template <bool UB>
+__device__ __forceinline__ void exact_keys_block(const SelectArgs& a, int b, int64_t namb, const int32_t* amb, uint64_t* ak,
+                                 const ExLds& L, float margin) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4, c = lane & 15;
-    const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    const int64_t namb = sq[UB ? SQ_NAMB2 : SQ_NAMB];
-    if ((int64_t)blockIdx.x * 64 >= namb) return;
     const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
     const int n8 = a.n / 8;
-    if (QLDS) {
-        constexpr int QP = EX_QT_MAX / 8 / SEL_THREADS;
-        u16x8_t v[QP];
-#pragma unroll
-        for (int j = 0; j < QP; ++j) {
-            const int p = tid + SEL_THREADS * j;
-            v[j] = (p < a.H * n8) ? *reinterpret_cast<const u16x8_t*>(qtb + 8 * (int64_t)p)
-                                  : u16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
-        }
-#pragma unroll
-        for (int j = 0; j < QP; ++j) {
-            const int p = tid + SEL_THREADS * j;
-            if (p < a.H * n8) *reinterpret_cast<u16x8_t*>(&s_qt[8 * p]) = v[j];
-        }
+    if (L.qlds) {
+        for (int p = tid; p < a.H * n8; p += RES_THREADS)
+            *reinterpret_cast<u16x8_t*>(&L.qt[8 * p]) = *reinterpret_cast<const u16x8_t*>(qtb + 8 * (int64_t)p);
     }
-    if (UB && tid < a.H) s_hs[tid] = reinterpret_cast<const float4*>(a.hsc)[(int64_t)b * a.H + tid];
+    if (UB && tid < a.H) {
+        const float4 hs = reinterpret_cast<const float4*>(a.hsc)[(int64_t)b * a.H + tid];
+        const float ax = scaled_a(a.cert_mult, hs.x);
+        L.hs[tid] = make_float4(ax, hs.y, hs.z, hs.w);
+    }
     __syncthreads();
-    const uint16_t* qsrc = QLDS ? s_qt : qtb;
-    const uint16_t* xb = a.x + (int64_t)b * a.xbs;
-    const int32_t* amb = a.amb + (int64_t)b * a.A;
-    uint64_t* ak = a.ambkey + (int64_t)b * a.A;
-    const float E = ru_f32(UB ? ub_error_of(sq, a.n) * (1.0 + 0x1p-20) : key_error_of(sq, a.n));
-    const float margin = next_up_f32(2.0f * E);
-    const int KS = a.n / 32, HT = (a.H + 15) / 16;
-    for (int64_t t0 = ((int64_t)blockIdx.x * 4 + wave) * 16; t0 < namb; t0 += (int64_t)gridDim.x * 64) {
-        const int64_t i = min(t0 + c, namb - 1);
-        const int64_t u = amb[i];
-        const uint16_t* x = xb + u * a.xs;
-        f32x4_t acc[8];
+    if (wave < L.nwx && namb > 0) {
+        const uint16_t* qsrc = L.qlds ? L.qt : qtb;
+        const uint16_t* xb = a.x + (int64_t)b * a.xbs;
+        uint16_t* sx = L.x + (size_t)wave * 16 * a.n;
+        unsigned long long* best = L.best + wave * 16;
+        uint32_t* list = L.list + wave * 64;
+        const int KS = a.n / 32, HT = (a.H + 15) / 16;
+        for (int64_t t0 = (int64_t)wave * 16; t0 < namb; t0 += (int64_t)L.nwx * 16) {
+            const int64_t i = min(t0 + c, namb - 1);
+            const int64_t u = amb[i];
+            const uint16_t* x = xb + u * a.xs;
+            f32x4_t acc[8];
 #pragma unroll
-        for (int ht = 0; ht < 8; ++ht) acc[ht] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        for (int ks = 0; ks < KS; ++ks) {
-            const bf16x8_t xf = *reinterpret_cast<const bf16x8_t*>(x + 32 * ks + 8 * g);
-            *reinterpret_cast<bf16x8_t*>(&s_x[wave][c * a.n + 32 * ks + 8 * g]) = xf;
+            for (int ht = 0; ht < 8; ++ht) acc[ht] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            for (int ks = 0; ks < KS; ++ks) {
+                const bf16x8_t xf = *reinterpret_cast<const bf16x8_t*>(x + 32 * ks + 8 * g);
+                *reinterpret_cast<bf16x8_t*>(&sx[c * a.n + 32 * ks + 8 * g]) = xf;
 #pragma unroll
-            for (int ht = 0; ht < 8; ++ht) {
-                if (ht < HT) {
-                    const int h = (16 * ht + c) % a.H;
-                    const bf16x8_t qf = *reinterpret_cast<const bf16x8_t*>(qsrc + (int64_t)h * a.n + 32 * ks + 8 * g);
-                    acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf, xf, acc[ht], 0, 0, 0);
-                }
-            }
-        }
-        // acc[ht][q] = screened value of head 16 ht + 4 g + q for row c
-        float et = 0.f, ep = 0.f, ga = 0.f;
-        if (UB) {
-            const int64_t o = (int64_t)b * a.T + u;
-            et = a.eta[o];
-            ep = a.eps[o];
-            ga = a.gam[o];
-        }
-        float m = -INFINITY;
-#pragma unroll
-        for (int ht = 0; ht < 8; ++ht)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int h = 16 * ht + 4 * g + q;
-                float v = -INFINITY;
-                if (ht < HT && h < a.H) {
-                    v = acc[ht][q];
-                    if (UB) {
-                        const float4 hs = s_hs[h];
-                        v += fmaf(hs.x, et, fmaf(hs.y, ep, hs.z * ga));
+                for (int ht = 0; ht < 8; ++ht) {
+                    if (ht < HT) {
+                        const int h = (16 * ht + c) % a.H;
+                        const bf16x8_t qf = *reinterpret_cast<const bf16x8_t*>(qsrc + (int64_t)h * a.n + 32 * ks + 8 * g);
+                        acc[ht] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf, xf, acc[ht], 0, 0, 0);
                     }
                 }
-                acc[ht][q] = v;
-                m = fmaxf(m, v);
             }
-        m = fmaxf(m, __shfl_xor(m, 16));
-        m = fmaxf(m, __shfl_xor(m, 32));
-        const float thr = next_down_f32(m - margin);
-        if (lane < 16) s_best[wave][lane] = (unsigned long long)f64_to_ord(-INFINITY);
-        // the rows are in LDS for every lane of the wave (LDS operations of a
-        // wave complete in order)
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        __builtin_amdgcn_wave_barrier();
-        // candidates in rounds of up to 64 pairs, one fp64 chain per lane
-        int nl = 0;
-        auto flush = [&]() {
-            if (lane < nl) {
-                const uint32_t e = s_list[wave][lane];
-                const int cr = (int)(e >> 8), h = (int)(e & 255);
-                const int64_t ir = t0 + cr;
-                const int64_t ur = amb[ir];
-                const int64_t o = (int64_t)b * a.T + ur;
-                const float4 hs = UB ? s_hs[h] : make_float4(0.f, 0.f, 0.f, 0.f);
-                const double v = exact_chain<UB>(qsrc + (int64_t)h * a.n, &s_x[wave][cr * a.n], a.n, hs,
-                                                 UB ? (double)a.eta[o] : 0.0, UB ? (double)a.eps[o] : 0.0,
-                                                 UB ? (double)a.gam[o] : 0.0);
-                atomicMax(&s_best[wave][cr], (unsigned long long)f64_to_ord(v));
+            // acc[ht][q] = screened value of head 16 ht + 4 g + q for row c
+            float et = 0.f, ep = 0.f, ga = 0.f;
+            if (UB) {
+                const int64_t o = (int64_t)b * a.T + u;
+                et = a.eta[o];
+                ep = a.eps[o];
+                ga = a.gam[o];
             }
-            nl = 0;
-        };
+            float m = -INFINITY;
 #pragma unroll
-        for (int ht = 0; ht < 8; ++ht)
+            for (int ht = 0; ht < 8; ++ht)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const bool cand = (t0 + c < namb) && acc[ht][q] >= thr && acc[ht][q] > -INFINITY;
-                const uint64_t bal = __ballot(cand);
-                const int cnt = __popcll(bal);
-                if (cnt == 0) continue;
-                if (nl + cnt > 64) flush();
-                if (cand) {
-                    const int pos = nl + __popcll(bal & ((1ull << lane) - 1ull));
-                    s_list[wave][pos] = ((uint32_t)c << 8) | (uint32_t)(16 * ht + 4 * g + q);
+                for (int q = 0; q < 4; ++q) {
+                    const int h = 16 * ht + 4 * g + q;
+                    float v = -INFINITY;
+                    if (ht < HT && h < a.H) {
+                        v = acc[ht][q];
+                        if (UB) {
+                            const float4 hs = L.hs[h];
+                            v += fmaf(hs.x, et, fmaf(hs.y, ep, hs.z * ga));
+                        }
+                    }
+                    acc[ht][q] = v;
+                    m = fmaxf(m, v);
                 }
-                nl += cnt;
-            }
-        flush();
-        if (lane < 16 && t0 + lane < namb) ak[t0 + lane] = s_best[wave][lane];
+            m = fmaxf(m, __shfl_xor(m, 16));
+            m = fmaxf(m, __shfl_xor(m, 32));
+            const float thr = next_down_f32(m - margin);
+            if (lane < 16) best[lane] = (unsigned long long)f64_to_ord(-INFINITY);
+            // the rows are in LDS for every lane of the wave (LDS operations of a
+            // wave complete in order)
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            __builtin_amdgcn_wave_barrier();
+            // candidates in rounds of up to 64 pairs, one fp64 chain per lane
+            int nl = 0;
+            auto flush = [&]() {
+                if (lane < nl) {
+                    const uint32_t e = list[lane];
+                    const int cr = (int)(e >> 8), h = (int)(e & 255);
+                    const int64_t ur = amb[t0 + cr];
+                    const int64_t o = (int64_t)b * a.T + ur;
+                    const float4 hs = UB ? L.hs[h] : make_float4(0.f, 0.f, 0.f, 0.f);
+                    const double v = exact_chain<UB>(qsrc + (int64_t)h * a.n, &sx[cr * a.n], a.n, hs,
+                                                     UB ? (double)a.eta[o] : 0.0, UB ? (double)a.eps[o] : 0.0,
+                                                     UB ? (double)a.gam[o] : 0.0);
+                    atomicMax(&best[cr], (unsigned long long)f64_to_ord(v));
+                }
+                nl = 0;
+            };
+#pragma unroll
+            for (int ht = 0; ht < 8; ++ht)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const bool cand = (t0 + c < namb) && acc[ht][q] >= thr && acc[ht][q] > -INFINITY;
+                    const uint64_t bal = __ballot(cand);
+                    const int cnt = __popcll(bal);
+                    if (cnt == 0) continue;
+                    if (nl + cnt > 64) flush();
+                    if (cand) {
+                        const int pos = nl + __popcll(bal & ((1ull << lane) - 1ull));
+                        list[pos] = ((uint32_t)c << 8) | (uint32_t)(16 * ht + 4 * g + q);
+                    }
+                    nl += cnt;
+                }
+            flush();
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            __builtin_amdgcn_wave_barrier();
+            if (lane < 16 && t0 + lane < namb) ak[t0 + lane] = best[lane];
+            // the next tile's row stores must not overtake this tile's chain reads
+            __builtin_amdgcn_wave_barrier();
+        }
+    }
+    __syncthreads();
+}
+
+// Undecided rows of the count regions: wave w walks regions w, w + 16, ...;
+// `keep` decides per (row, key~) whether the row stays undecided (and writes
+// its flag).  The kept rows are appended to amb (order irrelevant).
+template <typename F>
+__device__ __forceinline__ void walk_regions(const SelectArgs& a, int b, bool with_keys, uint32_t* s_namb,
+                                             int32_t* amb, F keep) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (int64_t i = wave; i < a.nblk; i += RES_WAVES) {
+        const uint32_t cnt = a.blk[((int64_t)b * a.nblk + i) * BLK_WORDS + BW_CAND];
+        const int32_t* cr = a.cand + (int64_t)b * a.A + i * CB_KEYS;
+        const float* ck = a.candkey + (int64_t)b * a.A + i * CB_KEYS;
+        for (uint32_t j0 = 0; j0 < cnt; j0 += 64) {
+            const uint32_t j = j0 + lane;
+            const bool live = j < cnt;
+            const int32_t u = live ? cr[j] : 0;
+            const float kv = (live && with_keys) ? ck[j] : 0.f;
+            const bool und = live && keep(u, kv);
+            const uint64_t bal = __ballot(und);
+            if (bal == 0) continue;
+            const int leader = __ffsll((unsigned long long)bal) - 1;
+            uint32_t base = 0;
+            if (lane == leader) base = atomicAdd(s_namb, (uint32_t)__popcll(bal));
+            base = __shfl(base, leader);
+            if (und) amb[base + __popcll(bal & ((1ull << lane) - 1ull))] = u;
+        }
     }
 }
 
-template <bool UB>
-static hipError_t run_exact_keys(const SelectArgs& a, hipStream_t s) {
-    dim3 g(EX_BLOCKS, a.B);
-    if ((int64_t)a.H * a.n <= EX_QT_MAX)
-        hipLaunchKernelGGL((exact_keys_kernel<UB, true>), g, dim3(SEL_THREADS), 0, s, a);
-    else
-        hipLaunchKernelGGL((exact_keys_kernel<UB, false>), g, dim3(SEL_THREADS), 0, s, a);
-    return hipGetLastError();
-}
-
-// Rank of each ambiguous row among the ambiguous rows by (exact key desc,
-// index asc); the first k - n_in are selected.  theta = the key at rank
-// k - n_in - 1, which is the k-th largest exact key overall.  A block ranks
-// RK_ROWS rows: thread (row r, quarter q) counts the rows ahead of r in the
-// q-th quarter of each tile of the list (staged in LDS), then the four
-// partial counts are summed.
-constexpr int RK_ROWS = SEL_THREADS / 4;
-constexpr int RK_TILE = 2048;
-
-__global__ __launch_bounds__(SEL_THREADS) void rank_select_kernel(SelectArgs a) {
-    __shared__ double s_k[RK_TILE];
-    __shared__ int32_t s_u[RK_TILE];
-    __shared__ uint32_t s_r[4][RK_ROWS];
-    const int b = blockIdx.y;
+// Ordered compaction: rows u < A whose flag equals `target`, ascending, into
+// out[0 .. min(total, cap)); returns the total (all threads).  fb is the
+// sequence's flag row, padded to a multiple of 64 bytes and 16-byte aligned.
+__device__ __forceinline__ int64_t compact_flags(const uint8_t* fb, int64_t A, uint8_t target, int32_t* out, int64_t cap,
+                                 uint32_t* s_w) {
     const int tid = threadIdx.x;
-    const int r = tid % RK_ROWS, q = tid / RK_ROWS;
-    __shared__ uint32_t s_red[SEL_THREADS / 64];
-    const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    const int64_t namb = sq[SQ_NAMB];
-    if ((int64_t)blockIdx.x * RK_ROWS >= namb) return;
-    // rows certainly in S: the sum of the chunk counts of the classification
-    uint32_t nin = 0;
-    for (int64_t c = tid; c < a.nch; c += SEL_THREADS) nin += a.ccount[((int64_t)b * a.nch + c) * CC_WORDS + CC_IN];
-    nin = block_sum_u32(nin, s_red);
-    const int64_t need = a.k - (int64_t)nin;
-    const uint64_t* kb = a.ambkey + (int64_t)b * a.A;
-    const int32_t* ub = a.amb + (int64_t)b * a.A;
-    for (int64_t base = (int64_t)blockIdx.x * RK_ROWS; base < namb; base += (int64_t)gridDim.x * RK_ROWS) {
-        const int64_t i = base + r;
-        const bool have = i < namb;
-        const double ki = have ? ord_to_f64(kb[i]) : 0.0;
-        const int32_t ui = have ? ub[i] : 0;
-        uint32_t rank = 0;
-        for (int64_t t0 = 0; t0 < namb; t0 += RK_TILE) {
-            const int lim = (int)min((int64_t)RK_TILE, namb - t0);
-            __syncthreads();
-            constexpr int PER = RK_TILE / SEL_THREADS;
-            double kv[PER];
-            int32_t uv[PER];
+    int64_t carry = 0;
+    for (int64_t c0 = 0; c0 < A; c0 += (int64_t)RES_THREADS * COMPACT_PER) {
+        const int64_t u0 = c0 + (int64_t)COMPACT_PER * tid;
+        u32x4_t v[COMPACT_PER / 16];
 #pragma unroll
-            for (int j = 0; j < PER; ++j) {
-                const int e = tid + SEL_THREADS * j;
-                kv[j] = (e < lim) ? ord_to_f64(kb[t0 + e]) : 0.0;
-                uv[j] = (e < lim) ? ub[t0 + e] : 0;
-            }
+        for (int i = 0; i < COMPACT_PER / 16; ++i)
+            v[i] = (u0 < A) ? *reinterpret_cast<const u32x4_t*>(fb + u0 + 16 * i) : u32x4_t{0u, 0u, 0u, 0u};
+        const int lim = (int)max((int64_t)0, min((int64_t)COMPACT_PER, A - u0));
+        uint32_t cnt = 0;
 #pragma unroll
-            for (int j = 0; j < PER; ++j) {
-                s_k[tid + SEL_THREADS * j] = kv[j];
-                s_u[tid + SEL_THREADS * j] = uv[j];
+        for (int e = 0; e < COMPACT_PER; ++e) {
+            const uint32_t byte = (v[e >> 4][(e >> 2) & 3] >> (8 * (e & 3))) & 0xFFu;
+            cnt += (e < lim && byte == target);
+        }
+        uint32_t tot;
+        int64_t pos = carry + block_excl_scan<RES_THREADS>(cnt, s_w, tot);
+#pragma unroll
+        for (int e = 0; e < COMPACT_PER; ++e) {
+            const uint32_t byte = (v[e >> 4][(e >> 2) & 3] >> (8 * (e & 3))) & 0xFFu;
+            if (e < lim && byte == target) {
+                if (pos < cap) out[pos] = (int32_t)(u0 + e);
+                ++pos;
             }
-            __syncthreads();
-            if (have) {
-                const int qlen = (lim + 3) / 4;
-                const int j0 = q * qlen, j1 = min(lim, j0 + qlen);
-#pragma unroll 4
-                for (int j = j0; j < j1; ++j) {
-                    const double kj = s_k[j];
-                    rank += (kj > ki) || (kj == ki && s_u[j] < ui);
+        }
+        carry += tot;
+    }
+    return carry;
+}
+
+// Rank of the undecided rows by (exact key desc, index asc): the first
+// `need` of them get flag 1; returns (in thread 0's view, via *theta_ord) the
+// key of the last of them.  Pairwise counting with the list staged in LDS
+// when it is short; otherwise a radix select on the 96-bit composite
+// (order key, ~index), whose larger values come first.
+__device__ __forceinline__ void rank_winners(const int32_t* amb, const uint64_t* ak, int64_t namb, int64_t need, uint8_t* fb,
+                             uint8_t* lds, uint64_t* s_theta) {
+    const int tid = threadIdx.x;
+    if (namb <= RANK_QUAD_MAX) {
+        uint64_t* s_k = reinterpret_cast<uint64_t*>(lds);
+        int32_t* s_u = reinterpret_cast<int32_t*>(lds + RANK_QUAD_MAX * 8);
+        if (tid < namb) {
+            s_k[tid] = ak[tid];
+            s_u[tid] = amb[tid];
+        }
+        __syncthreads();
+        if (tid < namb) {
+            const uint64_t ki = s_k[tid];
+            const int32_t ui = s_u[tid];
+            int64_t rank = 0;
+            for (int64_t j = 0; j < namb; ++j) {
+                const uint64_t kj = s_k[j];
+                rank += (kj > ki) || (kj == ki && s_u[j] < ui);
+            }
+            if (rank < need) {
+                fb[ui] = 1;
+                if (rank == need - 1) *s_theta = ki;
+            }
+        }
+        __syncthreads();
+        return;
+    }
+    uint32_t* s_h = reinterpret_cast<uint32_t*>(lds);            // 256 bins
+    uint32_t* s_sel = s_h + 256;                                  // chosen digit, count above it
+    uint64_t pre_hi = 0, mask_hi = 0;
+    uint32_t pre_lo = 0, mask_lo = 0;
+    uint32_t rem = (uint32_t)need;
+    for (int p = 0; p < 12; ++p) {
+        if (tid < 256) s_h[tid] = 0u;
+        __syncthreads();
+        for (int64_t i = tid; i < namb; i += RES_THREADS) {
+            const uint64_t hi = ak[i];
+            const uint32_t lo = ~(uint32_t)amb[i];
+            if ((hi & mask_hi) == pre_hi && (lo & mask_lo) == pre_lo) {
+                const uint32_t dg = p < 8 ? (uint32_t)(hi >> (56 - 8 * p)) & 255u : (lo >> (24 - 8 * (p - 8))) & 255u;
+                atomicAdd(&s_h[dg], 1u);
+            }
+        }
+        __syncthreads();
+        if (tid < 64) {
+            // lane l owns digits 4 l .. 4 l + 3; counts from the top digit down
+            uint32_t loc = s_h[4 * tid] + s_h[4 * tid + 1] + s_h[4 * tid + 2] + s_h[4 * tid + 3];
+            uint32_t suf = loc;
+            for (int o = 1; o < 64; o <<= 1) {
+                const uint32_t t = __shfl_down(suf, o);
+                if (tid + o < 64) suf += t;
+            }
+            if (suf - loc < rem && rem <= suf) {
+                uint32_t run = suf - loc;
+                for (int d = 4 * tid + 3; d >= 4 * tid; --d) {
+                    if (run + s_h[d] >= rem) {
+                        s_sel[0] = (uint32_t)d;
+                        s_sel[1] = run;
+                        break;
+                    }
+                    run += s_h[d];
                 }
             }
         }
-        s_r[q][r] = rank;
         __syncthreads();
-        if (q == 0 && have) {
-            const int64_t rk = (int64_t)s_r[0][r] + s_r[1][r] + s_r[2][r] + s_r[3][r];
-            if (rk < need) {
-                a.flags[(int64_t)b * a.A + ui] = 1;
-                atomicAdd(&a.ccount[((int64_t)b * a.nch + ui / CHUNK) * CC_WORDS + CC_SELAMB], 1u);
-                if (rk == need - 1) a.theta[b] = ki;
+        const uint32_t d = s_sel[0];
+        rem -= s_sel[1];
+        if (p < 8) {
+            pre_hi |= (uint64_t)d << (56 - 8 * p);
+            mask_hi |= (uint64_t)255 << (56 - 8 * p);
+        } else {
+            pre_lo |= d << (24 - 8 * (p - 8));
+            mask_lo |= 255u << (24 - 8 * (p - 8));
+        }
+        __syncthreads();
+    }
+    for (int64_t i = tid; i < namb; i += RES_THREADS) {
+        const uint64_t hi = ak[i];
+        const uint32_t lo = ~(uint32_t)amb[i];
+        if (hi > pre_hi || (hi == pre_hi && lo >= pre_lo)) fb[amb[i]] = 1;
+    }
+    if (tid == 0) *s_theta = pre_hi;
+    __syncthreads();
+}
+
+// ------------------------------------------------------------- 3. resolve
+
+__global__ __launch_bounds__(RES_THREADS, 1) void sel_resolve_kernel(SelectArgs a) {
+    extern __shared__ __align__(16) uint8_t lds[];
+    __shared__ uint32_t s_w[RES_WAVES];
+    __shared__ uint32_t s_namb, s_nin2;
+    __shared__ int s_bin;
+    __shared__ uint64_t s_theta;
+    const int b = blockIdx.x, tid = threadIdx.x;
+    uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
+    uint8_t* fb = a.flags + (int64_t)b * a.fstride;
+    const float* kt = a.kt + (int64_t)b * a.A;
+    int32_t* amb = a.amb + (int64_t)b * a.A;
+    uint64_t* ak = a.ambkey + (int64_t)b * a.A;
+    const float tlo = __uint_as_float(sq[SQ_BLO]), thi = __uint_as_float(sq[SQ_BHI]);
+    const float E = key_band_f32(sq, a.n);
+    // counts of the counting blocks
+    uint32_t nin = 0, nab = 0;
+    for (int64_t i = tid; i < a.nblk; i += RES_THREADS) {
+        const uint32_t* w = a.blk + ((int64_t)b * a.nblk + i) * BLK_WORDS;
+        nin += w[BW_IN];
+        nab += w[BW_ABOVE];
+    }
+    nin = block_sum<RES_THREADS>(nin, s_w);
+    nab = block_sum<RES_THREADS>(nab, s_w);
+    // fine histogram of the candidates inside [t_lo, t_hi]
+    uint32_t* s_h = reinterpret_cast<uint32_t*>(lds);
+    for (int i = tid; i < HIST_BINS; i += RES_THREADS) s_h[i] = 0u;
+    if (tid == 0) {
+        s_namb = 0u;
+        s_nin2 = 0u;
+        s_bin = -1;
+        s_theta = f64_to_ord(-INFINITY);
+    }
+    __syncthreads();
+    const float sc0 = bin_scale(tlo, thi);
+    uint32_t nmid = 0;
+    {
+        const int lane = tid & 63, wave = tid >> 6;
+        for (int64_t i = wave; i < a.nblk; i += RES_WAVES) {
+            const uint32_t cnt = a.blk[((int64_t)b * a.nblk + i) * BLK_WORDS + BW_CAND];
+            const float* ck = a.candkey + (int64_t)b * a.A + i * CB_KEYS;
+            for (uint32_t j = lane; j < cnt; j += 64) {
+                const float kv = ck[j];
+                if (kv >= tlo && kv <= thi) {
+                    atomicAdd(&s_h[bin_of(kv, tlo, sc0)], 1u);
+                    ++nmid;
+                }
             }
         }
     }
+    nmid = block_sum<RES_THREADS>(nmid, s_w);
+    const int64_t need = a.k - (int64_t)nab;
+    const bool ok = need >= 1 && need <= (int64_t)nmid;
+    float lo = tlo, hi = thi, sc = sc0;
+    if (!ok) {
+        // the sample missed: histogram the whole key range here
+        lo = ord_to_key(sq[SQ_KMIN]);
+        hi = ord_to_key(sq[SQ_KMAX]);
+        sc = bin_scale(lo, hi);
+        for (int i = tid; i < HIST_BINS; i += RES_THREADS) s_h[i] = 0u;
+        __syncthreads();
+        for (int64_t u = tid; u < a.A; u += RES_THREADS) atomicAdd(&s_h[bin_of(kt[u], lo, sc)], 1u);
+        __syncthreads();
+    }
+    const uint32_t target = (uint32_t)(ok ? need : a.k);
+    const int d = find_rank_bin<HIST_BINS, RES_THREADS>(s_h, target, s_w);
+    if (d >= 0) s_bin = d;
+    __syncthreads();
+    const int db = s_bin < 0 ? 0 : s_bin;
+    const float HI = band_hi(ru_f32(edge_hi_of(db, lo, hi, sc)), E);
+    const float LO = band_lo(rd_f32(edge_lo_of(db, lo, sc)), E);
+    // classification: selected (w > HI), excluded (v < LO), undecided
+    auto classify = [&](float kv) -> uint8_t { return (band_lo(kv, E) > HI) ? 1 : ((band_hi(kv, E) < LO) ? 0 : 2); };
+    uint32_t nin2 = 0;
+    if (ok) {
+        walk_regions(a, b, true, &s_namb, amb, [&](int32_t u, float kv) {
+            const uint8_t f = classify(kv);
+            fb[u] = f;
+            nin2 += (f == 1);
+            return f == 2;
+        });
+    } else {
+        // every row again: the counting pass's early classification used the missed bracket
+        const int lane = tid & 63;
+        for (int64_t u0 = (int64_t)(tid >> 6) * 64; u0 < a.A; u0 += RES_THREADS) {
+            const int64_t u = u0 + lane;
+            const bool live = u < a.A;
+            const uint8_t f = live ? classify(kt[u]) : 0;
+            if (live) fb[u] = f;
+            nin2 += (f == 1);
+            const bool und = live && f == 2;
+            const uint64_t bal = __ballot(und);
+            if (bal) {
+                const int leader = __ffsll((unsigned long long)bal) - 1;
+                uint32_t base = 0;
+                if (lane == leader) base = atomicAdd(&s_namb, (uint32_t)__popcll(bal));
+                base = __shfl(base, leader);
+                if (und) amb[base + __popcll(bal & ((1ull << lane) - 1ull))] = (int32_t)u;
+            }
+        }
+    }
+    nin2 = block_sum<RES_THREADS>(nin2, s_w);
+    const int64_t namb = s_namb;
+    const int64_t n_in = (ok ? (int64_t)nin : 0) + (int64_t)nin2;
+    const int64_t need2 = a.k - n_in;   // >= 1 and <= namb by the band argument
+    if (tid == 0) {
+        sq[SQ_TLO] = __float_as_uint(LO);
+        sq[SQ_THI] = __float_as_uint(HI);
+        sq[SQ_NAMB] = (uint32_t)namb;
+    }
+    // exact keys of the undecided rows, then their ranking
+    __threadfence_block();
+    __syncthreads();
+    const ExLds L = ex_carve(lds, a.H, a.n);
+    exact_keys_block<false>(a, b, namb, amb, ak, L, next_up_f32(2.0f * E));
+    __threadfence_block();
+    __syncthreads();
+    rank_winners(amb, ak, namb, need2, fb, lds, &s_theta);
+    if (tid == 0) a.theta[b] = ord_to_f64(s_theta);
+    __threadfence_block();
+    __syncthreads();
+    compact_flags(fb, a.A, 1, a.sel + (int64_t)b * a.k, a.k, s_w);
+}
+
+__global__ __launch_bounds__(SEL_THREADS) void fill_u8_kernel(uint8_t* p, int64_t n, uint8_t v) {
+    for (int64_t i = (int64_t)blockIdx.x * SEL_THREADS + threadIdx.x; i < n; i += (int64_t)gridDim.x * SEL_THREADS)
+        p[i] = v;
+}
+
+__global__ __launch_bounds__(64) void theta_empty_kernel(double* theta, int B) {
+    for (int b = threadIdx.x; b < B; b += 64) theta[b] = -INFINITY;
 }
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
     hipError_t e;
     if (a.k == 0) {
-        hipLaunchKernelGGL(select_empty_kernel, dim3(a.B), dim3(64), 0, s, a);
+        // nothing selected: theta = -inf, every flag 0
+        hipLaunchKernelGGL(theta_empty_kernel, dim3(1), dim3(64), 0, s, a.theta, a.B);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (a.A == 0) return hipSuccess;
-        hipLaunchKernelGGL(fill_u8_kernel, dim3(256), dim3(SEL_THREADS), 0, s, a.flags, (int64_t)a.B * a.A, (uint8_t)0);
+        hipLaunchKernelGGL(fill_u8_kernel, dim3(256), dim3(SEL_THREADS), 0, s, a.flags, (int64_t)a.B * a.fstride,
+                           (uint8_t)0);
         return hipGetLastError();
     }
-    dim3 cg((unsigned)((a.A + COUNT_KEYS_PER_BLOCK - 1) / COUNT_KEYS_PER_BLOCK), a.B);
-    hipLaunchKernelGGL(count_kernel, cg, dim3(SEL_THREADS), 0, s, a);
+    hipLaunchKernelGGL(sel_bracket_kernel, dim3(a.B), dim3(SEL_THREADS), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(bracket_kernel, dim3(a.B), dim3(SEL_THREADS), 0, s, a);
+    hipLaunchKernelGGL(sel_count_kernel, dim3((unsigned)a.nblk, a.B), dim3(SEL_THREADS), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(classify_kernel, dim3((unsigned)a.nch, a.B), dim3(SEL_THREADS), 0, s, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = run_exact_keys<false>(a, s)) != hipSuccess) return e;
-    hipLaunchKernelGGL(rank_select_kernel, dim3(RANK_BLOCKS, a.B), dim3(SEL_THREADS), 0, s, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    return run_compact(a, a.flags, 1, CC_IN, CC_SELAMB, a.sel, a.k, a.k, nullptr, s);
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&sel_resolve_kernel),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, RES_LDS);
+    hipLaunchKernelGGL(sel_resolve_kernel, dim3(a.B), dim3(RES_THREADS), RES_LDS, s, a);
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------- admit
 
-__global__ __launch_bounds__(SEL_THREADS) void admit_classify_kernel(SelectArgs a) {
-    __shared__ uint32_t s_red[SEL_THREADS / 64];
-    constexpr int PER = CHUNK / SEL_THREADS;
-    const int b = blockIdx.y;
-    const int c = blockIdx.x;
-    const int tid = threadIdx.x;
-    uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
+// Classification of UB~ against theta (rows outside S): admitted (3), not
+// admitted (0) or undecided (4), listed in the block's candidate region.  If
+// the scorer's bound used another certificate multiplier than this call, or
+// none, every row outside S is undecided (its exact bound decides).
+__global__ __launch_bounds__(SEL_THREADS) void adm_classify_kernel(SelectArgs a) {
+    __shared__ uint32_t s_w[SEL_THREADS / 64];
+    const int b = blockIdx.y, tid = threadIdx.x;
+    const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
+    const int64_t ub0 = (int64_t)blockIdx.x * CB_KEYS;
+    const int64_t ue = min(a.A, ub0 + CB_KEYS);
     const double th = a.theta[b];
+    const bool same = sq[SQ_CMULT] == __float_as_uint(a.cert_mult);
     const double E = ub_error_of(sq, a.n) * (1.0 + 0x1p-20);
     const float* ubb = a.ub + (int64_t)b * a.A;
-    const uint8_t* fb = a.flags + (int64_t)b * a.A;
-    uint8_t* f2 = a.flags2 + (int64_t)b * a.A;
-    int32_t* amb = a.amb + (int64_t)b * a.A;
-    const int64_t u0 = (int64_t)c * CHUNK;
-    const int64_t u1 = min(a.A, u0 + CHUNK);
-    float t[PER];
-    uint8_t fin[PER];
+    const uint8_t* fb = a.flags + (int64_t)b * a.fstride;
+    uint8_t* f2 = a.flags2 + (int64_t)b * a.fstride;
+    float t[CB_PER];
+    uint8_t fin[CB_PER];
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        const int64_t u = u0 + tid + (int64_t)j * SEL_THREADS;
-        t[j] = (u < u1) ? ubb[u] : 0.f;
-        fin[j] = (u < u1) ? fb[u] : (uint8_t)1;
+    for (int j = 0; j < CB_PER; ++j) {
+        const int64_t u = ub0 + tid + (int64_t)SEL_THREADS * j;
+        t[j] = (u < ue) ? ubb[u] : 0.f;
+        fin[j] = (u < ue) ? fb[u] : (uint8_t)1;
     }
-    uint32_t nadm = 0;
+    uint32_t nadm = 0, mask = 0;
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        const int64_t u = u0 + tid + (int64_t)j * SEL_THREADS;
-        uint8_t f = 0;
-        if (u < u1) {
+    for (int j = 0; j < CB_PER; ++j) {
+        const int64_t u = ub0 + tid + (int64_t)SEL_THREADS * j;
+        if (u < ue) {
+            uint8_t f = 0;
             if (fin[j] != 1) {
                 if (th == -INFINITY) {
                     f = 3;
+                } else if (!same) {
+                    f = 4;
                 } else {
                     const double tv = (double)t[j];
                     const double band = E + fabs(tv) * 0x1p-50 + fabs(th) * 0x1p-50;
@@ -818,29 +877,49 @@ __global__ __launch_bounds__(SEL_THREADS) void admit_classify_kernel(SelectArgs 
                 }
             }
             f2[u] = f;
+            nadm += (f == 3);
+            mask |= (f == 4) ? (1u << j) : 0u;
         }
-        nadm += (f == 3);
-        wave_append(f == 4, (int32_t)u, &sq[SQ_NAMB2], amb);
     }
-    nadm = block_sum_u32(nadm, s_red);
-    if (tid == 0) a.ccount[((int64_t)b * a.nch + c) * CC_WORDS + CC_ADM] = nadm;
+    const uint32_t namb = region_append(mask, a.cand + (int64_t)b * a.A + ub0, nullptr, t, ub0, s_w);
+    nadm = block_sum<SEL_THREADS>(nadm, s_w);
+    if (tid == 0) {
+        uint32_t* w = a.blk + ((int64_t)b * a.nblk + blockIdx.x) * BLK_WORDS;
+        w[BW_IN] = nadm;
+        w[BW_CAND] = namb;
+    }
 }
 
-// Ambiguous rows of the admission, decided on their exact bound.
-__global__ __launch_bounds__(SEL_THREADS) void admit_decide_kernel(SelectArgs a) {
-    const int b = blockIdx.y;
-    const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
-    const int64_t namb = sq[SQ_NAMB2];
+// One block per sequence: exact bounds of the undecided rows (fp64), the
+// decision UB > theta, then the ordered compaction of the admitted rows.
+__global__ __launch_bounds__(RES_THREADS, 1) void adm_resolve_kernel(SelectArgs a) {
+    extern __shared__ __align__(16) uint8_t lds[];
+    __shared__ uint32_t s_w[RES_WAVES];
+    __shared__ uint32_t s_namb;
+    const int b = blockIdx.x, tid = threadIdx.x;
+    uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
+    uint8_t* f2 = a.flags2 + (int64_t)b * a.fstride;
+    int32_t* amb = a.amb + (int64_t)b * a.A;
+    uint64_t* ak = a.ambkey + (int64_t)b * a.A;
     const double th = a.theta[b];
-    const uint64_t* ak = a.ambkey + (int64_t)b * a.A;
-    const int32_t* amb = a.amb + (int64_t)b * a.A;
-    for (int64_t i = (int64_t)blockIdx.x * SEL_THREADS + threadIdx.x; i < namb; i += (int64_t)gridDim.x * SEL_THREADS) {
-        if (ord_to_f64(ak[i]) > th) {
-            const int32_t u = amb[i];
-            a.flags2[(int64_t)b * a.A + u] = 3;
-            atomicAdd(&a.ccount[((int64_t)b * a.nch + u / CHUNK) * CC_WORDS + CC_ADMAMB], 1u);
-        }
-    }
+    const bool same = sq[SQ_CMULT] == __float_as_uint(a.cert_mult);
+    if (tid == 0) s_namb = 0u;
+    __syncthreads();
+    walk_regions(a, b, false, &s_namb, amb, [](int32_t, float) { return true; });
+    __syncthreads();
+    const int64_t namb = s_namb;
+    if (tid == 0) sq[SQ_NAMB2] = (uint32_t)namb;
+    __threadfence_block();
+    __syncthreads();
+    const ExLds L = ex_carve(lds, a.H, a.n);
+    const float margin = same ? next_up_f32(2.0f * ru_f32(ub_error_of(sq, a.n) * (1.0 + 0x1p-20))) : INFINITY;
+    exact_keys_block<true>(a, b, namb, amb, ak, L, margin);
+    for (int64_t i = tid; i < namb; i += RES_THREADS)
+        if (ord_to_f64(ak[i]) > th) f2[amb[i]] = 3;
+    __threadfence_block();
+    __syncthreads();
+    const int64_t total = compact_flags(f2, a.A, 3, a.adm ? a.adm + (int64_t)b * a.cap : nullptr, a.adm ? a.cap : 0, s_w);
+    if (tid == 0) a.adm_count[b] = (int32_t)total;
 }
 
 __global__ __launch_bounds__(64) void zero_counts_kernel(int32_t* p, int n) {
@@ -853,12 +932,12 @@ hipError_t launch_admit(const SelectArgs& a, hipStream_t s) {
         hipLaunchKernelGGL(zero_counts_kernel, dim3(1), dim3(64), 0, s, a.adm_count, a.B);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL(admit_classify_kernel, dim3((unsigned)a.nch, a.B), dim3(SEL_THREADS), 0, s, a);
+    hipLaunchKernelGGL(adm_classify_kernel, dim3((unsigned)a.nblk, a.B), dim3(SEL_THREADS), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = run_exact_keys<true>(a, s)) != hipSuccess) return e;
-    hipLaunchKernelGGL(admit_decide_kernel, dim3(DECIDE_BLOCKS, a.B), dim3(SEL_THREADS), 0, s, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    return run_compact(a, a.flags2, 3, CC_ADM, CC_ADMAMB, a.adm, a.cap, a.cap, a.adm_count, s);
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&adm_resolve_kernel),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, RES_LDS);
+    hipLaunchKernelGGL(adm_resolve_kernel, dim3(a.B), dim3(RES_THREADS), RES_LDS, s, a);
+    return hipGetLastError();
 }
 
 }  // namespace vkv

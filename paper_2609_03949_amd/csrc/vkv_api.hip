@@ -103,22 +103,27 @@ static void attend_split(const vkv_step* st, int64_t k, int64_t cap, int64_t* sp
     *splits = std::max<int64_t>(1, (nmax + rows - 1) / rows);
 }
 
+static int64_t flag_stride(int64_t A) { return (std::max<int64_t>(A, 1) + 63) / 64 * 64; }
+
 static WsLayout layout(const vkv_step* st, int64_t k, int64_t cap) {
     WsLayout L{};
     const int64_t B = st->B, H = st->H;
     L.A = st->T - st->W;
     L.n = index_width(st);
-    L.nch = std::max<int64_t>(1, (L.A + CHUNK - 1) / CHUNK);
+    L.nblk = std::max<int64_t>(1, (L.A + CB_KEYS - 1) / CB_KEYS);
     L.cap = cap;
     const int64_t Aw = std::max<int64_t>(L.A, 1);
+    const int64_t Af = flag_stride(L.A);
     size_t o = 0;
     L.qt = o; o = up256(o + (size_t)(B * H * L.n * 2));
     L.hsc = o; o = up256(o + (size_t)(B * H * 16));
     L.seq = o; o = up256(o + (size_t)(B * SQ_WORDS * 4));
     L.kt = o; o = up256(o + (size_t)(B * Aw * 4));
-    L.flags = o; o = up256(o + (size_t)(B * Aw));
-    L.flags2 = o; o = up256(o + (size_t)(B * Aw));
-    L.ccount = o; o = up256(o + (size_t)(B * L.nch * CC_WORDS * 4));
+    L.flags = o; o = up256(o + (size_t)(B * Af));
+    L.flags2 = o; o = up256(o + (size_t)(B * Af));
+    L.blk = o; o = up256(o + (size_t)(B * L.nblk * BLK_WORDS * 4));
+    L.cand = o; o = up256(o + (size_t)(B * Aw * 4));
+    L.candkey = o; o = up256(o + (size_t)(B * Aw * 4));
     L.amb = o; o = up256(o + (size_t)(B * Aw * 4));
     L.ambkey = o; o = up256(o + (size_t)(B * Aw * 8));
     // everything above is independent of k and cap; the attention partials last
@@ -159,14 +164,14 @@ struct Chunk {
 
 // bytes per sequence of each workspace array (the leading-dimension strides of layout())
 struct WsStrides {
-    size_t qt, hsc, seq, kt, flags, ccount, amb, ambkey, part_o, part_ml;
+    size_t qt, hsc, seq, kt, flags, blk, cand, amb, ambkey, part_o, part_ml;
 };
 
 static WsStrides ws_strides(const vkv_step* st, const WsLayout& L) {
     const int64_t H = st->H, Aw = std::max<int64_t>(L.A, 1);
     return WsStrides{(size_t)(H * L.n * 2), (size_t)(H * 16),
-                     (size_t)(SQ_WORDS * 4), (size_t)(Aw * 4), (size_t)Aw,
-                     (size_t)(L.nch * CC_WORDS * 4), (size_t)(Aw * 4), (size_t)(Aw * 8),
+                     (size_t)(SQ_WORDS * 4), (size_t)(Aw * 4), (size_t)flag_stride(L.A),
+                     (size_t)(L.nblk * BLK_WORDS * 4), (size_t)(Aw * 4), (size_t)(Aw * 4), (size_t)(Aw * 8),
                      (size_t)(L.splits * ((H + ATT_HEADS - 1) / ATT_HEADS) * ATT_HEADS * D_LAT * 2),
                      (size_t)(L.splits * H * 2 * 4)};
 }
@@ -179,7 +184,8 @@ static QprepArgs qprep_args(const vkv_step* st, const WsLayout& L, char* w, Chun
                      reinterpret_cast<float*>(w + L.hsc + b0 * z.hsc), reinterpret_cast<uint32_t*>(w + L.seq + b0 * z.seq)};
 }
 
-static ScoreArgs score_args(const vkv_step* st, const WsLayout& L, char* w, Chunk c, float* key, float* ub) {
+static ScoreArgs score_args(const vkv_step* st, const WsLayout& L, char* w, Chunk c, float* key, float* ub,
+                            float cert_mult) {
     const WsStrides z = ws_strides(st, L);
     const int64_t b0 = c.b0;
     ScoreArgs a{};
@@ -199,6 +205,7 @@ static ScoreArgs score_args(const vkv_step* st, const WsLayout& L, char* w, Chun
     a.B = (int)c.nb;
     a.H = (int)st->H;
     a.n = (int)L.n;
+    a.cert_mult = cert_mult;
     return a;
 }
 
@@ -218,14 +225,18 @@ static SelectArgs select_args(const vkv_step* st, const WsLayout& L, char* w, Ch
     a.kt = reinterpret_cast<const float*>(w + L.kt + b0 * z.kt);
     a.flags = reinterpret_cast<uint8_t*>(w + L.flags + b0 * z.flags);
     a.flags2 = reinterpret_cast<uint8_t*>(w + L.flags2 + b0 * z.flags);
-    a.ccount = reinterpret_cast<uint32_t*>(w + L.ccount + b0 * z.ccount);
+    a.blk = reinterpret_cast<uint32_t*>(w + L.blk + b0 * z.blk);
+    a.cand = reinterpret_cast<int32_t*>(w + L.cand + b0 * z.cand);
+    a.candkey = reinterpret_cast<float*>(w + L.candkey + b0 * z.cand);
     a.amb = reinterpret_cast<int32_t*>(w + L.amb + b0 * z.amb);
     a.ambkey = reinterpret_cast<uint64_t*>(w + L.ambkey + b0 * z.ambkey);
     a.A = L.A;
-    a.nch = L.nch;
+    a.nblk = L.nblk;
+    a.fstride = (int64_t)z.flags;
     a.B = (int)c.nb;
     a.H = (int)st->H;
     a.n = (int)L.n;
+    a.cert_mult = 1.0f;
     return a;
 }
 
@@ -427,9 +438,16 @@ static int check_prep(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_byte
     return check_ws(ctx, ws, ws_bytes, layout(st, 0, 0).part_o);
 }
 
-static int check_score(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, float* ub) {
+static int check_cert_mult(vkv_ctx* ctx, float cert_mult) {
+    if (!(cert_mult >= 0.f) || !(cert_mult < 1e30f))
+        return fail(ctx, VKV_E_ARG, "cert_mult must be finite and >= 0 (1 = the sound bound)");
+    return VKV_OK;
+}
+
+static int check_score(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, float* ub, float cert_mult) {
     int rc = check_prep(ctx, st, ws, ws_bytes);
     if (rc) return rc;
+    if (ub && (rc = check_cert_mult(ctx, cert_mult))) return rc;
     if (ub && (!st->eta || !st->eps || !st->gam)) return fail(ctx, VKV_E_ARG, "ub needs eta, eps and gam");
     if (ub && st->mode == VKV_MODE_DIGEST) return fail(ctx, VKV_E_UNSUPPORTED, "the bound needs the branch summand in the key");
     return VKV_OK;
@@ -446,9 +464,11 @@ static int check_select(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_by
 }
 
 static int check_admit(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, const int32_t* sel,
-                       const double* theta, const float* ub, int32_t* adm, int32_t* adm_count, int64_t cap) {
+                       const double* theta, const float* ub, float cert_mult, int32_t* adm, int32_t* adm_count,
+                       int64_t cap) {
     int rc = check_prep(ctx, st, ws, ws_bytes);
     if (rc) return rc;
+    if ((rc = check_cert_mult(ctx, cert_mult))) return rc;
     const int64_t A = st->T - st->W;
     if (st->mode == VKV_MODE_DIGEST) return fail(ctx, VKV_E_UNSUPPORTED, "admission needs the branch summand in the key");
     if (!st->eta || !st->eps || !st->gam) return fail(ctx, VKV_E_ARG, "admission needs eta, eps and gam");
@@ -478,8 +498,9 @@ static hipError_t run_prep(const vkv_step* st, char* w, Chunk c, hipStream_t s) 
     return launch_qprep(qprep_args(st, layout(st, 0, 0), w, c), s);
 }
 
-static hipError_t run_score(const vkv_step* st, char* w, Chunk c, float* key, float* ub, hipStream_t s) {
-    return launch_score(score_args(st, layout(st, 0, 0), w, c, key, ub), s);
+static hipError_t run_score(const vkv_step* st, char* w, Chunk c, float* key, float* ub, float cert_mult,
+                            hipStream_t s) {
+    return launch_score(score_args(st, layout(st, 0, 0), w, c, key, ub, cert_mult), s);
 }
 
 static hipError_t run_select(const vkv_step* st, char* w, Chunk c, int64_t k, int32_t* sel, double* theta,
@@ -492,9 +513,11 @@ static hipError_t run_select(const vkv_step* st, char* w, Chunk c, int64_t k, in
 }
 
 static hipError_t run_admit(const vkv_step* st, char* w, Chunk c, int64_t k, const int32_t* sel, const double* theta,
-                            const float* ub, int32_t* adm, int32_t* adm_count, int64_t cap, hipStream_t s) {
+                            const float* ub, float cert_mult, int32_t* adm, int32_t* adm_count, int64_t cap,
+                            hipStream_t s) {
     const WsLayout L = layout(st, 0, 0);
     SelectArgs a = select_args(st, L, w, c);
+    a.cert_mult = cert_mult;
     a.ub = ub ? ub + c.b0 * L.A : nullptr;
     a.sel = sel ? const_cast<int32_t*>(sel) + c.b0 * k : nullptr;
     a.theta = const_cast<double*>(theta) + c.b0;
@@ -541,11 +564,12 @@ int vkv_query_prep(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, 
     return VKV_OK;
 }
 
-int vkv_score(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, float* key, float* ub, void* stream) {
+int vkv_score(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, float* key, float* ub, float cert_mult,
+              void* stream) {
     if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
-    int rc = check_score(ctx, st, ws, ws_bytes, ub);
+    int rc = check_score(ctx, st, ws, ws_bytes, ub, cert_mult);
     if (rc) return rc;
-    HIP_TRY(ctx, run_score(st, (char*)ws, Chunk{0, st->B}, key, ub, (hipStream_t)stream));
+    HIP_TRY(ctx, run_score(st, (char*)ws, Chunk{0, st->B}, key, ub, cert_mult, (hipStream_t)stream));
     return VKV_OK;
 }
 
@@ -560,12 +584,13 @@ int vkv_select(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int6
 }
 
 int vkv_admit(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, const int32_t* sel,
-              const double* theta, const float* ub, int32_t* adm, int32_t* adm_count, int64_t cap, void* stream) {
+              const double* theta, const float* ub, float cert_mult, int32_t* adm, int32_t* adm_count, int64_t cap,
+              void* stream) {
     if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
-    int rc = check_admit(ctx, st, ws, ws_bytes, k, sel, theta, ub, adm, adm_count, cap);
+    int rc = check_admit(ctx, st, ws, ws_bytes, k, sel, theta, ub, cert_mult, adm, adm_count, cap);
     if (rc) return rc;
     hipStream_t s = (hipStream_t)stream;
-    HIP_TRY(ctx, run_admit(st, (char*)ws, Chunk{0, st->B}, k, sel, theta, ub, adm, adm_count, cap, s));
+    HIP_TRY(ctx, run_admit(st, (char*)ws, Chunk{0, st->B}, k, sel, theta, ub, cert_mult, adm, adm_count, cap, s));
     return debug_check_adm(ctx, st, k, sel, adm, adm_count, cap, s);
 }
 
@@ -604,15 +629,16 @@ int vkv_score_timing(vkv_ctx* ctx, float* ms, int max) {
 }
 
 int vkv_step_run(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, float* key, float* ub,
-                 int32_t* sel, double* theta, int32_t* adm, int32_t* adm_count, int64_t cap, float scale, uint16_t* out,
-                 float* lse, void* stream) {
+                 int32_t* sel, double* theta, int32_t* adm, int32_t* adm_count, int64_t cap, float cert_mult,
+                 float scale, uint16_t* out, float* lse, void* stream) {
     if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
     const bool two_tier = adm_count != nullptr;
     float* ubp = two_tier ? ub : nullptr;
     int rc;
-    if ((rc = check_score(ctx, st, ws, ws_bytes, ubp))) return rc;
+    if ((rc = check_score(ctx, st, ws, ws_bytes, ubp, cert_mult))) return rc;
     if ((rc = check_select(ctx, st, ws, ws_bytes, k, sel, theta))) return rc;
-    if (two_tier && (rc = check_admit(ctx, st, ws, ws_bytes, k, sel, theta, ub, adm, adm_count, cap))) return rc;
+    if (two_tier && (rc = check_admit(ctx, st, ws, ws_bytes, k, sel, theta, ub, cert_mult, adm, adm_count, cap)))
+        return rc;
     const int64_t acap = two_tier ? cap : 0;
     if ((rc = check_attend(ctx, st, ws, ws_bytes, k, sel, two_tier ? adm : nullptr, two_tier ? adm_count : nullptr,
                            acap, scale, out, lse)))
@@ -623,15 +649,33 @@ int vkv_step_run(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, in
     HIP_TRY(ctx, run_prep(st, w, all, s));
     const bool timed = ctx->timing && ctx->tcount < TIMING_SLOTS;
     if (timed) HIP_TRY(ctx, hipEventRecord(ctx->tev[2 * ctx->tcount], s));
-    HIP_TRY(ctx, run_score(st, w, all, key, ubp, s));
+    HIP_TRY(ctx, run_score(st, w, all, key, ubp, cert_mult, s));
     if (timed) HIP_TRY(ctx, hipEventRecord(ctx->tev[2 * ctx->tcount++ + 1], s));
     HIP_TRY(ctx, run_select(st, w, all, k, sel, theta, s));
-    if (two_tier) HIP_TRY(ctx, run_admit(st, w, all, k, sel, theta, ub, adm, adm_count, cap, s));
+    if (two_tier) HIP_TRY(ctx, run_admit(st, w, all, k, sel, theta, ub, cert_mult, adm, adm_count, cap, s));
     HIP_TRY(ctx, run_attend(st, w, all, k, sel, two_tier ? adm : nullptr, two_tier ? adm_count : nullptr, acap,
                             scale, out, lse, s));
     if ((rc = debug_check_sel(ctx, st, k, sel, s))) return rc;
     if (two_tier) return debug_check_adm(ctx, st, k, sel, adm, adm_count, cap, s);
     return VKV_OK;
+}
+
+int vkv_check_rows(vkv_ctx* ctx, const vkv_step* st, int64_t k, const int32_t* sel, const int32_t* adm,
+                   const int32_t* adm_count, int64_t cap, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    int rc = check_step(ctx, st);
+    if (rc) return rc;
+    const int64_t A = st->T - st->W;
+    if (k < 0 || k > A) return fail(ctx, VKV_E_ARG, "k=%lld outside [0, A]", (long long)k);
+    if (cap < 0 || cap > A) return fail(ctx, VKV_E_ARG, "cap=%lld outside [0, A]", (long long)cap);
+    if ((k > 0 && !sel) || (cap > 0 && !adm)) return fail(ctx, VKV_E_ARG, "sel and adm are required");
+    hipStream_t s = (hipStream_t)stream;
+    const int saved = ctx->debug_rows;
+    ctx->debug_rows = 1;
+    rc = debug_check_sel(ctx, st, k, sel, s);
+    if (!rc && adm_count) rc = debug_check_adm(ctx, st, k, sel, adm, adm_count, cap, s);
+    ctx->debug_rows = saved;
+    return rc;
 }
 
 }  // extern "C"

@@ -115,38 +115,42 @@ __host__ __device__ __forceinline__ float ord_to_key(uint32_t o) {
 
 // ----------------------------------------------------------- workspace
 
-// Per-sequence state words (uint32 each), kept in the workspace.
+// Per-sequence state words (uint32 each), kept in the workspace.  Words 0-7
+// are the scorer's (cleared by the query prep of the step); the others are
+// written, never accumulated, by the selection and admission calls, so those
+// calls may be repeated on the same workspace.
 enum SeqWord : int {
     SQ_QMAX = 0,    // float bits: max_h ||qt_h|| (upper bound)
     SQ_NU2MAX = 1,  // float bits: max_u ||x_u||^2 (fp32 sum)
     SQ_BMAX = 2,    // float bits: max_u (amax eta + nmax eps + emax gam)
-    SQ_AMAX = 3,    // float bits: max_h a_h, n_h, e_h (written by the scorer launch)
+    SQ_AMAX = 3,    // float bits: max_h a'_h, n_h, e_h (written by the scorer launch)
     SQ_NMAX = 4,
     SQ_EMAX = 5,
     SQ_KMIN = 6,    // ordered encoding of min_u key~_u   (scorer, atomicMin)
     SQ_KMAX = 7,    // ordered encoding of max_u key~_u   (scorer, atomicMax)
-    SQ_TLO = 8,     // float bits: LO <= k-th largest of (key~ - E)
-    SQ_THI = 9,     // float bits: HI >= k-th largest of (key~ + E)
-    SQ_NBR = 10,    // keys~ inside the sampled bracket (listed by the counting pass)
-    SQ_NAMB = 12,   // ambiguous rows of the selection
-    SQ_NAMB2 = 13,  // ambiguous rows of the admission
-    SQ_BLO = 14,    // float bits: lower end of the sampled bracket of the k-th key~
-    SQ_BHI = 15,    // float bits: upper end of the sampled bracket
-    SQ_ABOVE = 16,  // keys~ above the sampled bracket
+    SQ_BLO = 8,     // float bits: lower end of the sampled bracket of the k-th key~
+    SQ_BHI = 9,     // float bits: upper end of the sampled bracket
+    SQ_CLO = 10,    // float bits: rows with key~ + E below this are certainly not selected
+    SQ_CHI = 11,    // float bits: rows with key~ - E above this are certainly selected
+    SQ_CMULT = 12,  // float bits: the certificate multiplier the scorer's bound used
+    SQ_TLO = 13,    // float bits: LO <= k-th largest of (key~ - E)   (diagnostic)
+    SQ_THI = 14,    // float bits: HI >= k-th largest of (key~ + E)   (diagnostic)
+    SQ_NAMB = 15,   // ambiguous rows of the selection                (diagnostic)
+    SQ_NAMB2 = 16,  // ambiguous rows of the admission                (diagnostic)
     SQ_WORDS = 32
 };
 
-constexpr int CHUNK = 2048;        // rows per classify / compaction block
-constexpr int CC_WORDS = 4;        // per-chunk counters
-enum ChunkWord : int { CC_IN = 0, CC_SELAMB = 1, CC_ADM = 2, CC_ADMAMB = 3 };
+constexpr int CB_KEYS = 4096;      // archive rows per counting / classification block
+constexpr int BLK_WORDS = 4;       // per counting block: the counts below
+enum BlockWord : int { BW_IN = 0, BW_CAND = 1, BW_ABOVE = 2 };   // (admission: BW_IN = admitted, BW_CAND = ambiguous)
 constexpr int HIST_BINS = 4096;
 constexpr int ATT_CHUNK = 32;      // rows per attention tile
 constexpr int ATT_HEADS = 128;     // heads per attention workgroup (8 waves x 16)
 constexpr int ATT_MAX_SPLIT_ROWS = 1024;   // rows of one split (row list held in LDS)
 
 struct WsLayout {
-    size_t qt, hsc, seq, kt, flags, flags2, ccount, amb, ambkey, part_o, part_ml, total;
-    int64_t A, n, nch, splits, rows_per_split, cap;
+    size_t qt, hsc, seq, kt, flags, flags2, blk, cand, candkey, amb, ambkey, part_o, part_ml, total;
+    int64_t A, n, nblk, splits, rows_per_split, cap;
 };
 
 // ------------------------------------------------------ kernel interfaces
@@ -176,6 +180,7 @@ struct ScoreArgs {
     uint32_t* seq;
     int64_t A;
     int B, H, n;
+    float cert_mult;       // (UB) multiplier of the sketch-residual term a_h eta_u
 };
 
 struct DigestArgs {
@@ -203,17 +208,21 @@ struct SelectArgs {
     const float* gam;
     int64_t T;
     uint32_t* seq;
-    uint8_t* flags;        // [B,A]
-    uint8_t* flags2;       // [B,A]
-    uint32_t* ccount;      // [B,nch,CC_WORDS]
-    int32_t* amb;          // [B,A] keys~ inside the sampled bracket (as float bits), then the ambiguous rows
+    uint8_t* flags;        // [B,A] selection: 1 selected, 0 not, 2 undecided
+    uint8_t* flags2;       // [B,A] admission: 3 admitted, 0 not, 4 undecided
+    uint32_t* blk;         // [B,nblk,BLK_WORDS] per counting block
+    int32_t* cand;         // [B,A] per counting block region: its candidate rows
+    float* candkey;        // [B,A] their keys~ (selection)
+    int32_t* amb;          // [B,A] the undecided rows, compacted
     uint64_t* ambkey;      // [B,A] their exact keys (order-preserving encoding of fp64)
     int32_t* sel;          // [B,k]
     double* theta;         // [B]
     int32_t* adm;          // [B,cap]
     int32_t* adm_count;    // [B]
-    int64_t A, k, cap, nch;
+    int64_t A, k, cap, nblk;
+    int64_t fstride;       // bytes per sequence of flags / flags2 (A rounded up to 64)
     int B, H, n;
+    float cert_mult;       // admission: multiplier of the sketch-residual term
 };
 
 struct AttendArgs {

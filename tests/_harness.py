@@ -9,6 +9,8 @@ import oracle
 import paper_2609_03949_amd as vkv
 from paper_2609_03949_amd import synth
 
+from _checks import rel_l2  # noqa: F401  (re-exported for the tests)
+
 
 def index_cols(mode: int, r: int) -> tuple[int, bool]:
     """(columns, has_rope) of the packed index used for a mode."""
@@ -38,7 +40,7 @@ def gpu_index(ctx, wl, two_tier: bool):
     return index, has_rope, eta, eps, gam
 
 
-def gpu_step(ctx, wl, k=None, two_tier=False, cap=None, index_pack=None):
+def gpu_step(ctx, wl, k=None, two_tier=False, cap=None, index_pack=None, cert_mult=1.0):
     """One full step through vkv_step_run.  Returns (host results, device bufs)."""
     k = wl["k"] if k is None else k
     if index_pack is None:
@@ -47,7 +49,7 @@ def gpu_step(ctx, wl, k=None, two_tier=False, cap=None, index_pack=None):
     step = vkv.Step(wl["cache"], wl["q_lat"], wl["q_rope"], wl["W"], wl["mode"],
                     wl["r"] if wl["mode"] != synth.MODE_ROPE else 0, index=index,
                     index_has_rope=has_rope, P=wl["P"], eta=eta, eps=eps, gam=gam)
-    bufs = vkv.Buffers(step, k, two_tier=two_tier, cap=cap)
+    bufs = vkv.Buffers(step, k, two_tier=two_tier, cap=cap, cert_mult=cert_mult)
     bufs.run(ctx, step, wl["scale"])
     torch.cuda.synchronize()
     res = {
@@ -76,7 +78,7 @@ def host_inputs(wl, seqs):
     return cache, q_lat, q_rope, P
 
 
-def oracle_step(wl, seqs, k=None, two_tier=False, cap=None, nthreads=0):
+def oracle_step(wl, seqs, k=None, two_tier=False, cap=None, nthreads=0, cert_mult=1.0):
     """The same step on the oracle for the listed sequences (inputs rebuilt
     from the generator's tensors; the index is built by the oracle itself)."""
     k = wl["k"] if k is None else k
@@ -92,7 +94,7 @@ def oracle_step(wl, seqs, k=None, two_tier=False, cap=None, nthreads=0):
             index = None
     res = oracle.step(cache, q_lat, q_rope, index, P, rr, mode, W, k, wl["scale"],
                       two_tier=two_tier, eta=eta, eps=eps, gam=gam, cap=cap,
-                      index_has_rope=has_rope, nthreads=nthreads)
+                      index_has_rope=has_rope, nthreads=nthreads, cert_mult=cert_mult)
     out = {}
     for j, b in enumerate(seqs):
         out[b] = {key: res[key][j] for key in ("sel", "theta", "out", "lse", "key")}
@@ -100,13 +102,6 @@ def oracle_step(wl, seqs, k=None, two_tier=False, cap=None, nthreads=0):
             out[b]["adm"] = res["adm"][j]
             out[b]["adm_count"] = res["adm_count"][j]
     return out, (cache, q_lat, q_rope, P, index, eta, eps, gam)
-
-
-def rel_l2(a: np.ndarray, b: np.ndarray) -> float:
-    """Relative L2 error per row (last axis), max over rows."""
-    num = np.linalg.norm(a - b, axis=-1)
-    den = np.maximum(np.linalg.norm(b, axis=-1), 1e-30)
-    return float(np.max(num / den))
 
 
 def bf16_bits_of(x: np.ndarray) -> np.ndarray:

@@ -100,7 +100,11 @@ def test_rope_mode_rules(lib):
 def test_null_context_is_refused(lib):
     s = _step()
     P = ctypes.c_void_p
-    assert lib.vkv_score(None, ctypes.byref(s), P(1 << 20), 1 << 20, P(1 << 20), None, None) == -1
+    assert lib.vkv_score(None, ctypes.byref(s), P(1 << 20), 1 << 20, P(1 << 20), None,
+                         ctypes.c_float(1.0), None) == -1
+    assert lib.vkv_admit(None, ctypes.byref(s), None, 0, 1, None, None, None, ctypes.c_float(1.0),
+                         None, None, 0, None) == -1
+    assert lib.vkv_check_rows(None, ctypes.byref(s), 1, None, None, None, 0, None) == -1
     assert lib.vkv_select(None, ctypes.byref(s), None, 0, 1, None, None, None) == -1
     assert lib.vkv_attend(None, ctypes.byref(s), None, 0, 1, None, None, None, 0, ctypes.c_float(0.1),
                           None, None, None) == -1

@@ -16,12 +16,13 @@ import oracle
 import paper_2609_03949_amd as vkv
 from paper_2609_03949_amd import synth
 
+import _checks
 from _harness import gpu_index, gpu_step, host_inputs, index_cols, oracle_step, rel_l2
 
 pytestmark = pytest.mark.gpu
 
-OUT_TOL = 2e-2
-LSE_TOL = 1e-3
+OUT_TOL = _checks.OUT_TOL
+LSE_TOL = _checks.LSE_TOL
 
 
 def say(msg):
@@ -38,22 +39,8 @@ def ctx():
     c.close()
 
 
-def check_step(wl, g, o, seqs, two_tier=False, exact_out=False):
-    for j, b in enumerate(seqs):
-        ob = o[b]
-        assert np.array_equal(g["sel"][b], ob["sel"]), f"sel differs for sequence {b}"
-        if len(ob["sel"]):
-            assert g["theta"][b] == ob["theta"], (b, g["theta"][b], ob["theta"])
-        if two_tier:
-            assert int(g["adm_count"][b]) == ob["adm_count"], (b, g["adm_count"][b], ob["adm_count"])
-            m = min(ob["adm_count"], g["adm"].shape[1])
-            assert np.array_equal(g["adm"][b, :m], ob["adm"][:m]), f"admitted set differs for {b}"
-        err = rel_l2(g["out"][b], ob["out"])
-        assert err < OUT_TOL, (b, err)
-        fin = np.isfinite(ob["lse"])
-        assert np.array_equal(fin, np.isfinite(g["lse"][b]))
-        assert np.all(np.abs(g["lse"][b][fin] - ob["lse"][fin]) < LSE_TOL)
-    return True
+def check_step(wl, g, o, seqs, two_tier=False):
+    return _checks.check_step(g, o, seqs, two_tier)
 
 
 # ------------------------------------------------------------ index build
@@ -705,21 +692,141 @@ FULL = ["cfg0", "cfg1", "cfg2_r64", "cfg2_r128", "cfg2_r192", "cfg2_r256", "cfg3
 
 
 @pytest.mark.parametrize("name", FULL)
-def test_full_config_sampled(ctx, name):
-    """Each config at its full size, in the bench's launch configuration,
-    checked on the first and last sequence (the oracle computes those whole)."""
+def test_full_config_every_sequence(ctx, name):
+    """Each config at its full size, in the bench's launch configuration: the
+    selected (and admitted) sets, theta, outputs and lse of every sequence
+    against the oracle, which computes each sequence whole."""
     cfg = synth.CONFIGS[name]
     say(f"full-size {synth.describe(cfg)}")
     wl = synth.make_workload(cfg, "cuda")
     g, _ = gpu_step(ctx, wl, two_tier=cfg.two_tier)
-    seqs = sorted({0, wl["B"] - 1})
-    o, _ = oracle_step(wl, seqs, two_tier=cfg.two_tier, nthreads=0)
-    check_step(wl, g, o, seqs, two_tier=cfg.two_tier)
+    seqs = list(range(wl["B"]))
+    for s0 in range(0, len(seqs), 8):
+        part = seqs[s0:s0 + 8]
+        o, _ = oracle_step(wl, part, two_tier=cfg.two_tier, nthreads=0)
+        check_step(wl, g, o, part, two_tier=cfg.two_tier)
+        say(f"  sequences {part[0]}..{part[-1]} match")
     if cfg.two_tier:
-        frac = [g["adm_count"][b] / (wl["A"] - wl["k"]) for b in seqs]
+        frac = [round(float(g["adm_count"][b] / (wl["A"] - wl["k"])), 4) for b in seqs]
         say(f"admitted fraction of non-selected archive rows: {frac}")
     needles = [len(np.intersect1d(g["sel"][b], wl["needles"][b].numpy())) / max(1, len(wl["needles"][b]))
                for b in seqs]
-    say(f"needle recall of S (context only): {needles}")
+    say(f"needle recall of S (context only): min {min(needles):.3f} mean {np.mean(needles):.3f}")
     del wl
     torch.cuda.empty_cache()
+
+
+# ------------------------------------------------- boundary contracts
+
+def test_stage_calls_are_idempotent(ctx):
+    """One vkv_query_prep + vkv_score, then vkv_select at k1, k2, k1 and
+    vkv_admit twice on the same workspace: every call's result equals the
+    oracle's, so nothing a call leaves in the workspace leaks into the next."""
+    say("idempotent stage calls")
+    cfg = synth.CONFIGS["cfg3"].with_(H=32)
+    B, T = 3, 20000
+    wl = synth.make_workload(cfg, "cuda", B=B, T=T)
+    index, has_rope, eta, eps, gam = gpu_index(ctx, wl, True)
+    step = vkv.Step(wl["cache"], wl["q_lat"], wl["q_rope"], wl["W"], wl["mode"], wl["r"], index=index,
+                    index_has_rope=has_rope, P=wl["P"], eta=eta, eps=eps, gam=gam)
+    A = wl["A"]
+    k1, k2 = 600, 37
+    ws = vkv.alloc_workspace(step, k1, A)
+    key = torch.empty(B, A, dtype=torch.float32, device="cuda")
+    ub = torch.empty_like(key)
+    vkv.query_prep(ctx, step, ws)
+    vkv.score(ctx, step, ws, key, ub)
+    cache, q_lat, q_rope, P = host_inputs(wl, range(B))
+    oidx, oeta, oeps, ogam = oracle.digest_build(cache, P, cfg.r, with_rope=True)
+    qt, a, nq, e = oracle.query_prep(q_lat, q_rope, P, cfg.r, cfg.mode)
+    xs = [oracle.index_rows(cache[b], oidx[b], cfg.mode, cfg.r, True) for b in range(B)]
+    okeys = [oracle.index_keys(qt[b], xs[b], A)[0] for b in range(B)]
+    oubs = [oracle.upper_bounds(qt[b], a[b], nq[b], e[b], xs[b], oeta[b], oeps[b], ogam[b], A)
+            for b in range(B)]
+    sels = {}
+    for k in (k1, k2, k1):
+        sel = torch.full((B, k), -5, dtype=torch.int32, device="cuda")
+        theta = torch.empty(B, dtype=torch.float64, device="cuda")
+        vkv.select(ctx, step, ws, k, sel, theta)
+        torch.cuda.synchronize()
+        for b in range(B):
+            osel, oth = oracle.select(okeys[b], k)
+            assert np.array_equal(sel[b].cpu().numpy(), osel), (k, b)
+            assert theta[b].item() == oth, (k, b)
+        sels[k] = (sel, theta)
+        say(f"  select k={k} matches")
+    sel, theta = sels[k1]
+    for rep in range(2):
+        adm = torch.full((B, A), -5, dtype=torch.int32, device="cuda")
+        cnt = torch.full((B,), -5, dtype=torch.int32, device="cuda")
+        vkv.admit(ctx, step, ws, k1, sel, theta, ub, adm, cnt, A)
+        torch.cuda.synchronize()
+        for b in range(B):
+            oadm, ocnt = oracle.admit(oubs[b], sel[b].cpu().numpy(), theta[b].item())
+            assert int(cnt[b]) == ocnt, (rep, b, int(cnt[b]), ocnt)
+            assert np.array_equal(adm[b, :ocnt].cpu().numpy(), oadm), (rep, b)
+        say(f"  admit call {rep} matches")
+
+
+@pytest.mark.parametrize("cm", [0.25, 0.05, 0.0])
+def test_certificate_multiplier_admission(ctx, cm):
+    """Eq. (trigger)'s z / sqrt(d_c - r) below 1 (a calibrated trigger): the
+    admitted sets stay bit-exact against the oracle at the same multiplier, and
+    shrink with it."""
+    say(f"cert_mult {cm}")
+    cfg = synth.CONFIGS["cfg3"].with_(H=64)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=12000)
+    g, _ = gpu_step(ctx, wl, k=375, two_tier=True, cert_mult=cm)
+    o, _ = oracle_step(wl, [0, 1], k=375, two_tier=True, cert_mult=cm)
+    check_step(wl, g, o, [0, 1], two_tier=True)
+    say(f"  admitted per sequence: {[int(c) for c in g['adm_count']]} of {wl['A'] - 375}")
+
+
+def test_admit_with_another_multiplier_than_the_scan(ctx):
+    """vkv_score formed UB~ with cert_mult 1, vkv_admit asks for 0.2: the band
+    shortcut is skipped and every row outside S is decided on its exact bound,
+    so the admitted set is the oracle's at 0.2."""
+    say("admit multiplier differs from the scan's")
+    cfg = synth.CONFIGS["cfg3"].with_(H=16)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=6000)
+    g, (step, bufs, _) = gpu_step(ctx, wl, k=180, two_tier=True, cert_mult=1.0)
+    vkv.admit(ctx, step, bufs.ws, 180, bufs.sel, bufs.theta, bufs.ub, bufs.adm, bufs.adm_count,
+              bufs.cap, None, 0.2)
+    torch.cuda.synchronize()
+    o, _ = oracle_step(wl, [0, 1], k=180, two_tier=True, cert_mult=0.2)
+    for b in range(2):
+        cnt = int(bufs.adm_count[b])
+        assert cnt == o[b]["adm_count"], (b, cnt, o[b]["adm_count"])
+        assert np.array_equal(bufs.adm[b, :cnt].cpu().numpy(), o[b]["adm"])
+
+
+def test_row_set_checker_fires_on_broken_lists(ctx):
+    """The executable row-set invariant (vkv_check_rows, the check
+    VKV_DEBUG_ROWS runs inside the calls) accepts a real step's lists and
+    refuses each broken form: unsorted, duplicated or out-of-archive selected
+    rows, an admitted row that is also selected, unsorted admitted rows and an
+    impossible count."""
+    say("row-set checker, known-bad lists")
+    cfg = synth.CONFIGS["cfg3"].with_(H=8)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=3000)
+    k = 64
+    g, (step, bufs, _) = gpu_step(ctx, wl, k=k, two_tier=True)
+    vkv.check_rows(ctx, step, k, bufs.sel, bufs.adm, bufs.adm_count, bufs.cap)
+    A = wl["A"]
+
+    def refused(sel=None, adm=None, cnt=None):
+        s = bufs.sel.clone() if sel is None else sel
+        a = bufs.adm.clone() if adm is None else adm
+        c = bufs.adm_count.clone() if cnt is None else cnt
+        with pytest.raises(vkv.VkvError) as ei:
+            vkv.check_rows(ctx, step, k, s, a, c, bufs.cap)
+        assert ei.value.code == -8, ei.value
+
+    s = bufs.sel.clone(); s[1, [5, 6]] = s[1, [6, 5]]; refused(sel=s)
+    s = bufs.sel.clone(); s[0, 9] = s[0, 8]; refused(sel=s)
+    s = bufs.sel.clone(); s[0, k - 1] = A; refused(sel=s)
+    n0 = int(bufs.adm_count[0])
+    assert n0 > 2
+    a = bufs.adm.clone(); a[0, 0] = bufs.sel[0, 0]; a[0, :n0] = a[0, :n0].sort().values; refused(adm=a)
+    a = bufs.adm.clone(); a[0, [0, 1]] = a[0, [1, 0]]; refused(adm=a)
+    c = bufs.adm_count.clone(); c[1] = A - k + 1; refused(cnt=c)
