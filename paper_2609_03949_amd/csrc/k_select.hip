@@ -44,7 +44,9 @@ constexpr int RES_LDS = 144 * 1024;          // dynamic LDS of a resolve block
 constexpr int SAMPLE_MAX = 2048;             // keys sampled per sequence to place the bracket
 constexpr int SAMPLE_BINS = 2048;            // bins of the sample's histogram
 constexpr int RANK_QUAD_MAX = RES_THREADS;   // undecided rows ranked pairwise; radix select above
-constexpr int COMPACT_PER = 64;              // flags per thread and round of the ordered compaction
+constexpr int CPT = 16;                      // candidates per thread of a resolve block held in registers
+constexpr int AMB_LDS = 2048;                // undecided rows kept in LDS by a resolve block (more: global list)
+constexpr int XIN_LDS = 8192;                // counting blocks whose extra counts a resolve block sums in LDS
 constexpr int EX_QT_MAX = 32768;             // qt elements staged in LDS (64 KB)
 
 // order-preserving encoding of fp64 (for 64-bit compares); -0 maps as +0
@@ -97,14 +99,19 @@ __device__ __forceinline__ float rd_f32(double x) {
 
 // --------------------------------------------------------- block helpers
 
+// Workgroup barrier for exchanges through LDS only: this wave's LDS operations
+// have completed, but its global stores may still be in flight (a full
+// __syncthreads() would wait for them as well).
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 template <int NT>
 __device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t* s_red) {
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
     if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = v;
-    __syncthreads();
+    lds_barrier();
     uint32_t t = 0;
     for (int w = 0; w < NT / 64; ++w) t += s_red[w];
-    __syncthreads();
+    lds_barrier();
     return t;
 }
 
@@ -118,14 +125,14 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* s_w, u
         if (lane >= o) incl += t;
     }
     if (lane == 63) s_w[w] = incl;
-    __syncthreads();
+    lds_barrier();
     uint32_t before = 0, tot = 0;
     for (int i = 0; i < NT / 64; ++i) {
         const uint32_t c = s_w[i];
         before += (i < w) ? c : 0u;
         tot += c;
     }
-    __syncthreads();
+    lds_barrier();
     total = tot;
     return before + incl - v;
 }
@@ -138,12 +145,12 @@ __device__ __forceinline__ uint32_t block_suffix_incl(uint32_t v, uint32_t* s_w)
         const uint32_t t = __shfl_down(v, o);
         if (lane + o < 64) v += t;
     }
-    __syncthreads();
+    lds_barrier();
     if (lane == 0) s_w[w] = v;
-    __syncthreads();
+    lds_barrier();
     uint32_t add = 0;
     for (int w2 = w + 1; w2 < NT / 64; ++w2) add += s_w[w2];
-    __syncthreads();
+    lds_barrier();
     return v + add;
 }
 
@@ -230,8 +237,8 @@ __global__ __launch_bounds__(SEL_THREADS) void sel_bracket_kernel(SelectArgs a) 
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
         const int i = tid + SEL_THREADS * j;
-        const int64_t u = (m == A) ? i : min(A - 1, (int64_t)(i / RUN) * stride + (i % RUN));
-        v[j] = (i < m) ? kt[u] : 0.f;
+        const int64_t u = (i >= m) ? 0 : (m == A) ? i : min(A - 1, (int64_t)(i / RUN) * stride + (i % RUN));
+        v[j] = kt[u];
         if (i < m) {
             lo = fminf(lo, v[j]);
             hi = fmaxf(hi, v[j]);
@@ -278,29 +285,38 @@ __global__ __launch_bounds__(SEL_THREADS) void sel_bracket_kernel(SelectArgs a) 
         sq[SQ_BHI] = __float_as_uint(t_hi);
         sq[SQ_CLO] = __float_as_uint(band_lo(t_lo, E));
         sq[SQ_CHI] = __float_as_uint(band_hi(t_hi, E));
+        sq[SQ_NCAND] = 0u;     // the lists of this call start empty
+        sq[SQ_NCAND2] = 0u;
     }
 }
 
 // ----------------------------------------------------------- 2. counting
 
-// Rows of the block's region whose predicate held, written at the start of
-// the region (thread order, then j order); returns the block's total.
-__device__ __forceinline__ uint32_t region_append(uint32_t mask, int32_t* cand, float* candkey,
-                                                  const float (&k)[CB_PER], int64_t ub0, uint32_t* s_w) {
+// Rows of the block whose predicate held (bit j of mask: row ub0 + tid + 256 j)
+// appended to the sequence's list, at an offset taken with one atomic per
+// block; keys (may be NULL) receive the rows' keys.  Writes stay below `lim`.
+__device__ __forceinline__ void block_append(uint32_t mask, int64_t ub0, uint32_t* counter, int32_t* list,
+                                             float* keys, const float (&k)[CB_PER], int64_t lim, uint32_t* s_w,
+                                             uint32_t* s_base) {
     uint32_t tot;
     uint32_t pos = block_excl_scan<SEL_THREADS>((uint32_t)__popc(mask), s_w, tot);
+    if (threadIdx.x == 0) *s_base = tot ? atomicAdd(counter, tot) : 0u;
+    lds_barrier();
+    int64_t at = (int64_t)*s_base + pos;
 #pragma unroll
     for (int j = 0; j < CB_PER; ++j)
         if (mask & (1u << j)) {
-            cand[pos] = (int32_t)(ub0 + threadIdx.x + (int64_t)SEL_THREADS * j);
-            if (candkey) candkey[pos] = k[j];
-            ++pos;
+            if (at < lim) {
+                list[at] = (int32_t)(ub0 + threadIdx.x + (int64_t)SEL_THREADS * j);
+                if (keys) keys[at] = k[j];
+            }
+            ++at;
         }
-    return tot;
 }
 
 __global__ __launch_bounds__(SEL_THREADS) void sel_count_kernel(SelectArgs a) {
     __shared__ uint32_t s_w[SEL_THREADS / 64];
+    __shared__ uint32_t s_base;
     const int b = blockIdx.y, tid = threadIdx.x;
     const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
     const int64_t ub0 = (int64_t)blockIdx.x * CB_KEYS;
@@ -310,7 +326,7 @@ __global__ __launch_bounds__(SEL_THREADS) void sel_count_kernel(SelectArgs a) {
 #pragma unroll
     for (int j = 0; j < CB_PER; ++j) {
         const int64_t u = ub0 + tid + (int64_t)SEL_THREADS * j;
-        k[j] = (u < ue) ? kt[u] : 0.f;
+        k[j] = kt[u < ue ? u : ub0];
     }
     const float CLO = __uint_as_float(sq[SQ_CLO]), CHI = __uint_as_float(sq[SQ_CHI]);
     const float thi = __uint_as_float(sq[SQ_BHI]);
@@ -328,13 +344,13 @@ __global__ __launch_bounds__(SEL_THREADS) void sel_count_kernel(SelectArgs a) {
             mask |= (f == 2) ? (1u << j) : 0u;
         }
     }
-    const uint32_t ncand = region_append(mask, a.cand + (int64_t)b * a.A + ub0,
-                                         a.candkey + (int64_t)b * a.A + ub0, k, ub0, s_w);
+    block_append(mask, ub0, a.seq + (int64_t)b * SQ_WORDS + SQ_NCAND, a.cand + (int64_t)b * a.A,
+                 a.candkey + (int64_t)b * a.A, k, a.A, s_w, &s_base);
     const uint32_t packed = block_sum<SEL_THREADS>(nin | (nabove << 16), s_w);   // both <= 4096
     if (tid == 0) {
         uint32_t* w = a.blk + ((int64_t)b * a.nblk + blockIdx.x) * BLK_WORDS;
         w[BW_IN] = packed & 0xFFFFu;
-        w[BW_CAND] = ncand;
+        w[BW_XIN] = 0u;
         w[BW_ABOVE] = packed >> 16;
     }
 }
@@ -376,6 +392,7 @@ __device__ __forceinline__ double exact_chain(const uint16_t* q, const uint16_t*
                                               double ep, double ga) {
     double acc = 0.0;
     const int n8 = n / 8;
+#pragma unroll 1
     for (int p0 = 0; p0 < n8; p0 += 8) {
         u16x8_t qv[8], xv[8];
 #pragma unroll
@@ -415,21 +432,32 @@ __device__ __forceinline__ void exact_keys_block(const SelectArgs& a, int b, int
     const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
     const int n8 = a.n / 8;
     if (L.qlds) {
-        for (int p = tid; p < a.H * n8; p += RES_THREADS)
-            *reinterpret_cast<u16x8_t*>(&L.qt[8 * p]) = *reinterpret_cast<const u16x8_t*>(qtb + 8 * (int64_t)p);
+        // H * n / 8 <= EX_QT_MAX / 8 pieces of 16 B: all loads in flight together
+        constexpr int QP = EX_QT_MAX / 8 / RES_THREADS;
+        const int np = a.H * n8;
+        u16x8_t v[QP];
+#pragma unroll
+        for (int j = 0; j < QP; ++j) {
+            const int p = tid + RES_THREADS * j;
+            v[j] = *reinterpret_cast<const u16x8_t*>(qtb + 8 * (int64_t)(p < np ? p : 0));
+        }
+#pragma unroll
+        for (int j = 0; j < QP; ++j) {
+            const int p = tid + RES_THREADS * j;
+            if (p < np) *reinterpret_cast<u16x8_t*>(&L.qt[8 * p]) = v[j];
+        }
     }
     if (UB && tid < a.H) {
         const float4 hs = reinterpret_cast<const float4*>(a.hsc)[(int64_t)b * a.H + tid];
         const float ax = scaled_a(a.cert_mult, hs.x);
         L.hs[tid] = make_float4(ax, hs.y, hs.z, hs.w);
     }
-    __syncthreads();
+    lds_barrier();
     if (wave < L.nwx && namb > 0) {
         const uint16_t* qsrc = L.qlds ? L.qt : qtb;
         const uint16_t* xb = a.x + (int64_t)b * a.xbs;
         uint16_t* sx = L.x + (size_t)wave * 16 * a.n;
         unsigned long long* best = L.best + wave * 16;
-        uint32_t* list = L.list + wave * 64;
         const int KS = a.n / 32, HT = (a.H + 15) / 16;
         for (int64_t t0 = (int64_t)wave * 16; t0 < namb; t0 += (int64_t)L.nwx * 16) {
             const int64_t i = min(t0 + c, namb - 1);
@@ -483,38 +511,26 @@ __device__ __forceinline__ void exact_keys_block(const SelectArgs& a, int b, int
             // wave complete in order)
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
             __builtin_amdgcn_wave_barrier();
-            // candidates in rounds of up to 64 pairs, one fp64 chain per lane
-            int nl = 0;
-            auto flush = [&]() {
-                if (lane < nl) {
-                    const uint32_t e = list[lane];
-                    const int cr = (int)(e >> 8), h = (int)(e & 255);
-                    const int64_t ur = amb[t0 + cr];
-                    const int64_t o = (int64_t)b * a.T + ur;
-                    const float4 hs = UB ? L.hs[h] : make_float4(0.f, 0.f, 0.f, 0.f);
-                    const double v = exact_chain<UB>(qsrc + (int64_t)h * a.n, &sx[cr * a.n], a.n, hs,
-                                                     UB ? (double)a.eta[o] : 0.0, UB ? (double)a.eps[o] : 0.0,
-                                                     UB ? (double)a.gam[o] : 0.0);
-                    atomicMax(&best[cr], (unsigned long long)f64_to_ord(v));
-                }
-                nl = 0;
-            };
+            // this lane's candidates: slot 4 ht + q (head 16 ht + 4 g + q of row c)
+            uint32_t cm = 0;
 #pragma unroll
             for (int ht = 0; ht < 8; ++ht)
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const bool cand = (t0 + c < namb) && acc[ht][q] >= thr && acc[ht][q] > -INFINITY;
-                    const uint64_t bal = __ballot(cand);
-                    const int cnt = __popcll(bal);
-                    if (cnt == 0) continue;
-                    if (nl + cnt > 64) flush();
-                    if (cand) {
-                        const int pos = nl + __popcll(bal & ((1ull << lane) - 1ull));
-                        list[pos] = ((uint32_t)c << 8) | (uint32_t)(16 * ht + 4 * g + q);
-                    }
-                    nl += cnt;
+                for (int q = 0; q < 4; ++q)
+                    cm |= ((t0 + c < namb) && acc[ht][q] >= thr && acc[ht][q] > -INFINITY) ? (1u << (4 * ht + q)) : 0u;
+            // one fp64 chain per lane and round until every lane's candidates are done
+            // (a single copy of the chain's code)
+            while (__ballot(cm != 0u)) {
+                if (cm) {
+                    const int sl = __ffs(cm) - 1;
+                    cm &= cm - 1u;
+                    const int h = 16 * (sl >> 2) + 4 * g + (sl & 3);
+                    const float4 hs = UB ? L.hs[h] : make_float4(0.f, 0.f, 0.f, 0.f);
+                    const double v = exact_chain<UB>(qsrc + (int64_t)h * a.n, &sx[c * a.n], a.n, hs, (double)et,
+                                                     (double)ep, (double)ga);
+                    atomicMax(&best[c], (unsigned long long)f64_to_ord(v));
                 }
-            flush();
+            }
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
             __builtin_amdgcn_wave_barrier();
             if (lane < 16 && t0 + lane < namb) ak[t0 + lane] = best[lane];
@@ -525,68 +541,7 @@ __device__ __forceinline__ void exact_keys_block(const SelectArgs& a, int b, int
     __syncthreads();
 }
 
-// Undecided rows of the count regions: wave w walks regions w, w + 16, ...;
-// `keep` decides per (row, key~) whether the row stays undecided (and writes
-// its flag).  The kept rows are appended to amb (order irrelevant).
-template <typename F>
-__device__ __forceinline__ void walk_regions(const SelectArgs& a, int b, bool with_keys, uint32_t* s_namb,
-                                             int32_t* amb, F keep) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    for (int64_t i = wave; i < a.nblk; i += RES_WAVES) {
-        const uint32_t cnt = a.blk[((int64_t)b * a.nblk + i) * BLK_WORDS + BW_CAND];
-        const int32_t* cr = a.cand + (int64_t)b * a.A + i * CB_KEYS;
-        const float* ck = a.candkey + (int64_t)b * a.A + i * CB_KEYS;
-        for (uint32_t j0 = 0; j0 < cnt; j0 += 64) {
-            const uint32_t j = j0 + lane;
-            const bool live = j < cnt;
-            const int32_t u = live ? cr[j] : 0;
-            const float kv = (live && with_keys) ? ck[j] : 0.f;
-            const bool und = live && keep(u, kv);
-            const uint64_t bal = __ballot(und);
-            if (bal == 0) continue;
-            const int leader = __ffsll((unsigned long long)bal) - 1;
-            uint32_t base = 0;
-            if (lane == leader) base = atomicAdd(s_namb, (uint32_t)__popcll(bal));
-            base = __shfl(base, leader);
-            if (und) amb[base + __popcll(bal & ((1ull << lane) - 1ull))] = u;
-        }
-    }
-}
 
-// Ordered compaction: rows u < A whose flag equals `target`, ascending, into
-// out[0 .. min(total, cap)); returns the total (all threads).  fb is the
-// sequence's flag row, padded to a multiple of 64 bytes and 16-byte aligned.
-__device__ __forceinline__ int64_t compact_flags(const uint8_t* fb, int64_t A, uint8_t target, int32_t* out, int64_t cap,
-                                 uint32_t* s_w) {
-    const int tid = threadIdx.x;
-    int64_t carry = 0;
-    for (int64_t c0 = 0; c0 < A; c0 += (int64_t)RES_THREADS * COMPACT_PER) {
-        const int64_t u0 = c0 + (int64_t)COMPACT_PER * tid;
-        u32x4_t v[COMPACT_PER / 16];
-#pragma unroll
-        for (int i = 0; i < COMPACT_PER / 16; ++i)
-            v[i] = (u0 < A) ? *reinterpret_cast<const u32x4_t*>(fb + u0 + 16 * i) : u32x4_t{0u, 0u, 0u, 0u};
-        const int lim = (int)max((int64_t)0, min((int64_t)COMPACT_PER, A - u0));
-        uint32_t cnt = 0;
-#pragma unroll
-        for (int e = 0; e < COMPACT_PER; ++e) {
-            const uint32_t byte = (v[e >> 4][(e >> 2) & 3] >> (8 * (e & 3))) & 0xFFu;
-            cnt += (e < lim && byte == target);
-        }
-        uint32_t tot;
-        int64_t pos = carry + block_excl_scan<RES_THREADS>(cnt, s_w, tot);
-#pragma unroll
-        for (int e = 0; e < COMPACT_PER; ++e) {
-            const uint32_t byte = (v[e >> 4][(e >> 2) & 3] >> (8 * (e & 3))) & 0xFFu;
-            if (e < lim && byte == target) {
-                if (pos < cap) out[pos] = (int32_t)(u0 + e);
-                ++pos;
-            }
-        }
-        carry += tot;
-    }
-    return carry;
-}
 
 // Rank of the undecided rows by (exact key desc, index asc): the first
 // `need` of them get flag 1; returns (in thread 0's view, via *theta_ord) the
@@ -594,7 +549,7 @@ __device__ __forceinline__ int64_t compact_flags(const uint8_t* fb, int64_t A, u
 // when it is short; otherwise a radix select on the 96-bit composite
 // (order key, ~index), whose larger values come first.
 __device__ __forceinline__ void rank_winners(const int32_t* amb, const uint64_t* ak, int64_t namb, int64_t need, uint8_t* fb,
-                             uint8_t* lds, uint64_t* s_theta) {
+                             uint32_t* xin, uint8_t* lds, uint64_t* s_theta) {
     const int tid = threadIdx.x;
     if (namb <= RANK_QUAD_MAX) {
         uint64_t* s_k = reinterpret_cast<uint64_t*>(lds);
@@ -603,7 +558,7 @@ __device__ __forceinline__ void rank_winners(const int32_t* amb, const uint64_t*
             s_k[tid] = ak[tid];
             s_u[tid] = amb[tid];
         }
-        __syncthreads();
+        lds_barrier();
         if (tid < namb) {
             const uint64_t ki = s_k[tid];
             const int32_t ui = s_u[tid];
@@ -614,10 +569,11 @@ __device__ __forceinline__ void rank_winners(const int32_t* amb, const uint64_t*
             }
             if (rank < need) {
                 fb[ui] = 1;
+                atomicAdd(&xin[(int64_t)(ui / CB_KEYS) * BLK_WORDS], 1u);
                 if (rank == need - 1) *s_theta = ki;
             }
         }
-        __syncthreads();
+        lds_barrier();
         return;
     }
     uint32_t* s_h = reinterpret_cast<uint32_t*>(lds);            // 256 bins
@@ -625,6 +581,7 @@ __device__ __forceinline__ void rank_winners(const int32_t* amb, const uint64_t*
     uint64_t pre_hi = 0, mask_hi = 0;
     uint32_t pre_lo = 0, mask_lo = 0;
     uint32_t rem = (uint32_t)need;
+#pragma unroll 1
     for (int p = 0; p < 12; ++p) {
         if (tid < 256) s_h[tid] = 0u;
         __syncthreads();
@@ -672,7 +629,10 @@ __device__ __forceinline__ void rank_winners(const int32_t* amb, const uint64_t*
     for (int64_t i = tid; i < namb; i += RES_THREADS) {
         const uint64_t hi = ak[i];
         const uint32_t lo = ~(uint32_t)amb[i];
-        if (hi > pre_hi || (hi == pre_hi && lo >= pre_lo)) fb[amb[i]] = 1;
+        if (hi > pre_hi || (hi == pre_hi && lo >= pre_lo)) {
+            fb[amb[i]] = 1;
+            atomicAdd(&xin[(int64_t)(amb[i] / CB_KEYS) * BLK_WORDS], 1u);
+        }
     }
     if (tid == 0) *s_theta = pre_hi;
     __syncthreads();
@@ -683,17 +643,36 @@ __device__ __forceinline__ void rank_winners(const int32_t* amb, const uint64_t*
 __global__ __launch_bounds__(RES_THREADS, 1) void sel_resolve_kernel(SelectArgs a) {
     extern __shared__ __align__(16) uint8_t lds[];
     __shared__ uint32_t s_w[RES_WAVES];
-    __shared__ uint32_t s_namb, s_nin2;
+    __shared__ uint32_t s_namb;
     __shared__ int s_bin;
     __shared__ uint64_t s_theta;
+    __shared__ int32_t s_amb[AMB_LDS];         // the undecided rows (the global list holds them all)
     const int b = blockIdx.x, tid = threadIdx.x;
     uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
     uint8_t* fb = a.flags + (int64_t)b * a.fstride;
     const float* kt = a.kt + (int64_t)b * a.A;
+    const int32_t* cr = a.cand + (int64_t)b * a.A;
+    const float* ck = a.candkey + (int64_t)b * a.A;
     int32_t* amb = a.amb + (int64_t)b * a.A;
     uint64_t* ak = a.ambkey + (int64_t)b * a.A;
     const float tlo = __uint_as_float(sq[SQ_BLO]), thi = __uint_as_float(sq[SQ_BHI]);
+    const int64_t ncand = min((int64_t)sq[SQ_NCAND], a.A);
     const float E = key_band_f32(sq, a.n);
+    // the first NT * CPT candidates stay in registers for both passes below
+    constexpr int64_t CH = (int64_t)RES_THREADS * CPT;
+    int32_t cu[CPT];
+    float cv[CPT];
+    // (loads are unconditional, from a clamped index, so that they are all in
+    // flight together and none is awaited inside a branch)
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) {
+        const int64_t i = tid + (int64_t)RES_THREADS * j;
+        const int64_t ic = min(i, max(ncand - 1, (int64_t)0));
+        const int32_t u = cr[ic];
+        const float kv = ck[ic];
+        cu[j] = (i < ncand) ? u : -1;
+        cv[j] = kv;
+    }
     // counts of the counting blocks
     uint32_t nin = 0, nab = 0;
     for (int64_t i = tid; i < a.nblk; i += RES_THREADS) {
@@ -701,34 +680,29 @@ __global__ __launch_bounds__(RES_THREADS, 1) void sel_resolve_kernel(SelectArgs 
         nin += w[BW_IN];
         nab += w[BW_ABOVE];
     }
-    nin = block_sum<RES_THREADS>(nin, s_w);
-    nab = block_sum<RES_THREADS>(nab, s_w);
-    // fine histogram of the candidates inside [t_lo, t_hi]
     uint32_t* s_h = reinterpret_cast<uint32_t*>(lds);
     for (int i = tid; i < HIST_BINS; i += RES_THREADS) s_h[i] = 0u;
     if (tid == 0) {
         s_namb = 0u;
-        s_nin2 = 0u;
         s_bin = -1;
         s_theta = f64_to_ord(-INFINITY);
     }
-    __syncthreads();
+    nin = block_sum<RES_THREADS>(nin, s_w);
+    nab = block_sum<RES_THREADS>(nab, s_w);
+    // fine histogram of the candidates inside [t_lo, t_hi]
     const float sc0 = bin_scale(tlo, thi);
     uint32_t nmid = 0;
-    {
-        const int lane = tid & 63, wave = tid >> 6;
-        for (int64_t i = wave; i < a.nblk; i += RES_WAVES) {
-            const uint32_t cnt = a.blk[((int64_t)b * a.nblk + i) * BLK_WORDS + BW_CAND];
-            const float* ck = a.candkey + (int64_t)b * a.A + i * CB_KEYS;
-            for (uint32_t j = lane; j < cnt; j += 64) {
-                const float kv = ck[j];
-                if (kv >= tlo && kv <= thi) {
-                    atomicAdd(&s_h[bin_of(kv, tlo, sc0)], 1u);
-                    ++nmid;
-                }
-            }
+    auto hist_one = [&](float kv) {
+        if (kv >= tlo && kv <= thi) {
+            atomicAdd(&s_h[bin_of(kv, tlo, sc0)], 1u);
+            ++nmid;
         }
-    }
+    };
+#pragma unroll
+    for (int j = 0; j < CPT; ++j)
+        if (cu[j] >= 0) hist_one(cv[j]);
+    for (int64_t c0 = CH; c0 < ncand; c0 += CH)
+        for (int64_t i = c0 + tid; i < min(ncand, c0 + CH); i += RES_THREADS) hist_one(ck[i]);
     nmid = block_sum<RES_THREADS>(nmid, s_w);
     const int64_t need = a.k - (int64_t)nab;
     const bool ok = need >= 1 && need <= (int64_t)nmid;
@@ -750,37 +724,88 @@ __global__ __launch_bounds__(RES_THREADS, 1) void sel_resolve_kernel(SelectArgs 
     const int db = s_bin < 0 ? 0 : s_bin;
     const float HI = band_hi(ru_f32(edge_hi_of(db, lo, hi, sc)), E);
     const float LO = band_lo(rd_f32(edge_lo_of(db, lo, sc)), E);
-    // classification: selected (w > HI), excluded (v < LO), undecided
+    // classification: selected (w > HI), excluded (v < LO), undecided.  The
+    // rows this block decides in are counted per counting block (in LDS after
+    // the histogram, or with global atomics for very long archives), for the
+    // ordered compaction that follows.
     auto classify = [&](float kv) -> uint8_t { return (band_lo(kv, E) > HI) ? 1 : ((band_hi(kv, E) < LO) ? 0 : 2); };
-    uint32_t nin2 = 0;
-    if (ok) {
-        walk_regions(a, b, true, &s_namb, amb, [&](int32_t u, float kv) {
-            const uint8_t f = classify(kv);
-            fb[u] = f;
-            nin2 += (f == 1);
-            return f == 2;
-        });
-    } else {
-        // every row again: the counting pass's early classification used the missed bracket
+    uint32_t* blkb = a.blk + (int64_t)b * a.nblk * BLK_WORDS;
+    const bool xlds = a.nblk <= XIN_LDS;
+    uint32_t* s_x = reinterpret_cast<uint32_t*>(lds + HIST_BINS * 4);
+    if (xlds)
+        for (int64_t i = tid; i < a.nblk; i += RES_THREADS) s_x[i] = 0u;
+    lds_barrier();
+    auto count_in = [&](int64_t u) {
+        if (xlds) atomicAdd(&s_x[u / CB_KEYS], 1u);
+        else atomicAdd(&blkb[(u / CB_KEYS) * BLK_WORDS + BW_XIN], 1u);
+    };
+    auto append = [&](bool und, int32_t u) {
+        const uint64_t bal = __ballot(und);
+        if (bal == 0) return;
         const int lane = tid & 63;
-        for (int64_t u0 = (int64_t)(tid >> 6) * 64; u0 < a.A; u0 += RES_THREADS) {
-            const int64_t u = u0 + lane;
+        const int leader = __ffsll((unsigned long long)bal) - 1;
+        uint32_t base = 0;
+        if (lane == leader) base = atomicAdd(&s_namb, (uint32_t)__popcll(bal));
+        base = __shfl(base, leader);
+        if (und) {
+            const uint32_t pos = base + __popcll(bal & ((1ull << lane) - 1ull));
+            amb[pos] = u;
+            if (pos < AMB_LDS) s_amb[pos] = u;
+        }
+    };
+    if (ok) {
+        // the candidates; every other row was decided by the counting pass
+#pragma unroll
+        for (int j = 0; j < CPT; ++j) {
+            uint8_t f = 0;
+            if (cu[j] >= 0) {
+                f = classify(cv[j]);
+                fb[cu[j]] = f;
+                if (f == 1) count_in(cu[j]);
+            }
+            append(f == 2, cu[j]);
+        }
+        for (int64_t c0 = CH; c0 < ncand; c0 += CH)
+            for (int64_t i0 = c0; i0 < min(ncand, c0 + CH); i0 += RES_THREADS) {
+                const int64_t i = i0 + tid;
+                uint8_t f = 0;
+                int32_t u = 0;
+                if (i < ncand) {
+                    u = cr[i];
+                    f = classify(ck[i]);
+                    fb[u] = f;
+                    if (f == 1) count_in(u);
+                }
+                append(f == 2, u);
+            }
+    } else {
+        // every row again: the counting pass's early classification used the
+        // missed bracket, so its counts of selected rows are void as well
+        for (int64_t i = tid; i < a.nblk; i += RES_THREADS) blkb[i * BLK_WORDS + BW_IN] = 0u;
+        for (int64_t u0 = 0; u0 < a.A; u0 += RES_THREADS) {
+            const int64_t u = u0 + tid;
             const bool live = u < a.A;
             const uint8_t f = live ? classify(kt[u]) : 0;
-            if (live) fb[u] = f;
-            nin2 += (f == 1);
-            const bool und = live && f == 2;
-            const uint64_t bal = __ballot(und);
-            if (bal) {
-                const int leader = __ffsll((unsigned long long)bal) - 1;
-                uint32_t base = 0;
-                if (lane == leader) base = atomicAdd(&s_namb, (uint32_t)__popcll(bal));
-                base = __shfl(base, leader);
-                if (und) amb[base + __popcll(bal & ((1ull << lane) - 1ull))] = (int32_t)u;
+            if (live) {
+                fb[u] = f;
+                if (f == 1) count_in(u);
             }
+            append(live && f == 2, (int32_t)u);
         }
     }
+    lds_barrier();
+    if (xlds)
+        for (int64_t i = tid; i < a.nblk; i += RES_THREADS) blkb[i * BLK_WORDS + BW_XIN] = s_x[i];
+    uint32_t nin2 = 0;
+    if (xlds)
+        for (int64_t i = tid; i < a.nblk; i += RES_THREADS) nin2 += s_x[i];
     nin2 = block_sum<RES_THREADS>(nin2, s_w);
+    if (!xlds) {
+        __threadfence_block();
+        __syncthreads();
+        for (int64_t i = tid; i < a.nblk; i += RES_THREADS) nin2 += blkb[i * BLK_WORDS + BW_XIN];
+        nin2 = block_sum<RES_THREADS>(nin2, s_w);
+    }
     const int64_t namb = s_namb;
     const int64_t n_in = (ok ? (int64_t)nin : 0) + (int64_t)nin2;
     const int64_t need2 = a.k - n_in;   // >= 1 and <= namb by the band argument
@@ -789,18 +814,81 @@ __global__ __launch_bounds__(RES_THREADS, 1) void sel_resolve_kernel(SelectArgs 
         sq[SQ_THI] = __float_as_uint(HI);
         sq[SQ_NAMB] = (uint32_t)namb;
     }
-    // exact keys of the undecided rows, then their ranking
-    __threadfence_block();
+    // exact keys of the undecided rows, then their ranking (the list from LDS
+    // when it fits there, else from global memory once it is visible)
+    const bool amb_lds = namb <= AMB_LDS;
+    if (!amb_lds) __threadfence_block();
     __syncthreads();
+    const int32_t* al = amb_lds ? s_amb : amb;
     const ExLds L = ex_carve(lds, a.H, a.n);
-    exact_keys_block<false>(a, b, namb, amb, ak, L, next_up_f32(2.0f * E));
-    __threadfence_block();
-    __syncthreads();
-    rank_winners(amb, ak, namb, need2, fb, lds, &s_theta);
+    exact_keys_block<false>(a, b, namb, al, ak, L, next_up_f32(2.0f * E));
+    rank_winners(al, ak, namb, need2, fb, blkb + BW_XIN, lds, &s_theta);
     if (tid == 0) a.theta[b] = ord_to_f64(s_theta);
-    __threadfence_block();
-    __syncthreads();
-    compact_flags(fb, a.A, 1, a.sel + (int64_t)b * a.k, a.k, s_w);
+}
+
+// ------------------------------------------------------ ordered compaction
+
+// 0x80 in each byte of v that equals t (t replicated in each byte of tt)
+__device__ __forceinline__ uint32_t bytes_equal(uint32_t v, uint32_t tt) {
+    const uint32_t x = v ^ tt;
+    return ~(((x & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | x | 0x7F7F7F7Fu);
+}
+
+struct CompactArgs {
+    const uint8_t* flags;  // [B, fstride]
+    int64_t fstride;
+    const uint32_t* blk;   // [B, nblk, BLK_WORDS]: rows decided in per counting block (BW_IN + BW_XIN)
+    int64_t nblk, A;
+    uint32_t target;
+    int32_t* out;          // [B, out_stride]
+    int64_t out_stride, cap;
+    int32_t* total;        // [B] or null: the number of rows with the target flag
+};
+
+// One block per counting block (4096 rows) of a sequence: its offset is the
+// sum of the decided-in counts of the blocks before it; thread t owns 16
+// consecutive rows (one 16-byte load of flags), then one block scan orders
+// the writes.
+__global__ __launch_bounds__(SEL_THREADS) void compact_kernel(CompactArgs a) {
+    __shared__ uint32_t s_w[SEL_THREADS / 64];
+    const int b = blockIdx.y, tid = threadIdx.x;
+    const int64_t c = blockIdx.x;
+    const uint32_t* w = a.blk + (int64_t)b * a.nblk * BLK_WORDS;
+    uint32_t part = 0;
+    for (int64_t j = tid; j < c; j += SEL_THREADS) part += w[j * BLK_WORDS + BW_IN] + w[j * BLK_WORDS + BW_XIN];
+    const int64_t u0 = c * CB_KEYS + 16 * tid;
+    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(a.flags + (int64_t)b * a.fstride + (u0 < a.A ? u0 : 0));
+    const uint32_t base = block_sum<SEL_THREADS>(part, s_w);
+    const uint32_t tt = 0x01010101u * a.target;
+    uint32_t m[4], cnt = 0;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+        const int64_t valid = min((int64_t)4, max((int64_t)0, a.A - (u0 + 4 * d)));
+        const uint32_t keep = valid >= 4 ? 0xFFFFFFFFu : ((1u << (8 * valid)) - 1u);
+        m[d] = bytes_equal(v[d], tt) & keep;
+        cnt += (uint32_t)__popc(m[d]);
+    }
+    uint32_t tot;
+    int64_t pos = (int64_t)base + block_excl_scan<SEL_THREADS>(cnt, s_w, tot);
+    int32_t* ob = a.out ? a.out + (int64_t)b * a.out_stride : nullptr;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+        uint32_t bits = m[d];
+        while (bits) {
+            const int e = (__ffs(bits) - 1) >> 3;
+            if (pos < a.cap) ob[pos] = (int32_t)(u0 + 4 * d + e);
+            ++pos;
+            bits &= bits - 1u;
+        }
+    }
+    if (a.total && c == a.nblk - 1 && tid == 0) a.total[b] = (int32_t)(base + tot);
+}
+
+static hipError_t run_compact(const SelectArgs& s, const uint8_t* flags, uint32_t target, int32_t* out, int64_t stride,
+                              int64_t cap, int32_t* total, hipStream_t st) {
+    const CompactArgs c{flags, s.fstride, s.blk, s.nblk, s.A, target, out, stride, cap, total};
+    hipLaunchKernelGGL(compact_kernel, dim3((unsigned)s.nblk, s.B), dim3(SEL_THREADS), 0, st, c);
+    return hipGetLastError();
 }
 
 __global__ __launch_bounds__(SEL_THREADS) void fill_u8_kernel(uint8_t* p, int64_t n, uint8_t v) {
@@ -830,7 +918,8 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&sel_resolve_kernel),
                               hipFuncAttributeMaxDynamicSharedMemorySize, RES_LDS);
     hipLaunchKernelGGL(sel_resolve_kernel, dim3(a.B), dim3(RES_THREADS), RES_LDS, s, a);
-    return hipGetLastError();
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return run_compact(a, a.flags, 1, a.sel, a.k, a.k, nullptr, s);
 }
 
 // ---------------------------------------------------------------- admit
@@ -841,6 +930,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
 // none, every row outside S is undecided (its exact bound decides).
 __global__ __launch_bounds__(SEL_THREADS) void adm_classify_kernel(SelectArgs a) {
     __shared__ uint32_t s_w[SEL_THREADS / 64];
+    __shared__ uint32_t s_base;
     const int b = blockIdx.y, tid = threadIdx.x;
     const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
     const int64_t ub0 = (int64_t)blockIdx.x * CB_KEYS;
@@ -856,10 +946,11 @@ __global__ __launch_bounds__(SEL_THREADS) void adm_classify_kernel(SelectArgs a)
 #pragma unroll
     for (int j = 0; j < CB_PER; ++j) {
         const int64_t u = ub0 + tid + (int64_t)SEL_THREADS * j;
-        t[j] = (u < ue) ? ubb[u] : 0.f;
-        fin[j] = (u < ue) ? fb[u] : (uint8_t)1;
+        const int64_t uc = u < ue ? u : ub0;
+        t[j] = ubb[uc];
+        fin[j] = (u < ue) ? fb[uc] : (uint8_t)1;
     }
-    uint32_t nadm = 0, mask = 0;
+    uint32_t mask = 0, nadm = 0;
 #pragma unroll
     for (int j = 0; j < CB_PER; ++j) {
         const int64_t u = ub0 + tid + (int64_t)SEL_THREADS * j;
@@ -881,12 +972,13 @@ __global__ __launch_bounds__(SEL_THREADS) void adm_classify_kernel(SelectArgs a)
             mask |= (f == 4) ? (1u << j) : 0u;
         }
     }
-    const uint32_t namb = region_append(mask, a.cand + (int64_t)b * a.A + ub0, nullptr, t, ub0, s_w);
+    block_append(mask, ub0, a.seq + (int64_t)b * SQ_WORDS + SQ_NCAND2, a.cand + (int64_t)b * a.A, nullptr, t,
+                 a.A, s_w, &s_base);
     nadm = block_sum<SEL_THREADS>(nadm, s_w);
     if (tid == 0) {
         uint32_t* w = a.blk + ((int64_t)b * a.nblk + blockIdx.x) * BLK_WORDS;
         w[BW_IN] = nadm;
-        w[BW_CAND] = namb;
+        w[BW_XIN] = 0u;
     }
 }
 
@@ -895,31 +987,30 @@ __global__ __launch_bounds__(SEL_THREADS) void adm_classify_kernel(SelectArgs a)
 __global__ __launch_bounds__(RES_THREADS, 1) void adm_resolve_kernel(SelectArgs a) {
     extern __shared__ __align__(16) uint8_t lds[];
     __shared__ uint32_t s_w[RES_WAVES];
-    __shared__ uint32_t s_namb;
     const int b = blockIdx.x, tid = threadIdx.x;
     uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
     uint8_t* f2 = a.flags2 + (int64_t)b * a.fstride;
-    int32_t* amb = a.amb + (int64_t)b * a.A;
+    const int32_t* amb = a.cand + (int64_t)b * a.A;    // the undecided rows listed by the classification
     uint64_t* ak = a.ambkey + (int64_t)b * a.A;
     const double th = a.theta[b];
     const bool same = sq[SQ_CMULT] == __float_as_uint(a.cert_mult);
-    if (tid == 0) s_namb = 0u;
+    const int64_t namb = min((int64_t)sq[SQ_NCAND2], a.A);
     __syncthreads();
-    walk_regions(a, b, false, &s_namb, amb, [](int32_t, float) { return true; });
-    __syncthreads();
-    const int64_t namb = s_namb;
-    if (tid == 0) sq[SQ_NAMB2] = (uint32_t)namb;
-    __threadfence_block();
-    __syncthreads();
+    if (tid == 0) {
+        sq[SQ_NAMB2] = (uint32_t)namb;
+        sq[SQ_NCAND2] = 0u;    // consumed: a repeated admission starts an empty list
+    }
     const ExLds L = ex_carve(lds, a.H, a.n);
     const float margin = same ? next_up_f32(2.0f * ru_f32(ub_error_of(sq, a.n) * (1.0 + 0x1p-20))) : INFINITY;
     exact_keys_block<true>(a, b, namb, amb, ak, L, margin);
+    // the undecided rows admitted on their exact bound (the classification left them at 4)
+    uint32_t* blkb = a.blk + (int64_t)b * a.nblk * BLK_WORDS;
     for (int64_t i = tid; i < namb; i += RES_THREADS)
-        if (ord_to_f64(ak[i]) > th) f2[amb[i]] = 3;
-    __threadfence_block();
-    __syncthreads();
-    const int64_t total = compact_flags(f2, a.A, 3, a.adm ? a.adm + (int64_t)b * a.cap : nullptr, a.adm ? a.cap : 0, s_w);
-    if (tid == 0) a.adm_count[b] = (int32_t)total;
+        if (ord_to_f64(ak[i]) > th) {
+            const int32_t u = amb[i];
+            f2[u] = 3;
+            atomicAdd(&blkb[(int64_t)(u / CB_KEYS) * BLK_WORDS + BW_XIN], 1u);
+        }
 }
 
 __global__ __launch_bounds__(64) void zero_counts_kernel(int32_t* p, int n) {
@@ -937,7 +1028,8 @@ hipError_t launch_admit(const SelectArgs& a, hipStream_t s) {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&adm_resolve_kernel),
                               hipFuncAttributeMaxDynamicSharedMemorySize, RES_LDS);
     hipLaunchKernelGGL(adm_resolve_kernel, dim3(a.B), dim3(RES_THREADS), RES_LDS, s, a);
-    return hipGetLastError();
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return run_compact(a, a.flags2, 3, a.adm, a.cap, a.cap, a.adm_count, s);
 }
 
 }  // namespace vkv

@@ -137,12 +137,16 @@ enum SeqWord : int {
     SQ_THI = 14,    // float bits: HI >= k-th largest of (key~ + E)   (diagnostic)
     SQ_NAMB = 15,   // ambiguous rows of the selection                (diagnostic)
     SQ_NAMB2 = 16,  // ambiguous rows of the admission                (diagnostic)
+    SQ_NCAND = 17,  // selection candidates listed by the counting pass (zeroed by the bracket launch)
+    SQ_NCAND2 = 18, // undecided admission rows listed by the classification (zeroed by its consumer)
     SQ_WORDS = 32
 };
 
 constexpr int CB_KEYS = 4096;      // archive rows per counting / classification block
 constexpr int BLK_WORDS = 4;       // per counting block: the counts below
-enum BlockWord : int { BW_IN = 0, BW_CAND = 1, BW_ABOVE = 2 };   // (admission: BW_IN = admitted, BW_CAND = ambiguous)
+// per counting block: rows it decided in (selected / admitted), rows above the
+// sampled bracket, and rows of its range the resolve block decided in
+enum BlockWord : int { BW_IN = 0, BW_XIN = 1, BW_ABOVE = 2 };
 constexpr int HIST_BINS = 4096;
 constexpr int ATT_CHUNK = 32;      // rows per attention tile
 constexpr int ATT_HEADS = 128;     // heads per attention workgroup (8 waves x 16)
@@ -211,8 +215,8 @@ struct SelectArgs {
     uint8_t* flags;        // [B,A] selection: 1 selected, 0 not, 2 undecided
     uint8_t* flags2;       // [B,A] admission: 3 admitted, 0 not, 4 undecided
     uint32_t* blk;         // [B,nblk,BLK_WORDS] per counting block
-    int32_t* cand;         // [B,A] per counting block region: its candidate rows
-    float* candkey;        // [B,A] their keys~ (selection)
+    int32_t* cand;         // [B,A] candidate rows (selection) / undecided rows (admission), listed
+    float* candkey;        // [B,A] the candidates' keys~ (selection)
     int32_t* amb;          // [B,A] the undecided rows, compacted
     uint64_t* ambkey;      // [B,A] their exact keys (order-preserving encoding of fp64)
     int32_t* sel;          // [B,k]
