@@ -246,6 +246,24 @@ int vkv_step_run(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, in
                  float* lse, void* stream);
 
 /*
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The same step
+ * as vkv_step_run (same arguments and results, the same kernels) on a
+ * workspace the library owns: a static device array of VKV_STATIC_WS_BYTES per
+ * device, held until the process ends.  The call allocates nothing.  Steps
+ * whose workspace (vkv_workspace_size) exceeds it are refused with
+ * VKV_E_WORKSPACE before anything is launched.  Every call on one device
+ * shares that device's array, which keeps the last call's contents (each step
+ * initialises what it reads); calls that overlap on one device -- on two
+ * streams, or from two host threads -- race and must be serialised by the
+ * caller.  The context must belong to the device the buffers live on.
+ */
+#define VKV_STATIC_WS_BYTES (64u << 20)
+int vkv_step_run_static(vkv_ctx* ctx, const vkv_step* st, int64_t k, float* key, float* ub,
+                        int32_t* sel, double* theta, int32_t* adm, int32_t* adm_count, int64_t cap,
+                        float cert_mult, float scale, uint16_t* out, float* lse, void* stream);
+
+/*
  * The executable row-set invariant (the deployment's per-step row-set
  * assertion, appendix "Measurement integrity: full protocol"), on caller
  * buffers: every sel[b] row lies in the archive [0, A) and the list is strictly

@@ -19,7 +19,7 @@ import torch  # noqa: F401  (loads the HIP runtime the library binds to)
 __all__ = [
     "VKV_MODE_ROPE", "VKV_MODE_DIGEST", "VKV_MODE_ROPE_DIGEST", "VkvError", "Context", "Step",
     "lib_path", "load", "digest_build", "workspace_size", "query_prep", "score", "select", "admit", "attend",
-    "step_run", "check_rows", "exported_symbols",
+    "step_run", "step_run_static", "check_rows", "exported_symbols",
 ]
 
 VKV_MODE_ROPE, VKV_MODE_DIGEST, VKV_MODE_ROPE_DIGEST = 1, 2, 3
@@ -31,7 +31,7 @@ _LIB_PATH = os.path.join(_HERE, "libvkv.so")
 exported_symbols = (
     "vkv_create", "vkv_destroy", "vkv_status_string", "vkv_last_error", "vkv_version",
     "vkv_digest_build", "vkv_workspace_size", "vkv_query_prep", "vkv_score", "vkv_select", "vkv_admit",
-    "vkv_attend", "vkv_step_run", "vkv_check_rows", "vkv_set_timing", "vkv_score_timing",
+    "vkv_attend", "vkv_step_run", "vkv_step_run_static", "vkv_check_rows", "vkv_set_timing", "vkv_score_timing",
 )
 
 
@@ -91,13 +91,15 @@ def load():
     lib.vkv_step_run.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P, P, P, P, i64,
                                  f32, f32, P, P, P]
     lib.vkv_check_rows.argtypes = [P, sp, i64, P, P, P, i64, P]
+    lib.vkv_step_run_static.argtypes = [P, sp, i64, P, P, P, P, P, P, i64, f32, f32, P, P, P]
     lib.vkv_set_timing.argtypes = [P, ctypes.c_int]
     lib.vkv_score_timing.argtypes = [P, ctypes.POINTER(ctypes.c_float), ctypes.c_int]
     for name in exported_symbols:
         getattr(lib, name).restype = getattr(lib, name).restype or ctypes.c_int
     for name in ("vkv_create", "vkv_destroy", "vkv_digest_build", "vkv_workspace_size",
                  "vkv_query_prep", "vkv_score",
-                 "vkv_select", "vkv_admit", "vkv_attend", "vkv_step_run", "vkv_check_rows", "vkv_version",
+                 "vkv_select", "vkv_admit", "vkv_attend", "vkv_step_run", "vkv_step_run_static",
+                 "vkv_check_rows", "vkv_version",
                  "vkv_set_timing", "vkv_score_timing"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
@@ -260,6 +262,17 @@ def step_run(ctx: Context, step: Step, ws: torch.Tensor, k: int, key: torch.Tens
                                    _ptr(ub), _ptr(sel), _ptr(theta), _ptr(adm), _ptr(adm_count),
                                    int(cap), float(cert_mult), float(scale), _ptr(out), _ptr(lse),
                                    _stream(stream)))
+
+
+def step_run_static(ctx: Context, step: Step, k: int, key: torch.Tensor, ub: Optional[torch.Tensor],
+                    sel: torch.Tensor, theta: torch.Tensor, adm: Optional[torch.Tensor],
+                    adm_count: Optional[torch.Tensor], cap: int, scale: float, out: torch.Tensor,
+                    lse: torch.Tensor, stream=None, cert_mult: float = 1.0):
+    """vkv_step_run_static: the step on the library's static workspace (no allocation)."""
+    ctx.check(ctx.lib.vkv_step_run_static(ctx.handle, step.ref, int(k), _ptr(key), _ptr(ub), _ptr(sel),
+                                          _ptr(theta), _ptr(adm), _ptr(adm_count), int(cap),
+                                          float(cert_mult), float(scale), _ptr(out), _ptr(lse),
+                                          _stream(stream)))
 
 
 def check_rows(ctx: Context, step: Step, k: int, sel: Optional[torch.Tensor],

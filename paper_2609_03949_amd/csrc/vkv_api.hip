@@ -13,9 +13,16 @@ using namespace vkv;
 
 constexpr int TIMING_SLOTS = 512;  // score launches timed between two vkv_score_timing calls
 
+// The workspace of vkv_step_run_static: one per device, held until the process
+// ends.  In host code `scratch` only names the symbol; its device address is
+// taken once per device with hipGetSymbolAddress (in vkv_create) and used
+// everywhere the host hands it to the kernels.
+static __device__ __align__(256) uint8_t scratch[VKV_STATIC_WS_BYTES];
+
 struct vkv_ctx {
     int device;
     int debug_rows;
+    void* scratch_ptr;     // this device's address of `scratch`
     double* gram;          // [1024] device scratch for the contractivity check
     int timing;            // vkv_step_run records events around its score launch
     hipEvent_t* tev;       // [2 * TIMING_SLOTS] start/end events of timed score launches
@@ -350,6 +357,11 @@ int vkv_create(vkv_ctx** out, int device) {
     vkv_ctx* c = (vkv_ctx*)calloc(1, sizeof(vkv_ctx));
     if (!c) return fail(nullptr, VKV_E_ARG, "out of host memory");
     c->device = device;
+    e = hipGetSymbolAddress(&c->scratch_ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !c->scratch_ptr) {
+        free(c);
+        return fail(nullptr, VKV_E_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    }
     const char* dbg = getenv("VKV_DEBUG_ROWS");
     c->debug_rows = (dbg && dbg[0] && strcmp(dbg, "0") != 0) ? 1 : 0;
     e = hipMalloc(&c->gram, 1024 * sizeof(double));
@@ -658,6 +670,27 @@ int vkv_step_run(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, in
     if ((rc = debug_check_sel(ctx, st, k, sel, s))) return rc;
     if (two_tier) return debug_check_adm(ctx, st, k, sel, adm, adm_count, cap, s);
     return VKV_OK;
+}
+
+int vkv_step_run_static(vkv_ctx* ctx, const vkv_step* st, int64_t k, float* key, float* ub, int32_t* sel,
+                        double* theta, int32_t* adm, int32_t* adm_count, int64_t cap, float cert_mult, float scale,
+                        uint16_t* out, float* lse, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    int rc = check_step(ctx, st);
+    if (rc) return rc;
+    const int64_t A = st->T - st->W;
+    if (k < 0 || k > A) return fail(ctx, VKV_E_ARG, "k=%lld outside [0, A=%lld]", (long long)k, (long long)A);
+    const int64_t acap = adm_count ? cap : 0;
+    if (acap < 0 || acap > A) return fail(ctx, VKV_E_ARG, "cap=%lld outside [0, A]", (long long)cap);
+    const size_t need = layout(st, k, acap).total;
+    if (need > (size_t)VKV_STATIC_WS_BYTES)
+        return fail(ctx, VKV_E_WORKSPACE,
+                    "this step needs a workspace of %zu bytes; vkv_step_run_static has %zu (use vkv_step_run with a "
+                    "caller workspace)",
+                    need, (size_t)VKV_STATIC_WS_BYTES);
+    (void)hipSetDevice(ctx->device);
+    return vkv_step_run(ctx, st, ctx->scratch_ptr, (size_t)VKV_STATIC_WS_BYTES, k, key, ub, sel, theta, adm, adm_count,
+                        cap, cert_mult, scale, out, lse, stream);
 }
 
 int vkv_check_rows(vkv_ctx* ctx, const vkv_step* st, int64_t k, const int32_t* sel, const int32_t* adm,
