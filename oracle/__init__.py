@@ -75,6 +75,18 @@ def _load():
         lib.vkvref_attend.argtypes = [P, P, i64, P, i64, P, i64, ctypes.c_double, P, P, i32]
         lib.vkvref_full_scores.restype = i32
         lib.vkvref_full_scores.argtypes = [P, P, i64, P, i64, i64, P, i32]
+        lib.vkvref_conformal_z.restype = i32
+        lib.vkvref_conformal_z.argtypes = [P, i64, i64, i64, ctypes.c_double, P, P, P]
+        lib.vkvref_row_max.restype = i32
+        lib.vkvref_row_max.argtypes = [P, P, i64, P, i64, P, i64, P, P]
+        lib.vkvref_trigger_margins.restype = i32
+        lib.vkvref_trigger_margins.argtypes = [P, i64, i32, P, P, P, P, i64, P, P, P, i64, ctypes.c_double,
+                                               P, P, i32]
+        lib.vkvref_fire.restype = i64
+        lib.vkvref_fire.argtypes = [P, i64, P, i64, i64, P, i64]
+        lib.vkvref_required_inflation.restype = i32
+        lib.vkvref_required_inflation.argtypes = [P, i64, i32, P, P, P, P, i64, P, P, P, i64, P, i64, i32, P,
+                                                  P, P, P]
         lib.vkvref_max_threads.restype = i32
         lib.vkvref_max_threads.argtypes = []
         _lib = lib
@@ -249,6 +261,90 @@ def admit(ub: np.ndarray, sel: np.ndarray, theta: float, cap: int | None = None)
     cnt = _load().vkvref_admit(_ptr(ub) if A else None, A, _ptr(sel) if sel.size else None,
                                sel.shape[0], float(theta), _ptr(adm), int(cap))
     return adm[:min(cnt, cap)].copy(), int(cnt)
+
+
+# ------------------------------------------------------- calibrated trigger
+
+def conformal_z(zq, tau=(9, 10), zmax: float = 8.0):
+    """z from the required inflations of the hard calibration queries (Sec. 4.2,
+    the z paragraph; the closed-form chain of Sec. 5.2).  tau is a rational
+    (numerator, denominator).  Returns (z, min_hard, k) with k = 0 when z is
+    the Z_max clamp."""
+    zq = np.ascontiguousarray(zq, np.float64)
+    z = ctypes.c_double(0.0)
+    mh = ctypes.c_int64(0)
+    k = ctypes.c_int64(0)
+    rc = _load().vkvref_conformal_z(_ptr(zq) if zq.size else None, zq.size, int(tau[0]), int(tau[1]),
+                                    float(zmax), ctypes.addressof(z), ctypes.addressof(mh),
+                                    ctypes.addressof(k))
+    if rc != 0:
+        raise ValueError("tau must be a rational in (0, 1)")
+    return float(z.value), int(mh.value), int(k.value)
+
+
+def row_max(q_lat_seq, q_rope_seq, cache_seq, rows):
+    """Per head: (max exact full score over ``rows``, the row attaining it,
+    lower index on ties) -- the tier-1 max logit s*_h of Sec. 4.2."""
+    q_lat_seq = _u16(q_lat_seq)
+    q_rope_seq = _u16(q_rope_seq)
+    cache_seq = _u16(cache_seq)
+    rows = np.ascontiguousarray(rows, np.int32)
+    H = q_lat_seq.shape[0]
+    smax = np.zeros(H, np.float64)
+    arg = np.zeros(H, np.int32)
+    _load().vkvref_row_max(_ptr(q_lat_seq), _ptr(q_rope_seq), H, _ptr(cache_seq), cache_seq.shape[1],
+                           _ptr(rows) if rows.size else None, rows.size, _ptr(smax), _ptr(arg))
+    return smax, arg
+
+
+def trigger_margins(qt_seq, a, nq, e, x, eta, eps, gam, A: int, smax, cert_mult: float,
+                    nthreads: int = 0) -> np.ndarray:
+    """margin_u = max_h (UB_h(u) - s*_h) over the archived rows (Eq. (trigger)
+    against the per-head tier-1 maximum)."""
+    qt_seq = _u16(qt_seq)
+    x = _u16(x)
+    H, n = qt_seq.shape
+    f = lambda v: np.ascontiguousarray(v, np.float32)
+    a, nq, e, eta, eps, gam = map(f, (a, nq, e, eta, eps, gam))
+    smax = np.ascontiguousarray(smax, np.float64)
+    m = np.zeros(max(A, 1), np.float64)
+    _load().vkvref_trigger_margins(_ptr(qt_seq), H, n, _ptr(a), _ptr(nq), _ptr(e), _ptr(x), x.shape[1],
+                                   _ptr(eta), _ptr(eps), _ptr(gam), int(A), float(cert_mult), _ptr(smax),
+                                   _ptr(m), int(nthreads))
+    return m[:A]
+
+
+def fire(margin, sel, topj: int = 0, cap: int | None = None):
+    """The fired rows (outside S, margin > 0), ascending, capped to the topj
+    largest margins when topj > 0.  Returns (rows, count)."""
+    margin = np.ascontiguousarray(margin, np.float64)
+    sel = np.ascontiguousarray(sel, np.int32)
+    A = margin.shape[0]
+    if cap is None:
+        cap = A
+    out = np.zeros(max(cap, 1), np.int32)
+    cnt = _load().vkvref_fire(_ptr(margin) if A else None, A, _ptr(sel) if sel.size else None, sel.size,
+                              int(topj), _ptr(out), int(cap))
+    return out[:min(cnt, cap)].copy(), int(cnt)
+
+
+def required_inflation(qt_seq, a, nq, e, x, eta, eps, gam, A: int, sel, r: int, tier1_max, argmax):
+    """Per head: (hard flag, z_q) of one calibration query (Sec. 4.2)."""
+    qt_seq = _u16(qt_seq)
+    x = _u16(x)
+    H, n = qt_seq.shape
+    f = lambda v: np.ascontiguousarray(v, np.float32)
+    a, nq, e, eta, eps, gam = map(f, (a, nq, e, eta, eps, gam))
+    sel = np.ascontiguousarray(sel, np.int32)
+    t1 = np.ascontiguousarray(tier1_max, np.float64)
+    am = np.ascontiguousarray(argmax, np.int32)
+    hard = np.zeros(H, np.int32)
+    zq = np.zeros(H, np.float64)
+    _load().vkvref_required_inflation(_ptr(qt_seq), H, n, _ptr(a), _ptr(nq), _ptr(e), _ptr(x), x.shape[1],
+                                      _ptr(eta), _ptr(eps), _ptr(gam), int(A),
+                                      _ptr(sel) if sel.size else None, sel.size, int(r), _ptr(t1),
+                                      _ptr(am), _ptr(hard), _ptr(zq))
+    return hard.astype(bool), zq
 
 
 def attend(q_lat_seq, q_rope_seq, cache_seq, rows, scale: float, nthreads: int = 0):

@@ -384,6 +384,194 @@ int64_t vkvref_admit(const double* ub, int64_t A, const int32_t* sel, int64_t k,
     return cnt;
 }
 
+/* ------------------------------------------------ calibrated trigger (z) */
+
+/* The conformal quantile of Sec. 4.2 (the z paragraph) with the closed-form
+ * chain of Sec. 5.2 (Recommended configuration), from the single recall
+ * target tau = tau_num / tau_den (a rational, so that the integer quantities
+ * below are exact):
+ *   alpha    = (1 - tau) / 2                 the gate's false-close budget
+ *   tau_s    = tau / (1 - alpha) = 2 tau_num / (tau_den + tau_num)
+ *   min_hard = ceil(tau_s / (1 - tau_s)) = ceil(2 tau_num / (tau_den - tau_num))
+ *   k        = ceil((n + 1) tau_s)           1-based rank in the sorted zq
+ *   z        = zq_(k), clamped to [0, zmax]
+ * With fewer than min_hard hard calibration queries (or k > n) the quantile
+ * does not exist and z = zmax (reading: the conservative end of the clamp).
+ * Returns 0 and writes z, min_hard and k (k = 0 when z is the clamp). */
+int vkvref_conformal_z(const double* zq, int64_t n, int64_t tau_num, int64_t tau_den, double zmax, double* z,
+                       int64_t* min_hard, int64_t* rank) {
+    if (tau_num <= 0 || tau_den <= tau_num) return -1;
+    const int64_t mh = (2 * tau_num + (tau_den - tau_num) - 1) / (tau_den - tau_num);
+    const int64_t k = ((n + 1) * 2 * tau_num + (tau_den + tau_num) - 1) / (tau_den + tau_num);
+    *min_hard = mh;
+    if (n < mh || k > n || k < 1) {
+        *z = zmax;
+        *rank = 0;
+        return 0;
+    }
+    double* v = (double*)malloc(sizeof(double) * (size_t)n);
+    memcpy(v, zq, sizeof(double) * (size_t)n);
+    /* insertion sort: n is a calibration window (tens to a few thousand) */
+    for (int64_t i = 1; i < n; ++i) {
+        double x = v[i];
+        int64_t j = i - 1;
+        while (j >= 0 && v[j] > x) {
+            v[j + 1] = v[j];
+            --j;
+        }
+        v[j + 1] = x;
+    }
+    double q = v[k - 1];
+    free(v);
+    if (q > zmax) q = zmax;
+    if (!(q > 0.0)) q = 0.0;   /* reading: an inflation, never a deflation */
+    *z = q;
+    *rank = k;
+    return 0;
+}
+
+/* Exact full score of one row for one head (Sec. 3, Eq. (setup), unscaled):
+ * latent dims 0..511 then branch dims 0..63, fp64 sequential from +0. */
+static double full_score(const uint16_t* ql, const uint16_t* qr, const uint16_t* row) {
+    double acc = 0.0;
+    for (int i = 0; i < D_LAT; ++i) acc = fma(vkvref_bf16_to_f64(ql[i]), vkvref_bf16_to_f64(row[i]), acc);
+    for (int i = 0; i < D_ROPE; ++i) acc = fma(vkvref_bf16_to_f64(qr[i]), vkvref_bf16_to_f64(row[D_LAT + i]), acc);
+    return acc;
+}
+
+/* Per head h: the maximum over the listed rows of the exact full score
+ * s_h(u) and the row attaining it (ties: the lower row index).  With the
+ * attended tier-1 rows this is the trigger threshold s*_h (the tier-1 max
+ * logit of Sec. 4.2 and its figure); with every row of the context it gives
+ * the causal argmax row of a calibration query.  N = 0: -inf and -1. */
+int vkvref_row_max(const uint16_t* q_lat, const uint16_t* q_rope, int64_t H, const uint16_t* cache_seq,
+                   int64_t row_stride, const int32_t* rows, int64_t N, double* smax, int32_t* argmax) {
+    for (int64_t h = 0; h < H; ++h) {
+        double best = -INFINITY;
+        int32_t arg = -1;
+        for (int64_t j = 0; j < N; ++j) {
+            const int32_t u = rows[j];
+            const double s = full_score(q_lat + h * D_LAT, q_rope + h * D_ROPE, cache_seq + (int64_t)u * row_stride);
+            if (s > best || (s == best && u < arg)) {
+                best = s;
+                arg = u;
+            }
+        }
+        smax[h] = best;
+        argmax[h] = arg;
+    }
+    return 0;
+}
+
+/* Trigger margins of the archived rows (Eq. (trigger) against the tier-1
+ * maximum, per head, fired if any head's bound exceeds its threshold):
+ *   margin_u = max_h fl64( fl64(s^_h(u) + B_h(u)) - s*_h ),  B_h as in
+ *   vkvref_upper_bounds with a'_h = ru_f32(cert_mult * a_h).
+ * margin_u > 0 iff some head has UB_h(u) > s*_h (an fp64 difference of two
+ * doubles is positive exactly when the first is larger). */
+int vkvref_trigger_margins(const uint16_t* qt, int64_t H, int n, const float* a, const float* nq,
+                           const float* e, const uint16_t* x, int64_t x_stride, const float* eta,
+                           const float* eps, const float* gam, int64_t A, double cert_mult,
+                           const double* smax, double* margin, int nthreads) {
+    double* q = (double*)malloc(sizeof(double) * (size_t)(H * n));
+    float* as = (float*)malloc(sizeof(float) * (size_t)(H > 0 ? H : 1));
+    for (int64_t i = 0; i < H * n; ++i) q[i] = vkvref_bf16_to_f64(qt[i]);
+    for (int64_t h = 0; h < H; ++h) as[h] = vkvref_ru_f32(cert_mult * (double)a[h]);
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(static)
+#endif
+    for (int64_t u = 0; u < A; ++u) {
+        double xv[D_ROW];
+        for (int d = 0; d < n; ++d) xv[d] = vkvref_bf16_to_f64(x[u * x_stride + d]);
+        double best = -INFINITY;
+        for (int64_t h = 0; h < H; ++h) {
+            const double* qh = q + h * n;
+            double acc = 0.0;
+            for (int d = 0; d < n; ++d) acc = fma(qh[d], xv[d], acc);
+            double bh = fma((double)as[h], (double)eta[u],
+                            fma((double)nq[h], (double)eps[u], (double)e[h] * (double)gam[u]));
+            double m = (acc + bh) - smax[h];
+            if (m > best) best = m;
+        }
+        margin[u] = best;
+    }
+    free(as);
+    free(q);
+    return 0;
+}
+
+/* The fired set: rows of [0, A) outside S with margin > 0, ascending; with
+ * topj > 0 only the topj of them with the largest margins (ties: the lower
+ * row index) -- the optional budgeted cap of Sec. 4.3 / the appendix's
+ * deployment specification.  Returns the number fired (after the cap);
+ * writes at most cap rows. */
+static int cmp_fire(const void* pa, const void* pb) {
+    const kv_t* a = (const kv_t*)pa;
+    const kv_t* b = (const kv_t*)pb;
+    if (a->key > b->key) return -1;
+    if (a->key < b->key) return 1;
+    return (a->idx < b->idx) ? -1 : (a->idx > b->idx);
+}
+
+int64_t vkvref_fire(const double* margin, int64_t A, const int32_t* sel, int64_t k, int64_t topj, int32_t* fired,
+                    int64_t cap) {
+    char* in = (char*)calloc((size_t)(A > 0 ? A : 1), 1);
+    for (int64_t i = 0; i < k; ++i) in[sel[i]] = 1;
+    kv_t* v = (kv_t*)malloc(sizeof(kv_t) * (size_t)(A > 0 ? A : 1));
+    int64_t nf = 0;
+    for (int64_t u = 0; u < A; ++u)
+        if (!in[u] && margin[u] > 0.0) {
+            v[nf].key = margin[u];
+            v[nf].idx = (int32_t)u;
+            ++nf;
+        }
+    if (topj > 0 && nf > topj) {
+        qsort(v, (size_t)nf, sizeof(kv_t), cmp_fire);
+        nf = topj;
+    }
+    int32_t* out = (int32_t*)malloc(sizeof(int32_t) * (size_t)(nf > 0 ? nf : 1));
+    for (int64_t i = 0; i < nf; ++i) out[i] = v[i].idx;
+    qsort(out, (size_t)nf, sizeof(int32_t), cmp_int);
+    for (int64_t i = 0; i < nf && i < cap; ++i) fired[i] = out[i];
+    free(out);
+    free(v);
+    free(in);
+    return nf;
+}
+
+/* Required inflation of one calibration query for head h (the z paragraph of
+ * Sec. 4.2): with u* = the causal argmax row over the whole context,
+ * the query is hard for h when u* is archived and outside the tier-1 set;
+ * then z_q = (s*_h - idx_h(u*)) / cert_h(u*) with
+ *   idx_h(u)  = fl64(s^_h(u) + fma(n_h, eps_u, e_h gam_u))   (the index score with its rounding slack)
+ *   cert_h(u) = a_h eta_u / sqrt(d_c - r)                       (the per-dimension certificate scale)
+ * so that the trigger score idx + z cert reaches s*_h exactly at z = z_q.
+ * Writes hard[h] (0/1) and zq[h] (+inf when cert = 0 and s* > idx). */
+int vkvref_required_inflation(const uint16_t* qt, int64_t H, int n, const float* a, const float* nq,
+                              const float* e, const uint16_t* x, int64_t x_stride, const float* eta,
+                              const float* eps, const float* gam, int64_t A, const int32_t* sel, int64_t k,
+                              int r, const double* tier1_max, const int32_t* argmax, int32_t* hard, double* zq) {
+    const double scale = sqrt((double)(D_LAT - r));
+    for (int64_t h = 0; h < H; ++h) {
+        const int32_t u = argmax[h];
+        int in_s = 0;
+        for (int64_t i = 0; i < k; ++i)
+            if (sel[i] == u) in_s = 1;
+        hard[h] = (u >= 0 && u < A && !in_s) ? 1 : 0;
+        zq[h] = 0.0;
+        if (!hard[h]) continue;
+        double acc = 0.0;
+        for (int d = 0; d < n; ++d)
+            acc = fma(vkvref_bf16_to_f64(qt[h * n + d]), vkvref_bf16_to_f64(x[(int64_t)u * x_stride + d]), acc);
+        const double idx = acc + fma((double)nq[h], (double)eps[u], (double)e[h] * (double)gam[u]);
+        const double cert = (double)a[h] * (double)eta[u] / scale;
+        const double gap = tier1_max[h] - idx;
+        zq[h] = cert > 0.0 ? gap / cert : (gap > 0.0 ? INFINITY : -INFINITY);
+    }
+    return 0;
+}
+
 /* ---------------------------------------------------------------- attend */
 
 /* Exact softmax attention of every head over the multiset of rows listed in

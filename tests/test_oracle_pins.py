@@ -622,3 +622,127 @@ def test_cert_mult_one_is_the_sound_bound_and_admission_is_monotone(oracle_mod):
     slack = (nq[0].max() * eps[0, :A].max() + e[0].max() * gam[0, :A].max()) * 1.001
     assert np.all(key[adm0] > theta - slack)
     assert len(adm0) < len(outside)
+
+
+# --------------------------------------------------- calibrated trigger (z)
+
+def test_conformal_chain_from_the_recall_target(oracle_mod):
+    """tau = 0.90 gives alpha = 0.05, tau_s = 18/19 and min_hard = 18 (Sec. 5.2);
+    z is the ceil((n+1) tau_s)-th smallest required inflation, clamped to Z_max."""
+    zq = np.arange(1, 19, dtype=np.float64) * 0.25          # 18 hand-made scores 0.25 .. 4.5
+    z, mh, k = oracle_mod.conformal_z(zq)
+    assert mh == 18 and k == math.ceil(19 * Fraction(18, 19)) == 18 and z == 4.5
+    z, mh, k = oracle_mod.conformal_z(zq[:17])              # one short of min_hard: the clamp
+    assert (z, k) == (8.0, 0)
+    zq = rng.permutation(np.linspace(0.1, 3.7, 37))
+    z, _, k = oracle_mod.conformal_z(zq)
+    assert k == math.ceil(38 * Fraction(18, 19)) == 36 and z == np.sort(zq)[35]
+    z, _, k = oracle_mod.conformal_z(np.full(100, 9.5))      # above Z_max
+    assert k == 96 and z == 8.0
+    z, _, _ = oracle_mod.conformal_z(np.full(30, -2.0))      # an inflation, never a deflation
+    assert z == 0.0
+    # another target: tau = 4/5 -> alpha = 1/10, tau_s = 8/9, min_hard = 8
+    z, mh, k = oracle_mod.conformal_z(np.arange(8.0), tau=(4, 5))
+    assert mh == 8 and k == 8 and z == 7.0
+
+
+def test_conformal_z_covers_a_fresh_query_at_tau_s(oracle_mod):
+    """Exchangeability alone: for i.i.d. required inflations, a fresh hard
+    query's z_q <= z with probability >= tau_s (here 18/19, n = 30)."""
+    r = np.random.default_rng(99)
+    trials, n, hit = 4000, 30, 0
+    for _ in range(trials):
+        v = r.standard_normal(n + 1) + 2.0
+        z, _, k = oracle_mod.conformal_z(v[:n], zmax=1e9)
+        hit += v[n] <= z
+    # k = ceil(31 * 18/19) = 30 of 30: coverage (k)/(n+1) = 30/31 >= 18/19
+    assert hit / trials >= 18 / 19 - 3 * math.sqrt((18 / 19) * (1 / 19) / trials)
+
+
+def test_row_max_is_exact_with_ties_to_the_lower_row(oracle_mod):
+    H, T = 3, 60
+    lat = small_int_bf16((T, 512), -2, 2)
+    rope = small_int_bf16((T, 64), -2, 2)
+    cache = np.concatenate([lat, rope], 1)
+    cache[40] = cache[11]                                   # a tie: rows 11 and 40
+    ql = small_int_bf16((H, 512), -2, 2)
+    qr = small_int_bf16((H, 64), -2, 2)
+    rows = np.array([40, 11, 3, 59, 27], np.int32)
+    smax, arg = oracle_mod.row_max(ql, qr, cache, rows)
+    S = dec(cache[rows]) @ np.concatenate([dec(ql), dec(qr)], 1).T   # exact (small integers)
+    for h in range(H):
+        best = S[:, h].max()
+        assert smax[h] == best
+        assert arg[h] == min(int(u) for u, v in zip(rows, S[:, h]) if v == best)
+    smax, arg = oracle_mod.row_max(ql, qr, cache, np.zeros(0, np.int32))
+    assert np.all(np.isneginf(smax)) and np.all(arg == -1)
+
+
+def test_trigger_with_one_threshold_is_the_admission_rule(oracle_mod):
+    """With s*_h = theta for every head, margin_u > 0 iff UB_u > theta: the
+    fired set (uncapped) equals the certified admission bit for bit, at the
+    sound multiplier and at a calibrated one."""
+    wl, cache, q_lat, q_rope, index, eta, eps, gam, qt, a, nq, e, x = _tiny_two_tier(
+        oracle_mod, basis="orthonormal", r=64, T=900, W=30, H=8, needles=4)
+    A = wl["A"]
+    key, _ = oracle_mod.index_keys(qt[0], x, A)
+    sel, theta = oracle_mod.select(key, 40)
+    for cm in (1.0, 0.1):
+        ub = oracle_mod.upper_bounds(qt[0], a[0], nq[0], e[0], x, eta[0], eps[0], gam[0], A, cert_mult=cm)
+        adm, cnt = oracle_mod.admit(ub, sel, theta)
+        m = oracle_mod.trigger_margins(qt[0], a[0], nq[0], e[0], x, eta[0], eps[0], gam[0], A,
+                                       np.full(8, theta), cm)
+        fired, fc = oracle_mod.fire(m, sel)
+        assert fc == cnt and np.array_equal(fired, adm)
+
+
+def test_trigger_margins_per_head_and_topj(oracle_mod):
+    """margin_u = max_h (UB_h(u) - s*_h) against per-head UB_h from the
+    single-head bound; the top-j cap keeps the j largest margins (ties to
+    the lower row), ascending."""
+    wl, cache, q_lat, q_rope, index, eta, eps, gam, qt, a, nq, e, x = _tiny_two_tier(
+        oracle_mod, basis="orthonormal", r=32, T=500, W=20, H=5, needles=3)
+    A = wl["A"]
+    smax = np.array([30.0, 25.0, 41.0, 10.0, 33.0])
+    cm = 0.2
+    m = oracle_mod.trigger_margins(qt[0], a[0], nq[0], e[0], x, eta[0], eps[0], gam[0], A, smax, cm)
+    per = np.stack([oracle_mod.upper_bounds(qt[0, h:h + 1], a[0, h:h + 1], nq[0, h:h + 1], e[0, h:h + 1],
+                                            x, eta[0], eps[0], gam[0], A, cert_mult=cm) - smax[h]
+                    for h in range(5)], 1)
+    assert np.array_equal(m, per.max(1))
+    sel = np.sort(rng.choice(A, 12, replace=False)).astype(np.int32)
+    fired, cnt = oracle_mod.fire(m, sel)
+    want = [u for u in range(A) if u not in set(sel) and m[u] > 0]
+    assert cnt == len(want) and list(fired) == want and cnt > 16
+    top, tc = oracle_mod.fire(m, sel, topj=16)
+    order = sorted(want, key=lambda u: (-m[u], u))[:16]
+    assert tc == 16 and list(top) == sorted(order)
+
+
+def test_required_inflation_is_where_the_target_starts_to_fire(oracle_mod):
+    """For a hard (query, head), the trigger with cert_mult = z_q / sqrt(d_c - r)
+    (times 1 + 1e-6) fires the causal argmax row for that head, and times
+    1 - 1e-6 it does not: z_q is exactly the required inflation."""
+    r = 32
+    wl, cache, q_lat, q_rope, index, eta, eps, gam, qt, a, nq, e, x = _tiny_two_tier(
+        oracle_mod, basis="orthonormal", r=r, T=700, W=20, H=6, needles=0)
+    A, T = wl["A"], wl["T"]
+    key, _ = oracle_mod.index_keys(qt[0], x, A)
+    sel, _ = oracle_mod.select(key, 20)
+    tier1 = np.concatenate([sel, np.arange(A, T, dtype=np.int32)])
+    s1, _ = oracle_mod.row_max(q_lat[0], q_rope[0], cache[0], tier1)
+    _, am = oracle_mod.row_max(q_lat[0], q_rope[0], cache[0], np.arange(T, dtype=np.int32))
+    hard, zq = oracle_mod.required_inflation(qt[0], a[0], nq[0], e[0], x, eta[0], eps[0], gam[0], A, sel, r,
+                                             s1, am)
+    assert hard.sum() >= 3
+    for h in np.nonzero(hard)[0]:
+        assert am[h] < A and am[h] not in set(sel)
+        assert np.isfinite(zq[h])
+        u = int(am[h])
+        for f, fires in ((1 + 1e-6, True), (1 - 1e-6, False)):
+            cm = zq[h] / math.sqrt(512 - r) * f
+            if cm < 0:
+                continue
+            m = oracle_mod.trigger_margins(qt[0, h:h + 1], a[0, h:h + 1], nq[0, h:h + 1], e[0, h:h + 1], x,
+                                           eta[0], eps[0], gam[0], A, s1[h:h + 1], cm)
+            assert (m[u] > 0) == fires, (h, f, m[u])
