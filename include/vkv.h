@@ -245,6 +245,85 @@ int vkv_step_run(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, in
                  int32_t* adm_count, int64_t cap, float cert_mult, float scale, uint16_t* out,
                  float* lse, void* stream);
 
+/* ------------------------------------------------- the calibrated trigger */
+
+/*
+ * Per head, the maximum over a row list of the exact full score (Sec. 3,
+ * Eq. (setup), unscaled; fp64 over the 576 dims, latent then branch) and the
+ * row attaining it, ties to the lower row index.  Over the attended tier-1
+ * rows (sel[b] and the recent window) it is the trigger threshold s*_h, the
+ * tier-1 maximum logit of Sec. 4.2 (its figure: attention max logit s*); over
+ * every row of the context it is the causal argmax row of a calibration query.
+ *   rows    [B, nrows] int32 (each list in [0, A)), or NULL for the whole archive [0, A)
+ *   add_recent != 0: the recent window [A, T) is part of the list
+ *   smax    [B, H] fp64 (-inf for an empty list), argmax [B, H] int32 (-1 then)
+ * bf16 MFMA screening with a certified band, fp64 for the rows that can hold
+ * the maximum: bit for bit the fp64 definition.
+ */
+int vkv_row_max(vkv_ctx* ctx, const vkv_step* st, const int32_t* rows, int64_t nrows,
+                int32_t add_recent, double* smax, int32_t* argmax, void* stream);
+
+/*
+ * The calibrated trigger (Sec. 4.2, Eq. (trigger): fetch the archived rows
+ * whose trigger score exceeds the tier-1 maximum; the optional top-j cap of
+ * Sec. 4.3 and the deployment specification's request lifecycle):
+ *   fired_b = { u in [0, A) \ S_b : UB_h(u) > s*_h for some h },
+ *   UB_h(u) = fl64( s^_h(u) + fma(a'_h, eta_u, fma(n_h, eps_u, e_h gam_u)) ),
+ *   a'_h = the smallest float >= cert_mult * a_h,  cert_mult = z / sqrt(d_c - r),
+ * with smax = s*_h [B, H] fp64 (vkv_row_max over S and the recent window).
+ * With topj > 0 only the topj fired rows of largest margin max_h (UB_h - s*_h)
+ * are kept (ties: the lower row).  fired [B, cap] int32 ascending, fired_count
+ * [B] = the number kept (may exceed cap; then cap rows are written).  Needs
+ * the step's vkv_query_prep / vkv_score (with ub, the same cert_mult for the
+ * band shortcut) / vkv_select on ws.  Decisions are exact: rows the fp32
+ * bound cannot decide get fp64 margins.  The fired rows attend as the
+ * admitted rows of vkv_attend.  May be repeated on the same ws.
+ */
+int vkv_trigger(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k,
+                const int32_t* sel, const float* ub, float cert_mult, const double* smax,
+                int64_t topj, int32_t* fired, int32_t* fired_count, int64_t cap, void* stream);
+
+/*
+ * Calibration statistic of the trigger (Sec. 4.2, the z paragraph): for each
+ * calibration query b (a sequence of the step: one query of the request
+ * against its context) and head h, with u* = argmax[b, h] the causal argmax
+ * row (vkv_row_max over the whole context) and s*_h = tier1_max[b, h]:
+ *   hard[b, h] = u* is archived and not in sel[b]
+ *   zq[b, h]   = (s*_h - idx_h(u*)) / cert_h(u*)  for hard pairs, else 0, with
+ *   idx_h(u) = fl64(s^_h(u) + fma(n_h, eps_u, e_h gam_u)),  cert_h(u) = a_h eta_u / sqrt(d_c - r)
+ * the inflation at which the trigger score of u* reaches s*_h.  Needs the
+ * step's vkv_query_prep on ws.  hard [B, H] int32, zq [B, H] fp64.
+ */
+int vkv_required_inflation(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k,
+                           const int32_t* sel, const double* tier1_max, const int32_t* argmax,
+                           int32_t* hard, double* zq, void* stream);
+
+/*
+ * The conformal quantile (Sec. 4.2, the z paragraph; Sec. 5.2, the closed-form
+ * chain from the recall target tau = tau_num / tau_den, e.g. 9 / 10):
+ *   alpha = (1 - tau) / 2,  tau_s = tau / (1 - alpha),
+ *   min_hard = ceil(tau_s / (1 - tau_s)),  k = ceil((n + 1) tau_s),
+ *   z = the k-th smallest of zq[0 .. n), clamped to [0, zmax]; z = zmax when
+ *   n < min_hard or k > n (the quantile does not exist).
+ * HOST pointers: zq (the z_q of the hard pairs), z, min_hard, rank (= k, or 0
+ * when z is the clamp).  A host-side order statistic; no device work.
+ */
+int vkv_conformal_z(const double* zq, int64_t n, int64_t tau_num, int64_t tau_den, double zmax,
+                    double* z, int64_t* min_hard, int64_t* rank);
+
+/*
+ * One step with the calibrated trigger in place of the admission:
+ * query_prep -> score (with ub at cert_mult) -> select -> vkv_row_max over
+ * S and the recent window (smax, argmax [B, H]: caller buffers, written) ->
+ * vkv_trigger -> attend over S, the recent window and the fired rows (the
+ * fetched rows join the softmax as exact copies, Lemma (Exchangeability)).
+ */
+int vkv_step_run_trigger(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k,
+                         float* key, float* ub, int32_t* sel, double* theta, float cert_mult,
+                         double* smax, int32_t* argmax, int64_t topj, int32_t* fired,
+                         int32_t* fired_count, int64_t cap, float scale, uint16_t* out, float* lse,
+                         void* stream);
+
 /*
  * For callers that cannot allocate device memory: code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc.  The same step

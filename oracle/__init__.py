@@ -416,3 +416,32 @@ def step(cache, q_lat, q_rope, index, P, r: int, mode: int, W: int, k: int, scal
         res["lse"][b] = lse
         res["key"][b] = key
     return res
+
+
+def step_trigger(cache, q_lat, q_rope, index, P, r: int, mode: int, W: int, k: int, scale: float,
+                 eta, eps, gam, cert_mult: float, topj: int = 0, seqs=None, index_has_rope: bool = True,
+                 nthreads: int = 0):
+    """One decode step with the calibrated trigger (Sec. 4.2): keys -> top-k ->
+    s*_h over S and the recent window -> fired rows (some head's bound above
+    its threshold; top-j cap) -> attention over S, the window and the fired
+    rows.  Returns per-sequence results."""
+    cache = _u16(cache)
+    B, T, _ = cache.shape
+    A = T - W
+    qt, a, nq, e = query_prep(q_lat, q_rope, P, r, mode)
+    res = {key: {} for key in ("sel", "theta", "smax", "argmax", "fired", "fired_count", "out", "lse",
+                               "margin")}
+    for b in (range(B) if seqs is None else seqs):
+        x = index_rows(cache[b], None if index is None else index[b], mode, r, index_has_rope)
+        key, _ = index_keys(qt[b], x, A, nthreads=nthreads)
+        sel, theta = select(key, k)
+        tier1 = np.concatenate([sel, np.arange(A, T, dtype=np.int32)])
+        smax, arg = row_max(q_lat[b], q_rope[b], cache[b], tier1)
+        m = trigger_margins(qt[b], a[b], nq[b], e[b], x, eta[b], eps[b], gam[b], A, smax, cert_mult, nthreads)
+        fired, cnt = fire(m, sel, topj)
+        rows = attend_list(sel, A, T, fired)
+        out, lse = attend(q_lat[b], q_rope[b], cache[b], rows, scale, nthreads)
+        for name, v in (("sel", sel), ("theta", theta), ("smax", smax), ("argmax", arg), ("fired", fired),
+                        ("fired_count", cnt), ("out", out), ("lse", lse), ("margin", m)):
+            res[name][b] = v
+    return res

@@ -19,7 +19,8 @@ import torch  # noqa: F401  (loads the HIP runtime the library binds to)
 __all__ = [
     "VKV_MODE_ROPE", "VKV_MODE_DIGEST", "VKV_MODE_ROPE_DIGEST", "VkvError", "Context", "Step",
     "lib_path", "load", "digest_build", "workspace_size", "query_prep", "score", "select", "admit", "attend",
-    "step_run", "step_run_static", "check_rows", "exported_symbols",
+    "step_run", "step_run_static", "check_rows", "row_max", "trigger", "required_inflation", "conformal_z",
+    "step_run_trigger", "exported_symbols",
 ]
 
 VKV_MODE_ROPE, VKV_MODE_DIGEST, VKV_MODE_ROPE_DIGEST = 1, 2, 3
@@ -32,6 +33,7 @@ exported_symbols = (
     "vkv_create", "vkv_destroy", "vkv_status_string", "vkv_last_error", "vkv_version",
     "vkv_digest_build", "vkv_workspace_size", "vkv_query_prep", "vkv_score", "vkv_select", "vkv_admit",
     "vkv_attend", "vkv_step_run", "vkv_step_run_static", "vkv_check_rows", "vkv_set_timing", "vkv_score_timing",
+    "vkv_row_max", "vkv_trigger", "vkv_required_inflation", "vkv_conformal_z", "vkv_step_run_trigger",
 )
 
 
@@ -92,6 +94,12 @@ def load():
                                  f32, f32, P, P, P]
     lib.vkv_check_rows.argtypes = [P, sp, i64, P, P, P, i64, P]
     lib.vkv_step_run_static.argtypes = [P, sp, i64, P, P, P, P, P, P, i64, f32, f32, P, P, P]
+    lib.vkv_row_max.argtypes = [P, sp, P, i64, i32, P, P, P]
+    lib.vkv_trigger.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, f32, P, i64, P, P, i64, P]
+    lib.vkv_required_inflation.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P, P, P, P]
+    lib.vkv_conformal_z.argtypes = [P, i64, i64, i64, ctypes.c_double, P, P, P]
+    lib.vkv_step_run_trigger.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P, P, f32, P, P, i64, P, P, i64,
+                                         f32, P, P, P]
     lib.vkv_set_timing.argtypes = [P, ctypes.c_int]
     lib.vkv_score_timing.argtypes = [P, ctypes.POINTER(ctypes.c_float), ctypes.c_int]
     for name in exported_symbols:
@@ -99,7 +107,8 @@ def load():
     for name in ("vkv_create", "vkv_destroy", "vkv_digest_build", "vkv_workspace_size",
                  "vkv_query_prep", "vkv_score",
                  "vkv_select", "vkv_admit", "vkv_attend", "vkv_step_run", "vkv_step_run_static",
-                 "vkv_check_rows", "vkv_version",
+                 "vkv_check_rows", "vkv_version", "vkv_row_max", "vkv_trigger", "vkv_required_inflation",
+                 "vkv_conformal_z", "vkv_step_run_trigger",
                  "vkv_set_timing", "vkv_score_timing"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
@@ -273,6 +282,55 @@ def step_run_static(ctx: Context, step: Step, k: int, key: torch.Tensor, ub: Opt
                                           _ptr(theta), _ptr(adm), _ptr(adm_count), int(cap),
                                           float(cert_mult), float(scale), _ptr(out), _ptr(lse),
                                           _stream(stream)))
+
+
+def row_max(ctx: Context, step: Step, rows: Optional[torch.Tensor], add_recent: bool,
+            smax: torch.Tensor, argmax: torch.Tensor, stream=None):
+    """vkv_row_max: per head, the exact max full score over ``rows`` [B,n]
+    (None: the whole archive), plus the recent window if ``add_recent``."""
+    n = rows.shape[1] if rows is not None else 0
+    ctx.check(ctx.lib.vkv_row_max(ctx.handle, step.ref, _ptr(rows), int(n), 1 if add_recent else 0,
+                                  _ptr(smax), _ptr(argmax), _stream(stream)))
+
+
+def trigger(ctx: Context, step: Step, ws: torch.Tensor, k: int, sel: torch.Tensor, ub: torch.Tensor,
+            cert_mult: float, smax: torch.Tensor, topj: int, fired: torch.Tensor,
+            fired_count: torch.Tensor, cap: int, stream=None):
+    ctx.check(ctx.lib.vkv_trigger(ctx.handle, step.ref, _ptr(ws), ws.numel(), int(k), _ptr(sel), _ptr(ub),
+                                  float(cert_mult), _ptr(smax), int(topj), _ptr(fired), _ptr(fired_count),
+                                  int(cap), _stream(stream)))
+
+
+def required_inflation(ctx: Context, step: Step, ws: torch.Tensor, k: int, sel: torch.Tensor,
+                       tier1_max: torch.Tensor, argmax: torch.Tensor, hard: torch.Tensor, zq: torch.Tensor,
+                       stream=None):
+    ctx.check(ctx.lib.vkv_required_inflation(ctx.handle, step.ref, _ptr(ws), ws.numel(), int(k), _ptr(sel),
+                                             _ptr(tier1_max), _ptr(argmax), _ptr(hard), _ptr(zq),
+                                             _stream(stream)))
+
+
+def conformal_z(zq, tau=(9, 10), zmax: float = 8.0):
+    """vkv_conformal_z on host values; returns (z, min_hard, k)."""
+    import numpy as _np
+    lib = load()
+    v = _np.ascontiguousarray(zq, _np.float64)
+    z = ctypes.c_double(0.0)
+    mh = ctypes.c_int64(0)
+    k = ctypes.c_int64(0)
+    rc = lib.vkv_conformal_z(v.ctypes.data if v.size else None, v.size, int(tau[0]), int(tau[1]), float(zmax),
+                             ctypes.byref(z), ctypes.byref(mh), ctypes.byref(k))
+    if rc != 0:
+        raise VkvError(rc, lib.vkv_last_error(None).decode())
+    return float(z.value), int(mh.value), int(k.value)
+
+
+def step_run_trigger(ctx: Context, step: Step, ws: torch.Tensor, k: int, key, ub, sel, theta,
+                     cert_mult: float, smax, argmax, topj: int, fired, fired_count, cap: int,
+                     scale: float, out, lse, stream=None):
+    ctx.check(ctx.lib.vkv_step_run_trigger(ctx.handle, step.ref, _ptr(ws), ws.numel(), int(k), _ptr(key),
+                                           _ptr(ub), _ptr(sel), _ptr(theta), float(cert_mult), _ptr(smax),
+                                           _ptr(argmax), int(topj), _ptr(fired), _ptr(fired_count), int(cap),
+                                           float(scale), _ptr(out), _ptr(lse), _stream(stream)))
 
 
 def check_rows(ctx: Context, step: Step, k: int, sel: Optional[torch.Tensor],

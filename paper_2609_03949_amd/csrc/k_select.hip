@@ -361,6 +361,7 @@ __global__ __launch_bounds__(SEL_THREADS) void sel_count_kernel(SelectArgs a) {
 struct ExLds {
     uint16_t* qt;                 // [H][n] (qlds) -- else qt is read from global memory
     float4* hs;                   // [128] head scalars (a', n, e) for bounds
+    double* off;                  // [128] per-head thresholds subtracted (trigger)
     unsigned long long* best;     // [waves][16]
     uint32_t* list;               // [waves][64]
     uint16_t* x;                  // [waves][16 rows][n]
@@ -377,6 +378,8 @@ __device__ __forceinline__ ExLds ex_carve(uint8_t* lds, int H, int n) {
     o = (o + 15) & ~(size_t)15;
     e.hs = reinterpret_cast<float4*>(lds + o);
     o += 128 * 16;
+    e.off = reinterpret_cast<double*>(lds + o);
+    o += 128 * 8;
     e.best = reinterpret_cast<unsigned long long*>(lds + o);
     o += RES_WAVES * 16 * 8;
     e.list = reinterpret_cast<uint32_t*>(lds + o);
@@ -425,9 +428,9 @@ __device__ __forceinline__ float scaled_a(float cm, float ah) { return ru_f32((d
 // (row, head) pair gets its fp64 chain (d ascending from +0) from one lane,
 // and the row's exact value is the maximum over its pairs.  margin = +inf
 // evaluates every head exactly.
-template <bool UB>
+template <bool UB, bool OFF = false>
 __device__ __forceinline__ void exact_keys_block(const SelectArgs& a, int b, int64_t namb, const int32_t* amb, uint64_t* ak,
-                                 const ExLds& L, float margin) {
+                                 const ExLds& L, float margin, int blk = 0, int nblks = 1) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4, c = lane & 15;
     const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
     const int n8 = a.n / 8;
@@ -452,6 +455,7 @@ __device__ __forceinline__ void exact_keys_block(const SelectArgs& a, int b, int
         const float ax = scaled_a(a.cert_mult, hs.x);
         L.hs[tid] = make_float4(ax, hs.y, hs.z, hs.w);
     }
+    if (OFF && tid < a.H) L.off[tid] = a.smax[(int64_t)b * a.H + tid];
     lds_barrier();
     if (wave < L.nwx && namb > 0) {
         const uint16_t* qsrc = L.qlds ? L.qt : qtb;
@@ -459,7 +463,7 @@ __device__ __forceinline__ void exact_keys_block(const SelectArgs& a, int b, int
         uint16_t* sx = L.x + (size_t)wave * 16 * a.n;
         unsigned long long* best = L.best + wave * 16;
         const int KS = a.n / 32, HT = (a.H + 15) / 16;
-        for (int64_t t0 = (int64_t)wave * 16; t0 < namb; t0 += (int64_t)L.nwx * 16) {
+        for (int64_t t0 = ((int64_t)blk * L.nwx + wave) * 16; t0 < namb; t0 += (int64_t)nblks * L.nwx * 16) {
             const int64_t i = min(t0 + c, namb - 1);
             const int64_t u = amb[i];
             const uint16_t* x = xb + u * a.xs;
@@ -499,6 +503,7 @@ __device__ __forceinline__ void exact_keys_block(const SelectArgs& a, int b, int
                             const float4 hs = L.hs[h];
                             v += fmaf(hs.x, et, fmaf(hs.y, ep, hs.z * ga));
                         }
+                        if (OFF) v -= (float)L.off[h];
                     }
                     acc[ht][q] = v;
                     m = fmaxf(m, v);
@@ -526,8 +531,9 @@ __device__ __forceinline__ void exact_keys_block(const SelectArgs& a, int b, int
                     cm &= cm - 1u;
                     const int h = 16 * (sl >> 2) + 4 * g + (sl & 3);
                     const float4 hs = UB ? L.hs[h] : make_float4(0.f, 0.f, 0.f, 0.f);
-                    const double v = exact_chain<UB>(qsrc + (int64_t)h * a.n, &sx[c * a.n], a.n, hs, (double)et,
-                                                     (double)ep, (double)ga);
+                    double v = exact_chain<UB>(qsrc + (int64_t)h * a.n, &sx[c * a.n], a.n, hs, (double)et,
+                                               (double)ep, (double)ga);
+                    if (OFF) v = v - L.off[h];
                     atomicMax(&best[c], (unsigned long long)f64_to_ord(v));
                 }
             }
@@ -549,7 +555,7 @@ __device__ __forceinline__ void exact_keys_block(const SelectArgs& a, int b, int
 // when it is short; otherwise a radix select on the 96-bit composite
 // (order key, ~index), whose larger values come first.
 __device__ __forceinline__ void rank_winners(const int32_t* amb, const uint64_t* ak, int64_t namb, int64_t need, uint8_t* fb,
-                             uint32_t* xin, uint8_t* lds, uint64_t* s_theta) {
+                             uint32_t* xin, uint8_t* lds, uint64_t* s_theta, uint8_t mark = 1) {
     const int tid = threadIdx.x;
     if (namb <= RANK_QUAD_MAX) {
         uint64_t* s_k = reinterpret_cast<uint64_t*>(lds);
@@ -568,7 +574,7 @@ __device__ __forceinline__ void rank_winners(const int32_t* amb, const uint64_t*
                 rank += (kj > ki) || (kj == ki && s_u[j] < ui);
             }
             if (rank < need) {
-                fb[ui] = 1;
+                fb[ui] = mark;
                 atomicAdd(&xin[(int64_t)(ui / CB_KEYS) * BLK_WORDS], 1u);
                 if (rank == need - 1) *s_theta = ki;
             }
@@ -630,7 +636,7 @@ __device__ __forceinline__ void rank_winners(const int32_t* amb, const uint64_t*
         const uint64_t hi = ak[i];
         const uint32_t lo = ~(uint32_t)amb[i];
         if (hi > pre_hi || (hi == pre_hi && lo >= pre_lo)) {
-            fb[amb[i]] = 1;
+            fb[amb[i]] = mark;
             atomicAdd(&xin[(int64_t)(amb[i] / CB_KEYS) * BLK_WORDS], 1u);
         }
     }
@@ -1011,6 +1017,171 @@ __global__ __launch_bounds__(RES_THREADS, 1) void adm_resolve_kernel(SelectArgs 
             f2[u] = 3;
             atomicAdd(&blkb[(int64_t)(u / CB_KEYS) * BLK_WORDS + BW_XIN], 1u);
         }
+}
+
+__global__ __launch_bounds__(64) void zero_counts_kernel(int32_t* p, int n);
+
+// ---------------------------------------------------------------- trigger
+//
+// The calibrated trigger (Sec. 4.2, Eq. (trigger) against the tier-1 maximum
+// logit; the optional top-j cap of the deployment specification): a row u
+// outside S fires iff some head has UB_h(u) > s*_h, UB_h with the certificate
+// term scaled by cert_mult = z / sqrt(d_c - r).  Its margin is
+// max_h (UB_h(u) - s*_h).  Three launches and the ordered compaction:
+//   classify (one block per 4096 rows): a row whose UB~ (the maximum over
+//     heads) stays below min_h s*_h by more than its band cannot fire; the
+//     others are candidates;
+//   exact (a few blocks per sequence): the exact margins of the candidates,
+//     a per-head fp32 screen and fp64 chains for the heads near the row's
+//     maximum (the exact-key machinery with the thresholds subtracted);
+//   fire (one block per sequence): margin > 0, and with a cap the top j by
+//     (margin desc, row asc).
+
+// the smallest threshold of sequence b (wave 0 of the block; result in all its lanes)
+__device__ __forceinline__ double min_threshold(const SelectArgs& a, int b) {
+    double m = INFINITY;
+    for (int h = threadIdx.x & 63; h < a.H; h += 64) m = fmin(m, a.smax[(int64_t)b * a.H + h]);
+    for (int o = 32; o > 0; o >>= 1) m = fmin(m, __shfl_xor(m, o));
+    return m;
+}
+
+__global__ __launch_bounds__(SEL_THREADS) void trig_classify_kernel(SelectArgs a) {
+    __shared__ uint32_t s_w[SEL_THREADS / 64];
+    __shared__ uint32_t s_base;
+    __shared__ double s_min;
+    const int b = blockIdx.y, tid = threadIdx.x;
+    const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
+    const int64_t ub0 = (int64_t)blockIdx.x * CB_KEYS;
+    const int64_t ue = min(a.A, ub0 + CB_KEYS);
+    const float* ubb = a.ub + (int64_t)b * a.A;
+    const uint8_t* fb = a.flags + (int64_t)b * a.fstride;
+    uint8_t* f2 = a.flags2 + (int64_t)b * a.fstride;
+    float t[CB_PER];
+    uint8_t fin[CB_PER];
+#pragma unroll
+    for (int j = 0; j < CB_PER; ++j) {
+        const int64_t u = ub0 + tid + (int64_t)SEL_THREADS * j;
+        const int64_t uc = u < ue ? u : ub0;
+        t[j] = ubb[uc];
+        fin[j] = (u < ue) ? fb[uc] : (uint8_t)1;
+    }
+    if (tid < 64) {
+        const double m = min_threshold(a, b);
+        if (tid == 0) s_min = m;
+    }
+    lds_barrier();
+    const double smin = s_min;
+    const bool same = sq[SQ_CMULT] == __float_as_uint(a.cert_mult);
+    const double E = ub_error_of(sq, a.n) * (1.0 + 0x1p-20);
+    uint32_t mask = 0;
+#pragma unroll
+    for (int j = 0; j < CB_PER; ++j) {
+        const int64_t u = ub0 + tid + (int64_t)SEL_THREADS * j;
+        if (u < ue) {
+            uint8_t f = 0;
+            if (fin[j] != 1) {
+                if (!same || smin == -INFINITY) {
+                    f = 5;
+                } else {
+                    const double tv = (double)t[j];
+                    const double band = E + fabs(tv) * 0x1p-50 + fabs(smin) * 0x1p-50;
+                    f = (tv + band <= smin) ? 0 : 5;
+                }
+            }
+            f2[u] = f;
+            mask |= (f == 5) ? (1u << j) : 0u;
+        }
+    }
+    block_append(mask, ub0, a.seq + (int64_t)b * SQ_WORDS + SQ_NCAND3, a.cand + (int64_t)b * a.A, nullptr, t,
+                 a.A, s_w, &s_base);
+    if (tid == 0) {
+        uint32_t* w = a.blk + ((int64_t)b * a.nblk + blockIdx.x) * BLK_WORDS;
+        w[BW_IN] = 0u;
+        w[BW_XIN] = 0u;
+    }
+}
+
+constexpr int TRIG_EX_BLOCKS = 4;   // blocks per sequence of the exact-margin pass
+
+__global__ __launch_bounds__(RES_THREADS, 1) void trig_exact_kernel(SelectArgs a) {
+    extern __shared__ __align__(16) uint8_t lds[];
+    __shared__ double s_absmax;
+    const int b = blockIdx.y, tid = threadIdx.x;
+    const uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
+    const int64_t namb = min((int64_t)sq[SQ_NCAND3], a.A);
+    if ((int64_t)blockIdx.x * 16 >= namb) return;
+    if (tid < 64) {
+        double m = 0.0;
+        for (int h = tid; h < a.H; h += 64) {
+            const double v = a.smax[(int64_t)b * a.H + h];
+            m = fmax(m, isfinite(v) ? fabs(v) : 0.0);
+        }
+        for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o));
+        if (tid == 0) s_absmax = m;
+    }
+    lds_barrier();
+    const bool same = sq[SQ_CMULT] == __float_as_uint(a.cert_mult);
+    // screen error: the bound's fp32 error plus the fp32 rounding of s*_h and of the difference
+    const double ubmax = (double)__uint_as_float(sq[SQ_QMAX]) * nu_max_of(sq, a.n) +
+                         (double)__uint_as_float(sq[SQ_BMAX]) * (1.0 + 0x1p-20);
+    const double Et = ub_error_of(sq, a.n) * (1.0 + 0x1p-20) + 0x1p-21 * (s_absmax + ubmax);
+    const float margin = same ? next_up_f32(2.0f * ru_f32(Et)) : INFINITY;
+    const ExLds L = ex_carve(lds, a.H, a.n);
+    exact_keys_block<true, true>(a, b, namb, a.cand + (int64_t)b * a.A, a.ambkey + (int64_t)b * a.A, L, margin,
+                                 blockIdx.x, gridDim.x);
+}
+
+__global__ __launch_bounds__(RES_THREADS, 1) void trig_fire_kernel(SelectArgs a) {
+    extern __shared__ __align__(16) uint8_t lds[];
+    __shared__ uint32_t s_w[RES_WAVES];
+    __shared__ uint64_t s_theta;
+    const int b = blockIdx.x, tid = threadIdx.x;
+    uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
+    uint8_t* f2 = a.flags2 + (int64_t)b * a.fstride;
+    const int32_t* cl = a.cand + (int64_t)b * a.A;
+    const uint64_t* ak = a.ambkey + (int64_t)b * a.A;
+    uint32_t* xin = a.blk + (int64_t)b * a.nblk * BLK_WORDS + BW_XIN;
+    const int64_t namb = min((int64_t)sq[SQ_NCAND3], a.A);
+    const uint64_t zero = f64_to_ord(0.0);
+    uint32_t nf = 0;
+    for (int64_t i = tid; i < namb; i += RES_THREADS) nf += ak[i] > zero;
+    nf = block_sum<RES_THREADS>(nf, s_w);
+    __syncthreads();
+    if (tid == 0) {
+        sq[SQ_NFIRED] = nf;
+        sq[SQ_NCAND3] = 0u;   // consumed: a repeated trigger starts an empty list
+        s_theta = 0;
+    }
+    if (a.topj > 0 && (int64_t)nf > a.topj) {
+        // the top j margins among the candidates are all fired (margin > 0 >= the rest)
+        rank_winners(cl, ak, namb, a.topj, f2, xin, lds, &s_theta, 6);
+    } else {
+        for (int64_t i = tid; i < namb; i += RES_THREADS)
+            if (ak[i] > zero) {
+                const int32_t u = cl[i];
+                f2[u] = 6;
+                atomicAdd(&xin[(int64_t)(u / CB_KEYS) * BLK_WORDS], 1u);
+            }
+    }
+}
+
+hipError_t launch_trigger(const SelectArgs& a, hipStream_t s) {
+    hipError_t e;
+    if (a.A == 0) {
+        hipLaunchKernelGGL(zero_counts_kernel, dim3(1), dim3(64), 0, s, a.adm_count, a.B);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL(trig_classify_kernel, dim3((unsigned)a.nblk, a.B), dim3(SEL_THREADS), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&trig_exact_kernel),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, RES_LDS);
+    hipLaunchKernelGGL(trig_exact_kernel, dim3(TRIG_EX_BLOCKS, a.B), dim3(RES_THREADS), RES_LDS, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&trig_fire_kernel),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, RES_LDS);
+    hipLaunchKernelGGL(trig_fire_kernel, dim3(a.B), dim3(RES_THREADS), RES_LDS, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return run_compact(a, a.flags2, 6, a.adm, a.cap, a.cap, a.adm_count, s);
 }
 
 __global__ __launch_bounds__(64) void zero_counts_kernel(int32_t* p, int n) {

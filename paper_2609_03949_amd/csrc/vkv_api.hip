@@ -672,6 +672,170 @@ int vkv_step_run(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, in
     return VKV_OK;
 }
 
+static hipError_t run_row_max(const vkv_step* st, const int32_t* rows, int64_t nrows, int all_archive, int add_recent,
+                              double* smax, int32_t* argmax, hipStream_t s) {
+    RowMaxArgs a{};
+    a.q_lat = st->q_lat;
+    a.q_rope = st->q_rope;
+    a.cache = st->cache;
+    a.cs = st->cache_row_stride;
+    a.cbs = st->cache_batch_stride;
+    a.rows = rows;
+    a.nrows = all_archive ? 0 : nrows;
+    a.A = st->T - st->W;
+    a.T = st->T;
+    a.all_archive = all_archive;
+    a.add_recent = add_recent;
+    a.B = (int)st->B;
+    a.H = (int)st->H;
+    a.smax = smax;
+    a.argmax = argmax;
+    return launch_row_max(a, s);
+}
+
+int vkv_row_max(vkv_ctx* ctx, const vkv_step* st, const int32_t* rows, int64_t nrows, int32_t add_recent,
+                double* smax, int32_t* argmax, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    int rc = check_step(ctx, st);
+    if (rc) return rc;
+    if (!smax || !argmax) return fail(ctx, VKV_E_ARG, "smax and argmax are required");
+    if (rows && (nrows < 0 || nrows > st->T - st->W))
+        return fail(ctx, VKV_E_ARG, "nrows=%lld outside [0, A]", (long long)nrows);
+    HIP_TRY(ctx, run_row_max(st, rows, nrows, rows ? 0 : 1, add_recent ? 1 : 0, smax, argmax, (hipStream_t)stream));
+    return VKV_OK;
+}
+
+static int check_trigger(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, const int32_t* sel,
+                         const float* ub, float cert_mult, const double* smax, int64_t topj, int32_t* fired,
+                         int32_t* fired_count, int64_t cap) {
+    int rc = check_prep(ctx, st, ws, ws_bytes);
+    if (rc) return rc;
+    if ((rc = check_cert_mult(ctx, cert_mult))) return rc;
+    const int64_t A = st->T - st->W;
+    if (st->mode == VKV_MODE_DIGEST) return fail(ctx, VKV_E_UNSUPPORTED, "the trigger needs the branch summand in the key");
+    if (!st->eta || !st->eps || !st->gam) return fail(ctx, VKV_E_ARG, "the trigger needs eta, eps and gam");
+    if (k < 0 || k > A) return fail(ctx, VKV_E_ARG, "k=%lld outside [0, A]", (long long)k);
+    if (cap < 0 || cap > A) return fail(ctx, VKV_E_ARG, "cap=%lld outside [0, A]", (long long)cap);
+    if (topj < 0) return fail(ctx, VKV_E_ARG, "topj must be >= 0 (0 = uncapped)");
+    if (!smax || !fired_count || (A > 0 && !ub) || (cap > 0 && !fired) || (k > 0 && !sel))
+        return fail(ctx, VKV_E_ARG, "sel, ub, smax, fired and fired_count are required");
+    return VKV_OK;
+}
+
+static hipError_t run_trigger(const vkv_step* st, char* w, int64_t k, const int32_t* sel, const float* ub,
+                              float cert_mult, const double* smax, int64_t topj, int32_t* fired,
+                              int32_t* fired_count, int64_t cap, hipStream_t s) {
+    const WsLayout L = layout(st, 0, 0);
+    SelectArgs a = select_args(st, L, w, Chunk{0, st->B});
+    a.ub = ub;
+    a.sel = const_cast<int32_t*>(sel);
+    a.adm = fired;
+    a.adm_count = fired_count;
+    a.k = k;
+    a.cap = cap;
+    a.cert_mult = cert_mult;
+    a.smax = smax;
+    a.topj = topj;
+    return launch_trigger(a, s);
+}
+
+int vkv_trigger(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, const int32_t* sel,
+                const float* ub, float cert_mult, const double* smax, int64_t topj, int32_t* fired,
+                int32_t* fired_count, int64_t cap, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    int rc = check_trigger(ctx, st, ws, ws_bytes, k, sel, ub, cert_mult, smax, topj, fired, fired_count, cap);
+    if (rc) return rc;
+    HIP_TRY(ctx, run_trigger(st, (char*)ws, k, sel, ub, cert_mult, smax, topj, fired, fired_count, cap,
+                             (hipStream_t)stream));
+    return debug_check_adm(ctx, st, k, sel, fired, fired_count, cap, (hipStream_t)stream);
+}
+
+int vkv_required_inflation(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, const int32_t* sel,
+                           const double* tier1_max, const int32_t* argmax, int32_t* hard, double* zq, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    int rc = check_prep(ctx, st, ws, ws_bytes);
+    if (rc) return rc;
+    const int64_t A = st->T - st->W;
+    if (st->mode == VKV_MODE_DIGEST) return fail(ctx, VKV_E_UNSUPPORTED, "the inflation needs the branch summand in the key");
+    if (!st->eta || !st->eps || !st->gam) return fail(ctx, VKV_E_ARG, "the inflation needs eta, eps and gam");
+    if (k < 0 || k > A) return fail(ctx, VKV_E_ARG, "k=%lld outside [0, A]", (long long)k);
+    if (!tier1_max || !argmax || !hard || !zq || (k > 0 && !sel))
+        return fail(ctx, VKV_E_ARG, "sel, tier1_max, argmax, hard and zq are required");
+    const WsLayout L = layout(st, 0, 0);
+    InflArgs a{};
+    index_operand(st, &a.x, &a.xs, &a.xbs);
+    a.qt = reinterpret_cast<const uint16_t*>((char*)ws + L.qt);
+    a.hsc = reinterpret_cast<const float*>((char*)ws + L.hsc);
+    a.eta = st->eta;
+    a.eps = st->eps;
+    a.gam = st->gam;
+    a.T = st->T;
+    a.A = A;
+    a.k = k;
+    a.sel = sel;
+    a.tier1 = tier1_max;
+    a.argmax = argmax;
+    a.B = (int)st->B;
+    a.H = (int)st->H;
+    a.n = (int)L.n;
+    a.r = (st->mode & 2) ? st->r : 0;
+    a.hard = hard;
+    a.zq = zq;
+    HIP_TRY(ctx, launch_inflation(a, (hipStream_t)stream));
+    return VKV_OK;
+}
+
+int vkv_conformal_z(const double* zq, int64_t n, int64_t tau_num, int64_t tau_den, double zmax, double* z,
+                    int64_t* min_hard, int64_t* rank) {
+    if (!z || !min_hard || !rank || (n > 0 && !zq) || n < 0) return fail(nullptr, VKV_E_ARG, "bad arguments");
+    if (tau_num <= 0 || tau_den <= tau_num) return fail(nullptr, VKV_E_ARG, "tau = tau_num / tau_den must lie in (0, 1)");
+    if (!(zmax >= 0.0)) return fail(nullptr, VKV_E_ARG, "zmax must be >= 0");
+    // tau_s = 2 tau_num / (tau_den + tau_num); min_hard = ceil(tau_s / (1 - tau_s)); k = ceil((n + 1) tau_s)
+    const int64_t mh = (2 * tau_num + (tau_den - tau_num) - 1) / (tau_den - tau_num);
+    const int64_t k = ((n + 1) * 2 * tau_num + (tau_den + tau_num) - 1) / (tau_den + tau_num);
+    *min_hard = mh;
+    if (n < mh || k > n) {
+        *z = zmax;
+        *rank = 0;
+        return VKV_OK;
+    }
+    std::vector<double> v(zq, zq + n);
+    std::nth_element(v.begin(), v.begin() + (k - 1), v.end());
+    double q = v[(size_t)(k - 1)];
+    if (q > zmax) q = zmax;
+    if (!(q > 0.0)) q = 0.0;
+    *z = q;
+    *rank = k;
+    return VKV_OK;
+}
+
+int vkv_step_run_trigger(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, float* key, float* ub,
+                         int32_t* sel, double* theta, float cert_mult, double* smax, int32_t* argmax, int64_t topj,
+                         int32_t* fired, int32_t* fired_count, int64_t cap, float scale, uint16_t* out, float* lse,
+                         void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    int rc;
+    if ((rc = check_score(ctx, st, ws, ws_bytes, ub, cert_mult))) return rc;
+    if (!ub) return fail(ctx, VKV_E_ARG, "the trigger needs ub");
+    if ((rc = check_select(ctx, st, ws, ws_bytes, k, sel, theta))) return rc;
+    if ((rc = check_trigger(ctx, st, ws, ws_bytes, k, sel, ub, cert_mult, smax, topj, fired, fired_count, cap)))
+        return rc;
+    if (!argmax) return fail(ctx, VKV_E_ARG, "argmax is required");
+    if ((rc = check_attend(ctx, st, ws, ws_bytes, k, sel, fired, fired_count, cap, scale, out, lse))) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    char* w = (char*)ws;
+    const Chunk all{0, st->B};
+    HIP_TRY(ctx, run_prep(st, w, all, s));
+    HIP_TRY(ctx, run_score(st, w, all, key, ub, cert_mult, s));
+    HIP_TRY(ctx, run_select(st, w, all, k, sel, theta, s));
+    // the tier-1 maximum logit per head over S and the recent window
+    HIP_TRY(ctx, run_row_max(st, sel, k, 0, 1, smax, argmax, s));
+    HIP_TRY(ctx, run_trigger(st, w, k, sel, ub, cert_mult, smax, topj, fired, fired_count, cap, s));
+    HIP_TRY(ctx, run_attend(st, w, all, k, sel, fired, fired_count, cap, scale, out, lse, s));
+    if ((rc = debug_check_sel(ctx, st, k, sel, s))) return rc;
+    return debug_check_adm(ctx, st, k, sel, fired, fired_count, cap, s);
+}
+
 int vkv_step_run_static(vkv_ctx* ctx, const vkv_step* st, int64_t k, float* key, float* ub, int32_t* sel,
                         double* theta, int32_t* adm, int32_t* adm_count, int64_t cap, float cert_mult, float scale,
                         uint16_t* out, float* lse, void* stream) {

@@ -139,6 +139,8 @@ enum SeqWord : int {
     SQ_NAMB2 = 16,  // ambiguous rows of the admission                (diagnostic)
     SQ_NCAND = 17,  // selection candidates listed by the counting pass (zeroed by the bracket launch)
     SQ_NCAND2 = 18, // undecided admission rows listed by the classification (zeroed by its consumer)
+    SQ_NCAND3 = 19, // trigger candidates listed by the trigger classification (zeroed by its consumer)
+    SQ_NFIRED = 20, // rows the trigger fired before the top-j cap (diagnostic)
     SQ_WORDS = 32
 };
 
@@ -227,6 +229,39 @@ struct SelectArgs {
     int64_t fstride;       // bytes per sequence of flags / flags2 (A rounded up to 64)
     int B, H, n;
     float cert_mult;       // admission: multiplier of the sketch-residual term
+    const double* smax;    // trigger: [B,H] per-head thresholds s*_h (the tier-1 max logit)
+    int64_t topj;          // trigger: cap on the fired rows (0 = uncapped)
+};
+
+struct RowMaxArgs {
+    const uint16_t* q_lat;  // [B,H,512]
+    const uint16_t* q_rope; // [B,H,64]
+    const uint16_t* cache;
+    int64_t cs, cbs;
+    const int32_t* rows;    // [B,nrows] listed rows (unless all_archive)
+    int64_t nrows, A, T;
+    int all_archive;        // the list is the archived rows [0, A)
+    int add_recent;         // the rows [A, T) follow the listed ones
+    int B, H;
+    double* smax;           // [B,H]
+    int32_t* argmax;        // [B,H]
+};
+
+struct InflArgs {
+    const uint16_t* x;      // index rows
+    int64_t xs, xbs;
+    const uint16_t* qt;     // [B,H,n]
+    const float* hsc;       // [B,H,4]
+    const float* eta;
+    const float* eps;
+    const float* gam;
+    int64_t T, A, k;
+    const int32_t* sel;     // [B,k]
+    const double* tier1;    // [B,H] s*_h
+    const int32_t* argmax;  // [B,H] the causal argmax rows
+    int B, H, n, r;
+    int32_t* hard;          // [B,H]
+    double* zq;             // [B,H]
 };
 
 struct AttendArgs {
@@ -255,6 +290,9 @@ hipError_t launch_gram_rows(const uint16_t* P, int r, double* rowsum, hipStream_
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_admit(const SelectArgs& a, hipStream_t s);
 hipError_t launch_attend(const AttendArgs& a, hipStream_t s);
+hipError_t launch_row_max(const RowMaxArgs& a, hipStream_t s);
+hipError_t launch_trigger(const SelectArgs& a, hipStream_t s);
+hipError_t launch_inflation(const InflArgs& a, hipStream_t s);
 
 // ------------------------------------------- fp64 matrix-core row products
 

@@ -109,3 +109,18 @@ def test_null_context_is_refused(lib):
     assert lib.vkv_attend(None, ctypes.byref(s), None, 0, 1, None, None, None, 0, ctypes.c_float(0.1),
                           None, None, None) == -1
     assert b"ctx" in lib.vkv_last_error(None)
+
+
+def test_conformal_z_host_function_matches_the_oracle(lib, oracle_mod):
+    """vkv_conformal_z is host code (no device): the library's quantile equals
+    the oracle's for assorted calibration sets, targets and clamps."""
+    import numpy as np
+    import paper_2609_03949_amd as vkv
+    rng = np.random.default_rng(7)
+    for n in (0, 5, 17, 18, 19, 37, 64, 500):
+        for tau in ((9, 10), (4, 5), (19, 20)):
+            for zmax in (8.0, 2.0):
+                zq = rng.standard_normal(n) * 3 + 1
+                assert vkv.conformal_z(zq, tau, zmax) == oracle_mod.conformal_z(zq, tau, zmax)
+    with pytest.raises(vkv.VkvError):
+        vkv.conformal_z([1.0], (10, 10))
