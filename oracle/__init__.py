@@ -445,3 +445,32 @@ def step_trigger(cache, q_lat, q_rope, index, P, r: int, mode: int, W: int, k: i
                         ("fired_count", cnt), ("out", out), ("lse", lse), ("margin", m)):
             res[name][b] = v
     return res
+
+
+# --------------------------------------------------- data-driven sketch basis
+
+SKETCH_SCALE = 1.0 - 2.0 ** -6   # keeps the bf16-rounded basis contractive
+
+
+def content_second_moment(q: np.ndarray) -> np.ndarray:
+    """C = sum_i q_i q_i^T over the prefix content queries q [m, 512] (bf16
+    bits; fp64, a library matmul of the exact values)."""
+    v = decode_bf16(_u16(q)).reshape(-1, D_LAT)
+    return v.T @ v
+
+
+def sketch_basis(q: np.ndarray, r: int):
+    """V_r = the top-r eigenvectors of the prefix content queries' second
+    moment (Sec. 4.2, the index entry: V_r from the context's own prefix
+    queries), as the digest basis P = RNE_bf16(SKETCH_SCALE * V_r^T) [r, 512].
+    Returns (P bits, V_r [512, r] fp64, eigenvalues [r] descending)."""
+    C = content_second_moment(q)
+    w, V = np.linalg.eigh(C)                 # ascending
+    order = np.argsort(-w, kind="stable")[:r]
+    V = V[:, order]
+    w = w[order]
+    # sign: the largest-magnitude component of each eigenvector positive
+    idx = np.argmax(np.abs(V), axis=0)
+    V = V * np.sign(V[idx, np.arange(r)])
+    P = np.vectorize(round_bf16, otypes=[np.uint16])(SKETCH_SCALE * V.T)
+    return P, V, w

@@ -746,3 +746,47 @@ def test_required_inflation_is_where_the_target_starts_to_fire(oracle_mod):
             m = oracle_mod.trigger_margins(qt[0, h:h + 1], a[0, h:h + 1], nq[0, h:h + 1], e[0, h:h + 1], x,
                                            eta[0], eps[0], gam[0], A, s1[h:h + 1], cm)
             assert (m[u] > 0) == fires, (h, f, m[u])
+
+
+# ---------------------------------------------- data-driven sketch basis V_r
+
+def _lowrank_queries(m, rank, noise, seed=5):
+    r_ = np.random.default_rng(seed)
+    U, _ = np.linalg.qr(r_.standard_normal((512, rank)))
+    g = r_.standard_normal((m, rank)) * 3.0
+    q = g @ U.T + noise * r_.standard_normal((m, 512))
+    return (q.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16), U
+
+
+def test_sketch_basis_recovers_a_planted_subspace(oracle_mod):
+    """Queries in a planted 48-dim subspace plus small noise: the top-48
+    eigenvectors span it (principal angles ~ noise / signal), they are
+    orthonormal, satisfy C v = lambda v, and the bf16 basis is contractive."""
+    q, U = _lowrank_queries(2000, 48, 0.05)
+    P, V, w = oracle_mod.sketch_basis(q, 48)
+    assert np.allclose(V.T @ V, np.eye(48), atol=1e-12)
+    C = oracle_mod.content_second_moment(q)
+    assert np.max(np.abs(C @ V - V * w)) < 1e-9 * w[0]
+    s = np.linalg.svd(U.T @ V, compute_uv=False)          # cosines of the principal angles
+    assert s.min() > 1 - 1e-4
+    assert w[47] > 100 * oracle_mod.sketch_basis(q, 49)[2][48]   # the eigengap after the planted rank
+    assert oracle_mod.gershgorin(P) < 1.0
+    assert np.all(np.abs(dec(P) - oracle_mod.SKETCH_SCALE * V.T) <= 2.0 ** -8 * np.abs(V.T) + 1e-30)
+
+
+def test_sketch_basis_is_rotation_equivariant_and_shrinks_the_residual(oracle_mod):
+    """The subspace does not depend on the order of the queries; on queries
+    of the planted subspace the residual ||(I - V V^T) q|| that the
+    certificate multiplies (Lemma (Index certificate)) drops to the noise."""
+    q, U = _lowrank_queries(1500, 32, 0.02, seed=8)
+    P1, V1, _ = oracle_mod.sketch_basis(q, 32)
+    P2, V2, _ = oracle_mod.sketch_basis(q[::-1].copy(), 32)
+    assert np.allclose(V1 @ V1.T, V2 @ V2.T, atol=1e-10)
+    qq = dec(q)
+    res = np.linalg.norm(qq - (qq @ V1) @ V1.T, axis=1) / np.linalg.norm(qq, axis=1)
+    # the noise outside the subspace: 0.02 sqrt(512 - 32) against a signal of 3 sqrt(32)
+    pred = 0.02 * math.sqrt(512 - 32) / (3.0 * math.sqrt(32))
+    assert 0.7 * pred < np.median(res) < 1.3 * pred and res.max() < 2.5 * pred
+    full = np.linalg.norm(qq - (qq @ np.linalg.qr(np.random.default_rng(1).standard_normal((512, 32)))[0])
+                          @ np.linalg.qr(np.random.default_rng(1).standard_normal((512, 32)))[0].T, axis=1)
+    assert np.median(full / np.linalg.norm(qq, axis=1)) > 0.9   # a random basis leaves almost all of it
