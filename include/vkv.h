@@ -143,6 +143,29 @@ int vkv_digest_build(vkv_ctx* ctx, const uint16_t* cache, int64_t B, int64_t T,
                      int64_t index_batch_stride, float* eta, float* eps, float* gam,
                      void* stream);
 
+/*
+ * The data-driven sketch basis (Sec. 4.2, the index entry: V_r is drawn from
+ * the context's own prefix queries).  q [m, 512] bf16 holds the prefix content
+ * queries (one row per query and head).  V_r spans the dominant r-dimensional
+ * eigenspace of their second moment C = sum_i q_i q_i^T (fp64; the products of
+ * bf16 values are exact), found by subspace iteration: a fixed +-1 start
+ * pattern, then `iters` rounds of V <- orth(C V), orth = Cholesky QR twice.  The
+ * subspace error shrinks as (lambda_{r+1}/lambda_r)^iters; the index scores
+ * depend on the subspace only, not on the basis within it.  Writes
+ * P [r, 512] bf16 = RNE_bf16((1 - 2^-6) V_r^T), the basis vkv_digest_build
+ * takes (the factor keeps the rounded basis contractive), and, if
+ * energy != NULL, energy [2] fp64 (device) = { trace(V_r^T C V_r), trace(C) }:
+ * the queries' second moment the sketch captures and the total (both
+ * basis-independent; their ratio is the captured fraction).  r: a multiple of
+ * 32 in [32, 512]; iters in [0, 64]; ws: vkv_sketch_workspace_size bytes,
+ * 256-byte aligned, fully overwritten.  Synchronises `stream` to read the
+ * factorisation's verdict and returns VKV_E_UNSUPPORTED if the queries span
+ * fewer than r dimensions (a non-positive pivot); P is then not usable.
+ */
+int vkv_sketch_workspace_size(int32_t r, size_t* bytes);
+int vkv_sketch_basis(vkv_ctx* ctx, const uint16_t* q, int64_t m, int32_t r, int32_t iters, void* ws,
+                     size_t ws_bytes, uint16_t* P, double* energy, void* stream);
+
 /* Bytes of device workspace a step with budget k and admission capacity cap
  * (0 without admission) needs; the workspace must be 256-byte aligned. */
 int vkv_workspace_size(const vkv_step* st, int64_t k, int64_t cap, size_t* bytes);

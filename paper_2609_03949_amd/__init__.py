@@ -20,7 +20,7 @@ __all__ = [
     "VKV_MODE_ROPE", "VKV_MODE_DIGEST", "VKV_MODE_ROPE_DIGEST", "VkvError", "Context", "Step",
     "lib_path", "load", "digest_build", "workspace_size", "query_prep", "score", "select", "admit", "attend",
     "step_run", "step_run_static", "check_rows", "row_max", "trigger", "required_inflation", "conformal_z",
-    "step_run_trigger", "exported_symbols",
+    "step_run_trigger", "sketch_workspace_size", "sketch_basis", "exported_symbols",
 ]
 
 VKV_MODE_ROPE, VKV_MODE_DIGEST, VKV_MODE_ROPE_DIGEST = 1, 2, 3
@@ -34,6 +34,7 @@ exported_symbols = (
     "vkv_digest_build", "vkv_workspace_size", "vkv_query_prep", "vkv_score", "vkv_select", "vkv_admit",
     "vkv_attend", "vkv_step_run", "vkv_step_run_static", "vkv_check_rows", "vkv_set_timing", "vkv_score_timing",
     "vkv_row_max", "vkv_trigger", "vkv_required_inflation", "vkv_conformal_z", "vkv_step_run_trigger",
+    "vkv_sketch_workspace_size", "vkv_sketch_basis",
 )
 
 
@@ -100,6 +101,8 @@ def load():
     lib.vkv_conformal_z.argtypes = [P, i64, i64, i64, ctypes.c_double, P, P, P]
     lib.vkv_step_run_trigger.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P, P, f32, P, P, i64, P, P, i64,
                                          f32, P, P, P]
+    lib.vkv_sketch_workspace_size.argtypes = [i32, ctypes.POINTER(ctypes.c_size_t)]
+    lib.vkv_sketch_basis.argtypes = [P, P, i64, i32, i32, P, ctypes.c_size_t, P, P, P]
     lib.vkv_set_timing.argtypes = [P, ctypes.c_int]
     lib.vkv_score_timing.argtypes = [P, ctypes.POINTER(ctypes.c_float), ctypes.c_int]
     for name in exported_symbols:
@@ -331,6 +334,25 @@ def step_run_trigger(ctx: Context, step: Step, ws: torch.Tensor, k: int, key, ub
                                            _ptr(ub), _ptr(sel), _ptr(theta), float(cert_mult), _ptr(smax),
                                            _ptr(argmax), int(topj), _ptr(fired), _ptr(fired_count), int(cap),
                                            float(scale), _ptr(out), _ptr(lse), _stream(stream)))
+
+
+def sketch_workspace_size(r: int) -> int:
+    lib = load()
+    n = ctypes.c_size_t(0)
+    rc = lib.vkv_sketch_workspace_size(int(r), ctypes.byref(n))
+    if rc != 0:
+        raise VkvError(rc, lib.vkv_last_error(None).decode())
+    return int(n.value)
+
+
+def sketch_basis(ctx: Context, q: torch.Tensor, r: int, iters: int, ws: torch.Tensor, P: torch.Tensor,
+                 energy: Optional[torch.Tensor] = None, stream=None):
+    """vkv_sketch_basis: P [r,512] bf16 from the prefix content queries
+    q [m,512] bf16; energy [2] fp64 = (captured, total) second moment
+    (synchronises the stream)."""
+    m = q.numel() // D_LAT
+    ctx.check(ctx.lib.vkv_sketch_basis(ctx.handle, _ptr(q), int(m), int(r), int(iters), _ptr(ws), ws.numel(),
+                                       _ptr(P), _ptr(energy), _stream(stream)))
 
 
 def check_rows(ctx: Context, step: Step, k: int, sel: Optional[torch.Tensor],

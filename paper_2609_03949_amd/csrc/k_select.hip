@@ -992,7 +992,6 @@ __global__ __launch_bounds__(SEL_THREADS) void adm_classify_kernel(SelectArgs a)
 // decision UB > theta, then the ordered compaction of the admitted rows.
 __global__ __launch_bounds__(RES_THREADS, 1) void adm_resolve_kernel(SelectArgs a) {
     extern __shared__ __align__(16) uint8_t lds[];
-    __shared__ uint32_t s_w[RES_WAVES];
     const int b = blockIdx.x, tid = threadIdx.x;
     uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
     uint8_t* f2 = a.flags2 + (int64_t)b * a.fstride;

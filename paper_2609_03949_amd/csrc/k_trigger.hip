@@ -257,7 +257,7 @@ hipError_t launch_row_max(const RowMaxArgs& a, hipStream_t s) {
 __global__ __launch_bounds__(64) void inflation_kernel(InflArgs a) {
     const int64_t t = (int64_t)blockIdx.x * 64 + threadIdx.x;
     if (t >= (int64_t)a.B * a.H) return;
-    const int b = (int)(t / a.H), h = (int)(t % a.H);
+    const int b = (int)(t / a.H);
     const int32_t u = a.argmax[t];
     bool in_s = false;
     if (u >= 0 && u < a.A && a.k > 0) {

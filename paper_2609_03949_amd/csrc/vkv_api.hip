@@ -836,6 +836,34 @@ int vkv_step_run_trigger(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_b
     return debug_check_adm(ctx, st, k, sel, fired, fired_count, cap, s);
 }
 
+int vkv_sketch_workspace_size(int32_t r, size_t* bytes) {
+    if (!bytes) return fail(nullptr, VKV_E_ARG, "bytes is NULL");
+    if (r < 32 || r > 512 || r % 32) return fail(nullptr, VKV_E_UNSUPPORTED, "r=%d: need a multiple of 32 in [32, 512]", r);
+    *bytes = up256(sketch_workspace_bytes(r));
+    return VKV_OK;
+}
+
+int vkv_sketch_basis(vkv_ctx* ctx, const uint16_t* q, int64_t m, int32_t r, int32_t iters, void* ws, size_t ws_bytes,
+                     uint16_t* P, double* energy, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    if (!q || !P) return fail(ctx, VKV_E_ARG, "q and P are required");
+    if (m < 1) return fail(ctx, VKV_E_SHAPE, "m=%lld: need at least one query", (long long)m);
+    if (r < 32 || r > 512 || r % 32) return fail(ctx, VKV_E_UNSUPPORTED, "r=%d: need a multiple of 32 in [32, 512]", r);
+    if (iters < 0 || iters > 64) return fail(ctx, VKV_E_ARG, "iters=%d outside [0, 64]", iters);
+    if (!al16(q) || !al16(P)) return fail(ctx, VKV_E_ALIGN, "q and P must be 16-byte aligned");
+    int rc = check_ws(ctx, ws, ws_bytes, up256(sketch_workspace_bytes(r)));
+    if (rc) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(ctx, launch_sketch(q, m, r, iters, ws, P, energy, s));
+    // the orthonormalisation's verdict (one int at the end of the workspace)
+    int bad = 0;
+    const size_t off = sketch_workspace_bytes(r) - 256;
+    HIP_TRY(ctx, hipMemcpyAsync(&bad, (char*)ws + off, sizeof(int), hipMemcpyDeviceToHost, s));
+    HIP_TRY(ctx, hipStreamSynchronize(s));
+    if (bad) return fail(ctx, VKV_E_UNSUPPORTED, "the queries span fewer than r=%d dimensions", r);
+    return VKV_OK;
+}
+
 int vkv_step_run_static(vkv_ctx* ctx, const vkv_step* st, int64_t k, float* key, float* ub, int32_t* sel,
                         double* theta, int32_t* adm, int32_t* adm_count, int64_t cap, float cert_mult, float scale,
                         uint16_t* out, float* lse, void* stream) {

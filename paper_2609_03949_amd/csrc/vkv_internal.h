@@ -293,6 +293,9 @@ hipError_t launch_attend(const AttendArgs& a, hipStream_t s);
 hipError_t launch_row_max(const RowMaxArgs& a, hipStream_t s);
 hipError_t launch_trigger(const SelectArgs& a, hipStream_t s);
 hipError_t launch_inflation(const InflArgs& a, hipStream_t s);
+size_t sketch_workspace_bytes(int r);
+hipError_t launch_sketch(const uint16_t* q, int64_t m, int r, int iters, void* ws, uint16_t* P, double* energy,
+                         hipStream_t s);
 
 // ------------------------------------------- fp64 matrix-core row products
 

@@ -39,6 +39,7 @@ class Config:
     rows: str = "gaussian"  # "gaussian", "mixture", "lognormal"
     two_tier: bool = False  # certified admission on top of the top-k
     seed: int = 0
+    queries: str = "gaussian"  # content queries: "gaussian" N(0, I), "lowrank" (QUERY_RANK-dim subspace + noise)
 
     @property
     def A(self) -> int:
@@ -84,7 +85,7 @@ NEEDLE_SIGMAS = 6.0    # planted needle score, in standard deviations of a branc
 def describe(cfg: Config) -> str:
     return (f"{cfg.name}: B={cfg.B} H={cfg.H} T={cfg.T} W={cfg.W} k={cfg.k} "
             f"mode={MODE_NAMES[cfg.mode]} r={cfg.r} basis={cfg.basis} rows={cfg.rows} "
-            f"needles={cfg.needles} two_tier={cfg.two_tier}")
+            f"needles={cfg.needles} two_tier={cfg.two_tier} queries={cfg.queries}")
 
 
 # ------------------------------------------------------------------ helpers
@@ -143,11 +144,49 @@ def _plant(x: torch.Tensor, qdir: torch.Tensor, target: float) -> torch.Tensor:
     return x + (target - (x * qdir).sum(-1, keepdim=True)) * qdir
 
 
+QUERY_RANK = 48       # dimension of the planted content-query subspace ("lowrank" queries)
+QUERY_NOISE = 0.05    # isotropic noise per coordinate around it (signal: 3 per subspace coordinate)
+
+
+def query_subspace(rank: int = QUERY_RANK, seed: int = BASIS_SEED + 1) -> torch.Tensor:
+    """Orthonormal [512, rank] fp64 basis of the planted content-query subspace (CPU)."""
+    g = _gen("cpu", seed + rank)
+    U, _ = torch.linalg.qr(torch.randn(D_LAT, rank, generator=g, dtype=torch.float64))
+    return U
+
+
+def lowrank_content(n: int, g: torch.Generator, device, rank: int = QUERY_RANK,
+                    noise: float = QUERY_NOISE) -> torch.Tensor:
+    """n content queries [n, 512] fp32: 3 N(0, I_rank) coordinates in the planted
+    subspace plus noise N(0, noise^2 I_512) (queries concentrated near a subspace,
+    the regime the data-driven sketch basis is for)."""
+    U = query_subspace(rank).float().to(device)
+    coef = 3.0 * torch.randn(n, rank, generator=g, device=device)
+    return coef @ U.T + noise * torch.randn(n, D_LAT, generator=g, device=device)
+
+
+def prefix_queries(cfg: Config, m: int, device, seed: Optional[int] = None,
+                   rank: int = QUERY_RANK) -> torch.Tensor:
+    """m prefix content queries [m, 512] bf16 from the same law as the decode
+    queries of ``cfg`` (another stream of the generator): the sample the sketch
+    basis is computed from."""
+    seed = cfg.seed if seed is None else seed
+    g = _gen(device, 9_100_003 + 1013 * seed)
+    if cfg.queries == "lowrank":
+        x = lowrank_content(m, g, device, rank)
+    else:
+        x = torch.randn(m, D_LAT, generator=g, device=device)
+    return bf16_bits(x).contiguous()
+
+
 def make_queries(cfg: Config, device, seed: Optional[int] = None, B: Optional[int] = None):
     B = cfg.B if B is None else B
     seed = cfg.seed if seed is None else seed
     g = _gen(device, 7_000_003 + 1009 * seed)
-    q_lat = torch.randn(B, cfg.H, D_LAT, generator=g, device=device)
+    if cfg.queries == "lowrank":
+        q_lat = lowrank_content(B * cfg.H, g, device).view(B, cfg.H, D_LAT)
+    else:
+        q_lat = torch.randn(B, cfg.H, D_LAT, generator=g, device=device)
     q_rope = torch.randn(B, cfg.H, D_ROPE, generator=g, device=device)
     return q_lat, q_rope
 
