@@ -474,3 +474,111 @@ def sketch_basis(q: np.ndarray, r: int):
     V = V * np.sign(V[idx, np.arange(r)])
     P = np.vectorize(round_bf16, otypes=[np.uint16])(SKETCH_SCALE * V.T)
     return P, V, w
+
+
+# ----------------------------------------- query-independent tier-1 selector
+
+SIGMA_BLOCK = 4096    # the close granularity: sigma is computed per fixed block of rows
+SIGMA_SINKS = 4       # the first rows of the context, always attended
+
+
+def lowpass_residual_norm(branch: np.ndarray, kappa: int) -> np.ndarray:
+    """sigma_u over one closed block (Sec. 4.1, the sigma equation).
+
+    branch [N, 64]: the 64-dim un-rotated branch r_u of the block's rows (bf16
+    bits).  Along the sequence axis, per channel: the real DFT, bins
+    f in [0, kappa) kept and the rest zeroed, the inverse real DFT; sigma_u is
+    the norm over the channels of what that low-pass reconstruction misses at
+    row u.  Written as the DFT sums (fp64, the twiddle angle reduced mod N):
+      X_f = sum_t x_t exp(-2 pi i f t / N),
+      L_t = (1/N) [X_0 + 2 sum_{0<f<kappa} Re(X_f exp(2 pi i f t / N))],
+    the inverse real transform of the kept half spectrum (each kept bin
+    f > 0 stands for its mirror N - f as well).  kappa in [1, N/2]."""
+    x = decode_bf16(_u16(branch)).reshape(-1, D_ROPE)
+    N = x.shape[0]
+    if not 1 <= kappa <= N // 2:
+        raise ValueError("kappa must lie in [1, N/2]")
+    t = np.arange(N, dtype=np.int64)
+    f = np.arange(kappa, dtype=np.int64)
+    ang = 2.0 * np.pi * ((f[:, None] * t[None, :]) % N) / N        # [kappa, N]
+    c, s = np.cos(ang), np.sin(ang)
+    re = c @ x                                                      # Re X_f
+    im = -(s @ x)                                                   # Im X_f
+    w = np.full(kappa, 2.0)
+    w[0] = 1.0
+    L = (c.T @ (w[:, None] * re) - s.T @ (w[:, None] * im)) / N     # [N, 64]
+    return np.sqrt(np.sum((x - L) ** 2, axis=1))
+
+
+def sigma_close(cache_seq: np.ndarray, n_closed: int, kappa: int, block: int = SIGMA_BLOCK) -> np.ndarray:
+    """sigma for the rows [0, n_closed) of one sequence, block by block (each
+    closed block of ``block`` rows is transformed on its own, App. H, block
+    close).  n_closed is a multiple of ``block``."""
+    cache_seq = _u16(cache_seq)
+    if n_closed % block:
+        raise ValueError("n_closed must be a multiple of the block")
+    out = np.zeros(n_closed)
+    for b0 in range(0, n_closed, block):
+        out[b0:b0 + block] = lowpass_residual_norm(cache_seq[b0:b0 + block, D_LAT:], kappa)
+    return out
+
+
+def _sigma_order(sigma: np.ndarray, rows: np.ndarray) -> np.ndarray:
+    """rows ordered by (sigma desc, row asc) -- the strict total order of the selection."""
+    return rows[np.lexsort((rows, -sigma[rows]))]
+
+
+def sigma_select(sigma: np.ndarray, m: int, nsink: int = SIGMA_SINKS) -> np.ndarray:
+    """The sigma tier of the closed rows (Sec. 4.1): the nsink first rows plus
+    the sigma-top-m of the other closed rows (sigma desc, lower row first on
+    ties), ascending int32.  m larger than the rows on offer keeps them all."""
+    n = len(sigma)
+    sinks = np.arange(min(nsink, n))
+    rest = np.arange(min(nsink, n), n)
+    top = _sigma_order(sigma, rest)[:m]
+    return np.sort(np.concatenate([sinks, top])).astype(np.int32)
+
+
+def sigma_select_incremental(sigma: np.ndarray, m: int, nsink: int = SIGMA_SINKS,
+                             block: int = SIGMA_BLOCK) -> list[np.ndarray]:
+    """The same tier maintained as blocks close (Corollary (Ranking
+    stationarity)): after each close the kept set is the top-m of the
+    previous kept set together with the new block's rows; decisions are never
+    revisited.  Returns the tier after every close."""
+    n = len(sigma)
+    kept = np.zeros(0, np.int64)
+    tiers = []
+    for b0 in range(0, n, block):
+        new = np.arange(max(b0, nsink), min(b0 + block, n))
+        kept = _sigma_order(sigma, np.concatenate([kept, new]))[:m]
+        sinks = np.arange(min(nsink, b0 + block, n))
+        tiers.append(np.sort(np.concatenate([sinks, kept])).astype(np.int32))
+    return tiers
+
+
+def step_kept(cache, q_lat, q_rope, index, P, r: int, mode: int, W: int, kept, scale: float,
+              eta, eps, gam, cert_mult: float, topj: int = 0, seqs=None, index_has_rope: bool = True,
+              nthreads: int = 0):
+    """One decode step on a given tier-1 set (App. H, per decode step): the
+    kept rows ``kept[b]`` of the archive [0, A) (for instance the sigma tier)
+    plus the recent window are attended; s*_h is their exact maximum logit;
+    archived rows outside the kept set fire when some head's bound exceeds
+    it (top-j cap); attention runs over kept, window and fired rows."""
+    cache = _u16(cache)
+    B, T, _ = cache.shape
+    A = T - W
+    qt, a, nq, e = query_prep(q_lat, q_rope, P, r, mode)
+    res = {key: {} for key in ("smax", "argmax", "fired", "fired_count", "out", "lse", "margin")}
+    for b in (range(B) if seqs is None else seqs):
+        sel = np.asarray(kept[b], np.int32)
+        x = index_rows(cache[b], None if index is None else index[b], mode, r, index_has_rope)
+        tier1 = np.concatenate([sel, np.arange(A, T, dtype=np.int32)])
+        smax, arg = row_max(q_lat[b], q_rope[b], cache[b], tier1)
+        m = trigger_margins(qt[b], a[b], nq[b], e[b], x, eta[b], eps[b], gam[b], A, smax, cert_mult, nthreads)
+        fired, cnt = fire(m, sel, topj)
+        rows = attend_list(sel, A, T, fired)
+        out, lse = attend(q_lat[b], q_rope[b], cache[b], rows, scale, nthreads)
+        for name, v in (("smax", smax), ("argmax", arg), ("fired", fired), ("fired_count", cnt), ("out", out),
+                        ("lse", lse), ("margin", m)):
+            res[name][b] = v
+    return res
