@@ -166,6 +166,56 @@ int vkv_sketch_workspace_size(int32_t r, size_t* bytes);
 int vkv_sketch_basis(vkv_ctx* ctx, const uint16_t* q, int64_t m, int32_t r, int32_t iters, void* ws,
                      size_t ws_bytes, uint16_t* P, double* energy, void* stream);
 
+/*
+ * The query-independent tier-1 selector (Sec. 4.1, the sigma equation; the
+ * block close of the deployment specification's request lifecycle).  Rows are
+ * closed in fixed blocks of VKV_SIGMA_BLOCK rows; for every closed block and
+ * each of the 64 channels of the un-rotated branch r_u (elements 512..575 of
+ * each cache row) the sequence-axis DFT keeps bins [0, kappa) and their
+ * mirrors, the rest is zeroed and the transform inverted; sigma_u is the norm
+ * over the channels of what this low-pass reconstruction misses at row u.
+ *
+ * vkv_sigma_close: sigma for rows [t0, t0 + nblk * VKV_SIGMA_BLOCK) of every
+ * sequence, t0 a multiple of VKV_SIGMA_BLOCK and the range within T; cache as
+ * in vkv_digest_build; kappa in [1, VKV_SIGMA_BLOCK / 2].  sigma [B,
+ * sigma_stride] fp64 (device), only the closed range is written.  Each block
+ * is transformed on its own, so closing blocks one call at a time or all at
+ * once gives the same bits.  fp64 FFT (error about 1e-15 of the block's
+ * norm).  ws: vkv_sigma_workspace_size(B, nblk) bytes, 256-byte aligned.
+ *
+ * vkv_sigma_select: the sigma tier of the first n_closed rows: rows
+ * [0, min(nsink, n_closed)) (the sinks) plus the m rows of largest sigma among
+ * the other closed rows (ties: the lower row), written ascending to kept
+ * [B, K] int32, K = min(nsink, n) + min(m, n - min(nsink, n)), n = n_closed.
+ * The tier of the rows closed so far equals the one kept incrementally as
+ * blocks close (Corollary (Ranking stationarity)), so one call after each
+ * close rebalances it.
+ */
+#define VKV_SIGMA_BLOCK 4096
+int vkv_sigma_workspace_size(int64_t B, int64_t nblk, size_t* bytes);
+int vkv_sigma_close(vkv_ctx* ctx, const uint16_t* cache, int64_t B, int64_t T, int64_t cache_row_stride,
+                    int64_t cache_batch_stride, int64_t t0, int64_t nblk, int32_t kappa, void* ws,
+                    size_t ws_bytes, double* sigma, int64_t sigma_stride, void* stream);
+int vkv_sigma_select(vkv_ctx* ctx, const double* sigma, int64_t B, int64_t n_closed, int64_t sigma_stride,
+                     int64_t m, int32_t nsink, int32_t* kept, void* stream);
+
+/*
+ * One decode step on a given tier-1 set (the per-decode-step line of the
+ * deployment specification's request lifecycle): the k rows kept[b] of the
+ * archive [0, A) (ascending, for instance the sigma tier) and the recent
+ * window are attended; query_prep -> score (ub at cert_mult) -> the exact
+ * maximum logit s*_h over kept and window (as vkv_row_max) -> the calibrated
+ * trigger against s*_h with the optional top-j cap (as vkv_trigger, kept in
+ * place of S) -> attention over kept, window and fired rows (as vkv_attend).
+ * kept must be ascending and inside [0, A) (VKV_DEBUG_ROWS checks it after
+ * the step); the other arguments and results are those of the calls named.
+ * ws: vkv_workspace_size(st, k, cap) bytes.
+ */
+int vkv_step_run_kept(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k,
+                      const int32_t* kept, float* key, float* ub, float cert_mult, double* smax,
+                      int32_t* argmax, int64_t topj, int32_t* fired, int32_t* fired_count, int64_t cap,
+                      float scale, uint16_t* out, float* lse, void* stream);
+
 /* Bytes of device workspace a step with budget k and admission capacity cap
  * (0 without admission) needs; the workspace must be 256-byte aligned. */
 int vkv_workspace_size(const vkv_step* st, int64_t k, int64_t cap, size_t* bytes);

@@ -20,7 +20,8 @@ __all__ = [
     "VKV_MODE_ROPE", "VKV_MODE_DIGEST", "VKV_MODE_ROPE_DIGEST", "VkvError", "Context", "Step",
     "lib_path", "load", "digest_build", "workspace_size", "query_prep", "score", "select", "admit", "attend",
     "step_run", "step_run_static", "check_rows", "row_max", "trigger", "required_inflation", "conformal_z",
-    "step_run_trigger", "sketch_workspace_size", "sketch_basis", "exported_symbols",
+    "step_run_trigger", "sketch_workspace_size", "sketch_basis", "sigma_workspace_size", "sigma_close",
+    "sigma_tier_size", "sigma_select", "step_run_kept", "SIGMA_BLOCK", "exported_symbols",
 ]
 
 VKV_MODE_ROPE, VKV_MODE_DIGEST, VKV_MODE_ROPE_DIGEST = 1, 2, 3
@@ -34,8 +35,10 @@ exported_symbols = (
     "vkv_digest_build", "vkv_workspace_size", "vkv_query_prep", "vkv_score", "vkv_select", "vkv_admit",
     "vkv_attend", "vkv_step_run", "vkv_step_run_static", "vkv_check_rows", "vkv_set_timing", "vkv_score_timing",
     "vkv_row_max", "vkv_trigger", "vkv_required_inflation", "vkv_conformal_z", "vkv_step_run_trigger",
-    "vkv_sketch_workspace_size", "vkv_sketch_basis",
+    "vkv_sketch_workspace_size", "vkv_sketch_basis", "vkv_sigma_workspace_size", "vkv_sigma_close",
+    "vkv_sigma_select", "vkv_step_run_kept",
 )
+SIGMA_BLOCK = 4096
 
 
 class VkvError(RuntimeError):
@@ -103,6 +106,11 @@ def load():
                                          f32, P, P, P]
     lib.vkv_sketch_workspace_size.argtypes = [i32, ctypes.POINTER(ctypes.c_size_t)]
     lib.vkv_sketch_basis.argtypes = [P, P, i64, i32, i32, P, ctypes.c_size_t, P, P, P]
+    lib.vkv_sigma_workspace_size.argtypes = [i64, i64, ctypes.POINTER(ctypes.c_size_t)]
+    lib.vkv_sigma_close.argtypes = [P, P, i64, i64, i64, i64, i64, i64, i32, P, ctypes.c_size_t, P, i64, P]
+    lib.vkv_sigma_select.argtypes = [P, P, i64, i64, i64, i64, i32, P, P]
+    lib.vkv_step_run_kept.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P, f32, P, P, i64, P, P, i64,
+                                      ctypes.c_float, P, P, P]
     lib.vkv_set_timing.argtypes = [P, ctypes.c_int]
     lib.vkv_score_timing.argtypes = [P, ctypes.POINTER(ctypes.c_float), ctypes.c_int]
     for name in exported_symbols:
@@ -353,6 +361,44 @@ def sketch_basis(ctx: Context, q: torch.Tensor, r: int, iters: int, ws: torch.Te
     m = q.numel() // D_LAT
     ctx.check(ctx.lib.vkv_sketch_basis(ctx.handle, _ptr(q), int(m), int(r), int(iters), _ptr(ws), ws.numel(),
                                        _ptr(P), _ptr(energy), _stream(stream)))
+
+
+def sigma_workspace_size(B: int, nblk: int) -> int:
+    lib = load()
+    n = ctypes.c_size_t(0)
+    rc = lib.vkv_sigma_workspace_size(int(B), int(nblk), ctypes.byref(n))
+    if rc != 0:
+        raise VkvError(rc, lib.vkv_last_error(None).decode())
+    return int(n.value)
+
+
+def sigma_close(ctx: Context, cache: torch.Tensor, t0: int, nblk: int, kappa: int, ws: torch.Tensor,
+                sigma: torch.Tensor, stream=None):
+    """vkv_sigma_close over cache [B, T, row_stride>=576] bf16 into sigma [B, S] fp64."""
+    B, T = cache.shape[0], cache.shape[1]
+    ctx.check(ctx.lib.vkv_sigma_close(ctx.handle, _ptr(cache), B, T, cache.stride(1), cache.stride(0), int(t0),
+                                      int(nblk), int(kappa), _ptr(ws), ws.numel(), _ptr(sigma), sigma.stride(0),
+                                      _stream(stream)))
+
+
+def sigma_tier_size(n_closed: int, m: int, nsink: int = 4) -> int:
+    lo = min(nsink, n_closed)
+    return lo + min(m, n_closed - lo)
+
+
+def sigma_select(ctx: Context, sigma: torch.Tensor, n_closed: int, m: int, nsink: int, kept: torch.Tensor,
+                 stream=None):
+    """vkv_sigma_select: kept [B, sigma_tier_size(n_closed, m, nsink)] int32."""
+    ctx.check(ctx.lib.vkv_sigma_select(ctx.handle, _ptr(sigma), sigma.shape[0], int(n_closed), sigma.stride(0),
+                                       int(m), int(nsink), _ptr(kept), _stream(stream)))
+
+
+def step_run_kept(ctx: Context, step: Step, ws: torch.Tensor, k: int, kept, key, ub, cert_mult: float, smax,
+                  argmax, topj: int, fired, fired_count, cap: int, scale: float, out, lse, stream=None):
+    ctx.check(ctx.lib.vkv_step_run_kept(ctx.handle, step.ref, _ptr(ws), ws.numel(), int(k), _ptr(kept), _ptr(key),
+                                        _ptr(ub), float(cert_mult), _ptr(smax), _ptr(argmax), int(topj),
+                                        _ptr(fired), _ptr(fired_count), int(cap), float(scale), _ptr(out),
+                                        _ptr(lse), _stream(stream)))
 
 
 def check_rows(ctx: Context, step: Step, k: int, sel: Optional[torch.Tensor],

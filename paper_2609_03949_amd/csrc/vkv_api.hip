@@ -836,6 +836,95 @@ int vkv_step_run_trigger(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_b
     return debug_check_adm(ctx, st, k, sel, fired, fired_count, cap, s);
 }
 
+int vkv_sigma_workspace_size(int64_t B, int64_t nblk, size_t* bytes) {
+    if (!bytes) return fail(nullptr, VKV_E_ARG, "bytes is NULL");
+    if (B < 0 || nblk < 0 || B > 65535 || nblk > 65535) return fail(nullptr, VKV_E_SHAPE, "B or nblk out of range");
+    *bytes = up256(sigma_workspace_bytes(B, nblk));
+    return VKV_OK;
+}
+
+int vkv_sigma_close(vkv_ctx* ctx, const uint16_t* cache, int64_t B, int64_t T, int64_t cache_row_stride,
+                    int64_t cache_batch_stride, int64_t t0, int64_t nblk, int32_t kappa, void* ws, size_t ws_bytes,
+                    double* sigma, int64_t sigma_stride, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    if (!cache) return fail(ctx, VKV_E_ARG, "cache is NULL");
+    if (B < 1 || B > 65535 || T < 1 || T >= (1ll << 31)) return fail(ctx, VKV_E_SHAPE, "B=%lld T=%lld", (long long)B, (long long)T);
+    if (!al16(cache) || cache_row_stride < D_ROW || cache_row_stride % 8 || cache_batch_stride % 8 ||
+        (B > 1 && cache_batch_stride < T * cache_row_stride))
+        return fail(ctx, VKV_E_ALIGN, "cache strides");
+    if (t0 < 0 || t0 % VKV_SIGMA_BLOCK || nblk < 0 || nblk > 65535 || t0 + nblk * VKV_SIGMA_BLOCK > T)
+        return fail(ctx, VKV_E_SHAPE, "t0=%lld nblk=%lld: blocks of %d rows from a multiple of %d, within T=%lld",
+                    (long long)t0, (long long)nblk, VKV_SIGMA_BLOCK, VKV_SIGMA_BLOCK, (long long)T);
+    if (kappa < 1 || kappa > VKV_SIGMA_BLOCK / 2) return fail(ctx, VKV_E_ARG, "kappa=%d outside [1, %d]", kappa, VKV_SIGMA_BLOCK / 2);
+    if (nblk == 0) return VKV_OK;
+    if (!sigma || ((uintptr_t)sigma & 7u)) return fail(ctx, VKV_E_ARG, "sigma must be an 8-byte aligned device pointer");
+    if (sigma_stride < t0 + nblk * VKV_SIGMA_BLOCK) return fail(ctx, VKV_E_ARG, "sigma_stride smaller than the closed rows");
+    int rc = check_ws(ctx, ws, ws_bytes, up256(sigma_workspace_bytes(B, nblk)));
+    if (rc) return rc;
+    SigmaArgs a{};
+    a.cache = cache;
+    a.crs = cache_row_stride;
+    a.cbs = cache_batch_stride;
+    a.t0 = t0;
+    a.nblk = nblk;
+    a.kappa = kappa;
+    a.B = (int)B;
+    a.part = reinterpret_cast<double*>(ws);
+    a.sigma = sigma;
+    a.sstride = sigma_stride;
+    HIP_TRY(ctx, launch_sigma(a, (hipStream_t)stream));
+    return VKV_OK;
+}
+
+int vkv_sigma_select(vkv_ctx* ctx, const double* sigma, int64_t B, int64_t n_closed, int64_t sigma_stride, int64_t m,
+                     int32_t nsink, int32_t* kept, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    if (B < 1 || B > 65535 || n_closed < 0 || n_closed >= (1ll << 31)) return fail(ctx, VKV_E_SHAPE, "B or n_closed out of range");
+    if (m < 0 || nsink < 0) return fail(ctx, VKV_E_ARG, "m and nsink must be >= 0");
+    const int64_t lo = std::min<int64_t>(nsink, n_closed);
+    const int64_t K = lo + std::min<int64_t>(m, n_closed - lo);
+    if (K == 0) return VKV_OK;
+    if (!sigma || !kept || ((uintptr_t)sigma & 7u)) return fail(ctx, VKV_E_ARG, "sigma and kept are required");
+    if (sigma_stride < n_closed) return fail(ctx, VKV_E_ARG, "sigma_stride smaller than n_closed");
+    SigmaSelArgs a{};
+    a.sigma = sigma;
+    a.sstride = sigma_stride;
+    a.n = n_closed;
+    a.m = m;
+    a.nsink = nsink;
+    a.kept = kept;
+    a.kstride = K;
+    a.B = (int)B;
+    HIP_TRY(ctx, launch_sigma_select(a, (hipStream_t)stream));
+    return VKV_OK;
+}
+
+int vkv_step_run_kept(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k, const int32_t* kept,
+                      float* key, float* ub, float cert_mult, double* smax, int32_t* argmax, int64_t topj,
+                      int32_t* fired, int32_t* fired_count, int64_t cap, float scale, uint16_t* out, float* lse,
+                      void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    int rc;
+    if ((rc = check_score(ctx, st, ws, ws_bytes, ub, cert_mult))) return rc;
+    if (!ub) return fail(ctx, VKV_E_ARG, "the trigger needs ub");
+    if ((rc = check_trigger(ctx, st, ws, ws_bytes, k, kept, ub, cert_mult, smax, topj, fired, fired_count, cap)))
+        return rc;
+    if (!argmax) return fail(ctx, VKV_E_ARG, "argmax is required");
+    if ((rc = check_attend(ctx, st, ws, ws_bytes, k, kept, fired, fired_count, cap, scale, out, lse))) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    char* w = (char*)ws;
+    const Chunk all{0, st->B};
+    const WsLayout L = layout(st, k, cap);
+    HIP_TRY(ctx, run_prep(st, w, all, s));
+    HIP_TRY(ctx, run_score(st, w, all, key, ub, cert_mult, s));
+    HIP_TRY(ctx, launch_mark_tier(reinterpret_cast<uint8_t*>(w + L.flags), flag_stride(L.A), L.A, (int)st->B, kept, k, s));
+    HIP_TRY(ctx, run_row_max(st, kept, k, 0, 1, smax, argmax, s));
+    HIP_TRY(ctx, run_trigger(st, w, k, kept, ub, cert_mult, smax, topj, fired, fired_count, cap, s));
+    HIP_TRY(ctx, run_attend(st, w, all, k, kept, fired, fired_count, cap, scale, out, lse, s));
+    if ((rc = debug_check_sel(ctx, st, k, kept, s))) return rc;
+    return debug_check_adm(ctx, st, k, kept, fired, fired_count, cap, s);
+}
+
 int vkv_sketch_workspace_size(int32_t r, size_t* bytes) {
     if (!bytes) return fail(nullptr, VKV_E_ARG, "bytes is NULL");
     if (r < 32 || r > 512 || r % 32) return fail(nullptr, VKV_E_UNSUPPORTED, "r=%d: need a multiple of 32 in [32, 512]", r);

@@ -293,6 +293,30 @@ hipError_t launch_attend(const AttendArgs& a, hipStream_t s);
 hipError_t launch_row_max(const RowMaxArgs& a, hipStream_t s);
 hipError_t launch_trigger(const SelectArgs& a, hipStream_t s);
 hipError_t launch_inflation(const InflArgs& a, hipStream_t s);
+struct SigmaArgs {
+    const uint16_t* cache;
+    int64_t crs, cbs;      // cache row / batch strides (elements)
+    int64_t t0, nblk;      // first row (a multiple of 4096) and number of blocks to close
+    int kappa, B;
+    double* part;          // [B, nblk, 8, 4096] squared residuals per channel group
+    double* sigma;         // [B, sstride]
+    int64_t sstride;
+};
+
+struct SigmaSelArgs {
+    const double* sigma;
+    int64_t sstride, n, m, nsink;
+    int32_t* kept;
+    int64_t kstride;
+    int B;
+};
+
+size_t sigma_workspace_bytes(int64_t B, int64_t nblk);
+hipError_t launch_sigma(const SigmaArgs& a, hipStream_t s);
+hipError_t launch_sigma_select(const SigmaSelArgs& a, hipStream_t s);
+hipError_t launch_mark_tier(uint8_t* flags, int64_t fstride, int64_t A, int B, const int32_t* sel, int64_t k,
+                            hipStream_t s);
+
 size_t sketch_workspace_bytes(int r);
 hipError_t launch_sketch(const uint16_t* q, int64_t m, int r, int iters, void* ws, uint16_t* P, double* energy,
                          hipStream_t s);

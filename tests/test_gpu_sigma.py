@@ -1,0 +1,240 @@
+"""GPU parity of the query-independent tier-1 selector (Sec. 4.1, the sigma
+equation; Corollary (Ranking stationarity); the block close and per-step lines
+of the deployment specification) and of a decode step on the tier it keeps.
+
+Bars:
+  * sigma (fp64 FFT on the GPU, fp64 DFT sums in the oracle): per row within
+    1e-12 of the block's Frobenius norm (both sides are accurate to a few
+    hundred ulps of it; a wrong bin, sign or index is off by O(1));
+  * closing blocks one call at a time gives the same bits as one call;
+  * the tier: on the GPU's own sigma it equals the oracle's selection bit for
+    bit (same inputs, exact order, ties to the lower row); against the
+    oracle's sigma it is equal wherever the m-th gap exceeds the sigma
+    tolerance, and otherwise a valid top-m within it;
+  * the kept-tier step: s*_h and its rows bit-exact, fired sets bit-exact,
+    outputs within the step tolerance.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import _checks
+import oracle
+import paper_2609_03949_amd as vkv
+from paper_2609_03949_amd import synth
+
+from _harness import gpu_index, host_inputs
+
+pytestmark = pytest.mark.gpu
+NB = vkv.SIGMA_BLOCK
+
+
+def say(msg):
+    print(f"[gpu-sigma] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    c = vkv.Context(0)
+    yield c
+    c.close()
+
+
+def _close(ctx, cache, t0, nblk, kappa, sigma=None):
+    B, T = cache.shape[0], cache.shape[1]
+    if sigma is None:
+        sigma = torch.full((B, T), -1.0, dtype=torch.float64, device="cuda")
+    ws = torch.empty(max(vkv.sigma_workspace_size(B, nblk), 256), dtype=torch.uint8, device="cuda")
+    vkv.sigma_close(ctx, cache, t0, nblk, kappa, ws, sigma)
+    torch.cuda.synchronize()
+    return sigma
+
+
+def _tier(ctx, sigma, n, m, nsink=4):
+    B = sigma.shape[0]
+    K = vkv.sigma_tier_size(n, m, nsink)
+    kept = torch.full((B, max(K, 1)), -7, dtype=torch.int32, device="cuda")
+    vkv.sigma_select(ctx, sigma, n, m, nsink, kept)
+    torch.cuda.synchronize()
+    return kept.cpu().numpy()[:, :K]
+
+
+def _check_sigma(sig_g, cache_bits, n, kappa):
+    """Per block: |sigma_gpu - sigma_oracle| <= 1e-12 * ||block||_F; returns the oracle's sigma."""
+    so = oracle.sigma_close(cache_bits, n, kappa)
+    worst = 0.0
+    for b0 in range(0, n, NB):
+        blk = oracle.decode_bf16(cache_bits[b0:b0 + NB, 512:])
+        fro = float(np.linalg.norm(blk))
+        err = float(np.max(np.abs(sig_g[b0:b0 + NB] - so[b0:b0 + NB])))
+        assert err <= 1e-12 * fro, (b0, err, fro)
+        worst = max(worst, err / fro)
+    return so, worst
+
+
+@pytest.mark.parametrize("kappa", [16, 64, 1, 2048])
+def test_sigma_close_matches_the_oracle(ctx, kappa):
+    say(f"sigma close kappa={kappa}")
+    cfg = synth.CONFIGS["cfg3"].with_(H=8)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=3 * NB + 100)
+    sig = _close(ctx, wl["cache"], 0, 3, kappa)
+    s = sig.cpu().numpy()
+    cache = synth.to_numpy_bits(wl["cache"])
+    for b in range(2):
+        _, worst = _check_sigma(s[b], cache[b], 3 * NB, kappa)
+        assert np.all(s[b, 3 * NB:] == -1.0)          # the open tail is not written
+        say(f"  seq {b}: max |dsigma| / ||block||_F = {worst:.2e}")
+
+
+def test_blockwise_close_equals_one_shot(ctx):
+    """Closing blocks one call at a time (as decode closes them) writes the
+    same bits as one call over all of them, in any order."""
+    cfg = synth.CONFIGS["cfg3"].with_(H=8)
+    wl = synth.make_workload(cfg, "cuda", B=3, T=4 * NB + 5)
+    one = _close(ctx, wl["cache"], 0, 4, 16)
+    inc = torch.full_like(one, -1.0)
+    for j in (2, 0, 3, 1):
+        _close(ctx, wl["cache"], j * NB, 1, 16, inc)
+    assert torch.equal(one[:, :4 * NB], inc[:, :4 * NB])
+
+
+def test_sigma_ranks_planted_jumps_first(ctx):
+    """A smooth branch (bins below kappa) with rows that jump off it: the
+    jumping rows lead the sigma tier (GPU end to end)."""
+    T = 2 * NB
+    t = torch.arange(T, dtype=torch.float64)[:, None]
+    ch = torch.arange(64, dtype=torch.float64)[None, :]
+    smooth = torch.cos(2 * np.pi * (1 + ch % 5) * (t % NB) / NB + ch)
+    g = torch.Generator().manual_seed(11)
+    jumps = torch.randperm(T - 8, generator=g)[:40].sort().values + 8
+    smooth[jumps, :16] += 1.5
+    cache = torch.zeros(1, T, 576, dtype=torch.bfloat16)
+    cache[0, :, 512:] = smooth.to(torch.bfloat16)
+    cache = cache.cuda()
+    sig = _close(ctx, cache, 0, 2, 16)
+    kept = _tier(ctx, sig, T, 40)
+    assert np.array_equal(kept[0, 4:], jumps.numpy())
+
+
+@pytest.mark.parametrize("n,m,nsink", [(3 * NB, 1000, 4), (3 * NB, 0, 4), (3 * NB, 3 * NB, 4), (3 * NB, 3 * NB - 4, 4),
+                                       (NB, 17, 0), (2, 5, 4), (0, 5, 4), (3 * NB, 4095, 4096)])
+def test_sigma_select_against_the_oracle(ctx, n, m, nsink):
+    say(f"sigma select n={n} m={m} nsink={nsink}")
+    B = 2
+    g = torch.Generator().manual_seed(n + m)
+    # exact ties: small integers (and one all-equal sequence)
+    sig = torch.randint(0, 50, (B, max(n, 1)), generator=g).to(torch.float64)
+    sig[1] = 3.0
+    sig = sig.cuda()
+    kept = _tier(ctx, sig, n, m, nsink)
+    s = sig.cpu().numpy()
+    for b in range(B):
+        want = oracle.sigma_select(s[b, :n], m, nsink)
+        assert np.array_equal(kept[b], want), b
+
+
+def test_tier_on_gpu_sigma_against_the_oracle_sigma(ctx):
+    cfg = synth.CONFIGS["cfg3"].with_(H=8)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=4 * NB)
+    n, m = 4 * NB, 1500
+    sig = _close(ctx, wl["cache"], 0, 4, 16)
+    kept = _tier(ctx, sig, n, m)
+    s = sig.cpu().numpy()
+    cache = synth.to_numpy_bits(wl["cache"])
+    for b in range(2):
+        assert np.array_equal(kept[b], oracle.sigma_select(s[b], m))
+        so, _ = _check_sigma(s[b], cache[b], n, 16)
+        want = oracle.sigma_select(so, m)
+        if not np.array_equal(kept[b], want):
+            # only rows within the sigma tolerance of the m-th value may differ
+            tol = 1e-12 * float(np.linalg.norm(oracle.decode_bf16(cache[b][:, 512:])))
+            order = np.sort(so[4:])[::-1]
+            assert abs(order[m - 1] - order[m]) <= 2 * tol
+        assert np.all(kept[b][:4] == np.arange(4))
+
+
+def test_incremental_close_and_rebalance(ctx):
+    """Decode closes one block at a time and rebalances with one global top-m
+    after each close: every tier equals the oracle's incremental tier, which
+    equals the one-shot tier (Corollary (Ranking stationarity))."""
+    cfg = synth.CONFIGS["cfg3"].with_(H=8)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=5 * NB)
+    m = 900
+    sig = torch.full((2, 5 * NB), -1.0, dtype=torch.float64, device="cuda")
+    tiers = []
+    for j in range(5):
+        _close(ctx, wl["cache"], j * NB, 1, 64, sig)
+        tiers.append(_tier(ctx, sig, (j + 1) * NB, m))
+    s = sig.cpu().numpy()
+    for b in range(2):
+        inc = oracle.sigma_select_incremental(s[b], m)
+        for j in range(5):
+            assert np.array_equal(tiers[j][b], inc[j]), (b, j)
+
+
+def _kept_step(ctx, wl, kept_t, cm, topj):
+    pack = gpu_index(ctx, wl, True)
+    index, has_rope, eta, eps, gam = pack
+    step = vkv.Step(wl["cache"], wl["q_lat"], wl["q_rope"], wl["W"], wl["mode"], wl["r"], index=index,
+                    index_has_rope=has_rope, P=wl["P"], eta=eta, eps=eps, gam=gam)
+    B, H, A = wl["B"], wl["H"], wl["A"]
+    k = kept_t.shape[1]
+    ws = vkv.alloc_workspace(step, k, A)
+    d = dict(dtype=torch.float32, device="cuda")
+    key = torch.empty(B, A, **d)
+    ub = torch.empty(B, A, **d)
+    smax = torch.empty(B, H, dtype=torch.float64, device="cuda")
+    arg = torch.empty(B, H, dtype=torch.int32, device="cuda")
+    fired = torch.empty(B, A, dtype=torch.int32, device="cuda")
+    cnt = torch.empty(B, dtype=torch.int32, device="cuda")
+    out = torch.empty(B, H, 512, dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty(B, H, **d)
+    vkv.step_run_kept(ctx, step, ws, k, kept_t, key, ub, cm, smax, arg, topj, fired, cnt, A, wl["scale"], out, lse)
+    torch.cuda.synchronize()
+    return dict(smax=smax.cpu().numpy(), arg=arg.cpu().numpy(), fired=fired.cpu().numpy(), cnt=cnt.cpu().numpy(),
+                out=out.float().cpu().numpy().astype(np.float64), lse=lse.cpu().numpy().astype(np.float64))
+
+
+@pytest.mark.parametrize("cm,topj", [(0.12, 16), (0.12, 0), (1.0, 0)])
+def test_step_on_the_sigma_tier_matches_the_oracle(ctx, cm, topj):
+    """The deployed per-step path: sigma tier of the closed blocks + the open
+    tail attended, index scan, calibrated trigger against the tier's maximum
+    logit, top-j fetch, attention."""
+    say(f"kept-tier step cert_mult={cm} topj={topj}")
+    cfg = synth.CONFIGS["cfg3"].with_(H=32, W=300)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=2 * NB + 300)
+    A = wl["A"]
+    assert A == 2 * NB
+    sig = _close(ctx, wl["cache"], 0, 2, 16)
+    kept_np = _tier(ctx, sig, A, 508)
+    kept_t = torch.from_numpy(kept_np).cuda().contiguous()
+    g = _kept_step(ctx, wl, kept_t, cm, topj)
+    cache, q_lat, q_rope, P = host_inputs(wl, [0, 1])
+    idx, eta, eps, gam = oracle.digest_build(cache, P, wl["r"], with_rope=True)
+    o = oracle.step_kept(cache, q_lat, q_rope, idx, P, wl["r"], wl["mode"], wl["W"], kept_np, wl["scale"],
+                         eta, eps, gam, cm, topj)
+    for b in range(2):
+        assert np.array_equal(g["smax"][b], o["smax"][b]), b
+        assert np.array_equal(g["arg"][b], o["argmax"][b]), b
+        assert int(g["cnt"][b]) == o["fired_count"][b], (b, int(g["cnt"][b]), o["fired_count"][b])
+        assert np.array_equal(g["fired"][b, :o["fired_count"][b]], o["fired"][b]), b
+        assert _checks.rel_l2(g["out"][b], o["out"][b]) < _checks.OUT_TOL
+        assert np.all(np.abs(g["lse"][b] - o["lse"][b]) < _checks.LSE_TOL)
+    say(f"  fired per sequence: {[int(c) for c in g['cnt']]} of {A - kept_np.shape[1]} archived outside the tier")
+
+
+def test_sigma_argument_errors(ctx):
+    cache = torch.zeros(1, 2 * NB, 576, dtype=torch.bfloat16, device="cuda")
+    sig = torch.zeros(1, 2 * NB, dtype=torch.float64, device="cuda")
+    ws = torch.empty(vkv.sigma_workspace_size(1, 2), dtype=torch.uint8, device="cuda")
+    for t0, nblk, kappa in ((100, 1, 16), (0, 3, 16), (0, 1, 0), (0, 1, 2049), (NB, 2, 16)):
+        with pytest.raises(vkv.VkvError):
+            vkv.sigma_close(ctx, cache, t0, nblk, kappa, ws, sig)
+    small = torch.empty(vkv.sigma_workspace_size(1, 1), dtype=torch.uint8, device="cuda")
+    with pytest.raises(vkv.VkvError) as ei:
+        vkv.sigma_close(ctx, cache, 0, 2, 16, small, sig)
+    assert ei.value.code == -7
