@@ -216,6 +216,20 @@ int vkv_step_run_kept(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_byte
                       int32_t* argmax, int64_t topj, int32_t* fired, int32_t* fired_count, int64_t cap,
                       float scale, uint16_t* out, float* lse, void* stream);
 
+/*
+ * The all-layer CSR pack of row lists (Sec. 4.3, the decode step's all-layer
+ * CSR pack): n lists of capacity cap, lists [n, cap] int32 (for instance the
+ * fired rows of every layer and sequence of a step, each list from
+ * vkv_trigger / vkv_step_run_kept), counts [n] (the lists' true counts; a
+ * count above cap packs cap rows, a negative one none) ->
+ * offsets [n + 1] = the exclusive prefix sums of the packed lengths and
+ * packed [offsets[n]] = the lists' rows back to back.  Worst-case buffers
+ * (packed of n * cap) make it fit for graph capture: it launches two kernels,
+ * never synchronises and allocates nothing.  n <= 65535.
+ */
+int vkv_pack_rows(vkv_ctx* ctx, const int32_t* lists, const int32_t* counts, int64_t n, int64_t cap,
+                  int32_t* offsets, int32_t* packed, void* stream);
+
 /* Bytes of device workspace a step with budget k and admission capacity cap
  * (0 without admission) needs; the workspace must be 256-byte aligned. */
 int vkv_workspace_size(const vkv_step* st, int64_t k, int64_t cap, size_t* bytes);

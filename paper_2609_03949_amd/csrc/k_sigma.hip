@@ -24,6 +24,10 @@
 // an MSB-first radix select over the fp64 bit patterns (sigma >= 0, so the
 // bits order like the values) finds the m-th key, then one ordered pass
 // writes the rows above it and the first rows equal to it, ascending.
+//
+// Also here: the flags of a caller's tier (for the step on a given kept set)
+// and the all-layer CSR pack of row lists (offsets by one block's prefix sum,
+// then one copy per list).
 #include "vkv_internal.h"
 
 namespace vkv {
@@ -318,6 +322,54 @@ hipError_t launch_mark_tier(uint8_t* flags, int64_t fstride, int64_t A, int B, c
     if (e != hipSuccess || k == 0) return e;
     const unsigned g2 = (unsigned)((k + 255) / 256 < 1024 ? (k + 255) / 256 : 1024);
     hipLaunchKernelGGL(tier_mark_kernel, dim3(g2, (unsigned)B), dim3(256), 0, s, flags, fstride, A, sel, k);
+    return hipGetLastError();
+}
+
+}  // namespace vkv
+
+namespace vkv {
+
+// ------------------------------------------------ all-layer CSR pack of row lists
+
+// offsets[i] = sum_{j < i} min(max(counts[j], 0), cap), i in [0, n]; one block, 1024 threads
+__global__ __launch_bounds__(1024) void pack_offsets_kernel(const int32_t* counts, int64_t n, int64_t cap,
+                                                            int32_t* offsets) {
+    __shared__ int64_t s_part[1024];
+    const int tid = threadIdx.x;
+    const int64_t per = (n + 1023) / 1024;
+    const int64_t i0 = tid * per, i1 = min(n, i0 + per);
+    int64_t s = 0;
+    for (int64_t i = i0; i < i1; ++i) {
+        const int64_t c = counts[i];
+        s += c < 0 ? 0 : (c < cap ? c : cap);
+    }
+    s_part[tid] = s;
+    __syncthreads();
+    int64_t base = 0;
+    for (int j = 0; j < tid; ++j) base += s_part[j];
+    for (int64_t i = i0; i < i1; ++i) {
+        offsets[i] = (int32_t)base;
+        const int64_t c = counts[i];
+        base += c < 0 ? 0 : (c < cap ? c : cap);
+    }
+    if (tid == 1023) offsets[n] = (int32_t)base;
+}
+
+__global__ __launch_bounds__(256) void pack_copy_kernel(const int32_t* lists, const int32_t* offsets, int64_t cap,
+                                                        int32_t* packed) {
+    const int64_t i = blockIdx.y;
+    const int64_t len = offsets[i + 1] - offsets[i];
+    for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < len; t += (int64_t)gridDim.x * 256)
+        packed[offsets[i] + t] = lists[i * cap + t];
+}
+
+hipError_t launch_pack_rows(const int32_t* lists, const int32_t* counts, int64_t n, int64_t cap, int32_t* offsets,
+                            int32_t* packed, hipStream_t s) {
+    hipLaunchKernelGGL(pack_offsets_kernel, dim3(1), dim3(1024), 0, s, counts, n, cap, offsets);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || n == 0 || cap == 0) return e;
+    const unsigned gx = (unsigned)((cap + 255) / 256 < 64 ? (cap + 255) / 256 : 64);
+    hipLaunchKernelGGL(pack_copy_kernel, dim3(gx, (unsigned)n), dim3(256), 0, s, lists, offsets, cap, packed);
     return hipGetLastError();
 }
 

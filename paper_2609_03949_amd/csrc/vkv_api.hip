@@ -925,6 +925,16 @@ int vkv_step_run_kept(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_byte
     return debug_check_adm(ctx, st, k, kept, fired, fired_count, cap, s);
 }
 
+int vkv_pack_rows(vkv_ctx* ctx, const int32_t* lists, const int32_t* counts, int64_t n, int64_t cap,
+                  int32_t* offsets, int32_t* packed, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    if (n < 0 || n > 65535 || cap < 0 || n * cap >= (1ll << 31)) return fail(ctx, VKV_E_SHAPE, "n or cap out of range");
+    if (!offsets || (n > 0 && !counts) || (n > 0 && cap > 0 && (!lists || !packed)))
+        return fail(ctx, VKV_E_ARG, "lists, counts, offsets and packed are required");
+    HIP_TRY(ctx, launch_pack_rows(lists, counts, n, cap, offsets, packed, (hipStream_t)stream));
+    return VKV_OK;
+}
+
 int vkv_sketch_workspace_size(int32_t r, size_t* bytes) {
     if (!bytes) return fail(nullptr, VKV_E_ARG, "bytes is NULL");
     if (r < 32 || r > 512 || r % 32) return fail(nullptr, VKV_E_UNSUPPORTED, "r=%d: need a multiple of 32 in [32, 512]", r);

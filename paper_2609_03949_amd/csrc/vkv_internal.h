@@ -317,6 +317,9 @@ hipError_t launch_sigma_select(const SigmaSelArgs& a, hipStream_t s);
 hipError_t launch_mark_tier(uint8_t* flags, int64_t fstride, int64_t A, int B, const int32_t* sel, int64_t k,
                             hipStream_t s);
 
+hipError_t launch_pack_rows(const int32_t* lists, const int32_t* counts, int64_t n, int64_t cap, int32_t* offsets,
+                            int32_t* packed, hipStream_t s);
+
 size_t sketch_workspace_bytes(int r);
 hipError_t launch_sketch(const uint16_t* q, int64_t m, int r, int iters, void* ws, uint16_t* P, double* energy,
                          hipStream_t s);
