@@ -232,8 +232,22 @@ __device__ __forceinline__ float wave_max16(float m) {
     return m;
 }
 
+// __shfl_xor whose lane arithmetic the compiler cannot share between call
+// sites: shared lane addresses would stay live across the scan loops and
+// crowd out the registers the loops need
+__device__ __forceinline__ float shfl_xor_local(float v, int o) {
+    int ln = __lane_id();
+    asm volatile("" : "+v"(ln));
+    return __int_as_float(__builtin_amdgcn_ds_bpermute((ln ^ o) << 2, __float_as_int(v)));
+}
+__device__ __forceinline__ float shfl_local(float v, int src) {
+    int ln = src;
+    asm volatile("" : "+v"(ln));
+    return __int_as_float(__builtin_amdgcn_ds_bpermute(ln << 2, __float_as_int(v)));
+}
+
 __device__ __forceinline__ float wave_max_all(float m) {
-    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, shfl_xor_local(m, o));
     return m;
 }
 
@@ -622,19 +636,18 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
             coef = fmaxf(coef, hsf[ht]);
         }
 #pragma unroll
-        for (int o = 1; o < 16; o <<= 1) coef = fmaxf(coef, __shfl_xor(coef, o));
+        for (int o = 1; o < 16; o <<= 1) coef = fmaxf(coef, shfl_xor_local(coef, o));
     }
     wait_vmcnt<0>();   // the first tiles (and the head scalars) resident
 
     TileOut to{-INFINITY, INFINITY, 0.f, 0.f};
     // row of group q (tiles 4q..4q+3) held by this lane: row c of tile 4q + g
     auto group_row = [&](int q) { return r0 + (int64_t)(TST * 16) * (4 * q + g) + c; };
-    auto group_out = [&](int q, float m, float s2, float u, float bm) {
+    auto group_out = [&](int q, float m, float s2, float u) {
         if (group_row(q) < bs1) {
             to.nu2m = fmaxf(to.nu2m, s2);
             to.kmax = fmaxf(to.kmax, m);
             to.kmin = fminf(to.kmin, m);
-            if (UB) to.bmm = fmaxf(to.bmm, bm);
         }
         s_key[64 * q + lane] = m;
         if (UB) s_ub[64 * q + lane] = u;
@@ -642,6 +655,11 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
 
     bf16x8_t xf[KS];
     float rvc = 0.f;
+    // (UB) the largest row scalar this lane has seen (scalar g of the rows c):
+    // the bound term's maximum is taken as sum_g (max over heads of scalar g of
+    // the heads) x (max over rows of scalar g of the rows), no smaller than the
+    // largest B_h(u) and cheaper to keep than per-row sums
+    float rvmax = 0.f;
     read_stage(0, xf, rvc);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // stage read out before it is refilled
     if (NST < ntl) issue(NST, 0);
@@ -652,18 +670,19 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
     // those shapes take the run-time loop throughout)
     const int nrun = (KS <= 6 && ntl > NST) ? (ntl - NST - 1) / RUN : 0;
     for (int s = 0; s < nrun; ++s) {
-        float pmv[RUN], psv[RUN], puv[RUN], pbv[RUN];
+        float pmv[RUN], psv[RUN], puv[RUN];
 #pragma unroll
         for (int j = 0; j < RUN; ++j) {
             f32x4_t acc[HT];
             contract(xf, acc);
             psv[j] = row_sq<KS>(xf);
-            if (UB) pbv[j] = coef * rvc;
+            if (UB) rvmax = fmaxf(rvmax, rvc);
             __builtin_amdgcn_sched_barrier(0);
             wait_vmcnt<(NST - 1) * LPT>();
-            bf16x8_t xn[KS];
+            // the next tile's fragments overwrite this tile's, whose matrix
+            // steps have been issued
             float rvn = 0.f;
-            read_stage((j + 1) % NST, xn, rvn);
+            read_stage((j + 1) % NST, xf, rvn);
             pmv[j] = head_max(acc);
             if (UB) {
                 add_bound(acc, rvc);
@@ -671,8 +690,6 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
             }
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // stage read out before it is refilled
             issue_full(RUN * s + j + 1 + NST, (j + 1) % NST);
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) xf[ks] = xn[ks];
             rvc = rvn;
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -680,26 +697,24 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
         for (int j4 = 0; j4 < RUN; j4 += 4)
             group_out((RUN * s + j4) / 4, group_max(pmv[j4], pmv[j4 + 1], pmv[j4 + 2], pmv[j4 + 3]),
                       group_sum(psv[j4], psv[j4 + 1], psv[j4 + 2], psv[j4 + 3]),
-                      UB ? group_max(puv[j4], puv[j4 + 1], puv[j4 + 2], puv[j4 + 3]) : 0.f,
-                      UB ? group_sum(pbv[j4], pbv[j4 + 1], pbv[j4 + 2], pbv[j4 + 3]) : 0.f);
+                      UB ? group_max(puv[j4], puv[j4 + 1], puv[j4 + 2], puv[j4 + 3]) : 0.f);
     }
 
     // the remaining tiles, with run-time stages and wait counts
     float pm0 = -INFINITY, pm1 = -INFINITY, pm2 = -INFINITY, pm3 = -INFINITY;
     float ps0 = 0.f, ps1 = 0.f, ps2 = 0.f, ps3 = 0.f;
     float pu0 = -INFINITY, pu1 = -INFINITY, pu2 = -INFINITY, pu3 = -INFINITY;
-    float pb0 = 0.f, pb1 = 0.f, pb2 = 0.f, pb3 = 0.f;
     for (int t = RUN * nrun; t < ntl; ++t) {
         f32x4_t acc[HT];
         contract(xf, acc);
         const float ps = row_sq<KS>(xf);
-        const float pb = UB ? coef * rvc : 0.f;
-        bf16x8_t xn[KS];
+        if (UB) rvmax = fmaxf(rvmax, rvc);
         float rvn = 0.f;
         const bool more = t + 1 < ntl;
+        __builtin_amdgcn_sched_barrier(0);
         if (more) {
             wait_tiles<LPT, NST>(min(NST - 1, ntl - 2 - t));
-            read_stage((t + 1) % NST, xn, rvn);
+            read_stage((t + 1) % NST, xf, rvn);   // over this tile's fragments (matrix steps issued)
         }
         const float pm = head_max(acc);
         float pu = -INFINITY;
@@ -712,24 +727,20 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
             pm1 = pm2 = pm3 = -INFINITY;
             ps1 = ps2 = ps3 = 0.f;
             pu1 = pu2 = pu3 = -INFINITY;
-            pb1 = pb2 = pb3 = 0.f;
         }
         put4(pm0, pm1, pm2, pm3, j, pm);
         put4(ps0, ps1, ps2, ps3, j, ps);
         if (UB) {
             put4(pu0, pu1, pu2, pu3, j, pu);
-            put4(pb0, pb1, pb2, pb3, j, pb);
         }
         if (more) {
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // stage read out before it is refilled
             if (t + 1 + NST < ntl) issue(t + 1 + NST, (t + 1) % NST);
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) xf[ks] = xn[ks];
             rvc = rvn;
         }
         if (j != 3 && more) continue;
         group_out(t >> 2, group_max(pm0, pm1, pm2, pm3), group_sum(ps0, ps1, ps2, ps3),
-                  UB ? group_max(pu0, pu1, pu2, pu3) : 0.f, UB ? group_sum(pb0, pb1, pb2, pb3) : 0.f);
+                  UB ? group_max(pu0, pu1, pu2, pu3) : 0.f);
     }
     // the span's keys (and bounds), each lane its own LDS words
     float* kto = a.kt + (int64_t)b * a.A;
@@ -743,6 +754,13 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
             if (kuo) kuo[row] = m;
             if (UB) ubo[row] = s_ub[64 * q + lane];
         }
+    }
+    if (UB) {
+        float m = rvmax;
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, shfl_xor_local(m, o));
+        const float v = coef * m;   // lane 16 g + c; coef = 0 for g = 3
+        to.bmm = (shfl_local(v, 0) + shfl_local(v, 16)) + shfl_local(v, 32);
     }
     score_finish(a, b, lane, to, UB);
 }
