@@ -52,11 +52,15 @@ __device__ __forceinline__ int32_t attended_row(const AttendArgs& a, int b, int6
 }
 
 // XOR applied to the piece index of tile row r (low three bits only, so each
-// aligned group of 8 pieces maps onto itself).  With 16-byte slots the bank
-// group of a slot is its index mod 16; f makes distinct groups for (a) the 16
-// rows of one piece (K operand reads) and (b) 8 consecutive rows x 2 adjacent
-// pieces (transposing V reads).
-__device__ __forceinline__ int piece_xor(int r) { return 2 * ((r >> 1) & 3) + ((r >> 3) & 1); }
+// aligned group of 8 pieces maps onto itself): f(r) = r mod 8.  Slot (r, p)
+// is 72 r + (p ^ f(r)) and 72 is a multiple of 8, so modulo 8 slots (one
+// 128-byte sweep of the banks) it is p ^ f(r).  The 128-bit K operand reads
+// are served eight lanes (eight rows of one piece) at a time, and r mod 8
+// gives those eight rows eight distinct slots; the transposing V reads (four
+// rows x two adjacent pieces per 16 lanes) stay distinct as well.  Measured with
+// SQ_LDS_BANK_CONFLICT: no conflicts on either read (the previous mapping,
+// which paired rows 2i and 2i + 1, doubled the K reads' LDS cycles).
+__device__ __forceinline__ int piece_xor(int r) { return r & 7; }
 
 __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
