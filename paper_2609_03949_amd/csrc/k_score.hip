@@ -28,22 +28,25 @@ namespace vkv {
 // the fp64 oracle on inputs spread over 2^60, where other summation orders
 // give other bits), so a chain of 128 of them, i ascending, is the fp64
 // definition.  Wave w computes basis tile w
-// (16 heads x 16 basis rows) of the current chunk of 128 basis rows; wave 0
-// also runs the Nq chains on the vector unit between its matrix steps.  The
-// query rows and the chunk of P are staged as bf16 by direct loads into rows
-// padded to QP_ROW bytes, so the operand reads (16 rows, one 16-bit element
-// each) fall into distinct banks; they are widened in registers.  Block
-// (0,b) also clears the step state of sequence b.
+// (16 heads x 16 basis rows) of the current chunk of 128 basis rows; one more
+// wave runs the Nq chains on the vector unit meanwhile (a chain of 512 fp64
+// steps on its own, so it overlaps the matrix chains instead of lengthening
+// one of them).  The query rows and the chunk of P are staged as bf16 by
+// direct loads into rows padded to QP_ROW bytes, so the operand reads (16
+// rows, one 16-bit element each) fall into distinct banks; they are widened
+// in registers.  The rope half of qt is loaded at the start and written at
+// the end.  Block (0,b) also clears the step state of sequence b.
 constexpr int QP_ROW = 1040;          // LDS bytes per staged row of 512 bf16
 constexpr int QP_CHUNK_ROWS = 128;    // basis rows staged at a time: one 16-row tile per wave
 constexpr int QP_MAX_WAVES = QP_CHUNK_ROWS / 16;
 
-__host__ __device__ inline int qp_waves(int r) {
+// waves with a basis tile (0 without a digest); one more wave takes the Nq chains
+__host__ __device__ inline int qp_tile_waves(int r) {
     const int t = r / 16;
-    return t < 1 ? 1 : (t > QP_MAX_WAVES ? QP_MAX_WAVES : t);
+    return t < 0 ? 0 : (t > QP_MAX_WAVES ? QP_MAX_WAVES : t);
 }
 
-__global__ __launch_bounds__(64 * QP_MAX_WAVES) void qprep_project_kernel(QprepArgs a) {
+__global__ __launch_bounds__(64 * (QP_MAX_WAVES + 1)) void qprep_project_kernel(QprepArgs a) {
     __shared__ __align__(16) uint8_t s_q[16 * QP_ROW];              // the block's 16 query rows, [h][i]
     __shared__ __align__(16) uint8_t s_p[QP_CHUNK_ROWS * QP_ROW];   // a chunk of P rows, then its w values
     __shared__ double s_nq[16];
@@ -55,6 +58,18 @@ __global__ __launch_bounds__(64 * QP_MAX_WAVES) void qprep_project_kernel(QprepA
     }
     const int r = (a.mode & 2) ? a.r : 0;
     const int off = (a.mode & 1) ? D_ROPE : 0;
+    const int nq_wave = qp_tile_waves(r);
+    // wave 0, lane 4 hl + t: rope pieces t and t + 4 of head hb0 + hl (loaded now, stored at the end)
+    const int hl = lane >> 2, t = lane & 3;
+    const int h = hb0 + hl;
+    const bool have = h < a.H;
+    const int64_t bhc = (int64_t)b * a.H + (have ? h : 0);
+    u16x8_t rope0 = u16x8_t{}, rope1 = u16x8_t{};
+    if (wave == 0 && (a.mode & 1) && have) {
+        const u16x8_t* src = reinterpret_cast<const u16x8_t*>(a.q_rope + bhc * D_ROPE);
+        rope0 = src[t];
+        rope1 = src[t + 4];
+    }
     typedef __attribute__((address_space(3))) void lds_t;
     typedef __attribute__((address_space(1))) void gbl_t;
     // query rows: one 1 KB direct load per row; rows past H are zero
@@ -76,7 +91,6 @@ __global__ __launch_bounds__(64 * QP_MAX_WAVES) void qprep_project_kernel(QprepA
     double anq = 0.0;
     // tail sums of lane 4 hl + t of wave 0, j ascending over all chunks:
     // t=1 ||w||^2, t=2 ||qd - w||^2, t=3 ||qd||^2 (t=0 takes Nq at the end)
-    const int hl = lane >> 2, t = lane & 3;
     double tsum = 0.0;
     const int nchunk = (r + QP_CHUNK_ROWS - 1) / QP_CHUNK_ROWS;
     for (int ch = 0; ch < (nchunk > 0 ? nchunk : 1); ++ch) {
@@ -87,15 +101,22 @@ __global__ __launch_bounds__(64 * QP_MAX_WAVES) void qprep_project_kernel(QprepA
                                              (lds_t*)(s_p + row * QP_ROW), 16, 0, 0);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
-        const bool tile = 16 * wave < nj;
-        const bool nq = ch == 0 && wave == 0;
+        const bool tile = wave < nq_wave && 16 * wave < nj;
+        const bool nq = ch == 0 && wave == nq_wave;
         f64x4_t acc = f64x4_t{0.0, 0.0, 0.0, 0.0};
-        if (tile && nq) acc = mfma_f64_rowdot512<true>(qa, pb, qn, anq);
-        else if (tile) acc = mfma_f64_rowdot512<false>(qa, pb, qn, anq);
-        else if (nq) {
-            for (int i = 0; i < D_LAT; ++i) {
-                const double x = bf16_bits_f64(qn[i]);
-                anq = fma(x, x, anq);
+        if (tile) {
+            acc = mfma_f64_rowdot512<false>(qa, pb, qn, anq);
+        } else if (nq) {
+            // Nq of head lane mod 16, i ascending (eight elements per LDS read)
+            const u16x8_t* qv = reinterpret_cast<const u16x8_t*>(qn);
+#pragma unroll 4
+            for (int i8 = 0; i8 < D_LAT / 8; ++i8) {
+                const u16x8_t v = qv[i8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const double x = bf16_bits_f64(v[e]);
+                    anq = fma(x, x, anq);
+                }
             }
         }
         __syncthreads();   // the chunk's rows are read out; its LDS takes the w values
@@ -116,15 +137,12 @@ __global__ __launch_bounds__(64 * QP_MAX_WAVES) void qprep_project_kernel(QprepA
         if (wave == 0 && t > 0 && nj > 0) {
             const double* w = s_w + hl * QP_CHUNK_ROWS;
             const double* dq = s_d + hl * QP_CHUNK_ROWS;
-            if (t == 1) {
-                for (int j = 0; j < nj; ++j) tsum = fma(w[j], w[j], tsum);
-            } else if (t == 2) {
-                for (int j = 0; j < nj; ++j) {
-                    const double ee = dq[j] - w[j];
-                    tsum = fma(ee, ee, tsum);
-                }
-            } else {
-                for (int j = 0; j < nj; ++j) tsum = fma(dq[j], dq[j], tsum);
+            // the three sums share one loop: x = w, qd - w or qd by lane
+#pragma unroll 8
+            for (int j = 0; j < nj; ++j) {
+                const double wj = w[j], dj = dq[j];
+                const double x = t == 1 ? wj : (t == 2 ? dj - wj : dj);
+                tsum = fma(x, x, tsum);
             }
         }
         __syncthreads();   // before the next chunk's rows overwrite the w values
@@ -135,16 +153,12 @@ __global__ __launch_bounds__(64 * QP_MAX_WAVES) void qprep_project_kernel(QprepA
     // evaluation order, the same as the oracle's):
     //   a_h >= sqrt(q^T (I - P^T P) q),  n_h >= ||qd_h||,  e_h >= ||qd_h - P q||
     // plus ||qt_h|| for the scorer's error bound.
-    const int h = hb0 + hl;
-    const bool have = h < a.H;
-    const int64_t bhc = (int64_t)b * a.H + (have ? h : 0);
     // rope half of qt (8 pieces of 16 B per head, 4 lanes per head) and
     // ||q_rope||^2 (an upper-bound input only; order irrelevant)
     double r2 = 0.0;
     if ((a.mode & 1) && have) {
-        const u16x8_t* src = reinterpret_cast<const u16x8_t*>(a.q_rope + bhc * D_ROPE);
         u16x8_t* dst = reinterpret_cast<u16x8_t*>(a.qt + bhc * a.n);
-        const u16x8_t v0 = src[t], v1 = src[t + 4];
+        const u16x8_t v0 = rope0, v1 = rope1;
         dst[t] = v0;
         dst[t + 4] = v1;
 #pragma unroll
@@ -217,7 +231,7 @@ __device__ __forceinline__ void staged_head_maxima(const float4* s_hs, int n, fl
 hipError_t launch_qprep(const QprepArgs& a, hipStream_t s) {
     const int r = (a.mode & 2) ? a.r : 0;
     dim3 g1((a.H + 15) / 16, a.B);
-    hipLaunchKernelGGL(qprep_project_kernel, g1, dim3(64 * qp_waves(r)), 0, s, a);
+    hipLaunchKernelGGL(qprep_project_kernel, g1, dim3(64 * (qp_tile_waves(r) + 1)), 0, s, a);
     return hipGetLastError();
 }
 
