@@ -428,24 +428,39 @@ __device__ __forceinline__ float scaled_a(float cm, float ah) { return ru_f32((d
 // (row, head) pair gets its fp64 chain (d ascending from +0) from one lane,
 // and the row's exact value is the maximum over its pairs.  margin = +inf
 // evaluates every head exactly.
+// The sequence's query rows qt (H * n / 8 <= EX_QT_MAX / 8 pieces of 16 B),
+// thread tid's pieces tid + RES_THREADS j: loads all in flight together.  A
+// caller may issue them early and hand them to exact_keys_block.
+constexpr int EX_QP = EX_QT_MAX / 8 / RES_THREADS;
+__device__ __forceinline__ void qt_prefetch(const SelectArgs& a, int b, u16x8_t (&v)[EX_QP]) {
+    const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
+    const int np = a.H * a.n / 8;
+    if (np > EX_QT_MAX / 8) return;
+#pragma unroll
+    for (int j = 0; j < EX_QP; ++j) {
+        const int p = threadIdx.x + RES_THREADS * j;
+        v[j] = *reinterpret_cast<const u16x8_t*>(qtb + 8 * (int64_t)(p < np ? p : 0));
+    }
+}
+
 template <bool UB, bool OFF = false>
 __device__ __forceinline__ void exact_keys_block(const SelectArgs& a, int b, int64_t namb, const int32_t* amb, uint64_t* ak,
-                                 const ExLds& L, float margin, int blk = 0, int nblks = 1) {
+                                 const ExLds& L, float margin, int blk = 0, int nblks = 1,
+                                 const u16x8_t (*pre)[EX_QP] = nullptr) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4, c = lane & 15;
     const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
     const int n8 = a.n / 8;
     if (L.qlds) {
-        // H * n / 8 <= EX_QT_MAX / 8 pieces of 16 B: all loads in flight together
-        constexpr int QP = EX_QT_MAX / 8 / RES_THREADS;
         const int np = a.H * n8;
-        u16x8_t v[QP];
+        u16x8_t v[EX_QP];
+        if (pre) {
 #pragma unroll
-        for (int j = 0; j < QP; ++j) {
-            const int p = tid + RES_THREADS * j;
-            v[j] = *reinterpret_cast<const u16x8_t*>(qtb + 8 * (int64_t)(p < np ? p : 0));
+            for (int j = 0; j < EX_QP; ++j) v[j] = (*pre)[j];
+        } else {
+            qt_prefetch(a, b, v);
         }
 #pragma unroll
-        for (int j = 0; j < QP; ++j) {
+        for (int j = 0; j < EX_QP; ++j) {
             const int p = tid + RES_THREADS * j;
             if (p < np) *reinterpret_cast<u16x8_t*>(&L.qt[8 * p]) = v[j];
         }
@@ -664,6 +679,9 @@ __global__ __launch_bounds__(RES_THREADS, 1) void sel_resolve_kernel(SelectArgs 
     const float tlo = __uint_as_float(sq[SQ_BLO]), thi = __uint_as_float(sq[SQ_BHI]);
     const int64_t ncand = min((int64_t)sq[SQ_NCAND], a.A);
     const float E = key_band_f32(sq, a.n);
+    // the query rows of the exact re-scoring at the end, in flight from here on
+    u16x8_t qpre[EX_QP];
+    qt_prefetch(a, b, qpre);
     // the first NT * CPT candidates stay in registers for both passes below
     constexpr int64_t CH = (int64_t)RES_THREADS * CPT;
     int32_t cu[CPT];
@@ -760,14 +778,19 @@ __global__ __launch_bounds__(RES_THREADS, 1) void sel_resolve_kernel(SelectArgs 
         }
     };
     if (ok) {
-        // the candidates; every other row was decided by the counting pass
+        // the candidates; every other row was decided by the counting pass.
+        // A candidate's flag is 2 from that pass, and every reader takes any
+        // flag but 1 as "not selected", so only the selected ones are written
+        // (the undecided ones get theirs from the ranking below).
 #pragma unroll
         for (int j = 0; j < CPT; ++j) {
             uint8_t f = 0;
             if (cu[j] >= 0) {
                 f = classify(cv[j]);
-                fb[cu[j]] = f;
-                if (f == 1) count_in(cu[j]);
+                if (f == 1) {
+                    fb[cu[j]] = 1;
+                    count_in(cu[j]);
+                }
             }
             append(f == 2, cu[j]);
         }
@@ -779,8 +802,10 @@ __global__ __launch_bounds__(RES_THREADS, 1) void sel_resolve_kernel(SelectArgs 
                 if (i < ncand) {
                     u = cr[i];
                     f = classify(ck[i]);
-                    fb[u] = f;
-                    if (f == 1) count_in(u);
+                    if (f == 1) {
+                        fb[u] = 1;
+                        count_in(u);
+                    }
                 }
                 append(f == 2, u);
             }
@@ -827,7 +852,7 @@ __global__ __launch_bounds__(RES_THREADS, 1) void sel_resolve_kernel(SelectArgs 
     __syncthreads();
     const int32_t* al = amb_lds ? s_amb : amb;
     const ExLds L = ex_carve(lds, a.H, a.n);
-    exact_keys_block<false>(a, b, namb, al, ak, L, next_up_f32(2.0f * E));
+    exact_keys_block<false>(a, b, namb, al, ak, L, next_up_f32(2.0f * E), 0, 1, &qpre);
     rank_winners(al, ak, namb, need2, fb, blkb + BW_XIN, lds, &s_theta);
     if (tid == 0) a.theta[b] = ord_to_f64(s_theta);
 }
