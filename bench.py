@@ -8,8 +8,10 @@ decode state resident in HBM.  Default workload: 32 sequences x 128 heads x
 digest index) -- the long-context configuration the metric is quoted on.
 
 Prints ONE JSON line.  ``value`` = archived rows scored per second =
-B * (T - W) / t_step.  ``roofline`` is for the dominant kernel (the index
-scan), timed with HIP events on the stream it runs on.
+B * (T - W) / t_step, with t_step the median of the timed steps (each step
+bracketed by HIP events on the step's stream).  ``roofline`` is for the
+dominant kernel (the index scan), timed with HIP events on the stream it runs
+on; ``roofline.step`` gives the whole step against the same HBM peak.
 """
 from __future__ import annotations
 
@@ -51,8 +53,8 @@ def traffic_for(kernel: str, workload: str, launches_per_step: int):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="cfg4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -131,27 +133,30 @@ def main():
         log("copy probe: 3 x 1 GiB device copies done")
         del src, dst
 
-    # ---- timed region: K steps through vkv_step_run; the library records HIP
-    # events around each score scan on the stream it runs on
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # ---- timed region: K steps through vkv_step_run, an event between
+    # consecutive steps on the step's stream; the library records HIP events
+    # around each score scan on the stream it runs on
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     ctx.set_timing(True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    ev0.record(stream)
-    for _ in range(args.steps):
+    evs[0].record(stream)
+    for i in range(args.steps):
         run_step()
-    ev1.record(stream)
+        evs[i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     score_launch_ms = ctx.score_timing()
     ctx.set_timing(False)
-    total_ms = ev0.elapsed_time(ev1)
-    ms_per_step = total_ms / args.steps
+    step_ms = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
+    total_ms = evs[0].elapsed_time(evs[-1])
+    ms_per_step = float(np.median(step_ms))
     assert len(score_launch_ms) == args.steps, (len(score_launch_ms), args.steps)
-    launch_ms = float(np.mean(score_launch_ms))
+    launch_ms = float(np.median(score_launch_ms))
     adm_total = int(bufs.adm_count.sum().item()) if two_tier else 0
-    log(f"step {ms_per_step:.4f} ms over {args.steps} steps; "
-        f"score launch {launch_ms:.4f} ms; wall {wall / args.steps * 1e3:.4f} ms")
+    log(f"step median {ms_per_step:.4f} ms (mean {total_ms / args.steps:.4f}, min {min(step_ms):.4f}, "
+        f"max {max(step_ms):.4f}) over {args.steps} steps; score launch median {launch_ms:.4f} ms; "
+        f"wall {wall / args.steps * 1e3:.4f} ms")
 
     # ---- diagnostics outside the timed region: each stage call timed alone
     stages = ["query_prep", "score", "select"] + (["admit"] if two_tier else []) + ["attend"]
@@ -200,6 +205,9 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
+        "ms_per_step_stats": {"median": ms_per_step, "mean": total_ms / args.steps,
+                              "min": float(min(step_ms)), "max": float(max(step_ms)),
+                              "p90": float(np.percentile(step_ms, 90))},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -226,7 +234,19 @@ def main():
             "traffic": traffic,
             "bytes_per_launch": scan_bytes,
             "launch_ms": launch_ms,
+            "launch_ms_is": "median of the timed launches",
             "launches_timed": len(score_launch_ms),
+            # the whole step (score, select, attend and the rest) against the
+            # same peak: algorithmic bytes of the step / median step time
+            "step": {
+                "bound": "hbm",
+                "achieved": step_gbs,
+                "peak": HBM_PEAK_GBS,
+                "unit": "GB/s",
+                "frac": step_gbs / HBM_PEAK_GBS,
+                "bytes_per_step": sb["total"],
+                "ms": ms_per_step,
+            },
         },
     }
 
@@ -236,12 +256,41 @@ def main():
     ctx.close()
 
 
+def cpu_model() -> dict:
+    """The host CPU as the kernel reports it (model name, family/model/stepping,
+    logical CPUs in this process's affinity set)."""
+    info = {}
+    try:
+        for line in open("/proc/cpuinfo"):
+            k, _, v = line.partition(":")
+            k, v = k.strip(), v.strip()
+            if k in ("model name", "cpu family", "model", "stepping", "vendor_id") and k not in info:
+                info[k] = v
+    except OSError:
+        pass
+    try:
+        import subprocess
+        out = subprocess.run(["lscpu"], capture_output=True, text=True).stdout.splitlines()
+        for l in out:
+            if l.startswith("Model name") and "lscpu_model" not in info:
+                info["lscpu_model"] = l.split(":", 1)[1].strip()
+            if l.startswith("Socket(s)"):
+                info["sockets"] = l.split(":", 1)[1].strip()
+    except Exception:
+        pass
+    info["logical_cpus_affinity"] = len(os.sched_getaffinity(0))
+    info["logical_cpus_total"] = os.cpu_count()
+    return info
+
+
 def cpu_baseline(wl, cfg, target_s: float):
     """The fp64 oracle, as it stands, on whole sequences of the same workload:
     index keys -> top-k -> [bound + admission] -> attention.  The oracle's own
     index build for the sample runs first and is not timed (it is the
-    compression event, timed separately on both sides)."""
-    import numpy as np
+    compression event, timed separately on both sides).  Two figures: the
+    oracle with its OpenMP threads over rows (``value``), and the same step on
+    one thread for one sequence (``value_1thread``)."""
+    import numpy as np  # noqa: F401
 
     import oracle
     from paper_2609_03949_amd import synth
@@ -257,51 +306,60 @@ def cpu_baseline(wl, cfg, target_s: float):
         has_rope, cols = False, r
     else:
         has_rope, cols = True, 64 + r
-    done_rows = 0
-    elapsed = 0.0
-    seqs_done = 0
-    b = 0
-    build_s = 0.0
-    while elapsed < target_s and b < wl["B"]:
+
+    def host_seq(b):
         import torch
         t = torch.tensor([b], device=wl["cache"].device)
         cache = synth.to_numpy_bits(wl["cache"].index_select(0, t))
         q_lat = synth.to_numpy_bits(wl["q_lat"].index_select(0, t))
         q_rope = synth.to_numpy_bits(wl["q_rope"].index_select(0, t))
         P = synth.to_numpy_bits(wl["P"]) if wl["P"] is not None else None
-        tb = time.perf_counter()
         index = eta = eps = gam = None
         if cols or cfg.two_tier:
             index, eta, eps, gam = oracle.digest_build(cache, P, rr, with_rope=has_rope,
                                                        scalars=cfg.two_tier, nthreads=nthreads)
             if not cols:
                 index = None
-        build_s += time.perf_counter() - tb
+        return cache, q_lat, q_rope, P, index, eta, eps, gam
+
+    def one_step(inputs, threads):
+        cache, q_lat, q_rope, P, index, eta, eps, gam = inputs
         t0 = time.perf_counter()
         oracle.step(cache, q_lat, q_rope, index, P, rr, mode, W, k, cfg.scale,
                     two_tier=cfg.two_tier, eta=eta, eps=eps, gam=gam, index_has_rope=has_rope,
-                    nthreads=nthreads)
-        elapsed += time.perf_counter() - t0
+                    nthreads=threads)
+        return time.perf_counter() - t0
+
+    done_rows = 0
+    elapsed = 0.0
+    seqs_done = 0
+    b = 0
+    build_s = 0.0
+    first = None
+    while elapsed < target_s and b < wl["B"]:
+        tb = time.perf_counter()
+        inputs = host_seq(b)
+        build_s += time.perf_counter() - tb
+        if first is None:
+            first = inputs
+        elapsed += one_step(inputs, nthreads)
         done_rows += wl["A"]
         seqs_done += 1
         b += 1
         log(f"cpu oracle: sequence {b - 1} done, {elapsed:.1f}s timed so far")
-    lscpu = ""
-    try:
-        import subprocess
-        lscpu = [l for l in subprocess.run(["lscpu"], capture_output=True, text=True).stdout.splitlines()
-                 if l.startswith("Model name")][0].split(":", 1)[1].strip()
-    except Exception:
-        pass
+    one_s = one_step(first, 1)
+    log(f"cpu oracle, one thread: one sequence in {one_s:.1f}s")
     return {
         "value": done_rows / elapsed,
         "unit": "rows/s",
         "cores": nthreads,
         "kind": "oracle",
         "sample": f"{seqs_done} whole sequence(s) of the same workload (A={wl['A']} archived rows each), "
-                  f"one full step each; fp64 oracle with OpenMP over rows; oracle index build "
-                  f"({build_s:.1f}s) not timed",
-        "cpu": lscpu,
+                  f"one full step each; fp64 oracle with OpenMP over rows ({nthreads} threads); oracle "
+                  f"index build ({build_s:.1f}s) not timed",
+        "value_1thread": wl["A"] / one_s,
+        "sample_1thread": f"sequence 0 of the same workload, one full step, one thread ({one_s:.2f}s)",
+        "cpu": cpu_model(),
         "timed_s": elapsed,
     }
 
