@@ -278,6 +278,11 @@ def cpu_model() -> dict:
                 info["sockets"] = l.split(":", 1)[1].strip()
     except Exception:
         pass
+    # AMD's family numbers: 25 (19h) is Zen 3 / Zen 4, 26 (1Ah) is Zen 5
+    if info.get("vendor_id") == "AuthenticAMD":
+        fam = {"25": "Zen 3 / Zen 4 (family 19h)", "26": "Zen 5 (family 1Ah)"}.get(info.get("cpu family", ""))
+        if fam:
+            info["core_family"] = fam
     info["logical_cpus_affinity"] = len(os.sched_getaffinity(0))
     info["logical_cpus_total"] = os.cpu_count()
     return info
