@@ -63,6 +63,13 @@ def main():
                     help="skip the per-stage diagnostic pass (each stage call timed alone)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (counter scale for --pmc runs)")
+    ap.add_argument("--path", choices=("index", "kept"), default="index",
+                    help="index: top-k of the index scan is the attended tier (vkv_step_run); kept: the "
+                         "deployed path -- the sigma tier of the closed blocks is attended, the index scan "
+                         "feeds the calibrated trigger (vkv_step_run_kept)")
+    ap.add_argument("--sketch", action="store_true",
+                    help="(kept path) content queries near a 48-dim subspace and the index basis V_r fitted "
+                         "on the GPU to 4096 prefix queries of the same law (vkv_sketch_basis)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: libvkv has no multi-GPU path "
@@ -78,6 +85,8 @@ def main():
 
     cfg = synth.CONFIGS[args.config]
     dev = torch.device("cuda:0")
+    if args.path == "kept":
+        return run_kept_path(args, cfg, dev)
     log(f"workload {synth.describe(cfg)}")
     t0 = time.time()
     wl = synth.make_workload(cfg, dev)
@@ -252,6 +261,132 @@ def main():
 
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, cfg, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+    ctx.close()
+
+
+def run_kept_path(args, cfg, dev):
+    """The deployed per-step path on the same workload (the deployment
+    specification's request lifecycle): the closed 4096-row blocks of every
+    sequence get their sigma once (block close), the sigma tier (4 sinks + the
+    sigma-top-(k-4) rows) is the attended tier, and each step runs query prep ->
+    index scan with the certificate -> the tier's exact maximum logit ->
+    calibrated trigger (z from this step's own queries, conformal quantile at
+    tau_s = 18/19) -> attention over tier, recent window and fired rows."""
+    import math
+
+    import numpy as np
+    import torch
+
+    import paper_2609_03949_amd as vkv
+    from paper_2609_03949_amd import budget, synth
+
+    if not (cfg.mode & 1):
+        raise SystemExit("the kept path needs the branch summand in the index key (a mode with rope)")
+    if args.sketch:
+        cfg = cfg.with_(queries="lowrank")
+    log(f"workload {synth.describe(cfg)} (kept path)")
+    wl = synth.make_workload(cfg, dev)
+    ctx = vkv.Context(0)
+    B, H, T, W, A, k, r = wl["B"], wl["H"], wl["T"], wl["W"], wl["A"], wl["k"], cfg.r
+    rr = r if cfg.mode != synth.MODE_ROPE else 0
+    sketch_ms = None
+    if args.sketch:
+        if rr == 0:
+            raise SystemExit("--sketch needs a digest (r > 0)")
+        qpre = synth.prefix_queries(cfg, 4096, dev)
+        kws = torch.empty(vkv.sketch_workspace_size(rr), dtype=torch.uint8, device=dev)
+        Pg = torch.empty(rr, 512, dtype=torch.bfloat16, device=dev)
+        energy = torch.empty(2, dtype=torch.float64, device=dev)
+        t0 = time.perf_counter()
+        vkv.sketch_basis(ctx, qpre, rr, 8, kws, Pg, energy)
+        sketch_ms = (time.perf_counter() - t0) * 1e3
+        en = energy.cpu().numpy()
+        log(f"sketch basis from 4096 prefix queries: {sketch_ms:.2f} ms, captures {en[0] / en[1] * 100:.2f}% "
+            f"of their second moment")
+        wl["P"] = Pg
+    cols = 64 + rr
+    index = torch.empty(B, T, cols, dtype=torch.bfloat16, device=dev)
+    eta = torch.empty(B, T, dtype=torch.float32, device=dev)
+    eps, gam = torch.empty_like(eta), torch.empty_like(eta)
+    vkv.digest_build(ctx, wl["cache"], wl["P"], rr, True, index, eta, eps, gam)
+    step = vkv.Step(wl["cache"], wl["q_lat"], wl["q_rope"], W, cfg.mode, rr, index=index, index_has_rope=True,
+                    P=wl["P"], eta=eta, eps=eps, gam=gam)
+    # block close: sigma of the closed blocks, then the tier (timed once; not per step)
+    nblk = A // vkv.SIGMA_BLOCK
+    n_closed = nblk * vkv.SIGMA_BLOCK
+    sig = torch.empty(B, max(n_closed, 1), dtype=torch.float64, device=dev)
+    sws = torch.empty(max(vkv.sigma_workspace_size(B, nblk), 256), dtype=torch.uint8, device=dev)
+    K = vkv.sigma_tier_size(n_closed, k - 4)
+    kept = torch.empty(B, max(K, 1), dtype=torch.int32, device=dev)
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    e0.record()
+    vkv.sigma_close(ctx, wl["cache"], 0, nblk, 16 if T <= 16384 else 64, sws, sig)
+    e1.record()
+    vkv.sigma_select(ctx, sig, n_closed, k - 4, 4, kept)
+    e2.record()
+    torch.cuda.synchronize()
+    close_ms, select_ms = e0.elapsed_time(e1), e1.elapsed_time(e2)
+    log(f"block close: sigma of {nblk} blocks x {B} sequences {close_ms:.3f} ms, tier select {select_ms:.3f} ms")
+    ws = vkv.alloc_workspace(step, K, A)
+    # calibration on this step's queries: the causal argmax over the whole
+    # context, the tier's maximum, the required inflations of the hard pairs
+    vkv.query_prep(ctx, step, ws)
+    smax_all = torch.empty(B, H, dtype=torch.float64, device=dev)
+    arg_all = torch.empty(B, H, dtype=torch.int32, device=dev)
+    smax_t = torch.empty_like(smax_all)
+    arg_t = torch.empty_like(arg_all)
+    vkv.row_max(ctx, step, None, True, smax_all, arg_all)
+    vkv.row_max(ctx, step, kept, True, smax_t, arg_t)
+    hard = torch.empty(B, H, dtype=torch.int32, device=dev)
+    zq = torch.empty(B, H, dtype=torch.float64, device=dev)
+    vkv.required_inflation(ctx, step, ws, K, kept, smax_t, arg_all, hard, zq)
+    torch.cuda.synchronize()
+    hz = zq[hard != 0].cpu().numpy()
+    z, min_hard, krank = vkv.conformal_z(hz, tau=(9, 10), zmax=8.0)
+    cm = z / math.sqrt(512 - rr)
+    log(f"calibration: {len(hz)} hard (query, head) pairs of {B * H}, z = {z:.4f} (rank {krank}), "
+        f"cert_mult = {cm:.5f}")
+    f32 = dict(dtype=torch.float32, device=dev)
+    key, ub = torch.empty(B, A, **f32), torch.empty(B, A, **f32)
+    smax = torch.empty(B, H, dtype=torch.float64, device=dev)
+    arg = torch.empty(B, H, dtype=torch.int32, device=dev)
+    fired = torch.empty(B, A, dtype=torch.int32, device=dev)
+    cnt = torch.empty(B, dtype=torch.int32, device=dev)
+    out = torch.empty(B, H, 512, dtype=torch.bfloat16, device=dev)
+    lse = torch.empty(B, H, **f32)
+    stream = torch.cuda.current_stream()
+
+    def run_step():
+        vkv.step_run_kept(ctx, step, ws, K, kept, key, ub, cm, smax, arg, 0, fired, cnt, A, cfg.scale, out, lse,
+                          stream)
+
+    for _ in range(args.warmup):
+        run_step()
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record(stream)
+    for i in range(args.steps):
+        run_step()
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    step_ms = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
+    ms = float(np.median(step_ms))
+    fired_total = int(cnt.sum().item())
+    frac = fired_total / (B * (A - K))
+    sb = budget.step_bytes(B, H, T, W, K, cfg.mode, r, True, fired_total)
+    log(f"kept path: step median {ms:.4f} ms; fired {fired_total} rows = {frac * 100:.3f}% of the archived rows "
+        f"outside the tier")
+    line = {
+        "metric": METRIC, "value": B * A / (ms * 1e-3), "unit": "rows/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": synth.describe(cfg), "path": "kept (sigma tier + calibrated trigger)",
+                   "B": B, "H": H, "T": T, "W": W, "tier": K, "r": r},
+        "tier_rows_per_seq": K, "fired_fraction": frac, "z": z, "cert_mult": cm, "hard_pairs": int(len(hz)),
+        "block_close_ms": close_ms, "tier_select_ms": select_ms, "sketch_basis_ms": sketch_ms,
+        "step_gbs": sb["total"] / (ms * 1e-3) / 1e9, "hbm_frac_step": sb["total"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+    }
     print(json.dumps(line), flush=True)
     ctx.close()
 

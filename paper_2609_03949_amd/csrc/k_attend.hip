@@ -401,10 +401,20 @@ __global__ __launch_bounds__(128) void attend_combine_kernel(AttendArgs a) {
                 ms[u][i] = hv ? ml[2 * (hb + i)] : -INFINITY;
                 ls[u][i] = hv ? ml[2 * (hb + i) + 1] : 0.f;
             }
-            const uint16_t* src = a.part_o + (((int64_t)b * a.splits + (live ? s : s0)) * HG + hg) * (ATT_HEADS * D_LAT) +
-                                  (int64_t)wave * (D_LAT / 16) * 64 * 4 + (tt * 64 + 16 * g + c0) * 4;
-            raw[u][0] = *reinterpret_cast<const u32x4_t*>(src);       // lanes c0, c0+1
-            raw[u][1] = *reinterpret_cast<const u32x4_t*>(src + 8);   // lanes c0+2, c0+3
+        }
+#pragma unroll
+        for (int u = 0; u < COMB_SPLITS; ++u) {
+            // splits without rows (the unused capacity of the admitted rows) are not read
+            const int s = s0 + u;
+            const bool rows = ms[u][0] != -INFINITY || ms[u][1] != -INFINITY || ms[u][2] != -INFINITY ||
+                              ms[u][3] != -INFINITY;
+            raw[u][0] = raw[u][1] = u32x4_t{0u, 0u, 0u, 0u};
+            if (rows) {
+                const uint16_t* src = a.part_o + (((int64_t)b * a.splits + s) * HG + hg) * (ATT_HEADS * D_LAT) +
+                                      (int64_t)wave * (D_LAT / 16) * 64 * 4 + (tt * 64 + 16 * g + c0) * 4;
+                raw[u][0] = *reinterpret_cast<const u32x4_t*>(src);       // lanes c0, c0+1
+                raw[u][1] = *reinterpret_cast<const u32x4_t*>(src + 8);   // lanes c0+2, c0+3
+            }
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {

@@ -214,6 +214,7 @@ __device__ __forceinline__ void store_head_maxima(const ScoreArgs& a, int b, int
         sq[SQ_QMAX] = __float_as_uint(m.w);
         // the multiplier the bound below used (an impossible float pattern without one)
         sq[SQ_CMULT] = a.ub ? __float_as_uint(a.cert_mult) : 0xFFFFFFFFu;
+        sq[SQ_TRGM] = (a.ub && a.thr) ? 1u : 0u;
     }
 }
 
@@ -324,6 +325,7 @@ template <bool UB>
 __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
     constexpr int KSMAX = D_ROW / 32;
     __shared__ float4 s_hs[UB ? 128 : 1];
+    __shared__ float s_thr[UB ? 128 : 1];   // -s*_h (trigger margins) or 0
     const int b = blockIdx.y;
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63, g = lane >> 4, c = lane & 15;
@@ -333,6 +335,7 @@ __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
         for (int h = tid; h < 16 * HT; h += 256) {
             const float4 v = reinterpret_cast<const float4*>(a.hsc)[(int64_t)b * a.H + (h % a.H)];
             s_hs[h] = make_float4(scaled_a(a.cert_mult, v.x), v.y, v.z, v.w);
+            s_thr[h] = a.thr ? -(float)a.thr[(int64_t)b * a.H + (h % a.H)] : 0.f;
         }
         __syncthreads();
     }
@@ -343,8 +346,11 @@ __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
     const int64_t rlast = rend - 1;
     const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
     const uint16_t* xb = a.x + (int64_t)b * a.xbs;
-    float amax = 0.f, nmax = 0.f, emax = 0.f;
-    if (UB) staged_head_maxima(s_hs, 16 * HT, amax, nmax, emax);
+    float amax = 0.f, nmax = 0.f, emax = 0.f, tabs = 0.f;
+    if (UB) {
+        staged_head_maxima(s_hs, 16 * HT, amax, nmax, emax);
+        for (int i = 0; i < 16 * HT; ++i) tabs = fmaxf(tabs, fabsf(s_thr[i]));
+    }
     TileOut to{-INFINITY, INFINITY, 0.f, 0.f};
     for (int64_t t0 = r0; t0 < rend; t0 += 16) {
         const int64_t row = t0 + c;
@@ -377,7 +383,7 @@ __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
                 m = fmaxf(m, acc[i]);
                 if (UB) {
                     const float4 hs = s_hs[16 * ht + 4 * g + i];
-                    ubv = fmaxf(ubv, acc[i] + fmaf(hs.x, et, fmaf(hs.y, ep, hs.z * ga)));
+                    ubv = fmaxf(ubv, (acc[i] + fmaf(hs.x, et, fmaf(hs.y, ep, hs.z * ga))) + s_thr[16 * ht + 4 * g + i]);
                 }
             }
         }
@@ -385,7 +391,7 @@ __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
         tile_epilogue(a, b, g, row, valid, m, row_sq<KSMAX>(xf), to);
         if (UB) {
             ubv = wave_max16(ubv);
-            if (valid) to.bmm = fmaxf(to.bmm, fmaf(amax, et, fmaf(nmax, ep, emax * ga)));
+            if (valid) to.bmm = fmaxf(to.bmm, fmaf(amax, et, fmaf(nmax, ep, emax * ga)) + tabs);
             if (g == 0 && valid) a.ub[(int64_t)b * a.A + row] = ubv;
         }
     }
@@ -425,9 +431,16 @@ __global__ __launch_bounds__(256, 2) void score_generic_kernel(ScoreArgs a) {
 // such step per head tile adds B_h(u) = a_h eta_u + n_h eps_u + e_h gam_u to
 // the finished scores, UB_u = max_h (s^_h(u) + B_h(u)).  Four fp32 products
 // and sums of non-negative terms (all scalars are >= 0) on top of the score:
-// the selection's band for UB covers that error.
+// the selection's band for UB covers that error.  With trigger thresholds
+// s*_h (the kept-tier step: the tier's maximum logit is known before the
+// scan), the fourth group carries -s*_h against a row scalar of 1, so the same
+// step yields the trigger margin max_h (s^_h(u) + B_h(u) - s*_h) (Eq. (trigger)
+// per head, fused into the scan); the band then also covers |s*_h|.
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void gbl_void_t;
+
+// the row scalar of head slot g = 3 when the bound carries the trigger threshold
+__device__ float k_one = 1.0f;
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -556,8 +569,9 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
     const int ntl = (int)((nbt - 1 - wave) / TST + 1);
     const int64_t r0 = bs0 + 16 * wave;
 
-    // (UB) A operand of the bound step: scalar g of head slot 16 ht + c (zero
-    // for g = 3), and in lane 16 g + c the maximum over heads of scalar g
+    // (UB) A operand of the bound step: scalar g of head slot 16 ht + c (for
+    // g = 3: -s*_h or zero), and in lane 16 g + c the maximum over heads of
+    // its magnitude
     float hsf[UB ? HT : 1];
     float coef = 0.f;
 
@@ -578,11 +592,12 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
         const float* base = (g == 1) ? a.eps : (g == 2) ? a.gam : a.eta;
         rvsrc = base + (int64_t)b * a.T + r0 + c;
     }
+    const bool ones = UB && g == 3 && a.thr;   // this lane's row scalar is the constant 1
     auto issue_rv = [&](int t, int stage, int nv) {
         if (UB) {
             const int cc = c < nv ? 0 : c - (nv - 1);
-            __builtin_amdgcn_global_load_lds((gbl_void_t*)(rvsrc + (int64_t)t * (TST * 16) - cc),
-                                             (lds_void_t*)(rvbase + 256 * stage), 4, 0, 2 /* nt */);
+            const float* src = ones ? &k_one : rvsrc + (int64_t)t * (TST * 16) - cc;
+            __builtin_amdgcn_global_load_lds((gbl_void_t*)src, (lds_void_t*)(rvbase + 256 * stage), 4, 0, 2 /* nt */);
         }
     };
     // loads of tile t into `stage`; rows past the span re-read its last row
@@ -645,9 +660,11 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
 #pragma unroll
         for (int ht = 0; ht < HT; ++ht) {
             const int h = (16 * ht + c) % a.H;
-            const float v = g < 3 ? a.hsc[((int64_t)b * a.H + h) * 4 + g] : 0.f;
+            // slot g = 3: -s*_h against a row scalar of 1 (trigger margins), else 0
+            const float v = g < 3 ? a.hsc[((int64_t)b * a.H + h) * 4 + g]
+                                  : (a.thr ? -(float)a.thr[(int64_t)b * a.H + h] : 0.f);
             hsf[ht] = g == 0 ? scaled_a(a.cert_mult, v) : v;
-            coef = fmaxf(coef, hsf[ht]);
+            coef = fmaxf(coef, fabsf(hsf[ht]));
         }
 #pragma unroll
         for (int o = 1; o < 16; o <<= 1) coef = fmaxf(coef, shfl_xor_local(coef, o));
@@ -773,8 +790,8 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
         float m = rvmax;
 #pragma unroll
         for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, shfl_xor_local(m, o));
-        const float v = coef * m;   // lane 16 g + c; coef = 0 for g = 3
-        to.bmm = (shfl_local(v, 0) + shfl_local(v, 16)) + shfl_local(v, 32);
+        const float v = coef * m;   // lane 16 g + c; for g = 3: max |s*_h| x 1, or 0
+        to.bmm = ((shfl_local(v, 0) + shfl_local(v, 16)) + shfl_local(v, 32)) + shfl_local(v, 48);
     }
     score_finish(a, b, lane, to, UB);
 }

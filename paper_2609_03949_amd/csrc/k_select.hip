@@ -1089,15 +1089,33 @@ __global__ __launch_bounds__(SEL_THREADS) void trig_classify_kernel(SelectArgs a
         t[j] = ubb[uc];
         fin[j] = (u < ue) ? fb[uc] : (uint8_t)1;
     }
+    // the scorer wrote either UB~ (max over heads of the bound) or, given the
+    // thresholds, the trigger margins max_h (UB~_h - s*_h)
+    const bool trgm = sq[SQ_TRGM] != 0u;
+    __shared__ double s_absmax;
     if (tid < 64) {
         const double m = min_threshold(a, b);
-        if (tid == 0) s_min = m;
+        double am = 0.0;
+        for (int h = tid; h < a.H; h += 64) {
+            const double v = a.smax[(int64_t)b * a.H + h];
+            am = fmax(am, isfinite(v) ? fabs(v) : 0.0);
+        }
+        for (int o = 32; o > 0; o >>= 1) am = fmax(am, __shfl_xor(am, o));
+        if (tid == 0) {
+            s_min = m;
+            s_absmax = am;
+        }
     }
     lds_barrier();
     const double smin = s_min;
     const bool same = sq[SQ_CMULT] == __float_as_uint(a.cert_mult);
     const double E = ub_error_of(sq, a.n) * (1.0 + 0x1p-20);
-    uint32_t mask = 0;
+    // margins: the bound's fp32 error plus the fp32 rounding of s*_h and of the
+    // difference (the screen of the exact pass uses the same band)
+    const double ubmax = (double)__uint_as_float(sq[SQ_QMAX]) * nu_max_of(sq, a.n) +
+                         (double)__uint_as_float(sq[SQ_BMAX]) * (1.0 + 0x1p-20);
+    const double Em = E + 0x1p-21 * (s_absmax + ubmax);
+    uint32_t mask = 0, nfire = 0;
 #pragma unroll
     for (int j = 0; j < CB_PER; ++j) {
         const int64_t u = ub0 + tid + (int64_t)SEL_THREADS * j;
@@ -1106,6 +1124,11 @@ __global__ __launch_bounds__(SEL_THREADS) void trig_classify_kernel(SelectArgs a
             if (fin[j] != 1) {
                 if (!same || smin == -INFINITY) {
                     f = 5;
+                } else if (trgm) {
+                    // every head's margin is below zero: not fired; some head's
+                    // above: fired (decided here unless the top-j cap ranks them)
+                    const double m = (double)t[j];
+                    f = (m + Em <= 0.0) ? 0 : ((a.topj == 0 && m - Em > 0.0) ? 6 : 5);
                 } else {
                     const double tv = (double)t[j];
                     const double band = E + fabs(tv) * 0x1p-50 + fabs(smin) * 0x1p-50;
@@ -1114,13 +1137,15 @@ __global__ __launch_bounds__(SEL_THREADS) void trig_classify_kernel(SelectArgs a
             }
             f2[u] = f;
             mask |= (f == 5) ? (1u << j) : 0u;
+            nfire += (f == 6);
         }
     }
     block_append(mask, ub0, a.seq + (int64_t)b * SQ_WORDS + SQ_NCAND3, a.cand + (int64_t)b * a.A, nullptr, t,
                  a.A, s_w, &s_base);
+    nfire = block_sum<SEL_THREADS>(nfire, s_w);
     if (tid == 0) {
         uint32_t* w = a.blk + ((int64_t)b * a.nblk + blockIdx.x) * BLK_WORDS;
-        w[BW_IN] = 0u;
+        w[BW_IN] = nfire;   // rows fired here; the exact pass adds its own to BW_XIN
         w[BW_XIN] = 0u;
     }
 }

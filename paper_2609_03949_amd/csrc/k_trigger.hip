@@ -61,18 +61,47 @@ __device__ __forceinline__ bool ahead(double s1, int64_t u1, double s0, int64_t 
     return s1 > s0 || (s1 == s0 && u1 < u0);
 }
 
+// s_waitcnt operand that waits for vmcnt 0 and leaves expcnt and lgkmcnt alone
+constexpr int VMCNT0 = 0x0F70;
+
+// Block (hg, b, sp): heads 16 hg .. of sequence b over the sp-th of nsplit
+// equal ranges of the list (the ranges are exact maxima of their own rows;
+// row_merge_kernel takes the best of them, so the result is the same for any
+// nsplit).  The blocks of one (b, sp) read the same rows, so when the number
+// of (b, sp) items is a multiple of 8 they are given linear ids that are equal
+// mod 8: workgroups are dealt to the 8 XCDs round-robin by linear id, so all
+// head groups of a range share one XCD's L2.
 __global__ __launch_bounds__(64) void row_max_kernel(RowMaxArgs a) {
     __shared__ int32_t s_row[16][RM_CAND];
     __shared__ float s_ub[16][RM_CAND];
     __shared__ int s_cnt[16];
     __shared__ int s_over[16];
-    const int hg = blockIdx.x, b = blockIdx.y;
+    const int HG = (a.H + 15) / 16;
+    const int64_t items = (int64_t)a.B * a.nsplit;
+    int hg, b, sp;
+    {
+        const int64_t L = blockIdx.x;
+        int64_t j;
+        if (items % 8 == 0) {
+            const int64_t rest = L / 8;
+            hg = (int)(rest % HG);
+            j = (L % 8) + 8 * (rest / HG);
+        } else {
+            hg = (int)(L % HG);
+            j = L / HG;
+        }
+        b = (int)(j % a.B);
+        sp = (int)(j / a.B);
+    }
     const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
     const int h0 = 16 * hg;
     const int hq = h0 + c;
     const bool hq_ok = hq < a.H;
     const int64_t n1 = a.all_archive ? a.A : a.nrows;
-    const int64_t N = n1 + (a.add_recent ? a.T - a.A : 0);
+    const int64_t Nall = n1 + (a.add_recent ? a.T - a.A : 0);
+    const int64_t per = (Nall + a.nsplit - 1) / a.nsplit;
+    const int64_t pbeg = min(Nall, (int64_t)sp * per);
+    const int64_t N = min(Nall, pbeg + per);   // this block's list positions: [pbeg, N)
     const uint16_t* cb = a.cache + (int64_t)b * a.cbs;
     auto row_of = [&](int64_t p) -> int64_t {
         return p < n1 ? (a.all_archive ? p : (int64_t)a.rows[(int64_t)b * a.nrows + p]) : a.A + (p - n1);
@@ -103,28 +132,39 @@ __global__ __launch_bounds__(64) void row_max_kernel(RowMaxArgs a) {
     float M[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
     __builtin_amdgcn_wave_barrier();
 
-    auto load_tile = [&](int64_t p0, bf16x8_t (&xf)[RM_KS], int64_t& u) {
+    // this lane's row of the tile at list position p0 (clamped to the range),
+    // as a 32-bit value that is widened only where it is used, so that the
+    // index load can stay in flight
+    auto row_at = [&](int64_t p0) -> int32_t {
         const int64_t p = min(p0 + c, N - 1);
-        u = row_of(p);
-        const uint16_t* src = cb + u * a.cs + 8 * g;
+        int32_t v = (int32_t)(p < n1 ? p : a.A + (p - n1));
+        if (!a.all_archive && p < n1) v = a.rows[(int64_t)b * a.nrows + p];
+        return v;
+    };
+    auto load_rows = [&](int32_t u, bf16x8_t (&xf)[RM_KS]) {
+        const uint16_t* src = cb + (int64_t)u * a.cs + 8 * g;
 #pragma unroll
         for (int ks = 0; ks < RM_KS; ++ks) xf[ks] = *reinterpret_cast<const bf16x8_t*>(src + 32 * ks);
     };
-    bf16x8_t xa[RM_KS];
-    int64_t ua = 0;
-    if (N > 0) load_tile(0, xa, ua);
-    for (int64_t p0 = 0; p0 < N; p0 += 16) {
-        // next tile's loads in flight while this one is scored
-        bf16x8_t xb[RM_KS];
-        int64_t ub = 0;
-        if (p0 + 16 < N) load_tile(p0 + 16, xb, ub);
+    // One tile (rows uc, data xc).  The wait at its start drains every load
+    // in flight: the tile's own rows and the row indices of the next tile,
+    // both issued a tile earlier.  Then the row indices two tiles ahead (unn)
+    // and the next tile's rows (xn, rows un) go out and are in flight while
+    // this one is scored.  The two row buffers swap roles from tile to tile,
+    // so no register copy waits for a load, and the explicit wait tells the
+    // compiler that nothing older is outstanding.
+    auto score_tile = [&](int64_t p0, bf16x8_t (&xc)[RM_KS], int32_t uc, bf16x8_t (&xn)[RM_KS], int32_t un,
+                          int32_t& unn) {
+        __builtin_amdgcn_s_waitcnt(VMCNT0);
+        unn = p0 + 32 < N ? row_at(p0 + 32) : 0;
+        if (p0 + 16 < N) load_rows(un, xn);
         const bool valid = p0 + c < N;
         f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
         float xs = 0.f;
 #pragma unroll
         for (int ks = 0; ks < RM_KS; ++ks) {
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[ks], xa[ks], acc, 0, 0, 0);
-            xs += sumsq8(xa[ks]);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[ks], xc[ks], acc, 0, 0, 0);
+            xs += sumsq8(xc[ks]);
         }
         xs += __shfl_xor(xs, 16);
         xs += __shfl_xor(xs, 32);
@@ -182,7 +222,7 @@ __global__ __launch_bounds__(64) void row_max_kernel(RowMaxArgs a) {
             if (cand) {
                 const int q = cnt + __popc(gm & ((1u << c) - 1u));
                 if (q < RM_CAND) {
-                    s_row[hl][q] = (int32_t)ua;
+                    s_row[hl][q] = (int32_t)uc;
                     s_ub[hl][q] = hi[i];
                 } else {
                     s_over[hl] = 1;   // more near-ties than the list holds: all rows are evaluated
@@ -191,15 +231,30 @@ __global__ __launch_bounds__(64) void row_max_kernel(RowMaxArgs a) {
             if (c == 0) s_cnt[hl] = min(cnt + __popc(gm), RM_CAND);
             __builtin_amdgcn_wave_barrier();
         }
-#pragma unroll
-        for (int ks = 0; ks < RM_KS; ++ks) xa[ks] = xb[ks];
-        ua = ub;
+    };
+    bf16x8_t xa[RM_KS], xb[RM_KS];
+    int32_t ua = 0, ub = 0;
+    if (N > pbeg) {
+        ua = row_at(pbeg);
+        load_rows(ua, xa);
+        ub = pbeg + 16 < N ? row_at(pbeg + 16) : 0;
+    }
+    for (int64_t p0 = pbeg; p0 < N; p0 += 32) {
+        int32_t ua2 = 0, ub2 = 0;
+        score_tile(p0, xa, ua, xb, ub, ua2);
+        if (p0 + 16 >= N) break;
+        score_tile(p0 + 16, xb, ub, xa, ua2, ub2);
+        ua = ua2;
+        ub = ub2;
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_wave_barrier();
-    // exact fp64 scores of the candidates that reach the final bound
+    // exact fp64 scores of the candidates that reach the final bound (M is
+    // read with constant indices: a dynamic index would move it to scratch
+    // memory, whose accesses in the tile loop wait for the prefetched tile)
 #pragma unroll 1
     for (int i = 0; i < 4; ++i) {
+        const float Mi = i == 0 ? M[0] : (i == 1 ? M[1] : (i == 2 ? M[2] : M[3]));
         const int hl = 4 * g + i, h = h0 + hl;
         const bool hv = h < a.H;
         const int64_t hb = (int64_t)b * a.H + (hv ? h : 0);
@@ -207,11 +262,11 @@ __global__ __launch_bounds__(64) void row_max_kernel(RowMaxArgs a) {
         const uint16_t* qr = a.q_rope + hb * D_ROPE;
         double best = -INFINITY;
         int64_t arg = -1;
-        if (hv && N > 0) {
+        if (hv && N > pbeg) {
             if (!s_over[hl]) {
                 const int cnt = s_cnt[hl];
                 for (int q = c; q < cnt; q += 16) {
-                    if (!(s_ub[hl][q] >= M[i])) continue;
+                    if (!(s_ub[hl][q] >= Mi)) continue;
                     const int64_t u = s_row[hl][q];
                     const double v = full_score64(ql, qr, cb + u * a.cs);
                     if (ahead(v, u, best, arg)) {
@@ -220,7 +275,7 @@ __global__ __launch_bounds__(64) void row_max_kernel(RowMaxArgs a) {
                     }
                 }
             } else {
-                for (int64_t p = c; p < N; p += 16) {
+                for (int64_t p = pbeg + c; p < N; p += 16) {
                     const int64_t u = row_of(p);
                     const double v = full_score64(ql, qr, cb + u * a.cs);
                     if (ahead(v, u, best, arg)) {
@@ -241,15 +296,42 @@ __global__ __launch_bounds__(64) void row_max_kernel(RowMaxArgs a) {
             }
         }
         if (c == 0 && hv) {
-            a.smax[hb] = best;
-            a.argmax[hb] = (int32_t)arg;
+            if (a.nsplit > 1) {
+                a.part_v[hb * a.nsplit + sp] = best;
+                a.part_u[hb * a.nsplit + sp] = (int32_t)arg;
+            } else {
+                a.smax[hb] = best;
+                a.argmax[hb] = (int32_t)arg;
+            }
         }
     }
 }
 
+// (max, lowest row) over the ranges of each (sequence, head)
+__global__ __launch_bounds__(64) void row_merge_kernel(RowMaxArgs a) {
+    const int64_t t = (int64_t)blockIdx.x * 64 + threadIdx.x;
+    if (t >= (int64_t)a.B * a.H) return;
+    double best = -INFINITY;
+    int64_t arg = -1;
+    for (int sp = 0; sp < a.nsplit; ++sp) {
+        const double v = a.part_v[t * a.nsplit + sp];
+        const int64_t u = a.part_u[t * a.nsplit + sp];
+        if (u >= 0 && ahead(v, u, best, arg)) {
+            best = v;
+            arg = u;
+        }
+    }
+    a.smax[t] = best;
+    a.argmax[t] = (int32_t)arg;
+}
+
 hipError_t launch_row_max(const RowMaxArgs& a, hipStream_t s) {
-    dim3 grid((unsigned)((a.H + 15) / 16), (unsigned)a.B);
-    hipLaunchKernelGGL(row_max_kernel, grid, dim3(64), 0, s, a);
+    const unsigned nblk = (unsigned)(((a.H + 15) / 16) * a.B * a.nsplit);
+    hipLaunchKernelGGL(row_max_kernel, dim3(nblk), dim3(64), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || a.nsplit <= 1) return e;
+    const int64_t n = (int64_t)a.B * a.H;
+    hipLaunchKernelGGL(row_merge_kernel, dim3((unsigned)((n + 63) / 64)), dim3(64), 0, s, a);
     return hipGetLastError();
 }
 

@@ -133,6 +133,7 @@ static WsLayout layout(const vkv_step* st, int64_t k, int64_t cap) {
     L.candkey = o; o = up256(o + (size_t)(B * Aw * 4));
     L.amb = o; o = up256(o + (size_t)(B * Aw * 4));
     L.ambkey = o; o = up256(o + (size_t)(B * Aw * 8));
+    L.rmx = o; o = up256(o + (size_t)(B * H * RM_MAX_SPLIT * 12));
     // everything above is independent of k and cap; the attention partials last
     attend_split(st, k, cap, &L.splits, &L.rows_per_split);
     const int64_t HG = (H + ATT_HEADS - 1) / ATT_HEADS;   // partials padded to whole head groups
@@ -511,8 +512,10 @@ static hipError_t run_prep(const vkv_step* st, char* w, Chunk c, hipStream_t s) 
 }
 
 static hipError_t run_score(const vkv_step* st, char* w, Chunk c, float* key, float* ub, float cert_mult,
-                            hipStream_t s) {
-    return launch_score(score_args(st, layout(st, 0, 0), w, c, key, ub, cert_mult), s);
+                            hipStream_t s, const double* thr = nullptr) {
+    ScoreArgs a = score_args(st, layout(st, 0, 0), w, c, key, ub, cert_mult);
+    a.thr = thr ? thr + c.b0 * st->H : nullptr;
+    return launch_score(a, s);
 }
 
 static hipError_t run_select(const vkv_step* st, char* w, Chunk c, int64_t k, int32_t* sel, double* theta,
@@ -673,8 +676,20 @@ int vkv_step_run(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, in
 }
 
 static hipError_t run_row_max(const vkv_step* st, const int32_t* rows, int64_t nrows, int all_archive, int add_recent,
-                              double* smax, int32_t* argmax, hipStream_t s) {
+                              double* smax, int32_t* argmax, hipStream_t s, char* ws = nullptr) {
     RowMaxArgs a{};
+    // with a workspace: row ranges in parallel, about 2048 waves in all, at least 64 rows each
+    a.nsplit = 1;
+    if (ws) {
+        const int64_t N = (all_archive ? st->T - st->W : nrows) + (add_recent ? st->W : 0);
+        const int64_t waves = ((st->H + 15) / 16) * st->B;
+        int64_t ns = std::max<int64_t>(1, 2048 / std::max<int64_t>(waves, 1));
+        ns = std::min<int64_t>({ns, (int64_t)RM_MAX_SPLIT, std::max<int64_t>(1, N / 64)});
+        a.nsplit = (int)ns;
+        const WsLayout L = layout(st, 0, 0);
+        a.part_v = reinterpret_cast<double*>(ws + L.rmx);
+        a.part_u = reinterpret_cast<int32_t*>(ws + L.rmx + (size_t)(st->B * st->H * RM_MAX_SPLIT * 8));
+    }
     a.q_lat = st->q_lat;
     a.q_rope = st->q_rope;
     a.cache = st->cache;
@@ -829,7 +844,7 @@ int vkv_step_run_trigger(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_b
     HIP_TRY(ctx, run_score(st, w, all, key, ub, cert_mult, s));
     HIP_TRY(ctx, run_select(st, w, all, k, sel, theta, s));
     // the tier-1 maximum logit per head over S and the recent window
-    HIP_TRY(ctx, run_row_max(st, sel, k, 0, 1, smax, argmax, s));
+    HIP_TRY(ctx, run_row_max(st, sel, k, 0, 1, smax, argmax, s, w));
     HIP_TRY(ctx, run_trigger(st, w, k, sel, ub, cert_mult, smax, topj, fired, fired_count, cap, s));
     HIP_TRY(ctx, run_attend(st, w, all, k, sel, fired, fired_count, cap, scale, out, lse, s));
     if ((rc = debug_check_sel(ctx, st, k, sel, s))) return rc;
@@ -915,10 +930,12 @@ int vkv_step_run_kept(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_byte
     char* w = (char*)ws;
     const Chunk all{0, st->B};
     const WsLayout L = layout(st, k, cap);
+    // the tier's maximum logit does not depend on the scan, so it comes first
+    // and the scan writes the trigger margins max_h (UB~_h - s*_h) directly
     HIP_TRY(ctx, run_prep(st, w, all, s));
-    HIP_TRY(ctx, run_score(st, w, all, key, ub, cert_mult, s));
     HIP_TRY(ctx, launch_mark_tier(reinterpret_cast<uint8_t*>(w + L.flags), flag_stride(L.A), L.A, (int)st->B, kept, k, s));
-    HIP_TRY(ctx, run_row_max(st, kept, k, 0, 1, smax, argmax, s));
+    HIP_TRY(ctx, run_row_max(st, kept, k, 0, 1, smax, argmax, s, w));
+    HIP_TRY(ctx, run_score(st, w, all, key, ub, cert_mult, s, smax));
     HIP_TRY(ctx, run_trigger(st, w, k, kept, ub, cert_mult, smax, topj, fired, fired_count, cap, s));
     HIP_TRY(ctx, run_attend(st, w, all, k, kept, fired, fired_count, cap, scale, out, lse, s));
     if ((rc = debug_check_sel(ctx, st, k, kept, s))) return rc;

@@ -141,6 +141,7 @@ enum SeqWord : int {
     SQ_NCAND2 = 18, // undecided admission rows listed by the classification (zeroed by its consumer)
     SQ_NCAND3 = 19, // trigger candidates listed by the trigger classification (zeroed by its consumer)
     SQ_NFIRED = 20, // rows the trigger fired before the top-j cap (diagnostic)
+    SQ_TRGM = 21,   // 1: the scorer's ub holds trigger margins max_h (UB~_h - s*_h)
     SQ_WORDS = 32
 };
 
@@ -155,7 +156,7 @@ constexpr int ATT_HEADS = 128;     // heads per attention workgroup (8 waves x 1
 constexpr int ATT_MAX_SPLIT_ROWS = 1024;   // rows of one split (row list held in LDS)
 
 struct WsLayout {
-    size_t qt, hsc, seq, kt, flags, flags2, blk, cand, candkey, amb, ambkey, part_o, part_ml, total;
+    size_t qt, hsc, seq, kt, flags, flags2, blk, cand, candkey, amb, ambkey, rmx, part_o, part_ml, total;
     int64_t A, n, nblk, splits, rows_per_split, cap;
 };
 
@@ -187,6 +188,7 @@ struct ScoreArgs {
     int64_t A;
     int B, H, n;
     float cert_mult;       // (UB) multiplier of the sketch-residual term a_h eta_u
+    const double* thr;     // (UB) [B,H] trigger thresholds s*_h, or null: ub holds max_h (UB~_h - s*_h)
 };
 
 struct DigestArgs {
@@ -245,7 +247,11 @@ struct RowMaxArgs {
     int B, H;
     double* smax;           // [B,H]
     int32_t* argmax;        // [B,H]
+    int nsplit;             // row ranges scanned in parallel (1: no scratch needed)
+    double* part_v;         // [B,H,nsplit] per-range maxima (nsplit > 1)
+    int32_t* part_u;        // [B,H,nsplit] their rows
 };
+constexpr int RM_MAX_SPLIT = 16;
 
 struct InflArgs {
     const uint16_t* x;      // index rows
