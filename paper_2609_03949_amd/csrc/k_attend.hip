@@ -45,6 +45,32 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void gbl_void_t;
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 
+// rows attended by sequence b: kept, window, admitted (up to the capacity)
+__device__ __forceinline__ int64_t attended_count(const AttendArgs& a, int b) {
+    const int64_t nadm = (a.adm && a.cap > 0) ? min((int64_t)max(a.adm_count[b], 0), a.cap) : 0;
+    return a.k + a.W + nadm;
+}
+
+// list positions [p0, p1) of split sp (empty past the end of the list)
+__device__ __forceinline__ void split_range(const AttendArgs& a, int sp, int64_t N, int64_t& p0, int64_t& p1) {
+    const int64_t base_end = (int64_t)a.base_splits * a.rows_per_split;
+    if (sp < a.base_splits) {
+        p0 = (int64_t)sp * a.rows_per_split;
+        p1 = min(N, p0 + a.rows_per_split);
+    } else {
+        p0 = base_end + (int64_t)(sp - a.base_splits) * a.rows_per_adm;
+        p1 = min(N, p0 + a.rows_per_adm);
+    }
+    p1 = max(p1, p0);
+}
+
+// the number of splits that hold rows of a list of N rows
+__device__ __forceinline__ int live_splits(const AttendArgs& a, int64_t N) {
+    const int64_t base_end = (int64_t)a.base_splits * a.rows_per_split;
+    if (N <= base_end) return (int)((N + a.rows_per_split - 1) / a.rows_per_split);
+    return a.base_splits + (int)((N - base_end + a.rows_per_adm - 1) / a.rows_per_adm);
+}
+
 __device__ __forceinline__ int32_t attended_row(const AttendArgs& a, int b, int64_t p) {
     if (p < a.k) return a.sel[(int64_t)b * a.k + p];
     if (p < a.k + a.W) return (int32_t)(a.A + (p - a.k));
@@ -123,10 +149,9 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
     const int tid = threadIdx.x;
     const int lane = tid & 63, g = lane >> 4, c = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int64_t nadm = (a.adm && a.cap > 0) ? min((int64_t)max(a.adm_count[b], 0), a.cap) : 0;
-    const int64_t N = a.k + a.W + nadm;
-    const int64_t p0 = (int64_t)sp * a.rows_per_split;
-    const int64_t p1 = min(N, p0 + a.rows_per_split);
+    const int64_t N = attended_count(a, b);
+    int64_t p0, p1;
+    split_range(a, sp, N, p0, p1);
     const int HG = (a.H + ATT_HEADS - 1) / ATT_HEADS;
     uint16_t* po = a.part_o + (((int64_t)b * a.splits + sp) * HG + hg) * (ATT_HEADS * D_LAT);
     float* pml = a.part_ml + ((int64_t)b * a.splits + sp) * a.H * 2;
@@ -387,13 +412,15 @@ __global__ __launch_bounds__(128) void attend_combine_kernel(AttendArgs a) {
     float acc[4][4] = {};
 #pragma unroll
     for (int i = 0; i < 4; ++i) M[i] = -INFINITY;
-    for (int s0 = 0; s0 < a.splits; s0 += COMB_SPLITS) {
+    // only the splits that hold rows are read (at most all of them)
+    const int nlive = min(a.splits, live_splits(a, attended_count(a, b)));
+    for (int s0 = 0; s0 < nlive; s0 += COMB_SPLITS) {
         float ms[COMB_SPLITS][4], ls[COMB_SPLITS][4];
         u32x4_t raw[COMB_SPLITS][2];
 #pragma unroll
         for (int u = 0; u < COMB_SPLITS; ++u) {
             const int s = s0 + u;
-            const bool live = s < a.splits;
+            const bool live = s < nlive;
             const float* ml = a.part_ml + (((int64_t)b * a.splits + (live ? s : s0)) * a.H) * 2;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {

@@ -37,23 +37,52 @@ __device__ __forceinline__ float sumsq8(bf16x8_t v) {
 }
 
 // exact fp64 full score of row `row` for the head whose query rows are ql / qr
+// (the products of two bf16 values are exact in fp64; they are added in
+// dimension order from +0).  Pieces of 32 dims are loaded one piece ahead of
+// the chain, so the memory round trips overlap the arithmetic.
 __device__ __forceinline__ double full_score64(const uint16_t* ql, const uint16_t* qr, const uint16_t* row) {
-    double acc = 0.0;
-#pragma unroll 1
-    for (int p0 = 0; p0 < D_ROW / 8; p0 += 8) {
-        u16x8_t qv[8], xv[8];
+    constexpr int NP = D_ROW / 32;   // 18 pieces of 4 x 8 dims
+    u16x8_t qv[2][4], xv[2][4];
+    auto load = [&](int p, int buf) __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int d = 8 * (p0 + j);
-            qv[j] = *reinterpret_cast<const u16x8_t*>(d < D_LAT ? ql + d : qr + (d - D_LAT));
-            xv[j] = *reinterpret_cast<const u16x8_t*>(row + d);
+        for (int j = 0; j < 4; ++j) {
+            const int d = 32 * p + 8 * j;
+            qv[buf][j] = *reinterpret_cast<const u16x8_t*>(d < D_LAT ? ql + d : qr + (d - D_LAT));
+            xv[buf][j] = *reinterpret_cast<const u16x8_t*>(row + d);
         }
+    };
+    double acc = 0.0;
+    auto chain = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc = fma((double)bf16_to_f32(qv[j][e]), (double)bf16_to_f32(xv[j][e]), acc);
+            for (int e = 0; e < 8; ++e)
+                acc = fma((double)bf16_to_f32(qv[buf][j][e]), (double)bf16_to_f32(xv[buf][j][e]), acc);
+    };
+    static_assert(NP % 2 == 0, "pieces taken in pairs");
+    load(0, 0);
+    // a loop, not unrolled: a fully unrolled chain lets the compiler issue all
+    // loads first and spill them
+#pragma unroll 1
+    for (int p = 0; p < NP; p += 2) {
+        load(p + 1, 1);
+        chain(0);
+        if (p + 2 < NP) load(p + 2, 0);
+        chain(1);
     }
     return acc;
+}
+
+// max over the 16 lanes of each row of the wave (DPP lane permutations)
+__device__ __forceinline__ float rowmax16(float v) {
+    auto perm = [](float x, auto ctrl) __attribute__((always_inline)) {
+        return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), decltype(ctrl)::value, 0xF, 0xF, true));
+    };
+    v = fmaxf(v, perm(v, std::integral_constant<int, 0xB1>{}));    // quad_perm [1,0,3,2]
+    v = fmaxf(v, perm(v, std::integral_constant<int, 0x4E>{}));    // quad_perm [2,3,0,1]
+    v = fmaxf(v, perm(v, std::integral_constant<int, 0x141>{}));   // row_half_mirror
+    v = fmaxf(v, perm(v, std::integral_constant<int, 0x140>{}));   // row_mirror
+    return v;
 }
 
 // (score desc, row asc): is (s1, u1) ahead of (s0, u0)?
@@ -61,42 +90,40 @@ __device__ __forceinline__ bool ahead(double s1, int64_t u1, double s0, int64_t 
     return s1 > s0 || (s1 == s0 && u1 < u0);
 }
 
-// s_waitcnt operand that waits for vmcnt 0 and leaves expcnt and lgkmcnt alone
-constexpr int VMCNT0 = 0x0F70;
+// Block (hgb, b, sp): RM_WAVES waves, wave w taking heads 16 (RM_WAVES hgb +
+// w) .. +15 of sequence b, over the sp-th of nsplit equal ranges of the list
+// (each range yields the exact maximum of its own rows; row_merge_kernel takes
+// the best of them, so the result is the same for any nsplit).  The block
+// streams its range in tiles of RM_TILE rows through a two-stage LDS ring that
+// all its waves read, so a row is fetched from memory once per block, not
+// once per 16 heads.  Tile t + 1's 16-byte pieces are loaded into registers
+// while tile t is scored and are written to the other stage after it; the row
+// indices go out one tile earlier still.  Stage slot (r, p) holds piece
+// p ^ (r mod 8) of tile row r, so the eight lanes that one 128-bit LDS read
+// serves (eight rows, one piece) hit distinct bank groups.
+constexpr int RM_WAVES = 8;
+constexpr int VMCNT0 = 0x0F70;   // s_waitcnt operand: vmcnt 0, expcnt and lgkmcnt left alone
+constexpr int RM_THREADS = 64 * RM_WAVES;
+constexpr int RM_TILE = 32;                                   // rows per tile
+constexpr int RM_PIECES = RM_TILE * (D_ROW / 8);              // 16-byte pieces per tile
+constexpr int RM_PER = (RM_PIECES + RM_THREADS - 1) / RM_THREADS;   // pieces per thread
 
-// Block (hg, b, sp): heads 16 hg .. of sequence b over the sp-th of nsplit
-// equal ranges of the list (the ranges are exact maxima of their own rows;
-// row_merge_kernel takes the best of them, so the result is the same for any
-// nsplit).  The blocks of one (b, sp) read the same rows, so when the number
-// of (b, sp) items is a multiple of 8 they are given linear ids that are equal
-// mod 8: workgroups are dealt to the 8 XCDs round-robin by linear id, so all
-// head groups of a range share one XCD's L2.
-__global__ __launch_bounds__(64) void row_max_kernel(RowMaxArgs a) {
-    __shared__ int32_t s_row[16][RM_CAND];
-    __shared__ float s_ub[16][RM_CAND];
-    __shared__ int s_cnt[16];
-    __shared__ int s_over[16];
+__global__ __launch_bounds__(RM_THREADS) void row_max_kernel(RowMaxArgs a) {
+    __shared__ __align__(16) uint8_t s_x[2][RM_TILE * 2 * D_ROW];
+    __shared__ int32_t s_id[2][RM_TILE];
+    __shared__ int32_t s_row[RM_WAVES][16][RM_CAND];
+    __shared__ float s_ub[RM_WAVES][16][RM_CAND];
     const int HG = (a.H + 15) / 16;
-    const int64_t items = (int64_t)a.B * a.nsplit;
-    int hg, b, sp;
-    {
-        const int64_t L = blockIdx.x;
-        int64_t j;
-        if (items % 8 == 0) {
-            const int64_t rest = L / 8;
-            hg = (int)(rest % HG);
-            j = (L % 8) + 8 * (rest / HG);
-        } else {
-            hg = (int)(L % HG);
-            j = L / HG;
-        }
-        b = (int)(j % a.B);
-        sp = (int)(j / a.B);
-    }
-    const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+    const int HGB = (HG + RM_WAVES - 1) / RM_WAVES;
+    const int hgb = (int)(blockIdx.x % HGB);
+    const int64_t jb = blockIdx.x / HGB;
+    const int b = (int)(jb % a.B), sp = (int)(jb / a.B);
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, g = lane >> 4, c = lane & 15;
+    const int hg = hgb * RM_WAVES + wave;
+    const bool wave_on = hg < HG;   // waves past the last head group only load
     const int h0 = 16 * hg;
     const int hq = h0 + c;
-    const bool hq_ok = hq < a.H;
+    const bool hq_ok = wave_on && hq < a.H;
     const int64_t n1 = a.all_archive ? a.A : a.nrows;
     const int64_t Nall = n1 + (a.add_recent ? a.T - a.A : 0);
     const int64_t per = (Nall + a.nsplit - 1) / a.nsplit;
@@ -106,10 +133,6 @@ __global__ __launch_bounds__(64) void row_max_kernel(RowMaxArgs a) {
     auto row_of = [&](int64_t p) -> int64_t {
         return p < n1 ? (a.all_archive ? p : (int64_t)a.rows[(int64_t)b * a.nrows + p]) : a.A + (p - n1);
     };
-    if (lane < 16) {
-        s_cnt[lane] = 0;
-        s_over[lane] = 0;
-    }
     // query fragments (A operand): head hq, dims 32 ks + 8 g; ||q_hq||^2 in fp32
     bf16x8_t qf[RM_KS];
     float qs = 0.f;
@@ -130,67 +153,85 @@ __global__ __launch_bounds__(64) void row_max_kernel(RowMaxArgs a) {
     for (int i = 0; i < 4; ++i) qub[i] = sqrtf(__shfl(qs, 4 * g + i) * (1.0f + 0x1p-12f)) * (1.0f + 0x1p-20f);
     constexpr float KE = 2.0f * (float)(D_ROW + D_ROW / 32) * 0x1p-23f;
     float M[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-    __builtin_amdgcn_wave_barrier();
+    // per head 4 g + i: entries in its list in byte i of ncand (the same in
+    // the group's 16 lanes), and in bit i of ovf whether an entry did not fit
+    // (set in the lane that had it); packed to spare registers in the loop
+    uint32_t ncand = 0, ovf = 0;
 
-    // this lane's row of the tile at list position p0 (clamped to the range),
-    // as a 32-bit value that is widened only where it is used, so that the
-    // index load can stay in flight
-    auto row_at = [&](int64_t p0) -> int32_t {
-        const int64_t p = min(p0 + c, N - 1);
-        int32_t v = (int32_t)(p < n1 ? p : a.A + (p - n1));
-        if (!a.all_archive && p < n1) v = a.rows[(int64_t)b * a.nrows + p];
-        return v;
-    };
-    auto load_rows = [&](int32_t u, bf16x8_t (&xf)[RM_KS]) {
-        const uint16_t* src = cb + (int64_t)u * a.cs + 8 * g;
+    // loader: thread tid moves pieces q = tid + RM_THREADS i of a tile, piece
+    // q mod 72 of tile row q / 72 (rows past the range repeat its last row;
+    // they are loaded, never scored)
+    auto load_ids = [&](int64_t t0, int32_t (&id)[RM_PER]) {
 #pragma unroll
-        for (int ks = 0; ks < RM_KS; ++ks) xf[ks] = *reinterpret_cast<const bf16x8_t*>(src + 32 * ks);
+        for (int i = 0; i < RM_PER; ++i) {
+            const int q = tid + RM_THREADS * i;
+            if (q < RM_PIECES) {
+                const int64_t p = min(t0 + q / (D_ROW / 8), N - 1);
+                int32_t v = (int32_t)(p < n1 ? p : a.A + (p - n1));
+                if (!a.all_archive && p < n1) v = a.rows[(int64_t)b * a.nrows + p];
+                id[i] = v;
+            }
+        }
     };
-    // One tile (rows uc, data xc).  The wait at its start drains every load
-    // in flight: the tile's own rows and the row indices of the next tile,
-    // both issued a tile earlier.  Then the row indices two tiles ahead (unn)
-    // and the next tile's rows (xn, rows un) go out and are in flight while
-    // this one is scored.  The two row buffers swap roles from tile to tile,
-    // so no register copy waits for a load, and the explicit wait tells the
-    // compiler that nothing older is outstanding.
-    auto score_tile = [&](int64_t p0, bf16x8_t (&xc)[RM_KS], int32_t uc, bf16x8_t (&xn)[RM_KS], int32_t un,
-                          int32_t& unn) {
-        __builtin_amdgcn_s_waitcnt(VMCNT0);
-        unn = p0 + 32 < N ? row_at(p0 + 32) : 0;
-        if (p0 + 16 < N) load_rows(un, xn);
+    u32x4_t xr[RM_PER];
+    auto load_pieces = [&](const int32_t (&id)[RM_PER]) {
+#pragma unroll
+        for (int i = 0; i < RM_PER; ++i) {
+            const int q = tid + RM_THREADS * i;
+            if (q < RM_PIECES) {
+                const int s = q % (D_ROW / 8);
+                xr[i] = *reinterpret_cast<const u32x4_t*>(cb + (int64_t)id[i] * a.cs + 8 * s);
+            }
+        }
+    };
+    auto store_pieces = [&](int st, const int32_t (&id)[RM_PER]) {
+#pragma unroll
+        for (int i = 0; i < RM_PER; ++i) {
+            const int q = tid + RM_THREADS * i;
+            if (q < RM_PIECES) {
+                const int r = q / (D_ROW / 8), s = q - (D_ROW / 8) * r;
+                *reinterpret_cast<u32x4_t*>(s_x[st] + r * (2 * D_ROW) + 16 * (s ^ (r & 7))) = xr[i];
+                if (s == 0) s_id[st][r] = id[i];
+            }
+        }
+    };
+
+    // one 16-row half of the tile in stage st (list positions p0 ..)
+    auto score_half = [&](int st, int m, int64_t p0) __attribute__((always_inline)) {
+        const int rl = 16 * m + c;   // this lane's tile row
         const bool valid = p0 + c < N;
+        const uint8_t* xrow = s_x[st] + rl * (2 * D_ROW);
         f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
         float xs = 0.f;
 #pragma unroll
         for (int ks = 0; ks < RM_KS; ++ks) {
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[ks], xc[ks], acc, 0, 0, 0);
-            xs += sumsq8(xc[ks]);
+            const bf16x8_t xv = *reinterpret_cast<const bf16x8_t*>(xrow + 16 * ((4 * ks + g) ^ (c & 7)));
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[ks], xv, acc, 0, 0, 0);
+            xs += sumsq8(xv);
         }
         xs += __shfl_xor(xs, 16);
         xs += __shfl_xor(xs, 32);
         const float xub = sqrtf(xs * (1.0f + 0x1p-12f)) * (1.0f + 0x1p-20f);
-        float lo[4], hi[4];
+        const int32_t uc = s_id[st][rl];
+        float hi[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const float e = next_up_f32(KE * qub[i] * xub * (1.0f + 0x1p-20f) + (float)D_ROW * 0x1p-120f);
-            lo[i] = valid ? next_down_f32(acc[i] - e) : -INFINITY;
+            const float lo = valid ? next_down_f32(acc[i] - e) : -INFINITY;
             hi[i] = valid ? next_up_f32(acc[i] + e) : -INFINITY;
-            // running certified lower bound of the maximum: over the 16 rows of the tile (lanes of the group)
-            float m = lo[i];
-            m = fmaxf(m, __shfl_xor(m, 1));
-            m = fmaxf(m, __shfl_xor(m, 2));
-            m = fmaxf(m, __shfl_xor(m, 4));
-            m = fmaxf(m, __shfl_xor(m, 8));
-            M[i] = fmaxf(M[i], m);
+            // running certified lower bound of the maximum: over the 16 rows (lanes of the group)
+            M[i] = fmaxf(M[i], rowmax16(lo));
         }
         // rows whose upper bound reaches the running bound join the head's list
+        // (most halves have none: one ballot per head then skips the rest)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int hl = 4 * g + i;
             const bool cand = hi[i] >= M[i] && valid;
             const uint64_t bal = __ballot(cand);
+            if (bal == 0) continue;
+            const int hl = 4 * g + i;
             const uint32_t gm = (uint32_t)(bal >> (16 * g)) & 0xFFFFu;
-            int cnt = s_cnt[hl];
+            int cnt = (int)((ncand >> (8 * i)) & 0xFFu);
             if (cnt + __popc(gm) > RM_CAND) {
                 // prune the entries the running bound has passed (16 lanes, 4 entries each)
                 int keep[4];
@@ -199,8 +240,8 @@ __global__ __launch_bounds__(64) void row_max_kernel(RowMaxArgs a) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const int q = c + 16 * j;
-                    kr[j] = s_row[hl][q];
-                    ku[j] = s_ub[hl][q];
+                    kr[j] = s_row[wave][hl][q];
+                    ku[j] = s_ub[wave][hl][q];
                     keep[j] = (q < cnt && ku[j] >= M[i]) ? 1 : 0;
                 }
                 __builtin_amdgcn_wave_barrier();
@@ -210,98 +251,141 @@ __global__ __launch_bounds__(64) void row_max_kernel(RowMaxArgs a) {
                     const uint32_t km = (uint32_t)(__ballot(keep[j]) >> (16 * g)) & 0xFFFFu;
                     if (keep[j]) {
                         const int q = base + __popc(km & ((1u << c) - 1u));
-                        s_row[hl][q] = kr[j];
-                        s_ub[hl][q] = ku[j];
+                        s_row[wave][hl][q] = kr[j];
+                        s_ub[wave][hl][q] = ku[j];
                     }
                     base += __popc(km);
                 }
                 cnt = base;
-                if (c == 0) s_cnt[hl] = cnt;
                 __builtin_amdgcn_wave_barrier();
             }
             if (cand) {
                 const int q = cnt + __popc(gm & ((1u << c) - 1u));
                 if (q < RM_CAND) {
-                    s_row[hl][q] = (int32_t)uc;
-                    s_ub[hl][q] = hi[i];
+                    s_row[wave][hl][q] = uc;
+                    s_ub[wave][hl][q] = hi[i];
                 } else {
-                    s_over[hl] = 1;   // more near-ties than the list holds: all rows are evaluated
+                    ovf |= 1u << i;   // more near-ties than the list holds: all rows are evaluated
                 }
             }
-            if (c == 0) s_cnt[hl] = min(cnt + __popc(gm), RM_CAND);
+            ncand = (ncand & ~(0xFFu << (8 * i))) | ((uint32_t)min(cnt + __popc(gm), RM_CAND) << (8 * i));
             __builtin_amdgcn_wave_barrier();
         }
     };
-    bf16x8_t xa[RM_KS], xb[RM_KS];
-    int32_t ua = 0, ub = 0;
-    if (N > pbeg) {
-        ua = row_at(pbeg);
-        load_rows(ua, xa);
-        ub = pbeg + 16 < N ? row_at(pbeg + 16) : 0;
+
+    const int64_t ntiles = N > pbeg ? (N - pbeg + RM_TILE - 1) / RM_TILE : 0;   // the same in every wave
+    int32_t id_a[RM_PER] = {}, id_b[RM_PER] = {};
+    if (ntiles > 0) {
+        load_ids(pbeg, id_a);
+        load_pieces(id_a);
+        store_pieces(0, id_a);
     }
-    for (int64_t p0 = pbeg; p0 < N; p0 += 32) {
-        int32_t ua2 = 0, ub2 = 0;
-        score_tile(p0, xa, ua, xb, ub, ua2);
-        if (p0 + 16 >= N) break;
-        score_tile(p0 + 16, xb, ub, xa, ua2, ub2);
-        ua = ua2;
-        ub = ub2;
+    if (ntiles > 1) load_ids(pbeg + RM_TILE, id_b);
+    __builtin_amdgcn_s_waitcnt(VMCNT0);
+    __syncthreads();
+    // tile t: id_next = row indices of tile t + 1 (loaded a tile ago); the
+    // indices of tile t + 2 go into id_next2.  The two index buffers swap roles
+    // from tile to tile, so no register copy waits for a load.
+    auto tile = [&](int64_t t, const int32_t (&id_next)[RM_PER], int32_t (&id_next2)[RM_PER])
+                    __attribute__((always_inline)) {
+        const int st = (int)(t & 1);
+        const int64_t p0 = pbeg + RM_TILE * t;
+        if (t + 1 < ntiles) load_pieces(id_next);
+        if (t + 2 < ntiles) load_ids(p0 + 2 * RM_TILE, id_next2);
+        if (wave_on) {
+            score_half(st, 0, p0);
+            score_half(st, 1, p0 + 16);
+        }
+        // every wave is past tile t - 1, whose stage this refills (the barrier
+        // that ended it); tile t + 1 becomes visible at the barrier below
+        if (t + 1 < ntiles) store_pieces(st ^ 1, id_next);
+        // nothing stays in flight past a tile (the indices of tile t + 2 have
+        // had the whole tile to land), so no path into the next tile leaves
+        // the compiler a load it has to wait for early
+        __builtin_amdgcn_s_waitcnt(VMCNT0);
+        __syncthreads();
+    };
+    for (int64_t t = 0; t < ntiles; t += 2) {
+        tile(t, id_b, id_a);
+        if (t + 1 >= ntiles) break;
+        tile(t + 1, id_a, id_b);
     }
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    if (!wave_on) return;
     __builtin_amdgcn_wave_barrier();
-    // exact fp64 scores of the candidates that reach the final bound (M is
-    // read with constant indices: a dynamic index would move it to scratch
-    // memory, whose accesses in the tile loop wait for the prefetched tile)
+    // Exact fp64 scores of the list entries whose bound reaches the final M_h.
+    // The four lists of a group are taken as one sequence of (head, entry)
+    // pairs dealt to its 16 lanes; a head whose list overflowed has all its
+    // rows evaluated instead.
+    int nl[4];
+    bool over[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const bool hv = h0 + 4 * g + i < a.H;
+        over[i] = hv && N > pbeg && ((uint32_t)(__ballot((ovf >> i) & 1u) >> (16 * g)) & 0xFFFFu) != 0;
+        nl[i] = (!hv || over[i] || N <= pbeg) ? 0 : (int)((ncand >> (8 * i)) & 0xFFu);
+    }
+    double best[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    int64_t arg[4] = {-1, -1, -1, -1};
+    auto offer = [&](int i, double v, int64_t u) __attribute__((always_inline)) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            if (k == i && ahead(v, u, best[k], arg[k])) {
+                best[k] = v;
+                arg[k] = u;
+            }
+    };
+    auto head_ptrs = [&](int i, const uint16_t*& ql, const uint16_t*& qr) __attribute__((always_inline)) {
+        const int h = min(h0 + 4 * g + i, a.H - 1);
+        const int64_t hb = (int64_t)b * a.H + h;
+        ql = a.q_lat + hb * D_LAT;
+        qr = a.q_rope + hb * D_ROPE;
+    };
+    const int total = nl[0] + nl[1] + nl[2] + nl[3];
+    for (int j = c; j < total; j += 16) {
+        const int i = j < nl[0] ? 0 : (j < nl[0] + nl[1] ? 1 : (j < nl[0] + nl[1] + nl[2] ? 2 : 3));
+        const int q = j - (i > 0 ? nl[0] : 0) - (i > 1 ? nl[1] : 0) - (i > 2 ? nl[2] : 0);
+        const float Mi = i == 0 ? M[0] : (i == 1 ? M[1] : (i == 2 ? M[2] : M[3]));
+        const int hl = 4 * g + i;
+        if (s_ub[wave][hl][q] >= Mi) {
+            const int64_t u = s_row[wave][hl][q];
+            const uint16_t *ql, *qr;
+            head_ptrs(i, ql, qr);
+            offer(i, full_score64(ql, qr, cb + u * a.cs), u);
+        }
+    }
 #pragma unroll 1
     for (int i = 0; i < 4; ++i) {
-        const float Mi = i == 0 ? M[0] : (i == 1 ? M[1] : (i == 2 ? M[2] : M[3]));
-        const int hl = 4 * g + i, h = h0 + hl;
-        const bool hv = h < a.H;
-        const int64_t hb = (int64_t)b * a.H + (hv ? h : 0);
-        const uint16_t* ql = a.q_lat + hb * D_LAT;
-        const uint16_t* qr = a.q_rope + hb * D_ROPE;
-        double best = -INFINITY;
-        int64_t arg = -1;
-        if (hv && N > pbeg) {
-            if (!s_over[hl]) {
-                const int cnt = s_cnt[hl];
-                for (int q = c; q < cnt; q += 16) {
-                    if (!(s_ub[hl][q] >= Mi)) continue;
-                    const int64_t u = s_row[hl][q];
-                    const double v = full_score64(ql, qr, cb + u * a.cs);
-                    if (ahead(v, u, best, arg)) {
-                        best = v;
-                        arg = u;
-                    }
-                }
-            } else {
-                for (int64_t p = pbeg + c; p < N; p += 16) {
-                    const int64_t u = row_of(p);
-                    const double v = full_score64(ql, qr, cb + u * a.cs);
-                    if (ahead(v, u, best, arg)) {
-                        best = v;
-                        arg = u;
-                    }
-                }
-            }
+        if (!over[i]) continue;
+        const uint16_t *ql, *qr;
+        head_ptrs(i, ql, qr);
+        for (int64_t p = pbeg + c; p < N; p += 16) {
+            const int64_t u = row_of(p);
+            offer(i, full_score64(ql, qr, cb + u * a.cs), u);
         }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int h = h0 + 4 * g + i;
+        double bv = best[i];
+        int64_t ba = arg[i];
         // (max, lowest row) over the 16 lanes of the group
 #pragma unroll
         for (int o = 1; o < 16; o <<= 1) {
-            const double ob = __shfl_xor(best, o);
-            const int64_t oa = (int64_t)__shfl_xor((long long)arg, o);
-            if (ahead(ob, oa, best, arg) && oa >= 0) {
-                best = ob;
-                arg = oa;
+            const double ob = __shfl_xor(bv, o);
+            const int64_t oa = (int64_t)__shfl_xor((long long)ba, o);
+            if (oa >= 0 && ahead(ob, oa, bv, ba)) {
+                bv = ob;
+                ba = oa;
             }
         }
-        if (c == 0 && hv) {
+        if (c == 0 && h < a.H) {
+            const int64_t hb = (int64_t)b * a.H + h;
             if (a.nsplit > 1) {
-                a.part_v[hb * a.nsplit + sp] = best;
-                a.part_u[hb * a.nsplit + sp] = (int32_t)arg;
+                a.part_v[hb * a.nsplit + sp] = bv;
+                a.part_u[hb * a.nsplit + sp] = (int32_t)ba;
             } else {
-                a.smax[hb] = best;
-                a.argmax[hb] = (int32_t)arg;
+                a.smax[hb] = bv;
+                a.argmax[hb] = (int32_t)ba;
             }
         }
     }
@@ -326,8 +410,9 @@ __global__ __launch_bounds__(64) void row_merge_kernel(RowMaxArgs a) {
 }
 
 hipError_t launch_row_max(const RowMaxArgs& a, hipStream_t s) {
-    const unsigned nblk = (unsigned)(((a.H + 15) / 16) * a.B * a.nsplit);
-    hipLaunchKernelGGL(row_max_kernel, dim3(nblk), dim3(64), 0, s, a);
+    const int HG = (a.H + 15) / 16;
+    const unsigned nblk = (unsigned)((HG + RM_WAVES - 1) / RM_WAVES * a.B * a.nsplit);
+    hipLaunchKernelGGL(row_max_kernel, dim3(nblk), dim3(RM_THREADS), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.nsplit <= 1) return e;
     const int64_t n = (int64_t)a.B * a.H;

@@ -98,16 +98,34 @@ static int check_step(vkv_ctx* ctx, const vkv_step* st) {
 
 // ----------------------------------------------------- workspace layout
 
-static void attend_split(const vkv_step* st, int64_t k, int64_t cap, int64_t* splits, int64_t* rps) {
-    const int64_t nmax = k + st->W + cap;
+// Attention splits: the k + W rows every step attends are cut into
+// base_splits splits of rps rows, about one workgroup per CU over the batch;
+// the admitted rows' capacity (cap, a worst case that is mostly unused) gets
+// splits of its own, with the same capacity spread over as many workgroups
+// but at least rps rows each and at most ATT_MAX_SPLIT_ROWS.  Splits past a
+// sequence's actual row count do no work, and the combine reads only the
+// splits that hold rows, so a large cap costs workspace, not time.
+static void attend_split(const vkv_step* st, int64_t k, int64_t cap, int64_t* splits, int64_t* rps,
+                         int64_t* base_splits, int64_t* rps_adm) {
+    const int64_t nfix = k + st->W;
     const int64_t groups = st->B * ((st->H + ATT_HEADS - 1) / ATT_HEADS);
-    int64_t want = std::max<int64_t>(1, (256 + groups - 1) / groups);      // ~1 workgroup per CU
-    int64_t rows = (nmax + want - 1) / want;
-    rows = std::max<int64_t>(rows, 128);
-    rows = std::min<int64_t>(rows, ATT_MAX_SPLIT_ROWS);
-    rows = (rows + ATT_CHUNK - 1) / ATT_CHUNK * ATT_CHUNK;
+    const int64_t want = std::max<int64_t>(1, (256 + groups - 1) / groups);      // ~1 workgroup per CU
+    auto rows_for = [&](int64_t n, int64_t lo, int64_t parts) {
+        int64_t rows = (n + parts - 1) / parts;
+        rows = std::max<int64_t>(rows, lo);
+        rows = std::min<int64_t>(rows, ATT_MAX_SPLIT_ROWS);
+        return (rows + ATT_CHUNK - 1) / ATT_CHUNK * ATT_CHUNK;
+    };
+    // with admitted rows, one of the ~1-per-CU workgroups is left for them, so
+    // that a few admitted rows do not start a second round of workgroups
+    const int64_t rows = rows_for(nfix, 128, cap > 0 ? std::max<int64_t>(1, want - 1) : want);
+    const int64_t nb = std::max<int64_t>(1, (nfix + rows - 1) / rows);
+    const int64_t rest = std::max<int64_t>(0, nfix + cap - nb * rows);   // positions past the base splits
+    const int64_t ra = rows_for(cap, rows, want);
     *rps = rows;
-    *splits = std::max<int64_t>(1, (nmax + rows - 1) / rows);
+    *base_splits = nb;
+    *rps_adm = ra;
+    *splits = nb + (rest + ra - 1) / ra;
 }
 
 static int64_t flag_stride(int64_t A) { return (std::max<int64_t>(A, 1) + 63) / 64 * 64; }
@@ -135,7 +153,7 @@ static WsLayout layout(const vkv_step* st, int64_t k, int64_t cap) {
     L.ambkey = o; o = up256(o + (size_t)(B * Aw * 8));
     L.rmx = o; o = up256(o + (size_t)(B * H * RM_MAX_SPLIT * 12));
     // everything above is independent of k and cap; the attention partials last
-    attend_split(st, k, cap, &L.splits, &L.rows_per_split);
+    attend_split(st, k, cap, &L.splits, &L.rows_per_split, &L.base_splits, &L.rows_per_adm);
     const int64_t HG = (H + ATT_HEADS - 1) / ATT_HEADS;   // partials padded to whole head groups
     L.part_o = o; o = up256(o + (size_t)(B * L.splits * HG * ATT_HEADS * D_LAT * 2));
     L.part_ml = o; o = up256(o + (size_t)(B * L.splits * H * 2 * 4));
@@ -267,7 +285,9 @@ static AttendArgs attend_args(const vkv_step* st, const WsLayout& L, char* w, Ch
     a.A = L.A;
     a.cap = cap;
     a.rows_per_split = L.rows_per_split;
+    a.rows_per_adm = L.rows_per_adm;
     a.splits = (int)L.splits;
+    a.base_splits = (int)L.base_splits;
     a.B = (int)c.nb;
     a.H = (int)st->H;
     a.scale_log2 = scale * 1.4426950408889634f;
@@ -678,12 +698,13 @@ int vkv_step_run(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, in
 static hipError_t run_row_max(const vkv_step* st, const int32_t* rows, int64_t nrows, int all_archive, int add_recent,
                               double* smax, int32_t* argmax, hipStream_t s, char* ws = nullptr) {
     RowMaxArgs a{};
-    // with a workspace: row ranges in parallel, about 2048 waves in all, at least 64 rows each
+    // with a workspace: row ranges in parallel, about one workgroup per CU in
+    // all (a workgroup holds 8 head groups of 16), at least 64 rows each
     a.nsplit = 1;
     if (ws) {
         const int64_t N = (all_archive ? st->T - st->W : nrows) + (add_recent ? st->W : 0);
-        const int64_t waves = ((st->H + 15) / 16) * st->B;
-        int64_t ns = std::max<int64_t>(1, 2048 / std::max<int64_t>(waves, 1));
+        const int64_t blocks = ((st->H + 127) / 128) * st->B;
+        int64_t ns = std::max<int64_t>(1, (256 + blocks - 1) / std::max<int64_t>(blocks, 1));
         ns = std::min<int64_t>({ns, (int64_t)RM_MAX_SPLIT, std::max<int64_t>(1, N / 64)});
         a.nsplit = (int)ns;
         const WsLayout L = layout(st, 0, 0);
