@@ -170,8 +170,8 @@ int vkv_sketch_basis(vkv_ctx* ctx, const uint16_t* q, int64_t m, int32_t r, int3
  * The query-independent tier-1 selector (Sec. 4.1, the sigma equation; the
  * block close of the deployment specification's request lifecycle).  Rows are
  * closed in fixed blocks of VKV_SIGMA_BLOCK rows; for every closed block and
- * each of the 64 channels of the un-rotated branch r_u (elements 512..575 of
- * each cache row) the sequence-axis DFT keeps bins [0, kappa) and their
+ * each of the 64 channels of the branch r_u as the cache row stores it
+ * (elements 512..575) the sequence-axis DFT keeps bins [0, kappa) and their
  * mirrors, the rest is zeroed and the transform inverted; sigma_u is the norm
  * over the channels of what this low-pass reconstruction misses at row u.
  *

@@ -485,8 +485,8 @@ SIGMA_SINKS = 4       # the first rows of the context, always attended
 def lowpass_residual_norm(branch: np.ndarray, kappa: int) -> np.ndarray:
     """sigma_u over one closed block (Sec. 4.1, the sigma equation).
 
-    branch [N, 64]: the 64-dim un-rotated branch r_u of the block's rows (bf16
-    bits).  Along the sequence axis, per channel: the real DFT, bins
+    branch [N, 64]: the 64-dim branch r_u of the block's rows as the cache
+    stores it (the trailing 64 dims of each row; bf16 bits).  Along the sequence axis, per channel: the real DFT, bins
     f in [0, kappa) kept and the rest zeroed, the inverse real DFT; sigma_u is
     the norm over the channels of what that low-pass reconstruction misses at
     row u.  Written as the DFT sums (fp64, the twiddle angle reduced mod N):

@@ -145,26 +145,18 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
     __shared__ __align__(16) uint8_t s_k[ATT_STAGES * TILE_BYTES];   // the ring of tile stages
     __shared__ int32_t s_rows[ATT_MAX_SPLIT_ROWS];                    // the split's rows
 
-    const int sp = blockIdx.x, hg = blockIdx.y, b = blockIdx.z;
+    const int hg = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x;
     const int lane = tid & 63, g = lane >> 4, c = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t N = attended_count(a, b);
-    int64_t p0, p1;
-    split_range(a, sp, N, p0, p1);
     const int HG = (a.H + ATT_HEADS - 1) / ATT_HEADS;
+
+    // one split: list positions [p0, p1), p0 < p1 (splits without rows are
+    // never run: the combine reads only the splits that hold rows)
+    auto run_split = [&](const int sp, const int64_t p0, const int64_t p1) __attribute__((always_inline)) {
     uint16_t* po = a.part_o + (((int64_t)b * a.splits + sp) * HG + hg) * (ATT_HEADS * D_LAT);
     float* pml = a.part_ml + ((int64_t)b * a.splits + sp) * a.H * 2;
-    if (p0 >= p1) {
-        if (tid < ATT_HEADS) {
-            const int h = hg * ATT_HEADS + tid;
-            if (h < a.H) {
-                pml[2 * h] = -INFINITY;
-                pml[2 * h + 1] = 0.f;
-            }
-        }
-        return;
-    }
     const int ntile = (int)((p1 - p0 + ATT_CHUNK - 1) / ATT_CHUNK);
     const int h0 = hg * ATT_HEADS + wave * 16;
     const int hq = h0 + c;
@@ -389,6 +381,22 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
         pml[2 * hq] = m_run;
         pml[2 * hq + 1] = l_run;
     }
+    };
+
+    // A base split's workgroup runs that split.  The admitted rows' splits:
+    // workgroup base_splits + j takes splits base_splits + j, + adm_blocks, ...
+    // until one holds no rows (they fill in order), so a mostly unused
+    // capacity costs a few idle workgroups and a full one is shared by all of
+    // them.  (One loop, so the split's code is generated once.)
+    const int stride = (int)blockIdx.x < a.base_splits ? 0 : a.adm_blocks;
+    for (int sp = blockIdx.x; sp < a.splits; sp += stride) {
+        int64_t p0, p1;
+        split_range(a, sp, N, p0, p1);
+        if (p0 >= p1) break;
+        run_split(sp, p0, p1);
+        if (stride == 0) break;
+        __syncthreads();   // the row list and the ring are free before the next split refills them
+    }
 }
 
 // Merge the splits of four heads by log-sum-exp (partials bf16, sums fp32);
@@ -497,7 +505,7 @@ __global__ __launch_bounds__(128) void attend_combine_kernel(AttendArgs a) {
 }
 
 hipError_t launch_attend(const AttendArgs& a, hipStream_t s) {
-    dim3 grid((unsigned)a.splits, (unsigned)((a.H + ATT_HEADS - 1) / ATT_HEADS), (unsigned)a.B);
+    dim3 grid((unsigned)(a.base_splits + a.adm_blocks), (unsigned)((a.H + ATT_HEADS - 1) / ATT_HEADS), (unsigned)a.B);
     hipLaunchKernelGGL(attend_kernel, grid, dim3(ATT_THREADS), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

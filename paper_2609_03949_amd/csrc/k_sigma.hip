@@ -1,8 +1,8 @@
 // k_sigma.hip -- the query-independent tier-1 selector sigma_u (Sec. 4.1, the
 // sigma equation; App. H, block close) and the tier it keeps.
 //
-// Per closed block of 4096 rows and per channel of the 64-dim un-rotated
-// branch r_u (the last 64 elements of each cache row), sigma keeps the
+// Per closed block of 4096 rows and per channel of the 64-dim branch r_u as
+// the cache row stores it (its last 64 elements), sigma keeps the
 // frequency bins [0, kappa) of the sequence-axis DFT (and their mirrors),
 // inverts, and takes the norm over the channels of what that low-pass
 // reconstruction misses at each row.

@@ -99,14 +99,16 @@ static int check_step(vkv_ctx* ctx, const vkv_step* st) {
 // ----------------------------------------------------- workspace layout
 
 // Attention splits: the k + W rows every step attends are cut into
-// base_splits splits of rps rows, about one workgroup per CU over the batch;
-// the admitted rows' capacity (cap, a worst case that is mostly unused) gets
-// splits of its own, with the same capacity spread over as many workgroups
-// but at least rps rows each and at most ATT_MAX_SPLIT_ROWS.  Splits past a
-// sequence's actual row count do no work, and the combine reads only the
-// splits that hold rows, so a large cap costs workspace, not time.
+// base_splits splits of rps rows, about one workgroup per CU over the batch
+// (one fewer per sequence when rows may be admitted); the admitted rows'
+// capacity (cap, a worst case that is mostly unused) gets splits of its own,
+// the capacity spread over as many splits as there are workgroups per
+// sequence but at least rps rows each and at most ATT_MAX_SPLIT_ROWS, taken
+// in turn by a bounded number of workgroups.  Splits past a sequence's actual
+// row count do no work and the combine reads only the splits that hold rows,
+// so a large cap costs workspace, not time.
 static void attend_split(const vkv_step* st, int64_t k, int64_t cap, int64_t* splits, int64_t* rps,
-                         int64_t* base_splits, int64_t* rps_adm) {
+                         int64_t* base_splits, int64_t* rps_adm, int64_t* adm_blocks) {
     const int64_t nfix = k + st->W;
     const int64_t groups = st->B * ((st->H + ATT_HEADS - 1) / ATT_HEADS);
     const int64_t want = std::max<int64_t>(1, (256 + groups - 1) / groups);      // ~1 workgroup per CU
@@ -122,10 +124,17 @@ static void attend_split(const vkv_step* st, int64_t k, int64_t cap, int64_t* sp
     const int64_t nb = std::max<int64_t>(1, (nfix + rows - 1) / rows);
     const int64_t rest = std::max<int64_t>(0, nfix + cap - nb * rows);   // positions past the base splits
     const int64_t ra = rows_for(cap, rows, want);
+    const int64_t nadm = (rest + ra - 1) / ra;
     *rps = rows;
     *base_splits = nb;
     *rps_adm = ra;
-    *splits = nb + (rest + ra - 1) / ra;
+    *splits = nb + nadm;
+    // the admitted splits are taken in turn by up to 4 want workgroups: one
+    // split each up to a capacity of about 4 splits per workgroup of the
+    // batch (a full admission then runs as independent workgroups; measured:
+    // taking two splits per workgroup made the near-total admission of the
+    // 16-sequence, 32768-row workload 34% slower), beyond it a few splits each
+    *adm_blocks = std::min<int64_t>(nadm, 4 * want);
 }
 
 static int64_t flag_stride(int64_t A) { return (std::max<int64_t>(A, 1) + 63) / 64 * 64; }
@@ -153,7 +162,7 @@ static WsLayout layout(const vkv_step* st, int64_t k, int64_t cap) {
     L.ambkey = o; o = up256(o + (size_t)(B * Aw * 8));
     L.rmx = o; o = up256(o + (size_t)(B * H * RM_MAX_SPLIT * 12));
     // everything above is independent of k and cap; the attention partials last
-    attend_split(st, k, cap, &L.splits, &L.rows_per_split, &L.base_splits, &L.rows_per_adm);
+    attend_split(st, k, cap, &L.splits, &L.rows_per_split, &L.base_splits, &L.rows_per_adm, &L.adm_blocks);
     const int64_t HG = (H + ATT_HEADS - 1) / ATT_HEADS;   // partials padded to whole head groups
     L.part_o = o; o = up256(o + (size_t)(B * L.splits * HG * ATT_HEADS * D_LAT * 2));
     L.part_ml = o; o = up256(o + (size_t)(B * L.splits * H * 2 * 4));
@@ -288,6 +297,7 @@ static AttendArgs attend_args(const vkv_step* st, const WsLayout& L, char* w, Ch
     a.rows_per_adm = L.rows_per_adm;
     a.splits = (int)L.splits;
     a.base_splits = (int)L.base_splits;
+    a.adm_blocks = (int)L.adm_blocks;
     a.B = (int)c.nb;
     a.H = (int)st->H;
     a.scale_log2 = scale * 1.4426950408889634f;

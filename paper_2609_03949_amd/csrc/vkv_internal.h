@@ -157,7 +157,7 @@ constexpr int ATT_MAX_SPLIT_ROWS = 1024;   // rows of one split (row list held i
 
 struct WsLayout {
     size_t qt, hsc, seq, kt, flags, flags2, blk, cand, candkey, amb, ambkey, rmx, part_o, part_ml, total;
-    int64_t A, n, nblk, splits, rows_per_split, base_splits, rows_per_adm, cap;
+    int64_t A, n, nblk, splits, rows_per_split, base_splits, rows_per_adm, adm_blocks, cap;
 };
 
 // ------------------------------------------------------ kernel interfaces
@@ -282,6 +282,7 @@ struct AttendArgs {
     int64_t rows_per_split;   // rows of each of the first base_splits splits (kept rows and window)
     int64_t rows_per_adm;     // rows of each later split (the admitted rows' capacity)
     int splits, base_splits;
+    int adm_blocks;           // workgroups that take the admitted splits in turn
     int B, H;
     float scale_log2;      // scale * log2(e)
     uint16_t* part_o;      // bf16 [B, splits, head groups, 8 waves, 32, 64 lanes, 4] (register order)
