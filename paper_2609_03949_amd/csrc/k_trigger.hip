@@ -6,12 +6,14 @@
 // Eq. (setup); the fp64 sum over the 576 dims, latent then branch, from +0)
 // and the row attaining it (ties: the lower row index).  Over the tier-1
 // rows it is the trigger threshold s*_h; over the whole context it is the
-// causal argmax row of a calibration query.  One wave per (sequence, 16
-// heads) streams the list: bf16 MFMA scores in fp32 with a per-(row, head)
-// certified band e = 2 (n + n/32) 2^-23 ||q_h|| ||x_u|| (n = 576, the
-// scan's error model), a running certified lower bound M_h of the maximum,
-// and in LDS the rows whose upper bound reaches M_h.  Only those get the
-// fp64 chain; the true maximum row always does.
+// causal argmax row of a calibration query.  A workgroup of 8 waves (16
+// heads each) streams one range of the list through an LDS tile ring that all
+// its waves read: bf16 MFMA scores in fp32 with a per-(row, head) certified
+// band e = 2 (n + n/32) 2^-23 ||q_h|| ||x_u|| (n = 576, the scan's error
+// model), a running certified lower bound M_h of the maximum, and in LDS the
+// rows whose upper bound reaches M_h.  Only those get the fp64 chain; the
+// true maximum row always does.  The ranges' maxima are merged by
+// row_merge_kernel.
 //
 // inflation_kernel: for each (calibration query, head), whether the causal
 // argmax row is archived and outside the tier-1 set (a hard query), and then
