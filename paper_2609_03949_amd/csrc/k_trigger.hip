@@ -40,11 +40,12 @@ __device__ __forceinline__ float sumsq8(bf16x8_t v) {
 
 // exact fp64 full score of row `row` for the head whose query rows are ql / qr
 // (the products of two bf16 values are exact in fp64; they are added in
-// dimension order from +0).  Pieces of 32 dims are loaded one piece ahead of
-// the chain, so the memory round trips overlap the arithmetic.
+// dimension order from +0).  Pieces of 32 dims are loaded two pieces ahead of
+// the chain (a ring of three), so the memory round trips overlap the
+// arithmetic.
 __device__ __forceinline__ double full_score64(const uint16_t* ql, const uint16_t* qr, const uint16_t* row) {
     constexpr int NP = D_ROW / 32;   // 18 pieces of 4 x 8 dims
-    u16x8_t qv[2][4], xv[2][4];
+    u16x8_t qv[3][4], xv[3][4];
     auto load = [&](int p, int buf) __attribute__((always_inline)) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -61,18 +62,33 @@ __device__ __forceinline__ double full_score64(const uint16_t* ql, const uint16_
             for (int e = 0; e < 8; ++e)
                 acc = fma((double)bf16_to_f32(qv[buf][j][e]), (double)bf16_to_f32(xv[buf][j][e]), acc);
     };
-    static_assert(NP % 2 == 0, "pieces taken in pairs");
+    static_assert(NP % 3 == 0, "pieces taken in threes");
     load(0, 0);
+    load(1, 1);
     // a loop, not unrolled: a fully unrolled chain lets the compiler issue all
     // loads first and spill them
 #pragma unroll 1
-    for (int p = 0; p < NP; p += 2) {
-        load(p + 1, 1);
+    for (int p = 0; p < NP; p += 3) {
+        load(p + 2, 2);
         chain(0);
-        if (p + 2 < NP) load(p + 2, 0);
+        if (p + 3 < NP) load(p + 3, 0);
         chain(1);
+        if (p + 4 < NP) load(p + 4, 1);
+        chain(2);
     }
     return acc;
+}
+
+// sum over the 16 lanes of each row of the wave (DPP lane permutations)
+__device__ __forceinline__ float rowsum16(float v) {
+    auto perm = [](float x, auto ctrl) __attribute__((always_inline)) {
+        return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), decltype(ctrl)::value, 0xF, 0xF, true));
+    };
+    v += perm(v, std::integral_constant<int, 0xB1>{});    // quad_perm [1,0,3,2]
+    v += perm(v, std::integral_constant<int, 0x4E>{});    // quad_perm [2,3,0,1]
+    v += perm(v, std::integral_constant<int, 0x141>{});   // row_half_mirror
+    v += perm(v, std::integral_constant<int, 0x140>{});   // row_mirror
+    return v;
 }
 
 // max over the 16 lanes of each row of the wave (DPP lane permutations)
@@ -107,12 +123,14 @@ constexpr int RM_WAVES = 8;
 constexpr int VMCNT0 = 0x0F70;   // s_waitcnt operand: vmcnt 0, expcnt and lgkmcnt left alone
 constexpr int RM_THREADS = 64 * RM_WAVES;
 constexpr int RM_TILE = 32;                                   // rows per tile
-constexpr int RM_PIECES = RM_TILE * (D_ROW / 8);              // 16-byte pieces per tile
-constexpr int RM_PER = (RM_PIECES + RM_THREADS - 1) / RM_THREADS;   // pieces per thread
+constexpr int RM_WROWS = RM_TILE / RM_WAVES;                  // tile rows each wave loads (4)
+constexpr int RM_WPIECES = RM_WROWS * (D_ROW / 8);            // their 16-byte pieces (288)
+constexpr int RM_PER = (RM_WPIECES + 63) / 64;                // pieces per lane (5)
 
 __global__ __launch_bounds__(RM_THREADS) void row_max_kernel(RowMaxArgs a) {
     __shared__ __align__(16) uint8_t s_x[2][RM_TILE * 2 * D_ROW];
     __shared__ int32_t s_id[2][RM_TILE];
+    __shared__ float s_xn[2][RM_TILE];   // ||x_u||^2 of the stage's rows (fp32)
     __shared__ int32_t s_row[RM_WAVES][16][RM_CAND];
     __shared__ float s_ub[RM_WAVES][16][RM_CAND];
     const int HG = (a.H + 15) / 16;
@@ -160,15 +178,17 @@ __global__ __launch_bounds__(RM_THREADS) void row_max_kernel(RowMaxArgs a) {
     // (set in the lane that had it); packed to spare registers in the loop
     uint32_t ncand = 0, ovf = 0;
 
-    // loader: thread tid moves pieces q = tid + RM_THREADS i of a tile, piece
-    // q mod 72 of tile row q / 72 (rows past the range repeat its last row;
-    // they are loaded, never scored)
+    // loader: wave w moves tile rows 4 w .. 4 w + 3; its lane l takes pieces
+    // q = l + 64 i (q < 288) of them, piece q mod 72 of row 4 w + q / 72 (rows
+    // past the range repeat its last row; they are loaded, never scored).  A
+    // row's pieces stay in one wave, so the wave also sums the row's squares
+    // once for all 8 waves (the per-(row, head) band needs ||x_u||).
     auto load_ids = [&](int64_t t0, int32_t (&id)[RM_PER]) {
 #pragma unroll
         for (int i = 0; i < RM_PER; ++i) {
-            const int q = tid + RM_THREADS * i;
-            if (q < RM_PIECES) {
-                const int64_t p = min(t0 + q / (D_ROW / 8), N - 1);
+            const int q = lane + 64 * i;
+            if (q < RM_WPIECES) {
+                const int64_t p = min(t0 + RM_WROWS * wave + q / (D_ROW / 8), N - 1);
                 int32_t v = (int32_t)(p < n1 ? p : a.A + (p - n1));
                 if (!a.all_archive && p < n1) v = a.rows[(int64_t)b * a.nrows + p];
                 id[i] = v;
@@ -179,22 +199,37 @@ __global__ __launch_bounds__(RM_THREADS) void row_max_kernel(RowMaxArgs a) {
     auto load_pieces = [&](const int32_t (&id)[RM_PER]) {
 #pragma unroll
         for (int i = 0; i < RM_PER; ++i) {
-            const int q = tid + RM_THREADS * i;
-            if (q < RM_PIECES) {
+            const int q = lane + 64 * i;
+            if (q < RM_WPIECES) {
                 const int s = q % (D_ROW / 8);
                 xr[i] = *reinterpret_cast<const u32x4_t*>(cb + (int64_t)id[i] * a.cs + 8 * s);
             }
         }
     };
     auto store_pieces = [&](int st, const int32_t (&id)[RM_PER]) {
+        float ns[RM_WROWS] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int i = 0; i < RM_PER; ++i) {
-            const int q = tid + RM_THREADS * i;
-            if (q < RM_PIECES) {
-                const int r = q / (D_ROW / 8), s = q - (D_ROW / 8) * r;
+            const int q = lane + 64 * i;
+            if (q < RM_WPIECES) {
+                const int j = q / (D_ROW / 8), s = q - (D_ROW / 8) * j;
+                const int r = RM_WROWS * wave + j;
                 *reinterpret_cast<u32x4_t*>(s_x[st] + r * (2 * D_ROW) + 16 * (s ^ (r & 7))) = xr[i];
                 if (s == 0) s_id[st][r] = id[i];
+                bf16x8_t v;
+                __builtin_memcpy(&v, &xr[i], 16);
+                const float ss = sumsq8(v);
+#pragma unroll
+                for (int jj = 0; jj < RM_WROWS; ++jj) ns[jj] += (j == jj) ? ss : 0.f;
             }
+        }
+        // each row's sum over the 64 lanes (16-lane rows by DPP, then across rows)
+#pragma unroll
+        for (int jj = 0; jj < RM_WROWS; ++jj) {
+            float v = rowsum16(ns[jj]);
+            v += __shfl_xor(v, 16);
+            v += __shfl_xor(v, 32);
+            if (lane == 0) s_xn[st][RM_WROWS * wave + jj] = v;
         }
     };
 
@@ -204,15 +239,14 @@ __global__ __launch_bounds__(RM_THREADS) void row_max_kernel(RowMaxArgs a) {
         const bool valid = p0 + c < N;
         const uint8_t* xrow = s_x[st] + rl * (2 * D_ROW);
         f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        float xs = 0.f;
 #pragma unroll
         for (int ks = 0; ks < RM_KS; ++ks) {
             const bf16x8_t xv = *reinterpret_cast<const bf16x8_t*>(xrow + 16 * ((4 * ks + g) ^ (c & 7)));
             acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[ks], xv, acc, 0, 0, 0);
-            xs += sumsq8(xv);
         }
-        xs += __shfl_xor(xs, 16);
-        xs += __shfl_xor(xs, 32);
+        // ||x||^2 summed by the loading wave (fp32 sums of the 576 exact
+        // squares in any order are within 576 * 2^-24 relative)
+        const float xs = s_xn[st][rl];
         const float xub = sqrtf(xs * (1.0f + 0x1p-12f)) * (1.0f + 0x1p-20f);
         const int32_t uc = s_id[st][rl];
         float hi[4];
@@ -342,18 +376,37 @@ __global__ __launch_bounds__(RM_THREADS) void row_max_kernel(RowMaxArgs a) {
         ql = a.q_lat + hb * D_LAT;
         qr = a.q_rope + hb * D_ROPE;
     };
+    // the pairs whose bound reaches the final M_h, compacted per lane group
+    // (into the tile ring, free now), so that the fp64 chains fill the lanes:
+    // most entries of the lists fall below the final bound
+    int16_t* s_pairs = reinterpret_cast<int16_t*>(&s_x[0][0]) + (wave * 4 + g) * (4 * RM_CAND);
     const int total = nl[0] + nl[1] + nl[2] + nl[3];
-    for (int j = c; j < total; j += 16) {
-        const int i = j < nl[0] ? 0 : (j < nl[0] + nl[1] ? 1 : (j < nl[0] + nl[1] + nl[2] ? 2 : 3));
-        const int q = j - (i > 0 ? nl[0] : 0) - (i > 1 ? nl[1] : 0) - (i > 2 ? nl[2] : 0);
-        const float Mi = i == 0 ? M[0] : (i == 1 ? M[1] : (i == 2 ? M[2] : M[3]));
-        const int hl = 4 * g + i;
-        if (s_ub[wave][hl][q] >= Mi) {
-            const int64_t u = s_row[wave][hl][q];
-            const uint16_t *ql, *qr;
-            head_ptrs(i, ql, qr);
-            offer(i, full_score64(ql, qr, cb + u * a.cs), u);
+    int totmax = max(total, __shfl_xor(total, 16));
+    totmax = max(totmax, __shfl_xor(totmax, 32));
+    int npass = 0;   // the same in the group's 16 lanes
+    for (int j0 = 0; j0 < totmax; j0 += 16) {
+        const int j = j0 + c;
+        bool pass = false;
+        int code = 0;
+        if (j < total) {
+            const int i = j < nl[0] ? 0 : (j < nl[0] + nl[1] ? 1 : (j < nl[0] + nl[1] + nl[2] ? 2 : 3));
+            const int q = j - (i > 0 ? nl[0] : 0) - (i > 1 ? nl[1] : 0) - (i > 2 ? nl[2] : 0);
+            const float Mi = i == 0 ? M[0] : (i == 1 ? M[1] : (i == 2 ? M[2] : M[3]));
+            pass = s_ub[wave][4 * g + i][q] >= Mi;
+            code = RM_CAND * i + q;
         }
+        const uint32_t gm = (uint32_t)(__ballot(pass) >> (16 * g)) & 0xFFFFu;
+        if (pass) s_pairs[npass + __popc(gm & ((1u << c) - 1u))] = (int16_t)code;
+        npass += __popc(gm);
+    }
+    __builtin_amdgcn_wave_barrier();
+    for (int j = c; j < npass; j += 16) {
+        const int code = s_pairs[j];
+        const int i = code / RM_CAND, q = code - RM_CAND * i;
+        const int64_t u = s_row[wave][4 * g + i][q];
+        const uint16_t *ql, *qr;
+        head_ptrs(i, ql, qr);
+        offer(i, full_score64(ql, qr, cb + u * a.cs), u);
     }
 #pragma unroll 1
     for (int i = 0; i < 4; ++i) {
