@@ -64,11 +64,13 @@ __device__ __forceinline__ void split_range(const AttendArgs& a, int sp, int64_t
     p1 = max(p1, p0);
 }
 
-// the number of splits that hold rows of a list of N rows
+// the number of splits that hold rows of a list of N rows (32-bit: lists,
+// splits and their rows are far below 2^31)
 __device__ __forceinline__ int live_splits(const AttendArgs& a, int64_t N) {
-    const int64_t base_end = (int64_t)a.base_splits * a.rows_per_split;
-    if (N <= base_end) return (int)((N + a.rows_per_split - 1) / a.rows_per_split);
-    return a.base_splits + (int)((N - base_end + a.rows_per_adm - 1) / a.rows_per_adm);
+    const int n = (int)N, rps = (int)a.rows_per_split, rpa = (int)a.rows_per_adm;
+    const int base_end = a.base_splits * rps;
+    if (n <= base_end) return (n + rps - 1) / rps;
+    return a.base_splits + (n - base_end + rpa - 1) / rpa;
 }
 
 __device__ __forceinline__ int32_t attended_row(const AttendArgs& a, int b, int64_t p) {
@@ -420,7 +422,7 @@ __global__ __launch_bounds__(128) void attend_combine_kernel(AttendArgs a) {
     float acc[4][4] = {};
 #pragma unroll
     for (int i = 0; i < 4; ++i) M[i] = -INFINITY;
-    // only the splits that hold rows are read (at most all of them)
+    // only the splits that hold rows are read (none for an empty list)
     const int nlive = min(a.splits, live_splits(a, attended_count(a, b)));
     for (int s0 = 0; s0 < nlive; s0 += COMB_SPLITS) {
         float ms[COMB_SPLITS][4], ls[COMB_SPLITS][4];
@@ -436,20 +438,13 @@ __global__ __launch_bounds__(128) void attend_combine_kernel(AttendArgs a) {
                 ms[u][i] = hv ? ml[2 * (hb + i)] : -INFINITY;
                 ls[u][i] = hv ? ml[2 * (hb + i) + 1] : 0.f;
             }
-        }
-#pragma unroll
-        for (int u = 0; u < COMB_SPLITS; ++u) {
-            // splits without rows (the unused capacity of the admitted rows) are not read
-            const int s = s0 + u;
-            const bool rows = ms[u][0] != -INFINITY || ms[u][1] != -INFINITY || ms[u][2] != -INFINITY ||
-                              ms[u][3] != -INFINITY;
-            raw[u][0] = raw[u][1] = u32x4_t{0u, 0u, 0u, 0u};
-            if (rows) {
-                const uint16_t* src = a.part_o + (((int64_t)b * a.splits + s) * HG + hg) * (ATT_HEADS * D_LAT) +
-                                      (int64_t)wave * (D_LAT / 16) * 64 * 4 + (tt * 64 + 16 * g + c0) * 4;
-                raw[u][0] = *reinterpret_cast<const u32x4_t*>(src);       // lanes c0, c0+1
-                raw[u][1] = *reinterpret_cast<const u32x4_t*>(src + 8);   // lanes c0+2, c0+3
-            }
+            // every split below nlive holds rows, so its partial was written;
+            // past it the batch re-reads split s0 (weight 0), so that all loads
+            // go out together, unconditionally (one round trip per batch)
+            const uint16_t* src = a.part_o + (((int64_t)b * a.splits + (live ? s : s0)) * HG + hg) * (ATT_HEADS * D_LAT) +
+                                  (int64_t)wave * (D_LAT / 16) * 64 * 4 + (tt * 64 + 16 * g + c0) * 4;
+            raw[u][0] = *reinterpret_cast<const u32x4_t*>(src);       // lanes c0, c0+1
+            raw[u][1] = *reinterpret_cast<const u32x4_t*>(src + 8);   // lanes c0+2, c0+3
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
