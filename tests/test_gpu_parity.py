@@ -234,6 +234,27 @@ def test_two_tier_partial_admission(ctx, basis, r, H):
     check_step(wl, g, o, [0, 1], two_tier=True)
 
 
+def test_admitted_splits_taken_in_turn(ctx):
+    """Many sequences and a near-total admission: the admitted rows' splits
+    outnumber the workgroups kept for them, so some workgroups take two
+    splits in turn (64 sequences of 16 heads leave 4 workgroups per sequence;
+    a capacity of 19744 rows makes 20 admitted splits of 1024 rows, taken by
+    16 workgroups).  Sampled sequences against the oracle."""
+    say("admitted splits taken in turn by a bounded set of workgroups")
+    cfg = synth.CONFIGS["cfg3"].with_(H=16)
+    wl = synth.make_workload(cfg, "cuda", B=64, T=20000)
+    k = 256
+    g, _ = gpu_step(ctx, wl, k=k, two_tier=True)
+    seqs = [0, 21, 63]
+    adm = g["adm_count"]
+    say(f"  admitted rows per sequence: min {int(adm.min())} max {int(adm.max())} of {wl['A'] - k}")
+    # the base splits cover 576 positions (3 x 192), so more than 16 admitted
+    # splits of 1024 rows hold rows once k + W + admitted - 576 > 16 x 1024
+    assert int(adm.min()) + k + wl["W"] - 576 > 16 * 1024
+    o, _ = oracle_step(wl, seqs, k=k, two_tier=True)
+    check_step(wl, g, o, seqs, two_tier=True)
+
+
 def test_two_tier_capacity_overflow(ctx):
     say("two-tier capacity overflow")
     cfg = synth.CONFIGS["cfg3"].with_(H=8)
