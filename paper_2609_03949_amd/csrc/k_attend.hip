@@ -147,12 +147,33 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
     __shared__ __align__(16) uint8_t s_k[ATT_STAGES * TILE_BYTES];   // the ring of tile stages
     __shared__ int32_t s_rows[ATT_MAX_SPLIT_ROWS];                    // the split's rows
 
-    const int hg = blockIdx.y, b = blockIdx.z;
+    const int HG = (a.H + ATT_HEADS - 1) / ATT_HEADS;
+    // Workgroup ids: first every base split (split, then head group, then
+    // sequence), then the admitted-row workgroups j = 0, 1, ... of every
+    // (head group, sequence).  Workgroups are dispatched in id order, so the
+    // base splits and the first admitted workgroup of each sequence (the only
+    // one with rows when few are admitted) go out before the idle ones.
+    int first, hg, b;
+    {
+        const int64_t L = blockIdx.x;
+        const int64_t nbase = (int64_t)a.B * HG * a.base_splits;
+        if (L < nbase) {
+            first = (int)(L % a.base_splits);
+            const int64_t r = L / a.base_splits;
+            hg = (int)(r % HG);
+            b = (int)(r / HG);
+        } else {
+            const int64_t L2 = L - nbase, per = (int64_t)a.B * HG;
+            first = a.base_splits + (int)(L2 / per);
+            const int64_t r = L2 % per;
+            hg = (int)(r % HG);
+            b = (int)(r / HG);
+        }
+    }
     const int tid = threadIdx.x;
     const int lane = tid & 63, g = lane >> 4, c = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t N = attended_count(a, b);
-    const int HG = (a.H + ATT_HEADS - 1) / ATT_HEADS;
 
     // one split: list positions [p0, p1), p0 < p1 (splits without rows are
     // never run: the combine reads only the splits that hold rows)
@@ -390,8 +411,8 @@ __global__ __launch_bounds__(ATT_THREADS, 1) void attend_kernel(AttendArgs a) {
     // until one holds no rows (they fill in order), so a mostly unused
     // capacity costs a few idle workgroups and a full one is shared by all of
     // them.  (One loop, so the split's code is generated once.)
-    const int stride = (int)blockIdx.x < a.base_splits ? 0 : a.adm_blocks;
-    for (int sp = blockIdx.x; sp < a.splits; sp += stride) {
+    const int stride = first < a.base_splits ? 0 : a.adm_blocks;
+    for (int sp = first; sp < a.splits; sp += stride) {
         int64_t p0, p1;
         split_range(a, sp, N, p0, p1);
         if (p0 >= p1) break;
@@ -500,8 +521,8 @@ __global__ __launch_bounds__(128) void attend_combine_kernel(AttendArgs a) {
 }
 
 hipError_t launch_attend(const AttendArgs& a, hipStream_t s) {
-    dim3 grid((unsigned)(a.base_splits + a.adm_blocks), (unsigned)((a.H + ATT_HEADS - 1) / ATT_HEADS), (unsigned)a.B);
-    hipLaunchKernelGGL(attend_kernel, grid, dim3(ATT_THREADS), 0, s, a);
+    const int64_t nwg = (int64_t)(a.base_splits + a.adm_blocks) * ((a.H + ATT_HEADS - 1) / ATT_HEADS) * a.B;
+    hipLaunchKernelGGL(attend_kernel, dim3((unsigned)nwg), dim3(ATT_THREADS), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const unsigned hgs = (unsigned)((a.H + ATT_HEADS - 1) / ATT_HEADS);
