@@ -209,7 +209,10 @@ int vkv_sigma_select(vkv_ctx* ctx, const double* sigma, int64_t B, int64_t n_clo
  * place of S) -> attention over kept, window and fired rows (as vkv_attend).
  * kept must be ascending and inside [0, A) (VKV_DEBUG_ROWS checks it after
  * the step); the other arguments and results are those of the calls named.
- * ws: vkv_workspace_size(st, k, cap) bytes.
+ * key may be NULL: the step reads only ub (here the trigger margins), and
+ * without a key buffer the scan writes no keys at all (faster: each wave of
+ * the scan then takes twice the rows).  ws: vkv_workspace_size(st, k, cap)
+ * bytes.
  */
 int vkv_step_run_kept(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_bytes, int64_t k,
                       const int32_t* kept, float* key, float* ub, float cert_mult, double* smax,

@@ -533,7 +533,9 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
     uint8_t* wbase = smem + wave * Gm::WAVE;
     uint8_t* rvbase = wbase + NST * STAGE;                                   // [NST][64] row scalars
     float* s_key = reinterpret_cast<float*>(wbase + NST * (STAGE + Gm::RV));   // [64 q + lane]
-    float* s_ub = s_key + 16 * Gm::KT / 2;                                    // (UB) [64 q + lane]
+    // (UB) [64 q + lane]: the second half of the buffer, or all of it without keys
+    const bool keys = !UB || !a.no_keys;
+    float* s_ub = keys ? s_key + 16 * Gm::KT / 2 : s_key;
     // block span [bs0, bs1); this wave's tile j covers rows r0 + 16 TST j + [0, 16)
     if (blockIdx.x == 0 && threadIdx.x < 64) store_head_maxima(a, b, threadIdx.x);
     const int64_t bs0 = (int64_t)blockIdx.x * STREAM_WAVES * 16 * tpw;
@@ -680,7 +682,7 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
             to.kmax = fmaxf(to.kmax, m);
             to.kmin = fminf(to.kmin, m);
         }
-        s_key[64 * q + lane] = m;
+        if (keys) s_key[64 * q + lane] = m;
         if (UB) s_ub[64 * q + lane] = u;
     };
 
@@ -780,9 +782,11 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(ScoreArgs a, int t
     for (int q = 0; q < (ntl + 3) / 4; ++q) {
         const int64_t row = group_row(q);
         if (row < bs1) {
-            const float m = s_key[64 * q + lane];
-            kto[row] = m;
-            if (kuo) kuo[row] = m;
+            if (keys) {
+                const float m = s_key[64 * q + lane];
+                kto[row] = m;
+                if (kuo) kuo[row] = m;
+            }
             if (UB) ubo[row] = s_ub[64 * q + lane];
         }
     }
@@ -808,7 +812,8 @@ static int stream_tpw(const ScoreArgs& a, int tmax) {
 
 template <int HT, int KS, bool UB>
 static void launch_stream(const ScoreArgs& a, hipStream_t s) {
-    const int tpw = stream_tpw(a, StreamGeom<KS, UB>::TPW_MAX);
+    // without keys the bounds take the whole key buffer (twice the tiles per wave)
+    const int tpw = stream_tpw(a, (UB && a.no_keys) ? StreamGeom<KS, UB>::KT : StreamGeom<KS, UB>::TPW_MAX);
     const int64_t rows_per_block = (int64_t)STREAM_WAVES * 16 * tpw;   // block span
     dim3 grid((unsigned)((a.A + rows_per_block - 1) / rows_per_block), a.B);
     const size_t sm = STREAM_WAVES * (size_t)StreamGeom<KS, UB>::WAVE;

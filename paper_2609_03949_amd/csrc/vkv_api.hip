@@ -542,9 +542,10 @@ static hipError_t run_prep(const vkv_step* st, char* w, Chunk c, hipStream_t s) 
 }
 
 static hipError_t run_score(const vkv_step* st, char* w, Chunk c, float* key, float* ub, float cert_mult,
-                            hipStream_t s, const double* thr = nullptr) {
+                            hipStream_t s, const double* thr = nullptr, bool no_keys = false) {
     ScoreArgs a = score_args(st, layout(st, 0, 0), w, c, key, ub, cert_mult);
     a.thr = thr ? thr + c.b0 * st->H : nullptr;
+    a.no_keys = (no_keys && ub && !key) ? 1 : 0;
     return launch_score(a, s);
 }
 
@@ -966,7 +967,8 @@ int vkv_step_run_kept(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_byte
     HIP_TRY(ctx, run_prep(st, w, all, s));
     HIP_TRY(ctx, launch_mark_tier(reinterpret_cast<uint8_t*>(w + L.flags), flag_stride(L.A), L.A, (int)st->B, kept, k, s));
     HIP_TRY(ctx, run_row_max(st, kept, k, 0, 1, smax, argmax, s, w));
-    HIP_TRY(ctx, run_score(st, w, all, key, ub, cert_mult, s, smax));
+    // the step reads only the margins: without a key buffer the scan writes no keys
+    HIP_TRY(ctx, run_score(st, w, all, key, ub, cert_mult, s, smax, key == nullptr));
     HIP_TRY(ctx, run_trigger(st, w, k, kept, ub, cert_mult, smax, topj, fired, fired_count, cap, s));
     HIP_TRY(ctx, run_attend(st, w, all, k, kept, fired, fired_count, cap, scale, out, lse, s));
     if ((rc = debug_check_sel(ctx, st, k, kept, s))) return rc;

@@ -189,6 +189,8 @@ struct ScoreArgs {
     int B, H, n;
     float cert_mult;       // (UB) multiplier of the sketch-residual term a_h eta_u
     const double* thr;     // (UB) [B,H] trigger thresholds s*_h, or null: ub holds max_h (UB~_h - s*_h)
+    int no_keys;           // (UB) 1: only ub is written (no key, no kt); the LDS key buffer then holds
+                           // bounds only, so a wave owns twice the tiles
 };
 
 struct DigestArgs {

@@ -176,7 +176,7 @@ def test_incremental_close_and_rebalance(ctx):
             assert np.array_equal(tiers[j][b], inc[j]), (b, j)
 
 
-def _kept_step(ctx, wl, kept_t, cm, topj):
+def _kept_step(ctx, wl, kept_t, cm, topj, with_key=True, raw=False):
     pack = gpu_index(ctx, wl, True)
     index, has_rope, eta, eps, gam = pack
     step = vkv.Step(wl["cache"], wl["q_lat"], wl["q_rope"], wl["W"], wl["mode"], wl["r"], index=index,
@@ -185,7 +185,7 @@ def _kept_step(ctx, wl, kept_t, cm, topj):
     k = kept_t.shape[1]
     ws = vkv.alloc_workspace(step, k, A)
     d = dict(dtype=torch.float32, device="cuda")
-    key = torch.empty(B, A, **d)
+    key = torch.empty(B, A, **d) if with_key else None   # without: the scan writes no keys
     ub = torch.empty(B, A, **d)
     smax = torch.empty(B, H, dtype=torch.float64, device="cuda")
     arg = torch.empty(B, H, dtype=torch.int32, device="cuda")
@@ -195,16 +195,19 @@ def _kept_step(ctx, wl, kept_t, cm, topj):
     lse = torch.empty(B, H, **d)
     vkv.step_run_kept(ctx, step, ws, k, kept_t, key, ub, cm, smax, arg, topj, fired, cnt, A, wl["scale"], out, lse)
     torch.cuda.synchronize()
+    if raw:
+        return dict(smax=smax, arg=arg, fired=fired, cnt=cnt, out=out, lse=lse)
     return dict(smax=smax.cpu().numpy(), arg=arg.cpu().numpy(), fired=fired.cpu().numpy(), cnt=cnt.cpu().numpy(),
                 out=out.float().cpu().numpy().astype(np.float64), lse=lse.cpu().numpy().astype(np.float64))
 
 
-@pytest.mark.parametrize("cm,topj", [(0.12, 16), (0.12, 0), (1.0, 0)])
-def test_step_on_the_sigma_tier_matches_the_oracle(ctx, cm, topj):
+@pytest.mark.parametrize("cm,topj,with_key", [(0.12, 16, True), (0.12, 0, True), (1.0, 0, True), (0.12, 16, False),
+                                              (1.0, 0, False)])
+def test_step_on_the_sigma_tier_matches_the_oracle(ctx, cm, topj, with_key):
     """The deployed per-step path: sigma tier of the closed blocks + the open
     tail attended, index scan, calibrated trigger against the tier's maximum
-    logit, top-j fetch, attention."""
-    say(f"kept-tier step cert_mult={cm} topj={topj}")
+    logit, top-j fetch, attention (with and without the diagnostic keys)."""
+    say(f"kept-tier step cert_mult={cm} topj={topj} with_key={with_key}")
     cfg = synth.CONFIGS["cfg3"].with_(H=32, W=300)
     wl = synth.make_workload(cfg, "cuda", B=2, T=2 * NB + 300)
     A = wl["A"]
@@ -212,7 +215,7 @@ def test_step_on_the_sigma_tier_matches_the_oracle(ctx, cm, topj):
     sig = _close(ctx, wl["cache"], 0, 2, 16)
     kept_np = _tier(ctx, sig, A, 508)
     kept_t = torch.from_numpy(kept_np).cuda().contiguous()
-    g = _kept_step(ctx, wl, kept_t, cm, topj)
+    g = _kept_step(ctx, wl, kept_t, cm, topj, with_key)
     cache, q_lat, q_rope, P = host_inputs(wl, [0, 1])
     idx, eta, eps, gam = oracle.digest_build(cache, P, wl["r"], with_rope=True)
     o = oracle.step_kept(cache, q_lat, q_rope, idx, P, wl["r"], wl["mode"], wl["W"], kept_np, wl["scale"],
@@ -225,6 +228,29 @@ def test_step_on_the_sigma_tier_matches_the_oracle(ctx, cm, topj):
         assert _checks.rel_l2(g["out"][b], o["out"][b]) < _checks.OUT_TOL
         assert np.all(np.abs(g["lse"][b] - o["lse"][b]) < _checks.LSE_TOL)
     say(f"  fired per sequence: {[int(c) for c in g['cnt']]} of {A - kept_np.shape[1]} archived outside the tier")
+
+
+def test_kept_step_without_keys_at_full_size(ctx):
+    """At the 128K-context size (32 sequences, 130560 archived rows each) the
+    scan without keys gives each wave twice the tiles of the scan with keys;
+    every result of the step is the same bit for bit."""
+    say("kept-tier step with and without keys, 32 x 131072 rows")
+    cfg = synth.CONFIGS["cfg4"]
+    wl = synth.make_workload(cfg, "cuda")
+    A = wl["A"]
+    g = torch.Generator().manual_seed(5)
+    kept = torch.stack([torch.cat([torch.arange(4), 4 + torch.randperm(A - 4, generator=g)[:4092]]).sort().values
+                        for _ in range(wl["B"])]).to(torch.int32).cuda().contiguous()
+    r1 = _kept_step(ctx, wl, kept, 0.06, 0, with_key=True, raw=True)
+    r0 = _kept_step(ctx, wl, kept, 0.06, 0, with_key=False, raw=True)
+    for name in ("smax", "arg", "cnt", "out", "lse"):
+        assert torch.equal(r0[name], r1[name]), name
+    cnt = r1["cnt"].cpu().numpy()
+    f0, f1 = r0["fired"].cpu().numpy(), r1["fired"].cpu().numpy()
+    for b in range(wl["B"]):
+        n = min(int(cnt[b]), A)
+        assert np.array_equal(f0[b, :n], f1[b, :n]), b
+    say(f"  fired rows: {int(cnt.sum())}")
 
 
 def test_sigma_argument_errors(ctx):
