@@ -127,6 +127,7 @@ constexpr int RM_WROWS = RM_TILE / RM_WAVES;                  // tile rows each 
 constexpr int RM_WPIECES = RM_WROWS * (D_ROW / 8);            // their 16-byte pieces (288)
 constexpr int RM_PER = (RM_WPIECES + 63) / 64;                // pieces per lane (5)
 
+template <bool OFF32>
 __global__ __launch_bounds__(RM_THREADS) void row_max_kernel(RowMaxArgs a) {
     __shared__ __align__(16) uint8_t s_x[2][RM_TILE * 2 * D_ROW];
     __shared__ int32_t s_id[2][RM_TILE];
@@ -168,10 +169,15 @@ __global__ __launch_bounds__(RM_THREADS) void row_max_kernel(RowMaxArgs a) {
     qs += __shfl_xor(qs, 32);
     // per accumulator slot i: head h0 + 4 g + i; an upper bound of its ||q||
     // (the fp32 sum of 576 exact squares is within 576 * 2^-24 relative)
-    float qub[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) qub[i] = sqrtf(__shfl(qs, 4 * g + i) * (1.0f + 0x1p-12f)) * (1.0f + 0x1p-20f);
+    // qk[i] = KE ||q|| inflated by 2^-19 (which covers the fp32 roundings of
+    // qk and of the product with ||x|| below), KE = 2 (n + n/32) 2^-23
     constexpr float KE = 2.0f * (float)(D_ROW + D_ROW / 32) * 0x1p-23f;
+    float qk[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float qub = sqrtf(__shfl(qs, 4 * g + i) * (1.0f + 0x1p-12f)) * (1.0f + 0x1p-20f);
+        qk[i] = (KE * qub) * (1.0f + 0x1p-19f);
+    }
     float M[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
     // per head 4 g + i: entries in its list in byte i of ncand (the same in
     // the group's 16 lanes), and in bit i of ovf whether an entry did not fit
@@ -183,26 +189,37 @@ __global__ __launch_bounds__(RM_THREADS) void row_max_kernel(RowMaxArgs a) {
     // past the range repeat its last row; they are loaded, never scored).  A
     // row's pieces stay in one wave, so the wave also sums the row's squares
     // once for all 8 waves (the per-(row, head) band needs ||x_u||).
+    // (list positions, row indices and, with OFF32, byte offsets inside the
+    // sequence's cache fit 32 bits; the bases are uniform, so the loads take
+    // a scalar base and a 32-bit lane offset)
+    const int32_t* rb = a.rows ? a.rows + (int64_t)b * a.nrows : nullptr;
+    const int32_t n1i = (int32_t)n1, Ai = (int32_t)a.A, Nm1 = (int32_t)(N - 1);
     auto load_ids = [&](int64_t t0, int32_t (&id)[RM_PER]) {
+        const int32_t t0i = (int32_t)t0 + RM_WROWS * wave;
 #pragma unroll
         for (int i = 0; i < RM_PER; ++i) {
             const int q = lane + 64 * i;
             if (q < RM_WPIECES) {
-                const int64_t p = min(t0 + RM_WROWS * wave + q / (D_ROW / 8), N - 1);
-                int32_t v = (int32_t)(p < n1 ? p : a.A + (p - n1));
-                if (!a.all_archive && p < n1) v = a.rows[(int64_t)b * a.nrows + p];
+                const int32_t p = min(t0i + q / (D_ROW / 8), Nm1);
+                int32_t v = p < n1i ? p : Ai + (p - n1i);
+                if (!a.all_archive && p < n1i) v = rb[p];
                 id[i] = v;
             }
         }
     };
     u32x4_t xr[RM_PER];
+    const uint8_t* cbb = reinterpret_cast<const uint8_t*>(cb);
+    const uint32_t rs32 = (uint32_t)(2 * a.cs);   // row stride in bytes (OFF32)
     auto load_pieces = [&](const int32_t (&id)[RM_PER]) {
 #pragma unroll
         for (int i = 0; i < RM_PER; ++i) {
             const int q = lane + 64 * i;
             if (q < RM_WPIECES) {
                 const int s = q % (D_ROW / 8);
-                xr[i] = *reinterpret_cast<const u32x4_t*>(cb + (int64_t)id[i] * a.cs + 8 * s);
+                if constexpr (OFF32)
+                    xr[i] = *reinterpret_cast<const u32x4_t*>(cbb + ((uint32_t)id[i] * rs32 + 16u * (uint32_t)s));
+                else
+                    xr[i] = *reinterpret_cast<const u32x4_t*>(cb + (int64_t)id[i] * a.cs + 8 * s);
             }
         }
     };
@@ -252,9 +269,15 @@ __global__ __launch_bounds__(RM_THREADS) void row_max_kernel(RowMaxArgs a) {
         float hi[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const float e = next_up_f32(KE * qub[i] * xub * (1.0f + 0x1p-20f) + (float)D_ROW * 0x1p-120f);
-            const float lo = valid ? next_down_f32(acc[i] - e) : -INFINITY;
-            hi[i] = valid ? next_up_f32(acc[i] + e) : -INFINITY;
+            // e >= the band KE ||q|| ||x|| (one rounding, inside qk's slack;
+            // the n 2^-120 term keeps e away from the subnormals).  The
+            // rounding to nearest of acc -+ ep moves it by at most
+            // 2^-24 (|acc| + ep), and ep - e >= 2^-23 (|acc| + e) exceeds that,
+            // so lo <= acc - e and hi >= acc + e without directed rounding.
+            const float e = fmaf(qk[i], xub, (float)D_ROW * 0x1p-120f);
+            const float ep = fmaf(fabsf(acc[i]) + e, 0x1p-22f, e);
+            const float lo = valid ? acc[i] - ep : -INFINITY;
+            hi[i] = valid ? acc[i] + ep : -INFINITY;
             // running certified lower bound of the maximum: over the 16 rows (lanes of the group)
             M[i] = fmaxf(M[i], rowmax16(lo));
         }
@@ -467,7 +490,11 @@ __global__ __launch_bounds__(64) void row_merge_kernel(RowMaxArgs a) {
 hipError_t launch_row_max(const RowMaxArgs& a, hipStream_t s) {
     const int HG = (a.H + 15) / 16;
     const unsigned nblk = (unsigned)((HG + RM_WAVES - 1) / RM_WAVES * a.B * a.nsplit);
-    hipLaunchKernelGGL(row_max_kernel, dim3(nblk), dim3(RM_THREADS), 0, s, a);
+    // 32-bit byte offsets when every row of a sequence lies within 4 GiB of its first
+    if ((a.T - 1) * a.cs * 2 + 2 * D_ROW <= (int64_t)UINT32_MAX)
+        hipLaunchKernelGGL(row_max_kernel<true>, dim3(nblk), dim3(RM_THREADS), 0, s, a);
+    else
+        hipLaunchKernelGGL(row_max_kernel<false>, dim3(nblk), dim3(RM_THREADS), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.nsplit <= 1) return e;
     const int64_t n = (int64_t)a.B * a.H;
