@@ -73,6 +73,49 @@ def test_row_max_is_exact(ctx, H, T, W):
             assert np.array_equal(arg[b].cpu().numpy(), oarg), (b, rows is None, add_recent)
 
 
+@pytest.mark.parametrize("nsplit_ws", [False, True])
+def test_row_max_all_rows_tied(ctx, nsplit_ws):
+    """Heads whose query is zero score every row 0: every row is a candidate,
+    the per-head lists overflow and the kernel scores the whole range exactly;
+    the maximum is 0 at the lowest listed row.  The other heads are ordinary.
+    Through vkv_row_max (one range) and through the kept-tier step (several
+    ranges merged)."""
+    H, T, W = 20, 6000, 64
+    say(f"row max with all rows tied, ranges={'several' if nsplit_ws else 'one'}")
+    cfg = synth.CONFIGS["cfg3"].with_(H=H, W=W)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=T)
+    wl["q_lat"][:, :3] = 0      # bf16 bits of +0
+    wl["q_rope"][:, :3] = 0
+    pack = gpu_index(ctx, wl, True)
+    step = _step_of(wl, pack)
+    A = wl["A"]
+    g = torch.Generator().manual_seed(11)
+    lists = torch.stack([torch.randperm(A, generator=g)[:1500].sort().values for _ in range(2)])
+    lists = lists.to(torch.int32).cuda().contiguous()
+    smax = torch.empty(2, H, dtype=torch.float64, device="cuda")
+    arg = torch.empty(2, H, dtype=torch.int32, device="cuda")
+    if nsplit_ws:
+        k = lists.shape[1]
+        ws = vkv.alloc_workspace(step, k, A)
+        d = dict(dtype=torch.float32, device="cuda")
+        ub = torch.empty(2, A, **d)
+        fired = torch.empty(2, A, dtype=torch.int32, device="cuda")
+        cnt = torch.empty(2, dtype=torch.int32, device="cuda")
+        out = torch.empty(2, H, 512, dtype=torch.bfloat16, device="cuda")
+        lse = torch.empty(2, H, **d)
+        vkv.step_run_kept(ctx, step, ws, k, lists, None, ub, 0.1, smax, arg, 0, fired, cnt, A, wl["scale"], out, lse)
+    else:
+        vkv.row_max(ctx, step, lists, True, smax, arg)
+    torch.cuda.synchronize()
+    cache, q_lat, q_rope, _ = host_inputs(wl, [0, 1])
+    for b in range(2):
+        lst = np.concatenate([lists[b].cpu().numpy(), np.arange(A, wl["T"], dtype=np.int32)])
+        osm, oarg = oracle.row_max(q_lat[b], q_rope[b], cache[b], lst)
+        assert np.all(osm[:3] == 0.0) and np.all(oarg[:3] == lst.min())
+        assert np.array_equal(smax[b].cpu().numpy(), osm), b
+        assert np.array_equal(arg[b].cpu().numpy(), oarg), b
+
+
 def _trigger_step(ctx, wl, k, cm, topj):
     pack = gpu_index(ctx, wl, True)
     step = _step_of(wl, pack)
