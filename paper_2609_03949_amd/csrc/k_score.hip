@@ -39,6 +39,8 @@ namespace vkv {
 constexpr int QP_ROW = 1040;          // LDS bytes per staged row of 512 bf16
 constexpr int QP_CHUNK_ROWS = 128;    // basis rows staged at a time: one 16-row tile per wave
 constexpr int QP_MAX_WAVES = QP_CHUNK_ROWS / 16;
+constexpr int QP_WSTRIDE = QP_CHUNK_ROWS + 1;   // doubles per head of the staged w values (heads in distinct banks)
+constexpr int QP_TAIL_BATCH = 16;              // staged values per LDS batch of the tail sums
 
 // waves with a basis tile (0 without a digest); one more wave takes the Nq chains
 __host__ __device__ inline int qp_tile_waves(int r) {
@@ -86,8 +88,8 @@ __global__ __launch_bounds__(64 * (QP_MAX_WAVES + 1)) void qprep_project_kernel(
     const uint16_t* qa = reinterpret_cast<const uint16_t*>(s_q + (lane & 15) * QP_ROW) + (lane >> 4);
     const uint16_t* pb = reinterpret_cast<const uint16_t*>(s_p + (16 * wave + (lane & 15)) * QP_ROW) + (lane >> 4);
     const uint16_t* qn = reinterpret_cast<const uint16_t*>(s_q + (lane & 15) * QP_ROW);   // Nq: head lane mod 16
-    double* s_w = reinterpret_cast<double*>(s_p);   // [16][QP_CHUNK_ROWS] w, then RNE(w), once the chunk is used
-    double* s_d = s_w + 16 * QP_CHUNK_ROWS;
+    double* s_w = reinterpret_cast<double*>(s_p);   // [16][QP_WSTRIDE] w, then RNE(w), once the chunk is used
+    double* s_d = s_w + 16 * QP_WSTRIDE;
     double anq = 0.0;
     // tail sums of lane 4 hl + t of wave 0, j ascending over all chunks:
     // t=1 ||w||^2, t=2 ||qd - w||^2, t=3 ||qd||^2 (t=0 takes Nq at the end)
@@ -127,22 +129,35 @@ __global__ __launch_bounds__(64 * (QP_MAX_WAVES + 1)) void qprep_project_kernel(
                 const int hh = 4 * i + (lane >> 4), jl = 16 * wave + (lane & 15);
                 const double v = acc[i];
                 const uint16_t d = f64_to_bf16_rne(v);
-                s_w[hh * QP_CHUNK_ROWS + jl] = v;
-                s_d[hh * QP_CHUNK_ROWS + jl] = (double)bf16_to_f32(d);
+                s_w[hh * QP_WSTRIDE + jl] = v;
+                s_d[hh * QP_WSTRIDE + jl] = (double)bf16_to_f32(d);
                 if (hb0 + hh < a.H) a.qt[((int64_t)b * a.H + hb0 + hh) * a.n + off + j0 + jl] = d;
             }
         }
         if (nq && lane < 16) s_nq[lane] = anq;
         __syncthreads();
         if (wave == 0 && t > 0 && nj > 0) {
-            const double* w = s_w + hl * QP_CHUNK_ROWS;
-            const double* dq = s_d + hl * QP_CHUNK_ROWS;
-            // the three sums share one loop: x = w, qd - w or qd by lane
-#pragma unroll 8
-            for (int j = 0; j < nj; ++j) {
-                const double wj = w[j], dj = dq[j];
-                const double x = t == 1 ? wj : (t == 2 ? dj - wj : dj);
-                tsum = fma(x, x, tsum);
+            const double* w = s_w + hl * QP_WSTRIDE;
+            const double* dq = s_d + hl * QP_WSTRIDE;
+            // the three sums share one loop: x = w, qd - w or qd by lane (qd - 0
+            // is qd exactly), chosen by selects.  The staged values are read in
+            // batches, all reads of a batch in flight before its chain starts.
+            for (int j0 = 0; j0 < nj; j0 += QP_TAIL_BATCH) {
+                double wv[QP_TAIL_BATCH], dv[QP_TAIL_BATCH];
+#pragma unroll
+                for (int e = 0; e < QP_TAIL_BATCH; ++e) {
+                    const int j = min(j0 + e, nj - 1);
+                    wv[e] = w[j];
+                    dv[e] = dq[j];
+                }
+#pragma unroll
+                for (int e = 0; e < QP_TAIL_BATCH; ++e) asm volatile("" : "+v"(wv[e]), "+v"(dv[e]));
+#pragma unroll
+                for (int e = 0; e < QP_TAIL_BATCH; ++e) {
+                    const double sub = (t == 2) ? wv[e] : 0.0;
+                    const double x = (j0 + e >= nj) ? 0.0 : ((t == 1) ? wv[e] : dv[e] - sub);
+                    tsum = fma(x, x, tsum);   // + 0 past the end: tsum >= 0 is unchanged
+                }
             }
         }
         __syncthreads();   // before the next chunk's rows overwrite the w values
