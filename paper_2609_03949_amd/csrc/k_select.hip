@@ -446,7 +446,7 @@ __device__ __forceinline__ void qt_prefetch(const SelectArgs& a, int b, u16x8_t 
 template <bool UB, bool OFF = false>
 __device__ __forceinline__ void exact_keys_block(const SelectArgs& a, int b, int64_t namb, const int32_t* amb, uint64_t* ak,
                                  const ExLds& L, float margin, int blk = 0, int nblks = 1,
-                                 const u16x8_t (*pre)[EX_QP] = nullptr) {
+                                 const u16x8_t (*pre)[EX_QP] = nullptr, uint64_t* ak_lds = nullptr) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4, c = lane & 15;
     const uint16_t* qtb = a.qt + (int64_t)b * a.H * a.n;
     const int n8 = a.n / 8;
@@ -485,9 +485,29 @@ __device__ __forceinline__ void exact_keys_block(const SelectArgs& a, int b, int
             f32x4_t acc[8];
 #pragma unroll
             for (int ht = 0; ht < 8; ++ht) acc[ht] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            float et = 0.f, ep = 0.f, ga = 0.f;
+            if constexpr (UB) {
+                // the row's pieces and its certificate scalars: all loads in
+                // flight together (one memory round trip; pieces past the row
+                // width re-read its last piece), then into the wave's LDS copy
+                // of its rows, from which each lane reads back its own pieces
+                constexpr int KSM = D_ROW / 32;
+                bf16x8_t xr[KSM];
+#pragma unroll
+                for (int ks = 0; ks < KSM; ++ks)
+                    xr[ks] = *reinterpret_cast<const bf16x8_t*>(x + 32 * min(ks, KS - 1) + 8 * g);
+                const int64_t o = (int64_t)b * a.T + u;
+                et = a.eta[o];
+                ep = a.eps[o];
+                ga = a.gam[o];
+#pragma unroll
+                for (int ks = 0; ks < KSM; ++ks)
+                    if (ks < KS) *reinterpret_cast<bf16x8_t*>(&sx[c * a.n + 32 * ks + 8 * g]) = xr[ks];
+            }
             for (int ks = 0; ks < KS; ++ks) {
-                const bf16x8_t xf = *reinterpret_cast<const bf16x8_t*>(x + 32 * ks + 8 * g);
-                *reinterpret_cast<bf16x8_t*>(&sx[c * a.n + 32 * ks + 8 * g]) = xf;
+                const bf16x8_t xf = UB ? *reinterpret_cast<const bf16x8_t*>(&sx[c * a.n + 32 * ks + 8 * g])
+                                       : *reinterpret_cast<const bf16x8_t*>(x + 32 * ks + 8 * g);
+                if (!UB) *reinterpret_cast<bf16x8_t*>(&sx[c * a.n + 32 * ks + 8 * g]) = xf;
 #pragma unroll
                 for (int ht = 0; ht < 8; ++ht) {
                     if (ht < HT) {
@@ -498,13 +518,6 @@ __device__ __forceinline__ void exact_keys_block(const SelectArgs& a, int b, int
                 }
             }
             // acc[ht][q] = screened value of head 16 ht + 4 g + q for row c
-            float et = 0.f, ep = 0.f, ga = 0.f;
-            if (UB) {
-                const int64_t o = (int64_t)b * a.T + u;
-                et = a.eta[o];
-                ep = a.eps[o];
-                ga = a.gam[o];
-            }
             float m = -INFINITY;
 #pragma unroll
             for (int ht = 0; ht < 8; ++ht)
@@ -554,7 +567,11 @@ __device__ __forceinline__ void exact_keys_block(const SelectArgs& a, int b, int
             }
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
             __builtin_amdgcn_wave_barrier();
-            if (lane < 16 && t0 + lane < namb) ak[t0 + lane] = best[lane];
+            if (lane < 16 && t0 + lane < namb) {
+                const uint64_t v = best[lane];
+                ak[t0 + lane] = v;
+                if (ak_lds && t0 + lane < RANK_QUAD_MAX) ak_lds[t0 + lane] = v;   // the ranking's copy
+            }
             // the next tile's row stores must not overtake this tile's chain reads
             __builtin_amdgcn_wave_barrier();
         }
@@ -569,16 +586,19 @@ __device__ __forceinline__ void exact_keys_block(const SelectArgs& a, int b, int
 // key of the last of them.  Pairwise counting with the list staged in LDS
 // when it is short; otherwise a radix select on the 96-bit composite
 // (order key, ~index), whose larger values come first.
+// ak_lds (optional): the keys already in LDS (the first RANK_QUAD_MAX of them).
 __device__ __forceinline__ void rank_winners(const int32_t* amb, const uint64_t* ak, int64_t namb, int64_t need, uint8_t* fb,
-                             uint32_t* xin, uint8_t* lds, uint64_t* s_theta, uint8_t mark = 1) {
+                             uint32_t* xin, uint8_t* lds, uint64_t* s_theta, uint8_t mark = 1,
+                             const uint64_t* ak_lds = nullptr) {
     const int tid = threadIdx.x;
     if (namb <= RANK_QUAD_MAX) {
-        uint64_t* s_k = reinterpret_cast<uint64_t*>(lds);
+        uint64_t* s_kc = reinterpret_cast<uint64_t*>(lds);
         int32_t* s_u = reinterpret_cast<int32_t*>(lds + RANK_QUAD_MAX * 8);
         if (tid < namb) {
-            s_k[tid] = ak[tid];
+            if (!ak_lds) s_kc[tid] = ak[tid];
             s_u[tid] = amb[tid];
         }
+        const uint64_t* s_k = ak_lds ? ak_lds : s_kc;
         lds_barrier();
         if (tid < namb) {
             const uint64_t ki = s_k[tid];
@@ -668,6 +688,7 @@ __global__ __launch_bounds__(RES_THREADS, 1) void sel_resolve_kernel(SelectArgs 
     __shared__ int s_bin;
     __shared__ uint64_t s_theta;
     __shared__ int32_t s_amb[AMB_LDS];         // the undecided rows (the global list holds them all)
+    __shared__ uint64_t s_ak[RANK_QUAD_MAX];   // their exact keys when few (for the ranking)
     const int b = blockIdx.x, tid = threadIdx.x;
     uint32_t* sq = a.seq + (int64_t)b * SQ_WORDS;
     uint8_t* fb = a.flags + (int64_t)b * a.fstride;
@@ -852,8 +873,8 @@ __global__ __launch_bounds__(RES_THREADS, 1) void sel_resolve_kernel(SelectArgs 
     __syncthreads();
     const int32_t* al = amb_lds ? s_amb : amb;
     const ExLds L = ex_carve(lds, a.H, a.n);
-    exact_keys_block<false>(a, b, namb, al, ak, L, next_up_f32(2.0f * E), 0, 1, &qpre);
-    rank_winners(al, ak, namb, need2, fb, blkb + BW_XIN, lds, &s_theta);
+    exact_keys_block<false>(a, b, namb, al, ak, L, next_up_f32(2.0f * E), 0, 1, &qpre, s_ak);
+    rank_winners(al, ak, namb, need2, fb, blkb + BW_XIN, lds, &s_theta, 1, s_ak);
     if (tid == 0) a.theta[b] = ord_to_f64(s_theta);
 }
 
