@@ -87,6 +87,10 @@ def _load():
         lib.vkvref_required_inflation.restype = i32
         lib.vkvref_required_inflation.argtypes = [P, i64, i32, P, P, P, P, i64, P, P, P, i64, P, i64, i32, P,
                                                   P, P, P]
+        lib.vkvref_page_box.restype = i32
+        lib.vkvref_page_box.argtypes = [P, i64, i32, i64, i64, P]
+        lib.vkvref_page_bound.restype = i32
+        lib.vkvref_page_bound.argtypes = [P, i64, i32, P, i64, P]
         lib.vkvref_max_threads.restype = i32
         lib.vkvref_max_threads.argtypes = []
         _lib = lib
@@ -217,6 +221,31 @@ def index_keys(qt_seq: np.ndarray, x: np.ndarray, A: int, check_exact: bool = Fa
     _load().vkvref_index_keys(_ptr(qt_seq), H, n, _ptr(x), x.shape[1], int(A), _ptr(key),
                               ctypes.addressof(bad) if check_exact else None, int(nthreads))
     return key[:A], (int(bad.value) if check_exact else None)
+
+
+def page_box(x: np.ndarray, A: int, page: int) -> np.ndarray:
+    """Per-page column ranges of the index rows [0, A): [npages, 2, n] bf16 bits
+    (lo, hi), pages of `page` rows (appendix on prior algorithms, page-bound
+    pruning)."""
+    x = _u16(x)
+    n = x.shape[1]
+    npg = (A + page - 1) // page
+    box = np.zeros((max(npg, 1), 2, n), np.uint16)
+    _load().vkvref_page_box(_ptr(x), x.shape[1], n, int(A), int(page), _ptr(box))
+    return box[:npg]
+
+
+def page_bound(qt_seq: np.ndarray, box: np.ndarray) -> np.ndarray:
+    """bound[j] = max_h sum_d max(qt_hd lo_d, qt_hd hi_d), fp64, d ascending (the
+    page-bound equation of the appendix on prior algorithms); >= the index key
+    of every row of page j."""
+    qt_seq = _u16(qt_seq)
+    box = np.ascontiguousarray(_u16(box))
+    H, n = qt_seq.shape
+    npg = box.shape[0]
+    out = np.zeros(max(npg, 1), np.float64)
+    _load().vkvref_page_bound(_ptr(qt_seq), H, n, _ptr(box), int(npg), _ptr(out))
+    return out[:npg]
 
 
 def select(key: np.ndarray, k: int):

@@ -13,6 +13,8 @@
  *     the trigger, maximised over heads; top-k by (score desc, index asc)
  *   - Cauchy-Schwarz certificate of the sketch residual                 Lemma (Index certificate)
  *   - exact softmax attention over the attended multiset                Lemma (Exchangeability)
+ *   - per-page boxes of index rows and the interval bound of a page     App. (dividend inside prior
+ *                                                                        algorithms), page-bound pruning
  *
  * Every floating-point step is fp64 with an explicitly stated order (a
  * plain sequential dot product), so that it is a fixed function of the
@@ -650,6 +652,62 @@ int vkvref_full_scores(const uint16_t* q_lat, const uint16_t* q_rope, int64_t H,
                           vkvref_bf16_to_f64(row[D_LAT + i]), acc);
             s[u * H + h] = acc;
         }
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------ page-box bound */
+
+/* Page-bound pruning (appendix "The dividend inside prior algorithms", the
+ * page-bound paragraph and its equation): the archived rows [0, A) are cut
+ * into pages of `page` consecutive rows (the last one ragged); the box of
+ * page j is the per-column range of its index rows,
+ *   lo_d = min_{u in page} x_u[d],   hi_d = max_{u in page} x_u[d],
+ * written as bf16 bits (min and max of bf16 values are bf16 values; a zero
+ * is written as +0).  Layout box[j][0][d] = lo, box[j][1][d] = hi. */
+int vkvref_page_box(const uint16_t* x, int64_t x_stride, int n, int64_t A, int64_t page, uint16_t* box) {
+    if (page < 1) return -1;
+    const int64_t np = (A + page - 1) / page;
+    for (int64_t j = 0; j < np; ++j) {
+        const int64_t u0 = j * page, u1 = (u0 + page < A) ? u0 + page : A;
+        for (int d = 0; d < n; ++d) {
+            double lo = INFINITY, hi = -INFINITY;
+            for (int64_t u = u0; u < u1; ++u) {
+                const double v = vkvref_bf16_to_f64(x[u * x_stride + d]);
+                if (v < lo) lo = v;
+                if (v > hi) hi = v;
+            }
+            box[(j * 2 + 0) * n + d] = (lo == 0.0) ? 0 : vkvref_round_bf16(lo);
+            box[(j * 2 + 1) * n + d] = (hi == 0.0) ? 0 : vkvref_round_bf16(hi);
+        }
+    }
+    return 0;
+}
+
+/* The page's interval bound, maximised over heads:
+ *   bound[j] = max_h sum_d max(qt[h,d] lo_d, qt[h,d] hi_d)
+ * The larger of the two products is qt[h,d] hi_d when qt[h,d] >= 0 and
+ * qt[h,d] lo_d otherwise, so each term is one product of bf16 values (exact
+ * in fp64), summed d ascending from +0 with one rounding per term: the order
+ * of the index key.  Every term is >= the key's term q_d x_u[d] for every row
+ * u of the page and fp64 rounding is monotone, so bound[j] >= key_u for every
+ * u in the page, bit for bit (the positive scale lambda is dropped as in the
+ * keys). */
+int vkvref_page_bound(const uint16_t* qt, int64_t H, int n, const uint16_t* box, int64_t npages, double* bound) {
+    for (int64_t j = 0; j < npages; ++j) {
+        const uint16_t* lo = box + (j * 2 + 0) * n;
+        const uint16_t* hi = box + (j * 2 + 1) * n;
+        double best = -INFINITY;
+        for (int64_t h = 0; h < H; ++h) {
+            double acc = 0.0;
+            for (int d = 0; d < n; ++d) {
+                const double q = vkvref_bf16_to_f64(qt[h * n + d]);
+                const double e = (q >= 0.0) ? vkvref_bf16_to_f64(hi[d]) : vkvref_bf16_to_f64(lo[d]);
+                acc = fma(q, e, acc);
+            }
+            if (acc > best) best = acc;
+        }
+        bound[j] = best;
     }
     return 0;
 }

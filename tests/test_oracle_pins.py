@@ -790,3 +790,92 @@ def test_sketch_basis_is_rotation_equivariant_and_shrinks_the_residual(oracle_mo
     full = np.linalg.norm(qq - (qq @ np.linalg.qr(np.random.default_rng(1).standard_normal((512, 32)))[0])
                           @ np.linalg.qr(np.random.default_rng(1).standard_normal((512, 32)))[0].T, axis=1)
     assert np.median(full / np.linalg.norm(qq, axis=1)) > 0.9   # a random basis leaves almost all of it
+
+
+# ------------------------------------------------------- page-box bound
+
+def _wide_bits(shape, lo, hi, seed):
+    """bf16 bits of sign * (1 + m/128) * 2^e, e uniform in [lo, hi), with some
+    zeros and negative zeros: fp64 sums of their products round often."""
+    r = np.random.default_rng(seed)
+    m = r.integers(0, 128, shape)
+    e = r.integers(lo, hi, shape)
+    sg = r.choice([-1.0, 1.0], shape)
+    v = (sg * np.ldexp(1.0 + m / 128.0, e)).astype(np.float32)
+    z = r.random(shape) < 0.05
+    v[z] = np.where(r.random(int(z.sum())) < 0.5, 0.0, -0.0)
+    return (v.view(np.uint32) >> 16).astype(np.uint16)
+
+
+def test_page_box_brackets_and_attains_every_column(oracle_mod):
+    """Box of each page (appendix on prior algorithms, page-bound pruning):
+    lo <= x_u <= hi for every row of the page, both ends attained by a row,
+    the last page ragged, zeros written as +0."""
+    A, n, page = 301, 24, 64
+    x = _wide_bits((A, n), -10, 10, 1)
+    box = oracle_mod.page_box(x, A, page)
+    assert box.shape == (5, 2, n)
+    xv = dec(x)
+    for j in range(5):
+        rows = xv[j * page:min(A, (j + 1) * page)]
+        lo, hi = dec(box[j, 0]), dec(box[j, 1])
+        assert np.array_equal(lo, rows.min(0)) and np.array_equal(hi, rows.max(0))
+    assert not np.any(box == 0x8000)
+
+
+def test_page_bound_is_the_maximum_over_the_box_corners(oracle_mod):
+    """The interval bound is max_h of the largest q.v over v in the box, which
+    a linear form attains at a corner: brute force over all 2^n corners in
+    exact rationals, on small integers (every fp64 sum exact)."""
+    n, H, A, page = 6, 5, 40, 8
+    q = small_int_bf16((H, n), -6, 6)
+    x = small_int_bf16((A, n), -7, 7)
+    box = oracle_mod.page_box(x, A, page)
+    bound = oracle_mod.page_bound(q, box)
+    import itertools
+    for j in range(box.shape[0]):
+        lo, hi = box[j, 0], box[j, 1]
+        best = None
+        for corner in itertools.product((0, 1), repeat=n):
+            v = [hi[d] if corner[d] else lo[d] for d in range(n)]
+            for h in range(H):
+                s = exact_dot(q[h], v)
+                best = s if best is None or s > best else best
+        assert Fraction(bound[j]) == best
+
+
+def test_page_bound_dominates_every_key_of_its_page(oracle_mod):
+    """bound[j] >= key_u for every row u of page j, bit for bit: each term is
+    >= the key's term and fp64 rounding is monotone (inputs spread over 2^40,
+    so the sums round at many steps)."""
+    n, H, A, page = 64, 16, 700, 32
+    q = _wide_bits((H, n), -20, 20, 2)
+    x = _wide_bits((A, n), -20, 20, 3)
+    key, bad = oracle_mod.index_keys(q, x, A, check_exact=True)
+    assert bad > 0   # the sums do round: the inequality is not only exact arithmetic
+    bound = oracle_mod.page_bound(q, oracle_mod.page_box(x, A, page))
+    for j in range(len(bound)):
+        assert np.all(key[j * page:min(A, (j + 1) * page)] <= bound[j])
+
+
+def test_page_bound_with_pages_of_one_row_is_the_key(oracle_mod):
+    """A one-row page's box is the row itself: the bound is that row's index
+    key bit for bit (same terms, same order)."""
+    n, H, A = 40, 8, 90
+    q = _wide_bits((H, n), -15, 15, 4)
+    x = _wide_bits((A, n), -15, 15, 5)
+    key, _ = oracle_mod.index_keys(q, x, A)
+    assert np.array_equal(oracle_mod.page_bound(q, oracle_mod.page_box(x, A, 1)), key)
+
+
+def test_page_bound_of_a_constant_page_and_of_a_zero_query(oracle_mod):
+    """A page whose rows are all equal bounds exactly its key; a zero query
+    bounds every page by 0."""
+    n, H = 32, 4
+    q = rand_bf16((H, n))
+    row = rand_bf16((1, n))
+    x = np.repeat(row, 16, 0)
+    key, _ = oracle_mod.index_keys(q, x, 16)
+    assert oracle_mod.page_bound(q, oracle_mod.page_box(x, 16, 16))[0] == key[0]
+    z = np.zeros((H, n), np.uint16)
+    assert np.all(oracle_mod.page_bound(z, oracle_mod.page_box(rand_bf16((100, n)), 100, 10)) == 0.0)
