@@ -70,6 +70,10 @@ def main():
     ap.add_argument("--sketch", action="store_true",
                     help="(kept path) content queries near a 48-dim subspace and the index basis V_r fitted "
                          "on the GPU to 4096 prefix queries of the same law (vkv_sketch_basis)")
+    ap.add_argument("--page", type=int, default=0,
+                    help="(index path) also build the page boxes of this many rows and time the page "
+                         "bounds; report the share of pages whose bound is below theta (outside the timed "
+                         "region, not in the step)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: libvkv has no multi-GPU path "
@@ -199,6 +203,30 @@ def main():
                                                        for s_ in range(reps)]))
         log(f"stages alone (ms): {json.dumps({k_: round(v, 4) for k_, v in per_stage.items()})}")
 
+    # ---- optional: page boxes and their interval bounds (page-bound pruning),
+    # outside the timed region; the share of pages below theta is what a scan
+    # that skips pages by the bound would save
+    page_info = None
+    if args.page > 0:
+        npg = (A + args.page - 1) // args.page
+        n_idx = cols if cols else 64
+        box = torch.empty(B, max(npg, 1), 2, n_idx, dtype=torch.bfloat16, device=dev)
+        bound = torch.empty(B, max(npg, 1), dtype=torch.float64, device=dev)
+        run_step()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev[0].record(stream)
+        vkv.page_box(ctx, step, args.page, box, stream)
+        ev[1].record(stream)
+        vkv.page_bound(ctx, step, bufs.ws, args.page, box, bound, stream)
+        ev[2].record(stream)
+        torch.cuda.synchronize()
+        below = int((bound[:, :npg] < bufs.theta[:, None]).sum().item())
+        page_info = {"page": args.page, "pages": B * npg, "below_theta": below,
+                     "box_ms": ev[0].elapsed_time(ev[1]), "bound_ms": ev[1].elapsed_time(ev[2])}
+        log(f"page bound (page {args.page}): {below} of {B * npg} pages below theta "
+            f"({100.0 * below / max(1, B * npg):.3f}%); boxes {page_info['box_ms']:.3f} ms, "
+            f"bounds {page_info['bound_ms']:.3f} ms")
+
     rows_per_s = B * A / (ms_per_step * 1e-3)
     sb = budget.step_bytes(B, H, T, W, k, mode, r, two_tier, adm_total)
     step_gbs = sb["total"] / (ms_per_step * 1e-3) / 1e9
@@ -233,6 +261,7 @@ def main():
         "stage_ms": per_stage,
         "attended_rows_per_seq": k + W + (adm_total / B if two_tier else 0),
         "index_build_ms": digest_ms,
+        **({"page_bound": page_info} if page_info else {}),
         "roofline": {
             "bound": "hbm",
             "kernel": "score_stream_kernel (index scan)",

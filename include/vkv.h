@@ -233,6 +233,35 @@ int vkv_step_run_kept(vkv_ctx* ctx, const vkv_step* st, void* ws, size_t ws_byte
 int vkv_pack_rows(vkv_ctx* ctx, const int32_t* lists, const int32_t* counts, int64_t n, int64_t cap,
                   int32_t* offsets, int32_t* packed, void* stream);
 
+/* Page-box bound (the page-bound pruning paragraph of the appendix "The
+ * dividend inside prior algorithms", and its equation).  The archived rows
+ * [0, A) of each sequence, A = T - W, are cut into npages = ceil(A / page)
+ * pages of `page` consecutive rows (the last one ragged).
+ *
+ * vkv_page_box: box [B][npages][2][n] (device, bf16 bits, n = the index
+ * width of the step) receives, per page and index column d, the smallest
+ * (box[b][j][0][d]) and the largest (box[b][j][1][d]) value of x_u[d] over
+ * the page's rows, x_u the index row as vkv_score reads it; a zero is written
+ * as +0.  It reads the index (the cache's branch columns in mode ROPE without
+ * an index) once; the boxes change only when rows are appended.
+ *
+ * vkv_page_bound: after vkv_query_prep on ws, bound [B][npages] (device, fp64)
+ * receives
+ *     bound[b][j] = max_h sum_d max(qt_hd lo_d, qt_hd hi_d)
+ * with each term one exact product (qt_hd hi_d for qt_hd >= 0, else
+ * qt_hd lo_d) and the terms summed d ascending with one fp64 rounding each,
+ * the order of the fp64 index key.  bound[b][j] >= the fp64 index key of
+ * every row of page j, bit for bit, so a page with bound < theta_b (the
+ * tier-1 threshold of vkv_select) holds no tier-1 row and a scan may skip it.
+ * box is what vkv_page_box wrote for the same page size.
+ *
+ * Both are asynchronous on `stream` and allocate nothing.  They return
+ * VKV_E_ARG for page < 1 or a NULL box or bound, and the step's validation
+ * errors; with A = 0 they launch nothing and accept NULL buffers. */
+int vkv_page_box(vkv_ctx* ctx, const vkv_step* st, int64_t page, uint16_t* box, void* stream);
+int vkv_page_bound(vkv_ctx* ctx, const vkv_step* st, const void* ws, size_t ws_bytes, int64_t page,
+                   const uint16_t* box, double* bound, void* stream);
+
 /* Bytes of device workspace a step with budget k and admission capacity cap
  * (0 without admission) needs; the workspace must be 256-byte aligned. */
 int vkv_workspace_size(const vkv_step* st, int64_t k, int64_t cap, size_t* bytes);

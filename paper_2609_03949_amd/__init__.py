@@ -21,7 +21,8 @@ __all__ = [
     "lib_path", "load", "digest_build", "workspace_size", "query_prep", "score", "select", "admit", "attend",
     "step_run", "step_run_static", "check_rows", "row_max", "trigger", "required_inflation", "conformal_z",
     "step_run_trigger", "sketch_workspace_size", "sketch_basis", "sigma_workspace_size", "sigma_close",
-    "sigma_tier_size", "sigma_select", "step_run_kept", "pack_rows", "SIGMA_BLOCK", "exported_symbols",
+    "sigma_tier_size", "sigma_select", "step_run_kept", "pack_rows", "page_box", "page_bound", "SIGMA_BLOCK",
+    "exported_symbols",
 ]
 
 VKV_MODE_ROPE, VKV_MODE_DIGEST, VKV_MODE_ROPE_DIGEST = 1, 2, 3
@@ -36,7 +37,7 @@ exported_symbols = (
     "vkv_attend", "vkv_step_run", "vkv_step_run_static", "vkv_check_rows", "vkv_set_timing", "vkv_score_timing",
     "vkv_row_max", "vkv_trigger", "vkv_required_inflation", "vkv_conformal_z", "vkv_step_run_trigger",
     "vkv_sketch_workspace_size", "vkv_sketch_basis", "vkv_sigma_workspace_size", "vkv_sigma_close",
-    "vkv_sigma_select", "vkv_step_run_kept", "vkv_pack_rows",
+    "vkv_sigma_select", "vkv_step_run_kept", "vkv_pack_rows", "vkv_page_box", "vkv_page_bound",
 )
 SIGMA_BLOCK = 4096
 
@@ -112,6 +113,8 @@ def load():
     lib.vkv_step_run_kept.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P, f32, P, P, i64, P, P, i64,
                                       ctypes.c_float, P, P, P]
     lib.vkv_pack_rows.argtypes = [P, P, P, i64, i64, P, P, P]
+    lib.vkv_page_box.argtypes = [P, sp, i64, P, P]
+    lib.vkv_page_bound.argtypes = [P, sp, P, ctypes.c_size_t, i64, P, P, P]
     lib.vkv_set_timing.argtypes = [P, ctypes.c_int]
     lib.vkv_score_timing.argtypes = [P, ctypes.POINTER(ctypes.c_float), ctypes.c_int]
     for name in exported_symbols:
@@ -408,6 +411,18 @@ def pack_rows(ctx: Context, lists: torch.Tensor, counts: torch.Tensor, offsets: 
     n, cap = lists.shape[0], lists.shape[-1]
     ctx.check(ctx.lib.vkv_pack_rows(ctx.handle, _ptr(lists), _ptr(counts), int(n), int(cap), _ptr(offsets),
                                     _ptr(packed), _stream(stream)))
+
+
+def page_box(ctx: Context, step: Step, page: int, box: torch.Tensor, stream=None):
+    """vkv_page_box: box [B, ceil(A / page), 2, n] bf16 <- per-page column ranges of the index rows."""
+    ctx.check(ctx.lib.vkv_page_box(ctx.handle, step.ref, int(page), _ptr(box), _stream(stream)))
+
+
+def page_bound(ctx: Context, step: Step, ws: torch.Tensor, page: int, box: torch.Tensor, bound: torch.Tensor,
+               stream=None):
+    """vkv_page_bound: bound [B, ceil(A / page)] float64 <- the pages' interval bounds (after query_prep)."""
+    ctx.check(ctx.lib.vkv_page_bound(ctx.handle, step.ref, _ptr(ws), ws.numel(), int(page), _ptr(box), _ptr(bound),
+                                     _stream(stream)))
 
 
 def check_rows(ctx: Context, step: Step, k: int, sel: Optional[torch.Tensor],

@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 PKG = os.path.dirname(HERE)
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libvkv.so")
-SOURCES = ["vkv_api.hip", "k_score.hip", "k_digest.hip", "k_select.hip", "k_attend.hip", "k_trigger.hip", "k_sketch.hip", "k_sigma.hip"]
+SOURCES = ["vkv_api.hip", "k_score.hip", "k_digest.hip", "k_select.hip", "k_attend.hip", "k_trigger.hip", "k_sketch.hip", "k_sigma.hip", "k_page.hip"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     "-ffp-contract=off",

@@ -985,6 +985,55 @@ int vkv_pack_rows(vkv_ctx* ctx, const int32_t* lists, const int32_t* counts, int
     return VKV_OK;
 }
 
+static int check_page(vkv_ctx* ctx, const vkv_step* st, int64_t page) {
+    int rc = check_step(ctx, st);
+    if (rc) return rc;
+    if (page < 1 || page > (1ll << 30)) return fail(ctx, VKV_E_ARG, "page=%lld outside [1, 2^30]", (long long)page);
+    return VKV_OK;
+}
+
+static PageArgs page_args(const vkv_step* st, int64_t page) {
+    PageArgs a{};
+    index_operand(st, &a.x, &a.xs, &a.xbs);
+    a.A = st->T - st->W;
+    a.page = page;
+    a.npages = (a.A + page - 1) / page;
+    a.n = index_width(st);
+    a.H = (int)st->H;
+    a.B = (int)st->B;
+    return a;
+}
+
+int vkv_page_box(vkv_ctx* ctx, const vkv_step* st, int64_t page, uint16_t* box, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    int rc = check_page(ctx, st, page);
+    if (rc) return rc;
+    PageArgs a = page_args(st, page);
+    if (a.npages == 0) return VKV_OK;   // no archived rows
+    if (!box) return fail(ctx, VKV_E_ARG, "box is required");
+    if (!al16(box)) return fail(ctx, VKV_E_ALIGN, "box must be 16-byte aligned");
+    a.box = box;
+    HIP_TRY(ctx, launch_page_box(a, (hipStream_t)stream));
+    return VKV_OK;
+}
+
+int vkv_page_bound(vkv_ctx* ctx, const vkv_step* st, const void* ws, size_t ws_bytes, int64_t page,
+                   const uint16_t* box, double* bound, void* stream) {
+    if (!ctx) return fail(nullptr, VKV_E_ARG, "ctx is NULL");
+    int rc = check_prep(ctx, st, const_cast<void*>(ws), ws_bytes);
+    if (rc) return rc;
+    if ((rc = check_page(ctx, st, page))) return rc;
+    PageArgs a = page_args(st, page);
+    if (a.npages == 0) return VKV_OK;   // no archived rows
+    if (!box || !bound) return fail(ctx, VKV_E_ARG, "box and bound are required");
+    if (!al16(box)) return fail(ctx, VKV_E_ALIGN, "box must be 16-byte aligned");
+    a.box = const_cast<uint16_t*>(box);
+    a.qt = reinterpret_cast<const uint16_t*>((const char*)ws + layout(st, 0, 0).qt);
+    a.bound = bound;
+    HIP_TRY(ctx, launch_page_bound(a, (hipStream_t)stream));
+    return VKV_OK;
+}
+
 int vkv_sketch_workspace_size(int32_t r, size_t* bytes) {
     if (!bytes) return fail(nullptr, VKV_E_ARG, "bytes is NULL");
     if (r < 32 || r > 512 || r % 32) return fail(nullptr, VKV_E_UNSUPPORTED, "r=%d: need a multiple of 32 in [32, 512]", r);

@@ -324,6 +324,19 @@ struct SigmaSelArgs {
 size_t sigma_workspace_bytes(int64_t B, int64_t nblk);
 hipError_t launch_sigma(const SigmaArgs& a, hipStream_t s);
 hipError_t launch_sigma_select(const SigmaSelArgs& a, hipStream_t s);
+// page boxes and interval bounds (page-bound pruning)
+struct PageArgs {
+    const uint16_t* x;     // index rows as the scorer reads them (first scored column)
+    int64_t xs, xbs;       // row / batch stride, elements
+    int64_t A, page, npages;
+    int n, H, B;
+    uint16_t* box;         // [B][npages][2][n]: lo row, hi row (bf16 bits)
+    const uint16_t* qt;    // [B][H][n]
+    double* bound;         // [B][npages]
+};
+hipError_t launch_page_box(const PageArgs& a, hipStream_t s);
+hipError_t launch_page_bound(const PageArgs& a, hipStream_t s);
+
 hipError_t launch_mark_tier(uint8_t* flags, int64_t fstride, int64_t A, int B, const int32_t* sel, int64_t k,
                             hipStream_t s);
 
