@@ -8,9 +8,10 @@
 //      CLO = down(t_lo - E), CHI = up(t_hi + E);
 //   2. count (one block per 4096 rows): rows with key~ - E > CHI are certainly
 //      selected, rows with key~ + E < CLO certainly not; the others are
-//      candidates, listed in the block's own region of the candidate array
-//      with their keys~; per-block counts (selected, candidates, keys~ above
-//      t_hi).  Nothing is accumulated across blocks or calls;
+//      candidates, appended with their keys~ to the sequence's candidate list
+//      at an offset taken with one atomic per block (the bracket launch of the
+//      same call empties the list); per-block counts (selected, candidates,
+//      keys~ above t_hi) are stored, not accumulated;
 //   3. resolve (one block per sequence): a histogram of the candidates inside
 //      [t_lo, t_hi] gives the fine bin of the k-th largest key~ (if the sample
 //      missed, the block histograms the whole key range instead and classifies
