@@ -213,6 +213,8 @@ def main():
         box = torch.empty(B, max(npg, 1), 2, n_idx, dtype=torch.bfloat16, device=dev)
         bound = torch.empty(B, max(npg, 1), dtype=torch.float64, device=dev)
         run_step()
+        vkv.page_box(ctx, step, args.page, box, stream)   # warm-up (first launches load the kernels)
+        vkv.page_bound(ctx, step, bufs.ws, args.page, box, bound, stream)
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
         ev[0].record(stream)
         vkv.page_box(ctx, step, args.page, box, stream)

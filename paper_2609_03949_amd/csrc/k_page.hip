@@ -20,25 +20,59 @@ namespace vkv {
 constexpr int PB_PAGES = 16;    // pages per bound block
 constexpr int PB_THREADS = 128; // one head per thread (H <= 128)
 
-// Box of page (blockIdx.x, b): thread d of the block takes columns d, d + blockDim.x, ...
-// Comparisons in fp32 (exact for bf16 values); the first of equal values is
-// kept and a zero is written as +0.
-__global__ __launch_bounds__(256) void page_box_kernel(PageArgs a) {
+// Boxes: a thread takes one 8-column piece of one page and walks the page's
+// rows with 16-byte loads (the n/8 threads of a page read each row as one
+// contiguous run); a block covers 256 / (n/8) pages of one sequence.
+// Comparisons in fp32 (exact for bf16 values); equal values have equal bits
+// except for zeros, which are written as +0.
+constexpr int BOX_THREADS = 256;
+constexpr int BOX_UNROLL = 8;    // rows in flight per thread
+
+__device__ __forceinline__ uint16_t box_bits(float v) {
+    return v == 0.f ? (uint16_t)0 : (uint16_t)(__float_as_uint(v) >> 16);
+}
+
+__global__ __launch_bounds__(BOX_THREADS) void page_box_kernel(PageArgs a) {
     const int b = blockIdx.y;
-    const int64_t j = blockIdx.x;
+    const int np8 = a.n / 8;                       // pieces per row
+    const int ppb = BOX_THREADS / np8;             // pages per block
+    const int t = threadIdx.x;
+    if (t >= ppb * np8) return;
+    const int64_t j = (int64_t)blockIdx.x * ppb + t / np8;
+    if (j >= a.npages) return;
+    const int pc = t % np8;
     const int64_t u0 = j * a.page, u1 = min(a.A, u0 + a.page);
-    const uint16_t* xb = a.x + (int64_t)b * a.xbs;
-    uint16_t* box = a.box + ((int64_t)b * a.npages + j) * 2 * a.n;
-    for (int d = threadIdx.x; d < a.n; d += blockDim.x) {
-        float lo = INFINITY, hi = -INFINITY;
-        for (int64_t u = u0; u < u1; ++u) {
-            const float v = bf16_to_f32(xb[u * a.xs + d]);
-            if (v < lo) lo = v;
-            if (v > hi) hi = v;
-        }
-        box[d] = lo == 0.f ? (uint16_t)0 : (uint16_t)(__float_as_uint(lo) >> 16);
-        box[a.n + d] = hi == 0.f ? (uint16_t)0 : (uint16_t)(__float_as_uint(hi) >> 16);
+    const uint16_t* src = a.x + (int64_t)b * a.xbs + u0 * a.xs + 8 * pc;
+    float lo[8], hi[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        lo[e] = INFINITY;
+        hi[e] = -INFINITY;
     }
+    const int nrow = (int)(u1 - u0);
+    for (int r0 = 0; r0 < nrow; r0 += BOX_UNROLL) {
+        u16x8_t v[BOX_UNROLL];
+#pragma unroll
+        for (int i = 0; i < BOX_UNROLL; ++i)   // rows past the page re-read its last row (no effect on min/max)
+            v[i] = *reinterpret_cast<const u16x8_t*>(src + (int64_t)min(r0 + i, nrow - 1) * a.xs);
+#pragma unroll
+        for (int i = 0; i < BOX_UNROLL; ++i)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float f = bf16_to_f32(v[i][e]);
+                lo[e] = f < lo[e] ? f : lo[e];
+                hi[e] = f > hi[e] ? f : hi[e];
+            }
+    }
+    u16x8_t ol, oh;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        ol[e] = box_bits(lo[e]);
+        oh[e] = box_bits(hi[e]);
+    }
+    uint16_t* box = a.box + ((int64_t)b * a.npages + j) * 2 * a.n;
+    reinterpret_cast<u16x8_t*>(box)[pc] = ol;
+    reinterpret_cast<u16x8_t*>(box + a.n)[pc] = oh;
 }
 
 __device__ __forceinline__ double bf16_f64(uint16_t b) { return (double)__uint_as_float((uint32_t)b << 16); }
@@ -103,8 +137,9 @@ __global__ __launch_bounds__(PB_THREADS) void page_bound_kernel(PageArgs a) {
 
 hipError_t launch_page_box(const PageArgs& a, hipStream_t s) {
     if (a.npages == 0) return hipSuccess;
-    const int threads = a.n >= 256 ? 256 : (a.n + 63) / 64 * 64;
-    hipLaunchKernelGGL(page_box_kernel, dim3((unsigned)a.npages, a.B), dim3(threads), 0, s, a);
+    const int ppb = BOX_THREADS / (a.n / 8);   // n <= 576: at least 3 pages per block
+    hipLaunchKernelGGL(page_box_kernel, dim3((unsigned)((a.npages + ppb - 1) / ppb), a.B), dim3(BOX_THREADS), 0, s,
+                       a);
     return hipGetLastError();
 }
 
