@@ -229,3 +229,42 @@ def test_pack_rows_edge_cases(ctx):
     assert offsets.cpu().tolist() == list(np.concatenate([[0], np.cumsum(lens)]))
     want = np.concatenate([np.arange(i * cap, i * cap + m) for i, m in enumerate(lens)])
     assert np.array_equal(packed.cpu().numpy()[:len(want)], want)
+
+
+def test_page_bound_under_capture(ctx):
+    """Query prep, page boxes and page bounds captured in one graph: replays on
+    refreshed queries equal the eager calls (they allocate nothing and never
+    synchronise)."""
+    say("page bound graph")
+    cfg = synth.CONFIGS["cfg3"].with_(H=32)
+    wl = synth.make_workload(cfg, "cuda", B=2, T=7000)
+    index, has_rope, *_ = gpu_index(ctx, wl, False)
+    step = vkv.Step(wl["cache"], wl["q_lat"], wl["q_rope"], wl["W"], wl["mode"], wl["r"], index=index,
+                    index_has_rope=has_rope, P=wl["P"])
+    page = 48
+    npg = (wl["A"] + page - 1) // page
+    n = synth.D_ROPE + wl["r"]
+    ws = vkv.alloc_workspace(step, 0)
+    box = torch.empty(2, npg, 2, n, dtype=torch.bfloat16, device="cuda")
+    bound = torch.empty(2, npg, dtype=torch.float64, device="cuda")
+
+    def run(w, bx, bd):
+        s = torch.cuda.current_stream()
+        vkv.query_prep(ctx, step, w, s)
+        vkv.page_box(ctx, step, page, bx, s)
+        vkv.page_bound(ctx, step, w, page, bx, bd, s)
+
+    g = _capture(lambda: run(ws, box, bound))
+    ws2 = vkv.alloc_workspace(step, 0)
+    box2, bound2 = torch.empty_like(box), torch.empty_like(bound)
+    for rep in range(3):
+        _new_queries(wl, 300 + rep)
+        bound.fill_(-1.0)
+        g.replay()
+        torch.cuda.synchronize()
+        got = bound.clone()
+        _eager_noise()
+        run(ws2, box2, bound2)
+        torch.cuda.synchronize()
+        assert torch.equal(box, box2) and torch.equal(got, bound2), rep
+        say(f"  replay {rep} equal to eager")
