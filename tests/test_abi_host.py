@@ -108,6 +108,8 @@ def test_null_context_is_refused(lib):
     assert lib.vkv_select(None, ctypes.byref(s), None, 0, 1, None, None, None) == -1
     assert lib.vkv_attend(None, ctypes.byref(s), None, 0, 1, None, None, None, 0, ctypes.c_float(0.1),
                           None, None, None) == -1
+    assert lib.vkv_page_box(None, ctypes.byref(s), 64, P(1 << 20), None) == -1
+    assert lib.vkv_page_bound(None, ctypes.byref(s), P(1 << 20), 1 << 20, 64, P(1 << 20), P(1 << 20), None) == -1
     assert b"ctx" in lib.vkv_last_error(None)
 
 

@@ -123,6 +123,30 @@ def test_page_bound_without_archived_rows(ctx):
     assert box.shape[1] == 0 and bound.shape[1] == 0
 
 
+def test_page_entry_points_refuse_bad_arguments(ctx):
+    cfg = synth.CONFIGS["cfg2_r64"].with_(H=8)
+    wl = synth.make_workload(cfg, "cuda", B=1, T=600)
+    index, has_rope, *_ = gpu_index(ctx, wl, False)
+    step = vkv.Step(wl["cache"], wl["q_lat"], wl["q_rope"], wl["W"], wl["mode"], wl["r"], index=index,
+                    index_has_rope=has_rope, P=wl["P"])
+    ws = vkv.alloc_workspace(step, 0)
+    box = torch.empty(1, 6, 2, wl["r"], dtype=torch.bfloat16, device="cuda")
+    bound = torch.empty(1, 6, dtype=torch.float64, device="cuda")
+    for bad in (0, -3):
+        with pytest.raises(vkv.VkvError) as e:
+            vkv.page_box(ctx, step, bad, box)
+        assert e.value.code == -1
+        with pytest.raises(vkv.VkvError) as e:
+            vkv.page_bound(ctx, step, ws, bad, box, bound)
+        assert e.value.code == -1
+    with pytest.raises(vkv.VkvError) as e:
+        vkv.page_bound(ctx, step, ws, 64, box, torch.empty(0, dtype=torch.float64, device="cuda"))
+    assert e.value.code == -1
+    with pytest.raises(vkv.VkvError) as e:   # a workspace too small for the query prep's outputs
+        vkv.page_bound(ctx, step, ws[:16], 64, box, bound)
+    assert e.value.code == -7
+
+
 @pytest.mark.parametrize("name,page", [("cfg1", 16), ("cfg4", 64)])
 def test_pruning_by_the_page_bound_is_sound_at_full_size(ctx, name, page):
     """At the full configuration: the bounds of sampled sequences against the
