@@ -298,30 +298,55 @@ hipError_t launch_sigma_select(const SigmaSelArgs& a, hipStream_t s) {
 // ------------------------------------------------ a caller's tier into the flags
 
 // flags[b][u] = 1 for the k rows of sel[b] inside [0, A), 0 for the other rows
-__global__ __launch_bounds__(256) void tier_clear_kernel(uint8_t* flags, int64_t fstride, int64_t A) {
-    const int b = blockIdx.y;
-    for (int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x; u < A; u += (int64_t)gridDim.x * 256)
-        flags[(int64_t)b * fstride + u] = 0;
+// The per-row tier flags of a kept table (ascending rows in [0, A)), in one
+// pass: block (c, b) owns rows [4096 c, 4096 (c + 1)) of sequence b, clears
+// their flags, finds the table's entries inside its range by two searches of
+// the ascending list, and marks them.  No block depends on another's writes.
+constexpr int TF_ROWS = 4096;
+
+// first position i of the ascending list ks[0, k) with ks[i] >= v (k if none),
+// by one wave: each round probes 64 evenly spaced positions and keeps the
+// interval between the last probe below v and the first one at or above it
+__device__ __forceinline__ int64_t wave_lower_bound(const int32_t* ks, int64_t k, int64_t v, int lane) {
+    int64_t lo = 0, hi = k;   // the answer lies in [lo, hi]
+    while (hi - lo > 64) {
+        const int64_t step = (hi - lo + 63) / 64;
+        const int64_t p = lo + (int64_t)lane * step;
+        const bool below = p < hi && (int64_t)ks[p] < v;
+        const int cnt = __popcll(__ballot(below));   // the probes below v are a prefix of the lanes
+        const int64_t nlo = cnt == 0 ? lo : lo + (int64_t)(cnt - 1) * step + 1;
+        hi = min(hi, lo + (int64_t)cnt * step);
+        lo = nlo;
+    }
+    const int64_t p = lo + lane;
+    const bool below = p < hi && (int64_t)ks[p] < v;
+    return lo + __popcll(__ballot(below));
 }
 
-__global__ __launch_bounds__(256) void tier_mark_kernel(uint8_t* flags, int64_t fstride, int64_t A, const int32_t* sel,
+__global__ __launch_bounds__(256) void tier_flags_kernel(uint8_t* flags, int64_t fstride, int64_t A, const int32_t* sel,
                                                          int64_t k) {
-    const int b = blockIdx.y;
-    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < k; i += (int64_t)gridDim.x * 256) {
-        const int32_t u = sel[(int64_t)b * k + i];
-        if (u >= 0 && u < A) flags[(int64_t)b * fstride + u] = 1;
+    __shared__ int64_t s_range[2];
+    const int b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t u0 = (int64_t)blockIdx.x * TF_ROWS, u1 = min(A, u0 + TF_ROWS);
+    uint8_t* fb = flags + (int64_t)b * fstride;
+    const int32_t* ks = sel + (int64_t)b * k;
+    for (int64_t u = u0 + tid; u < u1; u += 256) fb[u] = 0;
+    if (wave < 2) {   // wave 0: the first entry >= u0, wave 1: the first entry >= u1
+        const int64_t pos = wave_lower_bound(ks, k, wave == 0 ? u0 : u1, lane);
+        if (lane == 0) s_range[wave] = pos;
+    }
+    __syncthreads();   // the clears are done before any mark, and the range is known
+    for (int64_t i = s_range[0] + tid; i < s_range[1]; i += 256) {
+        const int32_t u = ks[i];
+        if (u >= u0 && u < u1) fb[u] = 1;
     }
 }
 
 hipError_t launch_mark_tier(uint8_t* flags, int64_t fstride, int64_t A, int B, const int32_t* sel, int64_t k,
                             hipStream_t s) {
     if (B == 0 || A == 0) return hipSuccess;
-    const unsigned g1 = (unsigned)((A + 255) / 256 < 1024 ? (A + 255) / 256 : 1024);
-    hipLaunchKernelGGL(tier_clear_kernel, dim3(g1, (unsigned)B), dim3(256), 0, s, flags, fstride, A);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || k == 0) return e;
-    const unsigned g2 = (unsigned)((k + 255) / 256 < 1024 ? (k + 255) / 256 : 1024);
-    hipLaunchKernelGGL(tier_mark_kernel, dim3(g2, (unsigned)B), dim3(256), 0, s, flags, fstride, A, sel, k);
+    const unsigned g = (unsigned)((A + TF_ROWS - 1) / TF_ROWS);
+    hipLaunchKernelGGL(tier_flags_kernel, dim3(g, (unsigned)B), dim3(256), 0, s, flags, fstride, A, sel, k);
     return hipGetLastError();
 }
 
