@@ -147,7 +147,7 @@ def test_page_entry_points_refuse_bad_arguments(ctx):
     assert e.value.code == -7
 
 
-@pytest.mark.parametrize("name,page", [("cfg1", 16), ("cfg4", 64)])
+@pytest.mark.parametrize("name,page", [("cfg0", 8), ("cfg1", 16), ("cfg2_r64", 32), ("cfg3", 64), ("cfg4", 64)])
 def test_pruning_by_the_page_bound_is_sound_at_full_size(ctx, name, page):
     """At the full configuration: the bounds of sampled sequences against the
     oracle bit for bit, and on every sequence no page whose bound is below
