@@ -126,3 +126,18 @@ def test_conformal_z_host_function_matches_the_oracle(lib, oracle_mod):
                 assert vkv.conformal_z(zq, tau, zmax) == oracle_mod.conformal_z(zq, tau, zmax)
     with pytest.raises(vkv.VkvError):
         vkv.conformal_z([1.0], (10, 10))
+
+
+def test_header_is_plain_c(tmp_path):
+    """include/vkv.h is a C header: it compiles as C99 with warnings on, and a
+    C translation unit can take the address of every declared entry point."""
+    import shutil
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "use.c"
+    names = declared_functions()
+    src.write_text('#include "vkv.h"\nvoid* table[] = {' + ", ".join(f"(void*)&{n}" for n in names) + "};\n")
+    r = subprocess.run([cc, "-std=c99", "-Wall", "-Werror", "-fsyntax-only", "-I", os.path.dirname(HEADER),
+                        str(src)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
